@@ -1,0 +1,417 @@
+"""QEvict per-decode-step method as a plain float64 CPU oracle.
+
+TEST INFRASTRUCTURE.  This module exists to check the GPU path: only tests,
+``__graft_entry__.smoke()`` and the benchmark's CPU-baseline leg may import or
+run it.  It shares no code with the GPU library and imports nothing from it.
+
+What it computes, and where the paper defines it (QEvict, arXiv 2608.05326):
+
+* Decode attention of each query head over the accessible keys and values,
+  softmax(q K^T / sqrt(d)) V, with grouped KV heads (Sec. 3.1, Preliminaries).
+* The cache partition into sink, recent region and windows, with each
+  historical window Full, Quantized or Evicted (Sec. 3.3, partition equation).
+* The cumulative window score: each window's attention mass averaged over the
+  H_q query heads, added at every decode step (Sec. 3.2, cumulative window
+  score equation; the per-step reading is listed with the other readings).
+* Routing: the candidate pool is the previous Full and Quantized windows plus
+  the windows that left the recent region; the top K_f by score go to Full,
+  the next K_q to Quantized, the rest are evicted (Sec. 3.3, candidate pool
+  and TopK equations; Algorithm 1).
+* Migration-stable asymmetric quantization: keys per channel across tokens,
+  values per token across channels; codes are produced once, at a window's
+  first demotion, and reused on every later move; promotion reconstructs the
+  low-bit values in bf16 and keeps the codes dormant (Sec. 3.3, paragraph on
+  migration-stable quantization; Algorithm 1).
+
+Everything is float64 except where the method stores a narrower format:
+bf16 keys/values, fp16 quantization scale and zero point, integer codes.
+Those roundings are exact (see ``numerics``).
+
+Readings where the paper is silent (window size W and routing interval R are
+separate parameters; scale/zero rounding; tie-breaks; mixed-precision rule;
+one-way policy) are spelled out next to the code that takes them.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+from .numerics import FP16_MAX, rd_fp16, rne_bf16, rne_fp16, ru_fp16
+
+__all__ = [
+    "OPEN", "AGED", "FULL", "QUANT", "EVICTED", "ACTIVE", "DORMANT",
+    "OracleConfig", "QEvictUnit", "quantize_groups", "quantize_window",
+    "dequantize_window", "route_order", "tier_split", "QuantRangeError",
+]
+
+# window states; OPEN and AGED are both inside / just out of the recent region
+OPEN, AGED, FULL, QUANT, EVICTED = 0, 1, 2, 3, 4
+# ledger entry states (Algorithm 1: an entry is active, dormant, or absent)
+ACTIVE, DORMANT = 1, 2
+
+
+class QuantRangeError(ValueError):
+    """A group's values fall outside the fp16 range of the scale/zero point."""
+
+
+@dataclasses.dataclass
+class OracleConfig:
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    window: int                   # W, tokens per window
+    group: int                    # G, quantization group length
+    bits: int                     # 4, 2, or 42 (mixed: int4 for the upper half of the quantized tier)
+    capacity_full: int            # K_f
+    capacity_quant: int           # K_q
+    sink: int = 0
+    recent: int = 0
+    softmax_scale: float | None = None   # default 1/sqrt(head_dim)
+    no_promotion: bool = False    # one-way Full -> Quantized -> Evicted policy
+
+    @property
+    def scale(self) -> float:
+        return self.softmax_scale if self.softmax_scale else 1.0 / math.sqrt(self.head_dim)
+
+    @property
+    def gqa(self) -> int:
+        return self.num_q_heads // self.num_kv_heads
+
+
+# ----------------------------------------------------------------------------
+# Quantization (Sec. 3.3, migration-stable quantization)
+# ----------------------------------------------------------------------------
+
+def _fp16_step(v: np.ndarray, direction: int) -> np.ndarray:
+    """Next fp16 value above (direction=+1) or below (-1) each non-negative v."""
+    b = v.astype(np.float16).view(np.uint16).astype(np.int32)
+    b = np.where(direction > 0, b + 1, np.maximum(b - 1, 0))
+    return b.astype(np.uint16).view(np.float16).astype(np.float64)
+
+
+def quantize_groups(x, bits: int):
+    """Asymmetric b-bit quantization of every row of ``x`` (one row = one group).
+
+    Reading of the paper's "asymmetric low-bit quantization" with fp16
+    parameters:
+      z = largest fp16 value <= min(x)            (zero point, rounded down)
+      s = smallest fp16 value >= 0 with z + s (2^b - 1) >= max(x)
+      c = round-half-even((x - z) / s), and c = 0 for every element when s = 0.
+    Then 0 <= c <= 2^b - 1 and |x - (z + s c)| <= s / 2 for every element.
+
+    Exactness: z and s are fp16 values (multiples of 2^-24 below 2^16 in
+    magnitude), so z + k s / 2 for an integer k <= 31 is a multiple of 2^-25
+    below 2^21 and is exact in float64.  The scale test and every rounding
+    boundary of the codes are therefore compared exactly; the float64
+    quotient only supplies a first guess that the comparisons correct.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    if x.ndim != 2:
+        raise ValueError("expected [groups, group_len]")
+    n = float(2 ** bits - 1)
+    lo = x.min(axis=1)
+    hi = x.max(axis=1)
+    if np.any(lo < -FP16_MAX) or np.any(hi > FP16_MAX) or not np.all(np.isfinite(x)):
+        raise QuantRangeError("group outside the fp16 range")
+    z = rd_fp16(lo)
+    s = ru_fp16((hi - z) / n)
+    for _ in range(4):   # at most one fp16 step away; loop until stable
+        small = z + s * n < hi
+        s = np.where(small, _fp16_step(s, +1), s)
+        prev = _fp16_step(s, -1)
+        big = (s > 0) & (z + prev * n >= hi)
+        s = np.where(big, prev, s)
+        if not (small.any() or big.any()):
+            break
+    assert np.all(z + s * n >= hi) and np.all((s == 0) | (z + _fp16_step(s, -1) * n < hi))
+
+    zc = z[:, None]
+    sc = np.where(s > 0, s, 1.0)[:, None]
+    c = np.rint((x - zc) / sc)
+    for _ in range(4):
+        lower = zc + (c - 0.5) * sc
+        upper = zc + (c + 0.5) * sc
+        moved = (x < lower) | (x > upper)
+        c = np.where(x < lower, c - 1, np.where(x > upper, c + 1, c))
+        if not moved.any():
+            break
+    lower = zc + (c - 0.5) * sc
+    upper = zc + (c + 0.5) * sc
+    assert np.all((x >= lower) & (x <= upper))
+    odd = np.mod(c, 2) == 1
+    c = np.where((x == upper) & odd, c + 1, c)      # tie at c + 1/2: go to the even neighbour
+    c = np.where((x == lower) & odd, c - 1, c)      # tie at c - 1/2
+    c = np.where(s[:, None] > 0, c, 0.0)
+    assert np.all((c >= 0) & (c <= n))
+    return z, s, c.astype(np.int64)
+
+
+def quantize_window(k, v, bits: int, group: int) -> dict:
+    """Quantize one window: k, v float64 [H_kv, W, d] (bf16 values).
+
+    Keys: one group per (KV head, channel, G consecutive tokens) -> per-channel
+    scale/zero across the token dimension.  Values: one group per (KV head,
+    token, G consecutive channels) -> per-token scale/zero across channels.
+    """
+    h, w, d = k.shape
+    if w % group or d % group:
+        raise ValueError("group must divide the window and the head dim")
+    kg = k.reshape(h, w // group, group, d).transpose(0, 1, 3, 2).reshape(-1, group)
+    kz, ks, kc = quantize_groups(kg, bits)
+    kc = kc.reshape(h, w // group, d, group).transpose(0, 1, 3, 2).reshape(h, w, d)
+    vg = v.reshape(-1, group)
+    vz, vs, vc = quantize_groups(vg, bits)
+    return dict(bits=bits, group=group,
+                kz=kz.reshape(h, w // group, d), ks=ks.reshape(h, w // group, d), kc=kc,
+                vz=vz.reshape(h, w, d // group), vs=vs.reshape(h, w, d // group),
+                vc=vc.reshape(h, w, d), state=ACTIVE)
+
+
+def dequantize_window(e: dict):
+    """x_hat = z + s c for keys and values (exact in float64)."""
+    g = e["group"]
+    kz = np.repeat(e["kz"], g, axis=1)
+    ks = np.repeat(e["ks"], g, axis=1)
+    vz = np.repeat(e["vz"], g, axis=2)
+    vs = np.repeat(e["vs"], g, axis=2)
+    return kz + ks * e["kc"], vz + vs * e["vc"]
+
+
+# ----------------------------------------------------------------------------
+# Routing (Sec. 3.3 candidate pool and TopK equations; Algorithm 1)
+# ----------------------------------------------------------------------------
+
+def route_order(cands, scores) -> list:
+    """Candidates by descending score; equal scores go to the lower window index."""
+    return sorted(cands, key=lambda w: (-scores[w], w))
+
+
+def tier_split(order, k_f: int, k_q: int, was_quantized=frozenset(), no_promotion=False):
+    """F = top K_f, Q = next K_q of the rest, E = remainder.
+
+    One-way policy reading: a window already in the quantized tier may not be
+    chosen for Full, so Full takes the top K_f of the candidates that are not
+    quantized; Quantized then takes the top K_q of everything else.
+    """
+    if no_promotion:
+        full = [w for w in order if w not in was_quantized][:k_f]
+    else:
+        full = list(order[:k_f])
+    fs = set(full)
+    rest = [w for w in order if w not in fs]
+    quant = rest[:k_q]
+    evict = rest[k_q:]
+    return full, quant, evict
+
+
+# ----------------------------------------------------------------------------
+# One (sequence, layer) cache
+# ----------------------------------------------------------------------------
+
+class QEvictUnit:
+    """The tiered cache of one sequence in one layer, stepped in float64."""
+
+    def __init__(self, cfg: OracleConfig, max_tokens: int):
+        self.cfg = cfg
+        c = cfg
+        self.max_tokens = max_tokens
+        self.n_win_cap = max(0, -(-(max_tokens - c.sink) // c.window))
+        # original bf16 keys / values of every token ever appended
+        self.k = np.zeros((c.num_kv_heads, max_tokens, c.head_dim))
+        self.v = np.zeros((c.num_kv_heads, max_tokens, c.head_dim))
+        self.T = 0
+        self.state = np.full(self.n_win_cap, -1, dtype=np.int64)   # -1: not started
+        self.score = np.zeros(self.n_win_cap)
+        self.full_k: dict[int, np.ndarray] = {}
+        self.full_v: dict[int, np.ndarray] = {}
+        self.ledger: dict[int, dict] = {}
+        self.stats = dict(promotions=0, admissions_full=0, first_quantizations=0,
+                          reactivations=0, evictions=0)
+        self.quant_count = 0          # quantizations performed over the lifetime
+
+    # -- geometry ---------------------------------------------------------
+    def win_range(self, w: int):
+        a = self.cfg.sink + w * self.cfg.window
+        return a, a + self.cfg.window
+
+    def _age(self):
+        """OPEN -> AGED once a window is complete and older than the recent region."""
+        c = self.cfg
+        for w in np.nonzero(self.state == OPEN)[0]:
+            if self.win_range(w)[1] <= self.T - c.recent:
+                self.state[w] = AGED
+
+    def _start_windows(self):
+        c = self.cfg
+        n = max(0, -(-(self.T - c.sink) // c.window))
+        for w in range(n):
+            if self.state[w] == -1:
+                self.state[w] = OPEN
+
+    # -- prefill (Sec. 3.2: prompt attention initialises the scores and the first assignment)
+    def prefill(self, k, v, init_scores):
+        """k, v: float64 [H_kv, T, d] bf16 values; init_scores: per window."""
+        c = self.cfg
+        T = k.shape[1]
+        self.k[:, :T] = k
+        self.v[:, :T] = v
+        self.T = T
+        self._start_windows()
+        n = int(np.sum(self.state >= 0))
+        init = np.asarray(init_scores, dtype=np.float64)
+        self.score[:n] = init[:n]
+        self._age()
+        self.route()
+
+    # -- one decode step ----------------------------------------------------
+    def append(self, k_new, v_new):
+        self.k[:, self.T] = k_new
+        self.v[:, self.T] = v_new
+        self.T += 1
+        self._start_windows()
+        self._age()
+
+    def accessible(self, g: int):
+        """Keys, values and owning window (-1 = sink) of every token KV head g attends to.
+
+        Windows appear in index order (chronological); Quantized windows enter as
+        their dequantized values z + s c.
+        """
+        c = self.cfg
+        ks, vs, owner = [], [], []
+        ns = min(c.sink, self.T)
+        if ns:
+            ks.append(self.k[g, :ns])
+            vs.append(self.v[g, :ns])
+            owner.append(np.full(ns, -1))
+        for w in np.nonzero(self.state >= 0)[0]:
+            st = self.state[w]
+            a, b = self.win_range(w)
+            b = min(b, self.T)
+            if st == FULL:
+                kk, vv = self.full_k[w][g], self.full_v[w][g]
+            elif st == QUANT:
+                kh, vh = dequantize_window(self.ledger[w])
+                kk, vv = kh[g], vh[g]
+            elif st in (OPEN, AGED):
+                kk, vv = self.k[g, a:b], self.v[g, a:b]
+            else:
+                continue
+            ks.append(kk)
+            vs.append(vv)
+            owner.append(np.full(len(kk), w))
+        return np.concatenate(ks), np.concatenate(vs), np.concatenate(owner)
+
+    def attend(self, q):
+        """Attention of all query heads; accumulate window scores.
+
+        q: float64 [H_q, d].  Returns (out [H_q, d], mass [H_q, n_win_cap],
+        sink_mass [H_q]).  The score update adds, for every accessible window,
+        the attention mass its tokens received averaged over the H_q heads.
+        """
+        c = self.cfg
+        out = np.zeros((c.num_q_heads, c.head_dim))
+        mass = np.zeros((c.num_q_heads, self.n_win_cap))
+        sink_mass = np.zeros(c.num_q_heads)
+        for g in range(c.num_kv_heads):
+            kk, vv, owner = self.accessible(g)
+            for j in range(c.gqa):
+                h = g * c.gqa + j
+                logits = (kk @ q[h]) * c.scale
+                e = np.exp(logits - logits.max())
+                p = e / e.sum()
+                out[h] = p @ vv
+                win = owner >= 0
+                mass[h] = np.bincount(owner[win], weights=p[win], minlength=self.n_win_cap)
+                sink_mass[h] = p[~win].sum()
+        live = (self.state >= 0) & (self.state != EVICTED)
+        self.score[live] += mass[:, live].sum(axis=0) / c.num_q_heads
+        return out, mass, sink_mass
+
+    def step(self, q, k_new, v_new):
+        self.append(k_new, v_new)
+        return self.attend(q)
+
+    # -- routing event (Algorithm 1) ---------------------------------------
+    def candidates(self):
+        return [int(w) for w in np.nonzero((self.state == FULL) | (self.state == QUANT)
+                                           | (self.state == AGED))[0]]
+
+    def adopt_scores(self, scores):
+        """Take another implementation's scores (lockstep comparison)."""
+        n = min(len(scores), self.n_win_cap)
+        live = (self.state[:n] >= 0) & (self.state[:n] != EVICTED)
+        self.score[:n][live] = np.asarray(scores, dtype=np.float64)[:n][live]
+
+    def route(self):
+        c = self.cfg
+        cand = self.candidates()
+        order = route_order(cand, self.score)
+        was_q = frozenset(w for w in cand if self.state[w] == QUANT)
+        full, quant, evict = tier_split(order, c.capacity_full, c.capacity_quant,
+                                        was_q, c.no_promotion)
+        # F: promote (dequantize, ledger dormant) or admit an aged window
+        for w in full:
+            if self.state[w] == QUANT:
+                kh, vh = dequantize_window(self.ledger[w])
+                self.full_k[w] = rne_bf16(kh)
+                self.full_v[w] = rne_bf16(vh)
+                self.ledger[w]["state"] = DORMANT
+                self.stats["promotions"] += 1
+            elif self.state[w] == AGED:
+                a, b = self.win_range(w)
+                self.full_k[w] = self.k[:, a:b].copy()
+                self.full_v[w] = self.v[:, a:b].copy()
+                self.stats["admissions_full"] += 1
+            self.state[w] = FULL
+        # Q: quantize once, or reactivate a dormant entry
+        half = -(-c.capacity_quant // 2)
+        for rank, w in enumerate(quant):
+            if w not in self.ledger:
+                if self.state[w] == FULL:
+                    src_k, src_v = self.full_k[w], self.full_v[w]
+                else:
+                    a, b = self.win_range(w)
+                    src_k, src_v = self.k[:, a:b], self.v[:, a:b]
+                bits = c.bits if c.bits in (2, 4) else (4 if rank < half else 2)
+                self.ledger[w] = quantize_window(src_k, src_v, bits, c.group)
+                self.stats["first_quantizations"] += 1
+                self.quant_count += 1
+            elif self.ledger[w]["state"] == DORMANT:
+                self.ledger[w]["state"] = ACTIVE
+                self.stats["reactivations"] += 1
+            self.full_k.pop(w, None)
+            self.full_v.pop(w, None)
+            self.state[w] = QUANT
+        # E: release, delete the ledger entry
+        for w in evict:
+            self.full_k.pop(w, None)
+            self.full_v.pop(w, None)
+            self.ledger.pop(w, None)
+            self.state[w] = EVICTED
+            self.stats["evictions"] += 1
+        return full, quant, evict
+
+    # -- perturbation used by the forced-promotion workload -------------------
+    def shift_key_zero_points(self, w: int, delta):
+        """z_c <- RNE_fp16(z_c + delta_c) for every key group of window w.
+
+        delta: [H_kv, d] (float32 values); the sum is formed in float64 first.
+        Shifting every key zero point by delta_c moves each dequantized key of
+        the window by (about) delta_c along channel c.
+        """
+        e = self.ledger[w]
+        d = np.asarray(delta, dtype=np.float32).astype(np.float64)
+        e["kz"] = rne_fp16(e["kz"] + d[:, None, :])
+
+    # -- views used by tests -------------------------------------------------
+    def tiers(self):
+        return self.state.copy()
+
+    def ledger_states(self):
+        out = np.zeros(self.n_win_cap, dtype=np.int64)
+        for w, e in self.ledger.items():
+            out[w] = e["state"]
+        return out
