@@ -1,0 +1,206 @@
+/*
+ * qevict.h -- C ABI of the QEvict tiered decode-step library for MI355X (gfx950).
+ *
+ * QEvict (arXiv 2608.05326) keeps the historical KV cache of every layer as
+ * contiguous windows of W tokens.  Outside a protected sink prefix and recent
+ * region, each window is Full (bf16), Quantized (asymmetric low-bit codes that
+ * attention still reads) or Evicted (Sec. 3.3, cache partition equation).
+ * Every decode step attends over the accessible windows and adds each window's
+ * attention mass, averaged over the query heads, to its cumulative score
+ * (Sec. 3.2, cumulative window score equation).  A routing event ranks the
+ * candidates by score and re-tiers them: top K_f -> Full, next K_q ->
+ * Quantized, the rest deleted, with promotion from the low-bit ledger and
+ * write-once quantization (Sec. 3.3 TopK equations; Algorithm 1).
+ *
+ * Conventions for every call:
+ *  - Tensor arguments are HIP device pointers to contiguous row-major data
+ *    unless a comment says "host".  bf16 values are passed as uint16_t bit
+ *    patterns.  The caller owns every buffer; the library never allocates or
+ *    frees device memory: all state lives in the caller's workspace.
+ *  - Work is enqueued on the HIP stream given to qevict_cache_init and is
+ *    asynchronous unless the comment says "synchronous".  Inputs must stay
+ *    valid until the stream has passed the call.
+ *  - Host-side validation runs before anything is enqueued; on error nothing
+ *    is enqueued and the cache is unchanged.  Errors found on the device
+ *    (non-finite score, exhausted slot pool) latch an error word that the next
+ *    synchronous call reports; the cache then only accepts destroy.
+ *  - qevict_last_error() returns a thread-local message for the last error.
+ *  - A handle is not thread-safe; distinct handles are independent.
+ *  - Per layer the call order is: prefill_assign, then per step
+ *    decode_attend followed by retier at the routing cadence.
+ */
+#ifndef QEVICT_H_
+#define QEVICT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define QEVICT_ABI_VERSION 1
+
+typedef struct qevict_cache qevict_cache;
+typedef int32_t qevict_status;
+
+enum {
+  QEVICT_OK = 0,
+  QEVICT_ERR_INVALID_ARG = -1,   /* null pointer, index out of range, bad shape        */
+  QEVICT_ERR_UNSUPPORTED = -2,   /* shape or option this build does not implement      */
+  QEVICT_ERR_WORKSPACE = -3,     /* workspace too small or misaligned                  */
+  QEVICT_ERR_BAD_STATE = -4,     /* call out of protocol order, or cache poisoned       */
+  QEVICT_ERR_NONFINITE = -5,     /* NaN/Inf in scores or quantizer input               */
+  QEVICT_ERR_CAPACITY = -6,      /* a manual move would exceed K_f or K_q              */
+  QEVICT_ERR_DEVICE = -7         /* a HIP runtime call failed                          */
+};
+
+/* Window tier codes returned by qevict_get_state. */
+enum {
+  QEVICT_TIER_UNUSED = 0,        /* window not reached yet                             */
+  QEVICT_TIER_OPEN = 1,          /* in the recent region, or aged and not yet routed   */
+  QEVICT_TIER_FULL = 2,
+  QEVICT_TIER_QUANT = 3,
+  QEVICT_TIER_EVICTED = 4
+};
+
+/* Ledger (persistent low-bit record) states (Algorithm 1). */
+enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT = 2 };
+
+#define QEVICT_BITS_MIXED_4_2 42       /* int4 for new ledgers ranked in the upper half of Q, int2 below */
+#define QEVICT_OUT_F32 0
+#define QEVICT_OUT_BF16 1
+#define QEVICT_FLAG_NO_PROMOTION 0x1u  /* one-way Full -> Quantized -> Evicted policy (App. K)      */
+#define QEVICT_FLAG_DEBUG_MASSES 0x2u  /* keep per-head window masses of the last step              */
+
+typedef struct {
+  int32_t abi_version;       /* QEVICT_ABI_VERSION                                          */
+  int32_t batch;             /* B sequences, all with the same length                       */
+  int32_t num_layers;
+  int32_t num_q_heads;       /* H_q                                                          */
+  int32_t num_kv_heads;      /* H_kv; H_q % H_kv == 0 and H_q / H_kv <= 16                  */
+  int32_t head_dim;          /* d; this build supports 128                                   */
+  int32_t window_tokens;     /* W; 32 or 64                                                  */
+  int32_t group_size;        /* G; this build requires G == W (keys: one group per channel   */
+                             /*  per window; values: W/... groups of G channels per token)    */
+  int32_t quant_bits;        /* 4, 2 or QEVICT_BITS_MIXED_4_2                                */
+  int32_t sink_tokens;       /* protected sink prefix |S|                                    */
+  int32_t recent_tokens;     /* protected recent region: a window is routed only once it is  */
+                             /* complete and older than this many latest tokens              */
+  int32_t max_context;       /* largest sequence length the cache will hold                  */
+  int32_t capacity_full;     /* K_f windows                                                  */
+  int32_t capacity_quant;    /* K_q windows                                                  */
+  int32_t retier_interval;   /* R: decode steps between routing events (sizes the ring)      */
+  int32_t out_dtype;         /* QEVICT_OUT_F32 or QEVICT_OUT_BF16                            */
+  uint32_t flags;            /* QEVICT_FLAG_*                                                */
+  float softmax_scale;       /* 0 selects 1/sqrt(head_dim)                                    */
+  int32_t num_splits;        /* split-K factor of the attention pass; 0 = automatic          */
+} qevict_config;
+
+typedef struct {
+  int32_t promotions;          /* Quantized -> Full (ledger becomes dormant)   */
+  int32_t admissions_full;     /* aged -> Full                                  */
+  int32_t first_quantizations; /* ledger created (Full or aged -> Quantized)    */
+  int32_t reactivations;       /* Full -> Quantized reusing a dormant ledger    */
+  int32_t evictions;           /* any -> Evicted                                 */
+  int32_t n_full, n_quant_int4, n_quant_int2;  /* tier sizes after the event */
+} qevict_retier_stats;
+
+/* Bytes of device workspace a cache with this config needs (host only). */
+qevict_status qevict_workspace_size(const qevict_config *cfg, size_t *bytes);
+
+/* Create a cache in the caller's workspace (device pointer, 256-byte aligned,
+ * at least qevict_workspace_size bytes; it must outlive the handle).
+ * hip_stream is a hipStream_t (NULL = default stream).  Enqueues the state
+ * initialisation; *out receives a host handle owned by the library. */
+qevict_status qevict_cache_init(const qevict_config *cfg, void *workspace, size_t bytes,
+                                void *hip_stream, qevict_cache **out);
+
+/* Release the host handle (the workspace is the caller's). */
+qevict_status qevict_cache_destroy(qevict_cache *c);
+
+/* Prefill of one layer (Sec. 3.2: prompt attention initialises the window
+ * scores and the first tier assignment).
+ *   k, v        [B, H_kv, prompt_len, d] bf16 prompt keys / values
+ *   init_scores [B, n_w] fp32, n_w = ceil((prompt_len - sink)/W): initial
+ *               cumulative score of every prompt window (also partial ones)
+ * The complete windows outside the sink and recent regions are routed at once
+ * (TopK on init_scores; Quantized windows are quantized from k, v).  The
+ * prompt buffers are only read by work enqueued here. */
+qevict_status qevict_prefill_assign(qevict_cache *c, int32_t layer, const uint16_t *k,
+                                    const uint16_t *v, int32_t prompt_len,
+                                    const float *init_scores);
+
+/* One decode step of one layer (Sec. 3.1 decode attention; Sec. 3.2 score).
+ *   q      [B, H_q, d]  bf16 queries
+ *   k_new, v_new [B, H_kv, d] bf16 key / value of the new token
+ *   out    [B, H_q, d]  out_dtype attention output
+ * Appends the token to the recent region, attends over sink, recent, Full and
+ * Quantized windows (codes dequantized in registers), and adds every live
+ * window's head-averaged attention mass to its cumulative score. */
+qevict_status qevict_decode_attend(qevict_cache *c, int32_t layer, const uint16_t *q,
+                                   const uint16_t *k_new, const uint16_t *v_new, void *out);
+
+/* Routing event of one layer (Sec. 3.3 candidate pool / TopK; Algorithm 1).
+ * Candidates are the Full and Quantized windows plus the windows that left
+ * the recent region; ranking is by score, ties to the lower window index.
+ * Runs the promote / quantize-once / reactivate / evict moves on the device.
+ * stats (host, nullable): when given, the call is synchronous and fills the
+ * batch totals. */
+qevict_status qevict_retier(qevict_cache *c, int32_t layer, qevict_retier_stats *stats);
+
+/* Manual single-window moves (synchronous), with the same ledger rules:
+ * quantize_window moves a Full window to Quantized (quantizing it once, or
+ * reactivating its dormant ledger); QEVICT_ERR_CAPACITY if Q already holds
+ * K_q windows.  promote_window moves a Quantized window to Full (bf16
+ * reconstruction, ledger dormant); QEVICT_ERR_CAPACITY if F is full.
+ * QEVICT_ERR_BAD_STATE if the window is not in the source tier. */
+qevict_status qevict_quantize_window(qevict_cache *c, int32_t layer, int32_t seq, int32_t window);
+qevict_status qevict_promote_window(qevict_cache *c, int32_t layer, int32_t seq, int32_t window);
+
+/* Inspection (synchronous; host output buffers, each of length >= cap,
+ * any may be NULL).  *n_windows receives the number of windows reached so far. */
+qevict_status qevict_get_state(qevict_cache *c, int32_t layer, int32_t seq, int8_t *tiers,
+                               float *scores, int8_t *ledger, int8_t *bits, int32_t cap,
+                               int32_t *n_windows);
+
+/* Copy one window out in natural layouts (synchronous; host buffers, NULL to skip).
+ *   codes_k, codes_v [H_kv, W, d] uint8 codes of the window's ledger
+ *   meta_k  [H_kv, 2, W/G, d] fp16 bits: scale then zero point per key group
+ *   meta_v  [H_kv, 2, W, d/G] fp16 bits: scale then zero point per value group
+ *   full_k, full_v [H_kv, W, d] bf16 bits of the Full-tier copy
+ * Returns QEVICT_ERR_BAD_STATE when a requested part does not exist. */
+qevict_status qevict_export_window(qevict_cache *c, int32_t layer, int32_t seq, int32_t window,
+                                   uint8_t *codes_k, uint8_t *codes_v, uint16_t *meta_k,
+                                   uint16_t *meta_v, uint16_t *full_k, uint16_t *full_v);
+
+/* Test workload support (synchronous): add delta [H_kv, d] (host fp32) to the
+ * key zero points of a window's ledger, z <- RNE_fp16(z + delta) with the sum
+ * formed in double, which shifts every dequantized key of the window. */
+qevict_status qevict_debug_shift_keys(qevict_cache *c, int32_t layer, int32_t seq, int32_t window,
+                                      const float *delta);
+
+/* Per-head window masses of the last decode step of a layer (synchronous;
+ * needs QEVICT_FLAG_DEBUG_MASSES).  masses: host [B, H_q, n_cap + 1] fp32,
+ * the last column is the sink mass; n_cap from qevict_get_state's capacity. */
+qevict_status qevict_debug_masses(qevict_cache *c, int32_t layer, float *masses, int32_t n_cap);
+
+/* Kernel timing with HIP events on the cache's stream (off by default).
+ * kernel: 0 attention pass, 1 split merge + score accumulation, 2 re-rank,
+ * 3 quantize, 4 promote.  read returns the summed milliseconds and the number
+ * of timed launches since enable, and is synchronous. */
+qevict_status qevict_profile_enable(qevict_cache *c, int32_t on);
+qevict_status qevict_profile_read(qevict_cache *c, int32_t kernel, double *total_ms, int64_t *count);
+
+/* Algorithmic bytes the last decode_attend of a layer had to read/write in
+ * the attention pass (live windows' codes/values, recent and sink tokens,
+ * queries, outputs, scores; synchronous). */
+qevict_status qevict_last_attend_bytes(qevict_cache *c, int32_t layer, int64_t *bytes);
+
+const char *qevict_status_string(qevict_status s);
+const char *qevict_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* QEVICT_H_ */

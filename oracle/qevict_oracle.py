@@ -273,8 +273,8 @@ class QEvictUnit:
         self._start_windows()
         self._age()
 
-    def accessible(self, g: int):
-        """Keys, values and owning window (-1 = sink) of every token KV head g attends to.
+    def accessible(self):
+        """Keys, values [H_kv, n, d] and owning window [n] (-1 = sink) of every token attended to.
 
         Windows appear in index order (chronological); Quantized windows enter as
         their dequantized values z + s c.
@@ -283,26 +283,25 @@ class QEvictUnit:
         ks, vs, owner = [], [], []
         ns = min(c.sink, self.T)
         if ns:
-            ks.append(self.k[g, :ns])
-            vs.append(self.v[g, :ns])
+            ks.append(self.k[:, :ns])
+            vs.append(self.v[:, :ns])
             owner.append(np.full(ns, -1))
         for w in np.nonzero(self.state >= 0)[0]:
             st = self.state[w]
             a, b = self.win_range(w)
             b = min(b, self.T)
             if st == FULL:
-                kk, vv = self.full_k[w][g], self.full_v[w][g]
+                kk, vv = self.full_k[w], self.full_v[w]
             elif st == QUANT:
-                kh, vh = dequantize_window(self.ledger[w])
-                kk, vv = kh[g], vh[g]
+                kk, vv = dequantize_window(self.ledger[w])
             elif st in (OPEN, AGED):
-                kk, vv = self.k[g, a:b], self.v[g, a:b]
+                kk, vv = self.k[:, a:b], self.v[:, a:b]
             else:
                 continue
             ks.append(kk)
             vs.append(vv)
-            owner.append(np.full(len(kk), w))
-        return np.concatenate(ks), np.concatenate(vs), np.concatenate(owner)
+            owner.append(np.full(kk.shape[1], w))
+        return np.concatenate(ks, axis=1), np.concatenate(vs, axis=1), np.concatenate(owner)
 
     def attend(self, q):
         """Attention of all query heads; accumulate window scores.
@@ -315,17 +314,16 @@ class QEvictUnit:
         out = np.zeros((c.num_q_heads, c.head_dim))
         mass = np.zeros((c.num_q_heads, self.n_win_cap))
         sink_mass = np.zeros(c.num_q_heads)
-        for g in range(c.num_kv_heads):
-            kk, vv, owner = self.accessible(g)
-            for j in range(c.gqa):
-                h = g * c.gqa + j
-                logits = (kk @ q[h]) * c.scale
-                e = np.exp(logits - logits.max())
-                p = e / e.sum()
-                out[h] = p @ vv
-                win = owner >= 0
-                mass[h] = np.bincount(owner[win], weights=p[win], minlength=self.n_win_cap)
-                sink_mass[h] = p[~win].sum()
+        kk, vv, owner = self.accessible()
+        win = owner >= 0
+        for h in range(c.num_q_heads):
+            g = h // c.gqa
+            logits = (kk[g] @ q[h]) * c.scale
+            e = np.exp(logits - logits.max())
+            p = e / e.sum()
+            out[h] = p @ vv[g]
+            mass[h] = np.bincount(owner[win], weights=p[win], minlength=self.n_win_cap)
+            sink_mass[h] = p[~win].sum()
         live = (self.state >= 0) & (self.state != EVICTED)
         self.score[live] += mass[:, live].sum(axis=0) / c.num_q_heads
         return out, mass, sink_mass

@@ -1,0 +1,14 @@
+"""QEvict tiered decode step for MI355X (gfx950): HIP kernels behind a C ABI.
+
+The library (libqevict.so, built from csrc/ by ``build.py``) implements the
+per-step hot path of QEvict (arXiv 2608.05326): split-K decode attention over
+bf16 and quantized windows with per-window mass accumulation, TopK re-tiering
+and the quantize / promote migrations.  ``qevict`` is the ctypes binding.
+"""
+from .qevict import (  # noqa: F401
+    Cache, Config, QEvictError, RetierStats, load_library, workspace_size, SYMBOLS,
+    TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED,
+    LEDGER_NONE, LEDGER_ACTIVE, LEDGER_DORMANT, BITS_MIXED_4_2, OUT_F32, OUT_BF16,
+    FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES,
+    KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_QUANTIZE, KERNEL_PROMOTE,
+)

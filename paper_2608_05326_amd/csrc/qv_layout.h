@@ -1,0 +1,151 @@
+// Device memory layout of the tiered KV cache (shared by host runtime and kernels).
+//
+// Everything lives in one caller-provided workspace:
+//   [header][unit 0][unit 1]...   unit u = layer * B + seq
+// Each unit block holds the bf16 window pool (Full tier), the recent-region
+// ring, the sink slots, the quantized-record pool (Quantized tier plus dormant
+// ledgers), the per-window state arrays, the live-window list, the migration
+// work lists and the split-K partials of that (sequence, layer).
+//
+// bf16 window slot, one KV head (W tokens x 128 channels, K then V):
+//   K part: chunk (tb, kb), tb = t/16, kb = c/32, 1 KiB each; lane L = 16q + r
+//           holds K[16 tb + r][32 kb + 8 q + j], j = 0..7 (16 bytes at 16 L).
+//           This is the A operand of a 16x16x32 MFMA with tokens as rows.
+//   V part: chunk (kt, cb), kt = t/32, cb = c/16; lane L = 16q + r holds
+//           V[tok(kt, q, j)][16 cb + r], j = 0..7, with
+//           tok(kt, q, j) = 32 kt + 16 (j/4) + 4 q + (j%4):
+//           the B operand of the P.V MFMA whose k index matches the row layout
+//           of the QK^T accumulator, so probabilities never move between lanes.
+// Quantized record, one KV head: [K codes][V codes][K meta][V meta]
+//   codes use the same (entry, lane) positions as the bf16 chunks, 8 codes per
+//   (entry, lane); code j = 2i + o sits at bit 16 o + b (4 e' + i), e' = the
+//   entry's position inside its 32-bit word (int4: one entry per word, int2:
+//   two), so an AND with 0x000F000F / 0x00030003 after a shift yields two codes
+//   in the two fp16 halves of a register.
+//   K meta: fp16 scale[128] then zero[128] (one key group per channel per window).
+//   V meta: per (kt, q, value group g): fp16 scale[8] then zero[8] for the 8
+//           tokens tok(kt, q, 0..7).
+#pragma once
+#include <stdint.h>
+
+#if defined(__HIPCC__)
+#define QV_HD __host__ __device__ inline
+#else
+#define QV_HD inline
+#endif
+
+namespace qv {
+
+constexpr int kHeadDim = 128;
+constexpr int kMaxGqa = 16;
+constexpr int kMaxCand = 4096;      // candidates per routing event (one workgroup sorts them)
+constexpr int kAttnThreads = 256;
+constexpr int kRetierThreads = 1024;
+
+// tier codes stored on the device (same numbers as the ABI)
+enum : int8_t { T_UNUSED = 0, T_OPEN = 1, T_FULL = 2, T_QUANT = 3, T_EVICTED = 4 };
+enum : int8_t { L_NONE = 0, L_ACTIVE = 1, L_DORMANT = 2 };
+// live-item kinds
+enum : int32_t { KIND_BF16 = 0, KIND_Q4 = 1, KIND_Q2 = 2 };
+// per-unit counters
+enum : int32_t { CNT_ITEMS = 0, CNT_QUANT = 1, CNT_PROMOTE = 2, CNT_ERROR = 3, CNT_BYTES_LO = 4,
+                 CNT_N = 16 };
+// device error bits
+enum : int32_t { ERR_NONFINITE = 1, ERR_POOL = 2, ERR_RANGE = 4, ERR_CAND = 8 };
+// stats slots (same order as qevict_retier_stats)
+enum : int32_t { ST_PROMO = 0, ST_ADMIT = 1, ST_FIRSTQ = 2, ST_REACT = 3, ST_EVICT = 4,
+                 ST_NF = 5, ST_NQ4 = 6, ST_NQ2 = 7, ST_N = 8 };
+// work-list sources
+enum : int32_t { SRC_FSLOT = 0, SRC_RING = 1, SRC_PROMPT = 2, SRC_QSLOT = 3 };
+constexpr int kQEntry = 5;   // ints per work-list entry: win, src_kind, src_idx, dst, bits
+
+struct Geometry {
+  int32_t B, H_q, H_kv, gqa, d, W, G;
+  int32_t bits_cfg;     // 4, 2 or 42
+  int32_t qbits_max;    // 4 or 2: code area size of a record
+  int32_t K_f, K_q, n_qslots;
+  int32_t NR, NS;       // ring slots, sink slots
+  int32_t sink, recent;
+  int32_t nwc;          // window capacity per unit
+  int32_t max_items;    // Full + Quantized + ring + sink items
+  int32_t max_fq;       // K_f + K_q
+  int32_t n_split;
+  int32_t out_bf16;
+  uint32_t flags;
+  float scale_log2;     // softmax scale * log2(e)
+  int64_t fhead_bytes;  // one KV head of a bf16 slot: W*d*2 (K) + W*d*2 (V)
+  int64_t fslot_bytes;  // H_kv * fhead_bytes
+  int64_t qcodes_bytes; // W*d*qbits_max/8, one of K or V
+  int64_t qrec_bytes;   // one KV head of a quantized record
+  int64_t qslot_bytes;  // H_kv * qrec_bytes
+  int32_t cost_bf16, cost_q4, cost_q2;   // split balancing weights per item
+};
+
+struct UnitLayout {
+  int64_t unit_bytes;
+  int64_t fpool, ring, sinkp, qpool;
+  int64_t tier, ledger, bits, fslot, qslot, score;
+  int64_t fowner, qowner;
+  int64_t item_win, item_ref, item_cost;
+  int64_t qlist, plist, counts, stats;
+  int64_t partial, mref, dbg_mass;
+};
+
+QV_HD int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+// ---- bf16 slot offsets (bytes inside one KV head block) ---------------------
+QV_HD int64_t k_elem_off(int t, int c) {
+  int tb = t >> 4, r = t & 15, kb = c >> 5, q = (c >> 3) & 3, j = c & 7;
+  return ((int64_t)((tb * 4 + kb) * 64 + q * 16 + r) * 16) + j * 2;
+}
+QV_HD void v_tok_pos(int t, int* kt, int* q, int* j) {
+  int tt = t & 31;
+  *kt = t >> 5;
+  *q = (tt & 15) >> 2;
+  *j = ((tt >> 4) << 2) | (tt & 3);
+}
+QV_HD int v_tok(int kt, int q, int j) { return 32 * kt + 16 * (j >> 2) + 4 * q + (j & 3); }
+QV_HD int64_t v_elem_off(int W, int t, int c) {
+  int kt, q, j;
+  v_tok_pos(t, &kt, &q, &j);
+  int cb = c >> 4, r = c & 15;
+  return (int64_t)W * kHeadDim * 2 + ((int64_t)((kt * 8 + cb) * 64 + q * 16 + r) * 16) + j * 2;
+}
+
+// ---- quantized record offsets -----------------------------------------------
+// location of code (entry e, lane L, element j) of one code area
+QV_HD void code_loc(int bits, int e, int L, int j, int64_t* byte_off, int* shift) {
+  int per_word = 4 / bits;                 // entries in one 32-bit word: int4 -> 1, int2 -> 2
+  int word = e / per_word, ee = e % per_word;
+  int i = j >> 1, o = j & 1;
+  *byte_off = ((int64_t)((word >> 2) * 64 + L) * 16) + (word & 3) * 4;
+  *shift = o * 16 + bits * (4 * ee + i);
+}
+QV_HD void k_code_pos(int t, int c, int* e, int* L, int* j) {
+  *e = (t >> 4) * 4 + (c >> 5);
+  *L = ((c >> 3) & 3) * 16 + (t & 15);
+  *j = c & 7;
+}
+QV_HD void v_code_pos(int t, int c, int* e, int* L, int* j) {
+  int kt, q, jj;
+  v_tok_pos(t, &kt, &q, &jj);
+  *e = kt * 8 + (c >> 4);
+  *L = q * 16 + (c & 15);
+  *j = jj;
+}
+// meta offsets inside a record (after the two code areas)
+QV_HD int64_t meta_k_off(const Geometry& g) { return 2 * g.qcodes_bytes; }
+QV_HD int64_t meta_v_off(const Geometry& g) { return 2 * g.qcodes_bytes + 4 * kHeadDim; }
+// byte offset of the V scale of token t, value group vg (zero point at +16)
+QV_HD int64_t meta_v_elem(const Geometry& g, int t, int vg) {
+  int kt, q, j;
+  v_tok_pos(t, &kt, &q, &j);
+  int ng = kHeadDim / g.G;
+  return meta_v_off(g) + ((int64_t)((kt * 4 + q) * ng + vg) * 32) + j * 2;
+}
+
+QV_HD int item_cost(const Geometry& g, int kind) {
+  return kind == KIND_BF16 ? g.cost_bf16 : (kind == KIND_Q4 ? g.cost_q4 : g.cost_q2);
+}
+
+}  // namespace qv

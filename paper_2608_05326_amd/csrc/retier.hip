@@ -1,0 +1,471 @@
+// Routing event: re-rank the candidate windows and re-tier them
+// (QEvict Sec. 3.3 candidate pool and TopK equations; Algorithm 1).
+//
+// One 1024-thread workgroup per sequence:
+//   1. candidates = current Full and Quantized windows (the live list, in
+//      window order) followed by the windows that left the recent region;
+//   2. 64-bit keys (score descending, then window ascending) sorted with a
+//      bitonic network in LDS;
+//   3. sorted position < K_f -> Full, < K_f + K_q -> Quantized, else Evicted
+//      (one-way policy: Full only from candidates that are not Quantized);
+//   4. Algorithm 1 transitions: promotions keep the ledger dormant, first
+//      demotions request a quantization, dormant ledgers are reactivated,
+//      evictions release slots and delete the ledger;
+//   5. freed slots are handed to the new requests in ascending slot order by
+//      prefix sums (deterministic), and the quantize / promote work lists and
+//      the new live list (window order, with split-balancing cost prefix) are
+//      written for the kernels that follow on the stream.
+#include "qv_device.h"
+
+namespace qv {
+
+// Total order key: ascending key = descending score, ties to the lower candidate
+// index (candidates are stored in window order, so this is the lower window).
+__device__ __forceinline__ uint64_t rank_key(float f, uint32_t cand) {
+  if (f == 0.f) f = 0.f;   // -0 and +0 compare equal
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)(~asc) << 32) | cand;
+}
+
+// Exclusive prefix sum of buf[0..n) (n <= kMaxCand) in place; returns the total.
+__device__ int block_scan(int32_t* buf, int n, int32_t* tmp) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int PER = kMaxCand / kRetierThreads;
+  int v[PER];
+  int sum = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int i = tid * PER + k;
+    v[k] = i < n ? buf[i] : 0;
+    sum += v[k];
+  }
+  int x = sum;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) tmp[wave] = x;
+  __syncthreads();
+  if (wave == 0) {
+    int w = lane < kRetierThreads / 64 ? tmp[lane] : 0;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(w, off);
+      if (lane >= off) w += y;
+    }
+    if (lane < kRetierThreads / 64) tmp[32 + lane] = w;
+  }
+  __syncthreads();
+  int run = x - sum + (wave > 0 ? tmp[32 + wave - 1] : 0);
+  const int total = tmp[32 + kRetierThreads / 64 - 1];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int i = tid * PER + k;
+    if (i < n) buf[i] = run;
+    run += v[k];
+  }
+  __syncthreads();
+  return total;
+}
+
+__global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
+  const Geometry& G = a.g;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  constexpr int NT = kRetierThreads;
+  constexpr int PER = kMaxCand / NT;
+
+  __shared__ uint64_t skey[kMaxCand];
+  __shared__ int32_t scw[kMaxCand];
+  __shared__ int32_t sinfo[kMaxCand];
+  __shared__ int32_t sa[kMaxCand];
+  __shared__ int32_t tmp[64];
+  __shared__ int32_t sstat[ST_N];
+  int32_t* sb = (int32_t*)skey;               // after the sort: two int arrays
+  int32_t* sc = (int32_t*)skey + kMaxCand;
+
+  uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
+  int8_t* tier = (int8_t*)(ub + a.L.tier);
+  int8_t* ledger = (int8_t*)(ub + a.L.ledger);
+  int8_t* bits = (int8_t*)(ub + a.L.bits);
+  int32_t* fslot = (int32_t*)(ub + a.L.fslot);
+  int32_t* qslot = (int32_t*)(ub + a.L.qslot);
+  float* score = (float*)(ub + a.L.score);
+  int32_t* fowner = (int32_t*)(ub + a.L.fowner);
+  int32_t* qowner = (int32_t*)(ub + a.L.qowner);
+  int32_t* iwin = (int32_t*)(ub + a.L.item_win);
+  int32_t* iref = (int32_t*)(ub + a.L.item_ref);
+  int32_t* icost = (int32_t*)(ub + a.L.item_cost);
+  int32_t* qlist = (int32_t*)(ub + a.L.qlist);
+  int32_t* plist = (int32_t*)(ub + a.L.plist);
+  int32_t* counts = (int32_t*)(ub + a.L.counts);
+  int32_t* stats = (int32_t*)(ub + a.L.stats);
+
+  if (tid < ST_N) sstat[tid] = 0;
+  if (a.prefill) {
+    for (int w = tid; w < a.n_init; w += NT) {
+      const float v = a.init_scores[(int64_t)b * a.n_init + w];
+      if (!__builtin_isfinite(v)) set_error(counts, ERR_NONFINITE);
+      score[w] = v;
+    }
+  }
+  __syncthreads();
+
+  const int n_fq = a.prefill ? 0 : counts[CNT_ITEMS];
+  const int n_aged = a.aged_w1 - a.aged_w0;
+  const int n_cand = n_fq + n_aged;
+  if (n_cand > kMaxCand) {
+    if (tid == 0) set_error(counts, ERR_CAND);
+    return;
+  }
+  int n_pow = 1;
+  while (n_pow < n_cand) n_pow <<= 1;
+  for (int c = tid; c < n_pow; c += NT) {
+    if (c < n_cand) {
+      const int w = c < n_fq ? iwin[c] : a.aged_w0 + (c - n_fq);
+      scw[c] = w;
+      const float f = score[w];
+      if (!__builtin_isfinite(f)) set_error(counts, ERR_NONFINITE);
+      skey[c] = rank_key(f, (uint32_t)c);
+    } else {
+      skey[c] = ~0ull;
+    }
+  }
+  __syncthreads();
+
+  // ---- bitonic sort, ascending ----
+  for (int k = 2; k <= n_pow; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < n_pow; i += NT) {
+        const int ixj = i ^ j;
+        if (ixj > i) {
+          const uint64_t x = skey[i], y = skey[ixj];
+          const bool up = (i & k) == 0;
+          if ((x > y) == up) {
+            skey[i] = y;
+            skey[ixj] = x;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  // ---- tier by sorted position ----
+  const bool one_way = (G.flags & 1u) != 0;
+  if (!one_way) {
+    for (int p = tid; p < n_cand; p += NT) {
+      const int c = (int)(skey[p] & 0xFFFFFFFFu);
+      const int nt = p < G.K_f ? T_FULL : (p < G.K_f + G.K_q ? T_QUANT : T_EVICTED);
+      const int rq = p - G.K_f;
+      sinfo[c] = nt | ((rq < 0 ? 0 : rq) << 8);
+    }
+    __syncthreads();
+  } else {
+    // Full only from candidates that are not currently Quantized
+    for (int p = tid; p < n_cand; p += NT) {
+      const int c = (int)(skey[p] & 0xFFFFFFFFu);
+      const int old = c < n_fq ? tier[scw[c]] : T_OPEN;
+      sa[p] = old != T_QUANT ? 1 : 0;
+    }
+    __syncthreads();
+    block_scan(sa, n_cand, tmp);
+    for (int p = tid; p < n_cand; p += NT) {
+      const int c = (int)(skey[p] & 0xFFFFFFFFu);
+      const int old = c < n_fq ? tier[scw[c]] : T_OPEN;
+      const bool f = old != T_QUANT && sa[p] < G.K_f;
+      sinfo[c] = f ? T_FULL : 0;
+    }
+    __syncthreads();
+    for (int p = tid; p < n_cand; p += NT) {
+      const int c = (int)(skey[p] & 0xFFFFFFFFu);
+      sa[p] = sinfo[c] == T_FULL ? 0 : 1;
+    }
+    __syncthreads();
+    block_scan(sa, n_cand, tmp);
+    for (int p = tid; p < n_cand; p += NT) {
+      const int c = (int)(skey[p] & 0xFFFFFFFFu);
+      if (sinfo[c] != T_FULL) {
+        const int rq = sa[p];
+        sinfo[c] = (rq < G.K_q ? T_QUANT : T_EVICTED) | (rq << 8);
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- transitions; release slots ----
+  const int half_q = (G.K_q + 1) / 2;
+  int my_old[PER], my_nt[PER], my_req[PER], my_bits[PER], my_oldf[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    my_req[k] = 0;
+    if (c >= n_cand) continue;
+    const int w = scw[c];
+    const int info = sinfo[c];
+    const int nt = info & 0xFF, rq = info >> 8;
+    const int old = c < n_fq ? tier[w] : T_OPEN;
+    const int led = c < n_fq ? ledger[w] : L_NONE;
+    my_old[k] = old;
+    my_nt[k] = nt;
+    my_oldf[k] = old == T_FULL ? fslot[w] : -1;
+    const bool needF = nt == T_FULL && old != T_FULL;
+    const bool needQ = nt == T_QUANT && old != T_QUANT && led == L_NONE;
+    my_req[k] = (needF ? 1 : 0) | (needQ ? 2 : 0);
+    my_bits[k] = G.bits_cfg == 42 ? (rq < half_q ? 4 : 2) : G.bits_cfg;
+    if (old == T_FULL && nt != T_FULL) fowner[fslot[w]] = -1;
+    if (nt == T_EVICTED && led != L_NONE) qowner[qslot[w]] = -1;
+  }
+  __syncthreads();
+
+  // ---- free lists and request ranks ----
+  for (int i = tid; i < G.K_f; i += NT) sa[i] = fowner[i] < 0 ? 1 : 0;
+  __syncthreads();
+  const int nfreeF = block_scan(sa, G.K_f, tmp);
+  for (int i = tid; i < G.K_f; i += NT)
+    if (fowner[i] < 0) sb[sa[i]] = i;   // sb: free Full slots ascending
+  __syncthreads();
+  for (int i = tid; i < G.n_qslots; i += NT) sa[i] = qowner[i] < 0 ? 1 : 0;
+  __syncthreads();
+  const int nfreeQ = block_scan(sa, G.n_qslots, tmp);
+  for (int i = tid; i < G.n_qslots; i += NT)
+    if (qowner[i] < 0) sc[sa[i]] = i;   // sc: free quantized slots ascending
+  __syncthreads();
+  for (int c = tid; c < n_cand; c += NT) sa[c] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    if (c < n_cand) sa[c] = my_req[k] & 1;
+  }
+  __syncthreads();
+  const int nreqF = block_scan(sa, n_cand, tmp);
+  int my_rankF[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    my_rankF[k] = c < n_cand ? sa[c] : 0;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    if (c < n_cand) sa[c] = (my_req[k] >> 1) & 1;
+  }
+  __syncthreads();
+  const int nreqQ = block_scan(sa, n_cand, tmp);
+
+  // ---- apply: new slots, ledger states, work lists ----
+  const int src_aged = a.prefill ? SRC_PROMPT : SRC_RING;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    if (c >= n_cand) continue;
+    const int w = scw[c];
+    const int old = my_old[k], nt = my_nt[k];
+    const int led = c < n_fq ? ledger[w] : L_NONE;
+    int fs = nt == T_FULL ? (old == T_FULL ? fslot[w] : -1) : -1;
+    if (my_req[k] & 1) {
+      const int rk = my_rankF[k];
+      if (rk < nfreeF) {
+        fs = sb[rk];
+        fowner[fs] = w;
+        int32_t* e = plist + rk * kQEntry;
+        if (old == T_QUANT) {
+          e[0] = w; e[1] = SRC_QSLOT; e[2] = qslot[w]; e[3] = fs; e[4] = bits[w];
+          ledger[w] = L_DORMANT;
+          atomicAdd(&sstat[ST_PROMO], 1);
+        } else {
+          e[0] = w; e[1] = src_aged; e[2] = a.prefill ? w : w % G.NR; e[3] = fs; e[4] = 0;
+          atomicAdd(&sstat[ST_ADMIT], 1);
+        }
+      } else {
+        set_error(counts, ERR_POOL);
+      }
+    }
+    if (my_req[k] & 2) {
+      const int rk = sa[c];
+      if (rk < nfreeQ) {
+        const int qs = sc[rk];
+        qowner[qs] = w;
+        qslot[w] = qs;
+        bits[w] = (int8_t)my_bits[k];
+        ledger[w] = L_ACTIVE;
+        int32_t* e = qlist + rk * kQEntry;
+        e[0] = w;
+        if (old == T_FULL) { e[1] = SRC_FSLOT; e[2] = my_oldf[k]; }
+        else { e[1] = src_aged; e[2] = a.prefill ? w : w % G.NR; }
+        e[3] = qs;
+        e[4] = my_bits[k];
+        atomicAdd(&sstat[ST_FIRSTQ], 1);
+      } else {
+        set_error(counts, ERR_POOL);
+      }
+    }
+    if (nt == T_QUANT && old == T_FULL && led == L_DORMANT) {
+      ledger[w] = L_ACTIVE;
+      atomicAdd(&sstat[ST_REACT], 1);
+    }
+    if (nt == T_EVICTED) {
+      ledger[w] = L_NONE;
+      qslot[w] = -1;
+      atomicAdd(&sstat[ST_EVICT], 1);
+    }
+    fslot[w] = fs;
+    tier[w] = (int8_t)nt;
+  }
+  __syncthreads();
+
+  // ---- rebuild the live list (window order) ----
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    if (c < n_cand) sa[c] = (my_nt[k] == T_FULL || my_nt[k] == T_QUANT) ? 1 : 0;
+  }
+  __syncthreads();
+  const int n_items = block_scan(sa, n_cand, tmp);
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    if (c < n_cand && (my_nt[k] == T_FULL || my_nt[k] == T_QUANT)) {
+      const int w = scw[c];
+      const int pos = sa[c];
+      int kind, slot;
+      if (my_nt[k] == T_FULL) {
+        kind = KIND_BF16;
+        slot = fslot[w];
+        atomicAdd(&sstat[ST_NF], 1);
+      } else {
+        kind = bits[w] == 4 ? KIND_Q4 : KIND_Q2;
+        slot = qslot[w];
+        atomicAdd(&sstat[kind == KIND_Q4 ? ST_NQ4 : ST_NQ2], 1);
+      }
+      iwin[pos] = w;
+      iref[pos] = (kind << 28) | slot;
+      sb[pos] = item_cost(G, kind);
+    }
+  }
+  __syncthreads();
+  const int tot_cost = block_scan(sb, n_items, tmp);
+  for (int i = tid; i < n_items; i += NT) icost[i] = sb[i];
+  if (tid == 0) {
+    icost[n_items] = tot_cost;
+    counts[CNT_ITEMS] = n_items;
+    counts[CNT_QUANT] = nreqQ < nfreeQ ? nreqQ : nfreeQ;
+    counts[CNT_PROMOTE] = nreqF < nfreeF ? nreqF : nfreeF;
+  }
+  if (tid < ST_N) stats[tid] = sstat[tid];
+}
+
+// Manual single-window move (one thread): F -> Q (quantize once or reactivate)
+// or Q -> F (promotion), with the same ledger rules as a routing event.
+__global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
+  const Geometry& G = a.g;
+  uint8_t* ub = a.base + (int64_t)seq * a.L.unit_bytes;
+  int8_t* tier = (int8_t*)(ub + a.L.tier);
+  int8_t* ledger = (int8_t*)(ub + a.L.ledger);
+  int8_t* bits = (int8_t*)(ub + a.L.bits);
+  int32_t* fslot = (int32_t*)(ub + a.L.fslot);
+  int32_t* qslot = (int32_t*)(ub + a.L.qslot);
+  int32_t* fowner = (int32_t*)(ub + a.L.fowner);
+  int32_t* qowner = (int32_t*)(ub + a.L.qowner);
+  int32_t* iwin = (int32_t*)(ub + a.L.item_win);
+  int32_t* iref = (int32_t*)(ub + a.L.item_ref);
+  int32_t* icost = (int32_t*)(ub + a.L.item_cost);
+  int32_t* qlist = (int32_t*)(ub + a.L.qlist);
+  int32_t* plist = (int32_t*)(ub + a.L.plist);
+  int32_t* counts = (int32_t*)(ub + a.L.counts);
+  const int w = window;
+  counts[CNT_QUANT] = 0;
+  counts[CNT_PROMOTE] = 0;
+  int kind = -1, slot = -1;
+  if (to_quant) {
+    const int fs = fslot[w];
+    if (ledger[w] == L_DORMANT) {
+      ledger[w] = L_ACTIVE;
+    } else {
+      int qs = -1;
+      for (int i = 0; i < G.n_qslots && qs < 0; ++i)
+        if (qowner[i] < 0) qs = i;
+      if (qs < 0) { set_error(counts, ERR_POOL); return; }
+      const int nb = G.bits_cfg == 42 ? 4 : G.bits_cfg;
+      qowner[qs] = w;
+      qslot[w] = qs;
+      bits[w] = (int8_t)nb;
+      ledger[w] = L_ACTIVE;
+      int32_t* e = qlist;
+      e[0] = w; e[1] = SRC_FSLOT; e[2] = fs; e[3] = qs; e[4] = nb;
+      counts[CNT_QUANT] = 1;
+    }
+    fowner[fs] = -1;
+    fslot[w] = -1;
+    tier[w] = T_QUANT;
+    kind = bits[w] == 4 ? KIND_Q4 : KIND_Q2;
+    slot = qslot[w];
+  } else {
+    int fs = -1;
+    for (int i = 0; i < G.K_f && fs < 0; ++i)
+      if (fowner[i] < 0) fs = i;
+    if (fs < 0) { set_error(counts, ERR_POOL); return; }
+    fowner[fs] = w;
+    fslot[w] = fs;
+    ledger[w] = L_DORMANT;
+    tier[w] = T_FULL;
+    int32_t* e = plist;
+    e[0] = w; e[1] = SRC_QSLOT; e[2] = qslot[w]; e[3] = fs; e[4] = bits[w];
+    counts[CNT_PROMOTE] = 1;
+    kind = KIND_BF16;
+    slot = fs;
+  }
+  // the window keeps its position in the live list; refresh its entry and the cost prefix
+  const int n = counts[CNT_ITEMS];
+  int run = 0;
+  for (int i = 0; i < n; ++i) {
+    if (iwin[i] == w) iref[i] = (kind << 28) | slot;
+    icost[i] = run;
+    run += item_cost(G, iref[i] >> 28);
+  }
+  icost[n] = run;
+}
+
+// State initialisation of every unit block (grid-stride over units).
+__global__ void k_init_units(Geometry G, UnitLayout L, uint8_t* base, int n_units) {
+  for (int u = blockIdx.x; u < n_units; u += gridDim.x) {
+    uint8_t* ub = base + (int64_t)u * L.unit_bytes;
+    for (int w = threadIdx.x; w < G.nwc; w += blockDim.x) {
+      ((int8_t*)(ub + L.tier))[w] = T_UNUSED;
+      ((int8_t*)(ub + L.ledger))[w] = L_NONE;
+      ((int8_t*)(ub + L.bits))[w] = 0;
+      ((int32_t*)(ub + L.fslot))[w] = -1;
+      ((int32_t*)(ub + L.qslot))[w] = -1;
+      ((float*)(ub + L.score))[w] = 0.f;
+    }
+    for (int i = threadIdx.x; i < G.K_f; i += blockDim.x) ((int32_t*)(ub + L.fowner))[i] = -1;
+    for (int i = threadIdx.x; i < G.n_qslots; i += blockDim.x) ((int32_t*)(ub + L.qowner))[i] = -1;
+    for (int i = threadIdx.x; i < CNT_N; i += blockDim.x) ((int32_t*)(ub + L.counts))[i] = 0;
+    for (int i = threadIdx.x; i < ST_N; i += blockDim.x) ((int32_t*)(ub + L.stats))[i] = 0;
+    if (threadIdx.x == 0) ((int32_t*)(ub + L.item_cost))[0] = 0;
+    // recent-ring and sink slots start as zeros (partial windows read them)
+    const int64_t nz = (int64_t)(G.NR + G.NS) * G.fslot_bytes / 16;
+    u32x4* z = (u32x4*)(ub + L.ring);
+    for (int64_t i = threadIdx.x; i < nz; i += blockDim.x) z[i] = (u32x4){0, 0, 0, 0};
+  }
+}
+
+hipError_t launch_retier(const RetierArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_retier, dim3(a.g.B), dim3(kRetierThreads), 0, st, a);
+  return hipGetLastError();
+}
+hipError_t launch_manual_move(const RetierArgs& a, int seq, int window, int to_quant, hipStream_t st) {
+  hipLaunchKernelGGL(k_manual_move, dim3(1), dim3(1), 0, st, a, seq, window, to_quant);
+  return hipGetLastError();
+}
+hipError_t launch_init_units(const Geometry& g, const UnitLayout& L, uint8_t* base, int n_units,
+                             hipStream_t st) {
+  hipLaunchKernelGGL(k_init_units, dim3(n_units < 1024 ? n_units : 1024), dim3(256), 0, st, g, L,
+                     base, n_units);
+  return hipGetLastError();
+}
+
+}  // namespace qv

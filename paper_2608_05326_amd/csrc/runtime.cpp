@@ -1,0 +1,779 @@
+// Host runtime of the QEvict tiered decode-step library: configuration
+// checks, workspace planning, per-layer protocol state, kernel launches and
+// the synchronous inspection calls.  No device memory is ever allocated here.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/qevict.h"
+#include "qv_layout.h"
+
+namespace qv {
+struct AttnArgs;
+struct RetierArgs;
+struct MigrateArgs;
+struct PackArgs;
+}  // namespace qv
+#include "qv_device.h"
+
+namespace qv {
+hipError_t launch_attend(const AttnArgs& a, hipStream_t st);
+hipError_t launch_merge(const AttnArgs& a, hipStream_t st);
+hipError_t launch_retier(const RetierArgs& a, hipStream_t st);
+hipError_t launch_manual_move(const RetierArgs& a, int seq, int window, int to_quant, hipStream_t st);
+hipError_t launch_init_units(const Geometry& g, const UnitLayout& L, uint8_t* base, int n_units,
+                             hipStream_t st);
+hipError_t launch_quantize(const MigrateArgs& a, int max_entries, hipStream_t st);
+hipError_t launch_promote(const MigrateArgs& a, int max_entries, hipStream_t st);
+hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st);
+}  // namespace qv
+
+using namespace qv;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+qevict_status fail(qevict_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+constexpr int64_t kHeaderBytes = 256;
+constexpr int kNumTimed = 5;
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+struct LayerState {
+  int T = 0;              // tokens held (all sequences)
+  int routed_end = 0;     // windows below this index have been routed
+  bool prefilled = false;
+  int64_t last_bytes = 0;
+};
+
+struct TimedLaunch {
+  int kernel;
+  hipEvent_t start, stop;
+};
+
+}  // namespace
+
+struct qevict_cache {
+  qevict_config cfg;
+  Geometry g;
+  UnitLayout L;
+  uint8_t* ws = nullptr;
+  size_t ws_bytes = 0;
+  hipStream_t stream = nullptr;
+  std::vector<LayerState> layers;
+  bool poisoned = false;
+  bool profiling = false;
+  std::vector<TimedLaunch> pending;
+  std::vector<hipEvent_t> free_events;
+  double prof_ms[kNumTimed] = {0};
+  int64_t prof_n[kNumTimed] = {0};
+};
+
+namespace {
+
+qevict_status check_config(const qevict_config* c) {
+  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "config is NULL");
+  if (c->abi_version != QEVICT_ABI_VERSION)
+    return fail(QEVICT_ERR_UNSUPPORTED, "abi_version %d, library implements %d", c->abi_version,
+                QEVICT_ABI_VERSION);
+  if (c->batch < 1 || c->num_layers < 1 || c->num_q_heads < 1 || c->num_kv_heads < 1)
+    return fail(QEVICT_ERR_INVALID_ARG, "batch, layers and head counts must be positive");
+  if (c->num_q_heads % c->num_kv_heads != 0)
+    return fail(QEVICT_ERR_INVALID_ARG, "num_q_heads %% num_kv_heads != 0");
+  if (c->num_q_heads / c->num_kv_heads > kMaxGqa || c->num_q_heads > 64)
+    return fail(QEVICT_ERR_UNSUPPORTED, "at most 16 query heads per KV head and 64 query heads");
+  if (c->head_dim != kHeadDim) return fail(QEVICT_ERR_UNSUPPORTED, "head_dim must be 128");
+  if (c->window_tokens != 32 && c->window_tokens != 64)
+    return fail(QEVICT_ERR_UNSUPPORTED, "window_tokens must be 32 or 64");
+  if (c->group_size != c->window_tokens)
+    return fail(QEVICT_ERR_UNSUPPORTED, "group_size must equal window_tokens");
+  if (c->quant_bits != 4 && c->quant_bits != 2 && c->quant_bits != QEVICT_BITS_MIXED_4_2)
+    return fail(QEVICT_ERR_UNSUPPORTED, "quant_bits must be 4, 2 or 42");
+  if (c->sink_tokens < 0 || c->recent_tokens < 0 || c->capacity_full < 0 || c->capacity_quant < 0)
+    return fail(QEVICT_ERR_INVALID_ARG, "negative sink, recent or capacity");
+  if (c->max_context <= c->sink_tokens)
+    return fail(QEVICT_ERR_INVALID_ARG, "max_context must exceed sink_tokens");
+  if (c->retier_interval < 1) return fail(QEVICT_ERR_INVALID_ARG, "retier_interval must be >= 1");
+  if (c->out_dtype != QEVICT_OUT_F32 && c->out_dtype != QEVICT_OUT_BF16)
+    return fail(QEVICT_ERR_INVALID_ARG, "out_dtype");
+  if (c->flags & ~(QEVICT_FLAG_NO_PROMOTION | QEVICT_FLAG_DEBUG_MASSES))
+    return fail(QEVICT_ERR_INVALID_ARG, "unknown flags 0x%x", c->flags);
+  if (!(c->softmax_scale >= 0.f) || !std::isfinite(c->softmax_scale))
+    return fail(QEVICT_ERR_INVALID_ARG, "softmax_scale");
+  if (c->num_splits < 0 || c->num_splits > 256)
+    return fail(QEVICT_ERR_INVALID_ARG, "num_splits must be in [0, 256]");
+  const int W = c->window_tokens;
+  const int nr = ceil_div(c->recent_tokens, W) + ceil_div(c->retier_interval, W) + 2;
+  if (c->capacity_full + c->capacity_quant + nr > kMaxCand)
+    return fail(QEVICT_ERR_UNSUPPORTED, "K_f + K_q + ring windows must be <= %d", kMaxCand);
+  if (c->capacity_full + c->capacity_quant < 1)
+    return fail(QEVICT_ERR_INVALID_ARG, "K_f + K_q must be >= 1");
+  return QEVICT_OK;
+}
+
+void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
+  memset(g, 0, sizeof *g);
+  memset(L, 0, sizeof *L);
+  g->B = c->batch;
+  g->H_q = c->num_q_heads;
+  g->H_kv = c->num_kv_heads;
+  g->gqa = c->num_q_heads / c->num_kv_heads;
+  g->d = c->head_dim;
+  g->W = c->window_tokens;
+  g->G = c->group_size;
+  g->bits_cfg = c->quant_bits;
+  g->qbits_max = c->quant_bits == 2 ? 2 : 4;
+  g->K_f = c->capacity_full;
+  g->K_q = c->capacity_quant;
+  g->n_qslots = c->capacity_quant + c->capacity_full;
+  g->NR = ceil_div(c->recent_tokens, g->W) + ceil_div(c->retier_interval, g->W) + 2;
+  g->NS = ceil_div(c->sink_tokens, g->W);
+  g->sink = c->sink_tokens;
+  g->recent = c->recent_tokens;
+  g->nwc = ceil_div(c->max_context - c->sink_tokens, g->W);
+  g->max_fq = g->K_f + g->K_q;
+  g->max_items = g->max_fq + g->NR + g->NS;
+  int ns = c->num_splits;
+  if (ns == 0) {
+    // about two workgroups per compute unit over the whole grid
+    ns = ceil_div(512, g->B * g->H_kv);
+    ns = ns < 1 ? 1 : (ns > 64 ? 64 : ns);
+    int per_split = ceil_div(g->max_items, ns);
+    if (per_split < 2) ns = ceil_div(g->max_items, 2);
+  }
+  g->n_split = ns;
+  g->out_bf16 = c->out_dtype == QEVICT_OUT_BF16;
+  g->flags = c->flags;
+  const float scale = c->softmax_scale > 0.f ? c->softmax_scale : 1.0f / std::sqrt((float)g->d);
+  g->scale_log2 = scale * 1.4426950408889634f;
+  g->fhead_bytes = (int64_t)g->W * g->d * 4;
+  g->fslot_bytes = g->fhead_bytes * g->H_kv;
+  g->qcodes_bytes = (int64_t)g->W * g->d * g->qbits_max / 8;
+  g->qrec_bytes = 2 * g->qcodes_bytes + 4 * g->d + (int64_t)g->W * (g->d / g->G) * 4;
+  g->qslot_bytes = g->qrec_bytes * g->H_kv;
+  // split-balancing weights (per 32 tokens): bf16 windows are byte heavy,
+  // quantized windows carry extra expansion work per byte
+  g->cost_bf16 = 16 * (g->W / 32);
+  g->cost_q4 = 8 * (g->W / 32);
+  g->cost_q2 = 7 * (g->W / 32);
+
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    int64_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  L->fpool = take((int64_t)g->K_f * g->fslot_bytes);
+  L->ring = take((int64_t)g->NR * g->fslot_bytes);
+  L->sinkp = take((int64_t)g->NS * g->fslot_bytes);   // directly after the ring (zeroed together)
+  L->qpool = take((int64_t)g->n_qslots * g->qslot_bytes);
+  L->tier = take(g->nwc);
+  L->ledger = take(g->nwc);
+  L->bits = take(g->nwc);
+  L->fslot = take(4LL * g->nwc);
+  L->qslot = take(4LL * g->nwc);
+  L->score = take(4LL * g->nwc);
+  L->fowner = take(4LL * (g->K_f + 1));
+  L->qowner = take(4LL * (g->n_qslots + 1));
+  L->item_win = take(4LL * (g->max_fq + 1));
+  L->item_ref = take(4LL * (g->max_fq + 1));
+  L->item_cost = take(4LL * (g->max_fq + 1));
+  L->qlist = take(4LL * kQEntry * (g->max_fq + 1));
+  L->plist = take(4LL * kQEntry * (g->max_fq + 1));
+  L->counts = take(4LL * CNT_N);
+  L->stats = take(4LL * ST_N);
+  L->partial = take(4LL * g->H_q * g->n_split * (g->d + 2));
+  L->mref = take(8LL * g->H_q * g->max_items);
+  L->dbg_mass = take((c->flags & QEVICT_FLAG_DEBUG_MASSES) ? 4LL * g->H_q * (g->nwc + 1) : 0);
+  L->unit_bytes = align256(off);
+}
+
+bool ring_and_sink_adjacent(const UnitLayout& L, const Geometry& g) {
+  return L.sinkp == align256(L.ring + (int64_t)g.NR * g.fslot_bytes);
+}
+
+qevict_status hip_fail(hipError_t e, const char* what) {
+  return fail(QEVICT_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+uint8_t* unit_base(qevict_cache* c, int layer, int seq) {
+  return c->ws + kHeaderBytes + ((int64_t)layer * c->g.B + seq) * c->L.unit_bytes;
+}
+
+qevict_status check_handle(qevict_cache* c, int layer) {
+  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
+  if (c->poisoned) return fail(QEVICT_ERR_BAD_STATE, "cache is in an error state; destroy it");
+  if (layer < 0 || layer >= c->cfg.num_layers)
+    return fail(QEVICT_ERR_INVALID_ARG, "layer %d out of range", layer);
+  return QEVICT_OK;
+}
+
+// ---- kernel timing ----
+hipEvent_t take_event(qevict_cache* c) {
+  if (!c->free_events.empty()) {
+    hipEvent_t e = c->free_events.back();
+    c->free_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void fold_pending(qevict_cache* c) {
+  if (c->pending.empty()) return;
+  (void)hipEventSynchronize(c->pending.back().stop);
+  for (auto& t : c->pending) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, t.start, t.stop) == hipSuccess) {
+      c->prof_ms[t.kernel] += ms;
+      c->prof_n[t.kernel] += 1;
+    }
+    c->free_events.push_back(t.start);
+    c->free_events.push_back(t.stop);
+  }
+  c->pending.clear();
+}
+
+template <typename F>
+hipError_t timed(qevict_cache* c, int kernel, F&& launch) {
+  if (!c->profiling) return launch();
+  if (c->pending.size() > 2048) fold_pending(c);
+  hipEvent_t a = take_event(c), b = take_event(c);
+  if (!a || !b) return launch();
+  (void)hipEventRecord(a, c->stream);
+  hipError_t e = launch();
+  (void)hipEventRecord(b, c->stream);
+  c->pending.push_back({kernel, a, b});
+  return e;
+}
+
+qevict_status device_errors(qevict_cache* c, int layer) {
+  int32_t cnt[CNT_N];
+  for (int b = 0; b < c->g.B; ++b) {
+    hipError_t e = hipMemcpyAsync(cnt, unit_base(c, layer, b) + c->L.counts, sizeof cnt,
+                                  hipMemcpyDeviceToHost, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) return hip_fail(e, "reading device error word");
+    if (cnt[CNT_ERROR]) {
+      c->poisoned = true;
+      const int f = cnt[CNT_ERROR];
+      if (f & ERR_NONFINITE) return fail(QEVICT_ERR_NONFINITE, "non-finite window score (seq %d)", b);
+      if (f & ERR_RANGE) return fail(QEVICT_ERR_NONFINITE, "quantizer input outside fp16 range (seq %d)", b);
+      return fail(QEVICT_ERR_BAD_STATE, "device error flags 0x%x (seq %d)", f, b);
+    }
+  }
+  return QEVICT_OK;
+}
+
+void fill_common(qevict_cache* c, int layer, Geometry* g, UnitLayout* L, uint8_t** base) {
+  *g = c->g;
+  *L = c->L;
+  *base = unit_base(c, layer, 0);
+}
+
+int n_started(const Geometry& g, int T) { return T <= g.sink ? 0 : ceil_div(T - g.sink, g.W); }
+int aged_end(const Geometry& g, int T) {
+  int n = T - g.recent - g.sink;
+  return n <= 0 ? 0 : n / g.W;
+}
+
+// double -> fp16 bits, round to nearest even (finite, in range)
+uint16_t host_rne_fp16(double x) {
+  uint16_t sign = std::signbit(x) ? 0x8000 : 0;
+  double a = std::fabs(x);
+  if (a == 0.0) return sign;
+  int e;
+  std::frexp(a, &e);              // a = m 2^e, m in [0.5, 1)
+  int q = e - 11;                  // unit in the last place for 11 significant bits
+  if (q < -24) q = -24;            // subnormal spacing
+  double y = std::nearbyint(std::ldexp(a, -q));   // default rounding: ties to even
+  double r = std::ldexp(y, q);
+  if (r > 65504.0) return (uint16_t)(sign | 0x7C00);
+  _Float16 h = (_Float16)(float)r;   // exact: r is an fp16 value
+  uint16_t bits;
+  memcpy(&bits, &h, 2);
+  return (uint16_t)(bits | sign);
+}
+
+double host_fp16_to_double(uint16_t h) {
+  _Float16 v;
+  memcpy(&v, &h, 2);
+  return (double)(float)v;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* qevict_status_string(qevict_status s) {
+  switch (s) {
+    case QEVICT_OK: return "ok";
+    case QEVICT_ERR_INVALID_ARG: return "invalid argument";
+    case QEVICT_ERR_UNSUPPORTED: return "unsupported";
+    case QEVICT_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case QEVICT_ERR_BAD_STATE: return "bad state";
+    case QEVICT_ERR_NONFINITE: return "non-finite value";
+    case QEVICT_ERR_CAPACITY: return "capacity exceeded";
+    case QEVICT_ERR_DEVICE: return "device error";
+    default: return "unknown status";
+  }
+}
+
+const char* qevict_last_error(void) { return g_last_error.c_str(); }
+
+qevict_status qevict_workspace_size(const qevict_config* cfg, size_t* bytes) {
+  qevict_status s = check_config(cfg);
+  if (s) return s;
+  if (!bytes) return fail(QEVICT_ERR_INVALID_ARG, "bytes is NULL");
+  Geometry g;
+  UnitLayout L;
+  plan(cfg, &g, &L);
+  *bytes = (size_t)(kHeaderBytes + (int64_t)cfg->num_layers * cfg->batch * L.unit_bytes);
+  return QEVICT_OK;
+}
+
+qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_t bytes,
+                                void* hip_stream, qevict_cache** out) {
+  qevict_status s = check_config(cfg);
+  if (s) return s;
+  if (!out) return fail(QEVICT_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  size_t need = 0;
+  qevict_workspace_size(cfg, &need);
+  if (!workspace || ((uintptr_t)workspace & 255))
+    return fail(QEVICT_ERR_WORKSPACE, "workspace must be a 256-byte aligned device pointer");
+  if (bytes < need) return fail(QEVICT_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", bytes, need);
+  qevict_cache* c = new qevict_cache();
+  c->cfg = *cfg;
+  plan(cfg, &c->g, &c->L);
+  if (!ring_and_sink_adjacent(c->L, c->g)) {
+    delete c;
+    return fail(QEVICT_ERR_UNSUPPORTED, "internal layout");
+  }
+  c->ws = (uint8_t*)workspace;
+  c->ws_bytes = bytes;
+  c->stream = (hipStream_t)hip_stream;
+  c->layers.resize(cfg->num_layers);
+  hipError_t e = launch_init_units(c->g, c->L, c->ws + kHeaderBytes, cfg->num_layers * cfg->batch,
+                                   c->stream);
+  if (e != hipSuccess) {
+    delete c;
+    return hip_fail(e, "initialising the cache");
+  }
+  *out = c;
+  return QEVICT_OK;
+}
+
+qevict_status qevict_cache_destroy(qevict_cache* c) {
+  if (!c) return QEVICT_OK;
+  for (auto& t : c->pending) {
+    (void)hipEventDestroy(t.start);
+    (void)hipEventDestroy(t.stop);
+  }
+  for (auto e : c->free_events) (void)hipEventDestroy(e);
+  delete c;
+  return QEVICT_OK;
+}
+
+qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16_t* k,
+                                    const uint16_t* v, int32_t prompt_len,
+                                    const float* init_scores) {
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  LayerState& ls = c->layers[layer];
+  const Geometry& g = c->g;
+  if (ls.prefilled) return fail(QEVICT_ERR_BAD_STATE, "layer %d already prefilled", layer);
+  if (!k || !v || !init_scores) return fail(QEVICT_ERR_INVALID_ARG, "null prompt pointer");
+  if (((uintptr_t)k & 15) || ((uintptr_t)v & 15))
+    return fail(QEVICT_ERR_INVALID_ARG, "prompt keys / values must be 16-byte aligned");
+  if (prompt_len < g.sink || prompt_len < 1 || prompt_len > c->cfg.max_context)
+    return fail(QEVICT_ERR_INVALID_ARG, "prompt_len %d outside [max(1, sink), max_context]", prompt_len);
+  const int n_hist = aged_end(g, prompt_len);
+  const int n_init = n_started(g, prompt_len);
+  if (n_hist > kMaxCand)
+    return fail(QEVICT_ERR_UNSUPPORTED, "%d prompt windows to route; at most %d", n_hist, kMaxCand);
+  if (n_init - n_hist > g.NR)
+    return fail(QEVICT_ERR_UNSUPPORTED, "recent region needs more ring slots than configured");
+
+  Geometry gg;
+  UnitLayout L;
+  uint8_t* base;
+  fill_common(c, layer, &gg, &L, &base);
+  PackArgs pa{gg, L, base, k, v, prompt_len, 0, g.sink};
+  hipError_t e = launch_pack_tokens(pa, c->stream);   // sink tokens
+  if (e == hipSuccess) {
+    pa.tok0 = g.sink + n_hist * g.W;
+    pa.tok1 = prompt_len;
+    e = launch_pack_tokens(pa, c->stream);            // tail: recent region and partial window
+  }
+  RetierArgs ra{gg, L, base, 1, 0, n_hist, init_scores, n_init};
+  if (e == hipSuccess) e = timed(c, 2, [&] { return launch_retier(ra, c->stream); });
+  MigrateArgs ma{gg, L, base, k, v, prompt_len};
+  if (e == hipSuccess) e = timed(c, 3, [&] { return launch_quantize(ma, g.K_q, c->stream); });
+  if (e == hipSuccess) e = timed(c, 4, [&] { return launch_promote(ma, g.K_f, c->stream); });
+  if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  ls.T = prompt_len;
+  ls.routed_end = n_hist;
+  ls.prefilled = true;
+  return QEVICT_OK;
+}
+
+qevict_status qevict_decode_attend(qevict_cache* c, int32_t layer, const uint16_t* q,
+                                   const uint16_t* k_new, const uint16_t* v_new, void* out) {
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  LayerState& ls = c->layers[layer];
+  const Geometry& g = c->g;
+  if (!ls.prefilled) return fail(QEVICT_ERR_BAD_STATE, "layer %d not prefilled", layer);
+  if (!q || !k_new || !v_new || !out) return fail(QEVICT_ERR_INVALID_ARG, "null pointer");
+  if (((uintptr_t)q & 15) || ((uintptr_t)k_new & 15))
+    return fail(QEVICT_ERR_INVALID_ARG, "q and k_new must be 16-byte aligned");
+  if (ls.T + 1 > c->cfg.max_context)
+    return fail(QEVICT_ERR_BAD_STATE, "max_context %d reached", c->cfg.max_context);
+  const int T = ls.T + 1;
+  const int n_ring = n_started(g, T) - ls.routed_end;
+  if (n_ring > g.NR)
+    return fail(QEVICT_ERR_BAD_STATE, "%d unrouted windows exceed the ring (%d); call retier", n_ring,
+                g.NR);
+  AttnArgs a;
+  fill_common(c, layer, &a.g, &a.L, &a.base);
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.out = out;
+  a.T = T;
+  a.ring_w0 = ls.routed_end;
+  a.n_ring = n_ring;
+  a.n_sink_items = g.NS;
+  hipError_t e = hipSuccess;
+  if (g.flags & QEVICT_FLAG_DEBUG_MASSES) {
+    for (int b = 0; b < g.B && e == hipSuccess; ++b)
+      e = hipMemsetAsync(unit_base(c, layer, b) + c->L.dbg_mass, 0, 4LL * g.H_q * (g.nwc + 1),
+                         c->stream);
+  }
+  if (e == hipSuccess) e = timed(c, 0, [&] { return launch_attend(a, c->stream); });
+  if (e == hipSuccess) e = timed(c, 1, [&] { return launch_merge(a, c->stream); });
+  if (e != hipSuccess) return hip_fail(e, "decode_attend launch");
+  ls.T = T;
+  return QEVICT_OK;
+}
+
+qevict_status qevict_retier(qevict_cache* c, int32_t layer, qevict_retier_stats* stats) {
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  LayerState& ls = c->layers[layer];
+  const Geometry& g = c->g;
+  if (!ls.prefilled) return fail(QEVICT_ERR_BAD_STATE, "layer %d not prefilled", layer);
+  const int a1 = aged_end(g, ls.T);
+  const int a0 = ls.routed_end;
+  Geometry gg;
+  UnitLayout L;
+  uint8_t* base;
+  fill_common(c, layer, &gg, &L, &base);
+  RetierArgs ra{gg, L, base, 0, a0, a1 > a0 ? a1 : a0, nullptr, 0};
+  MigrateArgs ma{gg, L, base, nullptr, nullptr, 0};
+  const int max_q = g.K_q < g.max_fq ? g.K_q : g.max_fq;
+  hipError_t e = timed(c, 2, [&] { return launch_retier(ra, c->stream); });
+  if (e == hipSuccess) e = timed(c, 3, [&] { return launch_quantize(ma, max_q, c->stream); });
+  if (e == hipSuccess) e = timed(c, 4, [&] { return launch_promote(ma, g.K_f, c->stream); });
+  if (e != hipSuccess) return hip_fail(e, "retier launch");
+  if (a1 > a0) ls.routed_end = a1;
+  if (stats) {
+    memset(stats, 0, sizeof *stats);
+    for (int b = 0; b < g.B; ++b) {
+      int32_t st[ST_N];
+      e = hipMemcpyAsync(st, unit_base(c, layer, b) + c->L.stats, sizeof st, hipMemcpyDeviceToHost,
+                         c->stream);
+      if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+      if (e != hipSuccess) return hip_fail(e, "reading retier stats");
+      stats->promotions += st[ST_PROMO];
+      stats->admissions_full += st[ST_ADMIT];
+      stats->first_quantizations += st[ST_FIRSTQ];
+      stats->reactivations += st[ST_REACT];
+      stats->evictions += st[ST_EVICT];
+      stats->n_full += st[ST_NF];
+      stats->n_quant_int4 += st[ST_NQ4];
+      stats->n_quant_int2 += st[ST_NQ2];
+    }
+    return device_errors(c, layer);
+  }
+  return QEVICT_OK;
+}
+
+static qevict_status read_window_state(qevict_cache* c, int layer, int seq, int window, int8_t* tier,
+                                       int8_t* led) {
+  uint8_t* ub = unit_base(c, layer, seq);
+  hipError_t e = hipMemcpyAsync(tier, ub + c->L.tier + window, 1, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(led, ub + c->L.ledger + window, 1, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  return e == hipSuccess ? QEVICT_OK : hip_fail(e, "reading window state");
+}
+
+static qevict_status manual_move(qevict_cache* c, int layer, int seq, int window, int to_quant) {
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  const Geometry& g = c->g;
+  if (!c->layers[layer].prefilled) return fail(QEVICT_ERR_BAD_STATE, "layer not prefilled");
+  if (seq < 0 || seq >= g.B) return fail(QEVICT_ERR_INVALID_ARG, "seq %d out of range", seq);
+  if (window < 0 || window >= g.nwc) return fail(QEVICT_ERR_INVALID_ARG, "window %d out of range", window);
+  if ((s = device_errors(c, layer))) return s;
+  int8_t tier = 0, led = 0;
+  if ((s = read_window_state(c, layer, seq, window, &tier, &led))) return s;
+  if (tier != (to_quant ? T_FULL : T_QUANT))
+    return fail(QEVICT_ERR_BAD_STATE, "window %d is not in the %s tier", window,
+                to_quant ? "Full" : "Quantized");
+  if (!to_quant && (g.flags & QEVICT_FLAG_NO_PROMOTION))
+    return fail(QEVICT_ERR_BAD_STATE, "promotion disabled by QEVICT_FLAG_NO_PROMOTION");
+  // tier occupancy
+  std::vector<int8_t> tiers(g.nwc);
+  hipError_t e = hipMemcpyAsync(tiers.data(), unit_base(c, layer, seq) + c->L.tier, g.nwc,
+                                hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(e, "reading tiers");
+  int nf = 0, nq = 0;
+  for (int8_t t : tiers) {
+    nf += t == T_FULL;
+    nq += t == T_QUANT;
+  }
+  if (to_quant && nq >= g.K_q) return fail(QEVICT_ERR_CAPACITY, "Quantized tier holds K_q windows");
+  if (!to_quant && nf >= g.K_f) return fail(QEVICT_ERR_CAPACITY, "Full tier holds K_f windows");
+  Geometry gg;
+  UnitLayout L;
+  uint8_t* base;
+  fill_common(c, layer, &gg, &L, &base);
+  RetierArgs ra{gg, L, base, 0, 0, 0, nullptr, 0};
+  // the migration kernels read work lists per sequence: run them on this sequence only
+  Geometry one = gg;
+  one.B = 1;
+  MigrateArgs ma{one, L, unit_base(c, layer, seq), nullptr, nullptr, 0};
+  e = launch_manual_move(ra, seq, window, to_quant, c->stream);
+  if (e == hipSuccess) e = launch_quantize(ma, 1, c->stream);
+  if (e == hipSuccess) e = launch_promote(ma, 1, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(e, "manual move");
+  return device_errors(c, layer);
+}
+
+qevict_status qevict_quantize_window(qevict_cache* c, int32_t layer, int32_t seq, int32_t window) {
+  return manual_move(c, layer, seq, window, 1);
+}
+
+qevict_status qevict_promote_window(qevict_cache* c, int32_t layer, int32_t seq, int32_t window) {
+  return manual_move(c, layer, seq, window, 0);
+}
+
+qevict_status qevict_get_state(qevict_cache* c, int32_t layer, int32_t seq, int8_t* tiers,
+                               float* scores, int8_t* ledger, int8_t* bits, int32_t cap,
+                               int32_t* n_windows) {
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  const Geometry& g = c->g;
+  if (seq < 0 || seq >= g.B) return fail(QEVICT_ERR_INVALID_ARG, "seq %d out of range", seq);
+  if (cap < 0) return fail(QEVICT_ERR_INVALID_ARG, "cap < 0");
+  const LayerState& ls = c->layers[layer];
+  const int nst = n_started(g, ls.T);
+  const int n = nst < cap ? nst : cap;
+  if (n_windows) *n_windows = nst;
+  uint8_t* ub = unit_base(c, layer, seq);
+  hipError_t e = hipSuccess;
+  if (tiers && n) e = hipMemcpyAsync(tiers, ub + c->L.tier, n, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess && scores && n)
+    e = hipMemcpyAsync(scores, ub + c->L.score, 4LL * n, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess && ledger && n)
+    e = hipMemcpyAsync(ledger, ub + c->L.ledger, n, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess && bits && n)
+    e = hipMemcpyAsync(bits, ub + c->L.bits, n, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(e, "get_state copy");
+  if (tiers)
+    for (int w = ls.routed_end; w < n; ++w) tiers[w] = T_OPEN;   // recent region / not yet routed
+  return device_errors(c, layer);
+}
+
+qevict_status qevict_export_window(qevict_cache* c, int32_t layer, int32_t seq, int32_t window,
+                                   uint8_t* codes_k, uint8_t* codes_v, uint16_t* meta_k,
+                                   uint16_t* meta_v, uint16_t* full_k, uint16_t* full_v) {
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  const Geometry& g = c->g;
+  if (seq < 0 || seq >= g.B) return fail(QEVICT_ERR_INVALID_ARG, "seq %d out of range", seq);
+  if (window < 0 || window >= g.nwc) return fail(QEVICT_ERR_INVALID_ARG, "window out of range");
+  uint8_t* ub = unit_base(c, layer, seq);
+  int8_t tier, led, nb;
+  int32_t fs, qs;
+  hipError_t e = hipMemcpyAsync(&tier, ub + c->L.tier + window, 1, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(&led, ub + c->L.ledger + window, 1, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(&nb, ub + c->L.bits + window, 1, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(&fs, ub + c->L.fslot + 4LL * window, 4, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(&qs, ub + c->L.qslot + 4LL * window, 4, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(e, "export_window state");
+  const int W = g.W, d = kHeadDim, ng = d / g.G;
+  const bool want_q = codes_k || codes_v || meta_k || meta_v;
+  const bool want_f = full_k || full_v;
+  if (want_q && (led == L_NONE || qs < 0)) return fail(QEVICT_ERR_BAD_STATE, "window has no ledger");
+  if (want_f && (tier != T_FULL || fs < 0)) return fail(QEVICT_ERR_BAD_STATE, "window is not Full");
+  std::vector<uint8_t> rec(g.qslot_bytes), slot(g.fslot_bytes);
+  if (want_q)
+    e = hipMemcpyAsync(rec.data(), ub + c->L.qpool + (int64_t)qs * g.qslot_bytes, g.qslot_bytes,
+                       hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess && want_f)
+    e = hipMemcpyAsync(slot.data(), ub + c->L.fpool + (int64_t)fs * g.fslot_bytes, g.fslot_bytes,
+                       hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(e, "export_window copy");
+  for (int h = 0; h < g.H_kv; ++h) {
+    const uint8_t* r = rec.data() + h * g.qrec_bytes;
+    const uint8_t* f = slot.data() + h * g.fhead_bytes;
+    for (int t = 0; t < W; ++t)
+      for (int ch = 0; ch < d; ++ch) {
+        const int64_t o = ((int64_t)h * W + t) * d + ch;
+        int ee, L, j, sh;
+        int64_t off;
+        if (codes_k) {
+          k_code_pos(t, ch, &ee, &L, &j);
+          code_loc(nb, ee, L, j, &off, &sh);
+          uint32_t w32;
+          memcpy(&w32, r + off, 4);
+          codes_k[o] = (uint8_t)((w32 >> sh) & ((1u << nb) - 1));
+        }
+        if (codes_v) {
+          v_code_pos(t, ch, &ee, &L, &j);
+          code_loc(nb, ee, L, j, &off, &sh);
+          uint32_t w32;
+          memcpy(&w32, r + g.qcodes_bytes + off, 4);
+          codes_v[o] = (uint8_t)((w32 >> sh) & ((1u << nb) - 1));
+        }
+        if (full_k) memcpy(full_k + o, f + k_elem_off(t, ch), 2);
+        if (full_v) memcpy(full_v + o, f + v_elem_off(W, t, ch), 2);
+      }
+    if (meta_k) {   // [h][2][W/G][d]; W == G: one group per channel
+      memcpy(meta_k + (int64_t)h * 2 * d, r + meta_k_off(g), 2 * d);
+      memcpy(meta_k + (int64_t)h * 2 * d + d, r + meta_k_off(g) + 2 * d, 2 * d);
+    }
+    if (meta_v) {   // [h][2][W][d/G]
+      for (int t = 0; t < W; ++t)
+        for (int vg = 0; vg < ng; ++vg) {
+          const int64_t mo = meta_v_elem(g, t, vg);
+          memcpy(meta_v + ((int64_t)h * 2 * W + t) * ng + vg, r + mo, 2);
+          memcpy(meta_v + ((int64_t)h * 2 * W + W + t) * ng + vg, r + mo + 16, 2);
+        }
+    }
+  }
+  return QEVICT_OK;
+}
+
+qevict_status qevict_debug_shift_keys(qevict_cache* c, int32_t layer, int32_t seq, int32_t window,
+                                      const float* delta) {
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  const Geometry& g = c->g;
+  if (seq < 0 || seq >= g.B || window < 0 || window >= g.nwc || !delta)
+    return fail(QEVICT_ERR_INVALID_ARG, "seq / window / delta");
+  uint8_t* ub = unit_base(c, layer, seq);
+  int8_t led;
+  int32_t qs;
+  hipError_t e = hipMemcpyAsync(&led, ub + c->L.ledger + window, 1, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(&qs, ub + c->L.qslot + 4LL * window, 4, hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(e, "shift_keys state");
+  if (led == L_NONE || qs < 0) return fail(QEVICT_ERR_BAD_STATE, "window has no ledger");
+  const int d = kHeadDim;
+  std::vector<uint16_t> z(d);
+  for (int h = 0; h < g.H_kv; ++h) {
+    uint8_t* zp = ub + c->L.qpool + (int64_t)qs * g.qslot_bytes + h * g.qrec_bytes + meta_k_off(g) + 2 * d;
+    e = hipMemcpyAsync(z.data(), zp, 2 * d, hipMemcpyDeviceToHost, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) return hip_fail(e, "shift_keys read");
+    for (int ch = 0; ch < d; ++ch)
+      z[ch] = host_rne_fp16(host_fp16_to_double(z[ch]) + (double)delta[h * d + ch]);
+    e = hipMemcpyAsync(zp, z.data(), 2 * d, hipMemcpyHostToDevice, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) return hip_fail(e, "shift_keys write");
+  }
+  return QEVICT_OK;
+}
+
+qevict_status qevict_debug_masses(qevict_cache* c, int32_t layer, float* masses, int32_t n_cap) {
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  const Geometry& g = c->g;
+  if (!(g.flags & QEVICT_FLAG_DEBUG_MASSES))
+    return fail(QEVICT_ERR_BAD_STATE, "cache created without QEVICT_FLAG_DEBUG_MASSES");
+  if (!masses || n_cap != g.nwc) return fail(QEVICT_ERR_INVALID_ARG, "n_cap must equal %d", g.nwc);
+  for (int b = 0; b < g.B; ++b) {
+    hipError_t e = hipMemcpyAsync(masses + (int64_t)b * g.H_q * (g.nwc + 1),
+                                  unit_base(c, layer, b) + c->L.dbg_mass, 4LL * g.H_q * (g.nwc + 1),
+                                  hipMemcpyDeviceToHost, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) return hip_fail(e, "debug masses");
+  }
+  return QEVICT_OK;
+}
+
+qevict_status qevict_profile_enable(qevict_cache* c, int32_t on) {
+  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
+  fold_pending(c);
+  c->profiling = on != 0;
+  for (int i = 0; i < kNumTimed; ++i) {
+    c->prof_ms[i] = 0;
+    c->prof_n[i] = 0;
+  }
+  return QEVICT_OK;
+}
+
+qevict_status qevict_profile_read(qevict_cache* c, int32_t kernel, double* total_ms, int64_t* count) {
+  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
+  if (kernel < 0 || kernel >= kNumTimed) return fail(QEVICT_ERR_INVALID_ARG, "kernel id");
+  fold_pending(c);
+  if (total_ms) *total_ms = c->prof_ms[kernel];
+  if (count) *count = c->prof_n[kernel];
+  return QEVICT_OK;
+}
+
+qevict_status qevict_last_attend_bytes(qevict_cache* c, int32_t layer, int64_t* bytes) {
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  if (!bytes) return fail(QEVICT_ERR_INVALID_ARG, "bytes is NULL");
+  const Geometry& g = c->g;
+  const LayerState& ls = c->layers[layer];
+  int64_t total = 0;
+  for (int b = 0; b < g.B; ++b) {
+    int32_t st[ST_N];
+    hipError_t e = hipMemcpyAsync(st, unit_base(c, layer, b) + c->L.stats, sizeof st,
+                                  hipMemcpyDeviceToHost, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) return hip_fail(e, "reading tier sizes");
+    const int64_t per_f = g.fslot_bytes;
+    const int64_t meta = (int64_t)g.H_kv * (4 * kHeadDim + (int64_t)g.W * (kHeadDim / g.G) * 4);
+    const int64_t per_q4 = (int64_t)g.H_kv * 2 * g.W * kHeadDim * 4 / 8 + meta;
+    const int64_t per_q2 = (int64_t)g.H_kv * 2 * g.W * kHeadDim * 2 / 8 + meta;
+    const int recent_tok = ls.T - g.sink - ls.routed_end * g.W;
+    const int64_t tok_bytes = (int64_t)2 * g.H_kv * kHeadDim * 2;
+    total += st[ST_NF] * per_f + st[ST_NQ4] * per_q4 + st[ST_NQ2] * per_q2 +
+             (int64_t)(recent_tok + g.sink) * tok_bytes +
+             (int64_t)2 * g.H_q * kHeadDim * 2 +                  // q in, out (bf16 equivalent)
+             (int64_t)(st[ST_NF] + st[ST_NQ4] + st[ST_NQ2] + n_started(g, ls.T) - ls.routed_end) * 8;
+  }
+  *bytes = total;
+  return QEVICT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,280 @@
+"""ctypes binding of libqevict.so (include/qevict.h), same names as the C ABI.
+
+Argument marshalling only: every step of the decode path runs in the HIP
+kernels of the library.  PyTorch supplies device memory (the workspace and the
+tensors) and the HIP stream.  Importing this module does not need a GPU;
+creating a cache does, and there is no CPU fallback: a missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libqevict.so")
+
+ABI_VERSION = 1
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_BAD_STATE, ERR_NONFINITE, \
+    ERR_CAPACITY, ERR_DEVICE = 0, -1, -2, -3, -4, -5, -6, -7
+TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED = 0, 1, 2, 3, 4
+LEDGER_NONE, LEDGER_ACTIVE, LEDGER_DORMANT = 0, 1, 2
+BITS_MIXED_4_2 = 42
+OUT_F32, OUT_BF16 = 0, 1
+FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES = 0x1, 0x2
+KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_QUANTIZE, KERNEL_PROMOTE = range(5)
+
+# exported symbols declared in include/qevict.h
+SYMBOLS = (
+    "qevict_workspace_size", "qevict_cache_init", "qevict_cache_destroy", "qevict_prefill_assign",
+    "qevict_decode_attend", "qevict_retier", "qevict_quantize_window", "qevict_promote_window",
+    "qevict_get_state", "qevict_export_window", "qevict_debug_shift_keys", "qevict_debug_masses",
+    "qevict_profile_enable", "qevict_profile_read", "qevict_last_attend_bytes",
+    "qevict_status_string", "qevict_last_error",
+)
+
+
+class QEvictError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"qevict status {status}: {message}")
+        self.status = status
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "abi_version", "batch", "num_layers", "num_q_heads", "num_kv_heads", "head_dim",
+        "window_tokens", "group_size", "quant_bits", "sink_tokens", "recent_tokens", "max_context",
+        "capacity_full", "capacity_quant", "retier_interval", "out_dtype")] + [
+        ("flags", ctypes.c_uint32), ("softmax_scale", ctypes.c_float), ("num_splits", ctypes.c_int32)]
+
+
+class RetierStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "promotions", "admissions_full", "first_quantizations", "reactivations", "evictions",
+        "n_full", "n_quant_int4", "n_quant_int2")]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+@dataclasses.dataclass
+class Config:
+    batch: int
+    num_q_heads: int
+    num_kv_heads: int
+    window_tokens: int
+    quant_bits: int
+    max_context: int
+    capacity_full: int
+    capacity_quant: int
+    num_layers: int = 1
+    head_dim: int = 128
+    group_size: int = 0          # 0: same as window_tokens
+    sink_tokens: int = 0
+    recent_tokens: int = 0
+    retier_interval: int = 1
+    out_dtype: int = OUT_F32
+    flags: int = 0
+    softmax_scale: float = 0.0
+    num_splits: int = 0
+
+    def to_c(self) -> _Config:
+        c = _Config()
+        c.abi_version = ABI_VERSION
+        for f in dataclasses.fields(self):
+            setattr(c, f.name, getattr(self, f.name))
+        if not self.group_size:
+            c.group_size = self.window_tokens
+        return c
+
+
+_lib = None
+
+
+def load_library(path: str | None = None):
+    """Load libqevict.so (built in-tree); raises if it has not been built."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is missing: build it with `python -m paper_2608_05326_amd.build`")
+    lib = ctypes.CDLL(p)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    P = ctypes.POINTER
+    sig = {
+        "qevict_workspace_size": [P(_Config), P(ctypes.c_size_t)],
+        "qevict_cache_init": [P(_Config), vp, ctypes.c_size_t, vp, P(vp)],
+        "qevict_cache_destroy": [vp],
+        "qevict_prefill_assign": [vp, i32, vp, vp, i32, vp],
+        "qevict_decode_attend": [vp, i32, vp, vp, vp, vp],
+        "qevict_retier": [vp, i32, P(RetierStats)],
+        "qevict_quantize_window": [vp, i32, i32, i32],
+        "qevict_promote_window": [vp, i32, i32, i32],
+        "qevict_get_state": [vp, i32, i32, vp, vp, vp, vp, i32, P(i32)],
+        "qevict_export_window": [vp, i32, i32, i32, vp, vp, vp, vp, vp, vp],
+        "qevict_debug_shift_keys": [vp, i32, i32, i32, vp],
+        "qevict_debug_masses": [vp, i32, vp, i32],
+        "qevict_profile_enable": [vp, i32],
+        "qevict_profile_read": [vp, i32, P(ctypes.c_double), P(i64)],
+        "qevict_last_attend_bytes": [vp, i32, P(i64)],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = i32
+    lib.qevict_status_string.argtypes = [i32]
+    lib.qevict_status_string.restype = ctypes.c_char_p
+    lib.qevict_last_error.argtypes = []
+    lib.qevict_last_error.restype = ctypes.c_char_p
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _check(lib, status: int):
+    if status != OK:
+        raise QEvictError(status, lib.qevict_last_error().decode())
+
+
+def workspace_size(cfg: Config) -> int:
+    lib = load_library()
+    n = ctypes.c_size_t()
+    _check(lib, lib.qevict_workspace_size(ctypes.byref(cfg.to_c()), ctypes.byref(n)))
+    return n.value
+
+
+def _ptr(t, torch_dtype=None, name="tensor"):
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous device tensor")
+    if torch_dtype is not None and t.dtype != torch_dtype:
+        raise ValueError(f"{name} must be {torch_dtype}, got {t.dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Cache:
+    """One tiered KV cache (all layers and sequences) in a torch-owned workspace."""
+
+    def __init__(self, cfg: Config, device="cuda", stream=None):
+        import torch
+
+        self.torch = torch
+        self.lib = load_library()
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        self.workspace = torch.empty(workspace_size(cfg), dtype=torch.uint8, device=self.device)
+        h = ctypes.c_void_p()
+        _check(self.lib, self.lib.qevict_cache_init(
+            ctypes.byref(cfg.to_c()), ctypes.c_void_p(self.workspace.data_ptr()),
+            self.workspace.numel(), ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h)))
+        self.handle = h
+        gr = cfg.group_size or cfg.window_tokens
+        self.n_cap = -(-(cfg.max_context - cfg.sink_tokens) // cfg.window_tokens)
+        self._gr = gr
+
+    # -- lifecycle --
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.qevict_cache_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _c(self, status):
+        _check(self.lib, status)
+
+    # -- the decode path --
+    def prefill_assign(self, layer: int, k, v, init_scores):
+        """k, v: bf16 [B, H_kv, T, d]; init_scores: float32 [B, n_w]."""
+        t = self.torch
+        self._c(self.lib.qevict_prefill_assign(
+            self.handle, layer, _ptr(k, t.bfloat16, "k"), _ptr(v, t.bfloat16, "v"), k.shape[2],
+            _ptr(init_scores, t.float32, "init_scores")))
+
+    def decode_attend(self, layer: int, q, k_new, v_new, out):
+        t = self.torch
+        odt = t.bfloat16 if self.cfg.out_dtype == OUT_BF16 else t.float32
+        self._c(self.lib.qevict_decode_attend(
+            self.handle, layer, _ptr(q, t.bfloat16, "q"), _ptr(k_new, t.bfloat16, "k_new"),
+            _ptr(v_new, t.bfloat16, "v_new"), _ptr(out, odt, "out")))
+
+    def retier(self, layer: int, stats: bool = False):
+        if stats:
+            s = RetierStats()
+            self._c(self.lib.qevict_retier(self.handle, layer, ctypes.byref(s)))
+            return s.as_dict()
+        self._c(self.lib.qevict_retier(self.handle, layer, None))
+        return None
+
+    def quantize_window(self, layer: int, seq: int, window: int):
+        self._c(self.lib.qevict_quantize_window(self.handle, layer, seq, window))
+
+    def promote_window(self, layer: int, seq: int, window: int):
+        self._c(self.lib.qevict_promote_window(self.handle, layer, seq, window))
+
+    # -- inspection --
+    def get_state(self, layer: int, seq: int) -> dict:
+        cap = self.n_cap
+        tiers = np.zeros(cap, np.int8)
+        scores = np.zeros(cap, np.float32)
+        ledger = np.zeros(cap, np.int8)
+        bits = np.zeros(cap, np.int8)
+        n = ctypes.c_int32()
+        self._c(self.lib.qevict_get_state(
+            self.handle, layer, seq, tiers.ctypes.data_as(ctypes.c_void_p),
+            scores.ctypes.data_as(ctypes.c_void_p), ledger.ctypes.data_as(ctypes.c_void_p),
+            bits.ctypes.data_as(ctypes.c_void_p), cap, ctypes.byref(n)))
+        m = n.value
+        return dict(tiers=tiers[:m], scores=scores[:m], ledger=ledger[:m], bits=bits[:m], n=m)
+
+    def export_window(self, layer: int, seq: int, window: int, quant=True, full=False) -> dict:
+        h, w, d = self.cfg.num_kv_heads, self.cfg.window_tokens, self.cfg.head_dim
+        gr = self._gr
+        out = {}
+        ptrs = [None] * 6
+        if quant:
+            out["codes_k"] = np.zeros((h, w, d), np.uint8)
+            out["codes_v"] = np.zeros((h, w, d), np.uint8)
+            out["meta_k"] = np.zeros((h, 2, w // gr, d), np.uint16)
+            out["meta_v"] = np.zeros((h, 2, w, d // gr), np.uint16)
+            for i, k in enumerate(("codes_k", "codes_v", "meta_k", "meta_v")):
+                ptrs[i] = out[k].ctypes.data_as(ctypes.c_void_p)
+        if full:
+            out["full_k"] = np.zeros((h, w, d), np.uint16)
+            out["full_v"] = np.zeros((h, w, d), np.uint16)
+            ptrs[4] = out["full_k"].ctypes.data_as(ctypes.c_void_p)
+            ptrs[5] = out["full_v"].ctypes.data_as(ctypes.c_void_p)
+        self._c(self.lib.qevict_export_window(self.handle, layer, seq, window, *ptrs))
+        return out
+
+    def debug_shift_keys(self, layer: int, seq: int, window: int, delta):
+        dlt = np.ascontiguousarray(delta, dtype=np.float32)
+        self._c(self.lib.qevict_debug_shift_keys(self.handle, layer, seq, window,
+                                                 dlt.ctypes.data_as(ctypes.c_void_p)))
+
+    def debug_masses(self, layer: int) -> np.ndarray:
+        c = self.cfg
+        m = np.zeros((c.batch, c.num_q_heads, self.n_cap + 1), np.float32)
+        self._c(self.lib.qevict_debug_masses(self.handle, layer, m.ctypes.data_as(ctypes.c_void_p),
+                                             self.n_cap))
+        return m
+
+    def profile_enable(self, on: bool = True):
+        self._c(self.lib.qevict_profile_enable(self.handle, 1 if on else 0))
+
+    def profile_read(self, kernel: int):
+        ms, n = ctypes.c_double(), ctypes.c_int64()
+        self._c(self.lib.qevict_profile_read(self.handle, kernel, ctypes.byref(ms), ctypes.byref(n)))
+        return ms.value, n.value
+
+    def last_attend_bytes(self, layer: int) -> int:
+        n = ctypes.c_int64()
+        self._c(self.lib.qevict_last_attend_bytes(self.handle, layer, ctypes.byref(n)))
+        return n.value

@@ -1,0 +1,220 @@
+"""Lockstep comparison of the HIP decode path with the float64 oracle.
+
+Both sides receive the same seeded synthetic inputs.  At every routing event
+the oracle first adopts the GPU's fp32 window scores (exactly, as float64), so
+both rank identical numbers; tier decisions, ledger states, bit widths,
+quantization codes and parameters, and promoted bf16 values must then agree
+bit for bit.  Attention outputs must agree to max-abs <= 2e-3 * ||o||_2 per
+(sequence, head) row, cumulative scores to 1e-4 relative with the floor
+1e-7 * sum of scores.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import paper_2608_05326_amd as qv
+import synthetic as syn
+from oracle.numerics import from_bf16_bits, from_fp16_bits
+from oracle.qevict_oracle import DORMANT, OracleConfig, QEvictUnit, QUANT
+
+OUT_TOL = 2e-3
+SCORE_TOL = 1e-4
+ORACLE_TO_ABI = np.array([0, 1, 1, 2, 3, 4])   # index = oracle state + 1
+
+
+def abi_tiers(unit: QEvictUnit, n: int) -> np.ndarray:
+    return ORACLE_TO_ABI[unit.state[:n] + 1].astype(np.int8)
+
+
+def to_dev_bf16(bits: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def gpu_config(wl: syn.Workload, layers: int, flags: int = 0, out_dtype: int = qv.OUT_F32,
+               num_splits: int = 0, capacity_full=None, capacity_quant=None) -> qv.Config:
+    return qv.Config(
+        batch=wl.batch, num_layers=layers, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+        window_tokens=wl.window, group_size=wl.group, quant_bits=wl.bits, max_context=wl.max_context,
+        capacity_full=wl.capacity_full if capacity_full is None else capacity_full,
+        capacity_quant=wl.capacity_quant if capacity_quant is None else capacity_quant,
+        sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=wl.retier_interval,
+        out_dtype=out_dtype, flags=flags, num_splits=num_splits)
+
+
+def oracle_config(cfg: qv.Config) -> OracleConfig:
+    return OracleConfig(cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.window_tokens,
+                        cfg.group_size or cfg.window_tokens, cfg.quant_bits, cfg.capacity_full,
+                        cfg.capacity_quant, sink=cfg.sink_tokens, recent=cfg.recent_tokens,
+                        no_promotion=bool(cfg.flags & qv.FLAG_NO_PROMOTION))
+
+
+class Lockstep:
+    """Drive a GPU cache and oracle units with the same workload.
+
+    layer_ids: which layers of the workload (seeds) the cache holds.
+    check_seqs: sequences mirrored by the oracle (others run on the GPU only).
+    """
+
+    def __init__(self, wl: syn.Workload, seed: int = 0, layer_ids=(0,), check_seqs=None,
+                 flags: int = 0, num_splits: int = 0, steps: int | None = None, log=print,
+                 capacity_full=None, capacity_quant=None):
+        self.wl, self.seed = wl, seed
+        self.layer_ids = list(layer_ids)
+        self.check_seqs = list(range(wl.batch)) if check_seqs is None else list(check_seqs)
+        self.steps = wl.steps if steps is None else steps
+        self.cfg = gpu_config(wl, len(self.layer_ids), flags | qv.FLAG_DEBUG_MASSES,
+                              num_splits=num_splits, capacity_full=capacity_full,
+                              capacity_quant=capacity_quant)
+        self.cache = qv.Cache(self.cfg)
+        self.ocfg = oracle_config(self.cfg)
+        self.units = {(li, b): QEvictUnit(self.ocfg, wl.max_context)
+                      for li in range(len(self.layer_ids)) for b in self.check_seqs}
+        self.log = log
+        self.inputs = {}
+        self.t = 0
+        self.max_out_err = 0.0
+        self.max_score_err = 0.0
+        self.promotions = 0
+        self.events = 0
+
+    # ---- helpers ---------------------------------------------------------
+    def _dec(self, li, b):
+        key = (li, b)
+        if key not in self.inputs:
+            self.inputs[key] = syn.decode_inputs(self.wl, self.seed, b, self.layer_ids[li], self.steps)
+        return self.inputs[key]
+
+    def compare_ledgers(self, li, b, windows):
+        u = self.units[(li, b)]
+        for w in windows:
+            e = u.ledger[w]
+            ex = self.cache.export_window(li, b, int(w), quant=True)
+            assert np.array_equal(ex["codes_k"], e["kc"].astype(np.uint8)), f"key codes, window {w}"
+            assert np.array_equal(ex["codes_v"], e["vc"].astype(np.uint8)), f"value codes, window {w}"
+            mk = from_fp16_bits(ex["meta_k"])
+            mv = from_fp16_bits(ex["meta_v"])
+            assert np.array_equal(mk[:, 0], e["ks"]) and np.array_equal(mk[:, 1], e["kz"]), \
+                f"key scale / zero, window {w}"
+            assert np.array_equal(mv[:, 0], e["vs"]) and np.array_equal(mv[:, 1], e["vz"]), \
+                f"value scale / zero, window {w}"
+
+    def compare_full(self, li, b, windows):
+        u = self.units[(li, b)]
+        for w in windows:
+            ex = self.cache.export_window(li, b, int(w), quant=False, full=True)
+            assert np.array_equal(from_bf16_bits(ex["full_k"]), u.full_k[w]), f"bf16 keys, window {w}"
+            assert np.array_equal(from_bf16_bits(ex["full_v"]), u.full_v[w]), f"bf16 values, window {w}"
+
+    def compare_state(self, li, b, check_scores=True):
+        u = self.units[(li, b)]
+        st = self.cache.get_state(li, b)
+        n = st["n"]
+        assert np.array_equal(st["tiers"], abi_tiers(u, n)), \
+            f"tiers differ at {np.nonzero(st['tiers'] != abi_tiers(u, n))[0][:10]}"
+        assert np.array_equal(st["ledger"], u.ledger_states()[:n]), "ledger states"
+        for w, e in u.ledger.items():
+            assert st["bits"][w] == e["bits"], f"bit width, window {w}"
+        if check_scores:
+            live = (u.state[:n] >= 0) & (u.state[:n] != 4)
+            so = u.score[:n][live]
+            sg = st["scores"][live].astype(np.float64)
+            floor = 1e-7 * np.abs(so).sum()
+            err = np.abs(sg - so) / np.maximum(np.abs(so), floor)
+            self.max_score_err = max(self.max_score_err, float(err.max(initial=0)))
+            assert np.all(err <= SCORE_TOL), f"score rel err {err.max():.3e} at window {np.argmax(err)}"
+        return st
+
+    # ---- phases ------------------------------------------------------------
+    def prefill(self):
+        wl = self.wl
+        for li, layer in enumerate(self.layer_ids):
+            ks, vs, inits = [], [], []
+            for b in range(wl.batch):
+                k, v = syn.prompt_kv(wl, self.seed, b, layer)
+                init = syn.init_scores(wl, self.seed, b, layer)
+                ks.append(k)
+                vs.append(v)
+                inits.append(init)
+                if (li, b) in self.units:
+                    self.units[(li, b)].prefill(from_bf16_bits(k), from_bf16_bits(v), init)
+            K = to_dev_bf16(np.stack(ks))
+            V = to_dev_bf16(np.stack(vs))
+            S = torch.from_numpy(np.stack(inits)).cuda()
+            self.cache.prefill_assign(li, K, V, S)
+            torch.cuda.synchronize()
+            del K, V
+            for b in self.check_seqs:
+                u = self.units[(li, b)]
+                self.compare_state(li, b)
+                self.compare_ledgers(li, b, sorted(u.ledger))
+                full = [w for w in range(u.n_win_cap) if u.state[w] == 2]
+                self.compare_full(li, b, full[:: max(1, len(full) // 16)])
+
+    def forced_shift(self, li, b_all):
+        """Shift the keys of a low-ranked quantized window toward this step's query."""
+        wl = self.wl
+        ev = self.t // wl.shift_every
+        for b in b_all:
+            st = self.cache.get_state(li, b)
+            q = np.nonzero(st["tiers"] == qv.TIER_QUANT)[0]
+            low = sorted(q, key=lambda w: (st["scores"][w], -w))
+            w = syn.pick_shift_window(wl, self.seed, b, self.layer_ids[li], ev, low)
+            qbits = self._dec(li, b)[0][self.t]
+            delta = syn.shift_delta(wl, qbits)
+            self.cache.debug_shift_keys(li, b, w, delta)
+            if (li, b) in self.units:
+                self.units[(li, b)].shift_key_zero_points(w, delta)
+
+    def step(self):
+        wl, t = self.wl, self.t
+        B, Hq, d = wl.batch, wl.num_q_heads, wl.head_dim
+        routing = (t + 1) % wl.retier_interval == 0
+        for li in range(len(self.layer_ids)):
+            if wl.forced_shift and t % wl.shift_every == 0:
+                self.forced_shift(li, range(B))
+            qs = np.stack([self._dec(li, b)[0][t] for b in range(B)])
+            kn = np.stack([self._dec(li, b)[1][t] for b in range(B)])
+            vn = np.stack([self._dec(li, b)[2][t] for b in range(B)])
+            out = torch.empty((B, Hq, d), dtype=torch.float32, device="cuda")
+            self.cache.decode_attend(li, to_dev_bf16(qs), to_dev_bf16(kn), to_dev_bf16(vn), out)
+            out = out.cpu().numpy()
+            for b in self.check_seqs:
+                u = self.units[(li, b)]
+                o, mass, sink = u.step(from_bf16_bits(qs[b]), from_bf16_bits(kn[b]),
+                                       from_bf16_bits(vn[b]))
+                err = np.abs(out[b] - o).max(axis=1) / np.linalg.norm(o, axis=1)
+                self.max_out_err = max(self.max_out_err, float(err.max()))
+                assert np.all(err <= OUT_TOL), f"step {t} seq {b}: out rel err {err.max():.3e}"
+                st = self.compare_state(li, b)
+                if routing:
+                    u.adopt_scores(st["scores"].astype(np.float64))
+            if routing:
+                stats = self.cache.retier(li, stats=True)
+                self.events += 1
+                self.promotions += stats["promotions"]
+                for b in self.check_seqs:
+                    u = self.units[(li, b)]
+                    before_ledger = set(u.ledger)
+                    before_state = u.state.copy()
+                    u.route()
+                    st = self.compare_state(li, b, check_scores=False)
+                    new_led = [w for w in u.ledger if w not in before_ledger]
+                    self.compare_ledgers(li, b, new_led)
+                    promoted = [w for w in range(u.n_win_cap)
+                                if before_state[w] == QUANT and u.state[w] == 2]
+                    admitted = [w for w in range(u.n_win_cap)
+                                if before_state[w] in (0, 1) and u.state[w] == 2]
+                    self.compare_full(li, b, promoted + admitted)
+                    for w in promoted:
+                        assert u.ledger[w]["state"] == DORMANT
+        self.t += 1
+
+    def run(self):
+        self.prefill()
+        for _ in range(self.steps):
+            self.step()
+        return self
+
+    def close(self):
+        self.cache.close()

@@ -1,0 +1,63 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every symbol include/qevict.h declares, and rejects bad configurations before
+touching the device."""
+import os
+import re
+
+import pytest
+
+import paper_2608_05326_amd as qv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "qevict.h")).read()
+    return sorted(set(re.findall(r"\b(qevict_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = qv.load_library()
+    names = _declared()
+    assert len(names) >= 17
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(qv.SYMBOLS)
+
+
+def _cfg(**kw):
+    base = dict(batch=1, num_q_heads=32, num_kv_heads=8, window_tokens=32, quant_bits=4,
+                max_context=32768 + 128, capacity_full=204, capacity_quant=307)
+    base.update(kw)
+    return qv.Config(**base)
+
+
+def test_workspace_size_of_the_8b_32k_layer():
+    n = qv.workspace_size(_cfg())
+    # bf16 pool 204 x 8 heads x 16 KiB + quantized records 511 x 8 x 5 KiB + small state
+    assert 204 * 8 * 16384 + 511 * 8 * 5120 < n < 60e6
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(num_q_heads=30), qv.qevict.ERR_INVALID_ARG),
+    (dict(head_dim=64), qv.qevict.ERR_UNSUPPORTED),
+    (dict(window_tokens=48), qv.qevict.ERR_UNSUPPORTED),
+    (dict(group_size=16), qv.qevict.ERR_UNSUPPORTED),
+    (dict(quant_bits=3), qv.qevict.ERR_UNSUPPORTED),
+    (dict(capacity_full=-1), qv.qevict.ERR_INVALID_ARG),
+    (dict(capacity_full=3000, capacity_quant=2000), qv.qevict.ERR_UNSUPPORTED),
+    (dict(num_q_heads=128, num_kv_heads=4), qv.qevict.ERR_UNSUPPORTED),
+    (dict(retier_interval=0), qv.qevict.ERR_INVALID_ARG),
+    (dict(flags=0x80), qv.qevict.ERR_INVALID_ARG),
+    (dict(max_context=0), qv.qevict.ERR_INVALID_ARG),
+])
+def test_bad_configs_are_rejected(kw, status):
+    with pytest.raises(qv.QEvictError) as e:
+        qv.workspace_size(_cfg(**kw))
+    assert e.value.status == status
+
+
+def test_status_strings():
+    lib = qv.load_library()
+    assert lib.qevict_status_string(0) == b"ok"
+    assert lib.qevict_status_string(-6) == b"capacity exceeded"

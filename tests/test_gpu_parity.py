@@ -1,0 +1,35 @@
+"""GPU parity of the HIP decode path against the float64 oracle (lockstep).
+
+Every case drives the C ABI through the ctypes binding on the GPU and the
+oracle on the CPU with the same seeded inputs; see gpu_harness for the bars.
+"""
+import numpy as np
+import pytest
+
+import synthetic as syn
+
+pytestmark = pytest.mark.gpu
+
+
+def _lockstep(name, **kw):
+    from tests.gpu_harness import Lockstep
+    wl = syn.get_workload(name)
+    ls = Lockstep(wl, **kw)
+    print(f"[lockstep] {name} seed={ls.seed} steps={ls.steps}", flush=True)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[lockstep] {name}: max out err {ls.max_out_err:.2e}, max score err {ls.max_score_err:.2e}, "
+          f"promotions {ls.promotions} over {ls.events} events", flush=True)
+    return ls
+
+
+def test_c1_forced_promotions():
+    ls = _lockstep("c1")
+    assert ls.promotions >= ls.wl.steps // ls.wl.shift_every
+
+
+@pytest.mark.parametrize("name", ["c1s", "c2s", "c4s", "c5s", "c3s"])
+def test_small_workloads_lockstep(name):
+    _lockstep(name)
