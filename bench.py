@@ -1,0 +1,246 @@
+"""Benchmark of the QEvict tiered decode step on one MI355X.
+
+Workload: the Llama-3-8B-shaped layer at 32K context (batch 1, 32 query / 8 KV
+heads, head_dim 128, windows of 32, 20% bf16 / 30% int4 group-32 / 50%
+evicted, routing every step, drifting queries).  One step is the whole hot
+path for one layer: append + tiered split-K attention + split merge and
+window-score accumulation (decode_attend) followed by the re-rank and the
+quantize / promote migrations (retier).
+
+Sixteen independent caches of this shape (one per "layer" of one workspace,
+each with its own seeds) are stepped round robin, so each step reads a cache
+last touched fifteen steps earlier: the 16 x ~49 MB working set exceeds the
+256 MB Infinity Cache and every step streams its windows from HBM.  Inputs
+for all timed steps are generated and copied to the GPU before timing.
+
+Prints one JSON line.  `value` is microseconds per step (lower is better);
+`roofline` reports the attention kernel's algorithmic bytes per launch over
+its average launch time measured with HIP events on the cache's stream.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tiered decode-attention µs/step + achieved HBM GB/s (8B shape, 32k ctx, 1 GPU)"
+HBM_PEAK_GBPS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=1024)
+    p.add_argument("--warmup", type=int, default=160)
+    p.add_argument("--instances", type=int, default=16, help="independent layer caches rotated")
+    p.add_argument("--workload", default="c2")
+    p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle baseline time budget")
+    p.add_argument("--no-cpu", action="store_true")
+    p.add_argument("--no-kernel-events", action="store_true",
+                   help="do not time each kernel launch with HIP events (no roofline)")
+    return p.parse_args()
+
+
+def to_dev(bits):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def attend_bytes(wl, n_full, n_q4, n_q2, recent_tokens):
+    """Algorithmic bytes of one attention pass of one sequence-layer.
+
+    Live bf16 windows (K + V), live quantized codes with fp16 scale/zero,
+    bf16 recent tokens, the bf16 query and output, and the window scores
+    read and written.  Evicted windows and split partials are not counted.
+    """
+    h, d, w = wl.num_kv_heads, wl.head_dim, wl.window
+    meta = h * (d * (w // wl.group) * 4 + w * (d // wl.group) * 4)
+    full = n_full * 2 * h * w * d * 2
+    q4 = n_q4 * (2 * h * w * d * 4 // 8 + meta)
+    q2 = n_q2 * (2 * h * w * d * 2 // 8 + meta)
+    recent = recent_tokens * 2 * h * d * 2
+    qo = 2 * wl.num_q_heads * d * 2
+    scores = 2 * (n_full + n_q4 + n_q2 + 1) * 4
+    return full + q4 + q2 + recent + qo + scores
+
+
+def cpu_baseline(wl, seed, budget_s):
+    """The float64 oracle stepping one sequence-layer of the same workload."""
+    from oracle.qevict_oracle import OracleConfig, QEvictUnit
+    import synthetic as syn
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = 1
+    cfg = OracleConfig(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, wl.group, wl.bits,
+                       wl.capacity_full, wl.capacity_quant)
+    u = QEvictUnit(cfg, wl.max_context)
+    k, v = syn.prompt_kv(wl, seed, 0, 0)
+    f = syn.bf16_bits_to_f32
+    u.prefill(f(k).astype(np.float64), f(v).astype(np.float64), syn.init_scores(wl, seed, 0, 0))
+    del k, v
+    qs, ks, vs = syn.decode_inputs(wl, seed, 0, 0, wl.steps)
+    n = 0
+    t0 = time.perf_counter()
+    while n < wl.steps and (n < 3 or time.perf_counter() - t0 < budget_s):
+        u.step(f(qs[n]).astype(np.float64), f(ks[n]).astype(np.float64), f(vs[n]).astype(np.float64))
+        u.route()
+        n += 1
+    dt = time.perf_counter() - t0
+    return {"value": round(dt / n * 1e6, 1), "unit": "us/step", "cores": cores, "kind": "oracle",
+            "sample": f"{n} decode steps (attend + score + route) of one 32K-context layer after "
+                      f"prefill, float64 numpy, {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU; the decode path has no "
+                                   "multi-GPU mode (see DESIGN.md for how it would shard)",
+                          "n_gpus": args.gpus}))
+        return 2
+    import torch
+    import paper_2608_05326_amd as qv
+    import synthetic as syn
+
+    wl = syn.get_workload(args.workload)
+    NL = args.instances
+    per_layer = -(-(args.warmup + args.steps) // NL) + 1
+    cfg = qv.Config(batch=wl.batch, num_layers=NL, num_q_heads=wl.num_q_heads,
+                    num_kv_heads=wl.num_kv_heads, window_tokens=wl.window, group_size=wl.group,
+                    quant_bits=wl.bits, max_context=wl.prompt_len + per_layer,
+                    capacity_full=wl.capacity_full, capacity_quant=wl.capacity_quant,
+                    sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=1)
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
+    cache = qv.Cache(cfg, stream=stream)
+    print(f"[bench] workspace {cache.workspace.numel() / 1e6:.1f} MB for {NL} layer caches",
+          file=sys.stderr, flush=True)
+
+    # ---- prefill every layer cache (prompt generated on the host, in parallel) ----
+    def gen(layer):
+        k, v = syn.prompt_kv(wl, args.seed, 0, layer)
+        return layer, k, v, syn.init_scores(wl, args.seed, 0, layer)
+
+    t0 = time.time()
+    with ThreadPoolExecutor(max_workers=8) as ex:
+        for layer, k, v, init in ex.map(gen, range(NL)):
+            K, V = to_dev(k[None]), to_dev(v[None])
+            S = torch.from_numpy(init[None].copy()).cuda()
+            cache.prefill_assign(layer, K, V, S)
+            torch.cuda.synchronize()
+            del K, V, S
+    print(f"[bench] prefilled {NL} layers in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    # ---- per-step inputs, resident on the GPU before timing ----
+    dec = [syn.decode_inputs(wl, args.seed, 0, layer, per_layer) for layer in range(NL)]
+    Q = [to_dev(d[0][:, None]) for d in dec]     # [steps, B, H_q, d]
+    KN = [to_dev(d[1][:, None]) for d in dec]
+    VN = [to_dev(d[2][:, None]) for d in dec]
+    out = torch.empty((wl.batch, wl.num_q_heads, wl.head_dim), dtype=torch.float32, device="cuda")
+
+    import ctypes
+    lib, h = cache.lib, cache.handle
+    optr = ctypes.c_void_p(out.data_ptr())
+    ptrs = [[(ctypes.c_void_p(Q[l][t].data_ptr()), ctypes.c_void_p(KN[l][t].data_ptr()),
+              ctypes.c_void_p(VN[l][t].data_ptr())) for t in range(per_layer)] for l in range(NL)]
+    counter = [0] * NL
+
+    def step(i):
+        layer = i % NL
+        t = counter[layer]
+        counter[layer] += 1
+        q, k, v = ptrs[layer][t]
+        rc = lib.qevict_decode_attend(h, layer, q, k, v, optr)
+        rc |= lib.qevict_retier(h, layer, None)
+        if rc:
+            raise RuntimeError(lib.qevict_last_error().decode())
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    st0 = [cache.get_state(l, 0) for l in range(NL)]
+
+    # ---- timed region ----
+    if not args.no_kernel_events:
+        cache.profile_enable(True)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    t_wall = time.perf_counter()
+    for i in range(args.warmup, args.warmup + args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    gpu_ms = ev0.elapsed_time(ev1)
+    ms_per_step = gpu_ms / args.steps
+
+    kern = {}
+    if not args.no_kernel_events:
+        for name, kid in (("attend", qv.KERNEL_ATTEND), ("merge", qv.KERNEL_MERGE),
+                          ("retier", qv.KERNEL_RETIER), ("quantize", qv.KERNEL_QUANTIZE),
+                          ("promote", qv.KERNEL_PROMOTE)):
+            ms, n = cache.profile_read(kid)
+            kern[name] = round(ms / max(n, 1) * 1e3, 2)
+        cache.profile_enable(False)
+
+    # ---- algorithmic bytes of the timed attention launches ----
+    total_bytes = 0
+    for i in range(args.warmup, args.warmup + args.steps):
+        layer = i % NL
+        st = st0[layer]
+        n_full = int(np.sum(st["tiers"] == qv.TIER_FULL))
+        bits = st["bits"][st["tiers"] == qv.TIER_QUANT]
+        T = wl.prompt_len + (i // NL) + 1
+        recent = (T - wl.sink) - ((T - wl.sink) // wl.window) * wl.window
+        recent = recent if recent else wl.window
+        total_bytes += attend_bytes(wl, n_full, int(np.sum(bits == 4)), int(np.sum(bits == 2)), recent)
+    bytes_per_step = total_bytes / args.steps
+
+    res = {
+        "metric": METRIC,
+        "value": round(ms_per_step * 1e3, 3),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16+int4 (fp32 accumulate)",
+        "data": "synthetic",
+        "config": {"workload": "Llama-3-8B-shaped layer, 32768-token context, batch 1, 32 query / 8 KV "
+                               "heads, head_dim 128, windows of 32, 20% bf16 / 30% int4 group 32 / 50% "
+                               "evicted, re-tier every step, drifting queries",
+                   "layer_caches_rotated": NL, "global_batch": wl.batch, "seq_len": wl.prompt_len,
+                   "parallelism": "single GPU"},
+        "step_GBps": round(bytes_per_step / (ms_per_step * 1e-3) / 1e9, 1),
+        "algorithmic_MB_per_step": round(bytes_per_step / 1e6, 3),
+        "host_wall_us_per_step": round(wall / args.steps * 1e6, 2),
+        "kernel_us": kern,
+    }
+    if kern.get("attend"):
+        ach = bytes_per_step / (kern["attend"] * 1e-6) / 1e9
+        res["roofline"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
+                           "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None}
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_seconds)
+    print(json.dumps(res))
+    cache.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

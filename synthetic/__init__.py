@@ -148,9 +148,12 @@ def _rng(wl: Workload, seed: int, seq: int, layer: int, stream: int) -> np.rando
 
 def f32_to_bf16_bits(x) -> np.ndarray:
     """float32 -> bf16 bit pattern, round to nearest even (finite inputs)."""
-    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
-    return b.astype(np.uint16)
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (b >> 16) & 1          # finite inputs: the sum below stays below 2^32
+    r += 0x7FFF
+    r += b
+    r >>= 16
+    return r.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b) -> np.ndarray:
@@ -168,22 +171,41 @@ def _outlier_mask(wl: Workload, seed: int, seq: int, layer: int) -> np.ndarray:
 
 
 def _keys(wl: Workload, rng: np.random.Generator, shape, scale) -> np.ndarray:
-    if wl.key_dist == "normal":
-        x = rng.standard_normal(shape, dtype=np.float32)
-    elif wl.key_dist == "student_t3":
-        x = rng.standard_t(3.0, size=shape).astype(np.float32)
-    else:
-        raise ValueError(wl.key_dist)
-    return x * scale
+    """Keys of the workload's distribution, drawn one leading-axis slice at a time."""
+    out = np.empty(shape, dtype=np.float32)
+    for i in range(shape[0]):
+        x = rng.standard_normal(shape[1:], dtype=np.float32)
+        if wl.key_dist == "student_t3":
+            # Student-t with 3 degrees of freedom: Z / sqrt(chi^2_3 / 3)
+            chi = np.zeros(shape[1:], dtype=np.float32)
+            for _ in range(3):
+                y = rng.standard_normal(shape[1:], dtype=np.float32)
+                y *= y
+                chi += y
+            chi /= 3.0
+            np.sqrt(chi, out=chi)
+            x /= chi
+        elif wl.key_dist != "normal":
+            raise ValueError(wl.key_dist)
+        x *= scale[i]
+        out[i] = x
+    return out
+
+
+def _normal(rng: np.random.Generator, shape) -> np.ndarray:
+    out = np.empty(shape, dtype=np.float32)
+    for i in range(shape[0]):
+        out[i] = rng.standard_normal(shape[1:], dtype=np.float32)
+    return out
 
 
 def prompt_kv(wl: Workload, seed: int, seq: int, layer: int):
     """Prompt keys and values, bf16 bits, shape [H_kv, prompt_len, d]."""
     shape = (wl.num_kv_heads, wl.prompt_len, wl.head_dim)
     scale = _outlier_mask(wl, seed, seq, layer)[:, None, :]
-    k = _keys(wl, _rng(wl, seed, seq, layer, _S_PROMPT_K), shape, scale)
-    v = _rng(wl, seed, seq, layer, _S_PROMPT_V).standard_normal(shape, dtype=np.float32)
-    return f32_to_bf16_bits(k), f32_to_bf16_bits(v)
+    k = f32_to_bf16_bits(_keys(wl, _rng(wl, seed, seq, layer, _S_PROMPT_K), shape, scale))
+    v = f32_to_bf16_bits(_normal(_rng(wl, seed, seq, layer, _S_PROMPT_V), shape))
+    return k, v
 
 
 def _drift_basis(wl: Workload, seed: int, seq: int, layer: int):
@@ -210,9 +232,9 @@ def decode_inputs(wl: Workload, seed: int, seq: int, layer: int, steps: int | No
         mu = wl.drift_amp * (np.cos(wl.drift_omega * t) * u + np.sin(wl.drift_omega * t) * v)
         qs = qs + mu[:, None, :].astype(np.float32)
     scale = _outlier_mask(wl, seed, seq, layer)
-    ks = _keys(wl, _rng(wl, seed, seq, layer, _S_DEC_K), (n, wl.num_kv_heads, wl.head_dim), scale)
-    vs = _rng(wl, seed, seq, layer, _S_DEC_V).standard_normal(
-        (n, wl.num_kv_heads, wl.head_dim), dtype=np.float32)
+    ks = _keys(wl, _rng(wl, seed, seq, layer, _S_DEC_K), (n, wl.num_kv_heads, wl.head_dim),
+               np.broadcast_to(scale, (n,) + scale.shape))
+    vs = _normal(_rng(wl, seed, seq, layer, _S_DEC_V), (n, wl.num_kv_heads, wl.head_dim))
     return f32_to_bf16_bits(qs), f32_to_bf16_bits(ks), f32_to_bf16_bits(vs)
 
 
