@@ -45,6 +45,7 @@ def parse():
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle baseline time budget")
     p.add_argument("--no-cpu", action="store_true")
+    p.add_argument("--splits", type=int, default=0, help="split-K factor (0 = library default)")
     p.add_argument("--no-kernel-events", action="store_true",
                    help="do not time each kernel launch with HIP events (no roofline)")
     return p.parse_args()
@@ -120,7 +121,8 @@ def main():
                     num_kv_heads=wl.num_kv_heads, window_tokens=wl.window, group_size=wl.group,
                     quant_bits=wl.bits, max_context=wl.prompt_len + per_layer,
                     capacity_full=wl.capacity_full, capacity_quant=wl.capacity_quant,
-                    sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=1)
+                    sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=1,
+                    num_splits=args.splits)
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)
     cache = qv.Cache(cfg, stream=stream)

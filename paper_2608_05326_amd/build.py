@@ -20,6 +20,13 @@ ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # keep LLVM from merging the tails of the bf16 / quantized branches of the
+    # attention kernel: the merged load gets a variable destination register
+    # index and pushes the operand buffer to scratch memory
+    "-mllvm", "-simplifycfg-sink-common=false",
+    # accumulate MFMA results in ordinary VGPRs: the attention output is also
+    # rescaled by VALU code, and AGPR accumulators would be copied every window
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", os.path.join(ROOT, "include"),
 ]
 

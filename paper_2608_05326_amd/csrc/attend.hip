@@ -28,10 +28,38 @@ __device__ __forceinline__ f32x4 mfma_f16(f16x8 a, f16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *(const u32x4*)p; }
-__device__ __forceinline__ void wave_sync_lds() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+// Completes this wave's LDS operations before the next ones (LDS traffic of one
+// wave is ordered; the memory clobber keeps the compiler from moving accesses).
+__device__ __forceinline__ void wave_sync_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// max / sum over the four 16-lane rows: lanes i, i^16, i^32, i^48 (gfx950 permlane swaps)
+__device__ __forceinline__ float rows_max(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const uint32_t a0 = a[0], a1 = a[1];
+  const float y = fmaxf(__uint_as_float(a0), __uint_as_float(a1));
+  const uint32_t v = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  const uint32_t b0 = b[0], b1 = b[1];
+  return fmaxf(__uint_as_float(b0), __uint_as_float(b1));
+}
+__device__ __forceinline__ float rows_sum(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const uint32_t a0 = a[0], a1 = a[1];
+  const float y = __uint_as_float(a0) + __uint_as_float(a1);
+  const uint32_t v = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  const uint32_t b0 = b[0], b1 = b[1];
+  return __uint_as_float(b0) + __uint_as_float(b1);
+}
+// sum over the 16 lanes of a row with DPP (quad swaps, half-row and row mirrors)
+__device__ __forceinline__ float row16_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false));
+  return x;
 }
 
 // 8 codes of one (entry, lane) as exact fp16 integers; ee = entry slot in its word
@@ -62,8 +90,13 @@ struct WaveState {
 };
 
 // Online-softmax update for one window; returns the probabilities in p[tb][v]
-// (relative to the new running max) and records the window's (m, l) pair.
-template <int TB>
+// relative to the wave's running reference maximum and records the window's
+// (reference, sum) pair.  The reference is raised (and O rescaled) only when a
+// window's maximum exceeds it by more than 2^8, so probabilities stay <= 2^8
+// and most windows skip the rescale.
+constexpr float kRescaleSlack = 8.0f;
+
+template <int TB, int NHS>
 __device__ __forceinline__ void softmax_window(const f32x4 (&acc)[TB], float bias, int ntok,
                                                float scale_log2, int qg, WaveState& st,
                                                float (&p)[TB][4], float* m_out, float* l_out) {
@@ -73,51 +106,315 @@ __device__ __forceinline__ void softmax_window(const f32x4 (&acc)[TB], float bia
   for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      int t = 16 * tb + 4 * qg + v;
+      const int t = 16 * tb + 4 * qg + v;
       float y = (acc[tb][v] + bias) * scale_log2;
       y = t < ntok ? y : -INFINITY;
       x[tb][v] = y;
       mw = fmaxf(mw, y);
     }
-  mw = fmaxf(mw, __shfl_xor(mw, 16));
-  mw = fmaxf(mw, __shfl_xor(mw, 32));
-  const float m_new = fmaxf(st.m, mw);
-  const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
+  mw = rows_max(mw);
+  if (__builtin_amdgcn_ballot_w64(mw > st.m + kRescaleSlack) != 0) {
+    const float m_new = fmaxf(st.m, mw);
+    const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
+    st.l *= alpha;
+    st.m = m_new;
+    // O rows 4*qg + v belong to head 4*qg + v, whose alpha lane r = 4*qg + v holds
+    if constexpr (NHS == 1) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float av = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), v));
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb) st.o[cb][v] *= av;
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float av = __shfl(alpha, 4 * qg + v);
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb) st.o[cb][v] *= av;
+      }
+    }
+  }
   float lw = 0.f;
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      p[tb][v] = __builtin_amdgcn_exp2f(x[tb][v] - m_new);
+      p[tb][v] = __builtin_amdgcn_exp2f(x[tb][v] - st.m);
       lw += p[tb][v];
     }
-  lw += __shfl_xor(lw, 16);
-  lw += __shfl_xor(lw, 32);
-  st.l = st.l * alpha + lw;
-  st.m = m_new;
-  *m_out = m_new;
+  lw = rows_sum(lw);
+  st.l += lw;
+  *m_out = st.m;
   *l_out = lw;
-  // rescale O rows 4*qg + v by the alpha of head 4*qg + v (held by lane 4*qg + v)
+}
+
+// Per-window operand buffer: bf16 windows hold their K chunks then V chunks;
+// quantized windows hold K codes, V codes, K scale/zero, V scale/zero.
+template <int W>
+struct ItemBuf {
+  static constexpr int N = W == 32 ? 16 : 32;
+  u32x4 d[N];
+};
+
+struct ItemInfo {
+  const uint8_t* p;
+  int kind, ntok, it;
+  bool open;
+};
+
+template <int W>
+__device__ __forceinline__ void fetch_item(const ItemInfo& in, ItemBuf<W>& buf, int lane, int qg,
+                                           int r, const Geometry& G) {
+  constexpr int TB = W / 16, KT = W / 32;
+  const uint8_t* p = in.p;
+  if (in.kind == KIND_BF16) {
+    const int64_t vbase = (int64_t)W * kHeadDim * 2;
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    float av = __shfl(alpha, 4 * qg + v);
+    for (int i = 0; i < 4 * TB; ++i) buf.d[i] = ld16(p + (i * 64 + lane) * 16);
 #pragma unroll
-    for (int cb = 0; cb < 8; ++cb) st.o[cb][v] *= av;
+    for (int i = 0; i < 8 * KT; ++i) buf.d[4 * TB + i] = ld16(p + vbase + (i * 64 + lane) * 16);
+  } else {
+    constexpr int NC = W / 16;            // 16-byte code loads per area at 4 bits
+    constexpr int NG = kHeadDim / W;      // value groups (G == W)
+    const int nld = in.kind == KIND_Q4 ? NC : NC / 2;
+    // every register of the buffer is defined on both paths (keeps it out of scratch)
+#pragma unroll
+    for (int i = 0; i < ItemBuf<W>::N; ++i) buf.d[i] = (u32x4){0, 0, 0, 0};
+#pragma unroll
+    for (int m = 0; m < NC; ++m) {
+      if (m < nld) {
+        buf.d[m] = ld16(p + (m * 64 + lane) * 16);
+        buf.d[NC + m] = ld16(p + G.qcodes_bytes + (m * 64 + lane) * 16);
+      }
+    }
+    const uint8_t* mk = p + meta_k_off(G);
+    buf.d[2 * NC] = ld16(mk + 16 * r);
+    buf.d[2 * NC + 1] = ld16(mk + 256 + 16 * r);
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+      for (int vg = 0; vg < NG; ++vg) {
+        const uint8_t* pm = p + meta_v_off(G) + ((kt * 4 + qg) * NG + vg) * 32;
+        buf.d[2 * NC + 2 + (kt * NG + vg) * 2] = ld16(pm);
+        buf.d[2 * NC + 3 + (kt * NG + vg) * 2] = ld16(pm + 16);
+      }
   }
 }
 
 template <int W, int NHS>
+__device__ __forceinline__ void process_item(const ItemInfo& in, ItemBuf<W>& buf, WaveState& st,
+                                             const bf16x8 (&qop)[4], const float (&qf)[NHS][8],
+                                             uint8_t* qlds, const AttnArgs& a, int b, int g,
+                                             int lane, int qg, int r, float2* mref) {
+  constexpr int TB = W / 16, KT = W / 32;
+  const Geometry& G = a.g;
+  const int gqa = G.gqa;
+  const int ntok = in.ntok;
+  f32x4 acc[TB];
+  float p_[TB][4];
+  float m_w, l_w;
+  if (in.kind == KIND_BF16) {
+    // buf.d[tb * 4 + kb]: K chunks; buf.d[4 * TB + kt * 8 + cb]: V chunks
+    if (ntok < W || in.open) {
+      const int pos = ntok - 1;
+      if (in.open) {   // the token appended this step: use it from the input and store it
+        const uint16_t* kn = a.k_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
+        const uint16_t* vn = a.v_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
+        uint8_t* pw = const_cast<uint8_t*>(in.p);
+        // keys: the lanes whose row is token pos take the new key (selects, no
+        // conditional writes into the operand registers)
+        const bool krow = r == (pos & 15);
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+          const u32x4 v = ld16(kn + 32 * kb + 8 * qg);
+#pragma unroll
+          for (int tb = 0; tb < TB; ++tb) {
+            const bool sel = krow && tb == (pos >> 4);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const uint32_t old = buf.d[tb * 4 + kb][i], nv = v[i];
+              buf.d[tb * 4 + kb][i] = sel ? nv : old;
+            }
+            if (sel) *(u32x4*)(pw + ((tb * 4 + kb) * 64 + lane) * 16) = v;
+          }
+        }
+        // values: element j of the lanes in group qp holds token pos
+        int ktp, qp, jp;
+        v_tok_pos(pos, &ktp, &qp, &jp);
+        const bool vgrp = qg == qp;
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb) {
+          const uint32_t val = vn[16 * cb + r];
+          if (vgrp) *(uint16_t*)(pw + v_elem_off(W, pos, 16 * cb + r)) = (uint16_t)val;
+#pragma unroll
+          for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const bool here = vgrp && kt == ktp && (jp >> 1) == i;
+              const uint32_t wv = buf.d[4 * TB + kt * 8 + cb][i];
+              const uint32_t lo = (wv & 0xFFFF0000u) | val, hi = (wv & 0x0000FFFFu) | (val << 16);
+              buf.d[4 * TB + kt * 8 + cb][i] = here ? ((jp & 1) ? hi : lo) : wv;
+            }
+        }
+      }
+      // tokens past the end of a partial window contribute nothing
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const bool lo_ok = v_tok(kt, qg, 2 * i) < ntok, hi_ok = v_tok(kt, qg, 2 * i + 1) < ntok;
+          const uint32_t mask = (lo_ok ? 0x0000FFFFu : 0u) | (hi_ok ? 0xFFFF0000u : 0u);
+#pragma unroll
+          for (int cb = 0; cb < 8; ++cb) buf.d[4 * TB + kt * 8 + cb][i] &= mask;
+        }
+    }
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      acc[tb] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+        acc[tb] = mfma_bf16(__builtin_bit_cast(bf16x8, buf.d[tb * 4 + kb]), qop[kb], acc[tb]);
+    }
+    softmax_window<TB, NHS>(acc, 0.f, ntok, G.scale_log2, qg, st, p_, &m_w, &l_w);
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      bf16x8 pv;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pv[j] = (__bf16)p_[2 * kt + (j >> 2)][j & 3];
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb)
+        st.o[cb] = mfma_bf16(pv, __builtin_bit_cast(bf16x8, buf.d[4 * TB + kt * 8 + cb]), st.o[cb]);
+    }
+  } else {
+    // ---- quantized window: int4 or int2 codes ----
+    constexpr int NC = W / 16;
+    constexpr int NG = kHeadDim / W;
+    const bool is4 = in.kind == KIND_Q4;
+    uint32_t kw[4 * NC], vw[4 * NC];
+#pragma unroll
+    for (int m = 0; m < NC; ++m)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        kw[4 * m + i] = buf.d[m][i];
+        vw[4 * m + i] = buf.d[NC + m][i];
+      }
+    const u32x4 ks8 = buf.d[2 * NC], kz8 = buf.d[2 * NC + 1];
+
+    // q*s split into exact fp16 hi + lo, written as the B operand layout
+    float bias_k[NHS];
+    wave_sync_lds();
+#pragma unroll
+    for (int k = 0; k < NHS; ++k) {
+      const int hh = qg + 4 * k;
+      float bsum = 0.f;
+      f16x8 hi8, lo8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint16_t sbits = (uint16_t)(ks8[i >> 1] >> (16 * (i & 1)));
+        const uint16_t zbits = (uint16_t)(kz8[i >> 1] >> (16 * (i & 1)));
+        const float sv = (float)__builtin_bit_cast(_Float16, sbits);
+        const float zv = (float)__builtin_bit_cast(_Float16, zbits);
+        const float qs = qf[k][i] * sv;   // exact: 8-bit x 11-bit significands
+        const _Float16 h = (_Float16)qs;
+        hi8[i] = h;
+        lo8[i] = (_Float16)(qs - (float)h);
+        bsum = fmaf(qf[k][i], zv, bsum);
+      }
+      if (hh < gqa) {
+        const int dst = 16 * (r & 3) + hh;   // lane of the B operand: head hh, channel group r & 3
+        const int kb = r >> 2;
+        *(u32x4*)(qlds + ((0 * 4 + kb) * 64 + dst) * 16) = __builtin_bit_cast(u32x4, hi8);
+        *(u32x4*)(qlds + ((1 * 4 + kb) * 64 + dst) * 16) = __builtin_bit_cast(u32x4, lo8);
+      }
+      bias_k[k] = row16_sum(bsum);   // q . z of head qg + 4k (same value in all 16 lanes)
+    }
+    float bias = 0.f;
+#pragma unroll
+    for (int k = 0; k < NHS; ++k) {
+      const float t = __shfl(bias_k[k], 16 * (r & 3));
+      if ((r >> 2) == k) bias = t;
+    }
+    wave_sync_lds();
+    f16x8 qhi[4], qlo[4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      qhi[kb] = __builtin_bit_cast(f16x8, ld16(qlds + ((0 * 4 + kb) * 64 + lane) * 16));
+      qlo[kb] = __builtin_bit_cast(f16x8, ld16(qlds + ((1 * 4 + kb) * 64 + lane) * 16));
+    }
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      acc[tb] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const int e = tb * 4 + kb;
+        int ee;
+        f16x8 cv;
+        if (is4) {
+          uint32_t w = code_word<4>(kw, e, &ee);
+          cv = unpack_codes<4>(w, ee);
+        } else {
+          uint32_t w = code_word<2>(kw, e, &ee);
+          cv = unpack_codes<2>(w, ee);
+        }
+        acc[tb] = mfma_f16(cv, qhi[kb], acc[tb]);
+        acc[tb] = mfma_f16(cv, qlo[kb], acc[tb]);
+      }
+    }
+    softmax_window<TB, NHS>(acc, bias, ntok, G.scale_log2, qg, st, p_, &m_w, &l_w);
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      f16x8 pv;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pv[j] = (_Float16)p_[2 * kt + (j >> 2)][j & 3];
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb) {
+        const int e = kt * 8 + cb;
+        const int vg = (16 * cb) / W;
+        int ee;
+        f16x8 cv;
+        if (is4) {
+          uint32_t w = code_word<4>(vw, e, &ee);
+          cv = unpack_codes<4>(w, ee);
+        } else {
+          uint32_t w = code_word<2>(vw, e, &ee);
+          cv = unpack_codes<2>(w, ee);
+        }
+        const u32x4 sv4 = buf.d[2 * NC + 2 + (kt * NG + vg) * 2];
+        const u32x4 zv4 = buf.d[2 * NC + 3 + (kt * NG + vg) * 2];
+        f16x8 vv;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          // vector elements go through scalars: bit-casting an element of an
+          // ext_vector directly reads element 0 with this compiler
+          const uint32_t si = sv4[i], zi = zv4[i];
+          f16x2 c2 = {cv[2 * i], cv[2 * i + 1]};
+          f16x2 r2 = __builtin_elementwise_fma(__builtin_bit_cast(f16x2, si), c2,
+                                               __builtin_bit_cast(f16x2, zi));
+          vv[2 * i] = r2[0];
+          vv[2 * i + 1] = r2[1];
+        }
+        st.o[cb] = mfma_f16(pv, vv, st.o[cb]);
+      }
+    }
+  }
+  if (qg == 0 && r < gqa) mref[(int64_t)in.it * G.H_q + g * gqa + r] = make_float2(m_w, l_w);
+}
+
+constexpr int kAttnSmemFixed = 4 * 16 * 130 * 4;   // q*s staging per wave / end-of-split merge
+
+template <int W, int NHS, int DEPTH>
 __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
-  constexpr int TB = W / 16;
-  constexpr int KT = W / 32;
   const Geometry& G = a.g;
   const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, qg = lane >> 4;
   const int gqa = G.gqa;
 
-  __shared__ __attribute__((aligned(16))) uint8_t smem[4 * 16 * 130 * 4];
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   uint8_t* qlds = smem + wave * 8192;   // [hi/lo][kb][lane] x 16 B
+  int32_t* s_cost = (int32_t*)(smem + kAttnSmemFixed);   // live-list cost prefix
+  int32_t* s_ref = s_cost + G.max_fq + 1;                // live-list entries
 
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
   const int32_t* counts = (const int32_t*)(ub + a.L.counts);
@@ -125,29 +422,12 @@ __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
   const int32_t* iref = (const int32_t*)(ub + a.L.item_ref);
   float2* mref = (float2*)(ub + a.L.mref);
 
-  // ---- this split's item range (equal cost) ----
+  // ---- one round of loads: live list, cost prefix, queries ----
   const int n_fq = counts[CNT_ITEMS];
-  const int n_extra = a.n_ring + a.n_sink_items;
-  const int n_all = n_fq + n_extra;
-  const int cF = G.cost_bf16;
-  const int64_t base_cost = icost[n_fq];
-  const int64_t total = base_cost + (int64_t)n_extra * cF;
-  const int S = G.n_split;
-  auto start_cost = [&](int i) -> int64_t {
-    return i <= n_fq ? (int64_t)icost[i] : base_cost + (int64_t)(i - n_fq) * cF;
-  };
-  auto lower = [&](int64_t c) {   // first item whose start cost >= c
-    int lo = 0, hi = n_all;
-    while (lo < hi) {
-      int mid = (lo + hi) >> 1;
-      if (start_cost(mid) >= c) hi = mid; else lo = mid + 1;
-    }
-    return lo;
-  };
-  const int first = lower((s * total + S - 1) / S);
-  const int last = lower(((s + 1) * total + S - 1) / S);
-
-  // ---- query operands ----
+  for (int i = tid; i <= G.max_fq; i += kAttnThreads) {
+    s_cost[i] = icost[i];
+    s_ref[i] = iref[i];
+  }
   const uint16_t* qbase = a.q + ((int64_t)b * G.H_q + (int64_t)g * gqa) * kHeadDim;
   bf16x8 qop[4];
 #pragma unroll
@@ -171,6 +451,33 @@ __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
   // zero this lane's q*s operand slots (padded heads keep zeros)
 #pragma unroll
   for (int i = 0; i < 8; ++i) *(u32x4*)(qlds + (i * 64 + lane) * 16) = (u32x4){0, 0, 0, 0};
+  __syncthreads();
+
+  // ---- this split's item range (equal estimated cost), found in one parallel pass ----
+  const int n_extra = a.n_ring + a.n_sink_items;
+  const int n_all = n_fq + n_extra;
+  const int cF = G.cost_bf16;
+  const int64_t base_cost = s_cost[n_fq];
+  const int64_t total = base_cost + (int64_t)n_extra * cF;
+  const int S = G.n_split;
+  auto start_cost = [&](int i) -> int64_t {
+    return i <= n_fq ? (int64_t)s_cost[i] : base_cost + (int64_t)(i - n_fq) * cF;
+  };
+  // first item whose start cost reaches the split's lower / upper cost bound
+  const int64_t lo_c = (s * total + S - 1) / S, hi_c = ((s + 1) * total + S - 1) / S;
+  __shared__ int s_range[2];
+  if (tid == 0) {
+    s_range[0] = n_all;
+    s_range[1] = n_all;
+  }
+  __syncthreads();
+  for (int i = tid; i < n_all; i += kAttnThreads) {
+    const int64_t c0 = i > 0 ? start_cost(i - 1) : -1, c1 = start_cost(i);
+    if (c1 >= lo_c && c0 < lo_c) s_range[0] = i;
+    if (c1 >= hi_c && c0 < hi_c) s_range[1] = i;
+  }
+  __syncthreads();
+  const int first = s_range[0], last = s_range[1];
 
   WaveState st;
   st.m = -INFINITY;
@@ -179,243 +486,65 @@ __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
   for (int cb = 0; cb < 8; ++cb) st.o[cb] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
   const int w_open = (a.T - 1 - G.sink) / W;
-  const uint8_t* fpool = ub + a.L.fpool;
-  const uint8_t* qpool = ub + a.L.qpool;
+  uint8_t* fpool = ub + a.L.fpool;
+  uint8_t* qpool = ub + a.L.qpool;
   uint8_t* ring = ub + a.L.ring;
-  const uint8_t* sinkp = ub + a.L.sinkp;
-  const int64_t vbase = (int64_t)W * kHeadDim * 2;
-
-  for (int it = first + wave; it < last; it += 4) {
-    int kind = KIND_BF16, ntok = W;
-    bool open = false;
-    const uint8_t* p;
+  uint8_t* sinkp = ub + a.L.sinkp;
+  auto info = [&](int it) {
+    ItemInfo in;
+    in.it = it;
+    in.kind = KIND_BF16;
+    in.ntok = W;
+    in.open = false;
     if (it < n_fq) {
-      const int32_t ref = iref[it];
-      kind = ref >> 28;
+      const int32_t ref = s_ref[it];
+      in.kind = ref >> 28;
       const int64_t slot = ref & 0x0FFFFFFF;
-      p = kind == KIND_BF16 ? fpool + slot * G.fslot_bytes + g * G.fhead_bytes
-                            : qpool + slot * G.qslot_bytes + g * G.qrec_bytes;
+      in.p = in.kind == KIND_BF16 ? fpool + slot * G.fslot_bytes + g * G.fhead_bytes
+                                  : qpool + slot * G.qslot_bytes + g * G.qrec_bytes;
     } else if (it < n_fq + a.n_ring) {
       const int w = a.ring_w0 + (it - n_fq);
-      p = ring + (int64_t)(w % G.NR) * G.fslot_bytes + g * G.fhead_bytes;
-      ntok = min(W, a.T - (G.sink + w * W));
-      open = (w == w_open);
+      in.p = ring + (int64_t)(w % G.NR) * G.fslot_bytes + g * G.fhead_bytes;
+      in.ntok = min(W, a.T - (G.sink + w * W));
+      in.open = (w == w_open);
     } else {
       const int j = it - n_fq - a.n_ring;
-      p = sinkp + (int64_t)j * G.fslot_bytes + g * G.fhead_bytes;
-      ntok = min(W, G.sink - j * W);
+      in.p = sinkp + (int64_t)j * G.fslot_bytes + g * G.fhead_bytes;
+      in.ntok = min(W, G.sink - j * W);
     }
+    return in;
+  };
 
-    f32x4 acc[TB];
-    float p_[TB][4];
-    float m_w, l_w;
-    if (kind == KIND_BF16) {
-      u32x4 kc[TB][4], vc[KT][8];
-#pragma unroll
-      for (int tb = 0; tb < TB; ++tb)
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) kc[tb][kb] = ld16(p + ((tb * 4 + kb) * 64 + lane) * 16);
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-        for (int cb = 0; cb < 8; ++cb) vc[kt][cb] = ld16(p + vbase + ((kt * 8 + cb) * 64 + lane) * 16);
-      if (ntok < W || open) {
-        const int pos = ntok - 1;
-        if (open) {   // the token appended this step: use it from the input and store it
-          const uint16_t* kn = a.k_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
-          const uint16_t* vn = a.v_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
-          uint8_t* pw = ring + (p - ring);
-#pragma unroll
-          for (int tb = 0; tb < TB; ++tb)
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-              if (tb == (pos >> 4) && r == (pos & 15)) {
-                u32x4 v = ld16(kn + 32 * kb + 8 * qg);
-                kc[tb][kb] = v;
-                *(u32x4*)(pw + ((tb * 4 + kb) * 64 + lane) * 16) = v;
-              }
-          int ktp, qp, jp;
-          v_tok_pos(pos, &ktp, &qp, &jp);
-          if (qg == qp) {
-#pragma unroll
-            for (int cb = 0; cb < 8; ++cb) {
-              const uint16_t val = vn[16 * cb + r];
-              *(uint16_t*)(pw + v_elem_off(W, pos, 16 * cb + r)) = val;
-#pragma unroll
-              for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                  if (kt == ktp && (jp >> 1) == i) {
-                    uint32_t wv = vc[kt][cb][i];
-                    wv = (jp & 1) ? ((wv & 0x0000FFFFu) | ((uint32_t)val << 16))
-                                  : ((wv & 0xFFFF0000u) | val);
-                    vc[kt][cb][i] = wv;
-                  }
-                }
-            }
-          }
-        }
-        // tokens past the end of a partial window contribute nothing
-#pragma unroll
-        for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const bool lo_ok = v_tok(kt, qg, 2 * i) < ntok, hi_ok = v_tok(kt, qg, 2 * i + 1) < ntok;
-            const uint32_t mask = (lo_ok ? 0x0000FFFFu : 0u) | (hi_ok ? 0xFFFF0000u : 0u);
-#pragma unroll
-            for (int cb = 0; cb < 8; ++cb) vc[kt][cb][i] &= mask;
-          }
-      }
-#pragma unroll
-      for (int tb = 0; tb < TB; ++tb) {
-        acc[tb] = (f32x4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-          acc[tb] = mfma_bf16(__builtin_bit_cast(bf16x8, kc[tb][kb]), qop[kb], acc[tb]);
-      }
-      softmax_window<TB>(acc, 0.f, ntok, G.scale_log2, qg, st, p_, &m_w, &l_w);
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt) {
-        bf16x8 pv;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) pv[j] = (__bf16)p_[2 * kt + (j >> 2)][j & 3];
-#pragma unroll
-        for (int cb = 0; cb < 8; ++cb)
-          st.o[cb] = mfma_bf16(pv, __builtin_bit_cast(bf16x8, vc[kt][cb]), st.o[cb]);
-      }
-    } else {
-      // ---- quantized window: int4 or int2 codes ----
-      const bool is4 = kind == KIND_Q4;
-      constexpr int NWMAX = W / 4;   // code words per lane at 4 bits
-      uint32_t kw[NWMAX], vw[NWMAX];
-      const int nld = is4 ? NWMAX / 4 : NWMAX / 8;
-#pragma unroll
-      for (int m = 0; m < NWMAX / 4; ++m) {
-        u32x4 x = {0, 0, 0, 0}, y = {0, 0, 0, 0};
-        if (m < nld) {
-          x = ld16(p + (m * 64 + lane) * 16);
-          y = ld16(p + G.qcodes_bytes + (m * 64 + lane) * 16);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) { kw[4 * m + i] = x[i]; vw[4 * m + i] = y[i]; }
-      }
-      const uint8_t* mk = p + meta_k_off(G);
-      const u32x4 ks8 = ld16(mk + 16 * r);          // scales of channels 8r .. 8r + 7
-      const u32x4 kz8 = ld16(mk + 256 + 16 * r);    // zero points
-      // value groups of G = W channels (the host enforces G == W)
-      constexpr int NG = kHeadDim / W;
-      u32x4 vms[KT][NG], vmz[KT][NG];
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-        for (int vg = 0; vg < NG; ++vg) {
-          const uint8_t* pm = p + meta_v_off(G) + ((kt * 4 + qg) * NG + vg) * 32;
-          vms[kt][vg] = ld16(pm);
-          vmz[kt][vg] = ld16(pm + 16);
-        }
-
-      // q*s split into exact fp16 hi + lo, written as the B operand layout
-      float bias_k[NHS];
-      wave_sync_lds();
-#pragma unroll
-      for (int k = 0; k < NHS; ++k) {
-        const int hh = qg + 4 * k;
-        float bsum = 0.f;
-        f16x8 hi8, lo8;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint16_t sbits = (uint16_t)(ks8[i >> 1] >> (16 * (i & 1)));
-          const uint16_t zbits = (uint16_t)(kz8[i >> 1] >> (16 * (i & 1)));
-          const float sv = (float)__builtin_bit_cast(_Float16, sbits);
-          const float zv = (float)__builtin_bit_cast(_Float16, zbits);
-          const float qs = qf[k][i] * sv;   // exact: 8-bit x 11-bit significands
-          const _Float16 h = (_Float16)qs;
-          hi8[i] = h;
-          lo8[i] = (_Float16)(qs - (float)h);
-          bsum = fmaf(qf[k][i], zv, bsum);
-        }
-        if (hh < gqa) {
-          const int dst = 16 * (r & 3) + hh;   // lane of the B operand: head hh, channel group r & 3
-          const int kb = r >> 2;
-          *(u32x4*)(qlds + ((0 * 4 + kb) * 64 + dst) * 16) = __builtin_bit_cast(u32x4, hi8);
-          *(u32x4*)(qlds + ((1 * 4 + kb) * 64 + dst) * 16) = __builtin_bit_cast(u32x4, lo8);
-        }
-        bsum += __shfl_xor(bsum, 1);
-        bsum += __shfl_xor(bsum, 2);
-        bsum += __shfl_xor(bsum, 4);
-        bsum += __shfl_xor(bsum, 8);
-        bias_k[k] = bsum;   // q . z of head qg + 4k
-      }
-      float bias = 0.f;
-#pragma unroll
-      for (int k = 0; k < NHS; ++k) {
-        const float t = __shfl(bias_k[k], 16 * (r & 3));
-        if ((r >> 2) == k) bias = t;
-      }
-      wave_sync_lds();
-      f16x8 qhi[4], qlo[4];
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        qhi[kb] = __builtin_bit_cast(f16x8, ld16(qlds + ((0 * 4 + kb) * 64 + lane) * 16));
-        qlo[kb] = __builtin_bit_cast(f16x8, ld16(qlds + ((1 * 4 + kb) * 64 + lane) * 16));
-      }
-#pragma unroll
-      for (int tb = 0; tb < TB; ++tb) {
-        acc[tb] = (f32x4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-          const int e = tb * 4 + kb;
-          int ee;
-          f16x8 cv;
-          if (is4) {
-            uint32_t w = code_word<4>(kw, e, &ee);
-            cv = unpack_codes<4>(w, ee);
-          } else {
-            uint32_t w = code_word<2>(kw, e, &ee);
-            cv = unpack_codes<2>(w, ee);
-          }
-          acc[tb] = mfma_f16(cv, qhi[kb], acc[tb]);
-          acc[tb] = mfma_f16(cv, qlo[kb], acc[tb]);
-        }
-      }
-      softmax_window<TB>(acc, bias, ntok, G.scale_log2, qg, st, p_, &m_w, &l_w);
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt) {
-        f16x8 pv;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) pv[j] = (_Float16)p_[2 * kt + (j >> 2)][j & 3];
-#pragma unroll
-        for (int cb = 0; cb < 8; ++cb) {
-          const int e = kt * 8 + cb;
-          const int vg = (16 * cb) / W;
-          int ee;
-          f16x8 cv;
-          if (is4) {
-            uint32_t w = code_word<4>(vw, e, &ee);
-            cv = unpack_codes<4>(w, ee);
-          } else {
-            uint32_t w = code_word<2>(vw, e, &ee);
-            cv = unpack_codes<2>(w, ee);
-          }
-          const u32x4 sv4 = vms[kt][vg], zv4 = vmz[kt][vg];
-          f16x8 vv;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            // vector elements go through scalars: bit-casting an element of an
-            // ext_vector directly reads element 0 with this compiler
-            const uint32_t si = sv4[i], zi = zv4[i];
-            f16x2 c2 = {cv[2 * i], cv[2 * i + 1]};
-            f16x2 r2 = __builtin_elementwise_fma(__builtin_bit_cast(f16x2, si), c2,
-                                                 __builtin_bit_cast(f16x2, zi));
-            vv[2 * i] = r2[0];
-            vv[2 * i + 1] = r2[1];
-          }
-          st.o[cb] = mfma_f16(pv, vv, st.o[cb]);
-        }
-      }
+  // ---- window loop: the next window's loads are in flight while one computes ----
+  if constexpr (DEPTH == 2) {
+    ItemBuf<W> A, B;
+    ItemInfo ia, ib;
+    int it = first + wave;
+    if (it < last) {
+      ia = info(it);
+      fetch_item<W>(ia, A, lane, qg, r, G);
     }
-    if (qg == 0 && r < gqa)
-      mref[(int64_t)(b * 0 + (g * gqa + r)) * G.max_items + it] = make_float2(m_w, l_w);
+    for (; it < last; it += 8) {
+      const bool has_b = it + 4 < last;
+      if (has_b) {
+        ib = info(it + 4);
+        fetch_item<W>(ib, B, lane, qg, r, G);
+      }
+      process_item<W, NHS>(ia, A, st, qop, qf, qlds, a, b, g, lane, qg, r, mref);
+      if (!has_b) break;
+      if (it + 8 < last) {
+        ia = info(it + 8);
+        fetch_item<W>(ia, A, lane, qg, r, G);
+      }
+      process_item<W, NHS>(ib, B, st, qop, qf, qlds, a, b, g, lane, qg, r, mref);
+    }
+  } else {
+    ItemBuf<W> A;
+    for (int it = first + wave; it < last; it += 4) {
+      const ItemInfo ia = info(it);
+      fetch_item<W>(ia, A, lane, qg, r, G);
+      process_item<W, NHS>(ia, A, st, qop, qf, qlds, a, b, g, lane, qg, r, mref);
+    }
   }
 
   // ---- merge the 4 waves of this split in LDS, write the split partial ----
@@ -464,7 +593,11 @@ __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
 // Split merge (one block per query head) and window-score accumulation
 // (mass blocks over the live items): mass_h(w) = 2^(m_w - M_h) l_w / L_h,
 // summed over the query heads of each KV group, then over the groups, / H_q.
-__global__ __launch_bounds__(256) void k_merge(AttnArgs a) {
+// Every reduction runs in a fixed order, so results do not depend on timing.
+constexpr int kMergeThreads = 256;
+constexpr int kMaxSplit = 256;
+
+__global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
   const Geometry& G = a.g;
   const int blk = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
@@ -472,73 +605,138 @@ __global__ __launch_bounds__(256) void k_merge(AttnArgs a) {
   const float* part = (const float*)(ub + a.L.partial);
   const int S = G.n_split;
   constexpr int PS = kHeadDim + 2;
+  __shared__ float sw[kMaxSplit];            // per-split weight 2^(M_s - M)
+  __shared__ float4 so[8][kHeadDim / 4];     // per split-group partial outputs
+  __shared__ float sM[64], sL[64];
+  __shared__ float red[kMergeThreads];
 
   if (blk < G.H_q) {
     const int h = blk;
     const float* ph = part + (int64_t)h * S * PS;
+    // M = max over splits
+    float m = -INFINITY;
+    for (int s = tid; s < S; s += kMergeThreads) m = fmaxf(m, ph[s * PS + kHeadDim]);
+    red[tid] = m;
+    __syncthreads();
+    for (int o = kMergeThreads / 2; o > 0; o >>= 1) {
+      if (tid < o) red[tid] = fmaxf(red[tid], red[tid + o]);
+      __syncthreads();
+    }
+    const float M = red[0];
+    __syncthreads();
+    float lsum = 0.f;
+    for (int s = tid; s < S; s += kMergeThreads) {
+      const float ms = ph[s * PS + kHeadDim];
+      const float f = (M > -INFINITY && ms > -INFINITY) ? __builtin_amdgcn_exp2f(ms - M) : 0.f;
+      sw[s] = f;
+      lsum += f * ph[s * PS + kHeadDim + 1];
+    }
+    red[tid] = lsum;
+    __syncthreads();
+    for (int o = kMergeThreads / 2; o > 0; o >>= 1) {
+      if (tid < o) red[tid] += red[tid + o];
+      __syncthreads();
+    }
+    const float L = red[0];
+    // outputs: 32 threads per split row (float4 each), 8 split rows per pass
+    const int c4 = tid & 31, grp = tid >> 5;
+    float4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s = grp; s < S; s += 8) {
+      const float f = sw[s];
+      const float2* row = (const float2*)(ph + s * PS);   // 8-byte aligned rows
+      const float2 x0 = row[2 * c4], x1 = row[2 * c4 + 1];
+      acc.x += f * x0.x;
+      acc.y += f * x0.y;
+      acc.z += f * x1.x;
+      acc.w += f * x1.y;
+    }
+    so[grp][c4] = acc;
+    __syncthreads();
     if (tid < kHeadDim) {
-      float M = -INFINITY;
-      for (int s = 0; s < S; ++s) M = fmaxf(M, ph[s * PS + kHeadDim]);
-      float L = 0.f, o = 0.f;
-      if (M > -INFINITY) {
-        for (int s = 0; s < S; ++s) {
-          const float ms = ph[s * PS + kHeadDim];
-          if (ms > -INFINITY) {
-            const float f = __builtin_amdgcn_exp2f(ms - M);
-            L += ph[s * PS + kHeadDim + 1] * f;
-            o += ph[s * PS + tid] * f;
-          }
-        }
-      }
+      const int c = tid;
+      float o = 0.f;
+#pragma unroll
+      for (int g8 = 0; g8 < 8; ++g8) o += ((const float*)&so[g8][0])[c];
       o = L > 0.f ? o / L : 0.f;
-      const int64_t oi = ((int64_t)b * G.H_q + h) * kHeadDim + tid;
+      const int64_t oi = ((int64_t)b * G.H_q + h) * kHeadDim + c;
       if (G.out_bf16) ((uint16_t*)a.out)[oi] = f32_to_bf16_rne(o);
       else ((float*)a.out)[oi] = o;
     }
     return;
   }
 
-  __shared__ float sM[64], sL[64];
-  if (tid < G.H_q) {
-    const float* ph = part + (int64_t)tid * S * PS;
+  // ---- mass blocks ----
+  // (M_h, L_h) of every head: threads split the (head, split) pairs
+  const int nh = G.H_q;
+  const int parts = kMergeThreads / nh;          // threads per head (H_q <= 64)
+  const int hh = tid % nh, pp = tid / nh;
+  float mloc = -INFINITY;
+  if (pp < parts) {
+    const float* ph = part + (int64_t)hh * S * PS;
+    for (int s = pp; s < S; s += parts) mloc = fmaxf(mloc, ph[s * PS + kHeadDim]);
+  }
+  red[tid] = mloc;
+  __syncthreads();
+  if (tid < nh) {
     float M = -INFINITY;
-    for (int s = 0; s < S; ++s) M = fmaxf(M, ph[s * PS + kHeadDim]);
-    float L = 0.f;
-    if (M > -INFINITY)
-      for (int s = 0; s < S; ++s) {
-        const float ms = ph[s * PS + kHeadDim];
-        if (ms > -INFINITY) L += ph[s * PS + kHeadDim + 1] * __builtin_amdgcn_exp2f(ms - M);
-      }
+    for (int q = 0; q < parts; ++q) M = fmaxf(M, red[q * nh + tid]);
     sM[tid] = M;
+  }
+  __syncthreads();
+  float lloc = 0.f;
+  if (pp < parts) {
+    const float M = sM[hh];
+    const float* ph = part + (int64_t)hh * S * PS;
+    if (M > -INFINITY)
+      for (int s = pp; s < S; s += parts) {
+        const float ms = ph[s * PS + kHeadDim];
+        if (ms > -INFINITY) lloc += ph[s * PS + kHeadDim + 1] * __builtin_amdgcn_exp2f(ms - M);
+      }
+  }
+  __syncthreads();
+  red[tid] = lloc;
+  __syncthreads();
+  if (tid < nh) {
+    float L = 0.f;
+    for (int q = 0; q < parts; ++q) L += red[q * nh + tid];
     sL[tid] = L;
   }
   __syncthreads();
+  // one thread per (item, head): item = blk_base + tid / H_q, head = tid % H_q
   const int n_fq = counts[CNT_ITEMS];
   const int n_all = n_fq + a.n_ring + a.n_sink_items;
-  const int pos = (blk - G.H_q) * 256 + tid;
-  if (pos >= n_all) return;
-  const int32_t* iwin = (const int32_t*)(ub + a.L.item_win);
-  const int win = pos < n_fq ? iwin[pos] : (pos < n_fq + a.n_ring ? a.ring_w0 + (pos - n_fq) : -1);
-  const float2* mref = (const float2*)(ub + a.L.mref);
-  float* dbg = (G.flags & 2u) ? (float*)(ub + a.L.dbg_mass) : nullptr;
-  float tot = 0.f;
-  for (int g = 0; g < G.H_kv; ++g) {
-    float sg = 0.f;
-    for (int j = 0; j < G.gqa; ++j) {
-      const int h = g * G.gqa + j;
-      const float2 mr = mref[(int64_t)h * G.max_items + pos];
-      const float mass = sL[h] > 0.f ? __builtin_amdgcn_exp2f(mr.x - sM[h]) * mr.y / sL[h] : 0.f;
-      sg += mass;
-      if (dbg) {
-        if (win >= 0) dbg[(int64_t)h * (G.nwc + 1) + win] = mass;
-        else atomicAdd(&dbg[(int64_t)h * (G.nwc + 1) + G.nwc], mass);
-      }
-    }
-    tot += sg;
+  const int per_blk = kMergeThreads / nh;
+  const int li = tid / nh;
+  const int pos = (blk - G.H_q) * per_blk + li;
+  const bool active = li < per_blk && pos < n_all;
+  const float2* __restrict__ mref = (const float2*)(ub + a.L.mref);
+  float mass = 0.f;
+  if (active) {
+    const float2 mr = mref[(int64_t)pos * nh + hh];
+    mass = sL[hh] > 0.f ? __builtin_amdgcn_exp2f(mr.x - sM[hh]) * mr.y / sL[hh] : 0.f;
   }
-  if (win >= 0) {
+  __shared__ float smass[kMergeThreads];
+  smass[tid] = mass;
+  __syncthreads();
+  if (!active) return;
+  const int32_t* __restrict__ iwin = (const int32_t*)(ub + a.L.item_win);
+  const int win = pos < n_fq ? iwin[pos] : (pos < n_fq + a.n_ring ? a.ring_w0 + (pos - n_fq) : -1);
+  if (G.flags & 2u) {   // per-head masses of this step, for inspection
+    float* dbg = (float*)(ub + a.L.dbg_mass);
+    if (win >= 0) dbg[(int64_t)hh * (G.nwc + 1) + win] = mass;
+    else atomicAdd(&dbg[(int64_t)hh * (G.nwc + 1) + G.nwc], mass);
+  }
+  if (hh == 0 && win >= 0) {
+    // heads of one KV group first, then the groups in order
+    const float* m = smass + li * nh;
+    float tot = 0.f;
+    for (int g = 0; g < G.H_kv; ++g) {
+      float sg = 0.f;
+      for (int j = 0; j < G.gqa; ++j) sg += m[g * G.gqa + j];
+      tot += sg;
+    }
     float* score = (float*)(ub + a.L.score);
-    score[win] += tot / (float)G.H_q;
+    score[win] += tot / (float)nh;
   }
 }
 
@@ -549,22 +747,28 @@ namespace qv {
 hipError_t launch_attend(const AttnArgs& a, hipStream_t st) {
   dim3 grid(a.g.n_split, a.g.H_kv, a.g.B);
   const int nhs = (a.g.gqa + 3) / 4;
+  const size_t smem = kAttnSmemFixed + 8 * (size_t)(a.g.max_fq + 1);
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, dim3(kAttnThreads), smem, st, a);
+  };
+  const bool dbl = a.g.prefetch_depth == 2;
   if (a.g.W == 32) {
-    if (nhs == 1) hipLaunchKernelGGL((k_attend<32, 1>), grid, dim3(kAttnThreads), 0, st, a);
-    else if (nhs == 2) hipLaunchKernelGGL((k_attend<32, 2>), grid, dim3(kAttnThreads), 0, st, a);
-    else hipLaunchKernelGGL((k_attend<32, 4>), grid, dim3(kAttnThreads), 0, st, a);
+    if (nhs == 1) dbl ? go(k_attend<32, 1, 2>) : go(k_attend<32, 1, 1>);
+    else if (nhs == 2) dbl ? go(k_attend<32, 2, 2>) : go(k_attend<32, 2, 1>);
+    else dbl ? go(k_attend<32, 4, 2>) : go(k_attend<32, 4, 1>);
   } else {
-    if (nhs == 1) hipLaunchKernelGGL((k_attend<64, 1>), grid, dim3(kAttnThreads), 0, st, a);
-    else if (nhs == 2) hipLaunchKernelGGL((k_attend<64, 2>), grid, dim3(kAttnThreads), 0, st, a);
-    else hipLaunchKernelGGL((k_attend<64, 4>), grid, dim3(kAttnThreads), 0, st, a);
+    if (nhs == 1) go(k_attend<64, 1, 1>);
+    else if (nhs == 2) go(k_attend<64, 2, 1>);
+    else go(k_attend<64, 4, 1>);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_merge(const AttnArgs& a, hipStream_t st) {
-  const int n_mass = (a.g.max_items + 255) / 256;
+  const int per_blk = kMergeThreads / a.g.H_q;
+  const int n_mass = (a.g.max_items + per_blk - 1) / per_blk;
   dim3 grid(a.g.H_q + n_mass, a.g.B);
-  hipLaunchKernelGGL(k_merge, grid, dim3(256), 0, st, a);
+  hipLaunchKernelGGL(k_merge, grid, dim3(kMergeThreads), 0, st, a);
   return hipGetLastError();
 }
 }  // namespace qv

@@ -80,10 +80,13 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   __shared__ int32_t scw[kMaxCand];
   __shared__ int32_t sinfo[kMaxCand];
   __shared__ int32_t sa[kMaxCand];
+  __shared__ int32_t sown[2 * kMaxCand];      // slot owners: Full slots, then quantized slots
   __shared__ int32_t tmp[64];
   __shared__ int32_t sstat[ST_N];
   int32_t* sb = (int32_t*)skey;               // after the sort: two int arrays
   int32_t* sc = (int32_t*)skey + kMaxCand;
+  int32_t* fown = sown;
+  int32_t* qown = sown + G.K_f;
 
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
   int8_t* tier = (int8_t*)(ub + a.L.tier);
@@ -103,15 +106,6 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   int32_t* stats = (int32_t*)(ub + a.L.stats);
 
   if (tid < ST_N) sstat[tid] = 0;
-  if (a.prefill) {
-    for (int w = tid; w < a.n_init; w += NT) {
-      const float v = a.init_scores[(int64_t)b * a.n_init + w];
-      if (!__builtin_isfinite(v)) set_error(counts, ERR_NONFINITE);
-      score[w] = v;
-    }
-  }
-  __syncthreads();
-
   const int n_fq = a.prefill ? 0 : counts[CNT_ITEMS];
   const int n_aged = a.aged_w1 - a.aged_w0;
   const int n_cand = n_fq + n_aged;
@@ -119,16 +113,53 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     if (tid == 0) set_error(counts, ERR_CAND);
     return;
   }
+
+  // ---- one round of loads: candidate state, slot owners ----
+  int my_w[PER], my_old[PER], my_led[PER], my_fs[PER], my_qs[PER], my_bits[PER];
+  float my_sc[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    my_w[k] = -1;
+    if (c < n_cand) my_w[k] = c < n_fq ? iwin[c] : a.aged_w0 + (c - n_fq);
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT, w = my_w[k];
+    if (c >= n_cand) continue;
+    float f;
+    if (a.prefill) {
+      f = a.init_scores[(int64_t)b * a.n_init + w];
+    } else {
+      f = score[w];
+    }
+    my_sc[k] = f;
+    const bool routed = c < n_fq;
+    my_old[k] = routed ? tier[w] : T_OPEN;    // T_OPEN: aged, entering the pool
+    my_led[k] = routed ? ledger[w] : L_NONE;
+    my_fs[k] = routed ? fslot[w] : -1;
+    my_qs[k] = routed ? qslot[w] : -1;
+    my_bits[k] = routed ? bits[w] : 0;
+  }
+  for (int i = tid; i < G.K_f; i += NT) fown[i] = fowner[i];
+  for (int i = tid; i < G.n_qslots; i += NT) qown[i] = qowner[i];
+  if (a.prefill) {   // every prompt window (partial ones too) starts at its initial score
+    for (int w = tid; w < a.n_init; w += NT) {
+      const float v = a.init_scores[(int64_t)b * a.n_init + w];
+      if (!__builtin_isfinite(v)) set_error(counts, ERR_NONFINITE);
+      score[w] = v;
+    }
+  }
   int n_pow = 1;
   while (n_pow < n_cand) n_pow <<= 1;
-  for (int c = tid; c < n_pow; c += NT) {
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
     if (c < n_cand) {
-      const int w = c < n_fq ? iwin[c] : a.aged_w0 + (c - n_fq);
-      scw[c] = w;
-      const float f = score[w];
-      if (!__builtin_isfinite(f)) set_error(counts, ERR_NONFINITE);
-      skey[c] = rank_key(f, (uint32_t)c);
-    } else {
+      scw[c] = my_w[k];
+      if (!__builtin_isfinite(my_sc[k])) set_error(counts, ERR_NONFINITE);
+      skey[c] = rank_key(my_sc[k], (uint32_t)c);
+    } else if (c < n_pow) {
       skey[c] = ~0ull;
     }
   }
@@ -164,23 +195,23 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     __syncthreads();
   } else {
     // Full only from candidates that are not currently Quantized
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int c = tid + k * NT;
+      if (c < n_cand) sinfo[c] = my_old[k];
+    }
+    __syncthreads();
     for (int p = tid; p < n_cand; p += NT) {
       const int c = (int)(skey[p] & 0xFFFFFFFFu);
-      const int old = c < n_fq ? tier[scw[c]] : T_OPEN;
-      sa[p] = old != T_QUANT ? 1 : 0;
+      sa[p] = sinfo[c] != T_QUANT ? 1 : 0;
     }
     __syncthreads();
     block_scan(sa, n_cand, tmp);
     for (int p = tid; p < n_cand; p += NT) {
       const int c = (int)(skey[p] & 0xFFFFFFFFu);
-      const int old = c < n_fq ? tier[scw[c]] : T_OPEN;
-      const bool f = old != T_QUANT && sa[p] < G.K_f;
+      const bool f = sinfo[c] != T_QUANT && sa[p] < G.K_f;
+      sa[p] = f ? 0 : 1;
       sinfo[c] = f ? T_FULL : 0;
-    }
-    __syncthreads();
-    for (int p = tid; p < n_cand; p += NT) {
-      const int c = (int)(skey[p] & 0xFFFFFFFFu);
-      sa[p] = sinfo[c] == T_FULL ? 0 : 1;
     }
     __syncthreads();
     block_scan(sa, n_cand, tmp);
@@ -194,45 +225,40 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     __syncthreads();
   }
 
-  // ---- transitions; release slots ----
+  // ---- transitions; release slots (in the LDS owner tables) ----
   const int half_q = (G.K_q + 1) / 2;
-  int my_old[PER], my_nt[PER], my_req[PER], my_bits[PER], my_oldf[PER];
+  int my_nt[PER], my_req[PER], my_nb[PER];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
     my_req[k] = 0;
+    my_nt[k] = T_EVICTED;
     if (c >= n_cand) continue;
-    const int w = scw[c];
     const int info = sinfo[c];
     const int nt = info & 0xFF, rq = info >> 8;
-    const int old = c < n_fq ? tier[w] : T_OPEN;
-    const int led = c < n_fq ? ledger[w] : L_NONE;
-    my_old[k] = old;
+    const int old = my_old[k], led = my_led[k];
     my_nt[k] = nt;
-    my_oldf[k] = old == T_FULL ? fslot[w] : -1;
     const bool needF = nt == T_FULL && old != T_FULL;
     const bool needQ = nt == T_QUANT && old != T_QUANT && led == L_NONE;
     my_req[k] = (needF ? 1 : 0) | (needQ ? 2 : 0);
-    my_bits[k] = G.bits_cfg == 42 ? (rq < half_q ? 4 : 2) : G.bits_cfg;
-    if (old == T_FULL && nt != T_FULL) fowner[fslot[w]] = -1;
-    if (nt == T_EVICTED && led != L_NONE) qowner[qslot[w]] = -1;
+    my_nb[k] = G.bits_cfg == 42 ? (rq < half_q ? 4 : 2) : G.bits_cfg;
+    if (old == T_FULL && nt != T_FULL) fown[my_fs[k]] = -1;
+    if (nt == T_EVICTED && led != L_NONE) qown[my_qs[k]] = -1;
   }
   __syncthreads();
 
   // ---- free lists and request ranks ----
-  for (int i = tid; i < G.K_f; i += NT) sa[i] = fowner[i] < 0 ? 1 : 0;
+  for (int i = tid; i < G.K_f; i += NT) sa[i] = fown[i] < 0 ? 1 : 0;
   __syncthreads();
   const int nfreeF = block_scan(sa, G.K_f, tmp);
   for (int i = tid; i < G.K_f; i += NT)
-    if (fowner[i] < 0) sb[sa[i]] = i;   // sb: free Full slots ascending
+    if (fown[i] < 0) sb[sa[i]] = i;   // sb: free Full slots ascending
   __syncthreads();
-  for (int i = tid; i < G.n_qslots; i += NT) sa[i] = qowner[i] < 0 ? 1 : 0;
+  for (int i = tid; i < G.n_qslots; i += NT) sa[i] = qown[i] < 0 ? 1 : 0;
   __syncthreads();
   const int nfreeQ = block_scan(sa, G.n_qslots, tmp);
   for (int i = tid; i < G.n_qslots; i += NT)
-    if (qowner[i] < 0) sc[sa[i]] = i;   // sc: free quantized slots ascending
-  __syncthreads();
-  for (int c = tid; c < n_cand; c += NT) sa[c] = 0;
+    if (qown[i] < 0) sc[sa[i]] = i;   // sc: free quantized slots ascending
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
@@ -262,19 +288,21 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
     if (c >= n_cand) continue;
-    const int w = scw[c];
+    const int w = my_w[k];
     const int old = my_old[k], nt = my_nt[k];
-    const int led = c < n_fq ? ledger[w] : L_NONE;
-    int fs = nt == T_FULL ? (old == T_FULL ? fslot[w] : -1) : -1;
+    int led = my_led[k];
+    int fs = nt == T_FULL && old == T_FULL ? my_fs[k] : -1;
+    int qs = my_qs[k];
+    int nb = my_bits[k];
     if (my_req[k] & 1) {
       const int rk = my_rankF[k];
       if (rk < nfreeF) {
         fs = sb[rk];
-        fowner[fs] = w;
+        fown[fs] = w;
         int32_t* e = plist + rk * kQEntry;
         if (old == T_QUANT) {
-          e[0] = w; e[1] = SRC_QSLOT; e[2] = qslot[w]; e[3] = fs; e[4] = bits[w];
-          ledger[w] = L_DORMANT;
+          e[0] = w; e[1] = SRC_QSLOT; e[2] = qs; e[3] = fs; e[4] = nb;
+          led = L_DORMANT;
           atomicAdd(&sstat[ST_PROMO], 1);
         } else {
           e[0] = w; e[1] = src_aged; e[2] = a.prefill ? w : w % G.NR; e[3] = fs; e[4] = 0;
@@ -287,35 +315,42 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     if (my_req[k] & 2) {
       const int rk = sa[c];
       if (rk < nfreeQ) {
-        const int qs = sc[rk];
-        qowner[qs] = w;
-        qslot[w] = qs;
-        bits[w] = (int8_t)my_bits[k];
-        ledger[w] = L_ACTIVE;
+        qs = sc[rk];
+        qown[qs] = w;
+        nb = my_nb[k];
+        led = L_ACTIVE;
         int32_t* e = qlist + rk * kQEntry;
         e[0] = w;
-        if (old == T_FULL) { e[1] = SRC_FSLOT; e[2] = my_oldf[k]; }
+        if (old == T_FULL) { e[1] = SRC_FSLOT; e[2] = my_fs[k]; }
         else { e[1] = src_aged; e[2] = a.prefill ? w : w % G.NR; }
         e[3] = qs;
-        e[4] = my_bits[k];
+        e[4] = nb;
         atomicAdd(&sstat[ST_FIRSTQ], 1);
       } else {
         set_error(counts, ERR_POOL);
       }
     }
     if (nt == T_QUANT && old == T_FULL && led == L_DORMANT) {
-      ledger[w] = L_ACTIVE;
+      led = L_ACTIVE;
       atomicAdd(&sstat[ST_REACT], 1);
     }
     if (nt == T_EVICTED) {
-      ledger[w] = L_NONE;
-      qslot[w] = -1;
+      led = L_NONE;
+      qs = -1;
       atomicAdd(&sstat[ST_EVICT], 1);
     }
-    fslot[w] = fs;
     tier[w] = (int8_t)nt;
+    ledger[w] = (int8_t)led;
+    bits[w] = (int8_t)nb;
+    fslot[w] = fs;
+    qslot[w] = qs;
+    my_fs[k] = fs;
+    my_qs[k] = qs;
+    my_bits[k] = nb;
   }
   __syncthreads();
+  for (int i = tid; i < G.K_f; i += NT) fowner[i] = fown[i];
+  for (int i = tid; i < G.n_qslots; i += NT) qowner[i] = qown[i];
 
   // ---- rebuild the live list (window order) ----
 #pragma unroll
@@ -329,19 +364,18 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
     if (c < n_cand && (my_nt[k] == T_FULL || my_nt[k] == T_QUANT)) {
-      const int w = scw[c];
       const int pos = sa[c];
       int kind, slot;
       if (my_nt[k] == T_FULL) {
         kind = KIND_BF16;
-        slot = fslot[w];
+        slot = my_fs[k];
         atomicAdd(&sstat[ST_NF], 1);
       } else {
-        kind = bits[w] == 4 ? KIND_Q4 : KIND_Q2;
-        slot = qslot[w];
+        kind = my_bits[k] == 4 ? KIND_Q4 : KIND_Q2;
+        slot = my_qs[k];
         atomicAdd(&sstat[kind == KIND_Q4 ? ST_NQ4 : ST_NQ2], 1);
       }
-      iwin[pos] = w;
+      iwin[pos] = my_w[k];
       iref[pos] = (kind << 28) | slot;
       sb[pos] = item_cost(G, kind);
     }

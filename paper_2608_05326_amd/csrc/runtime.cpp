@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -171,6 +172,8 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   g->cost_bf16 = 16 * (g->W / 32);
   g->cost_q4 = 8 * (g->W / 32);
   g->cost_q2 = 7 * (g->W / 32);
+  const char* pf = getenv("QEVICT_PREFETCH");
+  g->prefetch_depth = (pf && atoi(pf) == 2 && g->W == 32) ? 2 : 1;
 
   int64_t off = 0;
   auto take = [&](int64_t bytes) {
