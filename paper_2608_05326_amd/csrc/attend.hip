@@ -593,11 +593,15 @@ __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
 // Split merge (one block per query head) and window-score accumulation
 // (mass blocks over the live items): mass_h(w) = 2^(m_w - M_h) l_w / L_h,
 // summed over the query heads of each KV group, then over the groups, / H_q.
-// Every reduction runs in a fixed order, so results do not depend on timing.
+// Every thread issues all of its loads in one round; reductions run in a fixed
+// order, so results do not depend on timing.
 constexpr int kMergeThreads = 256;
-constexpr int kMaxSplit = 256;
+constexpr int kSplitGroups = 8;                     // split rows handled in parallel per block
 
+// NSPT: split rows one thread reads (>= S / 8 and >= S / (256 / H_q))
+template <int NSPT>
 __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
+  constexpr int kSplitsPerThread = NSPT;
   const Geometry& G = a.g;
   const int blk = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
@@ -605,104 +609,76 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
   const float* part = (const float*)(ub + a.L.partial);
   const int S = G.n_split;
   constexpr int PS = kHeadDim + 2;
-  __shared__ float sw[kMaxSplit];            // per-split weight 2^(M_s - M)
-  __shared__ float4 so[8][kHeadDim / 4];     // per split-group partial outputs
+  __shared__ float sred[2][kSplitGroups][kHeadDim / 4 * 4];
+  __shared__ float sml[2][kMergeThreads];
   __shared__ float sM[64], sL[64];
-  __shared__ float red[kMergeThreads];
 
   if (blk < G.H_q) {
+    // ---- output of head h: thread (c4, grp) owns channels 4c4..4c4+3 of splits grp + 8i ----
     const int h = blk;
     const float* ph = part + (int64_t)h * S * PS;
-    // M = max over splits
-    float m = -INFINITY;
-    for (int s = tid; s < S; s += kMergeThreads) m = fmaxf(m, ph[s * PS + kHeadDim]);
-    red[tid] = m;
-    __syncthreads();
-    for (int o = kMergeThreads / 2; o > 0; o >>= 1) {
-      if (tid < o) red[tid] = fmaxf(red[tid], red[tid + o]);
-      __syncthreads();
-    }
-    const float M = red[0];
-    __syncthreads();
-    float lsum = 0.f;
-    for (int s = tid; s < S; s += kMergeThreads) {
-      const float ms = ph[s * PS + kHeadDim];
-      const float f = (M > -INFINITY && ms > -INFINITY) ? __builtin_amdgcn_exp2f(ms - M) : 0.f;
-      sw[s] = f;
-      lsum += f * ph[s * PS + kHeadDim + 1];
-    }
-    red[tid] = lsum;
-    __syncthreads();
-    for (int o = kMergeThreads / 2; o > 0; o >>= 1) {
-      if (tid < o) red[tid] += red[tid + o];
-      __syncthreads();
-    }
-    const float L = red[0];
-    // outputs: 32 threads per split row (float4 each), 8 split rows per pass
     const int c4 = tid & 31, grp = tid >> 5;
-    float4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s = grp; s < S; s += 8) {
-      const float f = sw[s];
-      const float2* row = (const float2*)(ph + s * PS);   // 8-byte aligned rows
-      const float2 x0 = row[2 * c4], x1 = row[2 * c4 + 1];
-      acc.x += f * x0.x;
-      acc.y += f * x0.y;
-      acc.z += f * x1.x;
-      acc.w += f * x1.y;
+    float4 o[kSplitsPerThread];
+    float ms[kSplitsPerThread], ls[kSplitsPerThread];
+#pragma unroll
+    for (int i = 0; i < kSplitsPerThread; ++i) {
+      const int sp = grp + kSplitGroups * i;
+      if (sp < S) {
+        const float* row = ph + sp * PS;
+        const float2 x0 = ((const float2*)row)[2 * c4], x1 = ((const float2*)row)[2 * c4 + 1];
+        o[i] = make_float4(x0.x, x0.y, x1.x, x1.y);
+        ms[i] = row[kHeadDim];
+        ls[i] = row[kHeadDim + 1];
+      } else {
+        o[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        ms[i] = -INFINITY;
+        ls[i] = 0.f;
+      }
     }
-    so[grp][c4] = acc;
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kSplitsPerThread; ++i) m = fmaxf(m, ms[i]);
+    if (c4 == 0) sml[0][grp] = m;
+    __syncthreads();
+    float M = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < kSplitGroups; ++q) M = fmaxf(M, sml[0][q]);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float lsum = 0.f;
+    if (M > -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < kSplitsPerThread; ++i) {
+        const float f = ms[i] > -INFINITY ? __builtin_amdgcn_exp2f(ms[i] - M) : 0.f;
+        acc.x += f * o[i].x;
+        acc.y += f * o[i].y;
+        acc.z += f * o[i].z;
+        acc.w += f * o[i].w;
+        lsum += f * ls[i];
+      }
+    }
+    *(float4*)&sred[0][grp][4 * c4] = acc;
+    if (c4 == 0) sml[1][grp] = lsum;
     __syncthreads();
     if (tid < kHeadDim) {
       const int c = tid;
-      float o = 0.f;
+      float out = 0.f, L = 0.f;
 #pragma unroll
-      for (int g8 = 0; g8 < 8; ++g8) o += ((const float*)&so[g8][0])[c];
-      o = L > 0.f ? o / L : 0.f;
+      for (int q = 0; q < kSplitGroups; ++q) {
+        out += sred[0][q][c];
+        L += sml[1][q];
+      }
+      out = L > 0.f ? out / L : 0.f;
       const int64_t oi = ((int64_t)b * G.H_q + h) * kHeadDim + c;
-      if (G.out_bf16) ((uint16_t*)a.out)[oi] = f32_to_bf16_rne(o);
-      else ((float*)a.out)[oi] = o;
+      if (G.out_bf16) ((uint16_t*)a.out)[oi] = f32_to_bf16_rne(out);
+      else ((float*)a.out)[oi] = out;
     }
     return;
   }
 
-  // ---- mass blocks ----
-  // (M_h, L_h) of every head: threads split the (head, split) pairs
+  // ---- mass blocks: one thread per (item, head); every load in one round ----
   const int nh = G.H_q;
-  const int parts = kMergeThreads / nh;          // threads per head (H_q <= 64)
+  const int parts = kMergeThreads / nh;          // threads per head for (M_h, L_h)
   const int hh = tid % nh, pp = tid / nh;
-  float mloc = -INFINITY;
-  if (pp < parts) {
-    const float* ph = part + (int64_t)hh * S * PS;
-    for (int s = pp; s < S; s += parts) mloc = fmaxf(mloc, ph[s * PS + kHeadDim]);
-  }
-  red[tid] = mloc;
-  __syncthreads();
-  if (tid < nh) {
-    float M = -INFINITY;
-    for (int q = 0; q < parts; ++q) M = fmaxf(M, red[q * nh + tid]);
-    sM[tid] = M;
-  }
-  __syncthreads();
-  float lloc = 0.f;
-  if (pp < parts) {
-    const float M = sM[hh];
-    const float* ph = part + (int64_t)hh * S * PS;
-    if (M > -INFINITY)
-      for (int s = pp; s < S; s += parts) {
-        const float ms = ph[s * PS + kHeadDim];
-        if (ms > -INFINITY) lloc += ph[s * PS + kHeadDim + 1] * __builtin_amdgcn_exp2f(ms - M);
-      }
-  }
-  __syncthreads();
-  red[tid] = lloc;
-  __syncthreads();
-  if (tid < nh) {
-    float L = 0.f;
-    for (int q = 0; q < parts; ++q) L += red[q * nh + tid];
-    sL[tid] = L;
-  }
-  __syncthreads();
-  // one thread per (item, head): item = blk_base + tid / H_q, head = tid % H_q
   const int n_fq = counts[CNT_ITEMS];
   const int n_all = n_fq + a.n_ring + a.n_sink_items;
   const int per_blk = kMergeThreads / nh;
@@ -710,17 +686,55 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
   const int pos = (blk - G.H_q) * per_blk + li;
   const bool active = li < per_blk && pos < n_all;
   const float2* __restrict__ mref = (const float2*)(ub + a.L.mref);
-  float mass = 0.f;
-  if (active) {
-    const float2 mr = mref[(int64_t)pos * nh + hh];
-    mass = sL[hh] > 0.f ? __builtin_amdgcn_exp2f(mr.x - sM[hh]) * mr.y / sL[hh] : 0.f;
+  const float2 mr = active ? mref[(int64_t)pos * nh + hh] : make_float2(-INFINITY, 0.f);
+  const int32_t* __restrict__ iwin = (const int32_t*)(ub + a.L.item_win);
+  const int win = !active ? -1
+                  : (pos < n_fq ? iwin[pos] : (pos < n_fq + a.n_ring ? a.ring_w0 + (pos - n_fq) : -1));
+  float* score = (float*)(ub + a.L.score);
+  const float old_score = (active && hh == 0 && win >= 0) ? score[win] : 0.f;
+  float msv[kSplitsPerThread], lsv[kSplitsPerThread];
+#pragma unroll
+  for (int i = 0; i < kSplitsPerThread; ++i) {
+    const int sp = pp + parts * i;
+    const bool ok = pp < parts && sp < S;
+    const float* row = part + ((int64_t)hh * S + sp) * PS;
+    msv[i] = ok ? row[kHeadDim] : -INFINITY;
+    lsv[i] = ok ? row[kHeadDim + 1] : 0.f;
   }
-  __shared__ float smass[kMergeThreads];
+  float mloc = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kSplitsPerThread; ++i) mloc = fmaxf(mloc, msv[i]);
+  sml[0][tid] = mloc;
+  __syncthreads();
+  if (tid < nh) {
+    float M = -INFINITY;
+    for (int q = 0; q < parts; ++q) M = fmaxf(M, sml[0][q * nh + tid]);
+    sM[tid] = M;
+  }
+  __syncthreads();
+  {
+    const float M = sM[hh];
+    float lloc = 0.f;
+    if (M > -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < kSplitsPerThread; ++i)
+        if (msv[i] > -INFINITY) lloc += lsv[i] * __builtin_amdgcn_exp2f(msv[i] - M);
+    }
+    sml[1][tid] = lloc;
+  }
+  __syncthreads();
+  if (tid < nh) {
+    float L = 0.f;
+    for (int q = 0; q < parts; ++q) L += sml[1][q * nh + tid];
+    sL[tid] = L;
+  }
+  __syncthreads();
+  const float mass = (active && sL[hh] > 0.f) ? __builtin_amdgcn_exp2f(mr.x - sM[hh]) * mr.y / sL[hh]
+                                               : 0.f;
+  float* smass = &sml[0][0];
   smass[tid] = mass;
   __syncthreads();
   if (!active) return;
-  const int32_t* __restrict__ iwin = (const int32_t*)(ub + a.L.item_win);
-  const int win = pos < n_fq ? iwin[pos] : (pos < n_fq + a.n_ring ? a.ring_w0 + (pos - n_fq) : -1);
   if (G.flags & 2u) {   // per-head masses of this step, for inspection
     float* dbg = (float*)(ub + a.L.dbg_mass);
     if (win >= 0) dbg[(int64_t)hh * (G.nwc + 1) + win] = mass;
@@ -735,8 +749,9 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
       for (int j = 0; j < G.gqa; ++j) sg += m[g * G.gqa + j];
       tot += sg;
     }
-    float* score = (float*)(ub + a.L.score);
-    score[win] += tot / (float)nh;
+    const float ns = old_score + tot / (float)nh;
+    score[win] = ns;
+    ((float*)(ub + a.L.item_score))[pos] = ns;   // the next re-rank reads it by list position
   }
 }
 
@@ -768,7 +783,10 @@ hipError_t launch_merge(const AttnArgs& a, hipStream_t st) {
   const int per_blk = kMergeThreads / a.g.H_q;
   const int n_mass = (a.g.max_items + per_blk - 1) / per_blk;
   dim3 grid(a.g.H_q + n_mass, a.g.B);
-  hipLaunchKernelGGL(k_merge, grid, dim3(kMergeThreads), 0, st, a);
+  const int need = max((a.g.n_split + kSplitGroups - 1) / kSplitGroups,
+                       (a.g.n_split + per_blk - 1) / per_blk);
+  if (need <= 8) hipLaunchKernelGGL(k_merge<8>, grid, dim3(kMergeThreads), 0, st, a);
+  else hipLaunchKernelGGL(k_merge<32>, grid, dim3(kMergeThreads), 0, st, a);
   return hipGetLastError();
 }
 }  // namespace qv

@@ -47,6 +47,9 @@ enum : int8_t { T_UNUSED = 0, T_OPEN = 1, T_FULL = 2, T_QUANT = 3, T_EVICTED = 4
 enum : int8_t { L_NONE = 0, L_ACTIVE = 1, L_DORMANT = 2 };
 // live-item kinds
 enum : int32_t { KIND_BF16 = 0, KIND_Q4 = 1, KIND_Q2 = 2 };
+// item_aux of a live item: -1, or the quantized slot of the window's ledger
+// (dormant for a Full item, active for a Quantized one) with its bit width:
+// aux = qslot | (bits << 28)
 // per-unit counters
 enum : int32_t { CNT_ITEMS = 0, CNT_QUANT = 1, CNT_PROMOTE = 2, CNT_ERROR = 3, CNT_BYTES_LO = 4,
                  CNT_N = 16 };
@@ -87,7 +90,7 @@ struct UnitLayout {
   int64_t fpool, ring, sinkp, qpool;
   int64_t tier, ledger, bits, fslot, qslot, score;
   int64_t fowner, qowner;
-  int64_t item_win, item_ref, item_cost;
+  int64_t item_win, item_ref, item_cost, item_aux, item_score;
   int64_t qlist, plist, counts, stats;
   int64_t partial, mref, dbg_mass;
 };

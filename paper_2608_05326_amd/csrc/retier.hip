@@ -28,46 +28,164 @@ __device__ __forceinline__ uint64_t rank_key(float f, uint32_t cand) {
   return ((uint64_t)(~asc) << 32) | cand;
 }
 
-// Exclusive prefix sum of buf[0..n) (n <= kMaxCand) in place; returns the total.
-__device__ int block_scan(int32_t* buf, int n, int32_t* tmp) {
+// Inclusive prefix sum over the 64 lanes of a wave: row shifts 1, 2, 4, 8 within
+// 16-lane rows, then row broadcasts of lanes 15 and 31 (DPP, no LDS traffic).
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);   // row_bcast:15 -> rows 1, 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);   // row_bcast:31 -> rows 2, 3
+  return x;
+}
+
+// Exclusive prefix sums of NV arrays at once (each buf[v][0..n[v]), n <= kMaxCand),
+// in place; tot[v] receives each total.  One pair of barriers for all arrays.
+template <int NV>
+__device__ void block_scan_multi(int32_t* const (&buf)[NV], const int (&n)[NV], int (&tot)[NV],
+                                 int32_t* tmp /* >= NV * 16 */) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   constexpr int PER = kMaxCand / kRetierThreads;
-  int v[PER];
-  int sum = 0;
+  constexpr int NW = kRetierThreads / 64;
+  int v[NV][PER], sum[NV], x[NV];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int i = tid * PER + k;
-    v[k] = i < n ? buf[i] : 0;
-    sum += v[k];
-  }
-  int x = sum;
+  for (int a = 0; a < NV; ++a) {
+    sum[a] = 0;
 #pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  if (lane == 63) tmp[wave] = x;
-  __syncthreads();
-  if (wave == 0) {
-    int w = lane < kRetierThreads / 64 ? tmp[lane] : 0;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int y = __shfl_up(w, off);
-      if (lane >= off) w += y;
+    for (int k = 0; k < PER; ++k) {
+      const int i = tid * PER + k;
+      v[a][k] = i < n[a] ? buf[a][i] : 0;
+      sum[a] += v[a][k];
     }
-    if (lane < kRetierThreads / 64) tmp[32 + lane] = w;
+    x[a] = wave_inclusive_scan(sum[a]);
+    if (lane == 63) tmp[a * NW + wave] = x[a];
   }
   __syncthreads();
-  int run = x - sum + (wave > 0 ? tmp[32 + wave - 1] : 0);
-  const int total = tmp[32 + kRetierThreads / 64 - 1];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int i = tid * PER + k;
-    if (i < n) buf[i] = run;
-    run += v[k];
+  for (int a = 0; a < NV; ++a) {
+    int before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const int t = tmp[a * NW + w];
+      before += w < wave ? t : 0;
+      total += t;
+    }
+    tot[a] = total;
+    int run = x[a] - sum[a] + before;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = tid * PER + k;
+      if (i < n[a]) buf[a][i] = run;
+      run += v[a][k];
+    }
   }
   __syncthreads();
-  return total;
+}
+
+// Value of `x` held by lane (lane ^ J), J in {1, 2, 4, 8, 16, 32}; VALU only.
+template <int J>
+__device__ __forceinline__ uint32_t lane_xor(uint32_t x, int lane) {
+  if constexpr (J == 1) {
+    return __builtin_amdgcn_update_dpp(0u, x, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
+  } else if constexpr (J == 2) {
+    return __builtin_amdgcn_update_dpp(0u, x, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
+  } else if constexpr (J == 4) {
+    const uint32_t dn = __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xF, 0xF, false);  // row_shr:4
+    const uint32_t up = __builtin_amdgcn_update_dpp(0u, x, 0x104, 0xF, 0xF, false);  // row_shl:4
+    return (lane & 4) ? dn : up;
+  } else if constexpr (J == 8) {
+    return __builtin_amdgcn_update_dpp(0u, x, 0x128, 0xF, 0xF, false);  // row_ror:8
+  } else if constexpr (J == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    const uint32_t r0 = r[0], r1 = r[1];
+    return (lane & 16) ? r0 : r1;
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    const uint32_t r0 = r[0], r1 = r[1];
+    return (lane & 32) ? r0 : r1;
+  }
+}
+
+// One compare-exchange stage (block size k, distance j) on positions t + m * NT.
+template <int KP>
+__device__ __forceinline__ void cmpx_stage(uint64_t (&key)[KP], const uint64_t (&other)[KP], int k,
+                                           int j) {
+#pragma unroll
+  for (int m = 0; m < KP; ++m) {
+    const int i = threadIdx.x + m * kRetierThreads;
+    const bool up = (i & k) == 0, lower = (i & j) == 0;
+    const uint64_t a = key[m], b = other[m];
+    key[m] = (up == lower) ? (a < b ? a : b) : (a < b ? b : a);
+  }
+}
+
+template <int J, int KP>
+__device__ __forceinline__ void reg_stage(uint64_t (&key)[KP], int k, int lane) {
+  uint64_t other[KP];
+#pragma unroll
+  for (int m = 0; m < KP; ++m) {
+    const uint32_t lo = lane_xor<J>((uint32_t)key[m], lane);
+    const uint32_t hi = lane_xor<J>((uint32_t)(key[m] >> 32), lane);
+    other[m] = ((uint64_t)hi << 32) | lo;
+  }
+  cmpx_stage<KP>(key, other, k, J);
+}
+
+// Bitonic sort (ascending) of KP keys per thread; thread t holds positions
+// t + m * kRetierThreads.  Partners closer than 64 positions are exchanged in
+// registers (DPP / permlane), partners 64..1023 apart through LDS, farther ones
+// inside a thread.
+template <int KP>
+__device__ void bitonic_sort(uint64_t (&key)[KP], int n_pow, uint64_t* lds) {
+  const int t = threadIdx.x, lane = t & 63;
+  for (int k = 2; k <= n_pow; k <<= 1) {
+    for (int j = k >> 1; j >= 64; j >>= 1) {
+      if (j >= kRetierThreads) {
+        const int mj = j / kRetierThreads;
+#pragma unroll
+        for (int m = 0; m < KP; ++m) {
+          const int mp = m ^ mj;
+          if (mp > m && mp < KP) {
+            const int i = t + m * kRetierThreads;
+            const bool up = (i & k) == 0;
+            const uint64_t x = key[m], y = key[mp];
+            if ((x > y) == up) { key[m] = y; key[mp] = x; }
+          }
+        }
+      } else {
+        uint64_t other[KP];
+#pragma unroll
+        for (int m = 0; m < KP; ++m) lds[t + m * kRetierThreads] = key[m];
+        __syncthreads();
+#pragma unroll
+        for (int m = 0; m < KP; ++m) other[m] = lds[(t + m * kRetierThreads) ^ j];
+        __syncthreads();
+        cmpx_stage<KP>(key, other, k, j);
+      }
+    }
+    if (k > 32) reg_stage<32, KP>(key, k, lane);
+    if (k > 16) reg_stage<16, KP>(key, k, lane);
+    if (k > 8) reg_stage<8, KP>(key, k, lane);
+    if (k > 4) reg_stage<4, KP>(key, k, lane);
+    if (k > 2) reg_stage<2, KP>(key, k, lane);
+    reg_stage<1, KP>(key, k, lane);
+  }
+}
+
+template <int KP>
+__device__ void sort_candidates(uint64_t* skey, int n_cand, int n_pow) {
+  uint64_t key[KP];
+#pragma unroll
+  for (int m = 0; m < KP; ++m) {
+    const int i = threadIdx.x + m * kRetierThreads;
+    key[m] = i < n_cand ? skey[i] : ~0ull;
+  }
+  __syncthreads();
+  bitonic_sort<KP>(key, n_pow, skey);
+#pragma unroll
+  for (int m = 0; m < KP; ++m) skey[threadIdx.x + m * kRetierThreads] = key[m];
+  __syncthreads();
 }
 
 __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
@@ -77,13 +195,13 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   constexpr int PER = kMaxCand / NT;
 
   __shared__ uint64_t skey[kMaxCand];
-  __shared__ int32_t scw[kMaxCand];
   __shared__ int32_t sinfo[kMaxCand];
   __shared__ int32_t sa[kMaxCand];
+  __shared__ int32_t sd[kMaxCand];
   __shared__ int32_t sown[2 * kMaxCand];      // slot owners: Full slots, then quantized slots
   __shared__ int32_t tmp[64];
   __shared__ int32_t sstat[ST_N];
-  int32_t* sb = (int32_t*)skey;               // after the sort: two int arrays
+  int32_t* sb = (int32_t*)skey;               // after the sort: two more int arrays
   int32_t* sc = (int32_t*)skey + kMaxCand;
   int32_t* fown = sown;
   int32_t* qown = sown + G.K_f;
@@ -100,6 +218,8 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   int32_t* iwin = (int32_t*)(ub + a.L.item_win);
   int32_t* iref = (int32_t*)(ub + a.L.item_ref);
   int32_t* icost = (int32_t*)(ub + a.L.item_cost);
+  int32_t* iaux = (int32_t*)(ub + a.L.item_aux);
+  float* iscore = (float*)(ub + a.L.item_score);
   int32_t* qlist = (int32_t*)(ub + a.L.qlist);
   int32_t* plist = (int32_t*)(ub + a.L.plist);
   int32_t* counts = (int32_t*)(ub + a.L.counts);
@@ -114,32 +234,42 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     return;
   }
 
-  // ---- one round of loads: candidate state, slot owners ----
+  // ---- one round of loads: the live list carries every candidate's state ----
   int my_w[PER], my_old[PER], my_led[PER], my_fs[PER], my_qs[PER], my_bits[PER];
   float my_sc[PER];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
     my_w[k] = -1;
-    if (c < n_cand) my_w[k] = c < n_fq ? iwin[c] : a.aged_w0 + (c - n_fq);
-  }
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int c = tid + k * NT, w = my_w[k];
     if (c >= n_cand) continue;
-    float f;
-    if (a.prefill) {
-      f = a.init_scores[(int64_t)b * a.n_init + w];
+    if (c < n_fq) {
+      const int32_t ref = iref[c], aux = iaux[c];
+      const int kind = ref >> 28, slot = ref & 0x0FFFFFFF;
+      my_w[k] = iwin[c];
+      my_sc[k] = iscore[c];
+      if (kind == KIND_BF16) {
+        my_old[k] = T_FULL;
+        my_fs[k] = slot;
+        my_qs[k] = aux < 0 ? -1 : (aux & 0x0FFFFFFF);
+        my_led[k] = aux < 0 ? L_NONE : L_DORMANT;
+        my_bits[k] = aux < 0 ? 0 : (aux >> 28);
+      } else {
+        my_old[k] = T_QUANT;
+        my_fs[k] = -1;
+        my_qs[k] = slot;
+        my_led[k] = L_ACTIVE;
+        my_bits[k] = kind == KIND_Q4 ? 4 : 2;
+      }
     } else {
-      f = score[w];
+      const int w = a.aged_w0 + (c - n_fq);
+      my_w[k] = w;
+      my_sc[k] = a.prefill ? a.init_scores[(int64_t)b * a.n_init + w] : score[w];
+      my_old[k] = T_OPEN;   // aged, entering the pool
+      my_fs[k] = -1;
+      my_qs[k] = -1;
+      my_led[k] = L_NONE;
+      my_bits[k] = 0;
     }
-    my_sc[k] = f;
-    const bool routed = c < n_fq;
-    my_old[k] = routed ? tier[w] : T_OPEN;    // T_OPEN: aged, entering the pool
-    my_led[k] = routed ? ledger[w] : L_NONE;
-    my_fs[k] = routed ? fslot[w] : -1;
-    my_qs[k] = routed ? qslot[w] : -1;
-    my_bits[k] = routed ? bits[w] : 0;
   }
   for (int i = tid; i < G.K_f; i += NT) fown[i] = fowner[i];
   for (int i = tid; i < G.n_qslots; i += NT) qown[i] = qowner[i];
@@ -156,32 +286,16 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
     if (c < n_cand) {
-      scw[c] = my_w[k];
       if (!__builtin_isfinite(my_sc[k])) set_error(counts, ERR_NONFINITE);
       skey[c] = rank_key(my_sc[k], (uint32_t)c);
-    } else if (c < n_pow) {
-      skey[c] = ~0ull;
     }
   }
   __syncthreads();
 
-  // ---- bitonic sort, ascending ----
-  for (int k = 2; k <= n_pow; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = tid; i < n_pow; i += NT) {
-        const int ixj = i ^ j;
-        if (ixj > i) {
-          const uint64_t x = skey[i], y = skey[ixj];
-          const bool up = (i & k) == 0;
-          if ((x > y) == up) {
-            skey[i] = y;
-            skey[ixj] = x;
-          }
-        }
-      }
-      __syncthreads();
-    }
-  }
+  // ---- sort ----
+  if (n_pow <= NT) sort_candidates<1>(skey, n_cand, n_pow);
+  else if (n_pow <= 2 * NT) sort_candidates<2>(skey, n_cand, n_pow);
+  else sort_candidates<4>(skey, n_cand, n_pow);
 
   // ---- tier by sorted position ----
   const bool one_way = (G.flags & 1u) != 0;
@@ -206,7 +320,12 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       sa[p] = sinfo[c] != T_QUANT ? 1 : 0;
     }
     __syncthreads();
-    block_scan(sa, n_cand, tmp);
+    {
+      int32_t* const bufs[1] = {sa};
+      const int ns[1] = {n_cand};
+      int tots[1];
+      block_scan_multi<1>(bufs, ns, tots, tmp);
+    }
     for (int p = tid; p < n_cand; p += NT) {
       const int c = (int)(skey[p] & 0xFFFFFFFFu);
       const bool f = sinfo[c] != T_QUANT && sa[p] < G.K_f;
@@ -214,7 +333,12 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       sinfo[c] = f ? T_FULL : 0;
     }
     __syncthreads();
-    block_scan(sa, n_cand, tmp);
+    {
+      int32_t* const bufs[1] = {sa};
+      const int ns[1] = {n_cand};
+      int tots[1];
+      block_scan_multi<1>(bufs, ns, tots, tmp);
+    }
     for (int p = tid; p < n_cand; p += NT) {
       const int c = (int)(skey[p] & 0xFFFFFFFFu);
       if (sinfo[c] != T_FULL) {
@@ -247,46 +371,49 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   }
   __syncthreads();
 
-  // ---- free lists and request ranks ----
+  // ---- free lists and request ranks: four prefix sums in one pass ----
   for (int i = tid; i < G.K_f; i += NT) sa[i] = fown[i] < 0 ? 1 : 0;
+  for (int i = tid; i < G.n_qslots; i += NT) sd[i] = qown[i] < 0 ? 1 : 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    if (c < n_cand) {
+      sb[c] = my_req[k] & 1;
+      sc[c] = (my_req[k] >> 1) & 1;
+    }
+  }
   __syncthreads();
-  const int nfreeF = block_scan(sa, G.K_f, tmp);
+  int tots[4];
+  {
+    int32_t* const bufs[4] = {sa, sd, sb, sc};
+    const int ns[4] = {G.K_f, G.n_qslots, n_cand, n_cand};
+    block_scan_multi<4>(bufs, ns, tots, tmp);
+  }
+  const int nfreeF = tots[0], nfreeQ = tots[1], nreqF = tots[2], nreqQ = tots[3];
+  int my_rankF[PER], my_rankQ[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    my_rankF[k] = c < n_cand ? sb[c] : 0;
+    my_rankQ[k] = c < n_cand ? sc[c] : 0;
+  }
+  // free slot lists, ascending slot order (sinfo / sb are free now)
+  int32_t* freeF = sinfo;
+  int32_t* freeQ = sb;
+  __syncthreads();
   for (int i = tid; i < G.K_f; i += NT)
-    if (fown[i] < 0) sb[sa[i]] = i;   // sb: free Full slots ascending
-  __syncthreads();
-  for (int i = tid; i < G.n_qslots; i += NT) sa[i] = qown[i] < 0 ? 1 : 0;
-  __syncthreads();
-  const int nfreeQ = block_scan(sa, G.n_qslots, tmp);
+    if (fown[i] < 0) freeF[sa[i]] = i;
   for (int i = tid; i < G.n_qslots; i += NT)
-    if (qown[i] < 0) sc[sa[i]] = i;   // sc: free quantized slots ascending
+    if (qown[i] < 0) freeQ[sd[i]] = i;
   __syncthreads();
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int c = tid + k * NT;
-    if (c < n_cand) sa[c] = my_req[k] & 1;
-  }
-  __syncthreads();
-  const int nreqF = block_scan(sa, n_cand, tmp);
-  int my_rankF[PER];
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int c = tid + k * NT;
-    my_rankF[k] = c < n_cand ? sa[c] : 0;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int c = tid + k * NT;
-    if (c < n_cand) sa[c] = (my_req[k] >> 1) & 1;
-  }
-  __syncthreads();
-  const int nreqQ = block_scan(sa, n_cand, tmp);
 
   // ---- apply: new slots, ledger states, work lists ----
   const int src_aged = a.prefill ? SRC_PROMPT : SRC_RING;
+  int my_aux[PER];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
+    my_aux[k] = -1;
     if (c >= n_cand) continue;
     const int w = my_w[k];
     const int old = my_old[k], nt = my_nt[k];
@@ -297,7 +424,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     if (my_req[k] & 1) {
       const int rk = my_rankF[k];
       if (rk < nfreeF) {
-        fs = sb[rk];
+        fs = freeF[rk];
         fown[fs] = w;
         int32_t* e = plist + rk * kQEntry;
         if (old == T_QUANT) {
@@ -313,9 +440,9 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       }
     }
     if (my_req[k] & 2) {
-      const int rk = sa[c];
+      const int rk = my_rankQ[k];
       if (rk < nfreeQ) {
-        qs = sc[rk];
+        qs = freeQ[rk];
         qown[qs] = w;
         nb = my_nb[k];
         led = L_ACTIVE;
@@ -347,19 +474,31 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     my_fs[k] = fs;
     my_qs[k] = qs;
     my_bits[k] = nb;
+    my_aux[k] = qs >= 0 ? (qs | (nb << 28)) : -1;
   }
   __syncthreads();
   for (int i = tid; i < G.K_f; i += NT) fowner[i] = fown[i];
   for (int i = tid; i < G.n_qslots; i += NT) qowner[i] = qown[i];
 
-  // ---- rebuild the live list (window order) ----
+  // ---- rebuild the live list (window order) with its cost prefix ----
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
-    if (c < n_cand) sa[c] = (my_nt[k] == T_FULL || my_nt[k] == T_QUANT) ? 1 : 0;
+    if (c < n_cand) {
+      const bool live = my_nt[k] == T_FULL || my_nt[k] == T_QUANT;
+      sa[c] = live ? 1 : 0;
+      const int kind = my_nt[k] == T_FULL ? KIND_BF16 : (my_bits[k] == 4 ? KIND_Q4 : KIND_Q2);
+      sd[c] = live ? item_cost(G, kind) : 0;
+    }
   }
   __syncthreads();
-  const int n_items = block_scan(sa, n_cand, tmp);
+  int tots2[2];
+  {
+    int32_t* const bufs[2] = {sa, sd};
+    const int ns[2] = {n_cand, n_cand};
+    block_scan_multi<2>(bufs, ns, tots2, tmp);
+  }
+  const int n_items = tots2[0];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
@@ -377,14 +516,14 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       }
       iwin[pos] = my_w[k];
       iref[pos] = (kind << 28) | slot;
-      sb[pos] = item_cost(G, kind);
+      iaux[pos] = my_aux[k];
+      iscore[pos] = my_sc[k];
+      icost[pos] = sd[c];
     }
   }
   __syncthreads();
-  const int tot_cost = block_scan(sb, n_items, tmp);
-  for (int i = tid; i < n_items; i += NT) icost[i] = sb[i];
   if (tid == 0) {
-    icost[n_items] = tot_cost;
+    icost[n_items] = tots2[1];
     counts[CNT_ITEMS] = n_items;
     counts[CNT_QUANT] = nreqQ < nfreeQ ? nreqQ : nfreeQ;
     counts[CNT_PROMOTE] = nreqF < nfreeF ? nreqF : nfreeF;
@@ -407,6 +546,7 @@ __global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
   int32_t* iwin = (int32_t*)(ub + a.L.item_win);
   int32_t* iref = (int32_t*)(ub + a.L.item_ref);
   int32_t* icost = (int32_t*)(ub + a.L.item_cost);
+  int32_t* iaux = (int32_t*)(ub + a.L.item_aux);
   int32_t* qlist = (int32_t*)(ub + a.L.qlist);
   int32_t* plist = (int32_t*)(ub + a.L.plist);
   int32_t* counts = (int32_t*)(ub + a.L.counts);
@@ -455,8 +595,12 @@ __global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
   // the window keeps its position in the live list; refresh its entry and the cost prefix
   const int n = counts[CNT_ITEMS];
   int run = 0;
+  const int aux = qslot[w] >= 0 ? (qslot[w] | (bits[w] << 28)) : -1;
   for (int i = 0; i < n; ++i) {
-    if (iwin[i] == w) iref[i] = (kind << 28) | slot;
+    if (iwin[i] == w) {
+      iref[i] = (kind << 28) | slot;
+      iaux[i] = aux;
+    }
     icost[i] = run;
     run += item_cost(G, iref[i] >> 28);
   }

@@ -118,6 +118,9 @@ qevict_status check_config(const qevict_config* c) {
     return fail(QEVICT_ERR_INVALID_ARG, "softmax_scale");
   if (c->num_splits < 0 || c->num_splits > 256)
     return fail(QEVICT_ERR_INVALID_ARG, "num_splits must be in [0, 256]");
+  if (c->num_q_heads > 0 && c->num_splits > 32 * (256 / c->num_q_heads))
+    return fail(QEVICT_ERR_UNSUPPORTED, "num_splits above %d for %d query heads",
+                32 * (256 / c->num_q_heads), c->num_q_heads);
   const int W = c->window_tokens;
   const int nr = ceil_div(c->recent_tokens, W) + ceil_div(c->retier_interval, W) + 2;
   if (c->capacity_full + c->capacity_quant + nr > kMaxCand)
@@ -196,6 +199,8 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   L->item_win = take(4LL * (g->max_fq + 1));
   L->item_ref = take(4LL * (g->max_fq + 1));
   L->item_cost = take(4LL * (g->max_fq + 1));
+  L->item_aux = take(4LL * (g->max_fq + 1));
+  L->item_score = take(4LL * (g->max_items + 1));
   L->qlist = take(4LL * kQEntry * (g->max_fq + 1));
   L->plist = take(4LL * kQEntry * (g->max_fq + 1));
   L->counts = take(4LL * CNT_N);
