@@ -8,14 +8,18 @@ window-score accumulation (decode_attend) followed by the re-rank and the
 quantize / promote migrations (retier).
 
 Sixteen independent caches of this shape (one per "layer" of one workspace,
-each with its own seeds) are stepped round robin, so each step reads a cache
-last touched fifteen steps earlier: the 16 x ~49 MB working set exceeds the
-256 MB Infinity Cache and every step streams its windows from HBM.  Inputs
-for all timed steps are generated and copied to the GPU before timing.
+each with its own seeds) are stepped in rounds: the decode_attend of each
+cache, then the retier of each.  A cache is used again only after the other
+fifteen, so the 16 x ~49 MB working set exceeds the 256 MB Infinity Cache and
+every step streams its windows from HBM.  Inputs for all timed steps are
+generated and copied to the GPU before timing.
 
 Prints one JSON line.  `value` is microseconds per step (lower is better);
-`roofline` reports the attention kernel's algorithmic bytes per launch over
-its average launch time measured with HIP events on the cache's stream.
+`roofline` reports decode_attend's algorithmic bytes per call over its average
+duration, measured with HIP events on the cache's stream around the
+back-to-back decode_attend calls of each round; `roofline.traffic` is the HBM
+traffic per call from the committed FETCH_SIZE / WRITE_SIZE record over the
+same duration (null when the kernel sources changed since it was taken).
 """
 from __future__ import annotations
 
@@ -48,7 +52,28 @@ def parse():
     p.add_argument("--splits", type=int, default=0, help="split-K factor (0 = library default)")
     p.add_argument("--no-kernel-events", action="store_true",
                    help="do not time each kernel launch with HIP events (no roofline)")
+    p.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MB",
+                   help="only run 8 plain device-to-device copies of this many MB (hardware "
+                        "counter calibration) and exit")
     return p.parse_args()
+
+
+def calibrate_copy(mb):
+    """Eight copies of a known size, for scaling the FETCH_SIZE / WRITE_SIZE
+    counters.  The copies rotate over four source / destination pairs of 4x the
+    last-level cache size in total, so no source line is still cached."""
+    import torch
+    n = int(mb * 1e6) // 4
+    pairs = [(torch.ones(n, dtype=torch.float32, device="cuda"),
+              torch.empty(n, dtype=torch.float32, device="cuda")) for _ in range(4)]
+    torch.cuda.synchronize()
+    for i in range(8):
+        src, dst = pairs[i % 4]
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "copy", "bytes_read_per_copy": 4 * n, "bytes_written_per_copy": 4 * n,
+                      "copies": 8}))
+    return 0
 
 
 def to_dev(bits):
@@ -72,6 +97,36 @@ def attend_bytes(wl, n_full, n_q4, n_q2, recent_tokens):
     qo = 2 * wl.num_q_heads * d * 2
     scores = 2 * (n_full + n_q4 + n_q2 + 1) * 4
     return full + q4 + q2 + recent + qo + scores
+
+
+COUNTERS = os.path.join(ROOT, "profiles", "decode_attend_8b_32k_hbm_counters.md")
+
+
+def kernel_source_hash():
+    """sha256 over the HIP sources of the library (any kernel edit changes it)."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_2608_05326_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            h.update(f.encode())
+            h.update(open(os.path.join(d, f), "rb").read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per decode_attend from the committed FETCH_SIZE / WRITE_SIZE
+    counter record, or None when the kernels changed since it was taken."""
+    try:
+        lines = open(COUNTERS).read().splitlines()
+    except OSError:
+        return None
+    for ln in lines:
+        if ln.startswith("record: "):
+            rec = json.loads(ln[len("record: "):])
+            if rec.get("source_sha256") == kernel_source_hash():
+                return rec
+    return None
 
 
 def cpu_baseline(wl, seed, budget_s):
@@ -110,6 +165,8 @@ def main():
                                    "multi-GPU mode (see DESIGN.md for how it would shard)",
                           "n_gpus": args.gpus}))
         return 2
+    if args.calibrate_copy > 0:
+        return calibrate_copy(args.calibrate_copy)
     import torch
     import paper_2608_05326_amd as qv
     import synthetic as syn
@@ -158,44 +215,57 @@ def main():
               ctypes.c_void_p(VN[l][t].data_ptr())) for t in range(per_layer)] for l in range(NL)]
     counter = [0] * NL
 
-    def step(i):
-        layer = i % NL
+    def attend(layer):
         t = counter[layer]
         counter[layer] += 1
         q, k, v = ptrs[layer][t]
-        rc = lib.qevict_decode_attend(h, layer, q, k, v, optr)
-        rc |= lib.qevict_retier(h, layer, None)
-        if rc:
+        if lib.qevict_decode_attend(h, layer, q, k, v, optr):
             raise RuntimeError(lib.qevict_last_error().decode())
 
-    for i in range(args.warmup):
-        step(i)
+    def route(layer):
+        if lib.qevict_retier(h, layer, None):
+            raise RuntimeError(lib.qevict_last_error().decode())
+
+    # A step is one layer cache's decode_attend followed (before that cache is
+    # used again) by its retier.  Steps run in rounds over the layer caches:
+    # the attention of every cache of the round, then the routing of each, so
+    # the attention launches of a round run back to back and one pair of
+    # events brackets them.
+    def rounds(first, count, events=None):
+        i = first
+        while i < first + count:
+            layers = [(i + k) % NL for k in range(min(NL - i % NL, first + count - i))]
+            if events is not None:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            for l in layers:
+                attend(l)
+            if events is not None:
+                e1.record(stream)
+                events.append((e0, e1, len(layers)))
+            for l in layers:
+                route(l)
+            i += len(layers)
+
+    rounds(0, args.warmup)
     torch.cuda.synchronize()
     st0 = [cache.get_state(l, 0) for l in range(NL)]
 
     # ---- timed region ----
-    if not args.no_kernel_events:
-        cache.profile_enable(True)
     torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    attn_events = []
     ev0.record(stream)
     t_wall = time.perf_counter()
-    for i in range(args.warmup, args.warmup + args.steps):
-        step(i)
+    rounds(args.warmup, args.steps, None if args.no_kernel_events else attn_events)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
     gpu_ms = ev0.elapsed_time(ev1)
     ms_per_step = gpu_ms / args.steps
-
-    kern = {}
-    if not args.no_kernel_events:
-        for name, kid in (("attend", qv.KERNEL_ATTEND), ("merge", qv.KERNEL_MERGE),
-                          ("retier", qv.KERNEL_RETIER), ("quantize", qv.KERNEL_QUANTIZE),
-                          ("promote", qv.KERNEL_PROMOTE)):
-            ms, n = cache.profile_read(kid)
-            kern[name] = round(ms / max(n, 1) * 1e3, 2)
-        cache.profile_enable(False)
+    attend_us = None
+    if attn_events:
+        attend_us = sum(a.elapsed_time(b) for a, b, _ in attn_events) * 1e3 / sum(n for _, _, n in attn_events)
 
     # ---- algorithmic bytes of the timed attention launches ----
     total_bytes = 0
@@ -231,12 +301,17 @@ def main():
         "step_GBps": round(bytes_per_step / (ms_per_step * 1e-3) / 1e9, 1),
         "algorithmic_MB_per_step": round(bytes_per_step / 1e6, 3),
         "host_wall_us_per_step": round(wall / args.steps * 1e6, 2),
-        "kernel_us": kern,
+        "attend_us_per_launch": round(attend_us, 3) if attend_us else None,
     }
-    if kern.get("attend"):
-        ach = bytes_per_step / (kern["attend"] * 1e-6) / 1e9
+    if attend_us:
+        ach = bytes_per_step / (attend_us * 1e-6) / 1e9
+        rec = measured_traffic()
+        traffic = None
+        if rec:
+            traffic = round(rec["hbm_bytes_per_launch"] / (attend_us * 1e-6) / 1e9, 1)
+            res["traffic_MB_per_launch"] = round(rec["hbm_bytes_per_launch"] / 1e6, 3)
         res["roofline"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
-                           "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None}
+                           "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": traffic}
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_seconds)
     print(json.dumps(res))
