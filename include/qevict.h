@@ -4,13 +4,13 @@
  * QEvict (arXiv 2608.05326) keeps the historical KV cache of every layer as
  * contiguous windows of W tokens.  Outside a protected sink prefix and recent
  * region, each window is Full (bf16), Quantized (asymmetric low-bit codes that
- * attention still reads) or Evicted (Sec. 3.3, cache partition equation).
+ * attention still reads) or Evicted (Sec. 4.3, cache partition equation).
  * Every decode step attends over the accessible windows and adds each window's
  * attention mass, averaged over the query heads, to its cumulative score
- * (Sec. 3.2, cumulative window score equation).  A routing event ranks the
+ * (Sec. 4.2, cumulative window score equation).  A routing event ranks the
  * candidates by score and re-tiers them: top K_f -> Full, next K_q ->
  * Quantized, the rest deleted, with promotion from the low-bit ledger and
- * write-once quantization (Sec. 3.3 TopK equations; Algorithm 1).
+ * write-once quantization (Sec. 4.3 TopK equations; Algorithm 1).
  *
  * Conventions for every call:
  *  - Tensor arguments are HIP device pointers to contiguous row-major data
@@ -119,7 +119,7 @@ qevict_status qevict_cache_init(const qevict_config *cfg, void *workspace, size_
 /* Release the host handle (the workspace is the caller's). */
 qevict_status qevict_cache_destroy(qevict_cache *c);
 
-/* Prefill of one layer (Sec. 3.2: prompt attention initialises the window
+/* Prefill of one layer (Sec. 4.2: prompt attention initialises the window
  * scores and the first tier assignment).
  *   k, v        [B, H_kv, prompt_len, d] bf16 prompt keys / values
  *   init_scores [B, n_w] fp32, n_w = ceil((prompt_len - sink)/W): initial
@@ -131,7 +131,7 @@ qevict_status qevict_prefill_assign(qevict_cache *c, int32_t layer, const uint16
                                     const uint16_t *v, int32_t prompt_len,
                                     const float *init_scores);
 
-/* One decode step of one layer (Sec. 3.1 decode attention; Sec. 3.2 score).
+/* One decode step of one layer (Sec. 4.1 decode attention; Sec. 4.2 score).
  *   q      [B, H_q, d]  bf16 queries
  *   k_new, v_new [B, H_kv, d] bf16 key / value of the new token
  *   out    [B, H_q, d]  out_dtype attention output
@@ -141,7 +141,7 @@ qevict_status qevict_prefill_assign(qevict_cache *c, int32_t layer, const uint16
 qevict_status qevict_decode_attend(qevict_cache *c, int32_t layer, const uint16_t *q,
                                    const uint16_t *k_new, const uint16_t *v_new, void *out);
 
-/* Routing event of one layer (Sec. 3.3 candidate pool / TopK; Algorithm 1).
+/* Routing event of one layer (Sec. 4.3 candidate pool / TopK; Algorithm 1).
  * Candidates are the Full and Quantized windows plus the windows that left
  * the recent region; ranking is by score, ties to the lower window index.
  * Runs the promote / quantize-once / reactivate / evict moves on the device.

@@ -7,20 +7,20 @@ run it.  It shares no code with the GPU library and imports nothing from it.
 What it computes, and where the paper defines it (QEvict, arXiv 2608.05326):
 
 * Decode attention of each query head over the accessible keys and values,
-  softmax(q K^T / sqrt(d)) V, with grouped KV heads (Sec. 3.1, Preliminaries).
+  softmax(q K^T / sqrt(d)) V, with grouped KV heads (Sec. 4.1, Preliminaries).
 * The cache partition into sink, recent region and windows, with each
-  historical window Full, Quantized or Evicted (Sec. 3.3, partition equation).
+  historical window Full, Quantized or Evicted (Sec. 4.3, partition equation).
 * The cumulative window score: each window's attention mass averaged over the
-  H_q query heads, added at every decode step (Sec. 3.2, cumulative window
+  H_q query heads, added at every decode step (Sec. 4.2, cumulative window
   score equation; the per-step reading is listed with the other readings).
 * Routing: the candidate pool is the previous Full and Quantized windows plus
   the windows that left the recent region; the top K_f by score go to Full,
-  the next K_q to Quantized, the rest are evicted (Sec. 3.3, candidate pool
+  the next K_q to Quantized, the rest are evicted (Sec. 4.3, candidate pool
   and TopK equations; Algorithm 1).
 * Migration-stable asymmetric quantization: keys per channel across tokens,
   values per token across channels; codes are produced once, at a window's
   first demotion, and reused on every later move; promotion reconstructs the
-  low-bit values in bf16 and keeps the codes dormant (Sec. 3.3, paragraph on
+  low-bit values in bf16 and keeps the codes dormant (Sec. 4.3, paragraph on
   migration-stable quantization; Algorithm 1).
 
 Everything is float64 except where the method stores a narrower format:
@@ -81,7 +81,7 @@ class OracleConfig:
 
 
 # ----------------------------------------------------------------------------
-# Quantization (Sec. 3.3, migration-stable quantization)
+# Quantization (Sec. 4.3, migration-stable quantization)
 # ----------------------------------------------------------------------------
 
 def _fp16_step(v: np.ndarray, direction: int) -> np.ndarray:
@@ -180,7 +180,7 @@ def dequantize_window(e: dict):
 
 
 # ----------------------------------------------------------------------------
-# Routing (Sec. 3.3 candidate pool and TopK equations; Algorithm 1)
+# Routing (Sec. 4.3 candidate pool and TopK equations; Algorithm 1)
 # ----------------------------------------------------------------------------
 
 def route_order(cands, scores) -> list:
@@ -250,7 +250,7 @@ class QEvictUnit:
             if self.state[w] == -1:
                 self.state[w] = OPEN
 
-    # -- prefill (Sec. 3.2: prompt attention initialises the scores and the first assignment)
+    # -- prefill (Sec. 4.2: prompt attention initialises the scores and the first assignment)
     def prefill(self, k, v, init_scores):
         """k, v: float64 [H_kv, T, d] bf16 values; init_scores: per window."""
         c = self.cfg

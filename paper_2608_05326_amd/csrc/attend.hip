@@ -1,12 +1,12 @@
 // Tier-aware split-K decode attention and the split merge / window-score pass.
 //
 // Decode attention of each query head over the accessible tokens (QEvict
-// Sec. 3.1): sink and recent tokens and Full windows in bf16, Quantized
+// Sec. 4.1): sink and recent tokens and Full windows in bf16, Quantized
 // windows as z + s c with the codes expanded in registers.  The pass also
 // yields, per (query head, window), the window's softmax mass relative to a
 // reference maximum, which the merge turns into the exact attention mass the
 // window received and adds, averaged over the query heads, to the window's
-// cumulative score (Sec. 3.2, cumulative window score equation).
+// cumulative score (Sec. 4.2, cumulative window score equation).
 //
 // Work decomposition: one workgroup per (sequence, KV head, split); the live
 // windows of a sequence form a list in window order, cut into splits of equal

@@ -1,4 +1,4 @@
-// Window migrations between the tier pools (QEvict Sec. 3.3, migration-stable
+// Window migrations between the tier pools (QEvict Sec. 4.3, migration-stable
 // quantization; Algorithm 1 promote / quantize-once steps), driven by the work
 // lists the re-tier kernel wrote; grids are sized for the worst case and idle
 // workgroups exit at once, so no host synchronisation is needed.

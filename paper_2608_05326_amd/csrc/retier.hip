@@ -1,5 +1,5 @@
 // Routing event: re-rank the candidate windows and re-tier them
-// (QEvict Sec. 3.3 candidate pool and TopK equations; Algorithm 1).
+// (QEvict Sec. 4.3 candidate pool and TopK equations; Algorithm 1).
 //
 // One 1024-thread workgroup per sequence:
 //   1. candidates = current Full and Quantized windows (the live list, in

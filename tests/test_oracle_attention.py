@@ -1,4 +1,4 @@
-"""Pins for the oracle's attention and window scores (Sec. 3.1, Sec. 3.2).
+"""Pins for the oracle's attention and window scores (Sec. 4.1, Sec. 4.2).
 
 * With every window in the bf16 tier the output equals ordinary softmax
   attention over all tokens (torch's scaled_dot_product_attention, float64).

@@ -1,4 +1,4 @@
-"""Pins for the oracle's quantizer (Sec. 3.3, migration-stable quantization).
+"""Pins for the oracle's quantizer (Sec. 4.3, migration-stable quantization).
 
 * the hand-derived examples in tests/golden/quant_worked_examples.json;
 * a brute-force reference in exact rational arithmetic (fractions.Fraction)

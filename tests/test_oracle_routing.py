@@ -1,4 +1,4 @@
-"""Pins for the oracle's routing (Sec. 3.3 candidate pool / TopK equations, Algorithm 1).
+"""Pins for the oracle's routing (Sec. 4.3 candidate pool / TopK equations, Algorithm 1).
 
 * hand-derived examples (tests/golden/quant_worked_examples.json);
 * brute force on tiny caches: among all subsets of the candidates, exactly
