@@ -43,7 +43,7 @@ from .numerics import FP16_MAX, rd_fp16, rne_bf16, rne_fp16, ru_fp16
 __all__ = [
     "OPEN", "AGED", "FULL", "QUANT", "EVICTED", "ACTIVE", "DORMANT",
     "OracleConfig", "QEvictUnit", "quantize_groups", "quantize_window",
-    "dequantize_window", "route_order", "tier_split", "QuantRangeError",
+    "dequantize_window", "route_order", "tier_split", "QuantRangeError", "CapacityError",
 ]
 
 # window states; OPEN and AGED are both inside / just out of the recent region
@@ -54,6 +54,10 @@ ACTIVE, DORMANT = 1, 2
 
 class QuantRangeError(ValueError):
     """A group's values fall outside the fp16 range of the scale/zero point."""
+
+
+class CapacityError(ValueError):
+    """A single-window move would put more than K_f / K_q windows in a tier."""
 
 
 @dataclasses.dataclass
@@ -391,6 +395,44 @@ class QEvictUnit:
             self.state[w] = EVICTED
             self.stats["evictions"] += 1
         return full, quant, evict
+
+    # -- single-window moves outside a routing event --------------------------
+    # The same transitions Algorithm 1 applies to a window entering Q or F,
+    # for one window chosen by the caller, within the tier capacities.
+    def quantize_one(self, w: int):
+        """Full -> Quantized: reactivate a dormant ledger entry as it is, or
+        quantize the window's bf16 values once (mixed-width caches give such a
+        new entry the upper width, 4 bits)."""
+        c = self.cfg
+        if self.state[w] != FULL:
+            raise ValueError(f"window {w} is not in the Full tier")
+        if int(np.sum(self.state == QUANT)) >= c.capacity_quant:
+            raise CapacityError("the Quantized tier already holds K_q windows")
+        e = self.ledger.get(w)
+        if e is None:
+            bits = c.bits if c.bits in (2, 4) else 4
+            self.ledger[w] = quantize_window(self.full_k[w], self.full_v[w], bits, c.group)
+            self.quant_count += 1
+        else:
+            e["state"] = ACTIVE
+        del self.full_k[w], self.full_v[w]
+        self.state[w] = QUANT
+
+    def promote_one(self, w: int):
+        """Quantized -> Full: bf16 values from the ledger (RNE of z + s c), the
+        entry stays as a dormant record."""
+        c = self.cfg
+        if self.state[w] != QUANT:
+            raise ValueError(f"window {w} is not in the Quantized tier")
+        if c.no_promotion:
+            raise ValueError("promotion is disabled (one-way policy)")
+        if int(np.sum(self.state == FULL)) >= c.capacity_full:
+            raise CapacityError("the Full tier already holds K_f windows")
+        kh, vh = dequantize_window(self.ledger[w])
+        self.full_k[w] = rne_bf16(kh)
+        self.full_v[w] = rne_bf16(vh)
+        self.ledger[w]["state"] = DORMANT
+        self.state[w] = FULL
 
     # -- perturbation used by the forced-promotion workload -------------------
     def shift_key_zero_points(self, w: int, delta):

@@ -7,6 +7,8 @@ and the quantize / promote migrations.  ``qevict`` is the ctypes binding.
 """
 from .qevict import (  # noqa: F401
     Cache, Config, QEvictError, RetierStats, load_library, workspace_size, SYMBOLS,
+    OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_BAD_STATE, ERR_NONFINITE,
+    ERR_CAPACITY, ERR_DEVICE,
     TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED,
     LEDGER_NONE, LEDGER_ACTIVE, LEDGER_DORMANT, BITS_MIXED_4_2, OUT_F32, OUT_BF16,
     FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES,

@@ -128,16 +128,23 @@ class Lockstep:
     # ---- phases ------------------------------------------------------------
     def prefill(self):
         wl = self.wl
+        from concurrent.futures import ThreadPoolExecutor
+
+        def gen(b, layer):
+            k, v = syn.prompt_kv(wl, self.seed, b, layer)
+            return k, v, syn.init_scores(wl, self.seed, b, layer)
+
         for li, layer in enumerate(self.layer_ids):
+            with ThreadPoolExecutor(max_workers=min(8, wl.batch)) as ex:
+                prompts = list(ex.map(lambda b: gen(b, layer), range(wl.batch)))
             ks, vs, inits = [], [], []
-            for b in range(wl.batch):
-                k, v = syn.prompt_kv(wl, self.seed, b, layer)
-                init = syn.init_scores(wl, self.seed, b, layer)
+            for b, (k, v, init) in enumerate(prompts):
                 ks.append(k)
                 vs.append(v)
                 inits.append(init)
                 if (li, b) in self.units:
                     self.units[(li, b)].prefill(from_bf16_bits(k), from_bf16_bits(v), init)
+            del prompts
             K = to_dev_bf16(np.stack(ks))
             V = to_dev_bf16(np.stack(vs))
             S = torch.from_numpy(np.stack(inits)).cuda()

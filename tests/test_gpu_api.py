@@ -1,0 +1,275 @@
+"""GPU tests of the C ABI beyond lockstep parity: single-window moves against
+the oracle, protocol and argument errors, latched device errors, the one-way
+policy, bf16 output, run-to-run determinism, the all-Full special case
+against plain attention, and the smoke entry point.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+
+import synthetic as syn
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+# ---------------------------------------------------------------------------
+# single-window moves (qevict_quantize_window / qevict_promote_window)
+# ---------------------------------------------------------------------------
+
+def test_manual_moves_match_oracle():
+    from tests.gpu_harness import Lockstep
+    from oracle.qevict_oracle import FULL, QUANT
+    wl = syn.get_workload("c1s")
+    # 64 prompt windows: 8 Full, 56 Quantized, room for 4 more Quantized
+    ls = Lockstep(wl, capacity_full=8, capacity_quant=60, steps=4)
+    try:
+        ls.prefill()
+        u, c = ls.units[(0, 0)], ls.cache
+        f = [int(w) for w in np.nonzero(u.state == FULL)[0]]
+        w = f[2]
+        c.quantize_window(0, 0, w)          # first quantization
+        u.quantize_one(w)
+        ls.compare_state(0, 0)
+        ls.compare_ledgers(0, 0, [w])
+        first = c.export_window(0, 0, w, quant=True)
+        c.promote_window(0, 0, w)           # dequantize-promote, ledger dormant
+        u.promote_one(w)
+        ls.compare_state(0, 0)
+        ls.compare_full(0, 0, [w])
+        c.quantize_window(0, 0, w)          # reactivation: same codes, no requantization
+        u.quantize_one(w)
+        ls.compare_state(0, 0)
+        again = c.export_window(0, 0, w, quant=True)
+        for k in first:
+            assert np.array_equal(first[k], again[k]), k
+        q = [int(x) for x in np.nonzero(u.state == QUANT)[0]]
+        c.promote_window(0, 0, q[-1])       # a Quantized window with a fresh ledger
+        u.promote_one(q[-1])
+        ls.compare_state(0, 0)
+        ls.compare_full(0, 0, [q[-1]])
+        # attention and routing keep agreeing after the moves
+        for _ in range(ls.steps):
+            ls.step()
+    finally:
+        ls.close()
+
+
+def test_manual_move_errors():
+    import paper_2608_05326_amd as qv
+    from tests.gpu_harness import Lockstep
+    from oracle.qevict_oracle import EVICTED, FULL, QUANT
+    wl = syn.get_workload("c1s")         # 16 Full, 24 Quantized, 24 evicted: both tiers full
+    ls = Lockstep(wl, steps=0)
+    try:
+        ls.prefill()
+        u, c = ls.units[(0, 0)], ls.cache
+        f = int(np.nonzero(u.state == FULL)[0][0])
+        q = int(np.nonzero(u.state == QUANT)[0][0])
+        e = int(np.nonzero(u.state == EVICTED)[0][0])
+        cases = [(c.quantize_window, f, qv.ERR_CAPACITY), (c.promote_window, q, qv.ERR_CAPACITY),
+                 (c.quantize_window, q, qv.ERR_BAD_STATE), (c.promote_window, f, qv.ERR_BAD_STATE),
+                 (c.quantize_window, e, qv.ERR_BAD_STATE), (c.promote_window, e, qv.ERR_BAD_STATE),
+                 (c.quantize_window, 10 ** 6, qv.ERR_INVALID_ARG)]
+        for fn, w, code in cases:
+            with pytest.raises(qv.QEvictError) as ex:
+                fn(0, 0, w)
+            assert ex.value.status == code, (fn.__name__, w, ex.value)
+        ls.compare_state(0, 0)               # nothing changed
+    finally:
+        ls.close()
+
+
+# ---------------------------------------------------------------------------
+# protocol, arguments and latched device errors
+# ---------------------------------------------------------------------------
+
+def _small_cache(flags=0, out_dtype=None, max_context=None, layers=1):
+    import paper_2608_05326_amd as qv
+    from tests.gpu_harness import gpu_config
+    wl = syn.get_workload("c2s")
+    if max_context is not None:
+        wl = wl.replace(steps=max_context - wl.prompt_len)
+    cfg = gpu_config(wl, layers, flags, out_dtype=qv.OUT_F32 if out_dtype is None else out_dtype)
+    return wl, qv.Cache(cfg)
+
+
+def _prompt(wl, seq=0, layer=0):
+    from tests.gpu_harness import to_dev_bf16
+    torch = _torch()
+    k, v = syn.prompt_kv(wl, 0, seq, layer)
+    s = syn.init_scores(wl, 0, seq, layer)
+    return to_dev_bf16(k[None]), to_dev_bf16(v[None]), torch.from_numpy(s[None].copy()).cuda()
+
+
+def _step_inputs(wl, t, seq=0, layer=0):
+    from tests.gpu_harness import to_dev_bf16
+    qs, ks, vs = syn.decode_inputs(wl, 0, seq, layer, t + 1)
+    return to_dev_bf16(qs[t][None]), to_dev_bf16(ks[t][None]), to_dev_bf16(vs[t][None])
+
+
+def test_protocol_and_argument_errors():
+    import paper_2608_05326_amd as qv
+    torch = _torch()
+    wl, c = _small_cache(max_context=32 * 96 + 13 + 2)
+    try:
+        out = torch.empty((1, wl.num_q_heads, 128), dtype=torch.float32, device="cuda")
+        q, kn, vn = _step_inputs(wl, 0)
+        with pytest.raises(qv.QEvictError) as ex:          # decode before prefill
+            c.decode_attend(0, q, kn, vn, out)
+        assert ex.value.status == qv.ERR_BAD_STATE
+        with pytest.raises(qv.QEvictError) as ex:          # routing before prefill
+            c.retier(0)
+        assert ex.value.status == qv.ERR_BAD_STATE
+        with pytest.raises(qv.QEvictError) as ex:          # layer out of range
+            c.retier(1)
+        assert ex.value.status == qv.ERR_INVALID_ARG
+        K, V, S = _prompt(wl)
+        c.prefill_assign(0, K, V, S)
+        with pytest.raises(qv.QEvictError) as ex:          # second prefill of a layer
+            c.prefill_assign(0, K, V, S)
+        assert ex.value.status == qv.ERR_BAD_STATE
+        lib, h = c.lib, c.handle
+        null = ctypes.c_void_p(None)
+        p = lambda t: ctypes.c_void_p(t.data_ptr())
+        st = lib.qevict_decode_attend(h, 0, null, p(kn), p(vn), p(out))
+        assert st == qv.ERR_INVALID_ARG
+        st = lib.qevict_decode_attend(h, 0, ctypes.c_void_p(q.data_ptr() + 2), p(kn), p(vn), p(out))
+        assert st == qv.ERR_INVALID_ARG                     # misaligned query
+        # the cache is still usable after rejected calls
+        for t in range(2):
+            q, kn, vn = _step_inputs(wl, t)
+            c.decode_attend(0, q, kn, vn, out)
+            c.retier(0)
+        q, kn, vn = _step_inputs(wl, 2)
+        with pytest.raises(qv.QEvictError) as ex:          # max_context reached
+            c.decode_attend(0, q, kn, vn, out)
+        assert ex.value.status == qv.ERR_BAD_STATE
+        assert torch.isfinite(out).all()
+    finally:
+        c.close()
+
+
+def test_nonfinite_initial_score_latches_error():
+    import paper_2608_05326_amd as qv
+    wl, c = _small_cache()
+    try:
+        K, V, S = _prompt(wl)
+        S[0, 3] = float("nan")
+        c.prefill_assign(0, K, V, S)                        # enqueued; checked on the device
+        with pytest.raises(qv.QEvictError) as ex:
+            c.get_state(0, 0)
+        assert ex.value.status == qv.ERR_NONFINITE
+        with pytest.raises(qv.QEvictError) as ex:          # the cache now only accepts destroy
+            c.retier(0)
+        assert ex.value.status == qv.ERR_BAD_STATE
+    finally:
+        c.close()
+
+
+# ---------------------------------------------------------------------------
+# policies, output type, determinism
+# ---------------------------------------------------------------------------
+
+def test_one_way_policy_lockstep():
+    import paper_2608_05326_amd as qv
+    from tests.gpu_harness import Lockstep
+    ls = Lockstep(syn.get_workload("c2s"), flags=qv.FLAG_NO_PROMOTION, steps=16)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    assert ls.promotions == 0 and ls.events == 16
+
+
+def _run_gpu_only(wl, steps, out_dtype, flags=0):
+    torch = _torch()
+    wl_, c = _small_cache(flags=flags, out_dtype=out_dtype)
+    outs, states = [], []
+    try:
+        K, V, S = _prompt(wl)
+        c.prefill_assign(0, K, V, S)
+        dt = torch.bfloat16 if out_dtype == 1 else torch.float32
+        for t in range(steps):
+            q, kn, vn = _step_inputs(wl, t)
+            out = torch.empty((1, wl.num_q_heads, 128), dtype=dt, device="cuda")
+            c.decode_attend(0, q, kn, vn, out)
+            c.retier(0)
+            outs.append(out.cpu())
+            st = c.get_state(0, 0)
+            states.append(st)
+    finally:
+        c.close()
+    return outs, states
+
+
+def test_repeat_runs_are_bitwise_identical():
+    wl = syn.get_workload("c2s")
+    o1, s1 = _run_gpu_only(wl, 8, 0)
+    o2, s2 = _run_gpu_only(wl, 8, 0)
+    for a, b in zip(o1, o2):
+        assert _torch().equal(a, b)
+    for a, b in zip(s1, s2):
+        for k in ("tiers", "scores", "ledger", "bits"):
+            assert np.array_equal(a[k], b[k]), k
+
+
+def test_bf16_output_is_rounded_fp32_output():
+    torch = _torch()
+    wl = syn.get_workload("c2s")
+    o32, s32 = _run_gpu_only(wl, 6, 0)
+    o16, s16 = _run_gpu_only(wl, 6, 1)
+    for a, b in zip(o32, o16):
+        assert torch.equal(a.to(torch.bfloat16), b)
+    for a, b in zip(s32, s16):
+        assert np.array_equal(a["scores"], b["scores"])
+
+
+# ---------------------------------------------------------------------------
+# all-Full special case: plain attention over every token
+# ---------------------------------------------------------------------------
+
+def test_all_full_equals_plain_attention():
+    import paper_2608_05326_amd as qv
+    from tests.gpu_harness import gpu_config, to_dev_bf16
+    from oracle.numerics import from_bf16_bits
+    torch = _torch()
+    wl = syn.get_workload("c2s")
+    n_hist = wl.n_hist_windows
+    cfg = gpu_config(wl, 1, capacity_full=n_hist, capacity_quant=0)
+    c = qv.Cache(cfg)
+    try:
+        k, v = syn.prompt_kv(wl, 0, 0, 0)
+        c.prefill_assign(0, to_dev_bf16(k[None]), to_dev_bf16(v[None]),
+                         torch.from_numpy(syn.init_scores(wl, 0, 0, 0)[None].copy()).cuda())
+        qs, ks, vs = syn.decode_inputs(wl, 0, 0, 0, 5)
+        K = torch.from_numpy(from_bf16_bits(k))          # float64 [H_kv, T, d]
+        V = torch.from_numpy(from_bf16_bits(v))
+        G = wl.num_q_heads // wl.num_kv_heads
+        for t in range(5):
+            out = torch.empty((1, wl.num_q_heads, 128), dtype=torch.float32, device="cuda")
+            c.decode_attend(0, to_dev_bf16(qs[t][None]), to_dev_bf16(ks[t][None]),
+                            to_dev_bf16(vs[t][None]), out)
+            c.retier(0)
+            K = torch.cat([K, torch.from_numpy(from_bf16_bits(ks[t]))[:, None]], dim=1)
+            V = torch.cat([V, torch.from_numpy(from_bf16_bits(vs[t]))[:, None]], dim=1)
+            q = torch.from_numpy(from_bf16_bits(qs[t])).view(wl.num_kv_heads, G, 128)
+            ref = torch.softmax(q @ K.transpose(1, 2) / np.sqrt(128.0), dim=-1) @ V   # [H_kv, G, d]
+            ref = ref.reshape(wl.num_q_heads, 128).numpy()
+            got = out[0].cpu().numpy().astype(np.float64)
+            err = np.abs(got - ref).max(axis=1) / np.linalg.norm(ref, axis=1)
+            assert np.all(err <= 2e-3), err.max()
+        st = c.get_state(0, 0)
+        assert not np.any(st["tiers"] == qv.TIER_QUANT) and not np.any(st["tiers"] == qv.TIER_EVICTED)
+    finally:
+        c.close()
+
+
+def test_smoke_entry_point():
+    import __graft_entry__
+    __graft_entry__.smoke()

@@ -1,0 +1,46 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times (default split count), against the float64 oracle.
+
+Each case runs a few lockstep steps (outputs, scores, tiers, ledgers, codes,
+promoted values; see gpu_harness for the bars).  Where a workload has
+several sequences or layers, every sequence runs on the GPU and a sample of
+them is mirrored by the oracle.
+"""
+import pytest
+
+import synthetic as syn
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def _lockstep(name, **kw):
+    from tests.gpu_harness import Lockstep
+    wl = syn.get_workload(name)
+    ls = Lockstep(wl, **kw)
+    print(f"[fullsize] {name} prompt={wl.prompt_len} B={wl.batch} steps={ls.steps} "
+          f"layers={ls.layer_ids} checked seqs={ls.check_seqs}", flush=True)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[fullsize] {name}: max out err {ls.max_out_err:.2e}, max score err {ls.max_score_err:.2e}, "
+          f"promotions {ls.promotions} over {ls.events} events", flush=True)
+    return ls
+
+
+def test_8b_32k_bench_config():
+    _lockstep("c2", steps=6)
+
+
+def test_8b_128k_int2_w64():
+    _lockstep("c4", steps=3)
+
+
+def test_70b_64k_mixed_bits_batch4():
+    # routing every 8 steps: step 8 is the first routing event
+    _lockstep("c5", steps=9, check_seqs=[0, 3])
+
+
+def test_8b_32k_batch8_layer_sample():
+    # one of the 32 layers, all 8 sequences on the GPU, two mirrored
+    _lockstep("c3", steps=3, layer_ids=(31,), check_seqs=[0, 7])
