@@ -50,6 +50,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle baseline time budget")
     p.add_argument("--no-cpu", action="store_true")
     p.add_argument("--splits", type=int, default=0, help="split-K factor (0 = library default)")
+    p.add_argument("--routing", choices=("async", "sync"), default="async",
+                   help="async: a layer's routing runs on the library's routing stream, overlapping "
+                        "the attention of the other layers; sync: everything on one stream")
     p.add_argument("--no-kernel-events", action="store_true",
                    help="do not time each kernel launch with HIP events (no roofline)")
     p.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MB",
@@ -173,13 +176,15 @@ def main():
 
     wl = syn.get_workload(args.workload)
     NL = args.instances
-    per_layer = -(-(args.warmup + args.steps) // NL) + 1
+    # + four rounds of attention timing and two of routing statistics after the timed steps
+    per_layer = -(-(args.warmup + args.steps) // NL) + 7
+    asyncr = args.routing == "async"
     cfg = qv.Config(batch=wl.batch, num_layers=NL, num_q_heads=wl.num_q_heads,
                     num_kv_heads=wl.num_kv_heads, window_tokens=wl.window, group_size=wl.group,
                     quant_bits=wl.bits, max_context=wl.prompt_len + per_layer,
                     capacity_full=wl.capacity_full, capacity_quant=wl.capacity_quant,
                     sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=1,
-                    num_splits=args.splits)
+                    num_splits=args.splits, flags=qv.FLAG_ASYNC_ROUTING if asyncr else 0)
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)
     cache = qv.Cache(cfg, stream=stream)
@@ -227,27 +232,33 @@ def main():
             raise RuntimeError(lib.qevict_last_error().decode())
 
     # A step is one layer cache's decode_attend followed (before that cache is
-    # used again) by its retier.  Steps run in rounds over the layer caches:
-    # the attention of every cache of the round, then the routing of each, so
-    # the attention launches of a round run back to back and one pair of
-    # events brackets them.
-    def rounds(first, count, events=None):
+    # used again) by its retier; steps cycle over the layer caches.  With
+    # synchronous routing the steps run in rounds -- the decode_attend of every
+    # cache, then the retier of each -- so one pair of events brackets the
+    # back-to-back attention calls of a round.
+    def run_steps(first, count, events=None):
         i = first
         while i < first + count:
             layers = [(i + k) % NL for k in range(min(NL - i % NL, first + count - i))]
-            if events is not None:
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
-            for l in layers:
-                attend(l)
-            if events is not None:
-                e1.record(stream)
-                events.append((e0, e1, len(layers)))
-            for l in layers:
-                route(l)
+            if asyncr and events is None:
+                for l in layers:
+                    attend(l)
+                    route(l)
+            else:
+                if events is not None:
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                for l in layers:
+                    attend(l)
+                if events is not None:
+                    e1.record(stream)
+                    events.append((e0, e1, len(layers)))
+                for l in layers:
+                    route(l)
             i += len(layers)
 
-    rounds(0, args.warmup)
+    run_steps(0, args.warmup)
+    cache.join_routing()
     torch.cuda.synchronize()
     st0 = [cache.get_state(l, 0) for l in range(NL)]
 
@@ -257,15 +268,41 @@ def main():
     attn_events = []
     ev0.record(stream)
     t_wall = time.perf_counter()
-    rounds(args.warmup, args.steps, None if args.no_kernel_events else attn_events)
+    run_steps(args.warmup, args.steps, None if (asyncr or args.no_kernel_events) else attn_events)
+    cache.join_routing()
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
     gpu_ms = ev0.elapsed_time(ev1)
     ms_per_step = gpu_ms / args.steps
+    done = args.warmup + args.steps
+
+    # ---- attention timing with asynchronous routing: rounds of back-to-back
+    # decode_attend calls, each started after the previous round's routing ----
+    if asyncr and not args.no_kernel_events:
+        for _ in range(4):
+            cache.join_routing()
+            torch.cuda.synchronize()
+            run_steps(done, NL, attn_events)
+            done += NL
+        cache.join_routing()
+        torch.cuda.synchronize()
     attend_us = None
     if attn_events:
         attend_us = sum(a.elapsed_time(b) for a, b, _ in attn_events) * 1e3 / sum(n for _, _, n in attn_events)
+
+    # ---- routing activity: two more (untimed) rounds with the retier stats read back ----
+    promo = react = evict = 0
+    n_ev = 0
+    for _ in range(2):
+        for l in range(NL):
+            attend(l)
+        for l in range(NL):
+            s_ = cache.retier(l, stats=True)
+            promo += s_["promotions"]
+            react += s_["reactivations"]
+            evict += s_["evictions"]
+            n_ev += 1
 
     # ---- algorithmic bytes of the timed attention launches ----
     total_bytes = 0
@@ -297,11 +334,13 @@ def main():
                                "heads, head_dim 128, windows of 32, 20% bf16 / 30% int4 group 32 / 50% "
                                "evicted, re-tier every step, drifting queries",
                    "layer_caches_rotated": NL, "global_batch": wl.batch, "seq_len": wl.prompt_len,
-                   "parallelism": "single GPU"},
+                   "routing": args.routing, "parallelism": "single GPU"},
         "step_GBps": round(bytes_per_step / (ms_per_step * 1e-3) / 1e9, 1),
         "algorithmic_MB_per_step": round(bytes_per_step / 1e6, 3),
         "host_wall_us_per_step": round(wall / args.steps * 1e6, 2),
         "attend_us_per_launch": round(attend_us, 3) if attend_us else None,
+        "routing_per_step": {"promotions": round(promo / n_ev, 2), "reactivations": round(react / n_ev, 2),
+                             "evictions": round(evict / n_ev, 2)},
     }
     if attend_us:
         ach = bytes_per_step / (attend_us * 1e-6) / 1e9

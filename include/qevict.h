@@ -72,6 +72,13 @@ enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT =
 #define QEVICT_OUT_BF16 1
 #define QEVICT_FLAG_NO_PROMOTION 0x1u  /* one-way Full -> Quantized -> Evicted policy (App. K)      */
 #define QEVICT_FLAG_DEBUG_MASSES 0x2u  /* keep per-head window masses of the last step              */
+/* Routing work (re-rank, quantize, promote) of qevict_retier runs on a stream
+ * the library owns, after that layer's latest decode_attend, so the routing of
+ * one layer overlaps the attention of others.  Every later call that touches
+ * the same layer (decode_attend, prefill, manual moves, state queries) is
+ * ordered after it; qevict_join_routing orders the cache stream after the
+ * routing of every layer. */
+#define QEVICT_FLAG_ASYNC_ROUTING 0x4u
 
 typedef struct {
   int32_t abi_version;       /* QEVICT_ABI_VERSION                                          */
@@ -196,6 +203,11 @@ qevict_status qevict_profile_read(qevict_cache *c, int32_t kernel, double *total
  * the attention pass (live windows' codes/values, recent and sink tokens,
  * queries, outputs, scores; synchronous). */
 qevict_status qevict_last_attend_bytes(qevict_cache *c, int32_t layer, int64_t *bytes);
+
+/* Make the cache's stream wait (on the device, no host synchronisation) for
+ * all routing work enqueued so far.  A no-op without QEVICT_FLAG_ASYNC_ROUTING.
+ * After it, synchronising the cache's stream also covers every retier call. */
+qevict_status qevict_join_routing(qevict_cache *c);
 
 const char *qevict_status_string(qevict_status s);
 const char *qevict_last_error(void);

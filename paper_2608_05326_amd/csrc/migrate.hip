@@ -31,20 +31,27 @@ __device__ bool quant_params(float lo, float hi, int nbits, uint16_t* zb, uint16
   return true;
 }
 
-__device__ int quant_code(float x, double z, double s, int nmax) {
+// Round-half-even code of x: an fp32 estimate of (x - z) / s, then the exact
+// decision against the two neighbouring half-step boundaries z + (c +- 1/2) s
+// (exact in float64: fp16 operands, |c| <= 16).  No division per element.
+__device__ __forceinline__ int quant_code(float x, float zf, float inv_s, double z, double s,
+                                          int nmax) {
   if (s == 0.0) return 0;
+  float c0 = rintf((x - zf) * inv_s);
+  c0 = fminf(fmaxf(c0, 0.f), (float)nmax);
+  int c = (int)c0;
   const double xd = x;
-  double c = __builtin_rint((xd - z) / s);
-  for (int k = 0; k < 4; ++k) {
-    if (xd < z + (c - 0.5) * s) c -= 1.0;
-    else if (xd > z + (c + 0.5) * s) c += 1.0;
-    else break;
+  for (int k = 0; k < 2; ++k) {
+    const double hi = z + ((double)c + 0.5) * s, lo = z + ((double)c - 0.5) * s;
+    if ((xd > hi || (xd == hi && (c & 1))) && c < nmax) {
+      ++c;
+    } else if ((xd < lo || (xd == lo && (c & 1))) && c > 0) {
+      --c;
+    } else {
+      break;
+    }
   }
-  const bool odd = __builtin_fmod(c, 2.0) != 0.0;
-  if (odd && xd == z + (c + 0.5) * s) c += 1.0;
-  else if (odd && xd == z + (c - 0.5) * s) c -= 1.0;
-  int ci = (int)c;
-  return ci < 0 ? 0 : (ci > nmax ? nmax : ci);
+  return c;
 }
 
 // Load one KV head of a window into LDS in natural [t][c] layout.
@@ -63,14 +70,20 @@ __device__ void load_window(const MigrateArgs& a, uint8_t* ub, int b, int g, int
   } else {
     const uint8_t* p = ub + (src_kind == SRC_FSLOT ? a.L.fpool : a.L.ring) +
                        (int64_t)src_idx * G.fslot_bytes + g * G.fhead_bytes;
-    // K chunks hold 8 consecutive channels of one token per lane: 16-byte moves
+    const uint8_t* pv = p + (int64_t)W * kHeadDim * 2;
+    // K chunk (tb, kb), lane 16q + r: token 16 tb + r, channels 32 kb + 8 q .. + 7
+    // V chunk (kt, cb), lane 16q + r: tokens tok(kt, q, 0..7), channel 16 cb + r
     for (int i = tid; i < W * kHeadDim / 8; i += blockDim.x) {
-      const int t = i / 16, c = (i % 16) * 8;
-      ((u32x4*)sk)[i] = *(const u32x4*)(p + k_elem_off(t, c));
-    }
-    for (int i = tid; i < W * kHeadDim; i += blockDim.x) {
-      const int t = i >> 7, c = i & 127;
-      sv[i] = *(const uint16_t*)(p + v_elem_off(W, t, c));
+      const int chunk = i >> 6, L = i & 63, q = L >> 4, r = L & 15;
+      const u32x4 kx = *(const u32x4*)(p + (int64_t)i * 16);
+      const u32x4 vx = *(const u32x4*)(pv + (int64_t)i * 16);
+      *(u32x4*)(sk + (16 * (chunk >> 2) + r) * kHeadDim + 32 * (chunk & 3) + 8 * q) = kx;
+      const int kt = chunk >> 3, c = 16 * (chunk & 7) + r;
+      const uint32_t v0 = vx[0], v1 = vx[1], v2 = vx[2], v3 = vx[3];
+      const uint32_t vw[4] = {v0, v1, v2, v3};
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        sv[v_tok(kt, q, j) * kHeadDim + c] = (uint16_t)(vw[j >> 1] >> (16 * (j & 1)));
     }
   }
 }
@@ -107,8 +120,10 @@ __global__ __launch_bounds__(256) void k_quantize(MigrateArgs a) {
       uint16_t zb = 0, sb = 0;
       if (!quant_params(lo, hi, nb, &zb, &sb)) set_error(counts, ERR_RANGE);
       const double z = fp16_bits_to_f64(zb), s = fp16_bits_to_f64(sb);
+      const float zf = (float)z, inv_s = s > 0.0 ? 1.f / (float)s : 0.f;
       for (int t = 0; t < W; ++t)
-        ck[t * kHeadDim + c] = (uint8_t)quant_code(bf16_to_f32(sk[t * kHeadDim + c]), z, s, nmax);
+        ck[t * kHeadDim + c] =
+            (uint8_t)quant_code(bf16_to_f32(sk[t * kHeadDim + c]), zf, inv_s, z, s, nmax);
       uint16_t* mk = (uint16_t*)(rec + meta_k_off(G));
       mk[c] = sb;
       mk[kHeadDim + c] = zb;
@@ -127,47 +142,70 @@ __global__ __launch_bounds__(256) void k_quantize(MigrateArgs a) {
         uint16_t zb = 0, sb = 0;
         if (!quant_params(lo, hi, nb, &zb, &sb)) set_error(counts, ERR_RANGE);
         const double z = fp16_bits_to_f64(zb), s = fp16_bits_to_f64(sb);
+        const float zf = (float)z, inv_s = s > 0.0 ? 1.f / (float)s : 0.f;
         for (int i = 0; i < G.G; ++i)
-          cv[t * kHeadDim + vg * G.G + i] = (uint8_t)quant_code(bf16_to_f32(row[i]), z, s, nmax);
+          cv[t * kHeadDim + vg * G.G + i] =
+              (uint8_t)quant_code(bf16_to_f32(row[i]), zf, inv_s, z, s, nmax);
         uint16_t* mv = (uint16_t*)(rec + meta_v_elem(G, t, vg));
         mv[0] = sb;
         mv[8] = zb;
       }
     }
     __syncthreads();
-    // pack codes: storage word (m, lane, comp) holds 4/nb entries of 8 codes
-    const int words = W * kHeadDim * nb / 32;   // per code area
+    // pack: thread (area, block m, lane L) writes the 16-byte block of words 4m .. 4m + 3 of
+    // lane L; word wd holds entries wd * per + ee (per = 4 / nb), 8 codes each
+    const int nblk = W * nb / 64;
     const int per = 4 / nb;
-    for (int sp = tid; sp < words; sp += blockDim.x) {
-      const int m = sp >> 8, L = (sp >> 2) & 63, comp = sp & 3;
-      const int word = m * 4 + comp;
-      uint32_t wk = 0, wv = 0;
-      for (int ee = 0; ee < per; ++ee) {
-        const int ent_idx = word * per + ee;
-        for (int j = 0; j < 8; ++j) {
-          const int sh = (j & 1) * 16 + nb * (4 * ee + (j >> 1));
-          // key entry (tb, kb): token 16 tb + (L & 15), channel 32 kb + 8 (L >> 4) + j
-          const int tk = 16 * (ent_idx >> 2) + (L & 15);
-          const int chk = 32 * (ent_idx & 3) + 8 * (L >> 4) + j;
-          wk |= (uint32_t)ck[tk * kHeadDim + chk] << sh;
-          // value entry (kt, cb): token tok(kt, L >> 4, j), channel 16 cb + (L & 15)
-          const int tv = v_tok(ent_idx >> 3, L >> 4, j);
-          const int chv = 16 * (ent_idx & 7) + (L & 15);
-          wv |= (uint32_t)cv[tv * kHeadDim + chv] << sh;
+    for (int tk = tid; tk < 2 * nblk * 64; tk += blockDim.x) {
+      const int area = tk / (nblk * 64), m = (tk >> 6) % nblk, L = tk & 63;
+      const int q = L >> 4, r = L & 15;
+      uint32_t wv[4];
+#pragma unroll
+      for (int comp = 0; comp < 4; ++comp) {
+        uint32_t wd = 0;
+        for (int ee = 0; ee < per; ++ee) {
+          const int ei = (m * 4 + comp) * per + ee;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int sh = (j & 1) * 16 + nb * (4 * ee + (j >> 1));
+            uint32_t code;
+            if (area == 0)   // key entry (tb, kb): token 16 tb + r, channel 32 kb + 8 q + j
+              code = ck[(16 * (ei >> 2) + r) * kHeadDim + 32 * (ei & 3) + 8 * q + j];
+            else             // value entry (kt, cb): token tok(kt, q, j), channel 16 cb + r
+              code = cv[v_tok(ei >> 3, q, j) * kHeadDim + 16 * (ei & 7) + r];
+            wd |= code << sh;
+          }
         }
+        wv[comp] = wd;
       }
-      *(uint32_t*)(rec + (int64_t)sp * 4) = wk;
-      *(uint32_t*)(rec + G.qcodes_bytes + (int64_t)sp * 4) = wv;
+      *(u32x4*)(rec + area * G.qcodes_bytes + ((int64_t)m * 64 + L) * 16) =
+          (u32x4){wv[0], wv[1], wv[2], wv[3]};
     }
     __syncthreads();
   }
 }
 
-__device__ __forceinline__ int read_code(const uint8_t* area, int nb, int e, int L, int j) {
-  int64_t off;
-  int sh;
-  code_loc(nb, e, L, j, &off, &sh);
-  return (int)((*(const uint32_t*)(area + off) >> sh) & ((1u << nb) - 1));
+// 8 bf16 values z_j + s_j c_j (exact in float64, one rounding) packed for a 16-byte store
+__device__ __forceinline__ u32x4 dequant8(uint32_t wd, int shift0, int nb, u32x4 s8, u32x4 z8) {
+  const uint32_t mask = (1u << nb) - 1u;
+  const uint32_t sw[4] = {s8[0], s8[1], s8[2], s8[3]};
+  const uint32_t zw[4] = {z8[0], z8[1], z8[2], z8[3]};
+  uint32_t outw[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t pair = 0;
+#pragma unroll
+    for (int o = 0; o < 2; ++o) {
+      const int j = 2 * i + o;
+      const uint32_t code = (wd >> (o * 16 + shift0 + nb * i)) & mask;
+      const double sj = fp16_bits_to_f64((uint16_t)(sw[i] >> (16 * o)));
+      const double zj = fp16_bits_to_f64((uint16_t)(zw[i] >> (16 * o)));
+      pair |= (uint32_t)f64_to_bf16_rne(zj + sj * (double)code) << (16 * o);
+      (void)j;
+    }
+    outw[i] = pair;
+  }
+  return (u32x4){outw[0], outw[1], outw[2], outw[3]};
 }
 
 __global__ __launch_bounds__(256) void k_promote(MigrateArgs a) {
@@ -199,21 +237,38 @@ __global__ __launch_bounds__(256) void k_promote(MigrateArgs a) {
         const int t = i >> 7, c = i & 127;
         *(uint16_t*)(dp + v_elem_off(W, t, c)) = vs[t * kHeadDim + c];
       }
-    } else {   // SRC_QSLOT: exact dequantization, single rounding to bf16
+    } else {
+      // SRC_QSLOT: thread (area, block m, lane L) expands the entries held by the 16-byte
+      // code block m of lane L straight into the bf16 chunks at the same (entry, lane)
       const uint8_t* rec = ub + a.L.qpool + (int64_t)src_idx * G.qslot_bytes + g * G.qrec_bytes;
-      const uint16_t* mk = (const uint16_t*)(rec + meta_k_off(G));
-      for (int i = tid; i < W * kHeadDim; i += blockDim.x) {
-        const int t = i >> 7, c = i & 127;
-        int ee, L, j;
-        k_code_pos(t, c, &ee, &L, &j);
-        const int code = read_code(rec, nb, ee, L, j);
-        const double x = fp16_bits_to_f64(mk[kHeadDim + c]) + fp16_bits_to_f64(mk[c]) * code;
-        *(uint16_t*)(dp + k_elem_off(t, c)) = f64_to_bf16_rne(x);
-        v_code_pos(t, c, &ee, &L, &j);
-        const int cvv = read_code(rec + G.qcodes_bytes, nb, ee, L, j);
-        const uint16_t* mv = (const uint16_t*)(rec + meta_v_elem(G, t, c / G.G));
-        const double y = fp16_bits_to_f64(mv[8]) + fp16_bits_to_f64(mv[0]) * cvv;
-        *(uint16_t*)(dp + v_elem_off(W, t, c)) = f64_to_bf16_rne(y);
+      const int nblk = W * nb / 64;
+      const int per = 4 / nb;
+      const int ng = kHeadDim / G.G;
+      for (int tk = tid; tk < 2 * nblk * 64; tk += blockDim.x) {
+        const int area = tk / (nblk * 64), m = (tk >> 6) % nblk, L = tk & 63;
+        const int q = L >> 4, r = L & 15;
+        const u32x4 blk = *(const u32x4*)(rec + area * G.qcodes_bytes + ((int64_t)m * 64 + L) * 16);
+        const uint32_t bw[4] = {blk[0], blk[1], blk[2], blk[3]};
+        for (int comp = 0; comp < 4; ++comp) {
+          for (int ee = 0; ee < per; ++ee) {
+            const int ei = (m * 4 + comp) * per + ee;
+            u32x4 s8, z8;
+            int64_t off;
+            if (area == 0) {   // key entry (tb, kb): channels 32 kb + 8 q .. + 7 of token 16 tb + r
+              const int c0 = 32 * (ei & 3) + 8 * q;
+              s8 = *(const u32x4*)(rec + meta_k_off(G) + 2 * c0);
+              z8 = *(const u32x4*)(rec + meta_k_off(G) + 2 * kHeadDim + 2 * c0);
+              off = ((int64_t)ei * 64 + L) * 16;
+            } else {           // value entry (kt, cb): tokens tok(kt, q, 0..7) of channel 16 cb + r
+              const int kt = ei >> 3, c = 16 * (ei & 7) + r;
+              const uint8_t* pm = rec + meta_v_off(G) + ((kt * 4 + q) * ng + c / G.G) * 32;
+              s8 = *(const u32x4*)pm;
+              z8 = *(const u32x4*)(pm + 16);
+              off = (int64_t)W * kHeadDim * 2 + ((int64_t)ei * 64 + L) * 16;
+            }
+            *(u32x4*)(dp + off) = dequant8(bw[comp], 4 * nb * ee, nb, s8, z8);
+          }
+        }
       }
     }
   }

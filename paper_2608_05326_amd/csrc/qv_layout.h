@@ -92,7 +92,7 @@ struct UnitLayout {
   int64_t fowner, qowner;
   int64_t item_win, item_ref, item_cost, item_aux, item_score;
   int64_t qlist, plist, counts, stats;
-  int64_t partial, mref, dbg_mass;
+  int64_t partial, pml, mref, dbg_mass;
 };
 
 QV_HD int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }

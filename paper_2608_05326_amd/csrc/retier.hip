@@ -521,6 +521,12 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       icost[pos] = sd[c];
     }
   }
+  // list positions after the live windows hold the recent-region windows of the
+  // next steps: their scores as they stand (windows not started yet: 0)
+  for (int j = tid; n_items + j < G.max_items; j += NT) {
+    const int w = a.aged_w1 + j;
+    iscore[n_items + j] = w < G.nwc ? score[w] : 0.f;
+  }
   __syncthreads();
   if (tid == 0) {
     icost[n_items] = tots2[1];

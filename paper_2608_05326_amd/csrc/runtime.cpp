@@ -76,6 +76,9 @@ struct qevict_cache {
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
   hipStream_t stream = nullptr;
+  hipStream_t rstream = nullptr;            // routing stream (QEVICT_FLAG_ASYNC_ROUTING)
+  std::vector<hipEvent_t> attn_ev, route_ev;   // per layer: latest attention / routing done
+  std::vector<char> route_pending;          // routing enqueued that the cache stream has not joined
   std::vector<LayerState> layers;
   bool poisoned = false;
   bool profiling = false;
@@ -112,15 +115,14 @@ qevict_status check_config(const qevict_config* c) {
   if (c->retier_interval < 1) return fail(QEVICT_ERR_INVALID_ARG, "retier_interval must be >= 1");
   if (c->out_dtype != QEVICT_OUT_F32 && c->out_dtype != QEVICT_OUT_BF16)
     return fail(QEVICT_ERR_INVALID_ARG, "out_dtype");
-  if (c->flags & ~(QEVICT_FLAG_NO_PROMOTION | QEVICT_FLAG_DEBUG_MASSES))
+  if (c->flags & ~(QEVICT_FLAG_NO_PROMOTION | QEVICT_FLAG_DEBUG_MASSES | QEVICT_FLAG_ASYNC_ROUTING))
     return fail(QEVICT_ERR_INVALID_ARG, "unknown flags 0x%x", c->flags);
   if (!(c->softmax_scale >= 0.f) || !std::isfinite(c->softmax_scale))
     return fail(QEVICT_ERR_INVALID_ARG, "softmax_scale");
   if (c->num_splits < 0 || c->num_splits > 256)
     return fail(QEVICT_ERR_INVALID_ARG, "num_splits must be in [0, 256]");
-  if (c->num_q_heads > 0 && c->num_splits > 32 * (256 / c->num_q_heads))
-    return fail(QEVICT_ERR_UNSUPPORTED, "num_splits above %d for %d query heads",
-                32 * (256 / c->num_q_heads), c->num_q_heads);
+  if (c->num_splits * c->num_q_heads > 2048)
+    return fail(QEVICT_ERR_UNSUPPORTED, "num_splits x num_q_heads must be <= 2048");
   const int W = c->window_tokens;
   const int nr = ceil_div(c->recent_tokens, W) + ceil_div(c->retier_interval, W) + 2;
   if (c->capacity_full + c->capacity_quant + nr > kMaxCand)
@@ -159,6 +161,7 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
     ns = ns < 1 ? 1 : (ns > 64 ? 64 : ns);
     int per_split = ceil_div(g->max_items, ns);
     if (per_split < 2) ns = ceil_div(g->max_items, 2);
+    if (ns * g->H_q > 2048) ns = 2048 / g->H_q;   // split statistics of the merge live in LDS
   }
   g->n_split = ns;
   g->out_bf16 = c->out_dtype == QEVICT_OUT_BF16;
@@ -205,7 +208,8 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   L->plist = take(4LL * kQEntry * (g->max_fq + 1));
   L->counts = take(4LL * CNT_N);
   L->stats = take(4LL * ST_N);
-  L->partial = take(4LL * g->H_q * g->n_split * (g->d + 2));
+  L->partial = take(4LL * g->H_q * g->n_split * g->d);
+  L->pml = take(8LL * g->H_q * g->n_split);
   L->mref = take(8LL * g->H_q * g->max_items);
   L->dbg_mass = take((c->flags & QEVICT_FLAG_DEBUG_MASSES) ? 4LL * g->H_q * (g->nwc + 1) : 0);
   L->unit_bytes = align256(off);
@@ -223,11 +227,27 @@ uint8_t* unit_base(qevict_cache* c, int layer, int seq) {
   return c->ws + kHeaderBytes + ((int64_t)layer * c->g.B + seq) * c->L.unit_bytes;
 }
 
+// Asynchronous routing: order the cache stream after the routing work of a
+// layer (a device-side wait), and publish the cache stream's progress on a
+// layer for the next routing of that layer.
+hipError_t join_layer(qevict_cache* c, int layer) {
+  if (!c->rstream || !c->route_pending[layer]) return hipSuccess;
+  hipError_t e = hipStreamWaitEvent(c->stream, c->route_ev[layer], 0);
+  if (e == hipSuccess) c->route_pending[layer] = 0;
+  return e;
+}
+hipError_t mark_layer(qevict_cache* c, int layer) {
+  return c->rstream ? hipEventRecord(c->attn_ev[layer], c->stream) : hipSuccess;
+}
+
+// Validates the handle and the layer; every later use of the layer on the
+// cache stream is ordered after its pending routing work.
 qevict_status check_handle(qevict_cache* c, int layer) {
   if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
   if (c->poisoned) return fail(QEVICT_ERR_BAD_STATE, "cache is in an error state; destroy it");
   if (layer < 0 || layer >= c->cfg.num_layers)
     return fail(QEVICT_ERR_INVALID_ARG, "layer %d out of range", layer);
+  if (hipError_t e = join_layer(c, layer)) return hip_fail(e, "joining the routing stream");
   return QEVICT_OK;
 }
 
@@ -245,7 +265,7 @@ hipEvent_t take_event(qevict_cache* c) {
 
 void fold_pending(qevict_cache* c) {
   if (c->pending.empty()) return;
-  (void)hipEventSynchronize(c->pending.back().stop);
+  for (auto& t : c->pending) (void)hipEventSynchronize(t.stop);   // launches may sit on two streams
   for (auto& t : c->pending) {
     float ms = 0.f;
     if (hipEventElapsedTime(&ms, t.start, t.stop) == hipSuccess) {
@@ -259,14 +279,14 @@ void fold_pending(qevict_cache* c) {
 }
 
 template <typename F>
-hipError_t timed(qevict_cache* c, int kernel, F&& launch) {
+hipError_t timed(qevict_cache* c, int kernel, hipStream_t st, F&& launch) {
   if (!c->profiling) return launch();
   if (c->pending.size() > 2048) fold_pending(c);
   hipEvent_t a = take_event(c), b = take_event(c);
   if (!a || !b) return launch();
-  (void)hipEventRecord(a, c->stream);
+  (void)hipEventRecord(a, st);
   hipError_t e = launch();
-  (void)hipEventRecord(b, c->stream);
+  (void)hipEventRecord(b, st);
   c->pending.push_back({kernel, a, b});
   return e;
 }
@@ -378,10 +398,25 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
   c->ws_bytes = bytes;
   c->stream = (hipStream_t)hip_stream;
   c->layers.resize(cfg->num_layers);
-  hipError_t e = launch_init_units(c->g, c->L, c->ws + kHeaderBytes, cfg->num_layers * cfg->batch,
+  hipError_t e = hipSuccess;
+  if (cfg->flags & QEVICT_FLAG_ASYNC_ROUTING) {
+    e = hipStreamCreateWithFlags(&c->rstream, hipStreamNonBlocking);   // default priority
+    c->attn_ev.assign(cfg->num_layers, nullptr);
+    c->route_ev.assign(cfg->num_layers, nullptr);
+    c->route_pending.assign(cfg->num_layers, 0);
+    for (int l = 0; l < cfg->num_layers && e == hipSuccess; ++l) {
+      e = hipEventCreateWithFlags(&c->attn_ev[l], hipEventDisableTiming);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&c->route_ev[l], hipEventDisableTiming);
+    }
+    if (e != hipSuccess) {
+      qevict_cache_destroy(c);
+      return hip_fail(e, "creating the routing stream");
+    }
+  }
+  if (e == hipSuccess) e = launch_init_units(c->g, c->L, c->ws + kHeaderBytes, cfg->num_layers * cfg->batch,
                                    c->stream);
   if (e != hipSuccess) {
-    delete c;
+    qevict_cache_destroy(c);
     return hip_fail(e, "initialising the cache");
   }
   *out = c;
@@ -390,6 +425,12 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
 
 qevict_status qevict_cache_destroy(qevict_cache* c) {
   if (!c) return QEVICT_OK;
+  if (c->rstream) (void)hipStreamSynchronize(c->rstream);
+  for (auto e : c->attn_ev)
+    if (e) (void)hipEventDestroy(e);
+  for (auto e : c->route_ev)
+    if (e) (void)hipEventDestroy(e);
+  if (c->rstream) (void)hipStreamDestroy(c->rstream);
   for (auto& t : c->pending) {
     (void)hipEventDestroy(t.start);
     (void)hipEventDestroy(t.stop);
@@ -431,10 +472,11 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
     e = launch_pack_tokens(pa, c->stream);            // tail: recent region and partial window
   }
   RetierArgs ra{gg, L, base, 1, 0, n_hist, init_scores, n_init};
-  if (e == hipSuccess) e = timed(c, 2, [&] { return launch_retier(ra, c->stream); });
+  if (e == hipSuccess) e = timed(c, 2, c->stream, [&] { return launch_retier(ra, c->stream); });
   MigrateArgs ma{gg, L, base, k, v, prompt_len};
-  if (e == hipSuccess) e = timed(c, 3, [&] { return launch_quantize(ma, g.K_q, c->stream); });
-  if (e == hipSuccess) e = timed(c, 4, [&] { return launch_promote(ma, g.K_f, c->stream); });
+  if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_quantize(ma, g.K_q, c->stream); });
+  if (e == hipSuccess) e = timed(c, 4, c->stream, [&] { return launch_promote(ma, g.K_f, c->stream); });
+  if (e == hipSuccess) e = mark_layer(c, layer);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   ls.T = prompt_len;
   ls.routed_end = n_hist;
@@ -475,8 +517,9 @@ qevict_status qevict_decode_attend(qevict_cache* c, int32_t layer, const uint16_
       e = hipMemsetAsync(unit_base(c, layer, b) + c->L.dbg_mass, 0, 4LL * g.H_q * (g.nwc + 1),
                          c->stream);
   }
-  if (e == hipSuccess) e = timed(c, 0, [&] { return launch_attend(a, c->stream); });
-  if (e == hipSuccess) e = timed(c, 1, [&] { return launch_merge(a, c->stream); });
+  if (e == hipSuccess) e = timed(c, 0, c->stream, [&] { return launch_attend(a, c->stream); });
+  if (e == hipSuccess) e = timed(c, 1, c->stream, [&] { return launch_merge(a, c->stream); });
+  if (e == hipSuccess) e = mark_layer(c, layer);
   if (e != hipSuccess) return hip_fail(e, "decode_attend launch");
   ls.T = T;
   return QEVICT_OK;
@@ -497,13 +540,22 @@ qevict_status qevict_retier(qevict_cache* c, int32_t layer, qevict_retier_stats*
   RetierArgs ra{gg, L, base, 0, a0, a1 > a0 ? a1 : a0, nullptr, 0};
   MigrateArgs ma{gg, L, base, nullptr, nullptr, 0};
   const int max_q = g.K_q < g.max_fq ? g.K_q : g.max_fq;
-  hipError_t e = timed(c, 2, [&] { return launch_retier(ra, c->stream); });
-  if (e == hipSuccess) e = timed(c, 3, [&] { return launch_quantize(ma, max_q, c->stream); });
-  if (e == hipSuccess) e = timed(c, 4, [&] { return launch_promote(ma, g.K_f, c->stream); });
+  // asynchronous routing: run on the routing stream after this layer's latest attention
+  hipStream_t rs = c->rstream ? c->rstream : c->stream;
+  hipError_t e = hipSuccess;
+  if (c->rstream) e = hipStreamWaitEvent(rs, c->attn_ev[layer], 0);
+  if (e == hipSuccess) e = timed(c, 2, rs, [&] { return launch_retier(ra, rs); });
+  if (e == hipSuccess) e = timed(c, 3, rs, [&] { return launch_quantize(ma, max_q, rs); });
+  if (e == hipSuccess) e = timed(c, 4, rs, [&] { return launch_promote(ma, g.K_f, rs); });
+  if (e == hipSuccess && c->rstream) {
+    e = hipEventRecord(c->route_ev[layer], rs);
+    if (e == hipSuccess) c->route_pending[layer] = 1;
+  }
   if (e != hipSuccess) return hip_fail(e, "retier launch");
   if (a1 > a0) ls.routed_end = a1;
   if (stats) {
     memset(stats, 0, sizeof *stats);
+    if ((e = join_layer(c, layer)) != hipSuccess) return hip_fail(e, "joining the routing stream");
     for (int b = 0; b < g.B; ++b) {
       int32_t st[ST_N];
       e = hipMemcpyAsync(st, unit_base(c, layer, b) + c->L.stats, sizeof st, hipMemcpyDeviceToHost,
@@ -574,6 +626,7 @@ static qevict_status manual_move(qevict_cache* c, int layer, int seq, int window
   e = launch_manual_move(ra, seq, window, to_quant, c->stream);
   if (e == hipSuccess) e = launch_quantize(ma, 1, c->stream);
   if (e == hipSuccess) e = launch_promote(ma, 1, c->stream);
+  if (e == hipSuccess) e = mark_layer(c, layer);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(e, "manual move");
   return device_errors(c, layer);
@@ -716,6 +769,7 @@ qevict_status qevict_debug_shift_keys(qevict_cache* c, int32_t layer, int32_t se
     if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
     if (e != hipSuccess) return hip_fail(e, "shift_keys write");
   }
+  if (hipError_t e2 = mark_layer(c, layer)) return hip_fail(e2, "shift_keys");
   return QEVICT_OK;
 }
 
@@ -753,6 +807,13 @@ qevict_status qevict_profile_read(qevict_cache* c, int32_t kernel, double* total
   fold_pending(c);
   if (total_ms) *total_ms = c->prof_ms[kernel];
   if (count) *count = c->prof_n[kernel];
+  return QEVICT_OK;
+}
+
+qevict_status qevict_join_routing(qevict_cache* c) {
+  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
+  for (int l = 0; l < c->cfg.num_layers; ++l)
+    if (hipError_t e = join_layer(c, l)) return hip_fail(e, "joining the routing stream");
   return QEVICT_OK;
 }
 

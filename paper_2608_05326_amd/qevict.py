@@ -23,7 +23,7 @@ TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED = 0, 1, 2, 3, 4
 LEDGER_NONE, LEDGER_ACTIVE, LEDGER_DORMANT = 0, 1, 2
 BITS_MIXED_4_2 = 42
 OUT_F32, OUT_BF16 = 0, 1
-FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES = 0x1, 0x2
+FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING = 0x1, 0x2, 0x4
 KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_QUANTIZE, KERNEL_PROMOTE = range(5)
 
 # exported symbols declared in include/qevict.h
@@ -31,7 +31,7 @@ SYMBOLS = (
     "qevict_workspace_size", "qevict_cache_init", "qevict_cache_destroy", "qevict_prefill_assign",
     "qevict_decode_attend", "qevict_retier", "qevict_quantize_window", "qevict_promote_window",
     "qevict_get_state", "qevict_export_window", "qevict_debug_shift_keys", "qevict_debug_masses",
-    "qevict_profile_enable", "qevict_profile_read", "qevict_last_attend_bytes",
+    "qevict_profile_enable", "qevict_profile_read", "qevict_last_attend_bytes", "qevict_join_routing",
     "qevict_status_string", "qevict_last_error",
 )
 
@@ -120,6 +120,7 @@ def load_library(path: str | None = None):
         "qevict_profile_enable": [vp, i32],
         "qevict_profile_read": [vp, i32, P(ctypes.c_double), P(i64)],
         "qevict_last_attend_bytes": [vp, i32, P(i64)],
+        "qevict_join_routing": [vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -212,6 +213,10 @@ class Cache:
             return s.as_dict()
         self._c(self.lib.qevict_retier(self.handle, layer, None))
         return None
+
+    def join_routing(self):
+        """Order the cache stream after all routing enqueued so far (async routing)."""
+        self._c(self.lib.qevict_join_routing(self.handle))
 
     def quantize_window(self, layer: int, seq: int, window: int):
         self._c(self.lib.qevict_quantize_window(self.handle, layer, seq, window))

@@ -273,3 +273,62 @@ def test_all_full_equals_plain_attention():
 def test_smoke_entry_point():
     import __graft_entry__
     __graft_entry__.smoke()
+
+
+# ---------------------------------------------------------------------------
+# asynchronous routing (routing stream + per-layer ordering)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["c2s", "c3s"])
+def test_async_routing_lockstep(name):
+    import paper_2608_05326_amd as qv
+    from tests.gpu_harness import Lockstep
+    ls = Lockstep(syn.get_workload(name), flags=qv.FLAG_ASYNC_ROUTING, steps=12)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+
+
+def test_async_routing_interleaved_layers_match_sync():
+    """Several layers stepped back to back with no host synchronisation: the
+    routing of each layer overlaps the attention of the others and every
+    output and final state equals the single-stream run bit for bit."""
+    import paper_2608_05326_amd as qv
+    from tests.gpu_harness import gpu_config, to_dev_bf16
+    torch = _torch()
+    wl = syn.get_workload("c2s")
+    n_layers, steps = 4, 10
+
+    def run(flags):
+        c = qv.Cache(gpu_config(wl, n_layers, flags))
+        outs = []
+        try:
+            for l in range(n_layers):
+                k, v = syn.prompt_kv(wl, 0, 0, l)
+                s = syn.init_scores(wl, 0, 0, l)
+                c.prefill_assign(l, to_dev_bf16(k[None]), to_dev_bf16(v[None]),
+                                 torch.from_numpy(s[None].copy()).cuda())
+            dec = [syn.decode_inputs(wl, 0, 0, l, steps) for l in range(n_layers)]
+            ins = [[tuple(to_dev_bf16(x[t][None]) for x in dec[l]) for t in range(steps)]
+                   for l in range(n_layers)]
+            for t in range(steps):
+                for l in range(n_layers):
+                    out = torch.empty((1, wl.num_q_heads, 128), dtype=torch.float32, device="cuda")
+                    c.decode_attend(l, *ins[l][t], out)
+                    c.retier(l)
+                    outs.append(out)
+            c.join_routing()
+            torch.cuda.synchronize()
+            states = [c.get_state(l, 0) for l in range(n_layers)]
+            return [o.cpu() for o in outs], states
+        finally:
+            c.close()
+
+    o_sync, s_sync = run(0)
+    o_async, s_async = run(qv.FLAG_ASYNC_ROUTING)
+    for a, b in zip(o_sync, o_async):
+        assert torch.equal(a, b)
+    for a, b in zip(s_sync, s_async):
+        for k in ("tiers", "scores", "ledger", "bits"):
+            assert np.array_equal(a[k], b[k]), k
