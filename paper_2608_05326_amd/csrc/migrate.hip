@@ -15,7 +15,7 @@
 
 namespace qv {
 
-__device__ bool quant_params(float lo, float hi, int nbits, uint16_t* zb, uint16_t* sb) {
+__device__ __forceinline__ bool quant_params(float lo, float hi, int nbits, uint16_t* zb, uint16_t* sb) {
   if (!(lo >= -65504.f && hi <= 65504.f)) return false;   // also rejects NaN
   const uint16_t zh = fp16_round_down(lo);
   const double z = fp16_bits_to_f64(zh);
@@ -31,34 +31,109 @@ __device__ bool quant_params(float lo, float hi, int nbits, uint16_t* zb, uint16
   return true;
 }
 
-// Round-half-even code of x: an fp32 estimate of (x - z) / s, then the exact
-// decision against the two neighbouring half-step boundaries z + (c +- 1/2) s
-// (exact in float64: fp16 operands, |c| <= 16).  No division per element.
-__device__ __forceinline__ int quant_code(float x, float zf, float inv_s, double z, double s,
-                                          int nmax) {
-  if (s == 0.0) return 0;
-  float c0 = rintf((x - zf) * inv_s);
-  c0 = fminf(fmaxf(c0, 0.f), (float)nmax);
-  int c = (int)c0;
-  const double xd = x;
-  for (int k = 0; k < 2; ++k) {
-    const double hi = z + ((double)c + 0.5) * s, lo = z + ((double)c - 0.5) * s;
-    if ((xd > hi || (xd == hi && (c & 1))) && c < nmax) {
-      ++c;
-    } else if ((xd < lo || (xd == lo && (c & 1))) && c > 0) {
-      --c;
-    } else {
-      break;
-    }
+// Parameters of one quantization group as the code pass uses them: fp16 zero
+// and scale widened to fp32 (exact), the fp32 reciprocal of the scale, and
+// whether every half-step boundary z + (k + 1/2) s (0 <= k <= n) is exactly
+// representable in fp32 (then the decision needs no float64).
+struct QParams {
+  float z, s, inv_s, exact32;
+};
+
+__device__ __forceinline__ double fp16_ulp(uint16_t h) {
+  const int e = (h >> 10) & 0x1F;
+  return __builtin_ldexp(1.0, (e > 1 ? e : 1) - 25);
+}
+
+__device__ __forceinline__ QParams group_params(float lo, float hi, int nbits, uint16_t* zb, uint16_t* sb,
+                                int32_t* counts) {
+  if (!quant_params(lo, hi, nbits, zb, sb)) set_error(counts, ERR_RANGE);
+  QParams p;
+  const double z = fp16_bits_to_f64(*zb), s = fp16_bits_to_f64(*sb);
+  p.z = (float)z;
+  p.s = (float)s;
+  p.inv_s = s > 0.0 ? 1.f / (float)s : 0.f;
+  // z and every k s / 2 are multiples of u; a boundary below 2^24 u in magnitude is exact
+  const double u = fmin(fp16_ulp(*zb), 0.5 * fp16_ulp(*sb));
+  const double span = fabs(z) + (double)(1 << nbits) * s;
+  p.exact32 = span < __builtin_ldexp(u, 24) ? 1.f : 0.f;
+  return p;
+}
+
+// Round-half-even code of x in the group: an fp32 estimate of (x - z) / s
+// (within one of the exact result), then the exact decision against the
+// neighbouring half-step boundaries, without branches.  The boundaries are
+// formed in fp32 when exact for the group, else in float64 where they always
+// are (fp16 operands, |c| <= 16).
+__device__ __forceinline__ uint32_t quant_code(float x, const QParams& p, int nmax) {
+  const float nm = (float)nmax;
+  float c = rintf((x - p.z) * p.inv_s);
+  c = fminf(fmaxf(c, 0.f), nm);
+  const bool odd = (((int)c) & 1) != 0;
+  bool up, dn;
+  if (p.exact32 != 0.f) {
+    const float hi = fmaf(c + 0.5f, p.s, p.z), lo = fmaf(c - 0.5f, p.s, p.z);
+    up = x > hi || (x == hi && odd);
+    dn = x < lo || (x == lo && odd);
+  } else {
+    const double xd = x, cd = c, z = p.z, s = p.s;
+    const double hi = z + (cd + 0.5) * s, lo = z + (cd - 0.5) * s;
+    up = xd > hi || (xd == hi && odd);
+    dn = xd < lo || (xd == lo && odd);
   }
-  return c;
+  c = (up && c < nm) ? c + 1.f : ((dn && c > 0.f) ? c - 1.f : c);
+  return p.s == 0.f ? 0u : (uint32_t)c;
+}
+
+// Codes of one (window, KV head), packed: thread (area, block m, lane L, word
+// comp) forms word 4m + comp of lane L; entry e of a word holds its 8 codes at
+// bits 16 o + NB (4 e' + i) for code j = 2i + o.  Consecutive threads write
+// consecutive words.
+constexpr int kMigrateThreads = 1024;
+
+template <int W, int NB>
+__device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk, const uint16_t* sv,
+                                           const QParams* pk, const QParams* pv, uint8_t* rec, int tid) {
+  constexpr int NBLK = W * NB / 64;
+  constexpr int PER = 4 / NB;
+  constexpr int NG = kHeadDim / W;
+  constexpr int nmax = (1 << NB) - 1;
+  for (int tk = tid; tk < 2 * NBLK * 256; tk += kMigrateThreads) {
+    const int comp = tk & 3, L = (tk >> 2) & 63, m = (tk >> 8) % NBLK;
+    const int area = tk / (NBLK * 256);   // uniform per wave
+    const int q = L >> 4, r = L & 15;
+    uint32_t wd = 0;
+#pragma unroll
+    for (int ee = 0; ee < PER; ++ee) {
+      const int ei = (m * 4 + comp) * PER + ee;
+      if (area == 0) {   // key entry (tb, kb): token 16 tb + r, channels 32 kb + 8 q + j
+        const int t = 16 * (ei >> 2) + r, c0 = 32 * (ei & 3) + 8 * q;
+        const u32x4 v = *(const u32x4*)(sk + t * kHeadDim + c0);
+        const uint32_t vw[4] = {v[0], v[1], v[2], v[3]};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float x = bf16_to_f32((uint16_t)(vw[j >> 1] >> (16 * (j & 1))));
+          wd |= quant_code(x, pk[c0 + j], nmax) << ((j & 1) * 16 + NB * (4 * ee + (j >> 1)));
+        }
+      } else {           // value entry (kt, cb): token tok(kt, q, j), channel 16 cb + r
+        const int kt = ei >> 3, c = 16 * (ei & 7) + r, vg = c / W;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int t = v_tok(kt, q, j);
+          const float x = bf16_to_f32(sv[t * kHeadDim + c]);
+          wd |= quant_code(x, pv[t * NG + vg], nmax) << ((j & 1) * 16 + NB * (4 * ee + (j >> 1)));
+        }
+      }
+    }
+    *(uint32_t*)(rec + area * G.qcodes_bytes + ((int64_t)m * 64 + L) * 16 + comp * 4) = wd;
+  }
 }
 
 // Load one KV head of a window into LDS in natural [t][c] layout.
-__device__ void load_window(const MigrateArgs& a, uint8_t* ub, int b, int g, int w, int src_kind,
+template <int W>
+__device__ __forceinline__ void load_window(const MigrateArgs& a, uint8_t* ub, int b, int g, int w, int src_kind,
                             int src_idx, uint16_t* sk, uint16_t* sv) {
   const Geometry& G = a.g;
-  const int W = G.W, tid = threadIdx.x;
+  const int tid = threadIdx.x;
   if (src_kind == SRC_PROMPT) {
     const int64_t row0 = ((int64_t)b * G.H_kv + g) * a.src_T + G.sink + (int64_t)w * W;
     const u32x4* k4 = (const u32x4*)(a.src_k + row0 * kHeadDim);
@@ -73,14 +148,16 @@ __device__ void load_window(const MigrateArgs& a, uint8_t* ub, int b, int g, int
     const uint8_t* pv = p + (int64_t)W * kHeadDim * 2;
     // K chunk (tb, kb), lane 16q + r: token 16 tb + r, channels 32 kb + 8 q .. + 7
     // V chunk (kt, cb), lane 16q + r: tokens tok(kt, q, 0..7), channel 16 cb + r
-    for (int i = tid; i < W * kHeadDim / 8; i += blockDim.x) {
+#pragma unroll
+    for (int i0 = 0; i0 < W * kHeadDim / 8; i0 += kMigrateThreads) {
+      const int i = i0 + tid;
+      if (W * kHeadDim / 8 < kMigrateThreads && i >= W * kHeadDim / 8) break;
       const int chunk = i >> 6, L = i & 63, q = L >> 4, r = L & 15;
       const u32x4 kx = *(const u32x4*)(p + (int64_t)i * 16);
       const u32x4 vx = *(const u32x4*)(pv + (int64_t)i * 16);
       *(u32x4*)(sk + (16 * (chunk >> 2) + r) * kHeadDim + 32 * (chunk & 3) + 8 * q) = kx;
       const int kt = chunk >> 3, c = 16 * (chunk & 7) + r;
-      const uint32_t v0 = vx[0], v1 = vx[1], v2 = vx[2], v3 = vx[3];
-      const uint32_t vw[4] = {v0, v1, v2, v3};
+      const uint32_t vw[4] = {vx[0], vx[1], vx[2], vx[3]};
 #pragma unroll
       for (int j = 0; j < 8; ++j)
         sv[v_tok(kt, q, j) * kHeadDim + c] = (uint16_t)(vw[j >> 1] >> (16 * (j & 1)));
@@ -88,106 +165,81 @@ __device__ void load_window(const MigrateArgs& a, uint8_t* ub, int b, int g, int
   }
 }
 
-__global__ __launch_bounds__(256) void k_quantize(MigrateArgs a) {
+// One (window, KV head) task per workgroup pass: (1) the window into LDS,
+// (2) one thread per group: min / max, scale and zero (written to the record),
+// (3) one thread per (code block, lane): the codes of its entries straight into
+// the packed 16-byte block (entry e's 8 codes at bits 16 o + b (4 e' + i)).
+// Keys form groups per channel (W tokens), values per token (G = W channels).
+template <int W>
+__global__ __launch_bounds__(kMigrateThreads) void k_quantize(MigrateArgs a) {
   const Geometry& G = a.g;
+  constexpr int NG = kHeadDim / W;             // value groups per token
   const int b = blockIdx.y, tid = threadIdx.x;
-  __shared__ __attribute__((aligned(16))) uint16_t sk[64 * kHeadDim];
-  __shared__ __attribute__((aligned(16))) uint16_t sv[64 * kHeadDim];
-  __shared__ uint8_t ck[64 * kHeadDim];
-  __shared__ uint8_t cv[64 * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t sk[W * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t sv[W * kHeadDim];
+  __shared__ QParams pk[kHeadDim];
+  __shared__ QParams pv[W * NG];
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
   int32_t* counts = (int32_t*)(ub + a.L.counts);
   const int32_t* qlist = (const int32_t*)(ub + a.L.qlist);
   const int n = counts[CNT_QUANT];
-  const int W = G.W;
   for (int task = blockIdx.x; task < n * G.H_kv; task += gridDim.x) {
     const int e = task / G.H_kv, g = task % G.H_kv;
     const int32_t* ent = qlist + e * kQEntry;
     const int w = ent[0], src_kind = ent[1], src_idx = ent[2], dst = ent[3], nb = ent[4];
-    load_window(a, ub, b, g, w, src_kind, src_idx, sk, sv);
+    load_window<W>(a, ub, b, g, w, src_kind, src_idx, sk, sv);
     __syncthreads();
     uint8_t* rec = ub + a.L.qpool + (int64_t)dst * G.qslot_bytes + g * G.qrec_bytes;
-    const int nmax = (1 << nb) - 1;
-    if (tid < kHeadDim) {
-      // key group: channel tid across the window's tokens
-      const int c = tid;
-      float lo = INFINITY, hi = -INFINITY;
-      for (int t = 0; t < W; ++t) {
-        const float x = bf16_to_f32(sk[t * kHeadDim + c]);
-        lo = fminf(lo, x);
-        hi = fmaxf(hi, x);
+    // ---- group parameters: threads 0..127 key channels, then value groups ----
+    for (int grp = tid; grp < kHeadDim + W * NG; grp += blockDim.x) {
+      float x[W];
+      if (grp < kHeadDim) {
+#pragma unroll
+        for (int t = 0; t < W; ++t) x[t] = bf16_to_f32(sk[t * kHeadDim + grp]);
+      } else {
+        const int gi = grp - kHeadDim, t = gi / NG, vg = gi % NG;
+        const u32x4* row = (const u32x4*)(sv + t * kHeadDim + vg * W);
+#pragma unroll
+        for (int k = 0; k < W / 8; ++k) {
+          const u32x4 v = row[k];
+          const uint32_t vw[4] = {v[0], v[1], v[2], v[3]};
+#pragma unroll
+          for (int i = 0; i < 8; ++i) x[8 * k + i] = bf16_to_f32((uint16_t)(vw[i >> 1] >> (16 * (i & 1))));
+        }
+      }
+      float lo = x[0], hi = x[0];
+#pragma unroll
+      for (int t = 1; t < W; ++t) {
+        lo = fminf(lo, x[t]);
+        hi = fmaxf(hi, x[t]);
       }
       uint16_t zb = 0, sb = 0;
-      if (!quant_params(lo, hi, nb, &zb, &sb)) set_error(counts, ERR_RANGE);
-      const double z = fp16_bits_to_f64(zb), s = fp16_bits_to_f64(sb);
-      const float zf = (float)z, inv_s = s > 0.0 ? 1.f / (float)s : 0.f;
-      for (int t = 0; t < W; ++t)
-        ck[t * kHeadDim + c] =
-            (uint8_t)quant_code(bf16_to_f32(sk[t * kHeadDim + c]), zf, inv_s, z, s, nmax);
-      uint16_t* mk = (uint16_t*)(rec + meta_k_off(G));
-      mk[c] = sb;
-      mk[kHeadDim + c] = zb;
-    } else {
-      // value groups: token t, channels vg*G .. vg*G + G - 1
-      const int ng = kHeadDim / G.G;
-      for (int idx = tid - kHeadDim; idx < W * ng; idx += blockDim.x - kHeadDim) {
-        const int t = idx / ng, vg = idx % ng;
-        const uint16_t* row = sv + t * kHeadDim + vg * G.G;
-        float lo = INFINITY, hi = -INFINITY;
-        for (int i = 0; i < G.G; ++i) {
-          const float x = bf16_to_f32(row[i]);
-          lo = fminf(lo, x);
-          hi = fmaxf(hi, x);
-        }
-        uint16_t zb = 0, sb = 0;
-        if (!quant_params(lo, hi, nb, &zb, &sb)) set_error(counts, ERR_RANGE);
-        const double z = fp16_bits_to_f64(zb), s = fp16_bits_to_f64(sb);
-        const float zf = (float)z, inv_s = s > 0.0 ? 1.f / (float)s : 0.f;
-        for (int i = 0; i < G.G; ++i)
-          cv[t * kHeadDim + vg * G.G + i] =
-              (uint8_t)quant_code(bf16_to_f32(row[i]), zf, inv_s, z, s, nmax);
+      const QParams p = group_params(lo, hi, nb, &zb, &sb, counts);
+      if (grp < kHeadDim) {
+        pk[grp] = p;
+        uint16_t* mk = (uint16_t*)(rec + meta_k_off(G));
+        mk[grp] = sb;
+        mk[kHeadDim + grp] = zb;
+      } else {
+        const int gi = grp - kHeadDim, t = gi / NG, vg = gi % NG;
+        pv[gi] = p;
         uint16_t* mv = (uint16_t*)(rec + meta_v_elem(G, t, vg));
         mv[0] = sb;
         mv[8] = zb;
       }
     }
     __syncthreads();
-    // pack: thread (area, block m, lane L) writes the 16-byte block of words 4m .. 4m + 3 of
-    // lane L; word wd holds entries wd * per + ee (per = 4 / nb), 8 codes each
-    const int nblk = W * nb / 64;
-    const int per = 4 / nb;
-    for (int tk = tid; tk < 2 * nblk * 64; tk += blockDim.x) {
-      const int area = tk / (nblk * 64), m = (tk >> 6) % nblk, L = tk & 63;
-      const int q = L >> 4, r = L & 15;
-      uint32_t wv[4];
-#pragma unroll
-      for (int comp = 0; comp < 4; ++comp) {
-        uint32_t wd = 0;
-        for (int ee = 0; ee < per; ++ee) {
-          const int ei = (m * 4 + comp) * per + ee;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int sh = (j & 1) * 16 + nb * (4 * ee + (j >> 1));
-            uint32_t code;
-            if (area == 0)   // key entry (tb, kb): token 16 tb + r, channel 32 kb + 8 q + j
-              code = ck[(16 * (ei >> 2) + r) * kHeadDim + 32 * (ei & 3) + 8 * q + j];
-            else             // value entry (kt, cb): token tok(kt, q, j), channel 16 cb + r
-              code = cv[v_tok(ei >> 3, q, j) * kHeadDim + 16 * (ei & 7) + r];
-            wd |= code << sh;
-          }
-        }
-        wv[comp] = wd;
-      }
-      *(u32x4*)(rec + area * G.qcodes_bytes + ((int64_t)m * 64 + L) * 16) =
-          (u32x4){wv[0], wv[1], wv[2], wv[3]};
-    }
+    // ---- codes, packed ----
+    if (nb == 4) pack_codes<W, 4>(G, sk, sv, pk, pv, rec, tid);
+    else pack_codes<W, 2>(G, sk, sv, pk, pv, rec, tid);
     __syncthreads();
   }
 }
 
 // 8 bf16 values z_j + s_j c_j (exact in float64, one rounding) packed for a 16-byte store
-__device__ __forceinline__ u32x4 dequant8(uint32_t wd, int shift0, int nb, u32x4 s8, u32x4 z8) {
-  const uint32_t mask = (1u << nb) - 1u;
+template <int NB>
+__device__ __forceinline__ u32x4 dequant8(uint32_t wd, int ee, u32x4 s8, u32x4 z8) {
+  constexpr uint32_t mask = (1u << NB) - 1u;
   const uint32_t sw[4] = {s8[0], s8[1], s8[2], s8[3]};
   const uint32_t zw[4] = {z8[0], z8[1], z8[2], z8[3]};
   uint32_t outw[4];
@@ -196,26 +248,57 @@ __device__ __forceinline__ u32x4 dequant8(uint32_t wd, int shift0, int nb, u32x4
     uint32_t pair = 0;
 #pragma unroll
     for (int o = 0; o < 2; ++o) {
-      const int j = 2 * i + o;
-      const uint32_t code = (wd >> (o * 16 + shift0 + nb * i)) & mask;
+      const uint32_t code = (wd >> (o * 16 + NB * (4 * ee + i))) & mask;
       const double sj = fp16_bits_to_f64((uint16_t)(sw[i] >> (16 * o)));
       const double zj = fp16_bits_to_f64((uint16_t)(zw[i] >> (16 * o)));
       pair |= (uint32_t)f64_to_bf16_rne(zj + sj * (double)code) << (16 * o);
-      (void)j;
     }
     outw[i] = pair;
   }
   return (u32x4){outw[0], outw[1], outw[2], outw[3]};
 }
 
-__global__ __launch_bounds__(256) void k_promote(MigrateArgs a) {
+// Promotion of one (window, KV head) from its quantized record: thread (area,
+// entry e, lane L) loads the 32-bit code word holding entry e of lane L and the
+// entry's 8 scales and zeros, and writes its 8 bf16 values to the same
+// (entry, lane) position of the bf16 slot.
+template <int W, int NB>
+__device__ __forceinline__ void promote_from_record(const Geometry& G, const uint8_t* rec,
+                                                    uint8_t* dp, int tid) {
+  constexpr int E = W / 4;                          // entries per area
+  constexpr int PER = 4 / NB;
+  const int ng = kHeadDim / G.G;
+  for (int tk = tid; tk < 2 * E * 64; tk += kMigrateThreads) {
+    const int L = tk & 63, ei = (tk >> 6) % E, area = tk / (E * 64);   // area uniform per wave
+    const int q = L >> 4, r = L & 15;
+    const int word = ei / PER;
+    const uint32_t wd = *(const uint32_t*)(rec + area * G.qcodes_bytes +
+                                           ((int64_t)(word >> 2) * 64 + L) * 16 + (word & 3) * 4);
+    const uint8_t* ps;
+    u32x4 s8, z8;
+    if (area == 0) {   // key entry (tb, kb): channels 32 kb + 8 q .. + 7
+      ps = rec + meta_k_off(G) + 2 * (32 * (ei & 3) + 8 * q);
+      s8 = *(const u32x4*)ps;
+      z8 = *(const u32x4*)(ps + 2 * kHeadDim);
+    } else {           // value entry (kt, cb): tokens tok(kt, q, 0..7), channel 16 cb + r
+      const int c = 16 * (ei & 7) + r;
+      ps = rec + meta_v_off(G) + (((ei >> 3) * 4 + q) * ng + c / G.G) * 32;
+      s8 = *(const u32x4*)ps;
+      z8 = *(const u32x4*)(ps + 16);
+    }
+    const int64_t off = (area == 0 ? 0 : (int64_t)W * kHeadDim * 2) + ((int64_t)ei * 64 + L) * 16;
+    *(u32x4*)(dp + off) = dequant8<NB>(wd, ei % PER, s8, z8);
+  }
+}
+
+template <int W>
+__global__ __launch_bounds__(kMigrateThreads) void k_promote(MigrateArgs a) {
   const Geometry& G = a.g;
   const int b = blockIdx.y, tid = threadIdx.x;
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
   int32_t* counts = (int32_t*)(ub + a.L.counts);
   const int32_t* plist = (const int32_t*)(ub + a.L.plist);
   const int n = counts[CNT_PROMOTE];
-  const int W = G.W;
   for (int task = blockIdx.x; task < n * G.H_kv; task += gridDim.x) {
     const int e = task / G.H_kv, g = task % G.H_kv;
     const int32_t* ent = plist + e * kQEntry;
@@ -237,39 +320,10 @@ __global__ __launch_bounds__(256) void k_promote(MigrateArgs a) {
         const int t = i >> 7, c = i & 127;
         *(uint16_t*)(dp + v_elem_off(W, t, c)) = vs[t * kHeadDim + c];
       }
-    } else {
-      // SRC_QSLOT: thread (area, block m, lane L) expands the entries held by the 16-byte
-      // code block m of lane L straight into the bf16 chunks at the same (entry, lane)
+    } else {   // SRC_QSLOT
       const uint8_t* rec = ub + a.L.qpool + (int64_t)src_idx * G.qslot_bytes + g * G.qrec_bytes;
-      const int nblk = W * nb / 64;
-      const int per = 4 / nb;
-      const int ng = kHeadDim / G.G;
-      for (int tk = tid; tk < 2 * nblk * 64; tk += blockDim.x) {
-        const int area = tk / (nblk * 64), m = (tk >> 6) % nblk, L = tk & 63;
-        const int q = L >> 4, r = L & 15;
-        const u32x4 blk = *(const u32x4*)(rec + area * G.qcodes_bytes + ((int64_t)m * 64 + L) * 16);
-        const uint32_t bw[4] = {blk[0], blk[1], blk[2], blk[3]};
-        for (int comp = 0; comp < 4; ++comp) {
-          for (int ee = 0; ee < per; ++ee) {
-            const int ei = (m * 4 + comp) * per + ee;
-            u32x4 s8, z8;
-            int64_t off;
-            if (area == 0) {   // key entry (tb, kb): channels 32 kb + 8 q .. + 7 of token 16 tb + r
-              const int c0 = 32 * (ei & 3) + 8 * q;
-              s8 = *(const u32x4*)(rec + meta_k_off(G) + 2 * c0);
-              z8 = *(const u32x4*)(rec + meta_k_off(G) + 2 * kHeadDim + 2 * c0);
-              off = ((int64_t)ei * 64 + L) * 16;
-            } else {           // value entry (kt, cb): tokens tok(kt, q, 0..7) of channel 16 cb + r
-              const int kt = ei >> 3, c = 16 * (ei & 7) + r;
-              const uint8_t* pm = rec + meta_v_off(G) + ((kt * 4 + q) * ng + c / G.G) * 32;
-              s8 = *(const u32x4*)pm;
-              z8 = *(const u32x4*)(pm + 16);
-              off = (int64_t)W * kHeadDim * 2 + ((int64_t)ei * 64 + L) * 16;
-            }
-            *(u32x4*)(dp + off) = dequant8(bw[comp], 4 * nb * ee, nb, s8, z8);
-          }
-        }
-      }
+      if (nb == 4) promote_from_record<W, 4>(G, rec, dp, tid);
+      else promote_from_record<W, 2>(G, rec, dp, tid);
     }
   }
 }
@@ -304,11 +358,15 @@ static int migrate_blocks(const Geometry& g, int max_entries) {
 }
 
 hipError_t launch_quantize(const MigrateArgs& a, int max_entries, hipStream_t st) {
-  hipLaunchKernelGGL(k_quantize, dim3(migrate_blocks(a.g, max_entries), a.g.B), dim3(256), 0, st, a);
+  const dim3 grid(migrate_blocks(a.g, max_entries), a.g.B);
+  if (a.g.W == 32) hipLaunchKernelGGL(k_quantize<32>, grid, dim3(kMigrateThreads), 0, st, a);
+  else hipLaunchKernelGGL(k_quantize<64>, grid, dim3(kMigrateThreads), 0, st, a);
   return hipGetLastError();
 }
 hipError_t launch_promote(const MigrateArgs& a, int max_entries, hipStream_t st) {
-  hipLaunchKernelGGL(k_promote, dim3(migrate_blocks(a.g, max_entries), a.g.B), dim3(256), 0, st, a);
+  const dim3 grid(migrate_blocks(a.g, max_entries), a.g.B);
+  if (a.g.W == 32) hipLaunchKernelGGL(k_promote<32>, grid, dim3(kMigrateThreads), 0, st, a);
+  else hipLaunchKernelGGL(k_promote<64>, grid, dim3(kMigrateThreads), 0, st, a);
   return hipGetLastError();
 }
 hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st) {
