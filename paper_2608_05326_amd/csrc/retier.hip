@@ -83,6 +83,43 @@ __device__ void block_scan_multi(int32_t* const (&buf)[NV], const int (&n)[NV], 
   __syncthreads();
 }
 
+// Exclusive prefix counts of NV flag arrays held in registers in strided
+// layout (element c = tid + k * kRetierThreads, k < PER): rank[v][k] = set flags
+// before element c, tot[v] = set flags in all.  Wave ballots, then one wave per
+// array scans the 64 (slice, wave) counts; two barriers.
+template <int NV>
+__device__ __forceinline__ void flag_scan(const bool (&f)[NV][kMaxCand / kRetierThreads],
+                                          int (&rank)[NV][kMaxCand / kRetierThreads], int (&tot)[NV],
+                                          int32_t* tmp /* >= NV * 64 + NV */) {
+  constexpr int PER = kMaxCand / kRetierThreads;
+  constexpr int NW = kRetierThreads / 64;
+  static_assert(PER * NW == 64, "one wave scans the slice counts");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const uint64_t bl = __builtin_amdgcn_ballot_w64(f[v][k]);
+      rank[v][k] = __popcll(bl & below);
+      if (lane == 0) tmp[v * 64 + k * NW + wave] = __popcll(bl);
+    }
+  __syncthreads();
+  if (wave < NV) {
+    const int x = tmp[wave * 64 + lane];
+    const int inc = wave_inclusive_scan(x);
+    tmp[wave * 64 + lane] = inc - x;
+    if (lane == 63) tmp[NV * 64 + wave] = inc;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) rank[v][k] += tmp[v * 64 + k * NW + wave];
+    tot[v] = tmp[NV * 64 + v];
+  }
+}
+
 // Value of `x` held by lane (lane ^ J), J in {1, 2, 4, 8, 16, 32}; VALU only.
 template <int J>
 __device__ __forceinline__ uint32_t lane_xor(uint32_t x, int lane) {
@@ -139,6 +176,8 @@ __device__ __forceinline__ void reg_stage(uint64_t (&key)[KP], int k, int lane) 
 template <int KP>
 __device__ void bitonic_sort(uint64_t (&key)[KP], int n_pow, uint64_t* lds) {
   const int t = threadIdx.x, lane = t & 63;
+  // with one key per thread only the waves holding positions < n_pow take part
+  const bool act = KP > 1 || (t >> 6) < ((n_pow + 63) >> 6);
   for (int k = 2; k <= n_pow; k <<= 1) {
     for (int j = k >> 1; j >= 64; j >>= 1) {
       if (j >= kRetierThreads) {
@@ -155,21 +194,27 @@ __device__ void bitonic_sort(uint64_t (&key)[KP], int n_pow, uint64_t* lds) {
         }
       } else {
         uint64_t other[KP];
+        if (act) {
 #pragma unroll
-        for (int m = 0; m < KP; ++m) lds[t + m * kRetierThreads] = key[m];
+          for (int m = 0; m < KP; ++m) lds[t + m * kRetierThreads] = key[m];
+        }
         __syncthreads();
+        if (act) {
 #pragma unroll
-        for (int m = 0; m < KP; ++m) other[m] = lds[(t + m * kRetierThreads) ^ j];
+          for (int m = 0; m < KP; ++m) other[m] = lds[(t + m * kRetierThreads) ^ j];
+        }
         __syncthreads();
-        cmpx_stage<KP>(key, other, k, j);
+        if (act) cmpx_stage<KP>(key, other, k, j);
       }
     }
-    if (k > 32) reg_stage<32, KP>(key, k, lane);
-    if (k > 16) reg_stage<16, KP>(key, k, lane);
-    if (k > 8) reg_stage<8, KP>(key, k, lane);
-    if (k > 4) reg_stage<4, KP>(key, k, lane);
-    if (k > 2) reg_stage<2, KP>(key, k, lane);
-    reg_stage<1, KP>(key, k, lane);
+    if (act) {
+      if (k > 32) reg_stage<32, KP>(key, k, lane);
+      if (k > 16) reg_stage<16, KP>(key, k, lane);
+      if (k > 8) reg_stage<8, KP>(key, k, lane);
+      if (k > 4) reg_stage<4, KP>(key, k, lane);
+      if (k > 2) reg_stage<2, KP>(key, k, lane);
+      reg_stage<1, KP>(key, k, lane);
+    }
   }
 }
 
@@ -188,6 +233,76 @@ __device__ void sort_candidates(uint64_t* skey, int n_cand, int n_pow) {
   __syncthreads();
 }
 
+// Exchange-compare within a wave (lane index as position, J < 64).
+template <int J>
+__device__ __forceinline__ uint64_t wave_cmpx(uint64_t x, int k, int lane) {
+  const uint32_t lo = lane_xor<J>((uint32_t)x, lane);
+  const uint32_t hi = lane_xor<J>((uint32_t)(x >> 32), lane);
+  const uint64_t y = ((uint64_t)hi << 32) | lo;
+  const bool up = (lane & k) == 0, lower = (lane & J) == 0;
+  return (up == lower) ? (x < y ? x : y) : (x < y ? y : x);
+}
+
+// Ascending bitonic sort of one key per lane across a wave (lane exchanges only).
+__device__ __forceinline__ uint64_t wave_sort64(uint64_t x, int lane) {
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1) {
+    if (k >= 64) x = wave_cmpx<32>(x, k, lane);
+    if (k >= 32) x = wave_cmpx<16>(x, k, lane);
+    if (k >= 16) x = wave_cmpx<8>(x, k, lane);
+    if (k >= 8) x = wave_cmpx<4>(x, k, lane);
+    if (k >= 4) x = wave_cmpx<2>(x, k, lane);
+    x = wave_cmpx<1>(x, k, lane);
+  }
+  return x;
+}
+
+// Sort of up to kRetierThreads unique keys: every wave sorts its run of 64 in
+// registers, then a key's final position is its lane in its run plus, for each
+// other run, the number of that run's keys below it (binary searches in LDS
+// that advance together, NR = run count rounded up to a power of two).
+template <int NR>
+__device__ __forceinline__ int rank_in_runs(const uint64_t* skey, uint64_t x, int wave, int n_runs) {
+  int lo[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) lo[r] = 0;
+#pragma unroll
+  for (int step = 64; step >= 1; step >>= 1) {
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const int idx = lo[r] + step - 1;
+      const uint64_t v = skey[64 * r + (idx < 64 ? idx : 63)];
+      lo[r] += (r < n_runs && r != wave && idx < 64 && v < x) ? step : 0;
+    }
+  }
+  int rank = 0;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) rank += lo[r];
+  return rank;
+}
+
+__device__ void sort_runs(uint64_t* skey, int n_cand) {
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int n_runs = (n_cand + 63) >> 6;
+  uint64_t x = t < n_cand ? skey[t] : ~0ull;
+  __syncthreads();
+  if (wave < n_runs) {
+    x = wave_sort64(x, lane);
+    skey[t] = x;
+  }
+  __syncthreads();
+  int rank = lane;
+  if (wave < n_runs) {
+    if (n_runs <= 2) rank += rank_in_runs<2>(skey, x, wave, n_runs);
+    else if (n_runs <= 4) rank += rank_in_runs<4>(skey, x, wave, n_runs);
+    else if (n_runs <= 8) rank += rank_in_runs<8>(skey, x, wave, n_runs);
+    else rank += rank_in_runs<16>(skey, x, wave, n_runs);
+  }
+  __syncthreads();
+  if (wave < n_runs && x != ~0ull) skey[rank] = x;
+  __syncthreads();
+}
+
 __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   const Geometry& G = a.g;
   const int b = blockIdx.x, tid = threadIdx.x;
@@ -197,12 +312,10 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   __shared__ uint64_t skey[kMaxCand];
   __shared__ int32_t sinfo[kMaxCand];
   __shared__ int32_t sa[kMaxCand];
-  __shared__ int32_t sd[kMaxCand];
   __shared__ int32_t sown[2 * kMaxCand];      // slot owners: Full slots, then quantized slots
-  __shared__ int32_t tmp[64];
+  __shared__ int32_t tmp[4 * 64 + 16];
   __shared__ int32_t sstat[ST_N];
   int32_t* sb = (int32_t*)skey;               // after the sort: two more int arrays
-  int32_t* sc = (int32_t*)skey + kMaxCand;
   int32_t* fown = sown;
   int32_t* qown = sown + G.K_f;
 
@@ -226,6 +339,27 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   int32_t* stats = (int32_t*)(ub + a.L.stats);
 
   if (tid < ST_N) sstat[tid] = 0;
+  // ---- one round of loads: the live list carries every candidate's state.
+  // Entries are read up to the list's capacity without waiting for its length.
+  int spec_ref[PER], spec_aux[PER], spec_win[PER];
+  float spec_sc[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    const bool ok = !a.prefill && c < G.max_fq;
+    spec_ref[k] = ok ? iref[c] : 0;
+    spec_aux[k] = ok ? iaux[c] : -1;
+    spec_win[k] = ok ? iwin[c] : -1;
+    spec_sc[k] = ok ? iscore[c] : 0.f;
+  }
+  // scores of the windows that follow the routed range (the next steps' recent
+  // region; at most NR of them have started)
+  float ring_sc = 0.f;
+  if (tid < G.NR) {
+    const int w = a.aged_w1 + tid;
+    if (a.prefill) ring_sc = w < a.n_init ? a.init_scores[(int64_t)b * a.n_init + w] : 0.f;
+    else ring_sc = w < G.nwc ? score[w] : 0.f;
+  }
   const int n_fq = a.prefill ? 0 : counts[CNT_ITEMS];
   const int n_aged = a.aged_w1 - a.aged_w0;
   const int n_cand = n_fq + n_aged;
@@ -234,7 +368,6 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     return;
   }
 
-  // ---- one round of loads: the live list carries every candidate's state ----
   int my_w[PER], my_old[PER], my_led[PER], my_fs[PER], my_qs[PER], my_bits[PER];
   float my_sc[PER];
 #pragma unroll
@@ -243,10 +376,10 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     my_w[k] = -1;
     if (c >= n_cand) continue;
     if (c < n_fq) {
-      const int32_t ref = iref[c], aux = iaux[c];
+      const int32_t ref = spec_ref[k], aux = spec_aux[k];
       const int kind = ref >> 28, slot = ref & 0x0FFFFFFF;
-      my_w[k] = iwin[c];
-      my_sc[k] = iscore[c];
+      my_w[k] = spec_win[k];
+      my_sc[k] = spec_sc[k];
       if (kind == KIND_BF16) {
         my_old[k] = T_FULL;
         my_fs[k] = slot;
@@ -293,7 +426,8 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   __syncthreads();
 
   // ---- sort ----
-  if (n_pow <= NT) sort_candidates<1>(skey, n_cand, n_pow);
+  if (n_cand <= NT) sort_runs(skey, n_cand);
+  else if (n_pow <= NT) sort_candidates<1>(skey, n_cand, n_pow);
   else if (n_pow <= 2 * NT) sort_candidates<2>(skey, n_cand, n_pow);
   else sort_candidates<4>(skey, n_cand, n_pow);
 
@@ -371,40 +505,37 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   }
   __syncthreads();
 
-  // ---- free lists and request ranks: four prefix sums in one pass ----
-  for (int i = tid; i < G.K_f; i += NT) sa[i] = fown[i] < 0 ? 1 : 0;
-  for (int i = tid; i < G.n_qslots; i += NT) sd[i] = qown[i] < 0 ? 1 : 0;
+  // ---- free lists and request ranks: four flag prefix counts in one pass ----
+  int my_rankF[PER], my_rankQ[PER];
+  int nfreeF, nfreeQ, nreqF, nreqQ;
+  {
+    bool fl[4][PER];
+    int rk[4][PER], tots[4];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int c = tid + k * NT;
-    if (c < n_cand) {
-      sb[c] = my_req[k] & 1;
-      sc[c] = (my_req[k] >> 1) & 1;
+    for (int k = 0; k < PER; ++k) {
+      const int i = tid + k * NT;
+      fl[0][k] = i < G.K_f && fown[i] < 0;
+      fl[1][k] = i < G.n_qslots && qown[i] < 0;
+      fl[2][k] = (my_req[k] & 1) != 0;
+      fl[3][k] = (my_req[k] & 2) != 0;
+    }
+    flag_scan<4>(fl, rk, tots, tmp);
+    nfreeF = tots[0];
+    nfreeQ = tots[1];
+    nreqF = tots[2];
+    nreqQ = tots[3];
+    // free slot lists, ascending slot order (sinfo / sb are free now)
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = tid + k * NT;
+      if (fl[0][k]) sinfo[rk[0][k]] = i;
+      if (fl[1][k]) sb[rk[1][k]] = i;
+      my_rankF[k] = rk[2][k];
+      my_rankQ[k] = rk[3][k];
     }
   }
-  __syncthreads();
-  int tots[4];
-  {
-    int32_t* const bufs[4] = {sa, sd, sb, sc};
-    const int ns[4] = {G.K_f, G.n_qslots, n_cand, n_cand};
-    block_scan_multi<4>(bufs, ns, tots, tmp);
-  }
-  const int nfreeF = tots[0], nfreeQ = tots[1], nreqF = tots[2], nreqQ = tots[3];
-  int my_rankF[PER], my_rankQ[PER];
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int c = tid + k * NT;
-    my_rankF[k] = c < n_cand ? sb[c] : 0;
-    my_rankQ[k] = c < n_cand ? sc[c] : 0;
-  }
-  // free slot lists, ascending slot order (sinfo / sb are free now)
   int32_t* freeF = sinfo;
   int32_t* freeQ = sb;
-  __syncthreads();
-  for (int i = tid; i < G.K_f; i += NT)
-    if (fown[i] < 0) freeF[sa[i]] = i;
-  for (int i = tid; i < G.n_qslots; i += NT)
-    if (qown[i] < 0) freeQ[sd[i]] = i;
   __syncthreads();
 
   // ---- apply: new slots, ledger states, work lists ----
@@ -481,55 +612,40 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   for (int i = tid; i < G.n_qslots; i += NT) qowner[i] = qown[i];
 
   // ---- rebuild the live list (window order) with its cost prefix ----
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int c = tid + k * NT;
-    if (c < n_cand) {
-      const bool live = my_nt[k] == T_FULL || my_nt[k] == T_QUANT;
-      sa[c] = live ? 1 : 0;
-      const int kind = my_nt[k] == T_FULL ? KIND_BF16 : (my_bits[k] == 4 ? KIND_Q4 : KIND_Q2);
-      sd[c] = live ? item_cost(G, kind) : 0;
-    }
-  }
-  __syncthreads();
-  int tots2[2];
+  int n_items;
   {
-    int32_t* const bufs[2] = {sa, sd};
-    const int ns[2] = {n_cand, n_cand};
-    block_scan_multi<2>(bufs, ns, tots2, tmp);
-  }
-  const int n_items = tots2[0];
+    bool fl[3][PER];
+    int rk[3][PER], tots[3];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int c = tid + k * NT;
-    if (c < n_cand && (my_nt[k] == T_FULL || my_nt[k] == T_QUANT)) {
-      const int pos = sa[c];
-      int kind, slot;
-      if (my_nt[k] == T_FULL) {
-        kind = KIND_BF16;
-        slot = my_fs[k];
-        atomicAdd(&sstat[ST_NF], 1);
-      } else {
-        kind = my_bits[k] == 4 ? KIND_Q4 : KIND_Q2;
-        slot = my_qs[k];
-        atomicAdd(&sstat[kind == KIND_Q4 ? ST_NQ4 : ST_NQ2], 1);
-      }
+    for (int k = 0; k < PER; ++k) {
+      const int c = tid + k * NT;
+      const bool in = c < n_cand;
+      fl[0][k] = in && my_nt[k] == T_FULL;
+      fl[1][k] = in && my_nt[k] == T_QUANT && my_bits[k] == 4;
+      fl[2][k] = in && my_nt[k] == T_QUANT && my_bits[k] != 4;
+    }
+    flag_scan<3>(fl, rk, tots, tmp);
+    n_items = tots[0] + tots[1] + tots[2];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      if (!(fl[0][k] || fl[1][k] || fl[2][k])) continue;
+      const int pos = rk[0][k] + rk[1][k] + rk[2][k];
+      const int kind = fl[0][k] ? KIND_BF16 : (fl[1][k] ? KIND_Q4 : KIND_Q2);
+      const int slot = fl[0][k] ? my_fs[k] : my_qs[k];
+      atomicAdd(&sstat[fl[0][k] ? ST_NF : (fl[1][k] ? ST_NQ4 : ST_NQ2)], 1);
       iwin[pos] = my_w[k];
       iref[pos] = (kind << 28) | slot;
       iaux[pos] = my_aux[k];
       iscore[pos] = my_sc[k];
-      icost[pos] = sd[c];
+      icost[pos] = rk[0][k] * G.cost_bf16 + rk[1][k] * G.cost_q4 + rk[2][k] * G.cost_q2;
     }
+    if (tid == 0) icost[n_items] = tots[0] * G.cost_bf16 + tots[1] * G.cost_q4 + tots[2] * G.cost_q2;
   }
   // list positions after the live windows hold the recent-region windows of the
   // next steps: their scores as they stand (windows not started yet: 0)
-  for (int j = tid; n_items + j < G.max_items; j += NT) {
-    const int w = a.aged_w1 + j;
-    iscore[n_items + j] = w < G.nwc ? score[w] : 0.f;
-  }
+  for (int j = tid; n_items + j < G.max_items; j += NT) iscore[n_items + j] = j < G.NR ? ring_sc : 0.f;
   __syncthreads();
   if (tid == 0) {
-    icost[n_items] = tots2[1];
     counts[CNT_ITEMS] = n_items;
     counts[CNT_QUANT] = nreqQ < nfreeQ ? nreqQ : nfreeQ;
     counts[CNT_PROMOTE] = nreqF < nfreeF ? nreqF : nfreeF;
