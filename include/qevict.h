@@ -194,8 +194,9 @@ qevict_status qevict_debug_masses(qevict_cache *c, int32_t layer, float *masses,
 
 /* Kernel timing with HIP events on the cache's stream (off by default).
  * kernel: 0 attention pass, 1 split merge + score accumulation, 2 re-rank,
- * 3 quantize, 4 promote.  read returns the summed milliseconds and the number
- * of timed launches since enable, and is synchronous. */
+ * 3 migrations (quantize and promote / admit, one launch), 4 unused.  read
+ * returns the summed milliseconds and the number of timed launches since
+ * enable, and is synchronous. */
 qevict_status qevict_profile_enable(qevict_cache *c, int32_t on);
 qevict_status qevict_profile_read(qevict_cache *c, int32_t kernel, double *total_ms, int64_t *count);
 

@@ -564,6 +564,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
   }
   __syncthreads();
   float* part = (float*)(ub + a.L.partial);
+  float2* pml = (float2*)(ub + a.L.pml);
   for (int idx = tid; idx < gqa * kHeadDim; idx += kAttnThreads) {
     const int h = idx >> 7, c = idx & 127;
     float M = -INFINITY;
@@ -581,63 +582,57 @@ __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
         }
       }
     }
-    float* pp = part + ((int64_t)(g * gqa + h) * S + s) * (kHeadDim + 2);
-    pp[c] = o;
-    if (c == 0) {
-      pp[kHeadDim] = M;
-      pp[kHeadDim + 1] = L;
-    }
+    const int64_t row = (int64_t)(g * gqa + h) * S + s;
+    part[row * kHeadDim + c] = o;
+    if (c == 0) pml[row] = make_float2(M, L);
   }
 }
 
-// Split merge (one block per query head) and window-score accumulation
-// (mass blocks over the live items): mass_h(w) = 2^(m_w - M_h) l_w / L_h,
-// summed over the query heads of each KV group, then over the groups, / H_q.
-// Every thread issues all of its loads in one round; reductions run in a fixed
-// order, so results do not depend on timing.
+// Split merge and window-score accumulation.
+//
+// Output blocks (one per query head): M = max_s m_s, L = sum_s l_s 2^(m_s - M),
+// out = sum_s O_s 2^(m_s - M) / L.  Mass blocks (a few live windows each, one
+// thread per (window, head)): mass_h(w) = 2^(m_w - M_h) l_w / L_h, summed over
+// the query heads of each KV group, then over the groups, / H_q, added to the
+// window's cumulative score.  Every thread issues all of its global loads in
+// one round; the reductions run in a fixed order, so results do not depend
+// on timing.
 constexpr int kMergeThreads = 256;
-constexpr int kSplitGroups = 8;                     // split rows handled in parallel per block
+constexpr int kSplitGroups = 8;                     // split rows handled in parallel per output block
 
-// NSPT: split rows one thread reads (>= S / 8 and >= S / (256 / H_q))
+// NSPT: split rows one output-block thread reads (>= S / 8)
 template <int NSPT>
 __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
-  constexpr int kSplitsPerThread = NSPT;
   const Geometry& G = a.g;
   const int blk = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
   const int32_t* counts = (const int32_t*)(ub + a.L.counts);
   const float* part = (const float*)(ub + a.L.partial);
+  const float2* pml = (const float2*)(ub + a.L.pml);
   const int S = G.n_split;
-  constexpr int PS = kHeadDim + 2;
-  __shared__ float sred[2][kSplitGroups][kHeadDim / 4 * 4];
-  __shared__ float sml[2][kMergeThreads];
+  const int nh = G.H_q;
+  __shared__ float4 sred[kSplitGroups][kHeadDim / 4];
+  __shared__ float sml[2][kSplitGroups];
   __shared__ float sM[64], sL[64];
+  __shared__ float smass[kMergeThreads];
 
-  if (blk < G.H_q) {
+  if (blk < nh) {
     // ---- output of head h: thread (c4, grp) owns channels 4c4..4c4+3 of splits grp + 8i ----
     const int h = blk;
-    const float* ph = part + (int64_t)h * S * PS;
     const int c4 = tid & 31, grp = tid >> 5;
-    float4 o[kSplitsPerThread];
-    float ms[kSplitsPerThread], ls[kSplitsPerThread];
+    float4 o[NSPT];
+    float2 ml[NSPT];
 #pragma unroll
-    for (int i = 0; i < kSplitsPerThread; ++i) {
+    for (int i = 0; i < NSPT; ++i) {
       const int sp = grp + kSplitGroups * i;
-      if (sp < S) {
-        const float* row = ph + sp * PS;
-        const float2 x0 = ((const float2*)row)[2 * c4], x1 = ((const float2*)row)[2 * c4 + 1];
-        o[i] = make_float4(x0.x, x0.y, x1.x, x1.y);
-        ms[i] = row[kHeadDim];
-        ls[i] = row[kHeadDim + 1];
-      } else {
-        o[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-        ms[i] = -INFINITY;
-        ls[i] = 0.f;
-      }
+      const bool ok = sp < S;
+      o[i] = ok ? *(const float4*)(part + ((int64_t)h * S + sp) * kHeadDim + 4 * c4)
+                : make_float4(0.f, 0.f, 0.f, 0.f);
+      ml[i] = ok ? pml[(int64_t)h * S + sp] : make_float2(-INFINITY, 0.f);
     }
     float m = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < kSplitsPerThread; ++i) m = fmaxf(m, ms[i]);
+    for (int i = 0; i < NSPT; ++i) m = fmaxf(m, ml[i].x);
     if (c4 == 0) sml[0][grp] = m;
     __syncthreads();
     float M = -INFINITY;
@@ -647,111 +642,132 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
     float lsum = 0.f;
     if (M > -INFINITY) {
 #pragma unroll
-      for (int i = 0; i < kSplitsPerThread; ++i) {
-        const float f = ms[i] > -INFINITY ? __builtin_amdgcn_exp2f(ms[i] - M) : 0.f;
+      for (int i = 0; i < NSPT; ++i) {
+        const float f = ml[i].x > -INFINITY ? __builtin_amdgcn_exp2f(ml[i].x - M) : 0.f;
         acc.x += f * o[i].x;
         acc.y += f * o[i].y;
         acc.z += f * o[i].z;
         acc.w += f * o[i].w;
-        lsum += f * ls[i];
+        lsum += f * ml[i].y;
       }
     }
-    *(float4*)&sred[0][grp][4 * c4] = acc;
+    sred[grp][c4] = acc;
     if (c4 == 0) sml[1][grp] = lsum;
     __syncthreads();
-    if (tid < kHeadDim) {
-      const int c = tid;
-      float out = 0.f, L = 0.f;
+    if (tid < kHeadDim / 4) {
+      float4 out = make_float4(0.f, 0.f, 0.f, 0.f);
+      float L = 0.f;
 #pragma unroll
       for (int q = 0; q < kSplitGroups; ++q) {
-        out += sred[0][q][c];
+        const float4 x = sred[q][tid];
+        out.x += x.x;
+        out.y += x.y;
+        out.z += x.z;
+        out.w += x.w;
         L += sml[1][q];
       }
-      out = L > 0.f ? out / L : 0.f;
-      const int64_t oi = ((int64_t)b * G.H_q + h) * kHeadDim + c;
-      if (G.out_bf16) ((uint16_t*)a.out)[oi] = f32_to_bf16_rne(out);
-      else ((float*)a.out)[oi] = out;
+      const float inv = L > 0.f ? 1.f / L : 0.f;
+      const float v[4] = {out.x * inv, out.y * inv, out.z * inv, out.w * inv};
+      const int64_t oi = ((int64_t)b * nh + h) * kHeadDim + 4 * tid;
+      if (G.out_bf16) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ((uint16_t*)a.out)[oi + e] = f32_to_bf16_rne(v[e]);
+      } else {
+        *(float4*)((float*)a.out + oi) = make_float4(v[0], v[1], v[2], v[3]);
+      }
     }
     return;
   }
 
-  // ---- mass blocks: one thread per (item, head); every load in one round ----
-  const int nh = G.H_q;
-  const int parts = kMergeThreads / nh;          // threads per head for (M_h, L_h)
-  const int hh = tid % nh, pp = tid / nh;
-  const int n_fq = counts[CNT_ITEMS];
-  const int n_all = n_fq + a.n_ring + a.n_sink_items;
+  // ---- mass blocks: thread (li, hh) = (item of the block, query head) ----
   const int per_blk = kMergeThreads / nh;
-  const int li = tid / nh;
-  const int pos = (blk - G.H_q) * per_blk + li;
-  const bool active = li < per_blk && pos < n_all;
+  const int li = tid / nh, hh = tid % nh;
+  const int pos = (blk - nh) * per_blk + li;
+  const bool in_blk = li < per_blk;
+  // one round: this item's window statistics, list entry and score, all split statistics
+  const int n_fq = counts[CNT_ITEMS];
   const float2* __restrict__ mref = (const float2*)(ub + a.L.mref);
-  const float2 mr = active ? mref[(int64_t)pos * nh + hh] : make_float2(-INFINITY, 0.f);
   const int32_t* __restrict__ iwin = (const int32_t*)(ub + a.L.item_win);
-  const int win = !active ? -1
-                  : (pos < n_fq ? iwin[pos] : (pos < n_fq + a.n_ring ? a.ring_w0 + (pos - n_fq) : -1));
-  float* score = (float*)(ub + a.L.score);
-  const float old_score = (active && hh == 0 && win >= 0) ? score[win] : 0.f;
-  float msv[kSplitsPerThread], lsv[kSplitsPerThread];
-#pragma unroll
-  for (int i = 0; i < kSplitsPerThread; ++i) {
-    const int sp = pp + parts * i;
-    const bool ok = pp < parts && sp < S;
-    const float* row = part + ((int64_t)hh * S + sp) * PS;
-    msv[i] = ok ? row[kHeadDim] : -INFINITY;
-    lsv[i] = ok ? row[kHeadDim + 1] : 0.f;
-  }
-  float mloc = -INFINITY;
-#pragma unroll
-  for (int i = 0; i < kSplitsPerThread; ++i) mloc = fmaxf(mloc, msv[i]);
-  sml[0][tid] = mloc;
-  __syncthreads();
-  if (tid < nh) {
-    float M = -INFINITY;
-    for (int q = 0; q < parts; ++q) M = fmaxf(M, sml[0][q * nh + tid]);
-    sM[tid] = M;
-  }
-  __syncthreads();
+  float* iscore = (float*)(ub + a.L.item_score);
+  const bool maybe = in_blk && pos < G.max_items;
+  const float2 mr = maybe ? mref[(int64_t)pos * nh + hh] : make_float2(-INFINITY, 0.f);
+  const int wl = (maybe && hh == 0) ? iwin[min(pos, G.max_fq)] : -1;   // used when pos < n_fq
+  const float old_score = (maybe && hh == 0) ? iscore[pos] : 0.f;
+  // M_h, L_h: P consecutive threads per head (P a power of two, P * H_q <= 256),
+  // thread j folds splits j*C .. j*C + C - 1 from its own loads, then a
+  // butterfly over the P lanes combines the (max, sum) pairs
+  int P = 1;
+  while (2 * P * nh <= kMergeThreads) P *= 2;
+  const int C = (S + P - 1) / P;
+  constexpr int kMaxC = 32;   // C <= S * H_q / 128 + 1 <= 17 (S * H_q <= 2048)
   {
-    const float M = sM[hh];
-    float lloc = 0.f;
-    if (M > -INFINITY) {
+    const int h = tid / P, j = tid % P;
+    const bool hv = h < nh;
+    float2 st[kMaxC];
 #pragma unroll
-      for (int i = 0; i < kSplitsPerThread; ++i)
-        if (msv[i] > -INFINITY) lloc += lsv[i] * __builtin_amdgcn_exp2f(msv[i] - M);
+    for (int i = 0; i < kMaxC; ++i) {
+      const int sp = j * C + i;
+      st[i] = (hv && i < C && sp < S) ? pml[(int64_t)h * S + sp] : make_float2(-INFINITY, 0.f);
     }
-    sml[1][tid] = lloc;
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kMaxC; ++i) m = fmaxf(m, st[i].x);
+    float l = 0.f;
+    if (m > -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < kMaxC; ++i)
+        if (st[i].x > -INFINITY) l += st[i].y * __builtin_amdgcn_exp2f(st[i].x - m);
+    }
+    for (int o = 1; o < P; o <<= 1) {
+      const float m2 = __shfl_xor(m, o, 64), l2 = __shfl_xor(l, o, 64);
+      const float mm = fmaxf(m, m2);
+      float ls = 0.f;
+      if (m > -INFINITY) ls += l * __builtin_amdgcn_exp2f(m - mm);
+      if (m2 > -INFINITY) ls += l2 * __builtin_amdgcn_exp2f(m2 - mm);
+      m = mm;
+      l = ls;
+    }
+    if (hv && j == 0) {
+      sM[h] = m;
+      sL[h] = l;
+    }
   }
   __syncthreads();
-  if (tid < nh) {
-    float L = 0.f;
-    for (int q = 0; q < parts; ++q) L += sml[1][q * nh + tid];
-    sL[tid] = L;
+  const int n_all = n_fq + a.n_ring + a.n_sink_items;
+  const bool active = in_blk && pos < n_all;
+  const float mass = (active && sL[hh] > 0.f && mr.x > -INFINITY)
+                         ? __builtin_amdgcn_exp2f(mr.x - sM[hh]) * mr.y / sL[hh] : 0.f;
+  // sum over the heads of the item: adjacent heads first (the heads of one KV
+  // group), then the groups; a butterfly when H_q is a power of two
+  float tot = mass;
+  const bool pow2 = (nh & (nh - 1)) == 0;
+  if (pow2) {
+    for (int o = 1; o < nh; o <<= 1) tot += __shfl_xor(tot, o, 64);
+  } else {
+    smass[tid] = mass;
+    __syncthreads();
+    if (hh == 0 && in_blk) {
+      const float* m = smass + li * nh;
+      tot = 0.f;
+      for (int g = 0; g < G.H_kv; ++g) {
+        float sg = 0.f;
+        for (int j = 0; j < G.gqa; ++j) sg += m[g * G.gqa + j];
+        tot += sg;
+      }
+    }
   }
-  __syncthreads();
-  const float mass = (active && sL[hh] > 0.f) ? __builtin_amdgcn_exp2f(mr.x - sM[hh]) * mr.y / sL[hh]
-                                               : 0.f;
-  float* smass = &sml[0][0];
-  smass[tid] = mass;
-  __syncthreads();
   if (!active) return;
+  const int win = pos < n_fq ? wl : (pos < n_fq + a.n_ring ? a.ring_w0 + (pos - n_fq) : -1);
   if (G.flags & 2u) {   // per-head masses of this step, for inspection
     float* dbg = (float*)(ub + a.L.dbg_mass);
-    if (win >= 0) dbg[(int64_t)hh * (G.nwc + 1) + win] = mass;
+    const int w_h = pos < n_fq ? iwin[pos] : win;
+    if (w_h >= 0) dbg[(int64_t)hh * (G.nwc + 1) + w_h] = mass;
     else atomicAdd(&dbg[(int64_t)hh * (G.nwc + 1) + G.nwc], mass);
   }
   if (hh == 0 && win >= 0) {
-    // heads of one KV group first, then the groups in order
-    const float* m = smass + li * nh;
-    float tot = 0.f;
-    for (int g = 0; g < G.H_kv; ++g) {
-      float sg = 0.f;
-      for (int j = 0; j < G.gqa; ++j) sg += m[g * G.gqa + j];
-      tot += sg;
-    }
     const float ns = old_score + tot / (float)nh;
-    score[win] = ns;
-    ((float*)(ub + a.L.item_score))[pos] = ns;   // the next re-rank reads it by list position
+    ((float*)(ub + a.L.score))[win] = ns;
+    iscore[pos] = ns;   // the next re-rank and merge read it by list position
   }
 }
 
@@ -783,9 +799,9 @@ hipError_t launch_merge(const AttnArgs& a, hipStream_t st) {
   const int per_blk = kMergeThreads / a.g.H_q;
   const int n_mass = (a.g.max_items + per_blk - 1) / per_blk;
   dim3 grid(a.g.H_q + n_mass, a.g.B);
-  const int need = max((a.g.n_split + kSplitGroups - 1) / kSplitGroups,
-                       (a.g.n_split + per_blk - 1) / per_blk);
-  if (need <= 8) hipLaunchKernelGGL(k_merge<8>, grid, dim3(kMergeThreads), 0, st, a);
+  const int need = (a.g.n_split + kSplitGroups - 1) / kSplitGroups;
+  if (need <= 4) hipLaunchKernelGGL(k_merge<4>, grid, dim3(kMergeThreads), 0, st, a);
+  else if (need <= 8) hipLaunchKernelGGL(k_merge<8>, grid, dim3(kMergeThreads), 0, st, a);
   else hipLaunchKernelGGL(k_merge<32>, grid, dim3(kMergeThreads), 0, st, a);
   return hipGetLastError();
 }

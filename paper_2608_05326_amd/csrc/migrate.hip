@@ -171,69 +171,67 @@ __device__ __forceinline__ void load_window(const MigrateArgs& a, uint8_t* ub, i
 // the packed 16-byte block (entry e's 8 codes at bits 16 o + b (4 e' + i)).
 // Keys form groups per channel (W tokens), values per token (G = W channels).
 template <int W>
-__global__ __launch_bounds__(kMigrateThreads) void k_quantize(MigrateArgs a) {
+struct QuantLds {
+  uint16_t sk[W * kHeadDim];
+  uint16_t sv[W * kHeadDim];
+  QParams pk[kHeadDim];
+  QParams pv[W * (kHeadDim / W)];
+};
+
+template <int W>
+__device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub, int b, int g,
+                                              const int32_t* ent, QuantLds<W>& sm, int32_t* counts) {
   const Geometry& G = a.g;
   constexpr int NG = kHeadDim / W;             // value groups per token
-  const int b = blockIdx.y, tid = threadIdx.x;
-  __shared__ __attribute__((aligned(16))) uint16_t sk[W * kHeadDim];
-  __shared__ __attribute__((aligned(16))) uint16_t sv[W * kHeadDim];
-  __shared__ QParams pk[kHeadDim];
-  __shared__ QParams pv[W * NG];
-  uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
-  int32_t* counts = (int32_t*)(ub + a.L.counts);
-  const int32_t* qlist = (const int32_t*)(ub + a.L.qlist);
-  const int n = counts[CNT_QUANT];
-  for (int task = blockIdx.x; task < n * G.H_kv; task += gridDim.x) {
-    const int e = task / G.H_kv, g = task % G.H_kv;
-    const int32_t* ent = qlist + e * kQEntry;
-    const int w = ent[0], src_kind = ent[1], src_idx = ent[2], dst = ent[3], nb = ent[4];
-    load_window<W>(a, ub, b, g, w, src_kind, src_idx, sk, sv);
-    __syncthreads();
-    uint8_t* rec = ub + a.L.qpool + (int64_t)dst * G.qslot_bytes + g * G.qrec_bytes;
-    // ---- group parameters: threads 0..127 key channels, then value groups ----
-    for (int grp = tid; grp < kHeadDim + W * NG; grp += blockDim.x) {
-      float x[W];
-      if (grp < kHeadDim) {
+  const int tid = threadIdx.x;
+  const int w = ent[0], src_kind = ent[1], src_idx = ent[2], dst = ent[3], nb = ent[4];
+  uint16_t* sk = sm.sk;
+  uint16_t* sv = sm.sv;
+  load_window<W>(a, ub, b, g, w, src_kind, src_idx, sk, sv);
+  __syncthreads();
+  uint8_t* rec = ub + a.L.qpool + (int64_t)dst * G.qslot_bytes + g * G.qrec_bytes;
+  // ---- group parameters: threads 0..127 key channels, then value groups ----
+  for (int grp = tid; grp < kHeadDim + W * NG; grp += blockDim.x) {
+    float x[W];
+    if (grp < kHeadDim) {
 #pragma unroll
-        for (int t = 0; t < W; ++t) x[t] = bf16_to_f32(sk[t * kHeadDim + grp]);
-      } else {
-        const int gi = grp - kHeadDim, t = gi / NG, vg = gi % NG;
-        const u32x4* row = (const u32x4*)(sv + t * kHeadDim + vg * W);
+      for (int t = 0; t < W; ++t) x[t] = bf16_to_f32(sk[t * kHeadDim + grp]);
+    } else {
+      const int gi = grp - kHeadDim, t = gi / NG, vg = gi % NG;
+      const u32x4* row = (const u32x4*)(sv + t * kHeadDim + vg * W);
 #pragma unroll
-        for (int k = 0; k < W / 8; ++k) {
-          const u32x4 v = row[k];
-          const uint32_t vw[4] = {v[0], v[1], v[2], v[3]};
+      for (int k = 0; k < W / 8; ++k) {
+        const u32x4 v = row[k];
+        const uint32_t vw[4] = {v[0], v[1], v[2], v[3]};
 #pragma unroll
-          for (int i = 0; i < 8; ++i) x[8 * k + i] = bf16_to_f32((uint16_t)(vw[i >> 1] >> (16 * (i & 1))));
-        }
-      }
-      float lo = x[0], hi = x[0];
-#pragma unroll
-      for (int t = 1; t < W; ++t) {
-        lo = fminf(lo, x[t]);
-        hi = fmaxf(hi, x[t]);
-      }
-      uint16_t zb = 0, sb = 0;
-      const QParams p = group_params(lo, hi, nb, &zb, &sb, counts);
-      if (grp < kHeadDim) {
-        pk[grp] = p;
-        uint16_t* mk = (uint16_t*)(rec + meta_k_off(G));
-        mk[grp] = sb;
-        mk[kHeadDim + grp] = zb;
-      } else {
-        const int gi = grp - kHeadDim, t = gi / NG, vg = gi % NG;
-        pv[gi] = p;
-        uint16_t* mv = (uint16_t*)(rec + meta_v_elem(G, t, vg));
-        mv[0] = sb;
-        mv[8] = zb;
+        for (int i = 0; i < 8; ++i) x[8 * k + i] = bf16_to_f32((uint16_t)(vw[i >> 1] >> (16 * (i & 1))));
       }
     }
-    __syncthreads();
-    // ---- codes, packed ----
-    if (nb == 4) pack_codes<W, 4>(G, sk, sv, pk, pv, rec, tid);
-    else pack_codes<W, 2>(G, sk, sv, pk, pv, rec, tid);
-    __syncthreads();
+    float lo = x[0], hi = x[0];
+#pragma unroll
+    for (int t = 1; t < W; ++t) {
+      lo = fminf(lo, x[t]);
+      hi = fmaxf(hi, x[t]);
+    }
+    uint16_t zb = 0, sb = 0;
+    const QParams p = group_params(lo, hi, nb, &zb, &sb, counts);
+    if (grp < kHeadDim) {
+      sm.pk[grp] = p;
+      uint16_t* mk = (uint16_t*)(rec + meta_k_off(G));
+      mk[grp] = sb;
+      mk[kHeadDim + grp] = zb;
+    } else {
+      const int gi = grp - kHeadDim, t = gi / NG, vg = gi % NG;
+      sm.pv[gi] = p;
+      uint16_t* mv = (uint16_t*)(rec + meta_v_elem(G, t, vg));
+      mv[0] = sb;
+      mv[8] = zb;
+    }
   }
+  __syncthreads();
+  // ---- codes, packed ----
+  if (nb == 4) pack_codes<W, 4>(G, sk, sv, sm.pk, sm.pv, rec, tid);
+  else pack_codes<W, 2>(G, sk, sv, sm.pk, sm.pv, rec, tid);
 }
 
 // 8 bf16 values z_j + s_j c_j (exact in float64, one rounding) packed for a 16-byte store
@@ -292,39 +290,67 @@ __device__ __forceinline__ void promote_from_record(const Geometry& G, const uin
 }
 
 template <int W>
-__global__ __launch_bounds__(kMigrateThreads) void k_promote(MigrateArgs a) {
+__device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, int b, int g,
+                                             const int32_t* ent) {
   const Geometry& G = a.g;
-  const int b = blockIdx.y, tid = threadIdx.x;
+  const int tid = threadIdx.x;
+  const int w = ent[0], src_kind = ent[1], src_idx = ent[2], dst = ent[3], nb = ent[4];
+  uint8_t* dp = ub + a.L.fpool + (int64_t)dst * G.fslot_bytes + g * G.fhead_bytes;
+  if (src_kind == SRC_RING) {
+    const u32x4* sp = (const u32x4*)(ub + a.L.ring + (int64_t)src_idx * G.fslot_bytes +
+                                     g * G.fhead_bytes);
+    for (int i = tid; i < G.fhead_bytes / 16; i += blockDim.x) ((u32x4*)dp)[i] = sp[i];
+  } else if (src_kind == SRC_PROMPT) {
+    const int64_t row0 = ((int64_t)b * G.H_kv + g) * a.src_T + G.sink + (int64_t)w * W;
+    const uint16_t* ks = a.src_k + row0 * kHeadDim;
+    const uint16_t* vs = a.src_v + row0 * kHeadDim;
+    for (int i = tid; i < W * kHeadDim / 8; i += blockDim.x) {
+      const int t = i / 16, c = (i % 16) * 8;
+      *(u32x4*)(dp + k_elem_off(t, c)) = *(const u32x4*)(ks + t * kHeadDim + c);
+    }
+    for (int i = tid; i < W * kHeadDim; i += blockDim.x) {
+      const int t = i >> 7, c = i & 127;
+      *(uint16_t*)(dp + v_elem_off(W, t, c)) = vs[t * kHeadDim + c];
+    }
+  } else {   // SRC_QSLOT
+    const uint8_t* rec = ub + a.L.qpool + (int64_t)src_idx * G.qslot_bytes + g * G.qrec_bytes;
+    if (nb == 4) promote_from_record<W, 4>(G, rec, dp, tid);
+    else promote_from_record<W, 2>(G, rec, dp, tid);
+  }
+}
+
+// Migrations of one routing event, one (window, KV head) task per workgroup
+// pass: quantizations first, then promotions / admissions.  A promotion whose
+// bf16 slot is being vacated by a quantization in the same event (dep >= 0)
+// runs in that quantization's workgroup right after it, so the slot is read
+// before it is overwritten without any ordering across workgroups.
+template <int W>
+__global__ __launch_bounds__(kMigrateThreads) void k_migrate(MigrateArgs a) {
+  const Geometry& G = a.g;
+  const int b = blockIdx.y;
+  __shared__ __attribute__((aligned(16))) QuantLds<W> sm;
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
   int32_t* counts = (int32_t*)(ub + a.L.counts);
+  const int32_t* qlist = (const int32_t*)(ub + a.L.qlist);
   const int32_t* plist = (const int32_t*)(ub + a.L.plist);
-  const int n = counts[CNT_PROMOTE];
-  for (int task = blockIdx.x; task < n * G.H_kv; task += gridDim.x) {
-    const int e = task / G.H_kv, g = task % G.H_kv;
-    const int32_t* ent = plist + e * kQEntry;
-    const int w = ent[0], src_kind = ent[1], src_idx = ent[2], dst = ent[3], nb = ent[4];
-    uint8_t* dp = ub + a.L.fpool + (int64_t)dst * G.fslot_bytes + g * G.fhead_bytes;
-    if (src_kind == SRC_RING) {
-      const u32x4* sp = (const u32x4*)(ub + a.L.ring + (int64_t)src_idx * G.fslot_bytes +
-                                       g * G.fhead_bytes);
-      for (int i = tid; i < G.fhead_bytes / 16; i += blockDim.x) ((u32x4*)dp)[i] = sp[i];
-    } else if (src_kind == SRC_PROMPT) {
-      const int64_t row0 = ((int64_t)b * G.H_kv + g) * a.src_T + G.sink + (int64_t)w * W;
-      const uint16_t* ks = a.src_k + row0 * kHeadDim;
-      const uint16_t* vs = a.src_v + row0 * kHeadDim;
-      for (int i = tid; i < W * kHeadDim / 8; i += blockDim.x) {
-        const int t = i / 16, c = (i % 16) * 8;
-        *(u32x4*)(dp + k_elem_off(t, c)) = *(const u32x4*)(ks + t * kHeadDim + c);
+  const int nq = counts[CNT_QUANT], np = counts[CNT_PROMOTE];
+  for (int task = blockIdx.x; task < (nq + np) * G.H_kv; task += gridDim.x) {
+    if (task < nq * G.H_kv) {
+      const int e = task / G.H_kv, g = task % G.H_kv;
+      const int32_t* ent = qlist + e * kQEntry;
+      quantize_task<W>(a, ub, b, g, ent, sm, counts);
+      const int dep = ent[5];
+      if (dep >= 0) {
+        __syncthreads();
+        promote_task<W>(a, ub, b, g, plist + dep * kQEntry);
       }
-      for (int i = tid; i < W * kHeadDim; i += blockDim.x) {
-        const int t = i >> 7, c = i & 127;
-        *(uint16_t*)(dp + v_elem_off(W, t, c)) = vs[t * kHeadDim + c];
-      }
-    } else {   // SRC_QSLOT
-      const uint8_t* rec = ub + a.L.qpool + (int64_t)src_idx * G.qslot_bytes + g * G.qrec_bytes;
-      if (nb == 4) promote_from_record<W, 4>(G, rec, dp, tid);
-      else promote_from_record<W, 2>(G, rec, dp, tid);
+    } else {
+      const int t2 = task - nq * G.H_kv;
+      const int e = t2 / G.H_kv, g = t2 % G.H_kv;
+      const int32_t* ent = plist + e * kQEntry;
+      if (ent[5] < 0) promote_task<W>(a, ub, b, g, ent);
     }
+    __syncthreads();
   }
 }
 
@@ -357,16 +383,10 @@ static int migrate_blocks(const Geometry& g, int max_entries) {
   return n < 1 ? 1 : (n > 256 ? 256 : n);
 }
 
-hipError_t launch_quantize(const MigrateArgs& a, int max_entries, hipStream_t st) {
-  const dim3 grid(migrate_blocks(a.g, max_entries), a.g.B);
-  if (a.g.W == 32) hipLaunchKernelGGL(k_quantize<32>, grid, dim3(kMigrateThreads), 0, st, a);
-  else hipLaunchKernelGGL(k_quantize<64>, grid, dim3(kMigrateThreads), 0, st, a);
-  return hipGetLastError();
-}
-hipError_t launch_promote(const MigrateArgs& a, int max_entries, hipStream_t st) {
-  const dim3 grid(migrate_blocks(a.g, max_entries), a.g.B);
-  if (a.g.W == 32) hipLaunchKernelGGL(k_promote<32>, grid, dim3(kMigrateThreads), 0, st, a);
-  else hipLaunchKernelGGL(k_promote<64>, grid, dim3(kMigrateThreads), 0, st, a);
+hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, hipStream_t st) {
+  const dim3 grid(migrate_blocks(a.g, max_quant + max_promote), a.g.B);
+  if (a.g.W == 32) hipLaunchKernelGGL(k_migrate<32>, grid, dim3(kMigrateThreads), 0, st, a);
+  else hipLaunchKernelGGL(k_migrate<64>, grid, dim3(kMigrateThreads), 0, st, a);
   return hipGetLastError();
 }
 hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st) {

@@ -60,7 +60,10 @@ enum : int32_t { ST_PROMO = 0, ST_ADMIT = 1, ST_FIRSTQ = 2, ST_REACT = 3, ST_EVI
                  ST_NF = 5, ST_NQ4 = 6, ST_NQ2 = 7, ST_N = 8 };
 // work-list sources
 enum : int32_t { SRC_FSLOT = 0, SRC_RING = 1, SRC_PROMPT = 2, SRC_QSLOT = 3 };
-constexpr int kQEntry = 5;   // ints per work-list entry: win, src_kind, src_idx, dst, bits
+// ints per work-list entry: win, src_kind, src_idx, dst, bits, dep; dep pairs a
+// quantization that reads a bf16 slot with the promotion / admission that
+// writes the same slot (index of the other list's entry, or -1)
+constexpr int kQEntry = 6;
 
 struct Geometry {
   int32_t B, H_q, H_kv, gqa, d, W, G;

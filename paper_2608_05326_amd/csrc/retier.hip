@@ -536,15 +536,18 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   }
   int32_t* freeF = sinfo;
   int32_t* freeQ = sb;
+  int32_t* sdep = sa;   // per bf16 slot: quantization entry reading it in this event, or -1
+  for (int i = tid; i < G.K_f; i += NT) sdep[i] = -1;
   __syncthreads();
 
   // ---- apply: new slots, ledger states, work lists ----
   const int src_aged = a.prefill ? SRC_PROMPT : SRC_RING;
-  int my_aux[PER];
+  int my_aux[PER], my_pl[PER];   // promotion / admission entry to write once slot dependencies are known
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
     my_aux[k] = -1;
+    my_pl[k] = -1;
     if (c >= n_cand) continue;
     const int w = my_w[k];
     const int old = my_old[k], nt = my_nt[k];
@@ -557,13 +560,11 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       if (rk < nfreeF) {
         fs = freeF[rk];
         fown[fs] = w;
-        int32_t* e = plist + rk * kQEntry;
+        my_pl[k] = rk;
         if (old == T_QUANT) {
-          e[0] = w; e[1] = SRC_QSLOT; e[2] = qs; e[3] = fs; e[4] = nb;
           led = L_DORMANT;
           atomicAdd(&sstat[ST_PROMO], 1);
         } else {
-          e[0] = w; e[1] = src_aged; e[2] = a.prefill ? w : w % G.NR; e[3] = fs; e[4] = 0;
           atomicAdd(&sstat[ST_ADMIT], 1);
         }
       } else {
@@ -579,10 +580,17 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
         led = L_ACTIVE;
         int32_t* e = qlist + rk * kQEntry;
         e[0] = w;
-        if (old == T_FULL) { e[1] = SRC_FSLOT; e[2] = my_fs[k]; }
-        else { e[1] = src_aged; e[2] = a.prefill ? w : w % G.NR; }
+        if (old == T_FULL) {
+          e[1] = SRC_FSLOT;
+          e[2] = my_fs[k];
+          sdep[my_fs[k]] = rk;
+        } else {
+          e[1] = src_aged;
+          e[2] = a.prefill ? w : w % G.NR;
+        }
         e[3] = qs;
         e[4] = nb;
+        e[5] = -1;
         atomicAdd(&sstat[ST_FIRSTQ], 1);
       } else {
         set_error(counts, ERR_POOL);
@@ -608,6 +616,24 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     my_aux[k] = qs >= 0 ? (qs | (nb << 28)) : -1;
   }
   __syncthreads();
+  // promotion / admission entries: one whose bf16 slot is being quantized away in
+  // this event runs after that quantization (paired through the dep fields)
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    if (my_pl[k] < 0) continue;
+    const int rk = my_pl[k], w = my_w[k], fs = my_fs[k];
+    int32_t* e = plist + rk * kQEntry;
+    e[0] = w;
+    if (my_old[k] == T_QUANT) {
+      e[1] = SRC_QSLOT; e[2] = my_qs[k]; e[4] = my_bits[k];
+    } else {
+      e[1] = src_aged; e[2] = a.prefill ? w : w % G.NR; e[4] = 0;
+    }
+    e[3] = fs;
+    const int dep = sdep[fs];
+    e[5] = dep;
+    if (dep >= 0) qlist[dep * kQEntry + 5] = rk;
+  }
   for (int i = tid; i < G.K_f; i += NT) fowner[i] = fown[i];
   for (int i = tid; i < G.n_qslots; i += NT) qowner[i] = qown[i];
 
@@ -691,7 +717,7 @@ __global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
       bits[w] = (int8_t)nb;
       ledger[w] = L_ACTIVE;
       int32_t* e = qlist;
-      e[0] = w; e[1] = SRC_FSLOT; e[2] = fs; e[3] = qs; e[4] = nb;
+      e[0] = w; e[1] = SRC_FSLOT; e[2] = fs; e[3] = qs; e[4] = nb; e[5] = -1;
       counts[CNT_QUANT] = 1;
     }
     fowner[fs] = -1;
@@ -709,7 +735,7 @@ __global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
     ledger[w] = L_DORMANT;
     tier[w] = T_FULL;
     int32_t* e = plist;
-    e[0] = w; e[1] = SRC_QSLOT; e[2] = qslot[w]; e[3] = fs; e[4] = bits[w];
+    e[0] = w; e[1] = SRC_QSLOT; e[2] = qslot[w]; e[3] = fs; e[4] = bits[w]; e[5] = -1;
     counts[CNT_PROMOTE] = 1;
     kind = KIND_BF16;
     slot = fs;

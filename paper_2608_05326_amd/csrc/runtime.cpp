@@ -29,8 +29,7 @@ hipError_t launch_retier(const RetierArgs& a, hipStream_t st);
 hipError_t launch_manual_move(const RetierArgs& a, int seq, int window, int to_quant, hipStream_t st);
 hipError_t launch_init_units(const Geometry& g, const UnitLayout& L, uint8_t* base, int n_units,
                              hipStream_t st);
-hipError_t launch_quantize(const MigrateArgs& a, int max_entries, hipStream_t st);
-hipError_t launch_promote(const MigrateArgs& a, int max_entries, hipStream_t st);
+hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, hipStream_t st);
 hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st);
 }  // namespace qv
 
@@ -474,8 +473,7 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
   RetierArgs ra{gg, L, base, 1, 0, n_hist, init_scores, n_init};
   if (e == hipSuccess) e = timed(c, 2, c->stream, [&] { return launch_retier(ra, c->stream); });
   MigrateArgs ma{gg, L, base, k, v, prompt_len};
-  if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_quantize(ma, g.K_q, c->stream); });
-  if (e == hipSuccess) e = timed(c, 4, c->stream, [&] { return launch_promote(ma, g.K_f, c->stream); });
+  if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_migrate(ma, g.K_q, g.K_f, c->stream); });
   if (e == hipSuccess) e = mark_layer(c, layer);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   ls.T = prompt_len;
@@ -545,8 +543,7 @@ qevict_status qevict_retier(qevict_cache* c, int32_t layer, qevict_retier_stats*
   hipError_t e = hipSuccess;
   if (c->rstream) e = hipStreamWaitEvent(rs, c->attn_ev[layer], 0);
   if (e == hipSuccess) e = timed(c, 2, rs, [&] { return launch_retier(ra, rs); });
-  if (e == hipSuccess) e = timed(c, 3, rs, [&] { return launch_quantize(ma, max_q, rs); });
-  if (e == hipSuccess) e = timed(c, 4, rs, [&] { return launch_promote(ma, g.K_f, rs); });
+  if (e == hipSuccess) e = timed(c, 3, rs, [&] { return launch_migrate(ma, max_q, g.K_f, rs); });
   if (e == hipSuccess && c->rstream) {
     e = hipEventRecord(c->route_ev[layer], rs);
     if (e == hipSuccess) c->route_pending[layer] = 1;
@@ -624,8 +621,7 @@ static qevict_status manual_move(qevict_cache* c, int layer, int seq, int window
   one.B = 1;
   MigrateArgs ma{one, L, unit_base(c, layer, seq), nullptr, nullptr, 0};
   e = launch_manual_move(ra, seq, window, to_quant, c->stream);
-  if (e == hipSuccess) e = launch_quantize(ma, 1, c->stream);
-  if (e == hipSuccess) e = launch_promote(ma, 1, c->stream);
+  if (e == hipSuccess) e = launch_migrate(ma, 1, 1, c->stream);
   if (e == hipSuccess) e = mark_layer(c, layer);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(e, "manual move");

@@ -24,7 +24,7 @@ LEDGER_NONE, LEDGER_ACTIVE, LEDGER_DORMANT = 0, 1, 2
 BITS_MIXED_4_2 = 42
 OUT_F32, OUT_BF16 = 0, 1
 FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING = 0x1, 0x2, 0x4
-KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_QUANTIZE, KERNEL_PROMOTE = range(5)
+KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_MIGRATE = range(4)
 
 # exported symbols declared in include/qevict.h
 SYMBOLS = (
