@@ -278,12 +278,21 @@ def main():
     done = args.warmup + args.steps
 
     # ---- attention timing with asynchronous routing: rounds of back-to-back
-    # decode_attend calls, each started after the previous round's routing ----
+    # decode_attend calls with no routing running beside them (each round starts
+    # after the previous round's routing and routes only after its attention) ----
     if asyncr and not args.no_kernel_events:
         for _ in range(4):
             cache.join_routing()
             torch.cuda.synchronize()
-            run_steps(done, NL, attn_events)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for l in range(NL):
+                attend(l)
+            e1.record(stream)
+            attn_events.append((e0, e1, NL))
+            torch.cuda.synchronize()
+            for l in range(NL):
+                route(l)
             done += NL
         cache.join_routing()
         torch.cuda.synchronize()

@@ -149,11 +149,19 @@ __device__ __forceinline__ void softmax_window(const f32x4 (&acc)[TB], float bia
   *l_out = lw;
 }
 
-// Per-window operand buffer: bf16 windows hold their K chunks then V chunks;
-// quantized windows hold K codes, V codes, K scale/zero, V scale/zero.
+// Per-window operands in registers, split into the part the QK^T phase reads
+// (K) and the part the P.V phase reads (V).
+//   bf16 window: K chunks (tb, kb) at kh.d[tb * 4 + kb]; V chunks (kt, cb) at vh.d[kt * 8 + cb]
+//   quantized:   K codes kh.d[0 .. NC), K scale / zero (compact) kh.d[NC], kh.d[NC + 1];
+//                V codes vh.d[0 .. NC), V scale / zero per (kt, vg) at vh.d[NC + 2 (kt NG + vg)] (+1)
 template <int W>
-struct ItemBuf {
-  static constexpr int N = W == 32 ? 16 : 32;
+struct KHalf {
+  static constexpr int N = W / 4;
+  u32x4 d[N];
+};
+template <int W>
+struct VHalf {
+  static constexpr int N = W == 32 ? 10 : 16;
   u32x4 d[N];
 };
 
@@ -164,142 +172,110 @@ struct ItemInfo {
 };
 
 template <int W>
-__device__ __forceinline__ void fetch_item(const ItemInfo& in, ItemBuf<W>& buf, int lane, int qg,
-                                           int r, const Geometry& G) {
-  constexpr int TB = W / 16, KT = W / 32;
+__device__ __forceinline__ void fetch_k(const ItemInfo& in, KHalf<W>& kh, int lane, int r,
+                                        const Geometry& G) {
+  constexpr int TB = W / 16, NC = W / 16;
+  const uint8_t* p = in.p;
+  if (in.kind == KIND_BF16) {
+#pragma unroll
+    for (int i = 0; i < 4 * TB; ++i) kh.d[i] = ld16(p + (i * 64 + lane) * 16);
+  } else {
+    const int nld = in.kind == KIND_Q4 ? NC : NC / 2;
+    // every register of the buffer is defined on both paths (keeps it out of scratch)
+#pragma unroll
+    for (int i = 0; i < KHalf<W>::N; ++i) kh.d[i] = (u32x4){0, 0, 0, 0};
+#pragma unroll
+    for (int m = 0; m < NC; ++m)
+      if (m < nld) kh.d[m] = ld16(p + (m * 64 + lane) * 16);
+    const uint8_t* mk = p + meta_k_off(G);
+    kh.d[NC] = ld16(mk + 16 * r);
+    kh.d[NC + 1] = ld16(mk + 256 + 16 * r);
+  }
+}
+
+template <int W>
+__device__ __forceinline__ void fetch_v(const ItemInfo& in, VHalf<W>& vh, int lane, int qg,
+                                        const Geometry& G) {
+  constexpr int KT = W / 32, NC = W / 16, NG = kHeadDim / W;
   const uint8_t* p = in.p;
   if (in.kind == KIND_BF16) {
     const int64_t vbase = (int64_t)W * kHeadDim * 2;
 #pragma unroll
-    for (int i = 0; i < 4 * TB; ++i) buf.d[i] = ld16(p + (i * 64 + lane) * 16);
-#pragma unroll
-    for (int i = 0; i < 8 * KT; ++i) buf.d[4 * TB + i] = ld16(p + vbase + (i * 64 + lane) * 16);
+    for (int i = 0; i < VHalf<W>::N; ++i)
+      vh.d[i] = i < 8 * KT ? ld16(p + vbase + (i * 64 + lane) * 16) : (u32x4){0, 0, 0, 0};
   } else {
-    constexpr int NC = W / 16;            // 16-byte code loads per area at 4 bits
-    constexpr int NG = kHeadDim / W;      // value groups (G == W)
     const int nld = in.kind == KIND_Q4 ? NC : NC / 2;
-    // every register of the buffer is defined on both paths (keeps it out of scratch)
 #pragma unroll
-    for (int i = 0; i < ItemBuf<W>::N; ++i) buf.d[i] = (u32x4){0, 0, 0, 0};
+    for (int i = 0; i < VHalf<W>::N; ++i) vh.d[i] = (u32x4){0, 0, 0, 0};
 #pragma unroll
-    for (int m = 0; m < NC; ++m) {
-      if (m < nld) {
-        buf.d[m] = ld16(p + (m * 64 + lane) * 16);
-        buf.d[NC + m] = ld16(p + G.qcodes_bytes + (m * 64 + lane) * 16);
-      }
-    }
-    const uint8_t* mk = p + meta_k_off(G);
-    buf.d[2 * NC] = ld16(mk + 16 * r);
-    buf.d[2 * NC + 1] = ld16(mk + 256 + 16 * r);
+    for (int m = 0; m < NC; ++m)
+      if (m < nld) vh.d[m] = ld16(p + G.qcodes_bytes + (m * 64 + lane) * 16);
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
       for (int vg = 0; vg < NG; ++vg) {
         const uint8_t* pm = p + meta_v_off(G) + ((kt * 4 + qg) * NG + vg) * 32;
-        buf.d[2 * NC + 2 + (kt * NG + vg) * 2] = ld16(pm);
-        buf.d[2 * NC + 3 + (kt * NG + vg) * 2] = ld16(pm + 16);
+        vh.d[NC + (kt * NG + vg) * 2] = ld16(pm);
+        vh.d[NC + 1 + (kt * NG + vg) * 2] = ld16(pm + 16);
       }
   }
 }
 
+// QK^T and the online-softmax update of one window: probabilities in p_,
+// the window's (reference, sum) pair in m_w, l_w.  The open window takes this
+// step's key (and stores it into its ring slot).
 template <int W, int NHS>
-__device__ __forceinline__ void process_item(const ItemInfo& in, ItemBuf<W>& buf, WaveState& st,
-                                             const bf16x8 (&qop)[4], const float (&qf)[NHS][8],
-                                             uint8_t* qlds, const AttnArgs& a, int b, int g,
-                                             int lane, int qg, int r, float2* mref) {
-  constexpr int TB = W / 16, KT = W / 32;
+__device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W>& kh, WaveState& st,
+                                          const bf16x8 (&qop)[4], const float (&qf)[NHS][8],
+                                          uint8_t* qlds, const AttnArgs& a, int b, int g, int lane,
+                                          int qg, int r, float (&p_)[W / 16][4], float* m_w,
+                                          float* l_w) {
+  constexpr int TB = W / 16;
   const Geometry& G = a.g;
   const int gqa = G.gqa;
   const int ntok = in.ntok;
   f32x4 acc[TB];
-  float p_[TB][4];
-  float m_w, l_w;
   if (in.kind == KIND_BF16) {
-    // buf.d[tb * 4 + kb]: K chunks; buf.d[4 * TB + kt * 8 + cb]: V chunks
-    if (ntok < W || in.open) {
+    if (in.open) {   // the token appended this step: use it from the input and store it
       const int pos = ntok - 1;
-      if (in.open) {   // the token appended this step: use it from the input and store it
-        const uint16_t* kn = a.k_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
-        const uint16_t* vn = a.v_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
-        uint8_t* pw = const_cast<uint8_t*>(in.p);
-        // keys: the lanes whose row is token pos take the new key (selects, no
-        // conditional writes into the operand registers)
-        const bool krow = r == (pos & 15);
+      const uint16_t* kn = a.k_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
+      uint8_t* pw = const_cast<uint8_t*>(in.p);
+      // keys: the lanes whose row is token pos take the new key (selects, no
+      // conditional writes into the operand registers)
+      const bool krow = r == (pos & 15);
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-          const u32x4 v = ld16(kn + 32 * kb + 8 * qg);
+      for (int kb = 0; kb < 4; ++kb) {
+        const u32x4 v = ld16(kn + 32 * kb + 8 * qg);
 #pragma unroll
-          for (int tb = 0; tb < TB; ++tb) {
-            const bool sel = krow && tb == (pos >> 4);
+        for (int tb = 0; tb < TB; ++tb) {
+          const bool sel = krow && tb == (pos >> 4);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const uint32_t old = buf.d[tb * 4 + kb][i], nv = v[i];
-              buf.d[tb * 4 + kb][i] = sel ? nv : old;
-            }
-            if (sel) *(u32x4*)(pw + ((tb * 4 + kb) * 64 + lane) * 16) = v;
+          for (int i = 0; i < 4; ++i) {
+            const uint32_t old = kh.d[tb * 4 + kb][i], nv = v[i];
+            kh.d[tb * 4 + kb][i] = sel ? nv : old;
           }
-        }
-        // values: element j of the lanes in group qp holds token pos
-        int ktp, qp, jp;
-        v_tok_pos(pos, &ktp, &qp, &jp);
-        const bool vgrp = qg == qp;
-#pragma unroll
-        for (int cb = 0; cb < 8; ++cb) {
-          const uint32_t val = vn[16 * cb + r];
-          if (vgrp) *(uint16_t*)(pw + v_elem_off(W, pos, 16 * cb + r)) = (uint16_t)val;
-#pragma unroll
-          for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const bool here = vgrp && kt == ktp && (jp >> 1) == i;
-              const uint32_t wv = buf.d[4 * TB + kt * 8 + cb][i];
-              const uint32_t lo = (wv & 0xFFFF0000u) | val, hi = (wv & 0x0000FFFFu) | (val << 16);
-              buf.d[4 * TB + kt * 8 + cb][i] = here ? ((jp & 1) ? hi : lo) : wv;
-            }
+          if (sel) *(u32x4*)(pw + ((tb * 4 + kb) * 64 + lane) * 16) = v;
         }
       }
-      // tokens past the end of a partial window contribute nothing
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const bool lo_ok = v_tok(kt, qg, 2 * i) < ntok, hi_ok = v_tok(kt, qg, 2 * i + 1) < ntok;
-          const uint32_t mask = (lo_ok ? 0x0000FFFFu : 0u) | (hi_ok ? 0xFFFF0000u : 0u);
-#pragma unroll
-          for (int cb = 0; cb < 8; ++cb) buf.d[4 * TB + kt * 8 + cb][i] &= mask;
-        }
     }
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
       acc[tb] = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
-        acc[tb] = mfma_bf16(__builtin_bit_cast(bf16x8, buf.d[tb * 4 + kb]), qop[kb], acc[tb]);
+        acc[tb] = mfma_bf16(__builtin_bit_cast(bf16x8, kh.d[tb * 4 + kb]), qop[kb], acc[tb]);
     }
-    softmax_window<TB, NHS>(acc, 0.f, ntok, G.scale_log2, qg, st, p_, &m_w, &l_w);
-#pragma unroll
-    for (int kt = 0; kt < KT; ++kt) {
-      bf16x8 pv;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) pv[j] = (__bf16)p_[2 * kt + (j >> 2)][j & 3];
-#pragma unroll
-      for (int cb = 0; cb < 8; ++cb)
-        st.o[cb] = mfma_bf16(pv, __builtin_bit_cast(bf16x8, buf.d[4 * TB + kt * 8 + cb]), st.o[cb]);
-    }
+    softmax_window<TB, NHS>(acc, 0.f, ntok, G.scale_log2, qg, st, p_, m_w, l_w);
   } else {
     // ---- quantized window: int4 or int2 codes ----
     constexpr int NC = W / 16;
-    constexpr int NG = kHeadDim / W;
     const bool is4 = in.kind == KIND_Q4;
-    uint32_t kw[4 * NC], vw[4 * NC];
+    uint32_t kw[4 * NC];
 #pragma unroll
     for (int m = 0; m < NC; ++m)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        kw[4 * m + i] = buf.d[m][i];
-        vw[4 * m + i] = buf.d[NC + m][i];
-      }
-    const u32x4 ks8 = buf.d[2 * NC], kz8 = buf.d[2 * NC + 1];
+      for (int i = 0; i < 4; ++i) kw[4 * m + i] = kh.d[m][i];
+    const u32x4 ks8 = kh.d[NC], kz8 = kh.d[NC + 1];
 
     // q*s split into exact fp16 hi + lo, written as the B operand layout
     float bias_k[NHS];
@@ -361,7 +337,75 @@ __device__ __forceinline__ void process_item(const ItemInfo& in, ItemBuf<W>& buf
         acc[tb] = mfma_f16(cv, qlo[kb], acc[tb]);
       }
     }
-    softmax_window<TB, NHS>(acc, bias, ntok, G.scale_log2, qg, st, p_, &m_w, &l_w);
+    softmax_window<TB, NHS>(acc, bias, ntok, G.scale_log2, qg, st, p_, m_w, l_w);
+  }
+}
+
+// P.V of one window into the running output, then the window's statistics.
+// The open window takes this step's value (and stores it); tokens past the end
+// of a partial window contribute nothing.
+template <int W, int NHS>
+__device__ __forceinline__ void process_v(const ItemInfo& in, VHalf<W>& vh, WaveState& st,
+                                          const float (&p_)[W / 16][4], float m_w, float l_w,
+                                          const AttnArgs& a, int b, int g, int qg, int r,
+                                          float2* mref) {
+  constexpr int KT = W / 32;
+  const Geometry& G = a.g;
+  const int gqa = G.gqa;
+  const int ntok = in.ntok;
+  if (in.kind == KIND_BF16) {
+    if (ntok < W || in.open) {
+      const int pos = ntok - 1;
+      if (in.open) {
+        const uint16_t* vn = a.v_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
+        uint8_t* pw = const_cast<uint8_t*>(in.p);
+        // values: element j of the lanes in group qp holds token pos
+        int ktp, qp, jp;
+        v_tok_pos(pos, &ktp, &qp, &jp);
+        const bool vgrp = qg == qp;
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb) {
+          const uint32_t val = vn[16 * cb + r];
+          if (vgrp) *(uint16_t*)(pw + v_elem_off(W, pos, 16 * cb + r)) = (uint16_t)val;
+#pragma unroll
+          for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const bool here = vgrp && kt == ktp && (jp >> 1) == i;
+              const uint32_t wv = vh.d[kt * 8 + cb][i];
+              const uint32_t lo = (wv & 0xFFFF0000u) | val, hi = (wv & 0x0000FFFFu) | (val << 16);
+              vh.d[kt * 8 + cb][i] = here ? ((jp & 1) ? hi : lo) : wv;
+            }
+        }
+      }
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const bool lo_ok = v_tok(kt, qg, 2 * i) < ntok, hi_ok = v_tok(kt, qg, 2 * i + 1) < ntok;
+          const uint32_t mask = (lo_ok ? 0x0000FFFFu : 0u) | (hi_ok ? 0xFFFF0000u : 0u);
+#pragma unroll
+          for (int cb = 0; cb < 8; ++cb) vh.d[kt * 8 + cb][i] &= mask;
+        }
+    }
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      bf16x8 pv;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pv[j] = (__bf16)p_[2 * kt + (j >> 2)][j & 3];
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb)
+        st.o[cb] = mfma_bf16(pv, __builtin_bit_cast(bf16x8, vh.d[kt * 8 + cb]), st.o[cb]);
+    }
+  } else {
+    constexpr int NC = W / 16;
+    constexpr int NG = kHeadDim / W;
+    const bool is4 = in.kind == KIND_Q4;
+    uint32_t vw[4 * NC];
+#pragma unroll
+    for (int m = 0; m < NC; ++m)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) vw[4 * m + i] = vh.d[m][i];
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt) {
       f16x8 pv;
@@ -380,8 +424,8 @@ __device__ __forceinline__ void process_item(const ItemInfo& in, ItemBuf<W>& buf
           uint32_t w = code_word<2>(vw, e, &ee);
           cv = unpack_codes<2>(w, ee);
         }
-        const u32x4 sv4 = buf.d[2 * NC + 2 + (kt * NG + vg) * 2];
-        const u32x4 zv4 = buf.d[2 * NC + 3 + (kt * NG + vg) * 2];
+        const u32x4 sv4 = vh.d[NC + (kt * NG + vg) * 2];
+        const u32x4 zv4 = vh.d[NC + 1 + (kt * NG + vg) * 2];
         f16x8 vv;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -403,8 +447,9 @@ __device__ __forceinline__ void process_item(const ItemInfo& in, ItemBuf<W>& buf
 
 constexpr int kAttnSmemFixed = 4 * 16 * 130 * 4;   // q*s staging per wave / end-of-split merge
 
-template <int W, int NHS, int DEPTH>
-__global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
+// MINB workgroups of four waves per compute unit: at most 512 / MINB VGPRs per lane
+template <int W, int NHS, int MINB>
+__global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   const Geometry& G = a.g;
   const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -424,9 +469,27 @@ __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
 
   // ---- one round of loads: live list, cost prefix, queries ----
   const int n_fq = counts[CNT_ITEMS];
-  for (int i = tid; i <= G.max_fq; i += kAttnThreads) {
-    s_cost[i] = icost[i];
-    s_ref[i] = iref[i];
+  {
+    // the first 1024 entries in one round of loads, the rest (large lists) after
+    int32_t lc[4], lr[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = tid + k * kAttnThreads;
+      lc[k] = i <= G.max_fq ? icost[i] : 0;
+      lr[k] = i <= G.max_fq ? iref[i] : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = tid + k * kAttnThreads;
+      if (i <= G.max_fq) {
+        s_cost[i] = lc[k];
+        s_ref[i] = lr[k];
+      }
+    }
+    for (int i = tid + 4 * kAttnThreads; i <= G.max_fq; i += kAttnThreads) {
+      s_cost[i] = icost[i];
+      s_ref[i] = iref[i];
+    }
   }
   const uint16_t* qbase = a.q + ((int64_t)b * G.H_q + (int64_t)g * gqa) * kHeadDim;
   bf16x8 qop[4];
@@ -463,21 +526,24 @@ __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
   auto start_cost = [&](int i) -> int64_t {
     return i <= n_fq ? (int64_t)s_cost[i] : base_cost + (int64_t)(i - n_fq) * cF;
   };
-  // first item whose start cost reaches the split's lower / upper cost bound
-  const int64_t lo_c = (s * total + S - 1) / S, hi_c = ((s + 1) * total + S - 1) / S;
-  __shared__ int s_range[2];
-  if (tid == 0) {
-    s_range[0] = n_all;
-    s_range[1] = n_all;
-  }
+  // The split is cut into 4 equal-cost parts, one per wave: part u = 4s + w holds
+  // the items whose start cost lies in [ceil(u total / 4S), ceil((u + 1) total / 4S)).
+  // s_range[j] = first item whose start cost reaches the j-th cut of this split.
+  __shared__ int s_range[5];
+  if (tid < 5) s_range[tid] = n_all;
   __syncthreads();
+  const int64_t S4 = 4 * (int64_t)S;
+  int64_t cut[5];
+#pragma unroll
+  for (int j = 0; j < 5; ++j) cut[j] = ((4 * (int64_t)s + j) * total + S4 - 1) / S4;
   for (int i = tid; i < n_all; i += kAttnThreads) {
     const int64_t c0 = i > 0 ? start_cost(i - 1) : -1, c1 = start_cost(i);
-    if (c1 >= lo_c && c0 < lo_c) s_range[0] = i;
-    if (c1 >= hi_c && c0 < hi_c) s_range[1] = i;
+#pragma unroll
+    for (int j = 0; j < 5; ++j)
+      if (c1 >= cut[j] && c0 < cut[j]) s_range[j] = i;
   }
   __syncthreads();
-  const int first = s_range[0], last = s_range[1];
+  const int first = s_range[wave], last = s_range[wave + 1];
 
   WaveState st;
   st.m = -INFINITY;
@@ -515,36 +581,18 @@ __global__ __launch_bounds__(kAttnThreads) void k_attend(AttnArgs a) {
     return in;
   };
 
-  // ---- window loop: the next window's loads are in flight while one computes ----
-  if constexpr (DEPTH == 2) {
-    ItemBuf<W> A, B;
-    ItemInfo ia, ib;
-    int it = first + wave;
-    if (it < last) {
-      ia = info(it);
-      fetch_item<W>(ia, A, lane, qg, r, G);
-    }
-    for (; it < last; it += 8) {
-      const bool has_b = it + 4 < last;
-      if (has_b) {
-        ib = info(it + 4);
-        fetch_item<W>(ib, B, lane, qg, r, G);
-      }
-      process_item<W, NHS>(ia, A, st, qop, qf, qlds, a, b, g, lane, qg, r, mref);
-      if (!has_b) break;
-      if (it + 8 < last) {
-        ia = info(it + 8);
-        fetch_item<W>(ia, A, lane, qg, r, G);
-      }
-      process_item<W, NHS>(ib, B, st, qop, qf, qlds, a, b, g, lane, qg, r, mref);
-    }
-  } else {
-    ItemBuf<W> A;
-    for (int it = first + wave; it < last; it += 4) {
-      const ItemInfo ia = info(it);
-      fetch_item<W>(ia, A, lane, qg, r, G);
-      process_item<W, NHS>(ia, A, st, qop, qf, qlds, a, b, g, lane, qg, r, mref);
-    }
+  // ---- window loop: this wave's contiguous run of windows ----
+  constexpr int TB = W / 16;
+  KHalf<W> KA;
+  VHalf<W> V;
+  float p_[TB][4];
+  float m_w, l_w;
+  for (int it = first; it < last; ++it) {
+    const ItemInfo ia = info(it);
+    fetch_k<W>(ia, KA, lane, r, G);
+    fetch_v<W>(ia, V, lane, qg, G);
+    process_k<W, NHS>(ia, KA, st, qop, qf, qlds, a, b, g, lane, qg, r, p_, &m_w, &l_w);
+    process_v<W, NHS>(ia, V, st, p_, m_w, l_w, a, b, g, qg, r, mref);
   }
 
   // ---- merge the 4 waves of this split in LDS, write the split partial ----
@@ -699,7 +747,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
   int P = 1;
   while (2 * P * nh <= kMergeThreads) P *= 2;
   const int C = (S + P - 1) / P;
-  constexpr int kMaxC = 32;   // C <= S * H_q / 128 + 1 <= 17 (S * H_q <= 2048)
+  constexpr int kMaxC = 36;   // C <= S * H_q / 128 + 1 <= 33 (S * H_q <= 4096)
   {
     const int h = tid / P, j = tid % P;
     const bool hv = h < nh;
@@ -782,15 +830,15 @@ hipError_t launch_attend(const AttnArgs& a, hipStream_t st) {
   auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, dim3(kAttnThreads), smem, st, a);
   };
-  const bool dbl = a.g.prefetch_depth == 2;
+  // pipelined window loop where the extra K buffer keeps two waves per SIMD
   if (a.g.W == 32) {
-    if (nhs == 1) dbl ? go(k_attend<32, 1, 2>) : go(k_attend<32, 1, 1>);
-    else if (nhs == 2) dbl ? go(k_attend<32, 2, 2>) : go(k_attend<32, 2, 1>);
-    else dbl ? go(k_attend<32, 4, 2>) : go(k_attend<32, 4, 1>);
+    if (nhs == 1) go(k_attend<32, 1, 2>);
+    else if (nhs == 2) go(k_attend<32, 2, 2>);
+    else go(k_attend<32, 4, 2>);
   } else {
-    if (nhs == 1) go(k_attend<64, 1, 1>);
-    else if (nhs == 2) go(k_attend<64, 2, 1>);
-    else go(k_attend<64, 4, 1>);
+    if (nhs == 1) go(k_attend<64, 1, 2>);
+    else if (nhs == 2) go(k_attend<64, 2, 2>);
+    else go(k_attend<64, 4, 2>);
   }
   return hipGetLastError();
 }

@@ -85,7 +85,6 @@ struct Geometry {
   int64_t qrec_bytes;   // one KV head of a quantized record
   int64_t qslot_bytes;  // H_kv * qrec_bytes
   int32_t cost_bf16, cost_q4, cost_q2;   // split balancing weights per item
-  int32_t prefetch_depth;                 // attention: windows in flight per wave (1 or 2)
 };
 
 struct UnitLayout {

@@ -120,8 +120,8 @@ qevict_status check_config(const qevict_config* c) {
     return fail(QEVICT_ERR_INVALID_ARG, "softmax_scale");
   if (c->num_splits < 0 || c->num_splits > 256)
     return fail(QEVICT_ERR_INVALID_ARG, "num_splits must be in [0, 256]");
-  if (c->num_splits * c->num_q_heads > 2048)
-    return fail(QEVICT_ERR_UNSUPPORTED, "num_splits x num_q_heads must be <= 2048");
+  if (c->num_splits * c->num_q_heads > 4096)
+    return fail(QEVICT_ERR_UNSUPPORTED, "num_splits x num_q_heads must be <= 4096");
   const int W = c->window_tokens;
   const int nr = ceil_div(c->recent_tokens, W) + ceil_div(c->retier_interval, W) + 2;
   if (c->capacity_full + c->capacity_quant + nr > kMaxCand)
@@ -160,7 +160,7 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
     ns = ns < 1 ? 1 : (ns > 64 ? 64 : ns);
     int per_split = ceil_div(g->max_items, ns);
     if (per_split < 2) ns = ceil_div(g->max_items, 2);
-    if (ns * g->H_q > 2048) ns = 2048 / g->H_q;   // split statistics of the merge live in LDS
+    if (ns * g->H_q > 4096) ns = 4096 / g->H_q;   // split statistics one merge thread folds
   }
   g->n_split = ns;
   g->out_bf16 = c->out_dtype == QEVICT_OUT_BF16;
@@ -172,13 +172,20 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   g->qcodes_bytes = (int64_t)g->W * g->d * g->qbits_max / 8;
   g->qrec_bytes = 2 * g->qcodes_bytes + 4 * g->d + (int64_t)g->W * (g->d / g->G) * 4;
   g->qslot_bytes = g->qrec_bytes * g->H_kv;
-  // split-balancing weights (per 32 tokens): bf16 windows are byte heavy,
-  // quantized windows carry extra expansion work per byte
+  // split-balancing weights (per 32 tokens): a bf16 window moves twice the bytes
+  // of an int4 one, which carries the code expansion instead; measured per-wave
+  // times are close, so the weights are nearly equal
   g->cost_bf16 = 16 * (g->W / 32);
-  g->cost_q4 = 8 * (g->W / 32);
-  g->cost_q2 = 7 * (g->W / 32);
-  const char* pf = getenv("QEVICT_PREFETCH");
-  g->prefetch_depth = (pf && atoi(pf) == 2 && g->W == 32) ? 2 : 1;
+  g->cost_q4 = 16 * (g->W / 32);
+  g->cost_q2 = 14 * (g->W / 32);
+  if (const char* cw = getenv("QEVICT_COSTS")) {   // tuning: "bf16,int4,int2" per 32 tokens
+    int f = 0, q4 = 0, q2 = 0;
+    if (sscanf(cw, "%d,%d,%d", &f, &q4, &q2) == 3 && f > 0 && q4 > 0 && q2 > 0) {
+      g->cost_bf16 = f * (g->W / 32);
+      g->cost_q4 = q4 * (g->W / 32);
+      g->cost_q2 = q2 * (g->W / 32);
+    }
+  }
 
   int64_t off = 0;
   auto take = [&](int64_t bytes) {
@@ -231,7 +238,9 @@ uint8_t* unit_base(qevict_cache* c, int layer, int seq) {
 // layer for the next routing of that layer.
 hipError_t join_layer(qevict_cache* c, int layer) {
   if (!c->rstream || !c->route_pending[layer]) return hipSuccess;
-  hipError_t e = hipStreamWaitEvent(c->stream, c->route_ev[layer], 0);
+  // routing already finished: nothing to wait for (keeps wait packets off the stream)
+  hipError_t e = hipEventQuery(c->route_ev[layer]);
+  if (e == hipErrorNotReady) e = hipStreamWaitEvent(c->stream, c->route_ev[layer], 0);
   if (e == hipSuccess) c->route_pending[layer] = 0;
   return e;
 }
