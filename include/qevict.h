@@ -73,11 +73,14 @@ enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT =
 #define QEVICT_FLAG_NO_PROMOTION 0x1u  /* one-way Full -> Quantized -> Evicted policy (App. K)      */
 #define QEVICT_FLAG_DEBUG_MASSES 0x2u  /* keep per-head window masses of the last step              */
 /* Routing work (re-rank, quantize, promote) of qevict_retier runs on a stream
- * the library owns, after that layer's latest decode_attend, so the routing of
- * one layer overlaps the attention of others.  Every later call that touches
- * the same layer (decode_attend, prefill, manual moves, state queries) is
- * ordered after it; qevict_join_routing orders the cache stream after the
- * routing of every layer. */
+ * the library owns, so the routing of one layer overlaps the attention of the
+ * layers after it.  Requests are launched in batches (up to num_layers / 4,
+ * at most 8, layers per batch): a batch runs after everything enqueued on the
+ * cache's stream before it was launched, which includes each of its layers'
+ * latest decode_attend.  Every later call that touches a layer (decode_attend,
+ * prefill, retier, manual moves, state queries) launches that layer's queued
+ * request if needed and orders the cache's stream after its routing;
+ * qevict_join_routing does so for every layer. */
 #define QEVICT_FLAG_ASYNC_ROUTING 0x4u
 
 typedef struct {
@@ -205,8 +208,9 @@ qevict_status qevict_profile_read(qevict_cache *c, int32_t kernel, double *total
  * queries, outputs, scores; synchronous). */
 qevict_status qevict_last_attend_bytes(qevict_cache *c, int32_t layer, int64_t *bytes);
 
-/* Make the cache's stream wait (on the device, no host synchronisation) for
- * all routing work enqueued so far.  A no-op without QEVICT_FLAG_ASYNC_ROUTING.
+/* Launch every queued routing request and make the cache's stream wait (on
+ * the device, no host synchronisation) for all routing work requested so far.
+ * A no-op without QEVICT_FLAG_ASYNC_ROUTING.
  * After it, synchronising the cache's stream also covers every retier call. */
 qevict_status qevict_join_routing(qevict_cache *c);
 

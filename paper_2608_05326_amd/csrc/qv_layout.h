@@ -64,12 +64,16 @@ enum : int32_t { SRC_FSLOT = 0, SRC_RING = 1, SRC_PROMPT = 2, SRC_QSLOT = 3 };
 // quantization that reads a bf16 slot with the promotion / admission that
 // writes the same slot (index of the other list's entry, or -1)
 constexpr int kQEntry = 6;
+// spare bf16 pool slots beyond K_f (fewer when the owner tables would not fit)
+constexpr int kSpareFull = 8;
 
 struct Geometry {
   int32_t B, H_q, H_kv, gqa, d, W, G;
   int32_t bits_cfg;     // 4, 2 or 42
   int32_t qbits_max;    // 4 or 2: code area size of a record
   int32_t K_f, K_q, n_qslots;
+  int32_t n_fslots;     // bf16 pool slots: K_f plus spares (a promotion then takes a slot
+                        // that was free before the event, not one vacated in it)
   int32_t NR, NS;       // ring slots, sink slots
   int32_t sink, recent;
   int32_t nwc;          // window capacity per unit

@@ -313,11 +313,11 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   __shared__ int32_t sinfo[kMaxCand];
   __shared__ int32_t sa[kMaxCand];
   __shared__ int32_t sown[2 * kMaxCand];      // slot owners: Full slots, then quantized slots
-  __shared__ int32_t tmp[4 * 64 + 16];
+  __shared__ int32_t tmp[5 * 64 + 16];
   __shared__ int32_t sstat[ST_N];
   int32_t* sb = (int32_t*)skey;               // after the sort: two more int arrays
   int32_t* fown = sown;
-  int32_t* qown = sown + G.K_f;
+  int32_t* qown = sown + G.n_fslots;
 
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
   int8_t* tier = (int8_t*)(ub + a.L.tier);
@@ -404,7 +404,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       my_bits[k] = 0;
     }
   }
-  for (int i = tid; i < G.K_f; i += NT) fown[i] = fowner[i];
+  for (int i = tid; i < G.n_fslots; i += NT) fown[i] = fowner[i];
   for (int i = tid; i < G.n_qslots; i += NT) qown[i] = qowner[i];
   if (a.prefill) {   // every prompt window (partial ones too) starts at its initial score
     for (int w = tid; w < a.n_init; w += NT) {
@@ -500,35 +500,40 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     const bool needQ = nt == T_QUANT && old != T_QUANT && led == L_NONE;
     my_req[k] = (needF ? 1 : 0) | (needQ ? 2 : 0);
     my_nb[k] = G.bits_cfg == 42 ? (rq < half_q ? 4 : 2) : G.bits_cfg;
-    if (old == T_FULL && nt != T_FULL) fown[my_fs[k]] = -1;
+    if (old == T_FULL && nt != T_FULL) fown[my_fs[k]] = -2;   // vacated in this event
     if (nt == T_EVICTED && led != L_NONE) qown[my_qs[k]] = -1;
   }
   __syncthreads();
 
-  // ---- free lists and request ranks: four flag prefix counts in one pass ----
+  // ---- free lists and request ranks: five flag prefix counts in one pass ----
+  // The bf16 free list holds the slots free before this event first, then the
+  // slots vacated in it, so promotions use a vacated slot (and must wait for
+  // the quantization reading it) only once the spare slots are used up.
   int my_rankF[PER], my_rankQ[PER];
   int nfreeF, nfreeQ, nreqF, nreqQ;
   {
-    bool fl[4][PER];
-    int rk[4][PER], tots[4];
+    bool fl[5][PER];
+    int rk[5][PER], tots[5];
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int i = tid + k * NT;
-      fl[0][k] = i < G.K_f && fown[i] < 0;
+      fl[0][k] = i < G.n_fslots && fown[i] == -1;
       fl[1][k] = i < G.n_qslots && qown[i] < 0;
       fl[2][k] = (my_req[k] & 1) != 0;
       fl[3][k] = (my_req[k] & 2) != 0;
+      fl[4][k] = i < G.n_fslots && fown[i] == -2;
     }
-    flag_scan<4>(fl, rk, tots, tmp);
-    nfreeF = tots[0];
+    flag_scan<5>(fl, rk, tots, tmp);
+    nfreeF = tots[0] + tots[4];
     nfreeQ = tots[1];
     nreqF = tots[2];
     nreqQ = tots[3];
-    // free slot lists, ascending slot order (sinfo / sb are free now)
+    // free slot lists, ascending slot order within each group (sinfo / sb are free now)
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int i = tid + k * NT;
       if (fl[0][k]) sinfo[rk[0][k]] = i;
+      if (fl[4][k]) sinfo[tots[0] + rk[4][k]] = i;
       if (fl[1][k]) sb[rk[1][k]] = i;
       my_rankF[k] = rk[2][k];
       my_rankQ[k] = rk[3][k];
@@ -537,7 +542,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   int32_t* freeF = sinfo;
   int32_t* freeQ = sb;
   int32_t* sdep = sa;   // per bf16 slot: quantization entry reading it in this event, or -1
-  for (int i = tid; i < G.K_f; i += NT) sdep[i] = -1;
+  for (int i = tid; i < G.n_fslots; i += NT) sdep[i] = -1;
   __syncthreads();
 
   // ---- apply: new slots, ledger states, work lists ----
@@ -634,7 +639,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     e[5] = dep;
     if (dep >= 0) qlist[dep * kQEntry + 5] = rk;
   }
-  for (int i = tid; i < G.K_f; i += NT) fowner[i] = fown[i];
+  for (int i = tid; i < G.n_fslots; i += NT) fowner[i] = fown[i] < 0 ? -1 : fown[i];
   for (int i = tid; i < G.n_qslots; i += NT) qowner[i] = qown[i];
 
   // ---- rebuild the live list (window order) with its cost prefix ----
@@ -727,7 +732,7 @@ __global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
     slot = qslot[w];
   } else {
     int fs = -1;
-    for (int i = 0; i < G.K_f && fs < 0; ++i)
+    for (int i = 0; i < G.n_fslots && fs < 0; ++i)
       if (fowner[i] < 0) fs = i;
     if (fs < 0) { set_error(counts, ERR_POOL); return; }
     fowner[fs] = w;
@@ -767,7 +772,7 @@ __global__ void k_init_units(Geometry G, UnitLayout L, uint8_t* base, int n_unit
       ((int32_t*)(ub + L.qslot))[w] = -1;
       ((float*)(ub + L.score))[w] = 0.f;
     }
-    for (int i = threadIdx.x; i < G.K_f; i += blockDim.x) ((int32_t*)(ub + L.fowner))[i] = -1;
+    for (int i = threadIdx.x; i < G.n_fslots; i += blockDim.x) ((int32_t*)(ub + L.fowner))[i] = -1;
     for (int i = threadIdx.x; i < G.n_qslots; i += blockDim.x) ((int32_t*)(ub + L.qowner))[i] = -1;
     for (int i = threadIdx.x; i < CNT_N; i += blockDim.x) ((int32_t*)(ub + L.counts))[i] = 0;
     for (int i = threadIdx.x; i < ST_N; i += blockDim.x) ((int32_t*)(ub + L.stats))[i] = 0;

@@ -3,6 +3,7 @@
 // the synchronous inspection calls.  No device memory is ever allocated here.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -66,6 +67,13 @@ struct TimedLaunch {
   hipEvent_t start, stop;
 };
 
+struct RouteRequest {
+  int layer;
+  RetierArgs ra;
+  MigrateArgs ma;
+  int max_quant, max_promote;
+};
+
 }  // namespace
 
 struct qevict_cache {
@@ -75,9 +83,18 @@ struct qevict_cache {
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
   hipStream_t stream = nullptr;
-  hipStream_t rstream = nullptr;            // routing stream (QEVICT_FLAG_ASYNC_ROUTING)
-  std::vector<hipEvent_t> attn_ev, route_ev;   // per layer: latest attention / routing done
-  std::vector<char> route_pending;          // routing enqueued that the cache stream has not joined
+  // Asynchronous routing (QEVICT_FLAG_ASYNC_ROUTING): routing requests are queued
+  // and launched on rstream in batches of route_batch layers, behind one wait
+  // for the cache stream; a cross-stream wait costs the host far more than a
+  // launch, so it is paid once per batch.
+  hipStream_t rstream = nullptr;
+  hipEvent_t main_ev = nullptr;             // cache stream position a batch waits for
+  std::vector<hipEvent_t> batch_ev;         // ring: end of a launched batch
+  int next_batch_ev = 0;
+  int route_batch = 1;
+  std::vector<RouteRequest> route_queue;    // requested, not launched yet
+  std::vector<char> route_queued;           // per layer: in route_queue
+  std::vector<int> route_ev_idx;            // per layer: batch_ev of launched, unjoined routing, or -1
   std::vector<LayerState> layers;
   bool poisoned = false;
   bool profiling = false;
@@ -146,6 +163,14 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   g->K_f = c->capacity_full;
   g->K_q = c->capacity_quant;
   g->n_qslots = c->capacity_quant + c->capacity_full;
+  {
+    // the re-rank kernel keeps both owner tables (n_fslots + n_qslots entries)
+    // in 2 * kMaxCand LDS words and scans each over at most kMaxCand entries
+    int spare = kSpareFull;
+    spare = std::min(spare, 2 * kMaxCand - 2 * g->K_f - g->K_q);
+    spare = std::min(spare, kMaxCand - g->K_f);
+    g->n_fslots = g->K_f + std::max(spare, 0);
+  }
   g->NR = ceil_div(c->recent_tokens, g->W) + ceil_div(c->retier_interval, g->W) + 2;
   g->NS = ceil_div(c->sink_tokens, g->W);
   g->sink = c->sink_tokens;
@@ -193,7 +218,7 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
     off = align256(off + bytes);
     return o;
   };
-  L->fpool = take((int64_t)g->K_f * g->fslot_bytes);
+  L->fpool = take((int64_t)g->n_fslots * g->fslot_bytes);
   L->ring = take((int64_t)g->NR * g->fslot_bytes);
   L->sinkp = take((int64_t)g->NS * g->fslot_bytes);   // directly after the ring (zeroed together)
   L->qpool = take((int64_t)g->n_qslots * g->qslot_bytes);
@@ -203,7 +228,7 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   L->fslot = take(4LL * g->nwc);
   L->qslot = take(4LL * g->nwc);
   L->score = take(4LL * g->nwc);
-  L->fowner = take(4LL * (g->K_f + 1));
+  L->fowner = take(4LL * (g->n_fslots + 1));
   L->qowner = take(4LL * (g->n_qslots + 1));
   L->item_win = take(4LL * (g->max_fq + 1));
   L->item_ref = take(4LL * (g->max_fq + 1));
@@ -231,32 +256,6 @@ qevict_status hip_fail(hipError_t e, const char* what) {
 
 uint8_t* unit_base(qevict_cache* c, int layer, int seq) {
   return c->ws + kHeaderBytes + ((int64_t)layer * c->g.B + seq) * c->L.unit_bytes;
-}
-
-// Asynchronous routing: order the cache stream after the routing work of a
-// layer (a device-side wait), and publish the cache stream's progress on a
-// layer for the next routing of that layer.
-hipError_t join_layer(qevict_cache* c, int layer) {
-  if (!c->rstream || !c->route_pending[layer]) return hipSuccess;
-  // routing already finished: nothing to wait for (keeps wait packets off the stream)
-  hipError_t e = hipEventQuery(c->route_ev[layer]);
-  if (e == hipErrorNotReady) e = hipStreamWaitEvent(c->stream, c->route_ev[layer], 0);
-  if (e == hipSuccess) c->route_pending[layer] = 0;
-  return e;
-}
-hipError_t mark_layer(qevict_cache* c, int layer) {
-  return c->rstream ? hipEventRecord(c->attn_ev[layer], c->stream) : hipSuccess;
-}
-
-// Validates the handle and the layer; every later use of the layer on the
-// cache stream is ordered after its pending routing work.
-qevict_status check_handle(qevict_cache* c, int layer) {
-  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
-  if (c->poisoned) return fail(QEVICT_ERR_BAD_STATE, "cache is in an error state; destroy it");
-  if (layer < 0 || layer >= c->cfg.num_layers)
-    return fail(QEVICT_ERR_INVALID_ARG, "layer %d out of range", layer);
-  if (hipError_t e = join_layer(c, layer)) return hip_fail(e, "joining the routing stream");
-  return QEVICT_OK;
 }
 
 // ---- kernel timing ----
@@ -297,6 +296,56 @@ hipError_t timed(qevict_cache* c, int kernel, hipStream_t st, F&& launch) {
   (void)hipEventRecord(b, st);
   c->pending.push_back({kernel, a, b});
   return e;
+}
+
+// Asynchronous routing: launch the queued routing requests on the routing
+// stream, after everything enqueued on the cache stream so far.
+hipError_t flush_routing(qevict_cache* c) {
+  if (c->route_queue.empty()) return hipSuccess;
+  hipStream_t rs = c->rstream;
+  hipError_t e = hipEventRecord(c->main_ev, c->stream);
+  if (e == hipSuccess) e = hipStreamWaitEvent(rs, c->main_ev, 0);
+  for (const RouteRequest& r : c->route_queue) {
+    if (e == hipSuccess) e = timed(c, 2, rs, [&] { return launch_retier(r.ra, rs); });
+    if (e == hipSuccess)
+      e = timed(c, 3, rs, [&] { return launch_migrate(r.ma, r.max_quant, r.max_promote, rs); });
+  }
+  const int slot = c->next_batch_ev;
+  c->next_batch_ev = (slot + 1) % (int)c->batch_ev.size();
+  if (e == hipSuccess) e = hipEventRecord(c->batch_ev[slot], rs);
+  for (const RouteRequest& r : c->route_queue) {
+    c->route_queued[r.layer] = 0;
+    c->route_ev_idx[r.layer] = slot;
+  }
+  c->route_queue.clear();
+  return e;
+}
+
+// Order the cache stream after the routing work of a layer (launching it first
+// if it is still queued).  A finished batch needs no device-side wait.  An
+// event of the ring may have been recorded again by a later batch; waiting on
+// it then waits for more routing work than needed, never less.
+hipError_t join_layer(qevict_cache* c, int layer) {
+  if (!c->rstream) return hipSuccess;
+  hipError_t e = hipSuccess;
+  if (c->route_queued[layer] && (e = flush_routing(c)) != hipSuccess) return e;
+  const int idx = c->route_ev_idx[layer];
+  if (idx < 0) return hipSuccess;
+  e = hipEventQuery(c->batch_ev[idx]);
+  if (e == hipErrorNotReady) e = hipStreamWaitEvent(c->stream, c->batch_ev[idx], 0);
+  if (e == hipSuccess) c->route_ev_idx[layer] = -1;
+  return e;
+}
+
+// Validates the handle and the layer; every later use of the layer on the
+// cache stream is ordered after its pending routing work.
+qevict_status check_handle(qevict_cache* c, int layer) {
+  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
+  if (c->poisoned) return fail(QEVICT_ERR_BAD_STATE, "cache is in an error state; destroy it");
+  if (layer < 0 || layer >= c->cfg.num_layers)
+    return fail(QEVICT_ERR_INVALID_ARG, "layer %d out of range", layer);
+  if (hipError_t e = join_layer(c, layer)) return hip_fail(e, "joining the routing stream");
+  return QEVICT_OK;
 }
 
 qevict_status device_errors(qevict_cache* c, int layer) {
@@ -409,13 +458,15 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
   hipError_t e = hipSuccess;
   if (cfg->flags & QEVICT_FLAG_ASYNC_ROUTING) {
     e = hipStreamCreateWithFlags(&c->rstream, hipStreamNonBlocking);   // default priority
-    c->attn_ev.assign(cfg->num_layers, nullptr);
-    c->route_ev.assign(cfg->num_layers, nullptr);
-    c->route_pending.assign(cfg->num_layers, 0);
-    for (int l = 0; l < cfg->num_layers && e == hipSuccess; ++l) {
-      e = hipEventCreateWithFlags(&c->attn_ev[l], hipEventDisableTiming);
-      if (e == hipSuccess) e = hipEventCreateWithFlags(&c->route_ev[l], hipEventDisableTiming);
-    }
+    const int nl = cfg->num_layers;
+    c->route_batch = nl / 4 < 1 ? 1 : (nl / 4 > 8 ? 8 : nl / 4);
+    c->route_queued.assign(nl, 0);
+    c->route_ev_idx.assign(nl, -1);
+    c->batch_ev.assign(nl + 1, nullptr);
+    // both streams run on this device: a device-scope release is enough
+    const unsigned fl = hipEventDisableTiming | hipEventDisableSystemFence;
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&c->main_ev, fl);
+    for (int i = 0; i <= nl && e == hipSuccess; ++i) e = hipEventCreateWithFlags(&c->batch_ev[i], fl);
     if (e != hipSuccess) {
       qevict_cache_destroy(c);
       return hip_fail(e, "creating the routing stream");
@@ -433,10 +484,12 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
 
 qevict_status qevict_cache_destroy(qevict_cache* c) {
   if (!c) return QEVICT_OK;
-  if (c->rstream) (void)hipStreamSynchronize(c->rstream);
-  for (auto e : c->attn_ev)
-    if (e) (void)hipEventDestroy(e);
-  for (auto e : c->route_ev)
+  if (c->rstream) {
+    (void)flush_routing(c);
+    (void)hipStreamSynchronize(c->rstream);
+  }
+  if (c->main_ev) (void)hipEventDestroy(c->main_ev);
+  for (auto e : c->batch_ev)
     if (e) (void)hipEventDestroy(e);
   if (c->rstream) (void)hipStreamDestroy(c->rstream);
   for (auto& t : c->pending) {
@@ -483,7 +536,6 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
   if (e == hipSuccess) e = timed(c, 2, c->stream, [&] { return launch_retier(ra, c->stream); });
   MigrateArgs ma{gg, L, base, k, v, prompt_len};
   if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_migrate(ma, g.K_q, g.K_f, c->stream); });
-  if (e == hipSuccess) e = mark_layer(c, layer);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   ls.T = prompt_len;
   ls.routed_end = n_hist;
@@ -526,7 +578,6 @@ qevict_status qevict_decode_attend(qevict_cache* c, int32_t layer, const uint16_
   }
   if (e == hipSuccess) e = timed(c, 0, c->stream, [&] { return launch_attend(a, c->stream); });
   if (e == hipSuccess) e = timed(c, 1, c->stream, [&] { return launch_merge(a, c->stream); });
-  if (e == hipSuccess) e = mark_layer(c, layer);
   if (e != hipSuccess) return hip_fail(e, "decode_attend launch");
   ls.T = T;
   return QEVICT_OK;
@@ -547,15 +598,16 @@ qevict_status qevict_retier(qevict_cache* c, int32_t layer, qevict_retier_stats*
   RetierArgs ra{gg, L, base, 0, a0, a1 > a0 ? a1 : a0, nullptr, 0};
   MigrateArgs ma{gg, L, base, nullptr, nullptr, 0};
   const int max_q = g.K_q < g.max_fq ? g.K_q : g.max_fq;
-  // asynchronous routing: run on the routing stream after this layer's latest attention
-  hipStream_t rs = c->rstream ? c->rstream : c->stream;
   hipError_t e = hipSuccess;
-  if (c->rstream) e = hipStreamWaitEvent(rs, c->attn_ev[layer], 0);
-  if (e == hipSuccess) e = timed(c, 2, rs, [&] { return launch_retier(ra, rs); });
-  if (e == hipSuccess) e = timed(c, 3, rs, [&] { return launch_migrate(ma, max_q, g.K_f, rs); });
-  if (e == hipSuccess && c->rstream) {
-    e = hipEventRecord(c->route_ev[layer], rs);
-    if (e == hipSuccess) c->route_pending[layer] = 1;
+  if (c->rstream) {
+    // asynchronous routing: queue the request; a batch is launched on the
+    // routing stream once it is full (or the layer is needed again)
+    c->route_queue.push_back(RouteRequest{layer, ra, ma, max_q, g.K_f});
+    c->route_queued[layer] = 1;
+    if (stats || (int)c->route_queue.size() >= c->route_batch) e = flush_routing(c);
+  } else {
+    e = timed(c, 2, c->stream, [&] { return launch_retier(ra, c->stream); });
+    if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_migrate(ma, max_q, g.K_f, c->stream); });
   }
   if (e != hipSuccess) return hip_fail(e, "retier launch");
   if (a1 > a0) ls.routed_end = a1;
@@ -631,7 +683,6 @@ static qevict_status manual_move(qevict_cache* c, int layer, int seq, int window
   MigrateArgs ma{one, L, unit_base(c, layer, seq), nullptr, nullptr, 0};
   e = launch_manual_move(ra, seq, window, to_quant, c->stream);
   if (e == hipSuccess) e = launch_migrate(ma, 1, 1, c->stream);
-  if (e == hipSuccess) e = mark_layer(c, layer);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(e, "manual move");
   return device_errors(c, layer);
@@ -774,7 +825,6 @@ qevict_status qevict_debug_shift_keys(qevict_cache* c, int32_t layer, int32_t se
     if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
     if (e != hipSuccess) return hip_fail(e, "shift_keys write");
   }
-  if (hipError_t e2 = mark_layer(c, layer)) return hip_fail(e2, "shift_keys");
   return QEVICT_OK;
 }
 
@@ -817,6 +867,8 @@ qevict_status qevict_profile_read(qevict_cache* c, int32_t kernel, double* total
 
 qevict_status qevict_join_routing(qevict_cache* c) {
   if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
+  if (!c->rstream) return QEVICT_OK;
+  if (hipError_t e = flush_routing(c)) return hip_fail(e, "launching queued routing");
   for (int l = 0; l < c->cfg.num_layers; ++l)
     if (hipError_t e = join_layer(c, l)) return hip_fail(e, "joining the routing stream");
   return QEVICT_OK;

@@ -290,15 +290,18 @@ def test_async_routing_lockstep(name):
         ls.close()
 
 
-def test_async_routing_interleaved_layers_match_sync():
+@pytest.mark.parametrize("n_layers", [4, 9])
+def test_async_routing_interleaved_layers_match_sync(n_layers):
     """Several layers stepped back to back with no host synchronisation: the
     routing of each layer overlaps the attention of the others and every
-    output and final state equals the single-stream run bit for bit."""
+    output and final state equals the single-stream run bit for bit.  With 9
+    layers routing requests are launched two layers at a time, so the last
+    layer's request is still queued when its state is read."""
     import paper_2608_05326_amd as qv
     from tests.gpu_harness import gpu_config, to_dev_bf16
     torch = _torch()
     wl = syn.get_workload("c2s")
-    n_layers, steps = 4, 10
+    steps = 10
 
     def run(flags):
         c = qv.Cache(gpu_config(wl, n_layers, flags))
@@ -318,10 +321,11 @@ def test_async_routing_interleaved_layers_match_sync():
                     c.decode_attend(l, *ins[l][t], out)
                     c.retier(l)
                     outs.append(out)
+            last = c.get_state(n_layers - 1, 0)
             c.join_routing()
             torch.cuda.synchronize()
             states = [c.get_state(l, 0) for l in range(n_layers)]
-            return [o.cpu() for o in outs], states
+            return [o.cpu() for o in outs], states + [last]
         finally:
             c.close()
 
