@@ -94,7 +94,7 @@ typedef struct {
   int32_t group_size;        /* G; this build requires G == W (keys: one group per channel   */
                              /*  per window; values: W/... groups of G channels per token)    */
   int32_t quant_bits;        /* 4, 2 or QEVICT_BITS_MIXED_4_2                                */
-  int32_t sink_tokens;       /* protected sink prefix |S|                                    */
+  int32_t sink_tokens;       /* protected sink prefix |S| (at most 64 windows)               */
   int32_t recent_tokens;     /* protected recent region: a window is routed only once it is  */
                              /* complete and older than this many latest tokens              */
   int32_t max_context;       /* largest sequence length the cache will hold                  */

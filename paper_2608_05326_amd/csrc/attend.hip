@@ -458,8 +458,7 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   uint8_t* qlds = smem + wave * 8192;   // [hi/lo][kb][lane] x 16 B
-  int32_t* s_cost = (int32_t*)(smem + kAttnSmemFixed);   // live-list cost prefix
-  int32_t* s_ref = s_cost + G.max_fq + 1;                // live-list entries
+  int32_t* s_ref = (int32_t*)(smem + kAttnSmemFixed);   // live-list entries
 
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
   const int32_t* counts = (const int32_t*)(ub + a.L.counts);
@@ -467,29 +466,17 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   const int32_t* iref = (const int32_t*)(ub + a.L.item_ref);
   float2* mref = (float2*)(ub + a.L.mref);
 
-  // ---- one round of loads: live list, cost prefix, queries ----
-  const int n_fq = counts[CNT_ITEMS];
-  {
-    // the first 1024 entries in one round of loads, the rest (large lists) after
-    int32_t lc[4], lr[4];
+  // ---- one round of loads: list length and cost, the first 1024 entries of the
+  // live list with their cost prefixes (and the previous entry's), queries ----
+  const int n_fq = __builtin_amdgcn_readfirstlane(counts[CNT_ITEMS]);
+  const int base_cost = __builtin_amdgcn_readfirstlane(counts[CNT_COST]);
+  int32_t lc[4], lp[4], lr[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int i = tid + k * kAttnThreads;
-      lc[k] = i <= G.max_fq ? icost[i] : 0;
-      lr[k] = i <= G.max_fq ? iref[i] : 0;
-    }
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int i = tid + k * kAttnThreads;
-      if (i <= G.max_fq) {
-        s_cost[i] = lc[k];
-        s_ref[i] = lr[k];
-      }
-    }
-    for (int i = tid + 4 * kAttnThreads; i <= G.max_fq; i += kAttnThreads) {
-      s_cost[i] = icost[i];
-      s_ref[i] = iref[i];
-    }
+  for (int k = 0; k < 4; ++k) {
+    const int i = tid + k * kAttnThreads;
+    lc[k] = i <= G.max_fq ? icost[i] : 0;
+    lp[k] = i >= 1 && i <= G.max_fq + 1 ? icost[i - 1] : -1;
+    lr[k] = i < G.max_fq ? iref[i] : 0;
   }
   const uint16_t* qbase = a.q + ((int64_t)b * G.H_q + (int64_t)g * gqa) * kHeadDim;
   bf16x8 qop[4];
@@ -514,34 +501,57 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   // zero this lane's q*s operand slots (padded heads keep zeros)
 #pragma unroll
   for (int i = 0; i < 8; ++i) *(u32x4*)(qlds + (i * 64 + lane) * 16) = (u32x4){0, 0, 0, 0};
-  __syncthreads();
 
-  // ---- this split's item range (equal estimated cost), found in one parallel pass ----
+  // ---- this split's item range (equal estimated cost) ----
+  // Items: the live list, then the recent-region and sink windows (cost cF each).
+  // The split is cut into 4 equal-cost parts, one per wave: part u = 4s + w holds
+  // the items whose start cost lies in [ceil(u total / 4S), ceil((u + 1) total / 4S)).
+  // s_range[j] = first item whose start cost reaches the j-th cut of this split:
+  // start costs increase strictly, so the item with start(i - 1) < cut <= start(i)
+  // is unique, and cuts beyond the last item's start are set by that item.
+  // Costs are small integers (at most 32 per window, under 2^13 windows), so every
+  // prefix and cut fits in 32 bits; the cuts are uniform (scalar unit).
   const int n_extra = a.n_ring + a.n_sink_items;
   const int n_all = n_fq + n_extra;
   const int cF = G.cost_bf16;
-  const int64_t base_cost = s_cost[n_fq];
-  const int64_t total = base_cost + (int64_t)n_extra * cF;
+  const int total = base_cost + n_extra * cF;
   const int S = G.n_split;
-  auto start_cost = [&](int i) -> int64_t {
-    return i <= n_fq ? (int64_t)s_cost[i] : base_cost + (int64_t)(i - n_fq) * cF;
-  };
-  // The split is cut into 4 equal-cost parts, one per wave: part u = 4s + w holds
-  // the items whose start cost lies in [ceil(u total / 4S), ceil((u + 1) total / 4S)).
-  // s_range[j] = first item whose start cost reaches the j-th cut of this split.
   __shared__ int s_range[5];
-  if (tid < 5) s_range[tid] = n_all;
-  __syncthreads();
-  const int64_t S4 = 4 * (int64_t)S;
-  int64_t cut[5];
+  const uint32_t S4 = 4u * (uint32_t)S;
+  int cut[5];
 #pragma unroll
-  for (int j = 0; j < 5; ++j) cut[j] = ((4 * (int64_t)s + j) * total + S4 - 1) / S4;
-  for (int i = tid; i < n_all; i += kAttnThreads) {
-    const int64_t c0 = i > 0 ? start_cost(i - 1) : -1, c1 = start_cost(i);
+  for (int j = 0; j < 5; ++j) cut[j] = (int)(((4u * (uint32_t)s + j) * (uint32_t)total + S4 - 1) / S4);
+  auto place = [&](int i, int c0, int c1) {
+    // bit j: cut j falls in (c0, c1] (or, for the last item, beyond it)
+    uint32_t m = 0, m_end = 0;
 #pragma unroll
-    for (int j = 0; j < 5; ++j)
-      if (c1 >= cut[j] && c0 < cut[j]) s_range[j] = i;
+    for (int j = 0; j < 5; ++j) {
+      m |= (c1 >= cut[j] && c0 < cut[j]) ? 1u << j : 0u;
+      m_end |= cut[j] > c1 ? 1u << j : 0u;
+    }
+    if (i == n_all - 1) {
+      for (uint32_t e = m_end; e; e &= e - 1) s_range[__builtin_ctz(e)] = n_all;
+    }
+    for (; m; m &= m - 1) s_range[__builtin_ctz(m)] = i;
+  };
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (k * kAttnThreads >= n_all) break;   // uniform
+    const int i = tid + k * kAttnThreads;
+    if (i < n_fq) s_ref[i] = lr[k];
+    if (i < n_all) {
+      const int c1 = i <= n_fq ? lc[k] : base_cost + (i - n_fq) * cF;
+      const int c0 = i == 0 ? -1 : (i - 1 <= n_fq ? lp[k] : base_cost + (i - 1 - n_fq) * cF);
+      place(i, c0, c1);
+    }
   }
+  for (int i = tid + 4 * kAttnThreads; i < n_all; i += kAttnThreads) {   // long lists
+    if (i < n_fq) s_ref[i] = iref[i];
+    const int c1 = i <= n_fq ? icost[i] : base_cost + (i - n_fq) * cF;
+    const int c0 = i - 1 <= n_fq ? icost[i - 1] : base_cost + (i - 1 - n_fq) * cF;
+    place(i, c0, c1);
+  }
+  if (n_all == 0 && tid < 5) s_range[tid] = 0;
   __syncthreads();
   const int first = s_range[wave], last = s_range[wave + 1];
 
@@ -826,7 +836,7 @@ namespace qv {
 hipError_t launch_attend(const AttnArgs& a, hipStream_t st) {
   dim3 grid(a.g.n_split, a.g.H_kv, a.g.B);
   const int nhs = (a.g.gqa + 3) / 4;
-  const size_t smem = kAttnSmemFixed + 8 * (size_t)(a.g.max_fq + 1);
+  const size_t smem = kAttnSmemFixed + 4 * (size_t)(a.g.max_fq + 1);
   auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, dim3(kAttnThreads), smem, st, a);
   };

@@ -51,8 +51,9 @@ enum : int32_t { KIND_BF16 = 0, KIND_Q4 = 1, KIND_Q2 = 2 };
 // (dormant for a Full item, active for a Quantized one) with its bit width:
 // aux = qslot | (bits << 28)
 // per-unit counters
+// (CNT_COST: summed split-balancing cost of the live list, item_cost[CNT_ITEMS])
 enum : int32_t { CNT_ITEMS = 0, CNT_QUANT = 1, CNT_PROMOTE = 2, CNT_ERROR = 3, CNT_BYTES_LO = 4,
-                 CNT_N = 16 };
+                 CNT_COST = 5, CNT_N = 16 };
 // device error bits
 enum : int32_t { ERR_NONFINITE = 1, ERR_POOL = 2, ERR_RANGE = 4, ERR_CAND = 8 };
 // stats slots (same order as qevict_retier_stats)
@@ -66,6 +67,8 @@ enum : int32_t { SRC_FSLOT = 0, SRC_RING = 1, SRC_PROMPT = 2, SRC_QSLOT = 3 };
 constexpr int kQEntry = 6;
 // spare bf16 pool slots beyond K_f (fewer when the owner tables would not fit)
 constexpr int kSpareFull = 8;
+// sink windows per sequence (keeps the attention split costs in 32 bits)
+constexpr int kMaxSinkWindows = 64;
 
 struct Geometry {
   int32_t B, H_q, H_kv, gqa, d, W, G;

@@ -43,7 +43,7 @@ __device__ __forceinline__ int wave_inclusive_scan(int x) {
 // Exclusive prefix sums of NV arrays at once (each buf[v][0..n[v]), n <= kMaxCand),
 // in place; tot[v] receives each total.  One pair of barriers for all arrays.
 template <int NV>
-__device__ void block_scan_multi(int32_t* const (&buf)[NV], const int (&n)[NV], int (&tot)[NV],
+__device__ __forceinline__ void block_scan_multi(int32_t* const (&buf)[NV], const int (&n)[NV], int (&tot)[NV],
                                  int32_t* tmp /* >= NV * 16 */) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   constexpr int PER = kMaxCand / kRetierThreads;
@@ -85,39 +85,44 @@ __device__ void block_scan_multi(int32_t* const (&buf)[NV], const int (&n)[NV], 
 
 // Exclusive prefix counts of NV flag arrays held in registers in strided
 // layout (element c = tid + k * kRetierThreads, k < PER): rank[v][k] = set flags
-// before element c, tot[v] = set flags in all.  Wave ballots, then one wave per
-// array scans the 64 (slice, wave) counts; two barriers.
+// before element c, tot[v] = set flags in all.  Only slices k < kmax (uniform)
+// may hold set flags; the others are skipped.  Wave ballots, then one wave per
+// array scans the (slice, wave) counts; two barriers.
 template <int NV>
 __device__ __forceinline__ void flag_scan(const bool (&f)[NV][kMaxCand / kRetierThreads],
                                           int (&rank)[NV][kMaxCand / kRetierThreads], int (&tot)[NV],
-                                          int32_t* tmp /* >= NV * 64 + NV */) {
+                                          int32_t* tmp /* >= NV * 64 + NV */, int kmax) {
   constexpr int PER = kMaxCand / kRetierThreads;
   constexpr int NW = kRetierThreads / 64;
   static_assert(PER * NW == 64, "one wave scans the slice counts");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
 #pragma unroll
-  for (int v = 0; v < NV; ++v)
+  for (int k = 0; k < PER; ++k) {
+    if (k >= kmax) break;
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
+    for (int v = 0; v < NV; ++v) {
       const uint64_t bl = __builtin_amdgcn_ballot_w64(f[v][k]);
       rank[v][k] = __popcll(bl & below);
       if (lane == 0) tmp[v * 64 + k * NW + wave] = __popcll(bl);
     }
+  }
   __syncthreads();
   if (wave < NV) {
-    const int x = tmp[wave * 64 + lane];
+    const int x = lane < kmax * NW ? tmp[wave * 64 + lane] : 0;
     const int inc = wave_inclusive_scan(x);
     tmp[wave * 64 + lane] = inc - x;
     if (lane == 63) tmp[NV * 64 + wave] = inc;
   }
   __syncthreads();
 #pragma unroll
-  for (int v = 0; v < NV; ++v) {
+  for (int k = 0; k < PER; ++k) {
+    if (k >= kmax) break;
 #pragma unroll
-    for (int k = 0; k < PER; ++k) rank[v][k] += tmp[v * 64 + k * NW + wave];
-    tot[v] = tmp[NV * 64 + v];
+    for (int v = 0; v < NV; ++v) rank[v][k] += tmp[v * 64 + k * NW + wave];
   }
+#pragma unroll
+  for (int v = 0; v < NV; ++v) tot[v] = tmp[NV * 64 + v];
 }
 
 // Value of `x` held by lane (lane ^ J), J in {1, 2, 4, 8, 16, 32}; VALU only.
@@ -340,9 +345,13 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
 
   if (tid < ST_N) sstat[tid] = 0;
   // ---- one round of loads: the live list carries every candidate's state.
-  // Entries are read up to the list's capacity without waiting for its length.
-  int spec_ref[PER], spec_aux[PER], spec_win[PER];
-  float spec_sc[PER];
+  // Entries are read up to the list's capacity without waiting for its length;
+  // the slot owner tables and the scores of the windows entering the pool (a
+  // range known from the arguments) are read in the same round.
+  const int n_aged = a.aged_w1 - a.aged_w0;
+  const int ko = (max(G.n_fslots, G.n_qslots) + NT - 1) / NT;   // owner-table slices
+  int spec_ref[PER], spec_aux[PER], spec_win[PER], spec_fo[PER], spec_qo[PER];
+  float spec_sc[PER], spec_aged[PER];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
@@ -351,6 +360,11 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     spec_aux[k] = ok ? iaux[c] : -1;
     spec_win[k] = ok ? iwin[c] : -1;
     spec_sc[k] = ok ? iscore[c] : 0.f;
+    spec_fo[k] = k < ko && c < G.n_fslots ? fowner[c] : -1;
+    spec_qo[k] = k < ko && c < G.n_qslots ? qowner[c] : -1;
+    const int w = a.aged_w0 + c;
+    spec_aged[k] = c >= n_aged ? 0.f
+                 : (a.prefill ? a.init_scores[(int64_t)b * a.n_init + w] : score[w]);
   }
   // scores of the windows that follow the routed range (the next steps' recent
   // region; at most NR of them have started)
@@ -361,12 +375,30 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     else ring_sc = w < G.nwc ? score[w] : 0.f;
   }
   const int n_fq = a.prefill ? 0 : counts[CNT_ITEMS];
-  const int n_aged = a.aged_w1 - a.aged_w0;
   const int n_cand = n_fq + n_aged;
   if (n_cand > kMaxCand) {
     if (tid == 0) set_error(counts, ERR_CAND);
     return;
   }
+  const int kc = (n_cand + NT - 1) / NT;   // candidate slices in use
+  // owner tables and entering scores to LDS (sinfo is free until tiering)
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int c = tid + k * NT;
+    if (k < ko) {
+      if (c < G.n_fslots) fown[c] = spec_fo[k];
+      if (c < G.n_qslots) qown[c] = spec_qo[k];
+    }
+    if (c < n_aged) sinfo[c] = __float_as_int(spec_aged[k]);
+  }
+  if (a.prefill) {   // every prompt window (partial ones too) starts at its initial score
+    for (int w = tid; w < a.n_init; w += NT) {
+      const float v = a.init_scores[(int64_t)b * a.n_init + w];
+      if (!__builtin_isfinite(v)) set_error(counts, ERR_NONFINITE);
+      score[w] = v;
+    }
+  }
+  __syncthreads();
 
   int my_w[PER], my_old[PER], my_led[PER], my_fs[PER], my_qs[PER], my_bits[PER];
   float my_sc[PER];
@@ -374,7 +406,8 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
     my_w[k] = -1;
-    if (c >= n_cand) continue;
+    my_sc[k] = 0.f;
+    if (k >= kc || c >= n_cand) continue;
     if (c < n_fq) {
       const int32_t ref = spec_ref[k], aux = spec_aux[k];
       const int kind = ref >> 28, slot = ref & 0x0FFFFFFF;
@@ -394,35 +427,19 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
         my_bits[k] = kind == KIND_Q4 ? 4 : 2;
       }
     } else {
-      const int w = a.aged_w0 + (c - n_fq);
-      my_w[k] = w;
-      my_sc[k] = a.prefill ? a.init_scores[(int64_t)b * a.n_init + w] : score[w];
+      my_w[k] = a.aged_w0 + (c - n_fq);
+      my_sc[k] = __int_as_float(sinfo[c - n_fq]);
       my_old[k] = T_OPEN;   // aged, entering the pool
       my_fs[k] = -1;
       my_qs[k] = -1;
       my_led[k] = L_NONE;
       my_bits[k] = 0;
     }
-  }
-  for (int i = tid; i < G.n_fslots; i += NT) fown[i] = fowner[i];
-  for (int i = tid; i < G.n_qslots; i += NT) qown[i] = qowner[i];
-  if (a.prefill) {   // every prompt window (partial ones too) starts at its initial score
-    for (int w = tid; w < a.n_init; w += NT) {
-      const float v = a.init_scores[(int64_t)b * a.n_init + w];
-      if (!__builtin_isfinite(v)) set_error(counts, ERR_NONFINITE);
-      score[w] = v;
-    }
+    if (!__builtin_isfinite(my_sc[k])) set_error(counts, ERR_NONFINITE);
+    skey[c] = rank_key(my_sc[k], (uint32_t)c);
   }
   int n_pow = 1;
   while (n_pow < n_cand) n_pow <<= 1;
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int c = tid + k * NT;
-    if (c < n_cand) {
-      if (!__builtin_isfinite(my_sc[k])) set_error(counts, ERR_NONFINITE);
-      skey[c] = rank_key(my_sc[k], (uint32_t)c);
-    }
-  }
   __syncthreads();
 
   // ---- sort ----
@@ -491,7 +508,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     const int c = tid + k * NT;
     my_req[k] = 0;
     my_nt[k] = T_EVICTED;
-    if (c >= n_cand) continue;
+    if (k >= kc || c >= n_cand) continue;
     const int info = sinfo[c];
     const int nt = info & 0xFF, rq = info >> 8;
     const int old = my_old[k], led = my_led[k];
@@ -514,16 +531,18 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   {
     bool fl[5][PER];
     int rk[5][PER], tots[5];
+    const int km = max(kc, ko);
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int i = tid + k * NT;
-      fl[0][k] = i < G.n_fslots && fown[i] == -1;
-      fl[1][k] = i < G.n_qslots && qown[i] < 0;
+      const int fo = k < ko && i < G.n_fslots ? fown[i] : 0;
+      fl[0][k] = fo == -1;
+      fl[1][k] = k < ko && i < G.n_qslots && qown[i] < 0;
       fl[2][k] = (my_req[k] & 1) != 0;
       fl[3][k] = (my_req[k] & 2) != 0;
-      fl[4][k] = i < G.n_fslots && fown[i] == -2;
+      fl[4][k] = fo == -2;
     }
-    flag_scan<5>(fl, rk, tots, tmp);
+    flag_scan<5>(fl, rk, tots, tmp, km);
     nfreeF = tots[0] + tots[4];
     nfreeQ = tots[1];
     nreqF = tots[2];
@@ -531,6 +550,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     // free slot lists, ascending slot order within each group (sinfo / sb are free now)
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
+      if (k >= km) break;
       const int i = tid + k * NT;
       if (fl[0][k]) sinfo[rk[0][k]] = i;
       if (fl[4][k]) sinfo[tots[0] + rk[4][k]] = i;
@@ -553,7 +573,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     const int c = tid + k * NT;
     my_aux[k] = -1;
     my_pl[k] = -1;
-    if (c >= n_cand) continue;
+    if (k >= kc || c >= n_cand) continue;
     const int w = my_w[k];
     const int old = my_old[k], nt = my_nt[k];
     int led = my_led[k];
@@ -625,6 +645,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   // this event runs after that quantization (paired through the dep fields)
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
+    if (k >= kc) break;
     if (my_pl[k] < 0) continue;
     const int rk = my_pl[k], w = my_w[k], fs = my_fs[k];
     int32_t* e = plist + rk * kQEntry;
@@ -650,15 +671,16 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int c = tid + k * NT;
-      const bool in = c < n_cand;
+      const bool in = k < kc && c < n_cand;
       fl[0][k] = in && my_nt[k] == T_FULL;
       fl[1][k] = in && my_nt[k] == T_QUANT && my_bits[k] == 4;
       fl[2][k] = in && my_nt[k] == T_QUANT && my_bits[k] != 4;
     }
-    flag_scan<3>(fl, rk, tots, tmp);
+    flag_scan<3>(fl, rk, tots, tmp, kc);
     n_items = tots[0] + tots[1] + tots[2];
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
+      if (k >= kc) break;
       if (!(fl[0][k] || fl[1][k] || fl[2][k])) continue;
       const int pos = rk[0][k] + rk[1][k] + rk[2][k];
       const int kind = fl[0][k] ? KIND_BF16 : (fl[1][k] ? KIND_Q4 : KIND_Q2);
@@ -670,7 +692,11 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       iscore[pos] = my_sc[k];
       icost[pos] = rk[0][k] * G.cost_bf16 + rk[1][k] * G.cost_q4 + rk[2][k] * G.cost_q2;
     }
-    if (tid == 0) icost[n_items] = tots[0] * G.cost_bf16 + tots[1] * G.cost_q4 + tots[2] * G.cost_q2;
+    if (tid == 0) {
+      const int total = tots[0] * G.cost_bf16 + tots[1] * G.cost_q4 + tots[2] * G.cost_q2;
+      icost[n_items] = total;
+      counts[CNT_COST] = total;
+    }
   }
   // list positions after the live windows hold the recent-region windows of the
   // next steps: their scores as they stand (windows not started yet: 0)
@@ -758,6 +784,7 @@ __global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
     run += item_cost(G, iref[i] >> 28);
   }
   icost[n] = run;
+  counts[CNT_COST] = run;
 }
 
 // State initialisation of every unit block (grid-stride over units).

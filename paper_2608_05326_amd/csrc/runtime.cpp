@@ -128,6 +128,8 @@ qevict_status check_config(const qevict_config* c) {
     return fail(QEVICT_ERR_INVALID_ARG, "negative sink, recent or capacity");
   if (c->max_context <= c->sink_tokens)
     return fail(QEVICT_ERR_INVALID_ARG, "max_context must exceed sink_tokens");
+  if (ceil_div(c->sink_tokens, c->window_tokens) > kMaxSinkWindows)
+    return fail(QEVICT_ERR_UNSUPPORTED, "sink_tokens must span at most %d windows", kMaxSinkWindows);
   if (c->retier_interval < 1) return fail(QEVICT_ERR_INVALID_ARG, "retier_interval must be >= 1");
   if (c->out_dtype != QEVICT_OUT_F32 && c->out_dtype != QEVICT_OUT_BF16)
     return fail(QEVICT_ERR_INVALID_ARG, "out_dtype");
@@ -203,15 +205,6 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   g->cost_bf16 = 16 * (g->W / 32);
   g->cost_q4 = 16 * (g->W / 32);
   g->cost_q2 = 14 * (g->W / 32);
-  if (const char* cw = getenv("QEVICT_COSTS")) {   // tuning: "bf16,int4,int2" per 32 tokens
-    int f = 0, q4 = 0, q2 = 0;
-    if (sscanf(cw, "%d,%d,%d", &f, &q4, &q2) == 3 && f > 0 && q4 > 0 && q2 > 0) {
-      g->cost_bf16 = f * (g->W / 32);
-      g->cost_q4 = q4 * (g->W / 32);
-      g->cost_q2 = q2 * (g->W / 32);
-    }
-  }
-
   int64_t off = 0;
   auto take = [&](int64_t bytes) {
     int64_t o = off;
