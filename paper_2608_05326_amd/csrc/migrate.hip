@@ -84,6 +84,19 @@ __device__ __forceinline__ uint32_t quant_code(float x, const QParams& p, int nm
   return p.s == 0.f ? 0u : (uint32_t)c;
 }
 
+// A (window, KV head) migration is split into four parts, one per workgroup
+// pass: part = 2 area + h, area 0 the keys and 1 the values, h the channel half
+// [64 h, 64 h + 64).  Key groups (one channel), value groups (one token, G
+// channels, G = W), bf16 chunks and code words each fall in exactly one part:
+// key entry / chunk e has channel block 32 (e & 3), value entry / chunk e has
+// channel block 16 (e & 7), and an int2 word's two entries share their half.
+constexpr int kParts = 4;
+__device__ __forceinline__ int entry_half(int area, int e) { return area == 0 ? (e & 3) >> 1 : (e & 7) >> 2; }
+// bf16 chunk (= code entry) index of local chunk cl of channel half h of an area
+__device__ __forceinline__ int part_chunk(int area, int h, int cl) {
+  return area == 0 ? (cl >> 1) * 4 + 2 * h + (cl & 1) : (cl >> 2) * 8 + 4 * h + (cl & 3);
+}
+
 // Codes of one (window, KV head), packed: thread (area, block m, lane L, word
 // comp) forms word 4m + comp of lane L; entry e of a word holds its 8 codes at
 // bits 16 o + NB (4 e' + i) for code j = 2i + o.  Consecutive threads write
@@ -92,14 +105,16 @@ constexpr int kMigrateThreads = 1024;
 
 template <int W, int NB>
 __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk, const uint16_t* sv,
-                                           const QParams* pk, const QParams* pv, uint8_t* rec, int tid) {
+                                           const QParams* pk, const QParams* pv, uint8_t* rec, int tid,
+                                           int part) {
   constexpr int NBLK = W * NB / 64;
   constexpr int PER = 4 / NB;
   constexpr int NG = kHeadDim / W;
   constexpr int nmax = (1 << NB) - 1;
-  for (int tk = tid; tk < 2 * NBLK * 256; tk += kMigrateThreads) {
-    const int comp = tk & 3, L = (tk >> 2) & 63, m = (tk >> 8) % NBLK;
-    const int area = tk / (NBLK * 256);   // uniform per wave
+  const int area = part >> 1, h = part & 1;
+  for (int tk = tid; tk < NBLK * 256; tk += kMigrateThreads) {
+    const int comp = tk & 3, L = (tk >> 2) & 63, m = tk >> 8;
+    if (entry_half(area, (m * 4 + comp) * PER) != h) continue;
     const int q = L >> 4, r = L & 15;
     uint32_t wd = 0;
 #pragma unroll
@@ -128,39 +143,39 @@ __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk
   }
 }
 
-// Load one KV head of a window into LDS in natural [t][c] layout.
+// Load one part of one KV head of a window into LDS in natural [t][c] layout.
 template <int W>
 __device__ __forceinline__ void load_window(const MigrateArgs& a, uint8_t* ub, int b, int g, int w, int src_kind,
-                            int src_idx, uint16_t* sk, uint16_t* sv) {
+                            int src_idx, uint16_t* sk, uint16_t* sv, int part) {
   const Geometry& G = a.g;
   const int tid = threadIdx.x;
+  const int area = part >> 1, h = part & 1;
+  uint16_t* dst = area == 0 ? sk : sv;
   if (src_kind == SRC_PROMPT) {
     const int64_t row0 = ((int64_t)b * G.H_kv + g) * a.src_T + G.sink + (int64_t)w * W;
-    const u32x4* k4 = (const u32x4*)(a.src_k + row0 * kHeadDim);
-    const u32x4* v4 = (const u32x4*)(a.src_v + row0 * kHeadDim);
-    for (int i = tid; i < W * kHeadDim / 8; i += blockDim.x) {
-      ((u32x4*)sk)[i] = k4[i];
-      ((u32x4*)sv)[i] = v4[i];
+    const uint16_t* src = (area == 0 ? a.src_k : a.src_v) + row0 * kHeadDim;
+    for (int i = tid; i < W * 8; i += blockDim.x) {
+      const int t = i >> 3, c = 64 * h + 8 * (i & 7);
+      *(u32x4*)(dst + t * kHeadDim + c) = *(const u32x4*)(src + t * kHeadDim + c);
     }
   } else {
     const uint8_t* p = ub + (src_kind == SRC_FSLOT ? a.L.fpool : a.L.ring) +
-                       (int64_t)src_idx * G.fslot_bytes + g * G.fhead_bytes;
-    const uint8_t* pv = p + (int64_t)W * kHeadDim * 2;
+                       (int64_t)src_idx * G.fslot_bytes + g * G.fhead_bytes +
+                       (area == 0 ? 0 : (int64_t)W * kHeadDim * 2);
     // K chunk (tb, kb), lane 16q + r: token 16 tb + r, channels 32 kb + 8 q .. + 7
     // V chunk (kt, cb), lane 16q + r: tokens tok(kt, q, 0..7), channel 16 cb + r
+    for (int i = tid; i < (W / 8) * 64; i += blockDim.x) {
+      const int chunk = part_chunk(area, h, i >> 6), L = i & 63, q = L >> 4, r = L & 15;
+      const u32x4 x = *(const u32x4*)(p + ((int64_t)chunk * 64 + L) * 16);
+      if (area == 0) {
+        *(u32x4*)(sk + (16 * (chunk >> 2) + r) * kHeadDim + 32 * (chunk & 3) + 8 * q) = x;
+      } else {
+        const int kt = chunk >> 3, c = 16 * (chunk & 7) + r;
+        const uint32_t vw[4] = {x[0], x[1], x[2], x[3]};
 #pragma unroll
-    for (int i0 = 0; i0 < W * kHeadDim / 8; i0 += kMigrateThreads) {
-      const int i = i0 + tid;
-      if (W * kHeadDim / 8 < kMigrateThreads && i >= W * kHeadDim / 8) break;
-      const int chunk = i >> 6, L = i & 63, q = L >> 4, r = L & 15;
-      const u32x4 kx = *(const u32x4*)(p + (int64_t)i * 16);
-      const u32x4 vx = *(const u32x4*)(pv + (int64_t)i * 16);
-      *(u32x4*)(sk + (16 * (chunk >> 2) + r) * kHeadDim + 32 * (chunk & 3) + 8 * q) = kx;
-      const int kt = chunk >> 3, c = 16 * (chunk & 7) + r;
-      const uint32_t vw[4] = {vx[0], vx[1], vx[2], vx[3]};
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        sv[v_tok(kt, q, j) * kHeadDim + c] = (uint16_t)(vw[j >> 1] >> (16 * (j & 1)));
+        for (int j = 0; j < 8; ++j)
+          sv[v_tok(kt, q, j) * kHeadDim + c] = (uint16_t)(vw[j >> 1] >> (16 * (j & 1)));
+      }
     }
   }
 }
@@ -170,6 +185,17 @@ __device__ __forceinline__ void load_window(const MigrateArgs& a, uint8_t* ub, i
 // (3) one thread per (code block, lane): the codes of its entries straight into
 // the packed 16-byte block (entry e's 8 codes at bits 16 o + b (4 e' + i)).
 // Keys form groups per channel (W tokens), values per token (G = W channels).
+// One work-list entry (win, src_kind, src_idx, dst, bits, dep), held in registers.
+struct WorkEntry {
+  int32_t v[kQEntry];
+};
+__device__ __forceinline__ WorkEntry load_entry(const int32_t* list, int e) {
+  WorkEntry x;
+#pragma unroll
+  for (int i = 0; i < kQEntry; ++i) x.v[i] = list[e * kQEntry + i];
+  return x;
+}
+
 template <int W>
 struct QuantLds {
   uint16_t sk[W * kHeadDim];
@@ -180,24 +206,30 @@ struct QuantLds {
 
 template <int W>
 __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub, int b, int g,
-                                              const int32_t* ent, QuantLds<W>& sm, int32_t* counts) {
+                                              const WorkEntry& ent, QuantLds<W>& sm, int32_t* counts,
+                                              int part) {
   const Geometry& G = a.g;
   constexpr int NG = kHeadDim / W;             // value groups per token
+  constexpr int NGH = 64 / W;                  // value groups per token in one channel half
   const int tid = threadIdx.x;
-  const int w = ent[0], src_kind = ent[1], src_idx = ent[2], dst = ent[3], nb = ent[4];
+  const int area = part >> 1, h = part & 1;
+  const int w = ent.v[0], src_kind = ent.v[1], src_idx = ent.v[2], dst = ent.v[3], nb = ent.v[4];
   uint16_t* sk = sm.sk;
   uint16_t* sv = sm.sv;
-  load_window<W>(a, ub, b, g, w, src_kind, src_idx, sk, sv);
+  load_window<W>(a, ub, b, g, w, src_kind, src_idx, sk, sv, part);
   __syncthreads();
   uint8_t* rec = ub + a.L.qpool + (int64_t)dst * G.qslot_bytes + g * G.qrec_bytes;
-  // ---- group parameters: threads 0..127 key channels, then value groups ----
-  for (int grp = tid; grp < kHeadDim + W * NG; grp += blockDim.x) {
+  // ---- group parameters: one thread per group of this part (64 groups) ----
+  if (tid < 64) {
     float x[W];
-    if (grp < kHeadDim) {
+    int c = 0, t = 0, vg = 0;
+    if (area == 0) {
+      c = 64 * h + tid;
 #pragma unroll
-      for (int t = 0; t < W; ++t) x[t] = bf16_to_f32(sk[t * kHeadDim + grp]);
+      for (int tt = 0; tt < W; ++tt) x[tt] = bf16_to_f32(sk[tt * kHeadDim + c]);
     } else {
-      const int gi = grp - kHeadDim, t = gi / NG, vg = gi % NG;
+      t = tid / NGH;
+      vg = NGH * h + tid % NGH;
       const u32x4* row = (const u32x4*)(sv + t * kHeadDim + vg * W);
 #pragma unroll
       for (int k = 0; k < W / 8; ++k) {
@@ -209,20 +241,19 @@ __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub,
     }
     float lo = x[0], hi = x[0];
 #pragma unroll
-    for (int t = 1; t < W; ++t) {
-      lo = fminf(lo, x[t]);
-      hi = fmaxf(hi, x[t]);
+    for (int i = 1; i < W; ++i) {
+      lo = fminf(lo, x[i]);
+      hi = fmaxf(hi, x[i]);
     }
     uint16_t zb = 0, sb = 0;
     const QParams p = group_params(lo, hi, nb, &zb, &sb, counts);
-    if (grp < kHeadDim) {
-      sm.pk[grp] = p;
+    if (area == 0) {
+      sm.pk[c] = p;
       uint16_t* mk = (uint16_t*)(rec + meta_k_off(G));
-      mk[grp] = sb;
-      mk[kHeadDim + grp] = zb;
+      mk[c] = sb;
+      mk[kHeadDim + c] = zb;
     } else {
-      const int gi = grp - kHeadDim, t = gi / NG, vg = gi % NG;
-      sm.pv[gi] = p;
+      sm.pv[t * NG + vg] = p;
       uint16_t* mv = (uint16_t*)(rec + meta_v_elem(G, t, vg));
       mv[0] = sb;
       mv[8] = zb;
@@ -230,8 +261,8 @@ __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub,
   }
   __syncthreads();
   // ---- codes, packed ----
-  if (nb == 4) pack_codes<W, 4>(G, sk, sv, sm.pk, sm.pv, rec, tid);
-  else pack_codes<W, 2>(G, sk, sv, sm.pk, sm.pv, rec, tid);
+  if (nb == 4) pack_codes<W, 4>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
+  else pack_codes<W, 2>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
 }
 
 // 8 bf16 values z_j + s_j c_j (exact in float64, one rounding) packed for a 16-byte store
@@ -262,12 +293,14 @@ __device__ __forceinline__ u32x4 dequant8(uint32_t wd, int ee, u32x4 s8, u32x4 z
 // (entry, lane) position of the bf16 slot.
 template <int W, int NB>
 __device__ __forceinline__ void promote_from_record(const Geometry& G, const uint8_t* rec,
-                                                    uint8_t* dp, int tid) {
+                                                    uint8_t* dp, int tid, int part) {
   constexpr int E = W / 4;                          // entries per area
   constexpr int PER = 4 / NB;
   const int ng = kHeadDim / G.G;
-  for (int tk = tid; tk < 2 * E * 64; tk += kMigrateThreads) {
-    const int L = tk & 63, ei = (tk >> 6) % E, area = tk / (E * 64);   // area uniform per wave
+  const int area = part >> 1, h = part & 1;
+  for (int tk = tid; tk < E * 64; tk += kMigrateThreads) {
+    const int L = tk & 63, ei = tk >> 6;
+    if (entry_half(area, ei) != h) continue;
     const int q = L >> 4, r = L & 15;
     const int word = ei / PER;
     const uint32_t wd = *(const uint32_t*)(rec + area * G.qcodes_bytes +
@@ -291,39 +324,49 @@ __device__ __forceinline__ void promote_from_record(const Geometry& G, const uin
 
 template <int W>
 __device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, int b, int g,
-                                             const int32_t* ent) {
+                                             const WorkEntry& ent, int part) {
   const Geometry& G = a.g;
   const int tid = threadIdx.x;
-  const int w = ent[0], src_kind = ent[1], src_idx = ent[2], dst = ent[3], nb = ent[4];
+  const int area = part >> 1, h = part & 1;
+  const int w = ent.v[0], src_kind = ent.v[1], src_idx = ent.v[2], dst = ent.v[3], nb = ent.v[4];
   uint8_t* dp = ub + a.L.fpool + (int64_t)dst * G.fslot_bytes + g * G.fhead_bytes;
+  const int64_t area_off = area == 0 ? 0 : (int64_t)W * kHeadDim * 2;
   if (src_kind == SRC_RING) {
-    const u32x4* sp = (const u32x4*)(ub + a.L.ring + (int64_t)src_idx * G.fslot_bytes +
-                                     g * G.fhead_bytes);
-    for (int i = tid; i < G.fhead_bytes / 16; i += blockDim.x) ((u32x4*)dp)[i] = sp[i];
+    const uint8_t* sp = ub + a.L.ring + (int64_t)src_idx * G.fslot_bytes + g * G.fhead_bytes;
+    for (int i = tid; i < (W / 8) * 64; i += blockDim.x) {
+      const int64_t off = area_off + ((int64_t)part_chunk(area, h, i >> 6) * 64 + (i & 63)) * 16;
+      *(u32x4*)(dp + off) = *(const u32x4*)(sp + off);
+    }
   } else if (src_kind == SRC_PROMPT) {
     const int64_t row0 = ((int64_t)b * G.H_kv + g) * a.src_T + G.sink + (int64_t)w * W;
-    const uint16_t* ks = a.src_k + row0 * kHeadDim;
-    const uint16_t* vs = a.src_v + row0 * kHeadDim;
-    for (int i = tid; i < W * kHeadDim / 8; i += blockDim.x) {
-      const int t = i / 16, c = (i % 16) * 8;
-      *(u32x4*)(dp + k_elem_off(t, c)) = *(const u32x4*)(ks + t * kHeadDim + c);
-    }
-    for (int i = tid; i < W * kHeadDim; i += blockDim.x) {
-      const int t = i >> 7, c = i & 127;
-      *(uint16_t*)(dp + v_elem_off(W, t, c)) = vs[t * kHeadDim + c];
+    if (area == 0) {
+      const uint16_t* ks = a.src_k + row0 * kHeadDim;
+      for (int i = tid; i < W * 8; i += blockDim.x) {
+        const int t = i >> 3, c = 64 * h + 8 * (i & 7);
+        *(u32x4*)(dp + k_elem_off(t, c)) = *(const u32x4*)(ks + t * kHeadDim + c);
+      }
+    } else {
+      const uint16_t* vs = a.src_v + row0 * kHeadDim;
+      for (int i = tid; i < W * 64; i += blockDim.x) {
+        const int t = i >> 6, c = 64 * h + (i & 63);
+        *(uint16_t*)(dp + v_elem_off(W, t, c)) = vs[t * kHeadDim + c];
+      }
     }
   } else {   // SRC_QSLOT
     const uint8_t* rec = ub + a.L.qpool + (int64_t)src_idx * G.qslot_bytes + g * G.qrec_bytes;
-    if (nb == 4) promote_from_record<W, 4>(G, rec, dp, tid);
-    else promote_from_record<W, 2>(G, rec, dp, tid);
+    if (nb == 4) promote_from_record<W, 4>(G, rec, dp, tid, part);
+    else promote_from_record<W, 2>(G, rec, dp, tid, part);
   }
 }
 
-// Migrations of one routing event, one (window, KV head) task per workgroup
-// pass: quantizations first, then promotions / admissions.  A promotion whose
-// bf16 slot is being vacated by a quantization in the same event (dep >= 0)
-// runs in that quantization's workgroup right after it, so the slot is read
-// before it is overwritten without any ordering across workgroups.
+// Migrations of one routing event, one (window, KV head, part) task per
+// workgroup pass.  The first half of the grid takes the quantizations, the
+// second half the promotions / admissions, so a workgroup knows its list before
+// the counts arrive and reads the counts and its first entry in one round.  A
+// promotion whose bf16 slot is being vacated by a quantization in the same event
+// (dep >= 0) runs in that quantization's workgroup right after it, part by part,
+// so the slot is read before it is overwritten without any ordering across
+// workgroups.
 template <int W>
 __global__ __launch_bounds__(kMigrateThreads) void k_migrate(MigrateArgs a) {
   const Geometry& G = a.g;
@@ -333,24 +376,28 @@ __global__ __launch_bounds__(kMigrateThreads) void k_migrate(MigrateArgs a) {
   int32_t* counts = (int32_t*)(ub + a.L.counts);
   const int32_t* qlist = (const int32_t*)(ub + a.L.qlist);
   const int32_t* plist = (const int32_t*)(ub + a.L.plist);
-  const int nq = counts[CNT_QUANT], np = counts[CNT_PROMOTE];
-  for (int task = blockIdx.x; task < (nq + np) * G.H_kv; task += gridDim.x) {
-    if (task < nq * G.H_kv) {
-      const int e = task / G.H_kv, g = task % G.H_kv;
-      const int32_t* ent = qlist + e * kQEntry;
-      quantize_task<W>(a, ub, b, g, ent, sm, counts);
-      const int dep = ent[5];
+  const int half = gridDim.x / 2;
+  const bool quant = (int)blockIdx.x < half;
+  const int x0 = quant ? blockIdx.x : blockIdx.x - half;
+  const int32_t* list = quant ? qlist : plist;
+  const int per_entry = G.H_kv * kParts;
+  const int e0 = x0 / per_entry;
+  const WorkEntry first = load_entry(list, e0 <= G.max_fq ? e0 : 0);   // lists hold max_fq + 1 entries
+  const int n_tasks = (quant ? counts[CNT_QUANT] : counts[CNT_PROMOTE]) * per_entry;
+  for (int task = x0; task < n_tasks; task += half) {
+    const int e = task / per_entry, g = (task / kParts) % G.H_kv, part = task % kParts;
+    const WorkEntry ent = task == x0 ? first : load_entry(list, e);
+    if (quant) {
+      quantize_task<W>(a, ub, b, g, ent, sm, counts, part);
+      const int dep = ent.v[5];
       if (dep >= 0) {
         __syncthreads();
-        promote_task<W>(a, ub, b, g, plist + dep * kQEntry);
+        promote_task<W>(a, ub, b, g, load_entry(plist, dep), part);
       }
-    } else {
-      const int t2 = task - nq * G.H_kv;
-      const int e = t2 / G.H_kv, g = t2 % G.H_kv;
-      const int32_t* ent = plist + e * kQEntry;
-      if (ent[5] < 0) promote_task<W>(a, ub, b, g, ent);
+    } else if (ent.v[5] < 0) {
+      promote_task<W>(a, ub, b, g, ent, part);
     }
-    __syncthreads();
+    if (task + half < n_tasks) __syncthreads();   // LDS reused by the next task
   }
 }
 
@@ -378,13 +425,16 @@ __global__ __launch_bounds__(256) void k_pack_tokens(PackArgs a) {
   }
 }
 
-static int migrate_blocks(const Geometry& g, int max_entries) {
-  int n = max_entries * g.H_kv;
-  return n < 1 ? 1 : (n > 256 ? 256 : n);
+// Workgroups per half of the grid: enough for every task of a routing event of
+// up to `entries` windows, at most 128 (larger events loop).
+static int migrate_half(const Geometry& g, int entries) {
+  int n = entries * g.H_kv * kParts;
+  return n < 1 ? 1 : (n > 128 ? 128 : n);
 }
 
 hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, hipStream_t st) {
-  const dim3 grid(migrate_blocks(a.g, max_quant + max_promote), a.g.B);
+  const int mx = max_quant > max_promote ? max_quant : max_promote;
+  const dim3 grid(2 * migrate_half(a.g, mx), a.g.B);
   if (a.g.W == 32) hipLaunchKernelGGL(k_migrate<32>, grid, dim3(kMigrateThreads), 0, st, a);
   else hipLaunchKernelGGL(k_migrate<64>, grid, dim3(kMigrateThreads), 0, st, a);
   return hipGetLastError();

@@ -590,17 +590,19 @@ qevict_status qevict_retier(qevict_cache* c, int32_t layer, qevict_retier_stats*
   fill_common(c, layer, &gg, &L, &base);
   RetierArgs ra{gg, L, base, 0, a0, a1 > a0 ? a1 : a0, nullptr, 0};
   MigrateArgs ma{gg, L, base, nullptr, nullptr, 0};
-  const int max_q = g.K_q < g.max_fq ? g.K_q : g.max_fq;
+  // grid of the migration launch: sized for the windows a routing event usually
+  // moves (a few per step between events); larger events loop inside the kernel
+  const int max_q = std::min(std::max(g.K_q, g.K_f), 4 * c->cfg.retier_interval);
   hipError_t e = hipSuccess;
   if (c->rstream) {
     // asynchronous routing: queue the request; a batch is launched on the
     // routing stream once it is full (or the layer is needed again)
-    c->route_queue.push_back(RouteRequest{layer, ra, ma, max_q, g.K_f});
+    c->route_queue.push_back(RouteRequest{layer, ra, ma, max_q, max_q});
     c->route_queued[layer] = 1;
     if (stats || (int)c->route_queue.size() >= c->route_batch) e = flush_routing(c);
   } else {
     e = timed(c, 2, c->stream, [&] { return launch_retier(ra, c->stream); });
-    if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_migrate(ma, max_q, g.K_f, c->stream); });
+    if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_migrate(ma, max_q, max_q, c->stream); });
   }
   if (e != hipSuccess) return hip_fail(e, "retier launch");
   if (a1 > a0) ls.routed_end = a1;
