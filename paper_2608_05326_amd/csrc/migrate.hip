@@ -91,6 +91,9 @@ __device__ __forceinline__ uint32_t quant_code(float x, const QParams& p, int nm
 // key entry / chunk e has channel block 32 (e & 3), value entry / chunk e has
 // channel block 16 (e & 7), and an int2 word's two entries share their half.
 constexpr int kParts = 4;
+// LDS row of one token's 128 channels, padded by 16 bytes so that 16-byte
+// accesses to 16 consecutive tokens fall in distinct banks
+constexpr int kLdsRow = kHeadDim + 8;
 __device__ __forceinline__ int entry_half(int area, int e) { return area == 0 ? (e & 3) >> 1 : (e & 7) >> 2; }
 // bf16 chunk (= code entry) index of local chunk cl of channel half h of an area
 __device__ __forceinline__ int part_chunk(int area, int h, int cl) {
@@ -122,7 +125,7 @@ __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk
       const int ei = (m * 4 + comp) * PER + ee;
       if (area == 0) {   // key entry (tb, kb): token 16 tb + r, channels 32 kb + 8 q + j
         const int t = 16 * (ei >> 2) + r, c0 = 32 * (ei & 3) + 8 * q;
-        const u32x4 v = *(const u32x4*)(sk + t * kHeadDim + c0);
+        const u32x4 v = *(const u32x4*)(sk + t * kLdsRow + c0);
         const uint32_t vw[4] = {v[0], v[1], v[2], v[3]};
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -134,7 +137,7 @@ __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const int t = v_tok(kt, q, j);
-          const float x = bf16_to_f32(sv[t * kHeadDim + c]);
+          const float x = bf16_to_f32(sv[t * kLdsRow + c]);
           wd |= quant_code(x, pv[t * NG + vg], nmax) << ((j & 1) * 16 + NB * (4 * ee + (j >> 1)));
         }
       }
@@ -156,7 +159,7 @@ __device__ __forceinline__ void load_window(const MigrateArgs& a, uint8_t* ub, i
     const uint16_t* src = (area == 0 ? a.src_k : a.src_v) + row0 * kHeadDim;
     for (int i = tid; i < W * 8; i += blockDim.x) {
       const int t = i >> 3, c = 64 * h + 8 * (i & 7);
-      *(u32x4*)(dst + t * kHeadDim + c) = *(const u32x4*)(src + t * kHeadDim + c);
+      *(u32x4*)(dst + t * kLdsRow + c) = *(const u32x4*)(src + t * kHeadDim + c);
     }
   } else {
     const uint8_t* p = ub + (src_kind == SRC_FSLOT ? a.L.fpool : a.L.ring) +
@@ -168,13 +171,13 @@ __device__ __forceinline__ void load_window(const MigrateArgs& a, uint8_t* ub, i
       const int chunk = part_chunk(area, h, i >> 6), L = i & 63, q = L >> 4, r = L & 15;
       const u32x4 x = *(const u32x4*)(p + ((int64_t)chunk * 64 + L) * 16);
       if (area == 0) {
-        *(u32x4*)(sk + (16 * (chunk >> 2) + r) * kHeadDim + 32 * (chunk & 3) + 8 * q) = x;
+        *(u32x4*)(sk + (16 * (chunk >> 2) + r) * kLdsRow + 32 * (chunk & 3) + 8 * q) = x;
       } else {
         const int kt = chunk >> 3, c = 16 * (chunk & 7) + r;
         const uint32_t vw[4] = {x[0], x[1], x[2], x[3]};
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          sv[v_tok(kt, q, j) * kHeadDim + c] = (uint16_t)(vw[j >> 1] >> (16 * (j & 1)));
+          sv[v_tok(kt, q, j) * kLdsRow + c] = (uint16_t)(vw[j >> 1] >> (16 * (j & 1)));
       }
     }
   }
@@ -198,8 +201,8 @@ __device__ __forceinline__ WorkEntry load_entry(const int32_t* list, int e) {
 
 template <int W>
 struct QuantLds {
-  uint16_t sk[W * kHeadDim];
-  uint16_t sv[W * kHeadDim];
+  uint16_t sk[W * kLdsRow];
+  uint16_t sv[W * kLdsRow];
   QParams pk[kHeadDim];
   QParams pv[W * (kHeadDim / W)];
 };
@@ -226,11 +229,11 @@ __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub,
     if (area == 0) {
       c = 64 * h + tid;
 #pragma unroll
-      for (int tt = 0; tt < W; ++tt) x[tt] = bf16_to_f32(sk[tt * kHeadDim + c]);
+      for (int tt = 0; tt < W; ++tt) x[tt] = bf16_to_f32(sk[tt * kLdsRow + c]);
     } else {
       t = tid / NGH;
       vg = NGH * h + tid % NGH;
-      const u32x4* row = (const u32x4*)(sv + t * kHeadDim + vg * W);
+      const u32x4* row = (const u32x4*)(sv + t * kLdsRow + vg * W);
 #pragma unroll
       for (int k = 0; k < W / 8; ++k) {
         const u32x4 v = row[k];
