@@ -8,18 +8,21 @@ window-score accumulation (decode_attend) followed by the re-rank and the
 quantize / promote migrations (retier).
 
 Sixteen independent caches of this shape (one per "layer" of one workspace,
-each with its own seeds) are stepped in rounds: the decode_attend of each
-cache, then the retier of each.  A cache is used again only after the other
-fifteen, so the 16 x ~49 MB working set exceeds the 256 MB Infinity Cache and
-every step streams its windows from HBM.  Inputs for all timed steps are
-generated and copied to the GPU before timing.
+each with its own seeds) are stepped round robin.  A cache is used again only
+after the other fifteen, so the 16 x ~49 MB working set exceeds the 256 MB
+Infinity Cache and every step streams its windows from HBM.  Inputs for all
+timed steps are generated and copied to the GPU before timing.  By default the
+routing work runs on the library's routing stream (QEVICT_FLAG_ASYNC_ROUTING),
+overlapping the attention of the following layers; --routing sync keeps every
+kernel on one stream.
 
 Prints one JSON line.  `value` is microseconds per step (lower is better);
 `roofline` reports decode_attend's algorithmic bytes per call over its average
-duration, measured with HIP events on the cache's stream around the
-back-to-back decode_attend calls of each round; `roofline.traffic` is the HBM
-traffic per call from the committed FETCH_SIZE / WRITE_SIZE record over the
-same duration (null when the kernel sources changed since it was taken).
+duration, measured with HIP events on the cache's stream around rounds of 16
+back-to-back decode_attend calls with no routing running; `roofline.traffic`
+is the HBM traffic per call from the committed FETCH_SIZE / WRITE_SIZE record
+over the same duration (null when the library sources changed since it was
+taken).
 """
 from __future__ import annotations
 

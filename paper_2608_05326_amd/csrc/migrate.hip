@@ -429,10 +429,10 @@ __global__ __launch_bounds__(256) void k_pack_tokens(PackArgs a) {
 }
 
 // Workgroups per half of the grid: enough for every task of a routing event of
-// up to `entries` windows, at most 128 (larger events loop).
+// up to `entries` windows, at most 1024 (larger events loop).
 static int migrate_half(const Geometry& g, int entries) {
   int n = entries * g.H_kv * kParts;
-  return n < 1 ? 1 : (n > 128 ? 128 : n);
+  return n < 1 ? 1 : (n > 1024 ? 1024 : n);
 }
 
 hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, hipStream_t st) {

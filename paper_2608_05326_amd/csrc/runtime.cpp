@@ -90,6 +90,7 @@ struct qevict_cache {
   hipStream_t rstream = nullptr;
   hipEvent_t main_ev = nullptr;             // cache stream position a batch waits for
   std::vector<hipEvent_t> batch_ev;         // ring: end of a launched batch
+  std::vector<char> batch_joined;           // the cache stream already waits for that batch
   int next_batch_ev = 0;
   int route_batch = 1;
   std::vector<RouteRequest> route_queue;    // requested, not launched yet
@@ -306,6 +307,7 @@ hipError_t flush_routing(qevict_cache* c) {
   const int slot = c->next_batch_ev;
   c->next_batch_ev = (slot + 1) % (int)c->batch_ev.size();
   if (e == hipSuccess) e = hipEventRecord(c->batch_ev[slot], rs);
+  c->batch_joined[slot] = 0;
   for (const RouteRequest& r : c->route_queue) {
     c->route_queued[r.layer] = 0;
     c->route_ev_idx[r.layer] = slot;
@@ -324,8 +326,13 @@ hipError_t join_layer(qevict_cache* c, int layer) {
   if (c->route_queued[layer] && (e = flush_routing(c)) != hipSuccess) return e;
   const int idx = c->route_ev_idx[layer];
   if (idx < 0) return hipSuccess;
-  e = hipEventQuery(c->batch_ev[idx]);
-  if (e == hipErrorNotReady) e = hipStreamWaitEvent(c->stream, c->batch_ev[idx], 0);
+  if (!c->batch_joined[idx]) {
+    e = hipEventQuery(c->batch_ev[idx]);
+    if (e == hipErrorNotReady) {
+      e = hipStreamWaitEvent(c->stream, c->batch_ev[idx], 0);
+      if (e == hipSuccess) c->batch_joined[idx] = 1;   // covers the batch's other layers too
+    }
+  }
   if (e == hipSuccess) c->route_ev_idx[layer] = -1;
   return e;
 }
@@ -452,10 +459,11 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
   if (cfg->flags & QEVICT_FLAG_ASYNC_ROUTING) {
     e = hipStreamCreateWithFlags(&c->rstream, hipStreamNonBlocking);   // default priority
     const int nl = cfg->num_layers;
-    c->route_batch = nl / 4 < 1 ? 1 : (nl / 4 > 8 ? 8 : nl / 4);
+    c->route_batch = nl / 2 < 1 ? 1 : (nl / 2 > 8 ? 8 : nl / 2);
     c->route_queued.assign(nl, 0);
     c->route_ev_idx.assign(nl, -1);
     c->batch_ev.assign(nl + 1, nullptr);
+    c->batch_joined.assign(nl + 1, 0);
     // both streams run on this device: a device-scope release is enough
     const unsigned fl = hipEventDisableTiming | hipEventDisableSystemFence;
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->main_ev, fl);
