@@ -74,7 +74,7 @@ enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT =
 #define QEVICT_FLAG_DEBUG_MASSES 0x2u  /* keep per-head window masses of the last step              */
 /* Routing work (re-rank, quantize, promote) of qevict_retier runs on a stream
  * the library owns, so the routing of one layer overlaps the attention of the
- * layers after it.  Requests are launched in batches (up to num_layers / 4,
+ * layers after it.  Requests are launched in batches (up to num_layers / 2,
  * at most 8, layers per batch): a batch runs after everything enqueued on the
  * cache's stream before it was launched, which includes each of its layers'
  * latest decode_attend.  Every later call that touches a layer (decode_attend,

@@ -294,9 +294,9 @@ def test_async_routing_lockstep(name):
 def test_async_routing_interleaved_layers_match_sync(n_layers):
     """Several layers stepped back to back with no host synchronisation: the
     routing of each layer overlaps the attention of the others and every
-    output and final state equals the single-stream run bit for bit.  With 9
-    layers routing requests are launched two layers at a time, so the last
-    layer's request is still queued when its state is read."""
+    output and final state equals the single-stream run bit for bit.  Routing
+    requests are launched in batches (2 layers with 4 layers, 4 with 9), so with
+    9 layers the last layer's request is still queued when its state is read."""
     import paper_2608_05326_amd as qv
     from tests.gpu_harness import gpu_config, to_dev_bf16
     torch = _torch()
