@@ -470,6 +470,14 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   // live list with their cost prefixes (and the previous entry's), queries ----
   const int n_fq = __builtin_amdgcn_readfirstlane(counts[CNT_ITEMS]);
   const int base_cost = __builtin_amdgcn_readfirstlane(counts[CNT_COST]);
+  // the re-rank kernel's split plan for this step (first item, end item, first refs)
+  const bool plan_ok = __builtin_amdgcn_readfirstlane(counts[CNT_PLAN_T]) == a.T;
+  const int32_t* prec = (const int32_t*)(ub + a.L.plan) +
+                        (s * 4 + __builtin_amdgcn_readfirstlane(wave)) * kPlanRec;
+  static_assert(kPlanRec == 8, "plan record: first, end, 6 refs");
+  const int p_first = __builtin_amdgcn_readfirstlane(prec[0]);
+  const int p_last = __builtin_amdgcn_readfirstlane(prec[1]);
+  const int p_refs = lane < kPlanRefs ? prec[2 + lane] : 0;   // lane k: ref of item first + k
   int32_t lc[4], lp[4], lr[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
@@ -502,58 +510,67 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) *(u32x4*)(qlds + (i * 64 + lane) * 16) = (u32x4){0, 0, 0, 0};
 
-  // ---- this split's item range (equal estimated cost) ----
-  // Items: the live list, then the recent-region and sink windows (cost cF each).
-  // The split is cut into 4 equal-cost parts, one per wave: part u = 4s + w holds
-  // the items whose start cost lies in [ceil(u total / 4S), ceil((u + 1) total / 4S)).
-  // s_range[j] = first item whose start cost reaches the j-th cut of this split:
-  // start costs increase strictly, so the item with start(i - 1) < cut <= start(i)
-  // is unique, and cuts beyond the last item's start are set by that item.
-  // Costs are small integers (at most 32 per window, under 2^13 windows), so every
-  // prefix and cut fits in 32 bits; the cuts are uniform (scalar unit).
+  // ---- this wave's item range: from the plan, else computed here ----
   const int n_extra = a.n_ring + a.n_sink_items;
-  const int n_all = n_fq + n_extra;
-  const int cF = G.cost_bf16;
-  const int total = base_cost + n_extra * cF;
-  const int S = G.n_split;
-  __shared__ int s_range[5];
-  const uint32_t S4 = 4u * (uint32_t)S;
-  int cut[5];
+  int first, last;
+  if (plan_ok) {
+    first = p_first;
+    last = p_last;
+  } else {
+    // ---- this split's item range (equal estimated cost) ----
+    // Items: the live list, then the recent-region and sink windows (cost cF each).
+    // The split is cut into 4 equal-cost parts, one per wave: part u = 4s + w holds
+    // the items whose start cost lies in [ceil(u total / 4S), ceil((u + 1) total / 4S)).
+    // s_range[j] = first item whose start cost reaches the j-th cut of this split:
+    // start costs increase strictly, so the item with start(i - 1) < cut <= start(i)
+    // is unique, and cuts beyond the last item's start are set by that item.
+    // Costs are small integers (at most 32 per window, under 2^13 windows), so every
+    // prefix and cut fits in 32 bits; the cuts are uniform (scalar unit).
+    const int n_all = n_fq + n_extra;
+    const int cF = G.cost_bf16;
+    const int total = base_cost + n_extra * cF;
+    const int S = G.n_split;
+    __shared__ int s_range[5];
+    const uint32_t S4 = 4u * (uint32_t)S;
+    int cut[5];
 #pragma unroll
-  for (int j = 0; j < 5; ++j) cut[j] = (int)(((4u * (uint32_t)s + j) * (uint32_t)total + S4 - 1) / S4);
-  auto place = [&](int i, int c0, int c1) {
-    // bit j: cut j falls in (c0, c1] (or, for the last item, beyond it)
-    uint32_t m = 0, m_end = 0;
+    for (int j = 0; j < 5; ++j) cut[j] = (int)(((4u * (uint32_t)s + j) * (uint32_t)total + S4 - 1) / S4);
+    auto place = [&](int i, int c0, int c1) {
+      // bit j: cut j falls in (c0, c1] (or, for the last item, beyond it)
+      uint32_t m = 0, m_end = 0;
 #pragma unroll
-    for (int j = 0; j < 5; ++j) {
-      m |= (c1 >= cut[j] && c0 < cut[j]) ? 1u << j : 0u;
-      m_end |= cut[j] > c1 ? 1u << j : 0u;
+      for (int j = 0; j < 5; ++j) {
+        m |= (c1 >= cut[j] && c0 < cut[j]) ? 1u << j : 0u;
+        m_end |= cut[j] > c1 ? 1u << j : 0u;
+      }
+      if (i == n_all - 1) {
+        for (uint32_t e = m_end; e; e &= e - 1) s_range[__builtin_ctz(e)] = n_all;
+      }
+      for (; m; m &= m - 1) s_range[__builtin_ctz(m)] = i;
+    };
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (k * kAttnThreads >= n_all) break;   // uniform
+      const int i = tid + k * kAttnThreads;
+      if (i < n_fq) s_ref[i] = lr[k];
+      if (i < n_all) {
+        const int c1 = i <= n_fq ? lc[k] : base_cost + (i - n_fq) * cF;
+        const int c0 = i == 0 ? -1 : (i - 1 <= n_fq ? lp[k] : base_cost + (i - 1 - n_fq) * cF);
+        place(i, c0, c1);
+      }
     }
-    if (i == n_all - 1) {
-      for (uint32_t e = m_end; e; e &= e - 1) s_range[__builtin_ctz(e)] = n_all;
-    }
-    for (; m; m &= m - 1) s_range[__builtin_ctz(m)] = i;
-  };
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    if (k * kAttnThreads >= n_all) break;   // uniform
-    const int i = tid + k * kAttnThreads;
-    if (i < n_fq) s_ref[i] = lr[k];
-    if (i < n_all) {
-      const int c1 = i <= n_fq ? lc[k] : base_cost + (i - n_fq) * cF;
-      const int c0 = i == 0 ? -1 : (i - 1 <= n_fq ? lp[k] : base_cost + (i - 1 - n_fq) * cF);
+    for (int i = tid + 4 * kAttnThreads; i < n_all; i += kAttnThreads) {   // long lists
+      if (i < n_fq) s_ref[i] = iref[i];
+      const int c1 = i <= n_fq ? icost[i] : base_cost + (i - n_fq) * cF;
+      const int c0 = i - 1 <= n_fq ? icost[i - 1] : base_cost + (i - 1 - n_fq) * cF;
       place(i, c0, c1);
     }
+    if (n_all == 0 && tid < 5) s_range[tid] = 0;
+    __syncthreads();
+
+    first = s_range[wave];
+    last = s_range[wave + 1];
   }
-  for (int i = tid + 4 * kAttnThreads; i < n_all; i += kAttnThreads) {   // long lists
-    if (i < n_fq) s_ref[i] = iref[i];
-    const int c1 = i <= n_fq ? icost[i] : base_cost + (i - n_fq) * cF;
-    const int c0 = i - 1 <= n_fq ? icost[i - 1] : base_cost + (i - 1 - n_fq) * cF;
-    place(i, c0, c1);
-  }
-  if (n_all == 0 && tid < 5) s_range[tid] = 0;
-  __syncthreads();
-  const int first = s_range[wave], last = s_range[wave + 1];
 
   WaveState st;
   st.m = -INFINITY;
@@ -573,7 +590,13 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
     in.ntok = W;
     in.open = false;
     if (it < n_fq) {
-      const int32_t ref = s_ref[it];
+      int32_t ref;
+      if (plan_ok) {
+        const int k = it - first;
+        ref = k < kPlanRefs ? __builtin_amdgcn_readlane(p_refs, k) : iref[it];
+      } else {
+        ref = s_ref[it];
+      }
       in.kind = ref >> 28;
       const int64_t slot = ref & 0x0FFFFFFF;
       in.p = in.kind == KIND_BF16 ? fpool + slot * G.fslot_bytes + g * G.fhead_bytes
@@ -640,7 +663,7 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
         }
       }
     }
-    const int64_t row = (int64_t)(g * gqa + h) * S + s;
+    const int64_t row = (int64_t)(g * gqa + h) * G.n_split + s;
     part[row * kHeadDim + c] = o;
     if (c == 0) pml[row] = make_float2(M, L);
   }

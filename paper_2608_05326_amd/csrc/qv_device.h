@@ -37,6 +37,8 @@ struct RetierArgs {
   int32_t aged_w0, aged_w1; // aged windows entering the candidate pool
   const float* init_scores; // prefill: [B][n_init]
   int32_t n_init;
+  int32_t plan_T;           // sequence length of the next decode step (its split plan), or -1
+  int32_t plan_extra;       // recent-region + sink windows that step attends after the live list
 };
 
 struct MigrateArgs {

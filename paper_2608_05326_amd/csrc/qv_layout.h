@@ -51,9 +51,13 @@ enum : int32_t { KIND_BF16 = 0, KIND_Q4 = 1, KIND_Q2 = 2 };
 // (dormant for a Full item, active for a Quantized one) with its bit width:
 // aux = qslot | (bits << 28)
 // per-unit counters
-// (CNT_COST: summed split-balancing cost of the live list, item_cost[CNT_ITEMS])
+// (CNT_COST: summed split-balancing cost of the live list, item_cost[CNT_ITEMS];
+//  CNT_PLAN_T: sequence length the split plan was made for, -1 none)
 enum : int32_t { CNT_ITEMS = 0, CNT_QUANT = 1, CNT_PROMOTE = 2, CNT_ERROR = 3, CNT_BYTES_LO = 4,
-                 CNT_COST = 5, CNT_N = 16 };
+                 CNT_COST = 5, CNT_PLAN_T = 6, CNT_N = 16 };
+// split plan record: first item, end item, list refs of the first kPlanRefs items
+constexpr int kPlanRefs = 6;
+constexpr int kPlanRec = 2 + kPlanRefs;
 // device error bits
 enum : int32_t { ERR_NONFINITE = 1, ERR_POOL = 2, ERR_RANGE = 4, ERR_CAND = 8 };
 // stats slots (same order as qevict_retier_stats)
@@ -102,6 +106,7 @@ struct UnitLayout {
   int64_t item_win, item_ref, item_cost, item_aux, item_score;
   int64_t qlist, plist, counts, stats;
   int64_t partial, pml, mref, dbg_mass;
+  int64_t plan;         // per (split, wave): first item, end item, refs of its first kPlanRefs items
 };
 
 QV_HD int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }

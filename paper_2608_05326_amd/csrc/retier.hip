@@ -664,7 +664,10 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   for (int i = tid; i < G.n_qslots; i += NT) qowner[i] = qown[i];
 
   // ---- rebuild the live list (window order) with its cost prefix ----
-  int n_items;
+  int n_items, total_live;
+  int32_t* s_start = sa;     // LDS copies of the new list's cost prefix and refs
+  int32_t* s_pref = sinfo;   // (both arrays are free once the work lists are written)
+  __syncthreads();
   {
     bool fl[3][PER];
     int rk[3][PER], tots[3];
@@ -686,16 +689,20 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       const int kind = fl[0][k] ? KIND_BF16 : (fl[1][k] ? KIND_Q4 : KIND_Q2);
       const int slot = fl[0][k] ? my_fs[k] : my_qs[k];
       atomicAdd(&sstat[fl[0][k] ? ST_NF : (fl[1][k] ? ST_NQ4 : ST_NQ2)], 1);
+      const int ref = (kind << 28) | slot;
+      const int cost = rk[0][k] * G.cost_bf16 + rk[1][k] * G.cost_q4 + rk[2][k] * G.cost_q2;
       iwin[pos] = my_w[k];
-      iref[pos] = (kind << 28) | slot;
+      iref[pos] = ref;
       iaux[pos] = my_aux[k];
       iscore[pos] = my_sc[k];
-      icost[pos] = rk[0][k] * G.cost_bf16 + rk[1][k] * G.cost_q4 + rk[2][k] * G.cost_q2;
+      icost[pos] = cost;
+      s_start[pos] = cost;
+      s_pref[pos] = ref;
     }
+    total_live = tots[0] * G.cost_bf16 + tots[1] * G.cost_q4 + tots[2] * G.cost_q2;
     if (tid == 0) {
-      const int total = tots[0] * G.cost_bf16 + tots[1] * G.cost_q4 + tots[2] * G.cost_q2;
-      icost[n_items] = total;
-      counts[CNT_COST] = total;
+      icost[n_items] = total_live;
+      counts[CNT_COST] = total_live;
     }
   }
   // list positions after the live windows hold the recent-region windows of the
@@ -708,6 +715,43 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     counts[CNT_PROMOTE] = nreqF < nfreeF ? nreqF : nfreeF;
   }
   if (tid < ST_N) stats[tid] = sstat[tid];
+
+  // ---- split plan of the next decode step ----
+  // The attention splits the items (live list, then plan_extra recent-region and
+  // sink windows of cost cost_bf16) at the cuts ceil(u total / 4S), u = 0..4S;
+  // first[u] = the item whose start cost is the first to reach cut u (the unique
+  // item with start(i - 1) < cut <= start(i)), or the item count past the last
+  // start.  Record u = 4 s + w: first[u], first[u + 1] and the first refs.
+  if (a.plan_T > 0) {
+    int32_t* s_first = sown;   // owner tables are written back: free
+    const int cF = G.cost_bf16;
+    const int n_all = n_items + a.plan_extra;
+    const int total = total_live + a.plan_extra * cF;
+    const int S4 = 4 * G.n_split;
+    auto start = [&](int i) { return i < n_items ? s_start[i] : total_live + (i - n_items) * cF; };
+    for (int i = tid; i < n_all; i += NT) {
+      const int c1 = start(i), c0 = i == 0 ? -1 : start(i - 1);
+      // cut u lies in (c0, c1] <=> c0 S4 < u total <= c1 S4
+      const int u_lo = c0 < 0 ? 0 : (int)((uint32_t)c0 * (uint32_t)S4 / (uint32_t)total) + 1;
+      const int u_hi = (int)((uint32_t)c1 * (uint32_t)S4 / (uint32_t)total);
+      for (int u = u_lo; u <= u_hi && u <= S4; ++u) s_first[u] = i;
+      if (i == n_all - 1)
+        for (int u = u_hi + 1; u <= S4; ++u) s_first[u] = n_all;
+    }
+    if (n_all == 0)
+      for (int u = tid; u <= S4; u += NT) s_first[u] = 0;
+    __syncthreads();
+    int32_t* plan = (int32_t*)(ub + a.L.plan);
+    for (int u = tid; u < S4; u += NT) {
+      const int first = s_first[u];
+      int32_t* rec = plan + u * kPlanRec;
+      rec[0] = first;
+      rec[1] = s_first[u + 1];
+#pragma unroll
+      for (int k = 0; k < kPlanRefs; ++k) rec[2 + k] = first + k < n_items ? s_pref[first + k] : 0;
+    }
+  }
+  if (tid == 0) counts[CNT_PLAN_T] = a.plan_T;
 }
 
 // Manual single-window move (one thread): F -> Q (quantize once or reactivate)
@@ -785,6 +829,7 @@ __global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
   }
   icost[n] = run;
   counts[CNT_COST] = run;
+  counts[CNT_PLAN_T] = -1;   // the split plan no longer matches the list
 }
 
 // State initialisation of every unit block (grid-stride over units).

@@ -237,6 +237,7 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   L->pml = take(8LL * g->H_q * g->n_split);
   L->mref = take(8LL * g->H_q * g->max_items);
   L->dbg_mass = take((c->flags & QEVICT_FLAG_DEBUG_MASSES) ? 4LL * g->H_q * (g->nwc + 1) : 0);
+  L->plan = take(4LL * kPlanRec * 4 * g->n_split);
   L->unit_bytes = align256(off);
 }
 
@@ -373,6 +374,16 @@ void fill_common(qevict_cache* c, int layer, Geometry* g, UnitLayout* L, uint8_t
 }
 
 int n_started(const Geometry& g, int T) { return T <= g.sink ? 0 : ceil_div(T - g.sink, g.W); }
+// Split plan the re-rank kernel prepares for the next decode step (sequence length
+// T_next, windows below routed_end routed): that step's T, and its recent-region +
+// sink windows, or T = -1 when the step could not run.
+void plan_next(const Geometry& g, int max_context, int T_next, int routed_end, int32_t* plan_T,
+               int32_t* plan_extra) {
+  const int n_ring = n_started(g, T_next) - routed_end;
+  const bool ok = T_next <= max_context && n_ring >= 0 && n_ring <= g.NR;
+  *plan_T = ok ? T_next : -1;
+  *plan_extra = ok ? n_ring + g.NS : 0;
+}
 int aged_end(const Geometry& g, int T) {
   int n = T - g.recent - g.sink;
   return n <= 0 ? 0 : n / g.W;
@@ -533,7 +544,8 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
     pa.tok1 = prompt_len;
     e = launch_pack_tokens(pa, c->stream);            // tail: recent region and partial window
   }
-  RetierArgs ra{gg, L, base, 1, 0, n_hist, init_scores, n_init};
+  RetierArgs ra{gg, L, base, 1, 0, n_hist, init_scores, n_init, -1, 0};
+  plan_next(g, c->cfg.max_context, prompt_len + 1, n_hist, &ra.plan_T, &ra.plan_extra);
   if (e == hipSuccess) e = timed(c, 2, c->stream, [&] { return launch_retier(ra, c->stream); });
   MigrateArgs ma{gg, L, base, k, v, prompt_len};
   if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_migrate(ma, g.K_q, g.K_f, c->stream); });
@@ -596,7 +608,8 @@ qevict_status qevict_retier(qevict_cache* c, int32_t layer, qevict_retier_stats*
   UnitLayout L;
   uint8_t* base;
   fill_common(c, layer, &gg, &L, &base);
-  RetierArgs ra{gg, L, base, 0, a0, a1 > a0 ? a1 : a0, nullptr, 0};
+  RetierArgs ra{gg, L, base, 0, a0, a1 > a0 ? a1 : a0, nullptr, 0, -1, 0};
+  plan_next(g, c->cfg.max_context, ls.T + 1, a1 > a0 ? a1 : a0, &ra.plan_T, &ra.plan_extra);
   MigrateArgs ma{gg, L, base, nullptr, nullptr, 0};
   // grid of the migration launch: sized for the windows a routing event usually
   // moves (a few per step between events); larger events loop inside the kernel
@@ -679,7 +692,7 @@ static qevict_status manual_move(qevict_cache* c, int layer, int seq, int window
   UnitLayout L;
   uint8_t* base;
   fill_common(c, layer, &gg, &L, &base);
-  RetierArgs ra{gg, L, base, 0, 0, 0, nullptr, 0};
+  RetierArgs ra{gg, L, base, 0, 0, 0, nullptr, 0, -1, 0};
   // the migration kernels read work lists per sequence: run them on this sequence only
   Geometry one = gg;
   one.B = 1;
