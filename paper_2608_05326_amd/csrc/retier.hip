@@ -664,9 +664,23 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   for (int i = tid; i < G.n_qslots; i += NT) qowner[i] = qown[i];
 
   // ---- rebuild the live list (window order) with its cost prefix ----
+  // The split plan of the next decode step is filled in on the way: the attention
+  // splits the items (the live list, then plan_extra recent-region and sink
+  // windows of cost cost_bf16) at the cuts ceil(u total / 4S), u = 0..4S, and the
+  // wave of part u starts at the first item whose start cost reaches cut u.  The
+  // items' cost intervals (start, end] partition (0, total], so cut u >= 1 lies in
+  // exactly one of them and part u starts at the item after it (cut 0: item 0).
+  // Cut u lies in (start, end] <=> start 4S < u total <= end 4S.
   int n_items, total_live;
-  int32_t* s_start = sa;     // LDS copies of the new list's cost prefix and refs
-  int32_t* s_pref = sinfo;   // (both arrays are free once the work lists are written)
+  int32_t* s_pref = sinfo;   // LDS copy of the new list's refs (free once the work lists are written)
+  int32_t* s_first = sown;   // part u's first item (owner tables are written back)
+  const bool plan = a.plan_T > 0;
+  const int S4 = 4 * G.n_split;
+  auto cover = [&](int start, int end, int total, int next) {
+    const int u_lo = (int)((uint32_t)start * (uint32_t)S4 / (uint32_t)total) + 1;
+    const int u_hi = (int)((uint32_t)end * (uint32_t)S4 / (uint32_t)total);
+    for (int u = u_lo; u <= u_hi; ++u) s_first[u] = next;
+  };
   __syncthreads();
   {
     bool fl[3][PER];
@@ -681,6 +695,15 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     }
     flag_scan<3>(fl, rk, tots, tmp, kc);
     n_items = tots[0] + tots[1] + tots[2];
+    total_live = tots[0] * G.cost_bf16 + tots[1] * G.cost_q4 + tots[2] * G.cost_q2;
+    const int total = total_live + a.plan_extra * G.cost_bf16;   // the planned step's total
+    if (plan) {
+      if (tid == 0) s_first[0] = 0;
+      if (total == 0)
+        for (int u = tid; u <= S4; u += NT) s_first[u] = 0;
+      for (int j = tid; j < a.plan_extra; j += NT)   // recent-region and sink windows
+        cover(total_live + j * G.cost_bf16, total_live + (j + 1) * G.cost_bf16, total, n_items + j + 1);
+    }
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       if (k >= kc) break;
@@ -696,10 +719,9 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       iaux[pos] = my_aux[k];
       iscore[pos] = my_sc[k];
       icost[pos] = cost;
-      s_start[pos] = cost;
       s_pref[pos] = ref;
+      if (plan) cover(cost, cost + item_cost(G, kind), total, pos + 1);
     }
-    total_live = tots[0] * G.cost_bf16 + tots[1] * G.cost_q4 + tots[2] * G.cost_q2;
     if (tid == 0) {
       icost[n_items] = total_live;
       counts[CNT_COST] = total_live;
@@ -716,39 +738,18 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   }
   if (tid < ST_N) stats[tid] = sstat[tid];
 
-  // ---- split plan of the next decode step ----
-  // The attention splits the items (live list, then plan_extra recent-region and
-  // sink windows of cost cost_bf16) at the cuts ceil(u total / 4S), u = 0..4S;
-  // first[u] = the item whose start cost is the first to reach cut u (the unique
-  // item with start(i - 1) < cut <= start(i)), or the item count past the last
-  // start.  Record u = 4 s + w: first[u], first[u + 1] and the first refs.
-  if (a.plan_T > 0) {
-    int32_t* s_first = sown;   // owner tables are written back: free
-    const int cF = G.cost_bf16;
-    const int n_all = n_items + a.plan_extra;
-    const int total = total_live + a.plan_extra * cF;
-    const int S4 = 4 * G.n_split;
-    auto start = [&](int i) { return i < n_items ? s_start[i] : total_live + (i - n_items) * cF; };
-    for (int i = tid; i < n_all; i += NT) {
-      const int c1 = start(i), c0 = i == 0 ? -1 : start(i - 1);
-      // cut u lies in (c0, c1] <=> c0 S4 < u total <= c1 S4
-      const int u_lo = c0 < 0 ? 0 : (int)((uint32_t)c0 * (uint32_t)S4 / (uint32_t)total) + 1;
-      const int u_hi = (int)((uint32_t)c1 * (uint32_t)S4 / (uint32_t)total);
-      for (int u = u_lo; u <= u_hi && u <= S4; ++u) s_first[u] = i;
-      if (i == n_all - 1)
-        for (int u = u_hi + 1; u <= S4; ++u) s_first[u] = n_all;
-    }
-    if (n_all == 0)
-      for (int u = tid; u <= S4; u += NT) s_first[u] = 0;
-    __syncthreads();
-    int32_t* plan = (int32_t*)(ub + a.L.plan);
+  // ---- split plan records: part u = 4 s + w ----
+  if (plan) {
+    int32_t* prec = (int32_t*)(ub + a.L.plan);
     for (int u = tid; u < S4; u += NT) {
       const int first = s_first[u];
-      int32_t* rec = plan + u * kPlanRec;
-      rec[0] = first;
-      rec[1] = s_first[u + 1];
+      int32_t r[kPlanRefs];
 #pragma unroll
-      for (int k = 0; k < kPlanRefs; ++k) rec[2 + k] = first + k < n_items ? s_pref[first + k] : 0;
+      for (int k = 0; k < kPlanRefs; ++k) r[k] = first + k < n_items ? s_pref[first + k] : 0;
+      static_assert(kPlanRec == 8, "two 16-byte stores per record");
+      u32x4* q = (u32x4*)(prec + u * kPlanRec);
+      q[0] = (u32x4){(uint32_t)first, (uint32_t)s_first[u + 1], (uint32_t)r[0], (uint32_t)r[1]};
+      q[1] = (u32x4){(uint32_t)r[2], (uint32_t)r[3], (uint32_t)r[4], (uint32_t)r[5]};
     }
   }
   if (tid == 0) counts[CNT_PLAN_T] = a.plan_T;
