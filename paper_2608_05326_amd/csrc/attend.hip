@@ -775,19 +775,20 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
   const int wl = (maybe && hh == 0) ? iwin[min(pos, G.max_fq)] : -1;   // used when pos < n_fq
   const float old_score = (maybe && hh == 0) ? iscore[pos] : 0.f;
   // M_h, L_h: P consecutive threads per head (P a power of two, P * H_q <= 256),
-  // thread j folds splits j*C .. j*C + C - 1 from its own loads, then a
-  // butterfly over the P lanes combines the (max, sum) pairs
+  // thread j folds splits j, j + P, j + 2P, ... (consecutive threads read
+  // consecutive rows), then a butterfly over the P lanes combines the
+  // (max, sum) pairs
   int P = 1;
   while (2 * P * nh <= kMergeThreads) P *= 2;
   const int C = (S + P - 1) / P;
-  constexpr int kMaxC = 36;   // C <= S * H_q / 128 + 1 <= 33 (S * H_q <= 4096)
+  constexpr int kMaxC = 32;   // C <= S * H_q / 128 <= 32 (S * H_q <= 4096, P * H_q > 128)
   {
     const int h = tid / P, j = tid % P;
     const bool hv = h < nh;
     float2 st[kMaxC];
 #pragma unroll
     for (int i = 0; i < kMaxC; ++i) {
-      const int sp = j * C + i;
+      const int sp = j + P * i;
       st[i] = (hv && i < C && sp < S) ? pml[(int64_t)h * S + sp] : make_float2(-INFINITY, 0.f);
     }
     float m = -INFINITY;
