@@ -104,7 +104,12 @@ __device__ __forceinline__ int part_chunk(int area, int h, int cl) {
 // comp) forms word 4m + comp of lane L; entry e of a word holds its 8 codes at
 // bits 16 o + NB (4 e' + i) for code j = 2i + o.  Consecutive threads write
 // consecutive words.
-constexpr int kMigrateThreads = 1024;
+// 256 threads and, for 32-token windows, at most 96 VGPRs (five waves per SIMD):
+// a migration workgroup fits on a compute unit beside two attention workgroups,
+// so routing on its own stream does not hold back the attention of the next layers
+constexpr int kMigrateThreads = 256;
+template <int W>
+constexpr int migrate_waves_per_simd() { return W == 32 ? 5 : 4; }
 
 template <int W, int NB>
 __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk, const uint16_t* sv,
@@ -371,7 +376,7 @@ __device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, 
 // so the slot is read before it is overwritten without any ordering across
 // workgroups.
 template <int W>
-__global__ __launch_bounds__(kMigrateThreads) void k_migrate(MigrateArgs a) {
+__global__ __launch_bounds__(kMigrateThreads, migrate_waves_per_simd<W>()) void k_migrate(MigrateArgs a) {
   const Geometry& G = a.g;
   const int b = blockIdx.y;
   __shared__ __attribute__((aligned(16))) QuantLds<W> sm;
