@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define QEVICT_ABI_VERSION 1
+#define QEVICT_ABI_VERSION 2
 
 typedef struct qevict_cache qevict_cache;
 typedef int32_t qevict_status;
@@ -83,6 +83,18 @@ enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT =
  * qevict_join_routing does so for every layer. */
 #define QEVICT_FLAG_ASYNC_ROUTING 0x4u
 
+/* Window ranking functions (the hierarchy needs only an order over windows:
+ * Sec. 4.2 and the appendix on alternative ranking functions).
+ * CUMULATIVE: S(w) += (1/H_q) sum_h (mass of w under head h), every decode step
+ *   (Sec. 4.2, cumulative window score equation).
+ * DECAY: the exponentially decayed score S_t = lambda S_{t-R} + u_t, u_t the
+ *   attention w received since the previous routing event (appendix, decayed
+ *   score equation): the library multiplies every live window's score by
+ *   lambda in the first decode step after each routing event (and after
+ *   prefill), before adding that step's mass. */
+#define QEVICT_SCORE_CUMULATIVE 0
+#define QEVICT_SCORE_DECAY 1
+
 typedef struct {
   int32_t abi_version;       /* QEVICT_ABI_VERSION                                          */
   int32_t batch;             /* B sequences, all with the same length                       */
@@ -105,6 +117,8 @@ typedef struct {
   uint32_t flags;            /* QEVICT_FLAG_*                                                */
   float softmax_scale;       /* 0 selects 1/sqrt(head_dim)                                    */
   int32_t num_splits;        /* split-K factor of the attention pass; 0 = automatic          */
+  int32_t score_mode;        /* QEVICT_SCORE_CUMULATIVE (0) or QEVICT_SCORE_DECAY            */
+  float score_decay;         /* lambda of QEVICT_SCORE_DECAY, in (0, 1]                       */
 } qevict_config;
 
 typedef struct {

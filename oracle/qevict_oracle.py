@@ -13,6 +13,9 @@ What it computes, and where the paper defines it (QEvict, arXiv 2608.05326):
 * The cumulative window score: each window's attention mass averaged over the
   H_q query heads, added at every decode step (Sec. 4.2, cumulative window
   score equation; the per-step reading is listed with the other readings).
+  Optionally the exponentially decayed score S_t = lambda S_{t-R} + u_t of the
+  appendix on alternative ranking functions (decayed score equation), u_t the
+  attention a window received since the previous routing event.
 * Routing: the candidate pool is the previous Full and Quantized windows plus
   the windows that left the recent region; the top K_f by score go to Full,
   the next K_q to Quantized, the rest are evicted (Sec. 4.3, candidate pool
@@ -74,6 +77,7 @@ class OracleConfig:
     recent: int = 0
     softmax_scale: float | None = None   # default 1/sqrt(head_dim)
     no_promotion: bool = False    # one-way Full -> Quantized -> Evicted policy
+    score_decay: float = 1.0      # lambda of the decayed score; 1.0 = cumulative score
 
     @property
     def scale(self) -> float:
@@ -234,6 +238,9 @@ class QEvictUnit:
         self.stats = dict(promotions=0, admissions_full=0, first_quantizations=0,
                           reactivations=0, evictions=0)
         self.quant_count = 0          # quantizations performed over the lifetime
+        # decayed score: the first step after a routing event (or prefill) starts a new
+        # period, S = lambda S_previous_event + (attention received during the period)
+        self.new_period = False
 
     # -- geometry ---------------------------------------------------------
     def win_range(self, w: int):
@@ -329,6 +336,9 @@ class QEvictUnit:
             mass[h] = np.bincount(owner[win], weights=p[win], minlength=self.n_win_cap)
             sink_mass[h] = p[~win].sum()
         live = (self.state >= 0) & (self.state != EVICTED)
+        if self.new_period and c.score_decay != 1.0:
+            self.score[live] *= c.score_decay
+        self.new_period = False
         self.score[live] += mass[:, live].sum(axis=0) / c.num_q_heads
         return out, mass, sink_mass
 
@@ -394,6 +404,7 @@ class QEvictUnit:
             self.ledger.pop(w, None)
             self.state[w] = EVICTED
             self.stats["evictions"] += 1
+        self.new_period = True
         return full, quant, evict
 
     # -- single-window moves outside a routing event --------------------------

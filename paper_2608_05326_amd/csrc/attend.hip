@@ -847,7 +847,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
     else atomicAdd(&dbg[(int64_t)hh * (G.nwc + 1) + G.nwc], mass);
   }
   if (hh == 0 && win >= 0) {
-    const float ns = old_score + tot / (float)nh;
+    const float ns = old_score * a.decay + tot / (float)nh;
     ((float*)(ub + a.L.score))[win] = ns;
     iscore[pos] = ns;   // the next re-rank and merge read it by list position
   }

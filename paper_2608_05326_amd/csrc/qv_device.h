@@ -27,6 +27,7 @@ struct AttnArgs {
   int32_t ring_w0;          // first window not routed yet
   int32_t n_ring;           // windows in [ring_w0, ring_w0 + n_ring) are attended from the ring
   int32_t n_sink_items;     // sink slots holding sink tokens
+  float decay;              // factor on every updated window score before this step's mass
 };
 
 struct RetierArgs {

@@ -59,6 +59,7 @@ struct LayerState {
   int T = 0;              // tokens held (all sequences)
   int routed_end = 0;     // windows below this index have been routed
   bool prefilled = false;
+  bool decay_pending = false;   // a routing event (or prefill) since the last decode step
   int64_t last_bytes = 0;
 };
 
@@ -138,6 +139,10 @@ qevict_status check_config(const qevict_config* c) {
     return fail(QEVICT_ERR_INVALID_ARG, "unknown flags 0x%x", c->flags);
   if (!(c->softmax_scale >= 0.f) || !std::isfinite(c->softmax_scale))
     return fail(QEVICT_ERR_INVALID_ARG, "softmax_scale");
+  if (c->score_mode != QEVICT_SCORE_CUMULATIVE && c->score_mode != QEVICT_SCORE_DECAY)
+    return fail(QEVICT_ERR_INVALID_ARG, "score_mode");
+  if (c->score_mode == QEVICT_SCORE_DECAY && !(c->score_decay > 0.f && c->score_decay <= 1.f))
+    return fail(QEVICT_ERR_INVALID_ARG, "score_decay must be in (0, 1]");
   if (c->num_splits < 0 || c->num_splits > 256)
     return fail(QEVICT_ERR_INVALID_ARG, "num_splits must be in [0, 256]");
   if (c->num_splits * c->num_q_heads > 4096)
@@ -553,6 +558,7 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
   ls.T = prompt_len;
   ls.routed_end = n_hist;
   ls.prefilled = true;
+  ls.decay_pending = true;
   return QEVICT_OK;
 }
 
@@ -583,6 +589,7 @@ qevict_status qevict_decode_attend(qevict_cache* c, int32_t layer, const uint16_
   a.ring_w0 = ls.routed_end;
   a.n_ring = n_ring;
   a.n_sink_items = g.NS;
+  a.decay = (c->cfg.score_mode == QEVICT_SCORE_DECAY && ls.decay_pending) ? c->cfg.score_decay : 1.0f;
   hipError_t e = hipSuccess;
   if (g.flags & QEVICT_FLAG_DEBUG_MASSES) {
     for (int b = 0; b < g.B && e == hipSuccess; ++b)
@@ -593,6 +600,7 @@ qevict_status qevict_decode_attend(qevict_cache* c, int32_t layer, const uint16_
   if (e == hipSuccess) e = timed(c, 1, c->stream, [&] { return launch_merge(a, c->stream); });
   if (e != hipSuccess) return hip_fail(e, "decode_attend launch");
   ls.T = T;
+  ls.decay_pending = false;
   return QEVICT_OK;
 }
 
@@ -627,6 +635,7 @@ qevict_status qevict_retier(qevict_cache* c, int32_t layer, qevict_retier_stats*
   }
   if (e != hipSuccess) return hip_fail(e, "retier launch");
   if (a1 > a0) ls.routed_end = a1;
+  ls.decay_pending = true;
   if (stats) {
     memset(stats, 0, sizeof *stats);
     if ((e = join_layer(c, layer)) != hipSuccess) return hip_fail(e, "joining the routing stream");

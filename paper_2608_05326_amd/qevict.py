@@ -16,7 +16,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libqevict.so")
 
-ABI_VERSION = 1
+ABI_VERSION = 2
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_BAD_STATE, ERR_NONFINITE, \
     ERR_CAPACITY, ERR_DEVICE = 0, -1, -2, -3, -4, -5, -6, -7
 TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED = 0, 1, 2, 3, 4
@@ -25,6 +25,7 @@ BITS_MIXED_4_2 = 42
 OUT_F32, OUT_BF16 = 0, 1
 FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING = 0x1, 0x2, 0x4
 KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_MIGRATE = range(4)
+SCORE_CUMULATIVE, SCORE_DECAY = 0, 1
 
 # exported symbols declared in include/qevict.h
 SYMBOLS = (
@@ -47,7 +48,8 @@ class _Config(ctypes.Structure):
         "abi_version", "batch", "num_layers", "num_q_heads", "num_kv_heads", "head_dim",
         "window_tokens", "group_size", "quant_bits", "sink_tokens", "recent_tokens", "max_context",
         "capacity_full", "capacity_quant", "retier_interval", "out_dtype")] + [
-        ("flags", ctypes.c_uint32), ("softmax_scale", ctypes.c_float), ("num_splits", ctypes.c_int32)]
+        ("flags", ctypes.c_uint32), ("softmax_scale", ctypes.c_float), ("num_splits", ctypes.c_int32),
+        ("score_mode", ctypes.c_int32), ("score_decay", ctypes.c_float)]
 
 
 class RetierStats(ctypes.Structure):
@@ -79,6 +81,8 @@ class Config:
     flags: int = 0
     softmax_scale: float = 0.0
     num_splits: int = 0
+    score_mode: int = SCORE_CUMULATIVE
+    score_decay: float = 0.0
 
     def to_c(self) -> _Config:
         c = _Config()

@@ -32,21 +32,26 @@ def to_dev_bf16(bits: np.ndarray) -> torch.Tensor:
 
 
 def gpu_config(wl: syn.Workload, layers: int, flags: int = 0, out_dtype: int = qv.OUT_F32,
-               num_splits: int = 0, capacity_full=None, capacity_quant=None) -> qv.Config:
+               num_splits: int = 0, capacity_full=None, capacity_quant=None,
+               score_decay: float | None = None) -> qv.Config:
     return qv.Config(
         batch=wl.batch, num_layers=layers, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
         window_tokens=wl.window, group_size=wl.group, quant_bits=wl.bits, max_context=wl.max_context,
         capacity_full=wl.capacity_full if capacity_full is None else capacity_full,
         capacity_quant=wl.capacity_quant if capacity_quant is None else capacity_quant,
         sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=wl.retier_interval,
-        out_dtype=out_dtype, flags=flags, num_splits=num_splits)
+        out_dtype=out_dtype, flags=flags, num_splits=num_splits,
+        score_mode=qv.SCORE_DECAY if score_decay is not None else qv.SCORE_CUMULATIVE,
+        score_decay=score_decay or 0.0)
 
 
 def oracle_config(cfg: qv.Config) -> OracleConfig:
     return OracleConfig(cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.window_tokens,
                         cfg.group_size or cfg.window_tokens, cfg.quant_bits, cfg.capacity_full,
                         cfg.capacity_quant, sink=cfg.sink_tokens, recent=cfg.recent_tokens,
-                        no_promotion=bool(cfg.flags & qv.FLAG_NO_PROMOTION))
+                        no_promotion=bool(cfg.flags & qv.FLAG_NO_PROMOTION),
+                        score_decay=float(np.float32(cfg.score_decay))
+                        if cfg.score_mode == qv.SCORE_DECAY else 1.0)
 
 
 class Lockstep:
@@ -58,14 +63,14 @@ class Lockstep:
 
     def __init__(self, wl: syn.Workload, seed: int = 0, layer_ids=(0,), check_seqs=None,
                  flags: int = 0, num_splits: int = 0, steps: int | None = None, log=print,
-                 capacity_full=None, capacity_quant=None):
+                 capacity_full=None, capacity_quant=None, score_decay: float | None = None):
         self.wl, self.seed = wl, seed
         self.layer_ids = list(layer_ids)
         self.check_seqs = list(range(wl.batch)) if check_seqs is None else list(check_seqs)
         self.steps = wl.steps if steps is None else steps
         self.cfg = gpu_config(wl, len(self.layer_ids), flags | qv.FLAG_DEBUG_MASSES,
                               num_splits=num_splits, capacity_full=capacity_full,
-                              capacity_quant=capacity_quant)
+                              capacity_quant=capacity_quant, score_decay=score_decay)
         self.cache = qv.Cache(self.cfg)
         self.ocfg = oracle_config(self.cfg)
         self.units = {(li, b): QEvictUnit(self.ocfg, wl.max_context)

@@ -50,11 +50,20 @@ def test_workspace_size_of_the_8b_32k_layer():
     (dict(retier_interval=0), qv.qevict.ERR_INVALID_ARG),
     (dict(flags=0x80), qv.qevict.ERR_INVALID_ARG),
     (dict(max_context=0), qv.qevict.ERR_INVALID_ARG),
+    (dict(sink_tokens=65 * 32), qv.qevict.ERR_UNSUPPORTED),
+    (dict(score_mode=2), qv.qevict.ERR_INVALID_ARG),
+    (dict(score_mode=qv.SCORE_DECAY, score_decay=0.0), qv.qevict.ERR_INVALID_ARG),
+    (dict(score_mode=qv.SCORE_DECAY, score_decay=1.5), qv.qevict.ERR_INVALID_ARG),
 ])
 def test_bad_configs_are_rejected(kw, status):
     with pytest.raises(qv.QEvictError) as e:
         qv.workspace_size(_cfg(**kw))
     assert e.value.status == status
+
+
+def test_decayed_score_config_is_accepted():
+    assert qv.workspace_size(_cfg(score_mode=qv.SCORE_DECAY, score_decay=0.99)) == \
+        qv.workspace_size(_cfg())
 
 
 def test_status_strings():

@@ -33,3 +33,10 @@ def test_c1_forced_promotions():
 @pytest.mark.parametrize("name", ["c1s", "c2s", "c4s", "c5s", "c3s"])
 def test_small_workloads_lockstep(name):
     _lockstep(name)
+
+
+@pytest.mark.parametrize("name,decay", [("c2s", 0.99), ("c5s", 0.9)])
+def test_decayed_score_lockstep(name, decay):
+    """Exponentially decayed ranking (lambda per routing period; c5s routes every
+    8 steps): scores and routing against the oracle."""
+    _lockstep(name, score_decay=decay)
