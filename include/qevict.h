@@ -94,6 +94,12 @@ enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT =
  *   prefill), before adding that step's mass. */
 #define QEVICT_SCORE_CUMULATIVE 0
 #define QEVICT_SCORE_DECAY 1
+/* KEY_NORM: the attention-free key-norm score S(w) = -(1/W) sum_{i in w} |k_i|,
+ *   |k_i| the L2 norm of token i's key over all KV heads of the layer (appendix,
+ *   key-norm equation): prefill computes it for the prompt windows (init_scores
+ *   is ignored and may be NULL) and every decode step adds the new token's
+ *   share -|k_new| / W to its window; attention masses are not accumulated. */
+#define QEVICT_SCORE_KEY_NORM 2
 
 typedef struct {
   int32_t abi_version;       /* QEVICT_ABI_VERSION                                          */
@@ -117,7 +123,7 @@ typedef struct {
   uint32_t flags;            /* QEVICT_FLAG_*                                                */
   float softmax_scale;       /* 0 selects 1/sqrt(head_dim)                                    */
   int32_t num_splits;        /* split-K factor of the attention pass; 0 = automatic          */
-  int32_t score_mode;        /* QEVICT_SCORE_CUMULATIVE (0) or QEVICT_SCORE_DECAY            */
+  int32_t score_mode;        /* QEVICT_SCORE_CUMULATIVE (0), _DECAY or _KEY_NORM             */
   float score_decay;         /* lambda of QEVICT_SCORE_DECAY, in (0, 1]                       */
 } qevict_config;
 
@@ -147,7 +153,8 @@ qevict_status qevict_cache_destroy(qevict_cache *c);
  * scores and the first tier assignment).
  *   k, v        [B, H_kv, prompt_len, d] bf16 prompt keys / values
  *   init_scores [B, n_w] fp32, n_w = ceil((prompt_len - sink)/W): initial
- *               cumulative score of every prompt window (also partial ones)
+ *               cumulative score of every prompt window (also partial ones);
+ *               unused (may be NULL) with QEVICT_SCORE_KEY_NORM
  * The complete windows outside the sink and recent regions are routed at once
  * (TopK on init_scores; Quantized windows are quantized from k, v).  The
  * prompt buffers are only read by work enqueued here. */

@@ -15,7 +15,8 @@ What it computes, and where the paper defines it (QEvict, arXiv 2608.05326):
   score equation; the per-step reading is listed with the other readings).
   Optionally the exponentially decayed score S_t = lambda S_{t-R} + u_t of the
   appendix on alternative ranking functions (decayed score equation), u_t the
-  attention a window received since the previous routing event.
+  attention a window received since the previous routing event, or the
+  attention-free key-norm score of the same appendix (key-norm equation).
 * Routing: the candidate pool is the previous Full and Quantized windows plus
   the windows that left the recent region; the top K_f by score go to Full,
   the next K_q to Quantized, the rest are evicted (Sec. 4.3, candidate pool
@@ -78,6 +79,7 @@ class OracleConfig:
     softmax_scale: float | None = None   # default 1/sqrt(head_dim)
     no_promotion: bool = False    # one-way Full -> Quantized -> Evicted policy
     score_decay: float = 1.0      # lambda of the decayed score; 1.0 = cumulative score
+    key_norm: bool = False        # key-norm score instead of attention
 
     @property
     def scale(self) -> float:
@@ -262,8 +264,11 @@ class QEvictUnit:
                 self.state[w] = OPEN
 
     # -- prefill (Sec. 4.2: prompt attention initialises the scores and the first assignment)
-    def prefill(self, k, v, init_scores):
-        """k, v: float64 [H_kv, T, d] bf16 values; init_scores: per window."""
+    def prefill(self, k, v, init_scores, route=True):
+        """k, v: float64 [H_kv, T, d] bf16 values; init_scores: per window
+        (unused with the key-norm score, which the keys determine).  With
+        route=False the first assignment waits for finish_prefill(), so that a
+        lockstep comparison can look at the scores first."""
         c = self.cfg
         T = k.shape[1]
         self.k[:, :T] = k
@@ -271,17 +276,36 @@ class QEvictUnit:
         self.T = T
         self._start_windows()
         n = int(np.sum(self.state >= 0))
-        init = np.asarray(init_scores, dtype=np.float64)
-        self.score[:n] = init[:n]
+        if c.key_norm:
+            for w in range(n):
+                a, b = self.win_range(w)
+                self.score[w] = -self._key_norms(a, min(b, T)).sum() / c.window
+        else:
+            init = np.asarray(init_scores, dtype=np.float64)
+            self.score[:n] = init[:n]
+        if route:
+            self.finish_prefill()
+
+    def finish_prefill(self):
+        """The first assignment after the prompt (Sec. 4.2)."""
         self._age()
         self.route()
 
+    def _key_norms(self, a, b):
+        """L2 norm of each token's key in [a, b) over all KV heads and channels
+        (appendix on alternative ranking functions, key-norm equation)."""
+        return np.sqrt(np.sum(self.k[:, a:b, :] ** 2, axis=(0, 2)))
+
     # -- one decode step ----------------------------------------------------
     def append(self, k_new, v_new):
+        c = self.cfg
         self.k[:, self.T] = k_new
         self.v[:, self.T] = v_new
         self.T += 1
         self._start_windows()
+        if c.key_norm and self.T - 1 >= c.sink:   # the token's share of its window's key-norm score
+            w = (self.T - 1 - c.sink) // c.window
+            self.score[w] -= self._key_norms(self.T - 1, self.T)[0] / c.window
         self._age()
 
     def accessible(self):
@@ -339,7 +363,8 @@ class QEvictUnit:
         if self.new_period and c.score_decay != 1.0:
             self.score[live] *= c.score_decay
         self.new_period = False
-        self.score[live] += mass[:, live].sum(axis=0) / c.num_q_heads
+        if not c.key_norm:
+            self.score[live] += mass[:, live].sum(axis=0) / c.num_q_heads
         return out, mass, sink_mass
 
     def step(self, q, k_new, v_new):

@@ -696,6 +696,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
   __shared__ float sml[2][kSplitGroups];
   __shared__ float sM[64], sL[64];
   __shared__ float smass[kMergeThreads];
+  __shared__ float skn[kMergeThreads];
 
   if (blk < nh) {
     // ---- output of head h: thread (c4, grp) owns channels 4c4..4c4+3 of splits grp + 8i ----
@@ -815,6 +816,28 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
     }
   }
   __syncthreads();
+  // key-norm scores: this step's token adds -|k_new| / W (norm over all KV heads)
+  // to its window, found by the block holding that window's list position
+  int kn_pos = -1;
+  float kn_delta = 0.f;
+  if (a.key_norm && a.T - 1 >= G.sink) {
+    kn_pos = n_fq + ((a.T - 1 - G.sink) / G.W - a.ring_w0);
+    if (blk - nh == kn_pos / per_blk) {   // uniform per block
+      const uint16_t* kn = a.k_new + (int64_t)b * G.H_kv * kHeadDim;
+      float sq = 0.f;
+      for (int i = tid; i < G.H_kv * kHeadDim; i += kMergeThreads) {
+        const float x = bf16_to_f32(kn[i]);
+        sq = fmaf(x, x, sq);
+      }
+      skn[tid] = sq;
+      __syncthreads();
+      for (int o = kMergeThreads / 2; o > 0; o >>= 1) {
+        if (tid < o) skn[tid] += skn[tid + o];
+        __syncthreads();
+      }
+      kn_delta = -sqrtf(skn[0]) / (float)G.W;
+    }
+  }
   const int n_all = n_fq + a.n_ring + a.n_sink_items;
   const bool active = in_blk && pos < n_all;
   const float mass = (active && sL[hh] > 0.f && mr.x > -INFINITY)
@@ -847,7 +870,8 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
     else atomicAdd(&dbg[(int64_t)hh * (G.nwc + 1) + G.nwc], mass);
   }
   if (hh == 0 && win >= 0) {
-    const float ns = old_score * a.decay + tot / (float)nh;
+    const float ns = a.key_norm ? old_score + (pos == kn_pos ? kn_delta : 0.f)
+                                : old_score * a.decay + tot / (float)nh;
     ((float*)(ub + a.L.score))[win] = ns;
     iscore[pos] = ns;   // the next re-rank and merge read it by list position
   }

@@ -28,6 +28,7 @@ struct AttnArgs {
   int32_t n_ring;           // windows in [ring_w0, ring_w0 + n_ring) are attended from the ring
   int32_t n_sink_items;     // sink slots holding sink tokens
   float decay;              // factor on every updated window score before this step's mass
+  int32_t key_norm;         // 1: key-norm scores (no attention masses; the new token's key norm)
 };
 
 struct RetierArgs {
@@ -49,6 +50,13 @@ struct MigrateArgs {
   const uint16_t* src_k;    // prompt keys [B][H_kv][T][d] (prefill only)
   const uint16_t* src_v;
   int32_t src_T;
+};
+
+struct KeyNormArgs {        // key-norm scores of the prompt windows
+  Geometry g;
+  const uint16_t* k;        // [B][H_kv][T][d] bf16 prompt keys
+  int32_t T, n_init;
+  float* out;               // [B][n_init]
 };
 
 struct PackArgs {           // copy prompt tokens into ring / sink slots

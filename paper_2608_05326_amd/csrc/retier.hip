@@ -833,6 +833,50 @@ __global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
   counts[CNT_PLAN_T] = -1;   // the split plan no longer matches the list
 }
 
+// Key-norm scores of the prompt windows (appendix, key-norm equation):
+// S(w) = -(1/W) sum over the window's prompt tokens of |k_t|, |k_t| the L2 norm
+// of token t's key over all KV heads.  One workgroup per (window, sequence);
+// thread (token, head) sums its 128 squares, heads then tokens are summed in a
+// fixed order.
+__global__ __launch_bounds__(256) void k_key_norm_init(KeyNormArgs a) {
+  const Geometry& G = a.g;
+  const int w = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  __shared__ float ssq[256];
+  __shared__ float snorm[64];
+  const int t0 = G.sink + w * G.W, t1 = min(t0 + G.W, a.T);
+  const int nt = t1 - t0;
+  for (int base = 0; base < G.W; base += 256 / G.H_kv) {
+    const int lt = base + tid / G.H_kv, g = tid % G.H_kv;
+    float sq = 0.f;
+    if (tid < (256 / G.H_kv) * G.H_kv && lt < nt) {
+      const u32x4* row = (const u32x4*)(a.k + (((int64_t)b * G.H_kv + g) * a.T + t0 + lt) * kHeadDim);
+#pragma unroll 4
+      for (int i = 0; i < kHeadDim / 8; ++i) {
+        const u32x4 x = row[i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float lo = __uint_as_float(x[j] << 16), hi = __uint_as_float(x[j] & 0xFFFF0000u);
+          sq = fmaf(lo, lo, sq);
+          sq = fmaf(hi, hi, sq);
+        }
+      }
+    }
+    ssq[tid] = sq;
+    __syncthreads();
+    if (tid < 256 / G.H_kv && base + tid < G.W) {
+      float s2 = 0.f;
+      for (int h = 0; h < G.H_kv; ++h) s2 += ssq[tid * G.H_kv + h];
+      snorm[base + tid] = base + tid < nt ? sqrtf(s2) : 0.f;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    float s = 0.f;
+    for (int t = 0; t < G.W; ++t) s += snorm[t];
+    a.out[(int64_t)b * a.n_init + w] = -s / (float)G.W;
+  }
+}
+
 // State initialisation of every unit block (grid-stride over units).
 __global__ void k_init_units(Geometry G, UnitLayout L, uint8_t* base, int n_units) {
   for (int u = blockIdx.x; u < n_units; u += gridDim.x) {
@@ -855,6 +899,12 @@ __global__ void k_init_units(Geometry G, UnitLayout L, uint8_t* base, int n_unit
     u32x4* z = (u32x4*)(ub + L.ring);
     for (int64_t i = threadIdx.x; i < nz; i += blockDim.x) z[i] = (u32x4){0, 0, 0, 0};
   }
+}
+
+hipError_t launch_key_norm_init(const KeyNormArgs& a, hipStream_t st) {
+  if (a.n_init <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_key_norm_init, dim3(a.n_init, a.g.B), dim3(256), 0, st, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_retier(const RetierArgs& a, hipStream_t st) {

@@ -32,6 +32,7 @@ hipError_t launch_init_units(const Geometry& g, const UnitLayout& L, uint8_t* ba
                              hipStream_t st);
 hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, hipStream_t st);
 hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st);
+hipError_t launch_key_norm_init(const KeyNormArgs& a, hipStream_t st);
 }  // namespace qv
 
 using namespace qv;
@@ -139,7 +140,8 @@ qevict_status check_config(const qevict_config* c) {
     return fail(QEVICT_ERR_INVALID_ARG, "unknown flags 0x%x", c->flags);
   if (!(c->softmax_scale >= 0.f) || !std::isfinite(c->softmax_scale))
     return fail(QEVICT_ERR_INVALID_ARG, "softmax_scale");
-  if (c->score_mode != QEVICT_SCORE_CUMULATIVE && c->score_mode != QEVICT_SCORE_DECAY)
+  if (c->score_mode != QEVICT_SCORE_CUMULATIVE && c->score_mode != QEVICT_SCORE_DECAY &&
+      c->score_mode != QEVICT_SCORE_KEY_NORM)
     return fail(QEVICT_ERR_INVALID_ARG, "score_mode");
   if (c->score_mode == QEVICT_SCORE_DECAY && !(c->score_decay > 0.f && c->score_decay <= 1.f))
     return fail(QEVICT_ERR_INVALID_ARG, "score_decay must be in (0, 1]");
@@ -252,6 +254,12 @@ bool ring_and_sink_adjacent(const UnitLayout& L, const Geometry& g) {
 
 qevict_status hip_fail(hipError_t e, const char* what) {
   return fail(QEVICT_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Key-norm mode: prompt window scores are computed into a staging area after
+// the units ([B][n_w] fp32), then routed like caller-supplied initial scores.
+int64_t key_norm_staging_bytes(const qevict_config* cfg, const Geometry& g) {
+  return cfg->score_mode == QEVICT_SCORE_KEY_NORM ? align256(4LL * g.B * g.nwc) : 0;
 }
 
 uint8_t* unit_base(qevict_cache* c, int layer, int seq) {
@@ -445,7 +453,8 @@ qevict_status qevict_workspace_size(const qevict_config* cfg, size_t* bytes) {
   Geometry g;
   UnitLayout L;
   plan(cfg, &g, &L);
-  *bytes = (size_t)(kHeaderBytes + (int64_t)cfg->num_layers * cfg->batch * L.unit_bytes);
+  *bytes = (size_t)(kHeaderBytes + (int64_t)cfg->num_layers * cfg->batch * L.unit_bytes +
+                    key_norm_staging_bytes(cfg, g));
   return QEVICT_OK;
 }
 
@@ -526,7 +535,8 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
   LayerState& ls = c->layers[layer];
   const Geometry& g = c->g;
   if (ls.prefilled) return fail(QEVICT_ERR_BAD_STATE, "layer %d already prefilled", layer);
-  if (!k || !v || !init_scores) return fail(QEVICT_ERR_INVALID_ARG, "null prompt pointer");
+  const bool key_norm = c->cfg.score_mode == QEVICT_SCORE_KEY_NORM;
+  if (!k || !v || (!init_scores && !key_norm)) return fail(QEVICT_ERR_INVALID_ARG, "null prompt pointer");
   if (((uintptr_t)k & 15) || ((uintptr_t)v & 15))
     return fail(QEVICT_ERR_INVALID_ARG, "prompt keys / values must be 16-byte aligned");
   if (prompt_len < g.sink || prompt_len < 1 || prompt_len > c->cfg.max_context)
@@ -548,6 +558,13 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
     pa.tok0 = g.sink + n_hist * g.W;
     pa.tok1 = prompt_len;
     e = launch_pack_tokens(pa, c->stream);            // tail: recent region and partial window
+  }
+  if (key_norm && e == hipSuccess) {
+    float* staging = (float*)(c->ws + kHeaderBytes +
+                              (int64_t)c->cfg.num_layers * g.B * c->L.unit_bytes);
+    KeyNormArgs ka{gg, k, prompt_len, n_init, staging};
+    e = launch_key_norm_init(ka, c->stream);
+    init_scores = staging;
   }
   RetierArgs ra{gg, L, base, 1, 0, n_hist, init_scores, n_init, -1, 0};
   plan_next(g, c->cfg.max_context, prompt_len + 1, n_hist, &ra.plan_T, &ra.plan_extra);
@@ -590,6 +607,7 @@ qevict_status qevict_decode_attend(qevict_cache* c, int32_t layer, const uint16_
   a.n_ring = n_ring;
   a.n_sink_items = g.NS;
   a.decay = (c->cfg.score_mode == QEVICT_SCORE_DECAY && ls.decay_pending) ? c->cfg.score_decay : 1.0f;
+  a.key_norm = c->cfg.score_mode == QEVICT_SCORE_KEY_NORM;
   hipError_t e = hipSuccess;
   if (g.flags & QEVICT_FLAG_DEBUG_MASSES) {
     for (int b = 0; b < g.B && e == hipSuccess; ++b)

@@ -25,7 +25,7 @@ BITS_MIXED_4_2 = 42
 OUT_F32, OUT_BF16 = 0, 1
 FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING = 0x1, 0x2, 0x4
 KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_MIGRATE = range(4)
-SCORE_CUMULATIVE, SCORE_DECAY = 0, 1
+SCORE_CUMULATIVE, SCORE_DECAY, SCORE_KEY_NORM = 0, 1, 2
 
 # exported symbols declared in include/qevict.h
 SYMBOLS = (
@@ -196,12 +196,13 @@ class Cache:
         _check(self.lib, status)
 
     # -- the decode path --
-    def prefill_assign(self, layer: int, k, v, init_scores):
-        """k, v: bf16 [B, H_kv, T, d]; init_scores: float32 [B, n_w]."""
+    def prefill_assign(self, layer: int, k, v, init_scores=None):
+        """k, v: bf16 [B, H_kv, T, d]; init_scores: float32 [B, n_w] (None with
+        the key-norm score)."""
         t = self.torch
+        sc = None if init_scores is None else _ptr(init_scores, t.float32, "init_scores")
         self._c(self.lib.qevict_prefill_assign(
-            self.handle, layer, _ptr(k, t.bfloat16, "k"), _ptr(v, t.bfloat16, "v"), k.shape[2],
-            _ptr(init_scores, t.float32, "init_scores")))
+            self.handle, layer, _ptr(k, t.bfloat16, "k"), _ptr(v, t.bfloat16, "v"), k.shape[2], sc))
 
     def decode_attend(self, layer: int, q, k_new, v_new, out):
         t = self.torch

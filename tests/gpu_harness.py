@@ -33,7 +33,9 @@ def to_dev_bf16(bits: np.ndarray) -> torch.Tensor:
 
 def gpu_config(wl: syn.Workload, layers: int, flags: int = 0, out_dtype: int = qv.OUT_F32,
                num_splits: int = 0, capacity_full=None, capacity_quant=None,
-               score_decay: float | None = None) -> qv.Config:
+               score_decay: float | None = None, key_norm: bool = False) -> qv.Config:
+    mode = qv.SCORE_KEY_NORM if key_norm else \
+        qv.SCORE_DECAY if score_decay is not None else qv.SCORE_CUMULATIVE
     return qv.Config(
         batch=wl.batch, num_layers=layers, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
         window_tokens=wl.window, group_size=wl.group, quant_bits=wl.bits, max_context=wl.max_context,
@@ -41,8 +43,7 @@ def gpu_config(wl: syn.Workload, layers: int, flags: int = 0, out_dtype: int = q
         capacity_quant=wl.capacity_quant if capacity_quant is None else capacity_quant,
         sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=wl.retier_interval,
         out_dtype=out_dtype, flags=flags, num_splits=num_splits,
-        score_mode=qv.SCORE_DECAY if score_decay is not None else qv.SCORE_CUMULATIVE,
-        score_decay=score_decay or 0.0)
+        score_mode=mode, score_decay=score_decay or 0.0)
 
 
 def oracle_config(cfg: qv.Config) -> OracleConfig:
@@ -51,7 +52,8 @@ def oracle_config(cfg: qv.Config) -> OracleConfig:
                         cfg.capacity_quant, sink=cfg.sink_tokens, recent=cfg.recent_tokens,
                         no_promotion=bool(cfg.flags & qv.FLAG_NO_PROMOTION),
                         score_decay=float(np.float32(cfg.score_decay))
-                        if cfg.score_mode == qv.SCORE_DECAY else 1.0)
+                        if cfg.score_mode == qv.SCORE_DECAY else 1.0,
+                        key_norm=cfg.score_mode == qv.SCORE_KEY_NORM)
 
 
 class Lockstep:
@@ -63,14 +65,17 @@ class Lockstep:
 
     def __init__(self, wl: syn.Workload, seed: int = 0, layer_ids=(0,), check_seqs=None,
                  flags: int = 0, num_splits: int = 0, steps: int | None = None, log=print,
-                 capacity_full=None, capacity_quant=None, score_decay: float | None = None):
+                 capacity_full=None, capacity_quant=None, score_decay: float | None = None,
+                 key_norm: bool = False):
         self.wl, self.seed = wl, seed
         self.layer_ids = list(layer_ids)
         self.check_seqs = list(range(wl.batch)) if check_seqs is None else list(check_seqs)
         self.steps = wl.steps if steps is None else steps
         self.cfg = gpu_config(wl, len(self.layer_ids), flags | qv.FLAG_DEBUG_MASSES,
                               num_splits=num_splits, capacity_full=capacity_full,
-                              capacity_quant=capacity_quant, score_decay=score_decay)
+                              capacity_quant=capacity_quant, score_decay=score_decay,
+                              key_norm=key_norm)
+        self.key_norm = key_norm
         self.cache = qv.Cache(self.cfg)
         self.ocfg = oracle_config(self.cfg)
         self.units = {(li, b): QEvictUnit(self.ocfg, wl.max_context)
@@ -148,16 +153,28 @@ class Lockstep:
                 vs.append(v)
                 inits.append(init)
                 if (li, b) in self.units:
-                    self.units[(li, b)].prefill(from_bf16_bits(k), from_bf16_bits(v), init)
+                    # the key-norm score comes from the keys: the GPU computes its own
+                    self.units[(li, b)].prefill(from_bf16_bits(k), from_bf16_bits(v), init,
+                                                route=not self.key_norm)
             del prompts
             K = to_dev_bf16(np.stack(ks))
             V = to_dev_bf16(np.stack(vs))
-            S = torch.from_numpy(np.stack(inits)).cuda()
+            S = None if self.key_norm else torch.from_numpy(np.stack(inits)).cuda()
             self.cache.prefill_assign(li, K, V, S)
             torch.cuda.synchronize()
             del K, V
             for b in self.check_seqs:
                 u = self.units[(li, b)]
+                if self.key_norm:
+                    # fp32 sums against fp64 ones: check the scores, then route both
+                    # with the GPU's so that near-ties rank alike
+                    st = self.cache.get_state(li, b)
+                    n = st["n"]
+                    so, sg = u.score[:n], st["scores"].astype(np.float64)
+                    err = np.abs(sg - so) / np.maximum(np.abs(so), 1e-7 * np.abs(so).sum())
+                    assert np.all(err <= SCORE_TOL), f"prefill key-norm score rel err {err.max():.3e}"
+                    u.adopt_scores(sg)
+                    u.finish_prefill()
                 self.compare_state(li, b)
                 self.compare_ledgers(li, b, sorted(u.ledger))
                 full = [w for w in range(u.n_win_cap) if u.state[w] == 2]

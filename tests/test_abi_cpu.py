@@ -51,7 +51,7 @@ def test_workspace_size_of_the_8b_32k_layer():
     (dict(flags=0x80), qv.qevict.ERR_INVALID_ARG),
     (dict(max_context=0), qv.qevict.ERR_INVALID_ARG),
     (dict(sink_tokens=65 * 32), qv.qevict.ERR_UNSUPPORTED),
-    (dict(score_mode=2), qv.qevict.ERR_INVALID_ARG),
+    (dict(score_mode=3), qv.qevict.ERR_INVALID_ARG),
     (dict(score_mode=qv.SCORE_DECAY, score_decay=0.0), qv.qevict.ERR_INVALID_ARG),
     (dict(score_mode=qv.SCORE_DECAY, score_decay=1.5), qv.qevict.ERR_INVALID_ARG),
 ])
@@ -61,9 +61,12 @@ def test_bad_configs_are_rejected(kw, status):
     assert e.value.status == status
 
 
-def test_decayed_score_config_is_accepted():
-    assert qv.workspace_size(_cfg(score_mode=qv.SCORE_DECAY, score_decay=0.99)) == \
-        qv.workspace_size(_cfg())
+def test_ranking_modes_are_accepted():
+    base = qv.workspace_size(_cfg())
+    assert qv.workspace_size(_cfg(score_mode=qv.SCORE_DECAY, score_decay=0.99)) == base
+    # key-norm mode stages the prompt windows' scores ([B][n_w] fp32) after the units
+    kn = qv.workspace_size(_cfg(score_mode=qv.SCORE_KEY_NORM))
+    assert base + 4 * 1028 <= kn <= base + 4 * 1028 + 256
 
 
 def test_status_strings():

@@ -40,3 +40,11 @@ def test_decayed_score_lockstep(name, decay):
     """Exponentially decayed ranking (lambda per routing period; c5s routes every
     8 steps): scores and routing against the oracle."""
     _lockstep(name, score_decay=decay)
+
+
+@pytest.mark.parametrize("name", ["c2s", "c4s"])
+def test_key_norm_lockstep(name):
+    """Key-norm ranking (scores from the keys alone, computed by the prefill
+    kernel and the merge's per-token update): scores and routing against the
+    oracle."""
+    _lockstep(name, key_norm=True)

@@ -11,7 +11,12 @@ previous routing event).
 * lambda just below 1 stays on the cumulative trajectory, on random inputs
   with routing;
 * a small lambda changes which windows survive: recent attention outweighs
-  old attention that the cumulative score still remembers.
+  old attention that the cumulative score still remembers;
+* key-norm score: a closed form for keys whose norm is the token index + 1
+  (prefill and decode), independence from the queries, routing keeps the
+  lowest-norm windows (a zero-key window first; doubling a window's keys
+  doubles its score), and windows completed during decode score as a prefill
+  of the same tokens does.
 """
 import numpy as np
 import pytest
@@ -122,3 +127,83 @@ def test_strong_decay_prefers_recent_attention():
     assert cum.state[0] == FULL and cum.state[1] == QUANT
     assert dec.state[1] == FULL and dec.state[0] == QUANT
     assert cum.score[0] > cum.score[1] and dec.score[1] > dec.score[0]
+
+
+# ---- key-norm score (appendix, key-norm equation) ----
+
+def _kn_unit(n_win, kf, kq, max_extra=40, heads=2):
+    cfg = OracleConfig(4, heads, 8, W, W, 4, kf, kq, key_norm=True)
+    return QEvictUnit(cfg, W * n_win + max_extra)
+
+
+def _ramp_keys(T, heads=2):
+    """Token i's key: head 0, channel 0 holds i + 1, everything else 0 (|k_i| = i + 1)."""
+    k = np.zeros((heads, T, 8))
+    k[0, :, 0] = np.arange(1, T + 1)
+    return k
+
+
+def test_key_norm_closed_form_prefill_and_decode():
+    n_win, steps = 4, 9
+    u = _kn_unit(n_win, 16, 0)
+    T0 = W * n_win
+    u.prefill(_ramp_keys(T0), np.ones((2, T0, 8)), None)
+    rng = np.random.default_rng(0)
+    for t in range(steps):
+        kn = np.zeros((2, 8))
+        kn[0, 0] = T0 + t + 1
+        u.step(rng.normal(size=(4, 8)), kn, np.ones((2, 8)))
+        u.route()
+    T = T0 + steps
+    for w in range(-(-T // W)):
+        n_tok = min(W, T - w * W)
+        expect = -sum(range(w * W + 1, w * W + n_tok + 1)) / W
+        assert u.score[w] == pytest.approx(expect, rel=1e-14), w
+
+
+def test_key_norm_ignores_attention():
+    def run(seed):
+        rng = np.random.default_rng(seed)
+        u = _kn_unit(8, 2, 2)
+        T0 = 8 * W
+        kk = np.random.default_rng(7).normal(size=(2, T0 + 12, 8))
+        u.prefill(kk[:, :T0], np.ones((2, T0, 8)), None)
+        for t in range(12):
+            u.step(rng.normal(size=(4, 8)) * 5, kk[:, T0 + t], np.ones((2, 8)))
+            u.route()
+        return u
+    a, b = run(1), run(2)
+    assert np.array_equal(a.score, b.score) and np.array_equal(a.state, b.state)
+
+
+def test_key_norm_keeps_the_lowest_norm_windows():
+    """Windows' keys scaled by distinct factors: Full gets the smallest norm,
+    Quantized the next, the rest are evicted; a zero-key window (score 0, the
+    largest possible) goes first."""
+    n_win = 6
+    factors = [3.0, 0.0, 5.0, 1.0, 2.0, 4.0]
+    u = _kn_unit(n_win, 2, 2)
+    rng = np.random.default_rng(3)
+    base = rng.normal(size=(2, W, 8))
+    k = np.concatenate([base * f for f in factors], axis=1)
+    u.prefill(k, np.ones((2, n_win * W, 8)), None)
+    order = sorted(range(n_win), key=lambda w: (factors[w], w))
+    assert [u.state[w] for w in order] == [FULL, FULL, QUANT, QUANT, EVICTED, EVICTED]
+    assert u.score[1] == 0.0
+    # scaling a window's keys by 2 doubles its score exactly
+    assert u.score[4] == pytest.approx(2.0 * u.score[3], rel=1e-15)
+
+
+def test_key_norm_decode_accumulation_matches_prefill():
+    """Scores of windows completed during decode equal the scores a prefill of
+    the same tokens gives."""
+    n0, steps = 5 * W, 3 * W + 2
+    kk = np.random.default_rng(11).normal(size=(2, n0 + steps, 8))
+    a = _kn_unit(8, 16, 0)
+    a.prefill(kk[:, :n0], np.ones((2, n0, 8)), None)
+    for t in range(steps):
+        a.step(np.zeros((4, 8)), kk[:, n0 + t], np.ones((2, 8)))
+    b = _kn_unit(8, 16, 0)
+    b.prefill(kk, np.ones((2, n0 + steps, 8)), None)
+    n = -(-(n0 + steps) // W)
+    assert np.allclose(a.score[:n], b.score[:n], rtol=1e-13, atol=0)
