@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define QEVICT_ABI_VERSION 2
+#define QEVICT_ABI_VERSION 3
 
 typedef struct qevict_cache qevict_cache;
 typedef int32_t qevict_status;
@@ -100,6 +100,14 @@ enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT =
  *   is ignored and may be NULL) and every decode step adds the new token's
  *   share -|k_new| / W to its window; attention masses are not accumulated. */
 #define QEVICT_SCORE_KEY_NORM 2
+/* PNORM: the attention p-norm S_t = (sum_r u_r^p)^(1/p) over the routing
+ *   periods r <= t, u_r the attention w received in period r (appendix,
+ *   p-norm equation; the prompt's init_scores are the first period's u).
+ *   Scores hold S^p, which orders windows exactly as S does: the sum over
+ *   completed periods plus u^p of the period in progress, so that a routing
+ *   event at any step ranks by the norm as it stands.  Uses 8 more bytes of
+ *   workspace per window (completed-period sum and running u). */
+#define QEVICT_SCORE_PNORM 3
 
 typedef struct {
   int32_t abi_version;       /* QEVICT_ABI_VERSION                                          */
@@ -123,8 +131,9 @@ typedef struct {
   uint32_t flags;            /* QEVICT_FLAG_*                                                */
   float softmax_scale;       /* 0 selects 1/sqrt(head_dim)                                    */
   int32_t num_splits;        /* split-K factor of the attention pass; 0 = automatic          */
-  int32_t score_mode;        /* QEVICT_SCORE_CUMULATIVE (0), _DECAY or _KEY_NORM             */
+  int32_t score_mode;        /* QEVICT_SCORE_CUMULATIVE (0), _DECAY, _KEY_NORM or _PNORM     */
   float score_decay;         /* lambda of QEVICT_SCORE_DECAY, in (0, 1]                       */
+  float score_p;             /* p of QEVICT_SCORE_PNORM, in [1, 16]                           */
 } qevict_config;
 
 typedef struct {

@@ -15,8 +15,10 @@ What it computes, and where the paper defines it (QEvict, arXiv 2608.05326):
   score equation; the per-step reading is listed with the other readings).
   Optionally the exponentially decayed score S_t = lambda S_{t-R} + u_t of the
   appendix on alternative ranking functions (decayed score equation), u_t the
-  attention a window received since the previous routing event, or the
-  attention-free key-norm score of the same appendix (key-norm equation).
+  attention a window received since the previous routing event, the
+  attention p-norm (sum over routing periods r of u_r^p)^(1/p) (p-norm
+  equation), or the attention-free key-norm score of the same appendix
+  (key-norm equation).
 * Routing: the candidate pool is the previous Full and Quantized windows plus
   the windows that left the recent region; the top K_f by score go to Full,
   the next K_q to Quantized, the rest are evicted (Sec. 4.3, candidate pool
@@ -80,6 +82,7 @@ class OracleConfig:
     no_promotion: bool = False    # one-way Full -> Quantized -> Evicted policy
     score_decay: float = 1.0      # lambda of the decayed score; 1.0 = cumulative score
     key_norm: bool = False        # key-norm score instead of attention
+    score_p: float = 0.0          # p of the attention p-norm score; 0 = not used
 
     @property
     def scale(self) -> float:
@@ -243,6 +246,10 @@ class QEvictUnit:
         # decayed score: the first step after a routing event (or prefill) starts a new
         # period, S = lambda S_previous_event + (attention received during the period)
         self.new_period = False
+        # p-norm score: u of every completed routing period, per window, and the
+        # attention received in the period in progress
+        self.u_hist: list[list[float]] = [[] for _ in range(self.n_win_cap)]
+        self.u_cur = np.zeros(self.n_win_cap)
 
     # -- geometry ---------------------------------------------------------
     def win_range(self, w: int):
@@ -283,6 +290,12 @@ class QEvictUnit:
         else:
             init = np.asarray(init_scores, dtype=np.float64)
             self.score[:n] = init[:n]
+            if c.score_p:                 # prompt attention is the first period's u
+                if np.any(init[:n] < 0):
+                    raise ValueError("p-norm score: negative initial score")
+                for w in range(n):
+                    self.u_hist[w] = [float(init[w])]
+                self._pnorm_scores(np.arange(n))
         if route:
             self.finish_prefill()
 
@@ -290,6 +303,13 @@ class QEvictUnit:
         """The first assignment after the prompt (Sec. 4.2)."""
         self._age()
         self.route()
+
+    def _pnorm_scores(self, windows):
+        """score = S^p = sum over completed periods of u_r^p plus u^p of the period
+        in progress (appendix, p-norm equation; S^p orders windows as S does)."""
+        p = self.cfg.score_p
+        for w in windows:
+            self.score[w] = sum(u ** p for u in self.u_hist[w]) + self.u_cur[w] ** p
 
     def _key_norms(self, a, b):
         """L2 norm of each token's key in [a, b) over all KV heads and channels
@@ -363,7 +383,10 @@ class QEvictUnit:
         if self.new_period and c.score_decay != 1.0:
             self.score[live] *= c.score_decay
         self.new_period = False
-        if not c.key_norm:
+        if c.score_p:
+            self.u_cur[live] += mass[:, live].sum(axis=0) / c.num_q_heads
+            self._pnorm_scores(np.nonzero(live)[0])
+        elif not c.key_norm:
             self.score[live] += mass[:, live].sum(axis=0) / c.num_q_heads
         return out, mass, sink_mass
 
@@ -430,6 +453,10 @@ class QEvictUnit:
             self.state[w] = EVICTED
             self.stats["evictions"] += 1
         self.new_period = True
+        if c.score_p:                     # the routing event closes the period
+            for w in np.nonzero(self.state >= 0)[0]:
+                self.u_hist[w].append(float(self.u_cur[w]))
+                self.u_cur[w] = 0.0
         return full, quant, evict
 
     # -- single-window moves outside a routing event --------------------------

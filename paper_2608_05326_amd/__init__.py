@@ -13,4 +13,5 @@ from .qevict import (  # noqa: F401
     LEDGER_NONE, LEDGER_ACTIVE, LEDGER_DORMANT, BITS_MIXED_4_2, OUT_F32, OUT_BF16,
     FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING,
     KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_MIGRATE, SCORE_CUMULATIVE, SCORE_DECAY, SCORE_KEY_NORM,
+    SCORE_PNORM,
 )

@@ -870,8 +870,21 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
     else atomicAdd(&dbg[(int64_t)hh * (G.nwc + 1) + G.nwc], mass);
   }
   if (hh == 0 && win >= 0) {
-    const float ns = a.key_norm ? old_score + (pos == kn_pos ? kn_delta : 0.f)
-                                : old_score * a.decay + tot / (float)nh;
+    float ns;
+    if (a.key_norm) {
+      ns = old_score + (pos == kn_pos ? kn_delta : 0.f);
+    } else if (a.pnorm_p > 0.f) {
+      // p-norm: {sum of completed periods' u^p, u of this period}; the score
+      // is their sum with u^p.  A period's first step closes the previous one,
+      // whose u^p the old score already includes.
+      float2* pu = (float2*)(ub + a.L.pnorm) + win;
+      float2 st = a.period_start ? make_float2(old_score, 0.f) : *pu;
+      st.y += tot / (float)nh;
+      ns = st.x + powf(st.y, a.pnorm_p);
+      *pu = st;
+    } else {
+      ns = old_score * a.decay + tot / (float)nh;
+    }
     ((float*)(ub + a.L.score))[win] = ns;
     iscore[pos] = ns;   // the next re-rank and merge read it by list position
   }

@@ -29,6 +29,8 @@ struct AttnArgs {
   int32_t n_sink_items;     // sink slots holding sink tokens
   float decay;              // factor on every updated window score before this step's mass
   int32_t key_norm;         // 1: key-norm scores (no attention masses; the new token's key norm)
+  float pnorm_p;            // > 0: attention p-norm scores with this p
+  int32_t period_start;     // 1: first step after a routing event (or prefill)
 };
 
 struct RetierArgs {
@@ -57,6 +59,13 @@ struct KeyNormArgs {        // key-norm scores of the prompt windows
   const uint16_t* k;        // [B][H_kv][T][d] bf16 prompt keys
   int32_t T, n_init;
   float* out;               // [B][n_init]
+};
+
+struct ScorePowArgs {       // p-norm ranking: prompt scores raised to the power p
+  const float* in;
+  float* out;
+  int32_t n;
+  float p;
 };
 
 struct PackArgs {           // copy prompt tokens into ring / sink slots

@@ -74,6 +74,8 @@ constexpr int kSpareFull = 8;
 // sink windows per sequence (keeps the attention split costs in 32 bits)
 constexpr int kMaxSinkWindows = 64;
 
+constexpr int kScorePnorm = 3;   // score_mode of the attention p-norm ranking
+
 struct Geometry {
   int32_t B, H_q, H_kv, gqa, d, W, G;
   int32_t bits_cfg;     // 4, 2 or 42
@@ -89,6 +91,7 @@ struct Geometry {
   int32_t n_split;
   int32_t out_bf16;
   uint32_t flags;
+  int32_t score_mode;   // window ranking function (cumulative, decayed, key norm, p-norm)
   float scale_log2;     // softmax scale * log2(e)
   int64_t fhead_bytes;  // one KV head of a bf16 slot: W*d*2 (K) + W*d*2 (V)
   int64_t fslot_bytes;  // H_kv * fhead_bytes
@@ -107,6 +110,7 @@ struct UnitLayout {
   int64_t qlist, plist, counts, stats;
   int64_t partial, pml, mref, dbg_mass;
   int64_t plan;         // per (split, wave): first item, end item, refs of its first kPlanRefs items
+  int64_t pnorm;        // p-norm ranking only: per window {sum of completed periods' u^p, running u}
 };
 
 QV_HD int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }

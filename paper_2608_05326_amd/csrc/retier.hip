@@ -877,6 +877,16 @@ __global__ __launch_bounds__(256) void k_key_norm_init(KeyNormArgs a) {
   }
 }
 
+// p-norm ranking: the prompt's initial scores are the first routing period's
+// attention u_0, entering the score as u_0^p (appendix, p-norm equation).  A
+// negative score yields NaN, which the re-rank kernel reports as non-finite.
+__global__ __launch_bounds__(256) void k_score_pow(ScorePowArgs a) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= a.n) return;
+  const float x = a.in[i];
+  a.out[i] = x >= 0.f ? powf(x, a.p) : __builtin_nanf("");
+}
+
 // State initialisation of every unit block (grid-stride over units).
 __global__ void k_init_units(Geometry G, UnitLayout L, uint8_t* base, int n_units) {
   for (int u = blockIdx.x; u < n_units; u += gridDim.x) {
@@ -888,6 +898,7 @@ __global__ void k_init_units(Geometry G, UnitLayout L, uint8_t* base, int n_unit
       ((int32_t*)(ub + L.fslot))[w] = -1;
       ((int32_t*)(ub + L.qslot))[w] = -1;
       ((float*)(ub + L.score))[w] = 0.f;
+      if (G.score_mode == kScorePnorm) ((float2*)(ub + L.pnorm))[w] = make_float2(0.f, 0.f);
     }
     for (int i = threadIdx.x; i < G.n_fslots; i += blockDim.x) ((int32_t*)(ub + L.fowner))[i] = -1;
     for (int i = threadIdx.x; i < G.n_qslots; i += blockDim.x) ((int32_t*)(ub + L.qowner))[i] = -1;
@@ -904,6 +915,12 @@ __global__ void k_init_units(Geometry G, UnitLayout L, uint8_t* base, int n_unit
 hipError_t launch_key_norm_init(const KeyNormArgs& a, hipStream_t st) {
   if (a.n_init <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_key_norm_init, dim3(a.n_init, a.g.B), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_pow(const ScorePowArgs& a, hipStream_t st) {
+  if (a.n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_score_pow, dim3((a.n + 255) / 256), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -33,9 +33,11 @@ hipError_t launch_init_units(const Geometry& g, const UnitLayout& L, uint8_t* ba
 hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, hipStream_t st);
 hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st);
 hipError_t launch_key_norm_init(const KeyNormArgs& a, hipStream_t st);
+hipError_t launch_score_pow(const ScorePowArgs& a, hipStream_t st);
 }  // namespace qv
 
 using namespace qv;
+static_assert(kScorePnorm == QEVICT_SCORE_PNORM, "score mode numbering");
 
 namespace {
 
@@ -60,7 +62,7 @@ struct LayerState {
   int T = 0;              // tokens held (all sequences)
   int routed_end = 0;     // windows below this index have been routed
   bool prefilled = false;
-  bool decay_pending = false;   // a routing event (or prefill) since the last decode step
+  bool period_start = false;    // a routing event (or prefill) since the last decode step
   int64_t last_bytes = 0;
 };
 
@@ -141,8 +143,10 @@ qevict_status check_config(const qevict_config* c) {
   if (!(c->softmax_scale >= 0.f) || !std::isfinite(c->softmax_scale))
     return fail(QEVICT_ERR_INVALID_ARG, "softmax_scale");
   if (c->score_mode != QEVICT_SCORE_CUMULATIVE && c->score_mode != QEVICT_SCORE_DECAY &&
-      c->score_mode != QEVICT_SCORE_KEY_NORM)
+      c->score_mode != QEVICT_SCORE_KEY_NORM && c->score_mode != QEVICT_SCORE_PNORM)
     return fail(QEVICT_ERR_INVALID_ARG, "score_mode");
+  if (c->score_mode == QEVICT_SCORE_PNORM && !(c->score_p >= 1.f && c->score_p <= 16.f))
+    return fail(QEVICT_ERR_INVALID_ARG, "score_p must be in [1, 16]");
   if (c->score_mode == QEVICT_SCORE_DECAY && !(c->score_decay > 0.f && c->score_decay <= 1.f))
     return fail(QEVICT_ERR_INVALID_ARG, "score_decay must be in (0, 1]");
   if (c->num_splits < 0 || c->num_splits > 256)
@@ -200,6 +204,7 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   g->n_split = ns;
   g->out_bf16 = c->out_dtype == QEVICT_OUT_BF16;
   g->flags = c->flags;
+  g->score_mode = c->score_mode;
   const float scale = c->softmax_scale > 0.f ? c->softmax_scale : 1.0f / std::sqrt((float)g->d);
   g->scale_log2 = scale * 1.4426950408889634f;
   g->fhead_bytes = (int64_t)g->W * g->d * 4;
@@ -245,6 +250,7 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   L->mref = take(8LL * g->H_q * g->max_items);
   L->dbg_mass = take((c->flags & QEVICT_FLAG_DEBUG_MASSES) ? 4LL * g->H_q * (g->nwc + 1) : 0);
   L->plan = take(4LL * kPlanRec * 4 * g->n_split);
+  L->pnorm = take(c->score_mode == QEVICT_SCORE_PNORM ? 8LL * g->nwc : 0);
   L->unit_bytes = align256(off);
 }
 
@@ -256,10 +262,12 @@ qevict_status hip_fail(hipError_t e, const char* what) {
   return fail(QEVICT_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
 }
 
-// Key-norm mode: prompt window scores are computed into a staging area after
-// the units ([B][n_w] fp32), then routed like caller-supplied initial scores.
-int64_t key_norm_staging_bytes(const qevict_config* cfg, const Geometry& g) {
-  return cfg->score_mode == QEVICT_SCORE_KEY_NORM ? align256(4LL * g.B * g.nwc) : 0;
+// Key-norm and p-norm modes: prompt window scores are computed into a staging
+// area after the units ([B][n_w] fp32), then routed like caller-supplied
+// initial scores.
+int64_t score_staging_bytes(const qevict_config* cfg, const Geometry& g) {
+  const bool used = cfg->score_mode == QEVICT_SCORE_KEY_NORM || cfg->score_mode == QEVICT_SCORE_PNORM;
+  return used ? align256(4LL * g.B * g.nwc) : 0;
 }
 
 uint8_t* unit_base(qevict_cache* c, int layer, int seq) {
@@ -454,7 +462,7 @@ qevict_status qevict_workspace_size(const qevict_config* cfg, size_t* bytes) {
   UnitLayout L;
   plan(cfg, &g, &L);
   *bytes = (size_t)(kHeaderBytes + (int64_t)cfg->num_layers * cfg->batch * L.unit_bytes +
-                    key_norm_staging_bytes(cfg, g));
+                    score_staging_bytes(cfg, g));
   return QEVICT_OK;
 }
 
@@ -559,11 +567,14 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
     pa.tok1 = prompt_len;
     e = launch_pack_tokens(pa, c->stream);            // tail: recent region and partial window
   }
+  float* staging = (float*)(c->ws + kHeaderBytes + (int64_t)c->cfg.num_layers * g.B * c->L.unit_bytes);
   if (key_norm && e == hipSuccess) {
-    float* staging = (float*)(c->ws + kHeaderBytes +
-                              (int64_t)c->cfg.num_layers * g.B * c->L.unit_bytes);
     KeyNormArgs ka{gg, k, prompt_len, n_init, staging};
     e = launch_key_norm_init(ka, c->stream);
+    init_scores = staging;
+  } else if (c->cfg.score_mode == QEVICT_SCORE_PNORM && e == hipSuccess) {
+    ScorePowArgs pa2{init_scores, staging, g.B * n_init, c->cfg.score_p};
+    e = launch_score_pow(pa2, c->stream);
     init_scores = staging;
   }
   RetierArgs ra{gg, L, base, 1, 0, n_hist, init_scores, n_init, -1, 0};
@@ -575,7 +586,7 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
   ls.T = prompt_len;
   ls.routed_end = n_hist;
   ls.prefilled = true;
-  ls.decay_pending = true;
+  ls.period_start = true;
   return QEVICT_OK;
 }
 
@@ -606,8 +617,10 @@ qevict_status qevict_decode_attend(qevict_cache* c, int32_t layer, const uint16_
   a.ring_w0 = ls.routed_end;
   a.n_ring = n_ring;
   a.n_sink_items = g.NS;
-  a.decay = (c->cfg.score_mode == QEVICT_SCORE_DECAY && ls.decay_pending) ? c->cfg.score_decay : 1.0f;
+  a.decay = (c->cfg.score_mode == QEVICT_SCORE_DECAY && ls.period_start) ? c->cfg.score_decay : 1.0f;
   a.key_norm = c->cfg.score_mode == QEVICT_SCORE_KEY_NORM;
+  a.pnorm_p = c->cfg.score_mode == QEVICT_SCORE_PNORM ? c->cfg.score_p : 0.f;
+  a.period_start = ls.period_start;
   hipError_t e = hipSuccess;
   if (g.flags & QEVICT_FLAG_DEBUG_MASSES) {
     for (int b = 0; b < g.B && e == hipSuccess; ++b)
@@ -618,7 +631,7 @@ qevict_status qevict_decode_attend(qevict_cache* c, int32_t layer, const uint16_
   if (e == hipSuccess) e = timed(c, 1, c->stream, [&] { return launch_merge(a, c->stream); });
   if (e != hipSuccess) return hip_fail(e, "decode_attend launch");
   ls.T = T;
-  ls.decay_pending = false;
+  ls.period_start = false;
   return QEVICT_OK;
 }
 
@@ -653,7 +666,7 @@ qevict_status qevict_retier(qevict_cache* c, int32_t layer, qevict_retier_stats*
   }
   if (e != hipSuccess) return hip_fail(e, "retier launch");
   if (a1 > a0) ls.routed_end = a1;
-  ls.decay_pending = true;
+  ls.period_start = true;
   if (stats) {
     memset(stats, 0, sizeof *stats);
     if ((e = join_layer(c, layer)) != hipSuccess) return hip_fail(e, "joining the routing stream");

@@ -16,7 +16,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libqevict.so")
 
-ABI_VERSION = 2
+ABI_VERSION = 3
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_BAD_STATE, ERR_NONFINITE, \
     ERR_CAPACITY, ERR_DEVICE = 0, -1, -2, -3, -4, -5, -6, -7
 TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED = 0, 1, 2, 3, 4
@@ -25,7 +25,7 @@ BITS_MIXED_4_2 = 42
 OUT_F32, OUT_BF16 = 0, 1
 FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING = 0x1, 0x2, 0x4
 KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_MIGRATE = range(4)
-SCORE_CUMULATIVE, SCORE_DECAY, SCORE_KEY_NORM = 0, 1, 2
+SCORE_CUMULATIVE, SCORE_DECAY, SCORE_KEY_NORM, SCORE_PNORM = 0, 1, 2, 3
 
 # exported symbols declared in include/qevict.h
 SYMBOLS = (
@@ -49,7 +49,7 @@ class _Config(ctypes.Structure):
         "window_tokens", "group_size", "quant_bits", "sink_tokens", "recent_tokens", "max_context",
         "capacity_full", "capacity_quant", "retier_interval", "out_dtype")] + [
         ("flags", ctypes.c_uint32), ("softmax_scale", ctypes.c_float), ("num_splits", ctypes.c_int32),
-        ("score_mode", ctypes.c_int32), ("score_decay", ctypes.c_float)]
+        ("score_mode", ctypes.c_int32), ("score_decay", ctypes.c_float), ("score_p", ctypes.c_float)]
 
 
 class RetierStats(ctypes.Structure):
@@ -83,6 +83,7 @@ class Config:
     num_splits: int = 0
     score_mode: int = SCORE_CUMULATIVE
     score_decay: float = 0.0
+    score_p: float = 0.0
 
     def to_c(self) -> _Config:
         c = _Config()

@@ -33,8 +33,9 @@ def to_dev_bf16(bits: np.ndarray) -> torch.Tensor:
 
 def gpu_config(wl: syn.Workload, layers: int, flags: int = 0, out_dtype: int = qv.OUT_F32,
                num_splits: int = 0, capacity_full=None, capacity_quant=None,
-               score_decay: float | None = None, key_norm: bool = False) -> qv.Config:
-    mode = qv.SCORE_KEY_NORM if key_norm else \
+               score_decay: float | None = None, key_norm: bool = False,
+               score_p: float | None = None) -> qv.Config:
+    mode = qv.SCORE_KEY_NORM if key_norm else qv.SCORE_PNORM if score_p is not None else \
         qv.SCORE_DECAY if score_decay is not None else qv.SCORE_CUMULATIVE
     return qv.Config(
         batch=wl.batch, num_layers=layers, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
@@ -43,7 +44,7 @@ def gpu_config(wl: syn.Workload, layers: int, flags: int = 0, out_dtype: int = q
         capacity_quant=wl.capacity_quant if capacity_quant is None else capacity_quant,
         sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=wl.retier_interval,
         out_dtype=out_dtype, flags=flags, num_splits=num_splits,
-        score_mode=mode, score_decay=score_decay or 0.0)
+        score_mode=mode, score_decay=score_decay or 0.0, score_p=score_p or 0.0)
 
 
 def oracle_config(cfg: qv.Config) -> OracleConfig:
@@ -53,7 +54,9 @@ def oracle_config(cfg: qv.Config) -> OracleConfig:
                         no_promotion=bool(cfg.flags & qv.FLAG_NO_PROMOTION),
                         score_decay=float(np.float32(cfg.score_decay))
                         if cfg.score_mode == qv.SCORE_DECAY else 1.0,
-                        key_norm=cfg.score_mode == qv.SCORE_KEY_NORM)
+                        key_norm=cfg.score_mode == qv.SCORE_KEY_NORM,
+                        score_p=float(np.float32(cfg.score_p))
+                        if cfg.score_mode == qv.SCORE_PNORM else 0.0)
 
 
 class Lockstep:
@@ -66,7 +69,7 @@ class Lockstep:
     def __init__(self, wl: syn.Workload, seed: int = 0, layer_ids=(0,), check_seqs=None,
                  flags: int = 0, num_splits: int = 0, steps: int | None = None, log=print,
                  capacity_full=None, capacity_quant=None, score_decay: float | None = None,
-                 key_norm: bool = False):
+                 key_norm: bool = False, score_p: float | None = None):
         self.wl, self.seed = wl, seed
         self.layer_ids = list(layer_ids)
         self.check_seqs = list(range(wl.batch)) if check_seqs is None else list(check_seqs)
@@ -74,8 +77,10 @@ class Lockstep:
         self.cfg = gpu_config(wl, len(self.layer_ids), flags | qv.FLAG_DEBUG_MASSES,
                               num_splits=num_splits, capacity_full=capacity_full,
                               capacity_quant=capacity_quant, score_decay=score_decay,
-                              key_norm=key_norm)
+                              key_norm=key_norm, score_p=score_p)
         self.key_norm = key_norm
+        # modes whose prompt scores the GPU computes itself (key norms, u_0^p)
+        self.gpu_prompt_scores = key_norm or score_p is not None
         self.cache = qv.Cache(self.cfg)
         self.ocfg = oracle_config(self.cfg)
         self.units = {(li, b): QEvictUnit(self.ocfg, wl.max_context)
@@ -155,7 +160,7 @@ class Lockstep:
                 if (li, b) in self.units:
                     # the key-norm score comes from the keys: the GPU computes its own
                     self.units[(li, b)].prefill(from_bf16_bits(k), from_bf16_bits(v), init,
-                                                route=not self.key_norm)
+                                                route=not self.gpu_prompt_scores)
             del prompts
             K = to_dev_bf16(np.stack(ks))
             V = to_dev_bf16(np.stack(vs))
@@ -165,14 +170,14 @@ class Lockstep:
             del K, V
             for b in self.check_seqs:
                 u = self.units[(li, b)]
-                if self.key_norm:
-                    # fp32 sums against fp64 ones: check the scores, then route both
+                if self.gpu_prompt_scores:
+                    # fp32 against fp64 arithmetic: check the scores, then route both
                     # with the GPU's so that near-ties rank alike
                     st = self.cache.get_state(li, b)
                     n = st["n"]
                     so, sg = u.score[:n], st["scores"].astype(np.float64)
                     err = np.abs(sg - so) / np.maximum(np.abs(so), 1e-7 * np.abs(so).sum())
-                    assert np.all(err <= SCORE_TOL), f"prefill key-norm score rel err {err.max():.3e}"
+                    assert np.all(err <= SCORE_TOL), f"prefill score rel err {err.max():.3e}"
                     u.adopt_scores(sg)
                     u.finish_prefill()
                 self.compare_state(li, b)

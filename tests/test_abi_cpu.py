@@ -51,7 +51,9 @@ def test_workspace_size_of_the_8b_32k_layer():
     (dict(flags=0x80), qv.qevict.ERR_INVALID_ARG),
     (dict(max_context=0), qv.qevict.ERR_INVALID_ARG),
     (dict(sink_tokens=65 * 32), qv.qevict.ERR_UNSUPPORTED),
-    (dict(score_mode=3), qv.qevict.ERR_INVALID_ARG),
+    (dict(score_mode=4), qv.qevict.ERR_INVALID_ARG),
+    (dict(score_mode=qv.SCORE_PNORM, score_p=0.5), qv.qevict.ERR_INVALID_ARG),
+    (dict(score_mode=qv.SCORE_PNORM, score_p=17.0), qv.qevict.ERR_INVALID_ARG),
     (dict(score_mode=qv.SCORE_DECAY, score_decay=0.0), qv.qevict.ERR_INVALID_ARG),
     (dict(score_mode=qv.SCORE_DECAY, score_decay=1.5), qv.qevict.ERR_INVALID_ARG),
 ])
@@ -67,6 +69,10 @@ def test_ranking_modes_are_accepted():
     # key-norm mode stages the prompt windows' scores ([B][n_w] fp32) after the units
     kn = qv.workspace_size(_cfg(score_mode=qv.SCORE_KEY_NORM))
     assert base + 4 * 1028 <= kn <= base + 4 * 1028 + 256
+    # p-norm mode: the same staging plus {completed-period sum, running u} per window and unit
+    pn = qv.workspace_size(_cfg(score_mode=qv.SCORE_PNORM, score_p=3.0))
+    n_units = 1 * 1
+    assert kn + n_units * 8 * 1028 <= pn <= kn + n_units * (8 * 1028 + 256)
 
 
 def test_status_strings():

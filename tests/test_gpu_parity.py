@@ -48,3 +48,10 @@ def test_key_norm_lockstep(name):
     kernel and the merge's per-token update): scores and routing against the
     oracle."""
     _lockstep(name, key_norm=True)
+
+
+@pytest.mark.parametrize("name", ["c2s", "c5s"])
+def test_pnorm_lockstep(name):
+    """Attention p-norm ranking, p = 3 (per step on c2s; periods of 8 steps on
+    c5s): scores (held as S^p) and routing against the oracle."""
+    _lockstep(name, score_p=3.0)

@@ -16,7 +16,11 @@ previous routing event).
   (prefill and decode), independence from the queries, routing keeps the
   lowest-norm windows (a zero-key window first; doubling a window's keys
   doubles its score), and windows completed during decode score as a prefill
-  of the same tokens does.
+  of the same tokens does;
+* attention p-norm: the uniform-attention periods (R = 1 to 4, several p),
+  p = 1 equals the cumulative score, and with all windows in Full the score
+  equals the p-th powers of the cumulative increments between routing
+  events, within the power-mean bounds of the largest period.
 """
 import numpy as np
 import pytest
@@ -207,3 +211,100 @@ def test_key_norm_decode_accumulation_matches_prefill():
     b.prefill(kk, np.ones((2, n0 + steps, 8)), None)
     n = -(-(n0 + steps) // W)
     assert np.allclose(a.score[:n], b.score[:n], rtol=1e-13, atol=0)
+
+
+# ---- attention p-norm (appendix, p-norm equation) ----
+
+def _pnorm_uniform_unit(p, n_win=3):
+    cfg = OracleConfig(2, 1, 8, W, W, 4, 16, 0, score_p=p)
+    u = QEvictUnit(cfg, W * n_win + 40)
+    T0 = W * n_win
+    u.prefill(np.zeros((1, T0, 8)), np.ones((1, T0, 8)), np.arange(1, n_win + 1) / 8.0)
+    return u
+
+
+@pytest.mark.parametrize("p,R", [(3.0, 1), (3.0, 3), (2.0, 4), (1.5, 2)])
+def test_pnorm_uniform_attention(p, R):
+    """Uniform attention: the attention of a period is a sum of (tokens of the
+    window) / (tokens held) over its steps; the score is the sum of the
+    periods' p-th powers, the prompt score being the first period."""
+    u = _pnorm_uniform_unit(p)
+    T0 = u.T
+    init = [1 / 8, 2 / 8, 3 / 8]
+    periods = {w: [init[w]] for w in range(3)}
+    cur: dict[int, float] = {}
+    steps = 13
+    for t in range(1, steps + 1):
+        u.step(np.ones((2, 8)), np.zeros((1, 8)), np.ones((1, 8)))
+        T = T0 + t
+        for w in range(-(-T // W)):
+            cur[w] = cur.get(w, 0.0) + min(W, T - W * w) / T
+        expect = {w: sum(x ** p for x in periods.get(w, [])) + cur[w] ** p for w in cur}
+        for w, v in expect.items():
+            assert u.score[w] == pytest.approx(v, rel=1e-13), (t, w)
+        if t % R == 0:
+            u.route()
+            for w, x in cur.items():
+                periods.setdefault(w, []).append(x)
+            cur = {w: 0.0 for w in cur}
+
+
+def _run_scores(seed=5, steps=12, R=1, **kw):
+    rng = np.random.default_rng(seed)
+    n_win = 10
+    cfg = OracleConfig(4, 2, 16, W, W, 4, 3, 3, **kw)
+    u = QEvictUnit(cfg, W * n_win + steps + 1)
+    u.prefill(_bf16(rng, (2, W * n_win, 16)), _bf16(rng, (2, W * n_win, 16)),
+              rng.permutation(n_win) / 10.0)
+    traj = []
+    for t in range(steps):
+        out, _, _ = u.step(_bf16(rng, (4, 16)) * 3.0, _bf16(rng, (2, 16)), _bf16(rng, (2, 16)))
+        if (t + 1) % R == 0:
+            u.route()
+        traj.append((out.copy(), u.score.copy(), u.state.copy()))
+    return traj, u
+
+
+@pytest.mark.parametrize("R", [1, 3])
+def test_pnorm_with_p_one_is_the_cumulative_score(R):
+    a, _ = _run_scores(R=R)
+    b, _ = _run_scores(R=R, score_p=1.0)
+    for (oa, sa, ta), (ob, sb, tb) in zip(a, b):
+        assert np.array_equal(ta, tb)
+        assert np.allclose(oa, ob, rtol=1e-12, atol=1e-14)
+        assert np.allclose(sa, sb, rtol=1e-12, atol=1e-14)
+
+
+def test_pnorm_from_the_cumulative_increments():
+    """With every window in Full (no routing decision depends on the score) the
+    attention is the same under any ranking, so the periods' u_r are the
+    increments of the cumulative score between routing events.  The p-norm run
+    must give S^p = sum_r u_r^p of those, and S must lie between max_r u_r and
+    n^(1/p) max_r u_r (p = 16 comes close to the maximum)."""
+    R, steps, n_win = 2, 12, 10
+
+    def run(**kw):
+        rng = np.random.default_rng(9)
+        cfg = OracleConfig(4, 2, 16, W, W, 4, 16, 0, **kw)
+        u = QEvictUnit(cfg, W * n_win + steps + 1)
+        u.prefill(_bf16(rng, (2, W * n_win, 16)), _bf16(rng, (2, W * n_win, 16)),
+                  rng.permutation(n_win) / 10.0)
+        at_events = [u.score.copy()]
+        for t in range(steps):
+            u.step(_bf16(rng, (4, 16)) * 3.0, _bf16(rng, (2, 16)), _bf16(rng, (2, 16)))
+            if (t + 1) % R == 0:
+                at_events.append(u.score.copy())
+                u.route()
+        return u, at_events
+
+    cum, ev = run()
+    for p in (3.0, 16.0):
+        pn, _ = run(score_p=p)
+        assert np.array_equal(cum.state, pn.state)
+        n = -(-cum.T // W)
+        for w in range(n):
+            u_r = [ev[0][w]] + [ev[i][w] - ev[i - 1][w] for i in range(1, len(ev))]
+            expect = sum(x ** p for x in u_r)
+            assert pn.score[w] == pytest.approx(expect, rel=1e-9), (p, w)
+            S, m = pn.score[w] ** (1 / p), max(u_r)
+            assert m * (1 - 1e-9) <= S <= len(u_r) ** (1 / p) * m * (1 + 1e-9)
