@@ -23,6 +23,10 @@ What it computes, and where the paper defines it (QEvict, arXiv 2608.05326):
   the windows that left the recent region; the top K_f by score go to Full,
   the next K_q to Quantized, the rest are evicted (Sec. 4.3, candidate pool
   and TopK equations; Algorithm 1).
+* Initial window scores from prompt attention: the mean over query heads of
+  the causal attention mass that the last n_obs prompt queries put on each
+  window (Sec. 4.2: prompt attention initialises the scores; the observation
+  window is a reading).
 * Migration-stable asymmetric quantization: keys per channel across tokens,
   values per token across channels; codes are produced once, at a window's
   first demotion, and reused on every later move; promotion reconstructs the
@@ -50,6 +54,7 @@ __all__ = [
     "OPEN", "AGED", "FULL", "QUANT", "EVICTED", "ACTIVE", "DORMANT",
     "OracleConfig", "QEvictUnit", "quantize_groups", "quantize_window",
     "dequantize_window", "route_order", "tier_split", "QuantRangeError", "CapacityError",
+    "prefill_window_scores",
 ]
 
 # window states; OPEN and AGED are both inside / just out of the recent region
@@ -190,6 +195,44 @@ def dequantize_window(e: dict):
     vz = np.repeat(e["vz"], g, axis=2)
     vs = np.repeat(e["vs"], g, axis=2)
     return kz + ks * e["kc"], vz + vs * e["vc"]
+
+
+# ----------------------------------------------------------------------------
+# Initial window scores from prompt attention (Sec. 4.2)
+# ----------------------------------------------------------------------------
+
+def prefill_window_scores(q_obs, k, sink: int, window: int, scale: float | None = None):
+    """Score of every prompt window before the first routing event.
+
+    q_obs: float64 [H_q, n_obs, d], the queries of prompt positions
+    T - n_obs .. T - 1; k: float64 [H_kv, T, d] prompt keys (query head h reads
+    KV head h // (H_q / H_kv)).  Each observation query attends causally to
+    keys 0 .. its own position with softmax(q k^T * scale); the score of window
+    w (tokens sink + w W .. sink + (w + 1) W - 1, the last one possibly
+    partial) is the attention mass its tokens receive, summed over the
+    observation queries and averaged over the H_q heads (the cumulative score of
+    Sec. 4.2 with the observation queries in place of decode steps).  Sink
+    tokens take part in the softmax and belong to no window.
+    Returns float64 [n_w], n_w = ceil((T - sink) / W).
+    """
+    H_q, n_obs, d = q_obs.shape
+    H_kv, T, _ = k.shape
+    gqa = H_q // H_kv
+    scale = scale if scale else 1.0 / math.sqrt(d)
+    n_w = max(0, -(-(T - sink) // window))
+    owner = np.full(T, -1)
+    owner[sink:] = (np.arange(sink, T) - sink) // window
+    scores = np.zeros(n_w)
+    for h in range(H_q):
+        kk = k[h // gqa]
+        for j in range(n_obs):
+            tau = T - n_obs + j
+            logits = (kk[:tau + 1] @ q_obs[h, j]) * scale
+            e = np.exp(logits - logits.max())
+            p = e / e.sum()
+            win = owner[:tau + 1] >= 0
+            scores += np.bincount(owner[:tau + 1][win], weights=p[win], minlength=n_w)
+    return scores / H_q
 
 
 # ----------------------------------------------------------------------------

@@ -23,10 +23,12 @@ import numpy as np
 __all__ = [
     "Workload", "WORKLOADS", "get_workload", "f32_to_bf16_bits", "bf16_bits_to_f32",
     "prompt_kv", "decode_inputs", "init_scores", "shift_delta", "pick_shift_window",
+    "observation_queries",
 ]
 
 # stream identifiers inside one (config, seed, seq, layer) seed sequence
-_S_PROMPT_K, _S_PROMPT_V, _S_DRIFT, _S_INIT, _S_DEC_Q, _S_DEC_K, _S_DEC_V, _S_OUTLIER, _S_SHIFT = range(9)
+_S_PROMPT_K, _S_PROMPT_V, _S_DRIFT, _S_INIT, _S_DEC_Q, _S_DEC_K, _S_DEC_V, _S_OUTLIER, _S_SHIFT, \
+    _S_OBS_Q = range(10)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -236,6 +238,22 @@ def decode_inputs(wl: Workload, seed: int, seq: int, layer: int, steps: int | No
                np.broadcast_to(scale, (n,) + scale.shape))
     vs = _normal(_rng(wl, seed, seq, layer, _S_DEC_V), (n, wl.num_kv_heads, wl.head_dim))
     return f32_to_bf16_bits(qs), f32_to_bf16_bits(ks), f32_to_bf16_bits(vs)
+
+
+def observation_queries(wl: Workload, seed: int, seq: int, layer: int, n_obs: int) -> np.ndarray:
+    """Queries of the last n_obs prompt positions, bf16 bits [H_q, n_obs, d].
+
+    The decode query recipe continued backwards: i.i.d. normal, plus (with
+    drift) the rotating mean at steps 1 - n_obs .. 0.
+    """
+    qs = _rng(wl, seed, seq, layer, _S_OBS_Q).standard_normal(
+        (wl.num_q_heads, n_obs, wl.head_dim), dtype=np.float32)
+    if wl.drift:
+        u, v = _drift_basis(wl, seed, seq, layer)
+        t = np.arange(1 - n_obs, 1, dtype=np.float64)[:, None]
+        mu = wl.drift_amp * (np.cos(wl.drift_omega * t) * u + np.sin(wl.drift_omega * t) * v)
+        qs = qs + mu[None, :, :].astype(np.float32)
+    return f32_to_bf16_bits(qs)
 
 
 def init_scores(wl: Workload, seed: int, seq: int, layer: int) -> np.ndarray:
