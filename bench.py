@@ -58,6 +58,8 @@ def parse():
                         "the attention of the other layers; sync: everything on one stream")
     p.add_argument("--no-kernel-events", action="store_true",
                    help="do not time each kernel launch with HIP events (no roofline)")
+    p.add_argument("--prefill-scores", action="store_true",
+                   help="time the initial-window-score kernels on the workload's prompt instead")
     p.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MB",
                    help="only run 8 plain device-to-device copies of this many MB (hardware "
                         "counter calibration) and exit")
@@ -135,15 +137,19 @@ def measured_traffic():
     return None
 
 
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        return 1
+
+
 def cpu_baseline(wl, seed, budget_s):
     """The float64 oracle stepping one sequence-layer of the same workload."""
     from oracle.qevict_oracle import OracleConfig, QEvictUnit
     import synthetic as syn
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        cores = 1
+    cores = blas_threads()
     cfg = OracleConfig(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, wl.group, wl.bits,
                        wl.capacity_full, wl.capacity_quant)
     u = QEvictUnit(cfg, wl.max_context)
@@ -164,6 +170,80 @@ def cpu_baseline(wl, seed, budget_s):
                       f"prefill, float64 numpy, {dt:.1f} s"}
 
 
+def bench_prefill_scores(args):
+    """Initial window scores of a prompt (qevict_prefill_scores): W observation
+    queries attending causally to the whole prompt, per-window masses.  Eight
+    prompts of the workload's shape are rotated so that their keys (64 MB each
+    at 32K) do not stay in the Infinity Cache between calls; one call reads the
+    keys twice (row statistics, then masses), the second read mostly from that
+    cache."""
+    import torch
+    import paper_2608_05326_amd as qv
+    import synthetic as syn
+    wl = syn.get_workload(args.workload)
+    n_obs = wl.window
+    NP = 8
+    cfg = qv.Config(batch=wl.batch, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                    window_tokens=wl.window, group_size=wl.group, quant_bits=wl.bits,
+                    max_context=wl.prompt_len + 64, capacity_full=wl.capacity_full,
+                    capacity_quant=wl.capacity_quant, sink_tokens=wl.sink, recent_tokens=wl.recent)
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
+    cache = qv.Cache(cfg, stream=stream)
+    Ks, Qs, hk, hq = [], [], None, None
+    for i in range(NP):
+        k = np.stack([syn.prompt_kv(wl, args.seed, b, i)[0] for b in range(wl.batch)])
+        q = np.stack([syn.observation_queries(wl, args.seed, b, i, n_obs) for b in range(wl.batch)])
+        if i == 0:
+            hk, hq = k[0], q[0]
+        Ks.append(to_dev(k))
+        Qs.append(to_dev(q))
+    n_w = -(-(wl.prompt_len - wl.sink) // wl.window)
+    out = torch.empty((wl.batch, n_w), dtype=torch.float32, device="cuda")
+    scratch = torch.empty(qv.qevict.prefill_scores_scratch_size(cfg, wl.prompt_len, n_obs),
+                          dtype=torch.uint8, device="cuda")
+    for i in range(max(args.warmup // 16, 2) * NP):
+        cache.prefill_scores(Qs[i % NP], Ks[i % NP], out, scratch)
+    steps = max(args.steps // 16, NP)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(steps):
+        cache.prefill_scores(Qs[i % NP], Ks[i % NP], out, scratch)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / steps
+    B, Hkv, Hq, T, d = wl.batch, wl.num_kv_heads, wl.num_q_heads, wl.prompt_len, wl.head_dim
+    min_bytes = B * (Hkv * T * d * 2 + Hq * n_obs * d * 2 + n_w * 4)
+    flops = 2 * (2 * B * Hq * n_obs * T * d)     # two QK^T passes over every (row, key) pair
+    ach = min_bytes / (us * 1e-6) / 1e9
+    res = {
+        "metric": "initial window scores µs per prompt layer (observation-query attention masses)",
+        "value": round(us, 3), "unit": "us/call", "n_gpus": 1, "steps": steps,
+        "warmup": max(args.warmup // 16, 2) * NP, "ms_per_step": round(us / 1e3, 5),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16 (fp32 accumulate)", "data": "synthetic",
+        "config": {"workload": f"{wl.prompt_len}-token prompt, batch {B}, {Hq} query / {Hkv} KV heads, "
+                               f"head_dim {d}, windows of {wl.window}, {n_obs} observation queries",
+                   "prompts_rotated": NP, "parallelism": "single GPU"},
+        "tflops": round(flops / (us * 1e-6) / 1e12, 1),
+        "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": None},
+    }
+    if not args.no_cpu:
+        from oracle.qevict_oracle import prefill_window_scores
+        f = syn.bf16_bits_to_f32
+        t0 = time.perf_counter()
+        prefill_window_scores(f(hq).astype(np.float64), f(hk).astype(np.float64), wl.sink, wl.window)
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": round(dt * 1e6 * B, 1), "unit": "us/call", "cores": blas_threads(),
+                               "kind": "oracle",
+                               "sample": f"one sequence's scores (float64 numpy, {dt:.1f} s), times {B}"}
+    print(json.dumps(res))
+    cache.close()
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -173,6 +253,8 @@ def main():
         return 2
     if args.calibrate_copy > 0:
         return calibrate_copy(args.calibrate_copy)
+    if args.prefill_scores:
+        return bench_prefill_scores(args)
     import torch
     import paper_2608_05326_amd as qv
     import synthetic as syn

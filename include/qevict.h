@@ -171,6 +171,32 @@ qevict_status qevict_prefill_assign(qevict_cache *c, int32_t layer, const uint16
                                     const uint16_t *v, int32_t prompt_len,
                                     const float *init_scores);
 
+/* Initial window scores from prompt attention (Sec. 4.2: prompt attention
+ * initialises the window scores).  The observation queries are those of the
+ * last n_obs prompt positions; each attends causally (keys 0 .. its own
+ * position, softmax(q k^T * scale), query head h on KV head h / (H_q/H_kv)),
+ * and the score of window w (tokens sink + w W .. sink + (w + 1) W - 1, the
+ * last one possibly partial) is the attention mass its tokens receive, summed
+ * over the observation queries and averaged over the H_q heads.  Sink tokens
+ * take part in the softmax and belong to no window.  The result is the
+ * init_scores argument of qevict_prefill_assign (any score mode that takes
+ * initial scores); the cache's state is neither read nor written.
+ *   q_obs   [B, H_q, n_obs, d] bf16, 16-byte aligned
+ *   n_obs   1 .. min(prompt_len, 4096)
+ *   k       [B, H_kv, prompt_len, d] bf16 prompt keys, 16-byte aligned
+ *   scratch device memory of qevict_prefill_scores_scratch_size bytes,
+ *           256-byte aligned, owned by the caller, overwritten
+ *   scores  [B, n_w] fp32 out, n_w = ceil((prompt_len - sink) / W) (0 when
+ *           prompt_len <= sink; scores may then be NULL), 16-byte aligned
+ * Work is enqueued on the cache's stream; the buffers must stay valid until
+ * it completes.  Reductions run in a fixed order: the result is bitwise
+ * repeatable. */
+qevict_status qevict_prefill_scores_scratch_size(const qevict_config *cfg, int32_t prompt_len,
+                                                 int32_t n_obs, size_t *bytes);
+qevict_status qevict_prefill_scores(qevict_cache *c, const uint16_t *q_obs, int32_t n_obs,
+                                    const uint16_t *k, int32_t prompt_len, void *scratch,
+                                    size_t scratch_bytes, float *scores);
+
 /* One decode step of one layer (Sec. 4.1 decode attention; Sec. 4.2 score).
  *   q      [B, H_q, d]  bf16 queries
  *   k_new, v_new [B, H_kv, d] bf16 key / value of the new token
@@ -227,7 +253,8 @@ qevict_status qevict_debug_masses(qevict_cache *c, int32_t layer, float *masses,
 
 /* Kernel timing with HIP events on the cache's stream (off by default).
  * kernel: 0 attention pass, 1 split merge + score accumulation, 2 re-rank,
- * 3 migrations (quantize and promote / admit, one launch), 4 unused.  read
+ * 3 migrations (quantize and promote / admit, one launch), 4 initial window
+ * scores (qevict_prefill_scores, its four launches together).  read
  * returns the summed milliseconds and the number of timed launches since
  * enable, and is synchronous. */
 qevict_status qevict_profile_enable(qevict_cache *c, int32_t on);

@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libqevict.so")
-SOURCES = ["runtime.cpp", "attend.hip", "retier.hip", "migrate.hip"]
+SOURCES = ["runtime.cpp", "attend.hip", "retier.hip", "migrate.hip", "prefill_scores.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",

@@ -61,6 +61,18 @@ struct KeyNormArgs {        // key-norm scores of the prompt windows
   float* out;               // [B][n_init]
 };
 
+struct ObsArgs {            // initial window scores from the observation queries' attention
+  const uint16_t* q;        // [B][H_q][n_obs][d] bf16
+  const uint16_t* k;        // [B][H_kv][T][d] bf16
+  int32_t B, H_q, H_kv, gqa, T, n_obs, n_rows, W, sink, n_w;
+  int32_t n_blk, T_pad;     // key blocks of 256; n_blk * 256
+  float scale_log2;
+  float2* blk_ml;           // [B][H_kv][n_rows][n_blk] (max, exp-sum) per key block
+  float2* row_ml;           // [B][H_kv][n_rows] (M, 1 / L)
+  float* key_mass;          // [B][H_kv][T_pad] mass per key, summed over rows
+  float* scores;            // [B][n_w]
+};
+
 struct ScorePowArgs {       // p-norm ranking: prompt scores raised to the power p
   const float* in;
   float* out;

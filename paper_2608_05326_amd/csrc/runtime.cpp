@@ -34,6 +34,7 @@ hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, 
 hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st);
 hipError_t launch_key_norm_init(const KeyNormArgs& a, hipStream_t st);
 hipError_t launch_score_pow(const ScorePowArgs& a, hipStream_t st);
+hipError_t launch_prefill_scores(const ObsArgs& a, hipStream_t st);
 }  // namespace qv
 
 using namespace qv;
@@ -587,6 +588,89 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
   ls.routed_end = n_hist;
   ls.prefilled = true;
   ls.period_start = true;
+  return QEVICT_OK;
+}
+
+// ---- initial window scores from the observation queries -------------------
+namespace {
+constexpr int kObsKeysPerBlock = 256;   // keys per workgroup of the observation passes
+
+struct ObsScratch {
+  int64_t blk_ml, row_ml, key_mass, bytes;
+};
+
+qevict_status obs_check(const qevict_config* cfg, int32_t prompt_len, int32_t n_obs) {
+  if (prompt_len < 1 || prompt_len > cfg->max_context)
+    return fail(QEVICT_ERR_INVALID_ARG, "prompt_len %d outside [1, max_context]", prompt_len);
+  if (n_obs < 1 || n_obs > prompt_len || n_obs > 4096)
+    return fail(QEVICT_ERR_INVALID_ARG, "n_obs %d outside [1, min(prompt_len, 4096)]", n_obs);
+  return QEVICT_OK;
+}
+
+ObsScratch obs_scratch(const qevict_config* cfg, int32_t prompt_len, int32_t n_obs) {
+  const int64_t rows = (int64_t)cfg->num_q_heads / cfg->num_kv_heads * n_obs;
+  const int64_t n_blk = ceil_div(prompt_len, kObsKeysPerBlock);
+  const int64_t bh = (int64_t)cfg->batch * cfg->num_kv_heads;
+  ObsScratch s;
+  s.blk_ml = 0;
+  s.row_ml = align256(s.blk_ml + 8 * bh * rows * n_blk);
+  s.key_mass = align256(s.row_ml + 8 * bh * rows);
+  s.bytes = align256(s.key_mass + 4 * bh * n_blk * kObsKeysPerBlock);
+  return s;
+}
+}  // namespace
+
+qevict_status qevict_prefill_scores_scratch_size(const qevict_config* cfg, int32_t prompt_len,
+                                                 int32_t n_obs, size_t* bytes) {
+  qevict_status s = check_config(cfg);
+  if (s) return s;
+  if (!bytes) return fail(QEVICT_ERR_INVALID_ARG, "bytes is NULL");
+  if ((s = obs_check(cfg, prompt_len, n_obs))) return s;
+  *bytes = (size_t)obs_scratch(cfg, prompt_len, n_obs).bytes;
+  return QEVICT_OK;
+}
+
+qevict_status qevict_prefill_scores(qevict_cache* c, const uint16_t* q_obs, int32_t n_obs,
+                                    const uint16_t* k, int32_t prompt_len, void* scratch,
+                                    size_t scratch_bytes, float* scores) {
+  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache handle is NULL");
+  const qevict_config& cfg = c->cfg;
+  qevict_status s = obs_check(&cfg, prompt_len, n_obs);
+  if (s) return s;
+  const Geometry& g = c->g;
+  const int n_w = prompt_len > g.sink ? ceil_div(prompt_len - g.sink, g.W) : 0;
+  if (!q_obs || !k || !scratch || (!scores && n_w > 0))
+    return fail(QEVICT_ERR_INVALID_ARG, "null pointer");
+  if (((uintptr_t)q_obs & 15) || ((uintptr_t)k & 15) || ((uintptr_t)scores & 15))
+    return fail(QEVICT_ERR_INVALID_ARG, "queries, keys and scores must be 16-byte aligned");
+  if ((uintptr_t)scratch & 255) return fail(QEVICT_ERR_WORKSPACE, "scratch must be 256-byte aligned");
+  const ObsScratch L = obs_scratch(&cfg, prompt_len, n_obs);
+  if ((int64_t)scratch_bytes < L.bytes)
+    return fail(QEVICT_ERR_WORKSPACE, "scratch has %zu bytes, needs %lld", scratch_bytes,
+                (long long)L.bytes);
+  ObsArgs a;
+  a.q = q_obs;
+  a.k = k;
+  a.B = g.B;
+  a.H_q = g.H_q;
+  a.H_kv = g.H_kv;
+  a.gqa = g.gqa;
+  a.T = prompt_len;
+  a.n_obs = n_obs;
+  a.n_rows = g.gqa * n_obs;
+  a.W = g.W;
+  a.sink = g.sink;
+  a.n_w = n_w;
+  a.n_blk = ceil_div(prompt_len, kObsKeysPerBlock);
+  a.T_pad = a.n_blk * kObsKeysPerBlock;
+  a.scale_log2 = g.scale_log2;
+  uint8_t* sb = (uint8_t*)scratch;
+  a.blk_ml = (float2*)(sb + L.blk_ml);
+  a.row_ml = (float2*)(sb + L.row_ml);
+  a.key_mass = (float*)(sb + L.key_mass);
+  a.scores = scores;
+  const hipError_t e = timed(c, 4, c->stream, [&] { return launch_prefill_scores(a, c->stream); });
+  if (e != hipSuccess) return hip_fail(e, "prefill_scores launch");
   return QEVICT_OK;
 }
 

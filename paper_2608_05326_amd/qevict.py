@@ -33,7 +33,8 @@ SYMBOLS = (
     "qevict_decode_attend", "qevict_retier", "qevict_quantize_window", "qevict_promote_window",
     "qevict_get_state", "qevict_export_window", "qevict_debug_shift_keys", "qevict_debug_masses",
     "qevict_profile_enable", "qevict_profile_read", "qevict_last_attend_bytes", "qevict_join_routing",
-    "qevict_status_string", "qevict_last_error",
+    "qevict_status_string", "qevict_last_error", "qevict_prefill_scores_scratch_size",
+    "qevict_prefill_scores",
 )
 
 
@@ -126,6 +127,8 @@ def load_library(path: str | None = None):
         "qevict_profile_read": [vp, i32, P(ctypes.c_double), P(i64)],
         "qevict_last_attend_bytes": [vp, i32, P(i64)],
         "qevict_join_routing": [vp],
+        "qevict_prefill_scores_scratch_size": [P(_Config), i32, i32, P(ctypes.c_size_t)],
+        "qevict_prefill_scores": [vp, vp, i32, vp, i32, vp, ctypes.c_size_t, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -149,6 +152,14 @@ def workspace_size(cfg: Config) -> int:
     lib = load_library()
     n = ctypes.c_size_t()
     _check(lib, lib.qevict_workspace_size(ctypes.byref(cfg.to_c()), ctypes.byref(n)))
+    return n.value
+
+
+def prefill_scores_scratch_size(cfg: Config, prompt_len: int, n_obs: int) -> int:
+    lib = load_library()
+    n = ctypes.c_size_t()
+    _check(lib, lib.qevict_prefill_scores_scratch_size(ctypes.byref(cfg.to_c()), prompt_len, n_obs,
+                                                       ctypes.byref(n)))
     return n.value
 
 
@@ -204,6 +215,31 @@ class Cache:
         sc = None if init_scores is None else _ptr(init_scores, t.float32, "init_scores")
         self._c(self.lib.qevict_prefill_assign(
             self.handle, layer, _ptr(k, t.bfloat16, "k"), _ptr(v, t.bfloat16, "v"), k.shape[2], sc))
+
+    def prefill_scores(self, q_obs, k, scores=None, scratch=None):
+        """Initial window scores from the observation queries' attention.
+        q_obs: bf16 [B, H_q, n_obs, d]; k: bf16 [B, H_kv, T, d]; returns float32
+        [B, n_w] (written into `scores` when given)."""
+        t = self.torch
+        cfg = self.cfg
+        B, n_obs, T = cfg.batch, q_obs.shape[2], k.shape[2]
+        if tuple(q_obs.shape) != (B, cfg.num_q_heads, n_obs, cfg.head_dim):
+            raise ValueError(f"q_obs shape {tuple(q_obs.shape)}")
+        if tuple(k.shape) != (B, cfg.num_kv_heads, T, cfg.head_dim):
+            raise ValueError(f"k shape {tuple(k.shape)}")
+        n_w = max(0, -(-(T - cfg.sink_tokens) // cfg.window_tokens))
+        if scores is None:
+            scores = t.empty((B, n_w), dtype=t.float32, device=self.device)
+        if scores.numel() != B * n_w:
+            raise ValueError(f"scores must hold {B} x {n_w} values")
+        need = prefill_scores_scratch_size(cfg, T, n_obs)
+        if scratch is None:
+            scratch = t.empty(need, dtype=t.uint8, device=self.device)
+        self._c(self.lib.qevict_prefill_scores(
+            self.handle, _ptr(q_obs, t.bfloat16, "q_obs"), n_obs, _ptr(k, t.bfloat16, "k"), T,
+            _ptr(scratch, None, "scratch"), scratch.numel() * scratch.element_size(),
+            _ptr(scores, t.float32, "scores") if n_w else None))
+        return scores
 
     def decode_attend(self, layer: int, q, k_new, v_new, out):
         t = self.torch

@@ -69,7 +69,7 @@ class Lockstep:
     def __init__(self, wl: syn.Workload, seed: int = 0, layer_ids=(0,), check_seqs=None,
                  flags: int = 0, num_splits: int = 0, steps: int | None = None, log=print,
                  capacity_full=None, capacity_quant=None, score_decay: float | None = None,
-                 key_norm: bool = False, score_p: float | None = None):
+                 key_norm: bool = False, score_p: float | None = None, observed_init: bool = False):
         self.wl, self.seed = wl, seed
         self.layer_ids = list(layer_ids)
         self.check_seqs = list(range(wl.batch)) if check_seqs is None else list(check_seqs)
@@ -81,6 +81,9 @@ class Lockstep:
         self.key_norm = key_norm
         # modes whose prompt scores the GPU computes itself (key norms, u_0^p)
         self.gpu_prompt_scores = key_norm or score_p is not None
+        # prompt scores from the observation queries' attention (GPU kernel,
+        # checked against the oracle's, then given to both sides)
+        self.observed_init = observed_init
         self.cache = qv.Cache(self.cfg)
         self.ocfg = oracle_config(self.cfg)
         self.units = {(li, b): QEvictUnit(self.ocfg, wl.max_context)
@@ -152,19 +155,29 @@ class Lockstep:
         for li, layer in enumerate(self.layer_ids):
             with ThreadPoolExecutor(max_workers=min(8, wl.batch)) as ex:
                 prompts = list(ex.map(lambda b: gen(b, layer), range(wl.batch)))
-            ks, vs, inits = [], [], []
-            for b, (k, v, init) in enumerate(prompts):
-                ks.append(k)
-                vs.append(v)
-                inits.append(init)
-                if (li, b) in self.units:
-                    # the key-norm score comes from the keys: the GPU computes its own
-                    self.units[(li, b)].prefill(from_bf16_bits(k), from_bf16_bits(v), init,
-                                                route=not self.gpu_prompt_scores)
+            ks = [p[0] for p in prompts]
+            vs = [p[1] for p in prompts]
+            inits = [p[2] for p in prompts]
             del prompts
             K = to_dev_bf16(np.stack(ks))
             V = to_dev_bf16(np.stack(vs))
             S = None if self.key_norm else torch.from_numpy(np.stack(inits)).cuda()
+            if self.observed_init:
+                from oracle.qevict_oracle import prefill_window_scores
+                qo = [syn.observation_queries(wl, self.seed, b, layer, wl.window) for b in range(wl.batch)]
+                S = self.cache.prefill_scores(to_dev_bf16(np.stack(qo)), K)
+                got = S.cpu().numpy()
+                for b in self.check_seqs:
+                    ref = prefill_window_scores(from_bf16_bits(qo[b]), from_bf16_bits(ks[b]),
+                                                wl.sink, wl.window)
+                    err = np.abs(got[b] - ref) / np.maximum(np.abs(ref), 1e-7 * np.abs(ref).sum())
+                    assert np.all(err <= SCORE_TOL), f"observed prompt score rel err {err.max():.3e}"
+                    inits[b] = got[b]
+            for b in range(wl.batch):
+                if (li, b) in self.units:
+                    # key-norm and p-norm prompt scores: the GPU computes its own
+                    self.units[(li, b)].prefill(from_bf16_bits(ks[b]), from_bf16_bits(vs[b]), inits[b],
+                                                route=not self.gpu_prompt_scores)
             self.cache.prefill_assign(li, K, V, S)
             torch.cuda.synchronize()
             del K, V

@@ -79,3 +79,16 @@ def test_status_strings():
     lib = qv.load_library()
     assert lib.qevict_status_string(0) == b"ok"
     assert lib.qevict_status_string(-6) == b"capacity exceeded"
+
+
+def test_prefill_scores_scratch_size():
+    cfg = _cfg()
+    # per (sequence, KV head): rows x blocks (max, sum) pairs, rows (M, 1/L), a mass per key
+    rows, n_blk = 4 * 32, -(-32768 // 256)
+    n = qv.qevict.prefill_scores_scratch_size(cfg, 32768, 32)
+    expect = 8 * (8 * rows * n_blk) + 8 * (8 * rows) + 4 * (8 * n_blk * 256)
+    assert expect <= n <= expect + 3 * 256
+    for T, n_obs in [(0, 1), (100, 0), (100, 101), (10 ** 6, 1), (8192, 4097)]:
+        with pytest.raises(qv.QEvictError) as e:
+            qv.qevict.prefill_scores_scratch_size(cfg, T, n_obs)
+        assert e.value.status == qv.qevict.ERR_INVALID_ARG
