@@ -175,8 +175,7 @@ def bench_prefill_scores(args):
     queries attending causally to the whole prompt, per-window masses.  Eight
     prompts of the workload's shape are rotated so that their keys (64 MB each
     at 32K) do not stay in the Infinity Cache between calls; one call reads the
-    keys twice (row statistics, then masses), the second read mostly from that
-    cache."""
+    keys once."""
     import torch
     import paper_2608_05326_amd as qv
     import synthetic as syn
@@ -215,7 +214,7 @@ def bench_prefill_scores(args):
     us = e0.elapsed_time(e1) * 1e3 / steps
     B, Hkv, Hq, T, d = wl.batch, wl.num_kv_heads, wl.num_q_heads, wl.prompt_len, wl.head_dim
     min_bytes = B * (Hkv * T * d * 2 + Hq * n_obs * d * 2 + n_w * 4)
-    flops = 2 * (2 * B * Hq * n_obs * T * d)     # two QK^T passes over every (row, key) pair
+    flops = 2 * B * Hq * n_obs * T * d           # one QK^T over every (row, key) pair
     ach = min_bytes / (us * 1e-6) / 1e9
     res = {
         "metric": "initial window scores µs per prompt layer (observation-query attention masses)",

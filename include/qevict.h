@@ -254,7 +254,7 @@ qevict_status qevict_debug_masses(qevict_cache *c, int32_t layer, float *masses,
 /* Kernel timing with HIP events on the cache's stream (off by default).
  * kernel: 0 attention pass, 1 split merge + score accumulation, 2 re-rank,
  * 3 migrations (quantize and promote / admit, one launch), 4 initial window
- * scores (qevict_prefill_scores, its four launches together).  read
+ * scores (qevict_prefill_scores, its three launches together).  read
  * returns the summed milliseconds and the number of timed launches since
  * enable, and is synchronous. */
 qevict_status qevict_profile_enable(qevict_cache *c, int32_t on);

@@ -32,27 +32,6 @@ __device__ __forceinline__ u32x4 ld16(const void* p) { return *(const u32x4*)p; 
 // wave is ordered; the memory clobber keeps the compiler from moving accesses).
 __device__ __forceinline__ void wave_sync_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-// max / sum over the four 16-lane rows: lanes i, i^16, i^32, i^48 (gfx950 permlane swaps)
-__device__ __forceinline__ float rows_max(float x) {
-  const uint32_t u = __float_as_uint(x);
-  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  const uint32_t a0 = a[0], a1 = a[1];
-  const float y = fmaxf(__uint_as_float(a0), __uint_as_float(a1));
-  const uint32_t v = __float_as_uint(y);
-  const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-  const uint32_t b0 = b[0], b1 = b[1];
-  return fmaxf(__uint_as_float(b0), __uint_as_float(b1));
-}
-__device__ __forceinline__ float rows_sum(float x) {
-  const uint32_t u = __float_as_uint(x);
-  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  const uint32_t a0 = a[0], a1 = a[1];
-  const float y = __uint_as_float(a0) + __uint_as_float(a1);
-  const uint32_t v = __float_as_uint(y);
-  const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-  const uint32_t b0 = b[0], b1 = b[1];
-  return __uint_as_float(b0) + __uint_as_float(b1);
-}
 // sum over the 16 lanes of a row with DPP (quad swaps, half-row and row mirrors)
 __device__ __forceinline__ float row16_sum(float x) {
   x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));

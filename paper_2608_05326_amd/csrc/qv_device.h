@@ -61,15 +61,41 @@ struct KeyNormArgs {        // key-norm scores of the prompt windows
   float* out;               // [B][n_init]
 };
 
+// max / sum over the four 16-lane rows: lanes i, i^16, i^32, i^48 (gfx950 permlane
+// swaps; every lane of the four gets the same value)
+__device__ __forceinline__ float rows_max(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const uint32_t a0 = a[0], a1 = a[1];
+  const float y = fmaxf(__uint_as_float(a0), __uint_as_float(a1));
+  const uint32_t v = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  const uint32_t b0 = b[0], b1 = b[1];
+  return fmaxf(__uint_as_float(b0), __uint_as_float(b1));
+}
+__device__ __forceinline__ float rows_sum(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const uint32_t a0 = a[0], a1 = a[1];
+  const float y = __uint_as_float(a0) + __uint_as_float(a1);
+  const uint32_t v = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  const uint32_t b0 = b[0], b1 = b[1];
+  return __uint_as_float(b0) + __uint_as_float(b1);
+}
+
 struct ObsArgs {            // initial window scores from the observation queries' attention
   const uint16_t* q;        // [B][H_q][n_obs][d] bf16
   const uint16_t* k;        // [B][H_kv][T][d] bf16
   int32_t B, H_q, H_kv, gqa, T, n_obs, n_rows, W, sink, n_w;
-  int32_t n_blk, T_pad;     // key blocks of 256; n_blk * 256
+  int32_t cbase;            // first key of chunk 0 (sink - 64 n_pre, <= 0)
+  int32_t n_pre;            // chunks before the first window (sink keys)
+  int32_t n_chunks;         // chunks of 64 keys
+  int32_t n_blk;            // workgroups of four chunks
   float scale_log2;
-  float2* blk_ml;           // [B][H_kv][n_rows][n_blk] (max, exp-sum) per key block
+  float2* cml;              // [B][H_kv][n_chunks][n_rows] (max, exp-sum) per chunk and row
+  float* wl;                // [B][H_kv][n_w][n_rows] window exp-sum relative to its chunk's max
   float2* row_ml;           // [B][H_kv][n_rows] (M, 1 / L)
-  float* key_mass;          // [B][H_kv][T_pad] mass per key, summed over rows
   float* scores;            // [B][n_w]
 };
 

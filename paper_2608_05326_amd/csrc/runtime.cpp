@@ -593,11 +593,24 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
 
 // ---- initial window scores from the observation queries -------------------
 namespace {
-constexpr int kObsKeysPerBlock = 256;   // keys per workgroup of the observation passes
+constexpr int kObsChunk = 64;   // keys per chunk (one wave) of the observation pass
 
 struct ObsScratch {
-  int64_t blk_ml, row_ml, key_mass, bytes;
+  int64_t cml, wl, row_ml, bytes;
 };
+
+struct ObsShape {
+  int n_w, n_pre, n_chunks;
+};
+
+ObsShape obs_shape(const qevict_config* cfg, int32_t prompt_len) {
+  ObsShape s;
+  const int sink = cfg->sink_tokens, W = cfg->window_tokens;
+  s.n_w = prompt_len > sink ? ceil_div(prompt_len - sink, W) : 0;
+  s.n_pre = ceil_div(sink, kObsChunk);
+  s.n_chunks = s.n_pre + (prompt_len > sink ? ceil_div(prompt_len - sink, kObsChunk) : 0);
+  return s;
+}
 
 qevict_status obs_check(const qevict_config* cfg, int32_t prompt_len, int32_t n_obs) {
   if (prompt_len < 1 || prompt_len > cfg->max_context)
@@ -609,13 +622,13 @@ qevict_status obs_check(const qevict_config* cfg, int32_t prompt_len, int32_t n_
 
 ObsScratch obs_scratch(const qevict_config* cfg, int32_t prompt_len, int32_t n_obs) {
   const int64_t rows = (int64_t)cfg->num_q_heads / cfg->num_kv_heads * n_obs;
-  const int64_t n_blk = ceil_div(prompt_len, kObsKeysPerBlock);
+  const ObsShape sh = obs_shape(cfg, prompt_len);
   const int64_t bh = (int64_t)cfg->batch * cfg->num_kv_heads;
   ObsScratch s;
-  s.blk_ml = 0;
-  s.row_ml = align256(s.blk_ml + 8 * bh * rows * n_blk);
-  s.key_mass = align256(s.row_ml + 8 * bh * rows);
-  s.bytes = align256(s.key_mass + 4 * bh * n_blk * kObsKeysPerBlock);
+  s.cml = 0;
+  s.wl = align256(s.cml + 8 * bh * sh.n_chunks * rows);
+  s.row_ml = align256(s.wl + 4 * bh * sh.n_w * rows);
+  s.bytes = align256(s.row_ml + 8 * bh * rows);
   return s;
 }
 }  // namespace
@@ -638,7 +651,8 @@ qevict_status qevict_prefill_scores(qevict_cache* c, const uint16_t* q_obs, int3
   qevict_status s = obs_check(&cfg, prompt_len, n_obs);
   if (s) return s;
   const Geometry& g = c->g;
-  const int n_w = prompt_len > g.sink ? ceil_div(prompt_len - g.sink, g.W) : 0;
+  const ObsShape sh = obs_shape(&cfg, prompt_len);
+  const int n_w = sh.n_w;
   if (!q_obs || !k || !scratch || (!scores && n_w > 0))
     return fail(QEVICT_ERR_INVALID_ARG, "null pointer");
   if (((uintptr_t)q_obs & 15) || ((uintptr_t)k & 15) || ((uintptr_t)scores & 15))
@@ -661,13 +675,15 @@ qevict_status qevict_prefill_scores(qevict_cache* c, const uint16_t* q_obs, int3
   a.W = g.W;
   a.sink = g.sink;
   a.n_w = n_w;
-  a.n_blk = ceil_div(prompt_len, kObsKeysPerBlock);
-  a.T_pad = a.n_blk * kObsKeysPerBlock;
+  a.n_pre = sh.n_pre;
+  a.cbase = g.sink - kObsChunk * sh.n_pre;
+  a.n_chunks = sh.n_chunks;
+  a.n_blk = ceil_div(sh.n_chunks, 4);
   a.scale_log2 = g.scale_log2;
   uint8_t* sb = (uint8_t*)scratch;
-  a.blk_ml = (float2*)(sb + L.blk_ml);
+  a.cml = (float2*)(sb + L.cml);
+  a.wl = (float*)(sb + L.wl);
   a.row_ml = (float2*)(sb + L.row_ml);
-  a.key_mass = (float*)(sb + L.key_mass);
   a.scores = scores;
   const hipError_t e = timed(c, 4, c->stream, [&] { return launch_prefill_scores(a, c->stream); });
   if (e != hipSuccess) return hip_fail(e, "prefill_scores launch");

@@ -83,10 +83,11 @@ def test_status_strings():
 
 def test_prefill_scores_scratch_size():
     cfg = _cfg()
-    # per (sequence, KV head): rows x blocks (max, sum) pairs, rows (M, 1/L), a mass per key
-    rows, n_blk = 4 * 32, -(-32768 // 256)
+    # per (sequence, KV head): a (max, sum) pair per row and 64-key chunk, a sum per
+    # row and window, (M, 1/L) per row
+    rows, n_chunks, n_w = 4 * 32, 32768 // 64, 32768 // 32
     n = qv.qevict.prefill_scores_scratch_size(cfg, 32768, 32)
-    expect = 8 * (8 * rows * n_blk) + 8 * (8 * rows) + 4 * (8 * n_blk * 256)
+    expect = 8 * (8 * rows * n_chunks) + 4 * (8 * rows * n_w) + 8 * (8 * rows)
     assert expect <= n <= expect + 3 * 256
     for T, n_obs in [(0, 1), (100, 0), (100, 101), (10 ** 6, 1), (8192, 4097)]:
         with pytest.raises(qv.QEvictError) as e:
