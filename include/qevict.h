@@ -145,6 +145,25 @@ typedef struct {
   int32_t n_full, n_quant_int4, n_quant_int2;  /* tier sizes after the event */
 } qevict_retier_stats;
 
+/* Tier capacities from a byte budget (Sec. 4.3, byte-constrained tier
+ * allocation): after the protected sink and recent regions (bf16 keys and
+ * values: 4 * H_kv * d bytes per token), a share q of the remaining historical
+ * budget B_hist goes to the Quantized tier and 1 - q to the Full tier:
+ *   K_f = floor((1 - q) B_hist / M_f),  K_q = floor(q B_hist / M_q).
+ * Per-window costs (one layer, one sequence):
+ *   M_f = 4 H_kv W d (bf16 keys and values) + 4 (slot index) + 4 (position)
+ *   M_q = 2 H_kv W d b / 8 (codes, b = 4 for QEVICT_BITS_MIXED_4_2: the slot
+ *         size) + 4 H_kv d W / G (key scale and zero point, fp16)
+ *         + 4 H_kv W d / G (value scale and zero point) + 4 + 4 (slot index,
+ *         position) + 2 (ledger state and bit width)
+ * budget_bytes is per layer and sequence; q is given in thousandths
+ * (0 .. 1000) and the arithmetic is exact in integers.  The capacity fields
+ * of cfg are ignored; every other field is validated as by
+ * qevict_workspace_size.  Fails with QEVICT_ERR_INVALID_ARG when the budget
+ * does not cover the protected regions (host only). */
+qevict_status qevict_capacities_for_budget(const qevict_config *cfg, int64_t budget_bytes,
+                                           int32_t q_permille, int32_t *k_full, int32_t *k_quant);
+
 /* Bytes of device workspace a cache with this config needs (host only). */
 qevict_status qevict_workspace_size(const qevict_config *cfg, size_t *bytes);
 

@@ -45,6 +45,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
+from fractions import Fraction
 
 import numpy as np
 
@@ -54,7 +55,7 @@ __all__ = [
     "OPEN", "AGED", "FULL", "QUANT", "EVICTED", "ACTIVE", "DORMANT",
     "OracleConfig", "QEvictUnit", "quantize_groups", "quantize_window",
     "dequantize_window", "route_order", "tier_split", "QuantRangeError", "CapacityError",
-    "prefill_window_scores",
+    "prefill_window_scores", "window_costs", "tier_capacities",
 ]
 
 # window states; OPEN and AGED are both inside / just out of the recent region
@@ -195,6 +196,45 @@ def dequantize_window(e: dict):
     vz = np.repeat(e["vz"], g, axis=2)
     vs = np.repeat(e["vs"], g, axis=2)
     return kz + ks * e["kc"], vz + vs * e["vc"]
+
+
+# ----------------------------------------------------------------------------
+# Byte-constrained tier allocation (Sec. 4.3; memory accounting appendix)
+# ----------------------------------------------------------------------------
+
+def window_costs(num_kv_heads: int, head_dim: int, window: int, group: int, bits: int):
+    """Bytes one window occupies in the Full tier (M_f) and in the Quantized tier
+    (M_q), for one layer and sequence.
+
+    Full: bf16 keys and values, plus a slot index and a position (4 bytes each).
+    Quantized: packed b-bit codes of keys and values (b = 4 for the mixed
+    int4/int2 tier, whose slots hold the larger record), fp16 scale and zero
+    point per key group (channel x W/G token groups) and per value group (token
+    x d/G channel groups), slot index and position, and a 2-byte ledger entry
+    (state, bit width) -- the codes, parameters, positions and persistent
+    indexing state the paper lists.
+    """
+    b = 2 if bits == 2 else 4
+    kv_elems = 2 * num_kv_heads * window * head_dim
+    m_f = 2 * kv_elems + 4 + 4
+    params = 2 * 2 * num_kv_heads * head_dim * (window // group) \
+        + 2 * 2 * num_kv_heads * window * (head_dim // group)
+    m_q = kv_elems * b // 8 + params + 4 + 4 + 2
+    return m_f, m_q
+
+
+def tier_capacities(budget_bytes: int, q_permille: int, num_kv_heads: int, head_dim: int,
+                    window: int, group: int, bits: int, sink: int, recent: int):
+    """K_f = floor((1 - q) B_hist / M_f), K_q = floor(q B_hist / M_q) (tier
+    capacities equation), B_hist = the budget left after the protected sink and
+    recent tokens (bf16 keys and values).  Exact rational arithmetic."""
+    protected = 2 * 2 * num_kv_heads * head_dim * (sink + recent)
+    if budget_bytes < protected:
+        raise ValueError("budget below the protected regions")
+    b_hist = budget_bytes - protected
+    q = Fraction(q_permille, 1000)
+    m_f, m_q = window_costs(num_kv_heads, head_dim, window, group, bits)
+    return math.floor((1 - q) * b_hist / m_f), math.floor(q * b_hist / m_q)
 
 
 # ----------------------------------------------------------------------------

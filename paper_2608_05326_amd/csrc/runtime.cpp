@@ -455,6 +455,34 @@ const char* qevict_status_string(qevict_status s) {
 
 const char* qevict_last_error(void) { return g_last_error.c_str(); }
 
+qevict_status qevict_capacities_for_budget(const qevict_config* cfg, int64_t budget_bytes,
+                                           int32_t q_permille, int32_t* k_full, int32_t* k_quant) {
+  if (!cfg || !k_full || !k_quant) return fail(QEVICT_ERR_INVALID_ARG, "null pointer");
+  qevict_config c = *cfg;
+  c.capacity_full = 1;   // capacities are the output: validate the rest
+  c.capacity_quant = 0;
+  qevict_status s = check_config(&c);
+  if (s) return s;
+  if (q_permille < 0 || q_permille > 1000) return fail(QEVICT_ERR_INVALID_ARG, "q_permille");
+  const int64_t Hkv = c.num_kv_heads, d = c.head_dim, W = c.window_tokens, G = c.group_size;
+  const int64_t bits = c.quant_bits == 2 ? 2 : 4;
+  const int64_t protect = 4 * Hkv * d * ((int64_t)c.sink_tokens + c.recent_tokens);
+  if (budget_bytes < protect)
+    return fail(QEVICT_ERR_INVALID_ARG, "budget %lld below the protected regions (%lld bytes)",
+                (long long)budget_bytes, (long long)protect);
+  const int64_t hist = budget_bytes - protect;
+  const int64_t m_f = 4 * Hkv * W * d + 8;
+  const int64_t m_q = 2 * Hkv * W * d * bits / 8 + 4 * Hkv * d * (W / G) + 4 * Hkv * W * (d / G) + 10;
+  // exact: floor(((1000 - q) / 1000) * hist / m_f); hist < 2^48 keeps the products in range
+  if (hist >= ((int64_t)1 << 48)) return fail(QEVICT_ERR_INVALID_ARG, "budget too large");
+  const int64_t kf = (1000 - q_permille) * hist / (1000 * m_f);
+  const int64_t kq = q_permille * hist / (1000 * m_q);
+  if (kf > INT32_MAX || kq > INT32_MAX) return fail(QEVICT_ERR_INVALID_ARG, "budget too large");
+  *k_full = (int32_t)kf;
+  *k_quant = (int32_t)kq;
+  return QEVICT_OK;
+}
+
 qevict_status qevict_workspace_size(const qevict_config* cfg, size_t* bytes) {
   qevict_status s = check_config(cfg);
   if (s) return s;

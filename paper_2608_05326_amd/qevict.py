@@ -34,7 +34,7 @@ SYMBOLS = (
     "qevict_get_state", "qevict_export_window", "qevict_debug_shift_keys", "qevict_debug_masses",
     "qevict_profile_enable", "qevict_profile_read", "qevict_last_attend_bytes", "qevict_join_routing",
     "qevict_status_string", "qevict_last_error", "qevict_prefill_scores_scratch_size",
-    "qevict_prefill_scores",
+    "qevict_prefill_scores", "qevict_capacities_for_budget",
 )
 
 
@@ -129,6 +129,7 @@ def load_library(path: str | None = None):
         "qevict_join_routing": [vp],
         "qevict_prefill_scores_scratch_size": [P(_Config), i32, i32, P(ctypes.c_size_t)],
         "qevict_prefill_scores": [vp, vp, i32, vp, i32, vp, ctypes.c_size_t, vp],
+        "qevict_capacities_for_budget": [P(_Config), i64, i32, P(i32), P(i32)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -153,6 +154,15 @@ def workspace_size(cfg: Config) -> int:
     n = ctypes.c_size_t()
     _check(lib, lib.qevict_workspace_size(ctypes.byref(cfg.to_c()), ctypes.byref(n)))
     return n.value
+
+
+def capacities_for_budget(cfg: Config, budget_bytes: int, q_permille: int) -> tuple[int, int]:
+    """(K_f, K_q) from a per-layer, per-sequence byte budget and quantized share q (thousandths)."""
+    lib = load_library()
+    kf, kq = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib, lib.qevict_capacities_for_budget(ctypes.byref(cfg.to_c()), budget_bytes, q_permille,
+                                                 ctypes.byref(kf), ctypes.byref(kq)))
+    return kf.value, kq.value
 
 
 def prefill_scores_scratch_size(cfg: Config, prompt_len: int, n_obs: int) -> int:

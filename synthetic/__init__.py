@@ -61,6 +61,8 @@ class Workload:
     shift_every: int = 4
     shift_scale: float = 3.0
     init_sigma: float = 1.0          # log-normal spread of the prefill window scores
+    budget_frac: str = ""            # byte budget as a fraction of the full cache (capacities
+    q_frac: str = ""                 # from the byte-budget equation), and the quantized share
 
     @property
     def gqa(self) -> int:
@@ -125,6 +127,14 @@ WORKLOADS = {
     "c5": Workload("c5", 5, batch=4, layers=1, num_q_heads=64, num_kv_heads=8, head_dim=128,
                    prompt_len=65536, window=32, group=32, bits=42, frac_full="0.2",
                    frac_quant="0.4", steps=128, retier_interval=8, **_drift_defaults()),
+    # The paper's default operating point on the 8B shape: five sink tokens, 32 recent
+    # tokens, routing every 8 steps, int2 tier, quantized fraction q = 0.70 of the
+    # historical byte budget (20% of the full cache), windows of 32 (this build's
+    # smallest window); capacities from the byte-budget equation.
+    "c6": Workload("c6", 6, batch=1, layers=1, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                   prompt_len=32768, window=32, group=32, bits=2, frac_full="0", frac_quant="0",
+                   steps=128, retier_interval=8, sink=5, recent=32, budget_frac="0.2", q_frac="0.7",
+                   **_drift_defaults()),
 }
 
 # Reduced-size variants with the same head layouts and tier policies: they span
@@ -136,6 +146,12 @@ WORKLOADS.update({
     "c3s": WORKLOADS["c3"].replace(name="c3s", batch=2, layers=2, prompt_len=32 * 64 + 5, steps=24),
     "c4s": WORKLOADS["c4"].replace(name="c4s", prompt_len=64 * 80 + 37, steps=24),
     "c5s": WORKLOADS["c5"].replace(name="c5s", batch=2, prompt_len=32 * 96 + 29, steps=40),
+    "c6s": WORKLOADS["c6"].replace(name="c6s", prompt_len=32 * 96 + 23, steps=40),
+    # a sink of two and a half windows, a recent region that is not a whole number
+    # of windows, routing every 3 steps, mixed int4 / int2
+    "c7s": WORKLOADS["c5"].replace(name="c7s", config_id=7, batch=2, prompt_len=32 * 90 + 3, steps=30,
+                                   sink=80, recent=70, retier_interval=3, frac_full="0.2",
+                                   frac_quant="0.3"),
 })
 
 

@@ -31,12 +31,30 @@ def to_dev_bf16(bits: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
 
 
+def budget_capacities(wl: syn.Workload):
+    """(K_f, K_q) of a workload given as a byte budget: a fraction of the full
+    bf16 cache of the prompt (2 x H_kv x d x T x 2 bytes per layer and
+    sequence) with quantized share q, through the library's capacity function."""
+    from fractions import Fraction
+    full = 2 * wl.num_kv_heads * wl.head_dim * wl.prompt_len * 2
+    budget = int(Fraction(wl.budget_frac) * full)
+    cfg = qv.Config(batch=wl.batch, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                    window_tokens=wl.window, group_size=wl.group, quant_bits=wl.bits,
+                    max_context=wl.max_context, capacity_full=0, capacity_quant=0,
+                    sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=wl.retier_interval)
+    return qv.qevict.capacities_for_budget(cfg, budget, int(Fraction(wl.q_frac) * 1000))
+
+
 def gpu_config(wl: syn.Workload, layers: int, flags: int = 0, out_dtype: int = qv.OUT_F32,
                num_splits: int = 0, capacity_full=None, capacity_quant=None,
                score_decay: float | None = None, key_norm: bool = False,
                score_p: float | None = None) -> qv.Config:
     mode = qv.SCORE_KEY_NORM if key_norm else qv.SCORE_PNORM if score_p is not None else \
         qv.SCORE_DECAY if score_decay is not None else qv.SCORE_CUMULATIVE
+    if wl.budget_frac:
+        kf, kq = budget_capacities(wl)
+        capacity_full = kf if capacity_full is None else capacity_full
+        capacity_quant = kq if capacity_quant is None else capacity_quant
     return qv.Config(
         batch=wl.batch, num_layers=layers, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
         window_tokens=wl.window, group_size=wl.group, quant_bits=wl.bits, max_context=wl.max_context,

@@ -44,3 +44,9 @@ def test_70b_64k_mixed_bits_batch4():
 def test_8b_32k_batch8_layer_sample():
     # one of the 32 layers, all 8 sequences on the GPU, two mirrored
     _lockstep("c3", steps=3, layer_ids=(31,), check_seqs=[0, 7])
+
+
+def test_8b_32k_paper_default_point():
+    # 5 sink + 32 recent tokens, int2, capacities from a 20% byte budget with q = 0.70
+    # (61 bf16 + 759 int2 windows), routing every 8 steps: step 8 is the first event
+    _lockstep("c6", steps=9)

@@ -55,3 +55,13 @@ def test_pnorm_lockstep(name):
     """Attention p-norm ranking, p = 3 (per step on c2s; periods of 8 steps on
     c5s): scores (held as S^p) and routing against the oracle."""
     _lockstep(name, score_p=3.0)
+
+
+@pytest.mark.parametrize("name", ["c6s", "c7s"])
+def test_sink_and_recent_lockstep(name):
+    """Protected sink and recent regions: c6s is the paper's default point (5
+    sink and 32 recent tokens, routing every 8 steps, int2, capacities from a
+    20% byte budget with q = 0.70); c7s has a sink of two and a half windows,
+    a recent region of 70 tokens, routing every 3 steps and mixed bits."""
+    ls = _lockstep(name)
+    assert ls.events > 0

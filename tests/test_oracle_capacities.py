@@ -1,0 +1,71 @@
+"""Pins for the byte-constrained tier capacities (Sec. 4.3 tier capacities
+equation; memory accounting appendix) and the library's copy of them.
+
+* a worked example at the paper's default point on the 8B shape (32K prompt,
+  20% of the full cache, q = 0.70, int2, W = 32, five sink and 32 recent
+  tokens), with the byte counts written out by hand below;
+* floor properties: the chosen capacities fit their shares and one more
+  window would not; q = 0 and q = 1 leave one tier empty;
+* the host function of the library returns the same capacities over a sweep
+  of configurations (no GPU needed).
+"""
+from fractions import Fraction
+
+import pytest
+
+from oracle.qevict_oracle import tier_capacities, window_costs
+
+
+def test_worked_example_paper_default_8b():
+    # full cache of one layer: 2 (K, V) x 8 heads x 128 channels x 32768 tokens x 2 B
+    full = 134_217_728
+    budget = 26_843_545                      # floor(0.2 x full)
+    # protected: 37 tokens x 4 KiB (bf16 K and V over 8 heads) = 151,552 B
+    b_hist = 26_691_993
+    # M_f = 131,072 (bf16 window) + 8;  M_q = 16,384 (int2 codes) + 4,096 (key params)
+    #       + 4,096 (value params) + 10
+    assert window_costs(8, 128, 32, 32, 2) == (131_080, 24_586)
+    assert budget == int(Fraction(2, 10) * full)
+    # K_f = floor(0.3 x 26,691,993 / 131,080) = floor(61.09), K_q = floor(0.7 x ... / 24,586) = floor(759.96)
+    assert tier_capacities(budget, 700, 8, 128, 32, 32, 2, 5, 32) == (61, 759)
+    assert budget - b_hist == 151_552
+
+
+@pytest.mark.parametrize("q", [0, 150, 500, 700, 999, 1000])
+@pytest.mark.parametrize("bits,W", [(2, 32), (4, 32), (42, 32), (2, 64)])
+def test_floor_properties(q, bits, W):
+    budget, sink, recent = 9_876_543, 5, 32
+    kf, kq = tier_capacities(budget, q, 8, 128, W, W, bits, sink, recent)
+    m_f, m_q = window_costs(8, 128, W, W, bits)
+    b_hist = budget - 4 * 8 * 128 * (sink + recent)
+    qf = Fraction(q, 1000)
+    assert kf * m_f <= (1 - qf) * b_hist < (kf + 1) * m_f
+    assert kq * m_q <= qf * b_hist < (kq + 1) * m_q
+    assert kf * m_f + kq * m_q <= b_hist
+    if q == 0:
+        assert kq == 0
+    if q == 1000:
+        assert kf == 0
+
+
+def test_budget_below_protected_regions():
+    with pytest.raises(ValueError):
+        tier_capacities(4 * 8 * 128 * 37 - 1, 700, 8, 128, 32, 32, 2, 5, 32)
+
+
+def test_library_matches_oracle():
+    import paper_2608_05326_amd as qv
+    for H_kv, W, bits, sink, recent, budget, q in [
+        (8, 32, 2, 5, 32, 26_843_545, 700), (8, 32, 4, 0, 0, 13_421_772, 300),
+        (8, 64, 2, 64, 128, 50_000_000, 900), (8, 32, 42, 40, 70, 7_000_000, 550),
+        (1, 32, 4, 0, 100, 3_000_000, 0), (4, 64, 2, 3, 0, 1_000_000, 1000),
+    ]:
+        cfg = qv.Config(batch=1, num_q_heads=4 * H_kv, num_kv_heads=H_kv, window_tokens=W,
+                        quant_bits=bits, max_context=65536, capacity_full=0, capacity_quant=0,
+                        sink_tokens=sink, recent_tokens=recent)
+        assert qv.qevict.capacities_for_budget(cfg, budget, q) == \
+            tier_capacities(budget, q, H_kv, 128, W, W, bits, sink, recent)
+    with pytest.raises(qv.QEvictError):
+        qv.qevict.capacities_for_budget(cfg, 10, 500)
+    with pytest.raises(qv.QEvictError):
+        qv.qevict.capacities_for_budget(cfg, budget, 1001)
