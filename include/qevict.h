@@ -164,6 +164,26 @@ typedef struct {
 qevict_status qevict_capacities_for_budget(const qevict_config *cfg, int64_t budget_bytes,
                                            int32_t q_permille, int32_t *k_full, int32_t *k_quant);
 
+/* Persistent cache bytes of one (layer, sequence) in the current state, split
+ * as the memory accounting appendix lists them (M_sink + M_recent + M_FP + M_Q
+ * + M_quant-meta + M_position + M_ledger); the per-window costs are those of
+ * qevict_capacities_for_budget, so a state with n_f Full and n_q Quantized
+ * windows (no dormant ledger) totals sink + recent + n_f M_f + n_q M_q.
+ *   sink        bf16 keys and values of the sink tokens held
+ *   recent      bf16 keys and values of the tokens after the routed windows
+ *   full        bf16 keys and values of the Full windows
+ *   quant_codes packed codes of the Quantized windows (each at its bit width)
+ *   quant_meta  their fp16 scales and zero points
+ *   position    slot index and position, 8 bytes per Full or Quantized window
+ *   ledger      codes and parameters kept by dormant ledger entries (promoted
+ *               windows), plus 2 bytes per ledger entry (active or dormant)
+ * Workspace beyond these (live lists, split statistics, spare slots) is not
+ * counted.  Synchronous, like qevict_get_state. */
+typedef struct {
+  int64_t sink, recent, full, quant_codes, quant_meta, position, ledger, total;
+} qevict_memory;
+qevict_status qevict_memory_report(qevict_cache *c, int32_t layer, int32_t seq, qevict_memory *out);
+
 /* Bytes of device workspace a cache with this config needs (host only). */
 qevict_status qevict_workspace_size(const qevict_config *cfg, size_t *bytes);
 

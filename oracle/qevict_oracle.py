@@ -55,7 +55,7 @@ __all__ = [
     "OPEN", "AGED", "FULL", "QUANT", "EVICTED", "ACTIVE", "DORMANT",
     "OracleConfig", "QEvictUnit", "quantize_groups", "quantize_window",
     "dequantize_window", "route_order", "tier_split", "QuantRangeError", "CapacityError",
-    "prefill_window_scores", "window_costs", "tier_capacities",
+    "prefill_window_scores", "window_costs", "tier_capacities", "memory_report",
 ]
 
 # window states; OPEN and AGED are both inside / just out of the recent region
@@ -235,6 +235,39 @@ def tier_capacities(budget_bytes: int, q_permille: int, num_kv_heads: int, head_
     q = Fraction(q_permille, 1000)
     m_f, m_q = window_costs(num_kv_heads, head_dim, window, group, bits)
     return math.floor((1 - q) * b_hist / m_f), math.floor(q * b_hist / m_q)
+
+
+def memory_report(unit: "QEvictUnit") -> dict:
+    """Persistent bytes of a unit by the memory accounting appendix's terms:
+    sink and recent tokens (bf16 K and V), Full windows, Quantized codes and
+    their scale / zero points, 8 bytes of slot index and position per Full or
+    Quantized window, and the ledger: dormant entries keep their codes and
+    parameters, every entry costs 2 bytes.  "recent" counts the tokens after
+    the windows that have been routed."""
+    c = unit.cfg
+    H, d, W, G = c.num_kv_heads, c.head_dim, c.window, c.group
+    tok = 2 * 2 * H * d
+    meta = 2 * 2 * H * d * (W // G) + 2 * 2 * H * W * (d // G)
+    r = dict(sink=tok * min(c.sink, unit.T), recent=0, full=0, quant_codes=0, quant_meta=0,
+             position=0, ledger=0)
+    routed = int(np.sum((unit.state == FULL) | (unit.state == QUANT) | (unit.state == EVICTED)))
+    r["recent"] = tok * max(0, unit.T - c.sink - W * routed)
+    for w in np.nonzero(unit.state >= 0)[0]:
+        st = unit.state[w]
+        if st == FULL:
+            r["full"] += tok * W
+            r["position"] += 8
+        elif st == QUANT:
+            e = unit.ledger[w]
+            r["quant_codes"] += 2 * H * W * d * e["bits"] // 8
+            r["quant_meta"] += meta
+            r["position"] += 8
+    for w, e in unit.ledger.items():
+        r["ledger"] += 2
+        if e["state"] == DORMANT:
+            r["ledger"] += 2 * H * W * d * e["bits"] // 8 + meta
+    r["total"] = sum(r.values())
+    return r
 
 
 # ----------------------------------------------------------------------------

@@ -908,6 +908,42 @@ qevict_status qevict_get_state(qevict_cache* c, int32_t layer, int32_t seq, int8
   return device_errors(c, layer);
 }
 
+qevict_status qevict_memory_report(qevict_cache* c, int32_t layer, int32_t seq, qevict_memory* out) {
+  if (!out) return fail(QEVICT_ERR_INVALID_ARG, "out is NULL");
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  const Geometry& g = c->g;
+  std::vector<int8_t> tiers(g.nwc), ledger(g.nwc), bits(g.nwc);
+  int32_t n = 0;
+  s = qevict_get_state(c, layer, seq, tiers.data(), nullptr, ledger.data(), bits.data(), g.nwc, &n);
+  if (s) return s;
+  const int64_t T = c->layers[layer].T, Hkv = g.H_kv, d = g.d, W = g.W, G = g.G;
+  const int64_t tok = 4 * Hkv * d;   // bf16 key and value of one token
+  const int64_t meta = 4 * Hkv * d * (W / G) + 4 * Hkv * W * (d / G);
+  int64_t routed = 0;
+  qevict_memory m{};
+  m.sink = tok * std::min<int64_t>(g.sink, T);
+  for (int w = 0; w < n; ++w) {
+    const int t = tiers[w];
+    if (t == T_FULL || t == T_QUANT || t == T_EVICTED) ++routed;
+    const int64_t codes = 2 * Hkv * W * d * bits[w] / 8;
+    if (t == T_FULL) {
+      m.full += tok * W;
+      m.position += 8;
+    } else if (t == T_QUANT) {
+      m.quant_codes += codes;
+      m.quant_meta += meta;
+      m.position += 8;
+    }
+    if (ledger[w] == L_DORMANT) m.ledger += codes + meta;
+    if (ledger[w] != L_NONE) m.ledger += 2;
+  }
+  m.recent = tok * std::max<int64_t>(0, T - g.sink - W * routed);
+  m.total = m.sink + m.recent + m.full + m.quant_codes + m.quant_meta + m.position + m.ledger;
+  *out = m;
+  return QEVICT_OK;
+}
+
 qevict_status qevict_export_window(qevict_cache* c, int32_t layer, int32_t seq, int32_t window,
                                    uint8_t* codes_k, uint8_t* codes_v, uint16_t* meta_k,
                                    uint16_t* meta_v, uint16_t* full_k, uint16_t* full_v) {

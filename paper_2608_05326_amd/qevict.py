@@ -34,7 +34,7 @@ SYMBOLS = (
     "qevict_get_state", "qevict_export_window", "qevict_debug_shift_keys", "qevict_debug_masses",
     "qevict_profile_enable", "qevict_profile_read", "qevict_last_attend_bytes", "qevict_join_routing",
     "qevict_status_string", "qevict_last_error", "qevict_prefill_scores_scratch_size",
-    "qevict_prefill_scores", "qevict_capacities_for_budget",
+    "qevict_prefill_scores", "qevict_capacities_for_budget", "qevict_memory_report",
 )
 
 
@@ -51,6 +51,14 @@ class _Config(ctypes.Structure):
         "capacity_full", "capacity_quant", "retier_interval", "out_dtype")] + [
         ("flags", ctypes.c_uint32), ("softmax_scale", ctypes.c_float), ("num_splits", ctypes.c_int32),
         ("score_mode", ctypes.c_int32), ("score_decay", ctypes.c_float), ("score_p", ctypes.c_float)]
+
+
+class MemoryReport(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in (
+        "sink", "recent", "full", "quant_codes", "quant_meta", "position", "ledger", "total")]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
 
 
 class RetierStats(ctypes.Structure):
@@ -130,6 +138,7 @@ def load_library(path: str | None = None):
         "qevict_prefill_scores_scratch_size": [P(_Config), i32, i32, P(ctypes.c_size_t)],
         "qevict_prefill_scores": [vp, vp, i32, vp, i32, vp, ctypes.c_size_t, vp],
         "qevict_capacities_for_budget": [P(_Config), i64, i32, P(i32), P(i32)],
+        "qevict_memory_report": [vp, i32, i32, P(MemoryReport)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -250,6 +259,12 @@ class Cache:
             _ptr(scratch, None, "scratch"), scratch.numel() * scratch.element_size(),
             _ptr(scores, t.float32, "scores") if n_w else None))
         return scores
+
+    def memory_report(self, layer: int, seq: int) -> dict:
+        """Persistent cache bytes of one (layer, sequence), by component."""
+        m = MemoryReport()
+        self._c(self.lib.qevict_memory_report(self.handle, layer, seq, ctypes.byref(m)))
+        return m.as_dict()
 
     def decode_attend(self, layer: int, q, k_new, v_new, out):
         t = self.torch

@@ -135,6 +135,12 @@ class Lockstep:
             assert np.array_equal(mv[:, 0], e["vs"]) and np.array_equal(mv[:, 1], e["vz"]), \
                 f"value scale / zero, window {w}"
 
+    def compare_memory(self, li, b):
+        from oracle.qevict_oracle import memory_report
+        got = self.cache.memory_report(li, b)
+        exp = memory_report(self.units[(li, b)])
+        assert got == exp, f"memory report {got} != {exp}"
+
     def compare_full(self, li, b, windows):
         u = self.units[(li, b)]
         for w in windows:
@@ -212,6 +218,7 @@ class Lockstep:
                     u.adopt_scores(sg)
                     u.finish_prefill()
                 self.compare_state(li, b)
+                self.compare_memory(li, b)
                 self.compare_ledgers(li, b, sorted(u.ledger))
                 full = [w for w in range(u.n_win_cap) if u.state[w] == 2]
                 self.compare_full(li, b, full[:: max(1, len(full) // 16)])
@@ -264,6 +271,7 @@ class Lockstep:
                     before_state = u.state.copy()
                     u.route()
                     st = self.compare_state(li, b, check_scores=False)
+                    self.compare_memory(li, b)
                     new_led = [w for w in u.ledger if w not in before_ledger]
                     self.compare_ledgers(li, b, new_led)
                     promoted = [w for w in range(u.n_win_cap)

@@ -69,3 +69,49 @@ def test_library_matches_oracle():
         qv.qevict.capacities_for_budget(cfg, 10, 500)
     with pytest.raises(qv.QEvictError):
         qv.qevict.capacities_for_budget(cfg, budget, 1001)
+
+
+def test_memory_report_of_a_routed_cache():
+    """A prompt of 11.25 windows of 4 tokens after 3 sink tokens, 5 recent
+    tokens, 2 Full and 3 int4 windows: the bytes counted by hand, and the total
+    agrees with the per-window costs of the capacity equation; then a smaller
+    cache where a promotion leaves a dormant ledger entry."""
+    import numpy as np
+    from oracle.qevict_oracle import FULL, QUANT, OracleConfig, QEvictUnit, memory_report
+    H, d, W = 2, 8, 4
+    cfg = OracleConfig(4, H, d, W, W, 4, 2, 3, sink=3, recent=5)
+    u = QEvictUnit(cfg, 3 + 4 * 12)
+    T = 3 + 4 * 10 + 5
+    rng = np.random.default_rng(0)
+    u.prefill(rng.normal(size=(H, T, d)), rng.normal(size=(H, T, d)), rng.permutation(12) / 12.0)
+    r = memory_report(u)
+    tok = 2 * 2 * H * d                       # 64 bytes per token
+    assert r["sink"] == 3 * 64 and tok == 64
+    # windows tile [3, 48): 11 complete and one of a single token; routed are the complete
+    # windows ending at or before T - 5 = 43, windows 0..9 (tokens 3..42), so
+    # 48 - 3 - 40 = 5 tokens count as recent
+    assert r["recent"] == 5 * 64
+    assert r["full"] == 2 * 4 * 64
+    codes = 2 * H * W * d * 4 // 8            # 64 bytes of int4 codes per window
+    # fp16 scale and zero point: keys per (head, channel) = 2 x 8 x 4 B, values per
+    # (head, token, group of 4 channels) = 2 x 4 x 2 x 4 B
+    meta = 64 + 64
+    assert r["quant_codes"] == 3 * codes and r["quant_meta"] == 3 * meta
+    assert r["position"] == 5 * 8
+    assert r["ledger"] == 3 * 2
+    m_f, m_q = window_costs(H, d, W, W, 4)
+    assert r["total"] == r["sink"] + r["recent"] + 2 * m_f + 3 * m_q
+    # four routed windows (2 Full, 2 Quantized, one Quantized slot free): demote a Full
+    # window, then promote a Quantized one, whose ledger turns dormant
+    v = QEvictUnit(cfg, 3 + 4 * 6)
+    T = 3 + 4 * 4 + 5
+    v.prefill(rng.normal(size=(H, T, d)), rng.normal(size=(H, T, d)), rng.permutation(6) / 6.0)
+    r = memory_report(v)
+    assert (r["full"], r["quant_codes"], r["ledger"]) == (2 * 4 * 64, 2 * codes, 2 * 2)
+    q = [w for w in range(6) if v.state[w] == QUANT][0]
+    f = [w for w in range(6) if v.state[w] == FULL][0]
+    v.quantize_one(f)
+    v.promote_one(q)
+    r2 = memory_report(v)
+    assert (r2["full"], r2["quant_codes"]) == (r["full"], r["quant_codes"])
+    assert r2["ledger"] == 3 * 2 + codes + meta    # three entries, one of them dormant
