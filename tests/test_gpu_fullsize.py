@@ -50,3 +50,20 @@ def test_8b_32k_paper_default_point():
     # 5 sink + 32 recent tokens, int2, capacities from a 20% byte budget with q = 0.70
     # (61 bf16 + 759 int2 windows), routing every 8 steps: step 8 is the first event
     _lockstep("c6", steps=9)
+
+
+def test_max_candidates_4000_windows():
+    # 4000 routed prompt windows of 32 tokens (the re-rank kernel sorts up to 4096
+    # candidates in one workgroup): K_f = 1000, K_q = 3000, two routing events
+    wl = syn.get_workload("c2").replace(name="cmax", prompt_len=32 * 4000 + 5, steps=2,
+                                        frac_full="0.25", frac_quant="0.75")
+    from tests.gpu_harness import Lockstep
+    ls = Lockstep(wl, steps=2)
+    print(f"[fullsize] cmax prompt={wl.prompt_len} K_f={ls.cfg.capacity_full} "
+          f"K_q={ls.cfg.capacity_quant}", flush=True)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[fullsize] cmax: max out err {ls.max_out_err:.2e}, max score err {ls.max_score_err:.2e}",
+          flush=True)

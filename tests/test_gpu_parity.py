@@ -65,3 +65,18 @@ def test_sink_and_recent_lockstep(name):
     a recent region of 70 tokens, routing every 3 steps and mixed bits."""
     ls = _lockstep(name)
     assert ls.events > 0
+
+
+@pytest.mark.parametrize("name,splits", [("c2s", 1), ("c2s", 7), ("c5s", 64)])
+def test_split_counts(name, splits):
+    """One split, an odd count, and 64 splits of 4 waves for about 50 items
+    (most waves get no window): outputs and masses against the oracle."""
+    _lockstep(name, num_splits=splits, steps=12)
+
+
+@pytest.mark.parametrize("kf,kq", [(0, 28), (19, 0), (40, 60)])
+def test_tier_extremes(kf, kq):
+    """Quantized tier only (K_f = 0), eviction only (K_q = 0, the two-tier
+    policy) and more capacity than windows (nothing is evicted)."""
+    ls = _lockstep("c2s", capacity_full=kf, capacity_quant=kq, steps=16)
+    assert ls.events == 16
