@@ -27,6 +27,11 @@ What it computes, and where the paper defines it (QEvict, arXiv 2608.05326):
   the causal attention mass that the last n_obs prompt queries put on each
   window (Sec. 4.2: prompt attention initialises the scores; the observation
   window is a reading).
+* RoPE-aware Quantized tier (Sec. 4.3: keys are quantized in the pre-RoPE
+  domain and re-rotated at their original positions after dequantization):
+  the cache receives keys as attention consumes them (post-RoPE); a window's
+  first quantization un-rotates them, and dequantized keys are rotated back
+  for attention and for promotion.
 * Migration-stable asymmetric quantization: keys per channel across tokens,
   values per token across channels; codes are produced once, at a window's
   first demotion, and reused on every later move; promotion reconstructs the
@@ -56,6 +61,7 @@ __all__ = [
     "OracleConfig", "QEvictUnit", "quantize_groups", "quantize_window",
     "dequantize_window", "route_order", "tier_split", "QuantRangeError", "CapacityError",
     "prefill_window_scores", "window_costs", "tier_capacities", "memory_report",
+    "rope_cos_sin", "rope_rotate", "rope_unrotate_f32",
 ]
 
 # window states; OPEN and AGED are both inside / just out of the recent region
@@ -89,6 +95,7 @@ class OracleConfig:
     score_decay: float = 1.0      # lambda of the decayed score; 1.0 = cumulative score
     key_norm: bool = False        # key-norm score instead of attention
     score_p: float = 0.0          # p of the attention p-norm score; 0 = not used
+    rope_base: float = 0.0        # RoPE base of the Quantized tier's keys; 0 = no RoPE
 
     @property
     def scale(self) -> float:
@@ -196,6 +203,47 @@ def dequantize_window(e: dict):
     vz = np.repeat(e["vz"], g, axis=2)
     vs = np.repeat(e["vs"], g, axis=2)
     return kz + ks * e["kc"], vz + vs * e["vc"]
+
+
+# ----------------------------------------------------------------------------
+# Rotary position embedding of the Quantized tier (Sec. 4.3)
+# ----------------------------------------------------------------------------
+# Half-split RoPE over d channels: channel i < d/2 pairs with i + d/2 and turns
+# by the angle p * base^(-2i/d) at position p.  cos and sin are taken in
+# float64 from the C library (Python's math module) and stored as float32, the
+# table both sides use.
+
+def rope_cos_sin(base: float, head_dim: int, positions):
+    """float32 cos, sin [len(positions), head_dim / 2]."""
+    half = head_dim // 2
+    inv = [math.pow(base, -2.0 * i / head_dim) for i in range(half)]
+    cs = np.empty((len(positions), half), dtype=np.float32)
+    sn = np.empty((len(positions), half), dtype=np.float32)
+    for r, p in enumerate(positions):
+        for i in range(half):
+            ang = float(p) * inv[i]
+            cs[r, i] = math.cos(ang)
+            sn[r, i] = math.sin(ang)
+    return cs, sn
+
+
+def rope_rotate(x, cos, sin):
+    """R(p) x in float64 (each product and sum rounded in float64).
+    x [H, n, d]; cos, sin [n, d/2] (float32 values)."""
+    h = x.shape[-1] // 2
+    c = cos.astype(np.float64)[None]
+    s = sin.astype(np.float64)[None]
+    a, b = x[..., :h], x[..., h:]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+
+
+def rope_unrotate_f32(x, cos, sin):
+    """R(-p) x with every product and sum rounded to float32 (x holds bf16 values)."""
+    h = x.shape[-1] // 2
+    a = x[..., :h].astype(np.float32)
+    b = x[..., h:].astype(np.float32)
+    c, s = cos[None], sin[None]
+    return np.concatenate([a * c + b * s, b * c - a * s], axis=-1)
 
 
 # ----------------------------------------------------------------------------
@@ -372,6 +420,26 @@ class QEvictUnit:
         a = self.cfg.sink + w * self.cfg.window
         return a, a + self.cfg.window
 
+    def _rope(self, w: int):
+        a, b = self.win_range(w)
+        return rope_cos_sin(self.cfg.rope_base, self.cfg.head_dim, range(a, b))
+
+    def _quantize(self, w: int, k, v, bits: int):
+        """First quantization of window w from its bf16 keys (as attention uses
+        them) and values; with RoPE the keys are first un-rotated (float32) and
+        rounded to bf16: the pre-RoPE keys the codes describe."""
+        if self.cfg.rope_base:
+            k = rne_bf16(rope_unrotate_f32(k, *self._rope(w)).astype(np.float64))
+        return quantize_window(k, v, bits, self.cfg.group)
+
+    def _dequantize(self, w: int):
+        """Keys and values of a ledger entry in the attention domain (float64):
+        with RoPE the keys are rotated back to their positions."""
+        kh, vh = dequantize_window(self.ledger[w])
+        if self.cfg.rope_base:
+            kh = rope_rotate(kh, *self._rope(w))
+        return kh, vh
+
     def _age(self):
         """OPEN -> AGED once a window is complete and older than the recent region."""
         c = self.cfg
@@ -464,7 +532,7 @@ class QEvictUnit:
             if st == FULL:
                 kk, vv = self.full_k[w], self.full_v[w]
             elif st == QUANT:
-                kk, vv = dequantize_window(self.ledger[w])
+                kk, vv = self._dequantize(w)
             elif st in (OPEN, AGED):
                 kk, vv = self.k[:, a:b], self.v[:, a:b]
             else:
@@ -531,7 +599,7 @@ class QEvictUnit:
         # F: promote (dequantize, ledger dormant) or admit an aged window
         for w in full:
             if self.state[w] == QUANT:
-                kh, vh = dequantize_window(self.ledger[w])
+                kh, vh = self._dequantize(w)
                 self.full_k[w] = rne_bf16(kh)
                 self.full_v[w] = rne_bf16(vh)
                 self.ledger[w]["state"] = DORMANT
@@ -552,7 +620,7 @@ class QEvictUnit:
                     a, b = self.win_range(w)
                     src_k, src_v = self.k[:, a:b], self.v[:, a:b]
                 bits = c.bits if c.bits in (2, 4) else (4 if rank < half else 2)
-                self.ledger[w] = quantize_window(src_k, src_v, bits, c.group)
+                self.ledger[w] = self._quantize(w, src_k, src_v, bits)
                 self.stats["first_quantizations"] += 1
                 self.quant_count += 1
             elif self.ledger[w]["state"] == DORMANT:
@@ -590,7 +658,7 @@ class QEvictUnit:
         e = self.ledger.get(w)
         if e is None:
             bits = c.bits if c.bits in (2, 4) else 4
-            self.ledger[w] = quantize_window(self.full_k[w], self.full_v[w], bits, c.group)
+            self.ledger[w] = self._quantize(w, self.full_k[w], self.full_v[w], bits)
             self.quant_count += 1
         else:
             e["state"] = ACTIVE
@@ -607,7 +675,7 @@ class QEvictUnit:
             raise ValueError("promotion is disabled (one-way policy)")
         if int(np.sum(self.state == FULL)) >= c.capacity_full:
             raise CapacityError("the Full tier already holds K_f windows")
-        kh, vh = dequantize_window(self.ledger[w])
+        kh, vh = self._dequantize(w)
         self.full_k[w] = rne_bf16(kh)
         self.full_v[w] = rne_bf16(vh)
         self.ledger[w]["state"] = DORMANT
