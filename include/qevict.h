@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define QEVICT_ABI_VERSION 3
+#define QEVICT_ABI_VERSION 4
 
 typedef struct qevict_cache qevict_cache;
 typedef int32_t qevict_status;
@@ -109,6 +109,18 @@ enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT =
  *   workspace per window (completed-period sum and running u). */
 #define QEVICT_SCORE_PNORM 3
 
+/* RoPE-aware Quantized tier (Sec. 4.3: keys are quantized in the pre-RoPE
+ * domain and RoPE is reapplied after dequantization).  With rope_base > 0 the
+ * keys the caller passes (prompt and decode) are taken as attention consumes
+ * them, rotated by half-split RoPE at their absolute positions (channel
+ * i < d/2 pairs with i + d/2, angle p * rope_base^(-2i/d)); Full, recent and
+ * sink tokens keep them as given.  A window's first quantization un-rotates its
+ * keys (float32, each product and sum rounded) and rounds them to bf16: the
+ * codes describe pre-RoPE keys.  Attention rotates dequantized keys back to
+ * their positions; promotion stores RNE_bf16 of the rotation, taken in float64
+ * from the exact z + s c.  cos and sin come from a float32 table of
+ * max_context x d/2 pairs in the workspace, filled at init from the C
+ * library's double-precision cos / sin. */
 typedef struct {
   int32_t abi_version;       /* QEVICT_ABI_VERSION                                          */
   int32_t batch;             /* B sequences, all with the same length                       */
@@ -134,6 +146,7 @@ typedef struct {
   int32_t score_mode;        /* QEVICT_SCORE_CUMULATIVE (0), _DECAY, _KEY_NORM or _PNORM     */
   float score_decay;         /* lambda of QEVICT_SCORE_DECAY, in (0, 1]                       */
   float score_p;             /* p of QEVICT_SCORE_PNORM, in [1, 16]                           */
+  float rope_base;           /* > 0: RoPE-aware Quantized tier (see below); 0: keys as given  */
 } qevict_config;
 
 typedef struct {

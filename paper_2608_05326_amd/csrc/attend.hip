@@ -133,9 +133,11 @@ __device__ __forceinline__ void softmax_window(const f32x4 (&acc)[TB], float bia
 //   bf16 window: K chunks (tb, kb) at kh.d[tb * 4 + kb]; V chunks (kt, cb) at vh.d[kt * 8 + cb]
 //   quantized:   K codes kh.d[0 .. NC), K scale / zero (compact) kh.d[NC], kh.d[NC + 1];
 //                V codes vh.d[0 .. NC), V scale / zero per (kt, vg) at vh.d[NC + 2 (kt NG + vg)] (+1)
-template <int W>
+template <int W, bool ROPE = false>
 struct KHalf {
-  static constexpr int N = W / 4;
+  // with RoPE a quantized window also holds the scale / zero of the lane's
+  // channels in all four channel blocks
+  static constexpr int N = ROPE && W / 16 + 8 > W / 4 ? W / 16 + 8 : W / 4;
   u32x4 d[N];
 };
 template <int W>
@@ -147,11 +149,12 @@ struct VHalf {
 struct ItemInfo {
   const uint8_t* p;
   int kind, ntok, it;
+  int win;   // window index of a live-list item (RoPE positions), else -1
   bool open;
 };
 
-template <int W>
-__device__ __forceinline__ void fetch_k(const ItemInfo& in, KHalf<W>& kh, int lane, int r,
+template <int W, bool ROPE>
+__device__ __forceinline__ void fetch_k(const ItemInfo& in, KHalf<W, ROPE>& kh, int lane, int r,
                                         const Geometry& G) {
   constexpr int TB = W / 16, NC = W / 16;
   const uint8_t* p = in.p;
@@ -162,13 +165,22 @@ __device__ __forceinline__ void fetch_k(const ItemInfo& in, KHalf<W>& kh, int la
     const int nld = in.kind == KIND_Q4 ? NC : NC / 2;
     // every register of the buffer is defined on both paths (keeps it out of scratch)
 #pragma unroll
-    for (int i = 0; i < KHalf<W>::N; ++i) kh.d[i] = (u32x4){0, 0, 0, 0};
+    for (int i = 0; i < KHalf<W, ROPE>::N; ++i) kh.d[i] = (u32x4){0, 0, 0, 0};
 #pragma unroll
     for (int m = 0; m < NC; ++m)
       if (m < nld) kh.d[m] = ld16(p + (m * 64 + lane) * 16);
     const uint8_t* mk = p + meta_k_off(G);
-    kh.d[NC] = ld16(mk + 16 * r);
-    kh.d[NC + 1] = ld16(mk + 256 + 16 * r);
+    if constexpr (ROPE) {   // scale / zero of channels 32 kb + 8 q .. + 7, kb = 0 .. 3
+      const int qg = lane >> 4;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        kh.d[NC + kb] = ld16(mk + 2 * (32 * kb + 8 * qg));
+        kh.d[NC + 4 + kb] = ld16(mk + 2 * kHeadDim + 2 * (32 * kb + 8 * qg));
+      }
+    } else {
+      kh.d[NC] = ld16(mk + 16 * r);
+      kh.d[NC + 1] = ld16(mk + 256 + 16 * r);
+    }
   }
 }
 
@@ -203,8 +215,121 @@ __device__ __forceinline__ void fetch_v(const ItemInfo& in, VHalf<W>& vh, int la
 // QK^T and the online-softmax update of one window: probabilities in p_,
 // the window's (reference, sum) pair in m_w, l_w.  The open window takes this
 // step's key (and stores it into its ring slot).
+// 8 fp16 values of a 16-byte register as floats
+__device__ __forceinline__ void f16x8_to_f32(u32x4 v, float (&f)[8]) {
+  const f16x8 h = __builtin_bit_cast(f16x8, v);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) f[i] = (float)h[i];
+}
+
+// QK^T of a quantized window with RoPE (keys quantized before rotation): the
+// query is turned back to the window's first position, q' = R(-p0) q, and the
+// dequantized keys z + s c are rotated by their offset j in the window (the
+// first rows of the position table), so q' . R(j) x = q . R(p0 + j) x.  Both
+// operands are split into fp16 hi + lo (three MFMAs per block: hi.hi, hi.lo,
+// lo.hi), the error of the rotation in float32 stays near 2^-22.
 template <int W, int NHS>
-__device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W>& kh, WaveState& st,
+__device__ __forceinline__ void qk_rope_quant(const ItemInfo& in, const KHalf<W, true>& kh,
+                                              const float (&qf)[NHS][8], uint8_t* qlds,
+                                              const Geometry& G, int lane, int qg, int r,
+                                              f32x4 (&acc)[W / 16]) {
+  constexpr int TB = W / 16, NC = W / 16;
+  const bool is4 = in.kind == KIND_Q4;
+  const int gqa = G.gqa;
+  uint32_t kw[4 * NC];
+#pragma unroll
+  for (int m = 0; m < NC; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) kw[4 * m + i] = kh.d[m][i];
+  // q' = R(-p0) q: lane r holds channels 8 r .. 8 r + 7, whose partners (+-64) lane r ^ 8 holds
+  const int p0 = G.sink + in.win * W;
+  const float* c0 = G.rope + 2 * ((int64_t)p0 * (kHeadDim / 2) + 8 * (r & 7));
+  float cs0[16];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const u32x4 v = ld16(c0 + 4 * k);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) cs0[4 * k + i] = __uint_as_float(v[i]);
+  }
+  wave_sync_lds();
+#pragma unroll
+  for (int k = 0; k < NHS; ++k) {
+    const int hh = qg + 4 * k;
+    f16x8 hi8, lo8;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float x = qf[k][i], y = __shfl_xor(qf[k][i], 8, 64);
+      const float c = cs0[2 * i], sn = cs0[2 * i + 1];
+      const float v = r < 8 ? x * c + y * sn : x * c - y * sn;
+      const _Float16 h = (_Float16)v;
+      hi8[i] = h;
+      lo8[i] = (_Float16)(v - (float)h);
+    }
+    if (hh < gqa) {
+      const int dst = 16 * (r & 3) + hh;   // lane of the B operand: head hh, channel group r & 3
+      const int kb = r >> 2;
+      *(u32x4*)(qlds + ((0 * 4 + kb) * 64 + dst) * 16) = __builtin_bit_cast(u32x4, hi8);
+      *(u32x4*)(qlds + ((1 * 4 + kb) * 64 + dst) * 16) = __builtin_bit_cast(u32x4, lo8);
+    }
+  }
+  wave_sync_lds();
+  f16x8 qhi[4], qlo[4];
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    qhi[kb] = __builtin_bit_cast(f16x8, ld16(qlds + ((0 * 4 + kb) * 64 + lane) * 16));
+    qlo[kb] = __builtin_bit_cast(f16x8, ld16(qlds + ((1 * 4 + kb) * 64 + lane) * 16));
+  }
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb) {
+    acc[tb] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    const int j = 16 * tb + r;   // token offset in the window
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f16x8 ca, cb;   // codes of channels 32 kb + 8 qg + i and their partners + 64
+      int ee;
+      if (is4) {
+        ca = unpack_codes<4>(code_word<4>(kw, tb * 4 + kb, &ee), ee);
+        cb = unpack_codes<4>(code_word<4>(kw, tb * 4 + kb + 2, &ee), ee);
+      } else {
+        ca = unpack_codes<2>(code_word<2>(kw, tb * 4 + kb, &ee), ee);
+        cb = unpack_codes<2>(code_word<2>(kw, tb * 4 + kb + 2, &ee), ee);
+      }
+      float sa[8], za[8], sb[8], zb[8];
+      f16x8_to_f32(kh.d[NC + kb], sa);
+      f16x8_to_f32(kh.d[NC + 4 + kb], za);
+      f16x8_to_f32(kh.d[NC + kb + 2], sb);
+      f16x8_to_f32(kh.d[NC + 4 + kb + 2], zb);
+      const float* cj = G.rope + 2 * ((int64_t)j * (kHeadDim / 2) + 32 * kb + 8 * qg);
+      float cs[16];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const u32x4 v = ld16(cj + 4 * k);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cs[4 * k + i] = __uint_as_float(v[i]);
+      }
+      f16x8 ahi, alo, bhi, blo;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float xa = fmaf(sa[i], (float)ca[i], za[i]), xb = fmaf(sb[i], (float)cb[i], zb[i]);
+        const float c = cs[2 * i], sn = cs[2 * i + 1];
+        const float ra = xa * c - xb * sn, rb = xb * c + xa * sn;
+        ahi[i] = (_Float16)ra;
+        alo[i] = (_Float16)(ra - (float)ahi[i]);
+        bhi[i] = (_Float16)rb;
+        blo[i] = (_Float16)(rb - (float)bhi[i]);
+      }
+      acc[tb] = mfma_f16(ahi, qhi[kb], acc[tb]);
+      acc[tb] = mfma_f16(ahi, qlo[kb], acc[tb]);
+      acc[tb] = mfma_f16(alo, qhi[kb], acc[tb]);
+      acc[tb] = mfma_f16(bhi, qhi[kb + 2], acc[tb]);
+      acc[tb] = mfma_f16(bhi, qlo[kb + 2], acc[tb]);
+      acc[tb] = mfma_f16(blo, qhi[kb + 2], acc[tb]);
+    }
+  }
+}
+
+template <int W, int NHS, bool ROPE>
+__device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh, WaveState& st,
                                           const bf16x8 (&qop)[4], const float (&qf)[NHS][8],
                                           uint8_t* qlds, const AttnArgs& a, int b, int g, int lane,
                                           int qg, int r, float (&p_)[W / 16][4], float* m_w,
@@ -244,6 +369,9 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W>& kh, Wave
       for (int kb = 0; kb < 4; ++kb)
         acc[tb] = mfma_bf16(__builtin_bit_cast(bf16x8, kh.d[tb * 4 + kb]), qop[kb], acc[tb]);
     }
+    softmax_window<TB, NHS>(acc, 0.f, ntok, G.scale_log2, qg, st, p_, m_w, l_w);
+  } else if constexpr (ROPE) {
+    qk_rope_quant<W, NHS>(in, kh, qf, qlds, G, lane, qg, r, acc);
     softmax_window<TB, NHS>(acc, 0.f, ntok, G.scale_log2, qg, st, p_, m_w, l_w);
   } else {
     // ---- quantized window: int4 or int2 codes ----
@@ -427,7 +555,7 @@ __device__ __forceinline__ void process_v(const ItemInfo& in, VHalf<W>& vh, Wave
 constexpr int kAttnSmemFixed = 4 * 16 * 130 * 4;   // q*s staging per wave / end-of-split merge
 
 // MINB workgroups of four waves per compute unit: at most 512 / MINB VGPRs per lane
-template <int W, int NHS, int MINB>
+template <int W, int NHS, int MINB, bool ROPE>
 __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   const Geometry& G = a.g;
   const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
@@ -443,6 +571,7 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   const int32_t* counts = (const int32_t*)(ub + a.L.counts);
   const int32_t* icost = (const int32_t*)(ub + a.L.item_cost);
   const int32_t* iref = (const int32_t*)(ub + a.L.item_ref);
+  const int32_t* iwin_l = (const int32_t*)(ub + a.L.item_win);
   float2* mref = (float2*)(ub + a.L.mref);
 
   // ---- one round of loads: list length and cost, the first 1024 entries of the
@@ -568,7 +697,9 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
     in.kind = KIND_BF16;
     in.ntok = W;
     in.open = false;
+    in.win = -1;
     if (it < n_fq) {
+      if constexpr (ROPE) in.win = iwin_l[it];
       int32_t ref;
       if (plan_ok) {
         const int k = it - first;
@@ -595,15 +726,15 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
 
   // ---- window loop: this wave's contiguous run of windows ----
   constexpr int TB = W / 16;
-  KHalf<W> KA;
+  KHalf<W, ROPE> KA;
   VHalf<W> V;
   float p_[TB][4];
   float m_w, l_w;
   for (int it = first; it < last; ++it) {
     const ItemInfo ia = info(it);
-    fetch_k<W>(ia, KA, lane, r, G);
+    fetch_k<W, ROPE>(ia, KA, lane, r, G);
     fetch_v<W>(ia, V, lane, qg, G);
-    process_k<W, NHS>(ia, KA, st, qop, qf, qlds, a, b, g, lane, qg, r, p_, &m_w, &l_w);
+    process_k<W, NHS, ROPE>(ia, KA, st, qop, qf, qlds, a, b, g, lane, qg, r, p_, &m_w, &l_w);
     process_v<W, NHS>(ia, V, st, p_, m_w, l_w, a, b, g, qg, r, mref);
   }
 
@@ -881,14 +1012,24 @@ hipError_t launch_attend(const AttnArgs& a, hipStream_t st) {
     hipLaunchKernelGGL(kern, grid, dim3(kAttnThreads), smem, st, a);
   };
   // pipelined window loop where the extra K buffer keeps two waves per SIMD
-  if (a.g.W == 32) {
-    if (nhs == 1) go(k_attend<32, 1, 2>);
-    else if (nhs == 2) go(k_attend<32, 2, 2>);
-    else go(k_attend<32, 4, 2>);
+  if (a.g.rope) {
+    if (a.g.W == 32) {
+      if (nhs == 1) go(k_attend<32, 1, 2, true>);
+      else if (nhs == 2) go(k_attend<32, 2, 2, true>);
+      else go(k_attend<32, 4, 2, true>);
+    } else {
+      if (nhs == 1) go(k_attend<64, 1, 2, true>);
+      else if (nhs == 2) go(k_attend<64, 2, 2, true>);
+      else go(k_attend<64, 4, 2, true>);
+    }
+  } else if (a.g.W == 32) {
+    if (nhs == 1) go(k_attend<32, 1, 2, false>);
+    else if (nhs == 2) go(k_attend<32, 2, 2, false>);
+    else go(k_attend<32, 4, 2, false>);
   } else {
-    if (nhs == 1) go(k_attend<64, 1, 2>);
-    else if (nhs == 2) go(k_attend<64, 2, 2>);
-    else go(k_attend<64, 4, 2>);
+    if (nhs == 1) go(k_attend<64, 1, 2, false>);
+    else if (nhs == 2) go(k_attend<64, 2, 2, false>);
+    else go(k_attend<64, 4, 2, false>);
   }
   return hipGetLastError();
 }

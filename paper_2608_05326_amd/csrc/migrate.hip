@@ -99,6 +99,25 @@ __device__ __forceinline__ int entry_half(int area, int e) { return area == 0 ? 
 __device__ __forceinline__ int part_chunk(int area, int h, int cl) {
   return area == 0 ? (cl >> 1) * 4 + 2 * h + (cl & 1) : (cl >> 2) * 8 + 4 * h + (cl & 3);
 }
+// With RoPE a pre-RoPE key channel depends on both channel halves, so the key
+// work of a window is not split: part 0 takes both halves, part 1 none.  The
+// channel halves a part covers: [h0, h0 + nh).
+struct Halves {
+  int h0, nh;
+};
+template <bool ROPE>
+__device__ __forceinline__ Halves part_halves(int area, int h) {
+  if (ROPE && area == 0) return Halves{0, h == 0 ? 2 : 0};
+  return Halves{h, 1};
+}
+template <bool ROPE>
+__device__ __forceinline__ bool owns_entry(int area, int h, int e) {
+  return (ROPE && area == 0) ? h == 0 : entry_half(area, e) == h;
+}
+// RoPE (cos, sin) of position p, channel pair i
+__device__ __forceinline__ float2 rope_cs(const Geometry& G, int p, int i) {
+  return *(const float2*)(G.rope + 2 * ((int64_t)p * (kHeadDim / 2) + i));
+}
 
 // Codes of one (window, KV head), packed: thread (area, block m, lane L, word
 // comp) forms word 4m + comp of lane L; entry e of a word holds its 8 codes at
@@ -108,10 +127,11 @@ __device__ __forceinline__ int part_chunk(int area, int h, int cl) {
 // a migration workgroup fits on a compute unit beside two attention workgroups,
 // so routing on its own stream does not hold back the attention of the next layers
 constexpr int kMigrateThreads = 256;
-template <int W>
-constexpr int migrate_waves_per_simd() { return W == 32 ? 5 : 4; }
+// (the RoPE variants hold both key halves and their rotation: one wave fewer)
+template <int W, bool ROPE = false>
+constexpr int migrate_waves_per_simd() { return (W == 32 ? 5 : 4) - (ROPE ? 1 : 0); }
 
-template <int W, int NB>
+template <int W, int NB, bool ROPE>
 __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk, const uint16_t* sv,
                                            const QParams* pk, const QParams* pv, uint8_t* rec, int tid,
                                            int part) {
@@ -122,7 +142,7 @@ __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk
   const int area = part >> 1, h = part & 1;
   for (int tk = tid; tk < NBLK * 256; tk += kMigrateThreads) {
     const int comp = tk & 3, L = (tk >> 2) & 63, m = tk >> 8;
-    if (entry_half(area, (m * 4 + comp) * PER) != h) continue;
+    if (!owns_entry<ROPE>(area, h, (m * 4 + comp) * PER)) continue;
     const int q = L >> 4, r = L & 15;
     uint32_t wd = 0;
 #pragma unroll
@@ -152,18 +172,19 @@ __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk
 }
 
 // Load one part of one KV head of a window into LDS in natural [t][c] layout.
-template <int W>
+template <int W, bool ROPE>
 __device__ __forceinline__ void load_window(const MigrateArgs& a, uint8_t* ub, int b, int g, int w, int src_kind,
                             int src_idx, uint16_t* sk, uint16_t* sv, int part) {
   const Geometry& G = a.g;
   const int tid = threadIdx.x;
   const int area = part >> 1, h = part & 1;
+  const Halves hv = part_halves<ROPE>(area, h);
   uint16_t* dst = area == 0 ? sk : sv;
   if (src_kind == SRC_PROMPT) {
     const int64_t row0 = ((int64_t)b * G.H_kv + g) * a.src_T + G.sink + (int64_t)w * W;
     const uint16_t* src = (area == 0 ? a.src_k : a.src_v) + row0 * kHeadDim;
-    for (int i = tid; i < W * 8; i += blockDim.x) {
-      const int t = i >> 3, c = 64 * h + 8 * (i & 7);
+    for (int i = tid; i < W * 8 * hv.nh; i += blockDim.x) {
+      const int t = (i >> 3) % W, c = 64 * (hv.h0 + i / (W * 8)) + 8 * (i & 7);
       *(u32x4*)(dst + t * kLdsRow + c) = *(const u32x4*)(src + t * kHeadDim + c);
     }
   } else {
@@ -172,8 +193,9 @@ __device__ __forceinline__ void load_window(const MigrateArgs& a, uint8_t* ub, i
                        (area == 0 ? 0 : (int64_t)W * kHeadDim * 2);
     // K chunk (tb, kb), lane 16q + r: token 16 tb + r, channels 32 kb + 8 q .. + 7
     // V chunk (kt, cb), lane 16q + r: tokens tok(kt, q, 0..7), channel 16 cb + r
-    for (int i = tid; i < (W / 8) * 64; i += blockDim.x) {
-      const int chunk = part_chunk(area, h, i >> 6), L = i & 63, q = L >> 4, r = L & 15;
+    for (int i = tid; i < (W / 8) * 64 * hv.nh; i += blockDim.x) {
+      const int ih = i / ((W / 8) * 64), il = i % ((W / 8) * 64);
+      const int chunk = part_chunk(area, hv.h0 + ih, il >> 6), L = il & 63, q = L >> 4, r = L & 15;
       const u32x4 x = *(const u32x4*)(p + ((int64_t)chunk * 64 + L) * 16);
       if (area == 0) {
         *(u32x4*)(sk + (16 * (chunk >> 2) + r) * kLdsRow + 32 * (chunk & 3) + 8 * q) = x;
@@ -204,6 +226,34 @@ __device__ __forceinline__ WorkEntry load_entry(const int32_t* list, int e) {
   return x;
 }
 
+// Pre-RoPE keys of a window held in LDS ([t][c] bf16, both halves, absolute
+// position of token t = p0 + t): channel i < 64 becomes x_i cos + x_{i+64} sin,
+// channel i + 64 becomes x_{i+64} cos - x_i sin, each product and sum rounded to
+// float32 (no fused multiply-add), then RNE to bf16.  All values are read
+// before any is written.
+template <int W>
+__device__ __forceinline__ void unrotate_keys(const Geometry& G, uint16_t* sk, int p0, int tid) {
+#pragma clang fp contract(off)
+  constexpr int PER = W * 64 / kMigrateThreads;   // channel pairs per thread
+  uint16_t lo[PER], hi[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e = tid + k * kMigrateThreads, t = e / 64, i = e % 64;
+    const float a = bf16_to_f32(sk[t * kLdsRow + i]), bb = bf16_to_f32(sk[t * kLdsRow + 64 + i]);
+    const float2 cs = rope_cs(G, p0 + t, i);
+    const float ac = a * cs.x, bs = bb * cs.y, bc = bb * cs.x, as = a * cs.y;
+    lo[k] = f32_to_bf16_rne(ac + bs);
+    hi[k] = f32_to_bf16_rne(bc - as);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e = tid + k * kMigrateThreads, t = e / 64, i = e % 64;
+    sk[t * kLdsRow + i] = lo[k];
+    sk[t * kLdsRow + 64 + i] = hi[k];
+  }
+}
+
 template <int W>
 struct QuantLds {
   uint16_t sk[W * kLdsRow];
@@ -212,7 +262,7 @@ struct QuantLds {
   QParams pv[W * (kHeadDim / W)];
 };
 
-template <int W>
+template <int W, bool ROPE>
 __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub, int b, int g,
                                               const WorkEntry& ent, QuantLds<W>& sm, int32_t* counts,
                                               int part) {
@@ -224,15 +274,20 @@ __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub,
   const int w = ent.v[0], src_kind = ent.v[1], src_idx = ent.v[2], dst = ent.v[3], nb = ent.v[4];
   uint16_t* sk = sm.sk;
   uint16_t* sv = sm.sv;
-  load_window<W>(a, ub, b, g, w, src_kind, src_idx, sk, sv, part);
+  load_window<W, ROPE>(a, ub, b, g, w, src_kind, src_idx, sk, sv, part);
   __syncthreads();
+  const Halves hv = part_halves<ROPE>(area, h);
+  if (ROPE && area == 0 && hv.nh == 2) {
+    unrotate_keys<W>(G, sk, G.sink + w * W, tid);
+    __syncthreads();
+  }
   uint8_t* rec = ub + a.L.qpool + (int64_t)dst * G.qslot_bytes + g * G.qrec_bytes;
-  // ---- group parameters: one thread per group of this part (64 groups) ----
-  if (tid < 64) {
+  // ---- group parameters: one thread per group of this part (64 per half) ----
+  if (tid < 64 * hv.nh) {
     float x[W];
     int c = 0, t = 0, vg = 0;
     if (area == 0) {
-      c = 64 * h + tid;
+      c = 64 * hv.h0 + tid;
 #pragma unroll
       for (int tt = 0; tt < W; ++tt) x[tt] = bf16_to_f32(sk[tt * kLdsRow + c]);
     } else {
@@ -269,8 +324,8 @@ __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub,
   }
   __syncthreads();
   // ---- codes, packed ----
-  if (nb == 4) pack_codes<W, 4>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
-  else pack_codes<W, 2>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
+  if (nb == 4) pack_codes<W, 4, ROPE>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
+  else pack_codes<W, 2, ROPE>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
 }
 
 // 8 bf16 values z_j + s_j c_j (exact in float64, one rounding) packed for a 16-byte store
@@ -295,20 +350,75 @@ __device__ __forceinline__ u32x4 dequant8(uint32_t wd, int ee, u32x4 s8, u32x4 z
   return (u32x4){outw[0], outw[1], outw[2], outw[3]};
 }
 
+// z + s c (exact in float64) of key entry e (channels 32 (e & 3) + 8 q .. + 7 of
+// token 16 (e >> 2) + r) for lane L = 16 q + r
+template <int NB>
+__device__ __forceinline__ void key_entry_f64(const Geometry& G, const uint8_t* rec, int e, int L,
+                                              double (&x)[8]) {
+  constexpr int PER = 4 / NB;
+  constexpr uint32_t mask = (1u << NB) - 1u;
+  const int q = L >> 4, word = e / PER, ee = e % PER;
+  const uint32_t wd = *(const uint32_t*)(rec + ((int64_t)(word >> 2) * 64 + L) * 16 + (word & 3) * 4);
+  const uint8_t* ps = rec + meta_k_off(G) + 2 * (32 * (e & 3) + 8 * q);
+  const u32x4 s8 = *(const u32x4*)ps, z8 = *(const u32x4*)(ps + 2 * kHeadDim);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int o = 0; o < 2; ++o) {
+      const uint32_t code = (wd >> (o * 16 + NB * (4 * ee + i))) & mask;
+      const double sj = fp16_bits_to_f64((uint16_t)(s8[i] >> (16 * o)));
+      const double zj = fp16_bits_to_f64((uint16_t)(z8[i] >> (16 * o)));
+      x[2 * i + o] = zj + sj * (double)code;
+    }
+}
+
+// Promoted bf16 keys of entry e with RoPE: the dequantized pre-RoPE keys of the
+// entry and of its partner entry e ^ 2 (channels +- 64) rotated to position
+// p0 + token: channel i < 64 takes x_i cos - x_{i+64} sin, channel i + 64 takes
+// x_{i+64} cos + x_i sin, products and sums rounded in float64, then RNE to bf16.
+template <int NB>
+__device__ __forceinline__ u32x4 rope_key8(const Geometry& G, const uint8_t* rec, int e, int L, int p0) {
+#pragma clang fp contract(off)
+  double x[8], y[8];
+  key_entry_f64<NB>(G, rec, e, L, x);
+  key_entry_f64<NB>(G, rec, e ^ 2, L, y);
+  const int kb = e & 3, q = L >> 4, r = L & 15;
+  const int p = p0 + 16 * (e >> 2) + r;
+  uint32_t outw[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t pair = 0;
+#pragma unroll
+    for (int o = 0; o < 2; ++o) {
+      const int j = 2 * i + o;
+      const float2 cs = rope_cs(G, p, (32 * kb + 8 * q + j) & 63);
+      const double t1 = x[j] * (double)cs.x, t2 = y[j] * (double)cs.y;
+      const double v = kb < 2 ? t1 - t2 : t1 + t2;
+      pair |= (uint32_t)f64_to_bf16_rne(v) << (16 * o);
+    }
+    outw[i] = pair;
+  }
+  return (u32x4){outw[0], outw[1], outw[2], outw[3]};
+}
+
 // Promotion of one (window, KV head) from its quantized record: thread (area,
 // entry e, lane L) loads the 32-bit code word holding entry e of lane L and the
 // entry's 8 scales and zeros, and writes its 8 bf16 values to the same
 // (entry, lane) position of the bf16 slot.
-template <int W, int NB>
+template <int W, int NB, bool ROPE>
 __device__ __forceinline__ void promote_from_record(const Geometry& G, const uint8_t* rec,
-                                                    uint8_t* dp, int tid, int part) {
+                                                    uint8_t* dp, int tid, int part, int p0) {
   constexpr int E = W / 4;                          // entries per area
   constexpr int PER = 4 / NB;
   const int ng = kHeadDim / G.G;
   const int area = part >> 1, h = part & 1;
   for (int tk = tid; tk < E * 64; tk += kMigrateThreads) {
     const int L = tk & 63, ei = tk >> 6;
-    if (entry_half(area, ei) != h) continue;
+    if (!owns_entry<ROPE>(area, h, ei)) continue;
+    if (ROPE && area == 0) {
+      *(u32x4*)(dp + ((int64_t)ei * 64 + L) * 16) = rope_key8<NB>(G, rec, ei, L, p0);
+      continue;
+    }
     const int q = L >> 4, r = L & 15;
     const int word = ei / PER;
     const uint32_t wd = *(const uint32_t*)(rec + area * G.qcodes_bytes +
@@ -330,7 +440,7 @@ __device__ __forceinline__ void promote_from_record(const Geometry& G, const uin
   }
 }
 
-template <int W>
+template <int W, bool ROPE>
 __device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, int b, int g,
                                              const WorkEntry& ent, int part) {
   const Geometry& G = a.g;
@@ -339,18 +449,20 @@ __device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, 
   const int w = ent.v[0], src_kind = ent.v[1], src_idx = ent.v[2], dst = ent.v[3], nb = ent.v[4];
   uint8_t* dp = ub + a.L.fpool + (int64_t)dst * G.fslot_bytes + g * G.fhead_bytes;
   const int64_t area_off = area == 0 ? 0 : (int64_t)W * kHeadDim * 2;
+  const Halves hv = part_halves<ROPE>(area, h);
   if (src_kind == SRC_RING) {
     const uint8_t* sp = ub + a.L.ring + (int64_t)src_idx * G.fslot_bytes + g * G.fhead_bytes;
-    for (int i = tid; i < (W / 8) * 64; i += blockDim.x) {
-      const int64_t off = area_off + ((int64_t)part_chunk(area, h, i >> 6) * 64 + (i & 63)) * 16;
+    for (int i = tid; i < (W / 8) * 64 * hv.nh; i += blockDim.x) {
+      const int ih = i / ((W / 8) * 64), il = i % ((W / 8) * 64);
+      const int64_t off = area_off + ((int64_t)part_chunk(area, hv.h0 + ih, il >> 6) * 64 + (il & 63)) * 16;
       *(u32x4*)(dp + off) = *(const u32x4*)(sp + off);
     }
   } else if (src_kind == SRC_PROMPT) {
     const int64_t row0 = ((int64_t)b * G.H_kv + g) * a.src_T + G.sink + (int64_t)w * W;
     if (area == 0) {
       const uint16_t* ks = a.src_k + row0 * kHeadDim;
-      for (int i = tid; i < W * 8; i += blockDim.x) {
-        const int t = i >> 3, c = 64 * h + 8 * (i & 7);
+      for (int i = tid; i < W * 8 * hv.nh; i += blockDim.x) {
+        const int t = (i >> 3) % W, c = 64 * (hv.h0 + i / (W * 8)) + 8 * (i & 7);
         *(u32x4*)(dp + k_elem_off(t, c)) = *(const u32x4*)(ks + t * kHeadDim + c);
       }
     } else {
@@ -362,8 +474,9 @@ __device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, 
     }
   } else {   // SRC_QSLOT
     const uint8_t* rec = ub + a.L.qpool + (int64_t)src_idx * G.qslot_bytes + g * G.qrec_bytes;
-    if (nb == 4) promote_from_record<W, 4>(G, rec, dp, tid, part);
-    else promote_from_record<W, 2>(G, rec, dp, tid, part);
+    const int p0 = G.sink + w * W;   // position of the window's first token
+    if (nb == 4) promote_from_record<W, 4, ROPE>(G, rec, dp, tid, part, p0);
+    else promote_from_record<W, 2, ROPE>(G, rec, dp, tid, part, p0);
   }
 }
 
@@ -375,8 +488,8 @@ __device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, 
 // (dep >= 0) runs in that quantization's workgroup right after it, part by part,
 // so the slot is read before it is overwritten without any ordering across
 // workgroups.
-template <int W>
-__global__ __launch_bounds__(kMigrateThreads, migrate_waves_per_simd<W>()) void k_migrate(MigrateArgs a) {
+template <int W, bool ROPE>
+__global__ __launch_bounds__(kMigrateThreads, (migrate_waves_per_simd<W, ROPE>())) void k_migrate(MigrateArgs a) {
   const Geometry& G = a.g;
   const int b = blockIdx.y;
   __shared__ __attribute__((aligned(16))) QuantLds<W> sm;
@@ -396,14 +509,14 @@ __global__ __launch_bounds__(kMigrateThreads, migrate_waves_per_simd<W>()) void 
     const int e = task / per_entry, g = (task / kParts) % G.H_kv, part = task % kParts;
     const WorkEntry ent = task == x0 ? first : load_entry(list, e);
     if (quant) {
-      quantize_task<W>(a, ub, b, g, ent, sm, counts, part);
+      quantize_task<W, ROPE>(a, ub, b, g, ent, sm, counts, part);
       const int dep = ent.v[5];
       if (dep >= 0) {
         __syncthreads();
-        promote_task<W>(a, ub, b, g, load_entry(plist, dep), part);
+        promote_task<W, ROPE>(a, ub, b, g, load_entry(plist, dep), part);
       }
     } else if (ent.v[5] < 0) {
-      promote_task<W>(a, ub, b, g, ent, part);
+      promote_task<W, ROPE>(a, ub, b, g, ent, part);
     }
     if (task + half < n_tasks) __syncthreads();   // LDS reused by the next task
   }
@@ -443,8 +556,13 @@ static int migrate_half(const Geometry& g, int entries) {
 hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, hipStream_t st) {
   const int mx = max_quant > max_promote ? max_quant : max_promote;
   const dim3 grid(2 * migrate_half(a.g, mx), a.g.B);
-  if (a.g.W == 32) hipLaunchKernelGGL(k_migrate<32>, grid, dim3(kMigrateThreads), 0, st, a);
-  else hipLaunchKernelGGL(k_migrate<64>, grid, dim3(kMigrateThreads), 0, st, a);
+  if (a.g.rope) {
+    if (a.g.W == 32) hipLaunchKernelGGL((k_migrate<32, true>), grid, dim3(kMigrateThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_migrate<64, true>), grid, dim3(kMigrateThreads), 0, st, a);
+  } else {
+    if (a.g.W == 32) hipLaunchKernelGGL((k_migrate<32, false>), grid, dim3(kMigrateThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_migrate<64, false>), grid, dim3(kMigrateThreads), 0, st, a);
+  }
   return hipGetLastError();
 }
 hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st) {

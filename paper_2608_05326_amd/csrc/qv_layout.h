@@ -92,6 +92,7 @@ struct Geometry {
   int32_t out_bf16;
   uint32_t flags;
   int32_t score_mode;   // window ranking function (cumulative, decayed, key norm, p-norm)
+  const float* rope;    // RoPE table [max_context][64] (cos, sin) pairs; null without RoPE
   float scale_log2;     // softmax scale * log2(e)
   int64_t fhead_bytes;  // one KV head of a bf16 slot: W*d*2 (K) + W*d*2 (V)
   int64_t fslot_bytes;  // H_kv * fhead_bytes

@@ -146,6 +146,8 @@ qevict_status check_config(const qevict_config* c) {
   if (c->score_mode != QEVICT_SCORE_CUMULATIVE && c->score_mode != QEVICT_SCORE_DECAY &&
       c->score_mode != QEVICT_SCORE_KEY_NORM && c->score_mode != QEVICT_SCORE_PNORM)
     return fail(QEVICT_ERR_INVALID_ARG, "score_mode");
+  if (!(c->rope_base >= 0.f) || !std::isfinite(c->rope_base))
+    return fail(QEVICT_ERR_INVALID_ARG, "rope_base must be finite and >= 0");
   if (c->score_mode == QEVICT_SCORE_PNORM && !(c->score_p >= 1.f && c->score_p <= 16.f))
     return fail(QEVICT_ERR_INVALID_ARG, "score_p must be in [1, 16]");
   if (c->score_mode == QEVICT_SCORE_DECAY && !(c->score_decay > 0.f && c->score_decay <= 1.f))
@@ -269,6 +271,26 @@ qevict_status hip_fail(hipError_t e, const char* what) {
 int64_t score_staging_bytes(const qevict_config* cfg, const Geometry& g) {
   const bool used = cfg->score_mode == QEVICT_SCORE_KEY_NORM || cfg->score_mode == QEVICT_SCORE_PNORM;
   return used ? align256(4LL * g.B * g.nwc) : 0;
+}
+
+// RoPE table after the staging area: (cos, sin) of p * base^(-2i/d), float32,
+// [max_context][d / 2]
+int64_t rope_table_bytes(const qevict_config* cfg) {
+  return cfg->rope_base > 0.f ? align256(8LL * cfg->max_context * (cfg->head_dim / 2)) : 0;
+}
+
+std::vector<float> rope_table(const qevict_config* cfg) {
+  const int half = cfg->head_dim / 2;
+  std::vector<double> inv(half);
+  for (int i = 0; i < half; ++i) inv[i] = std::pow((double)cfg->rope_base, -2.0 * i / cfg->head_dim);
+  std::vector<float> t(2LL * cfg->max_context * half);
+  for (int64_t p = 0; p < cfg->max_context; ++p)
+    for (int i = 0; i < half; ++i) {
+      const double ang = (double)p * inv[i];
+      t[2 * (p * half + i)] = (float)std::cos(ang);
+      t[2 * (p * half + i) + 1] = (float)std::sin(ang);
+    }
+  return t;
 }
 
 uint8_t* unit_base(qevict_cache* c, int layer, int seq) {
@@ -491,7 +513,7 @@ qevict_status qevict_workspace_size(const qevict_config* cfg, size_t* bytes) {
   UnitLayout L;
   plan(cfg, &g, &L);
   *bytes = (size_t)(kHeaderBytes + (int64_t)cfg->num_layers * cfg->batch * L.unit_bytes +
-                    score_staging_bytes(cfg, g));
+                    score_staging_bytes(cfg, g) + rope_table_bytes(cfg));
   return QEVICT_OK;
 }
 
@@ -534,6 +556,14 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
       qevict_cache_destroy(c);
       return hip_fail(e, "creating the routing stream");
     }
+  }
+  if (e == hipSuccess && cfg->rope_base > 0.f) {
+    float* tab = (float*)(c->ws + kHeaderBytes + (int64_t)cfg->num_layers * cfg->batch * c->L.unit_bytes +
+                          score_staging_bytes(cfg, c->g));
+    const std::vector<float> host = rope_table(cfg);
+    e = hipMemcpyAsync(tab, host.data(), host.size() * sizeof(float), hipMemcpyHostToDevice, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);   // the host table goes out of scope
+    c->g.rope = tab;
   }
   if (e == hipSuccess) e = launch_init_units(c->g, c->L, c->ws + kHeaderBytes, cfg->num_layers * cfg->batch,
                                    c->stream);

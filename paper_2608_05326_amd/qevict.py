@@ -16,7 +16,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libqevict.so")
 
-ABI_VERSION = 3
+ABI_VERSION = 4
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_BAD_STATE, ERR_NONFINITE, \
     ERR_CAPACITY, ERR_DEVICE = 0, -1, -2, -3, -4, -5, -6, -7
 TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED = 0, 1, 2, 3, 4
@@ -50,7 +50,8 @@ class _Config(ctypes.Structure):
         "window_tokens", "group_size", "quant_bits", "sink_tokens", "recent_tokens", "max_context",
         "capacity_full", "capacity_quant", "retier_interval", "out_dtype")] + [
         ("flags", ctypes.c_uint32), ("softmax_scale", ctypes.c_float), ("num_splits", ctypes.c_int32),
-        ("score_mode", ctypes.c_int32), ("score_decay", ctypes.c_float), ("score_p", ctypes.c_float)]
+        ("score_mode", ctypes.c_int32), ("score_decay", ctypes.c_float), ("score_p", ctypes.c_float),
+        ("rope_base", ctypes.c_float)]
 
 
 class MemoryReport(ctypes.Structure):
@@ -93,6 +94,7 @@ class Config:
     score_mode: int = SCORE_CUMULATIVE
     score_decay: float = 0.0
     score_p: float = 0.0
+    rope_base: float = 0.0
 
     def to_c(self) -> _Config:
         c = _Config()

@@ -48,7 +48,7 @@ def budget_capacities(wl: syn.Workload):
 def gpu_config(wl: syn.Workload, layers: int, flags: int = 0, out_dtype: int = qv.OUT_F32,
                num_splits: int = 0, capacity_full=None, capacity_quant=None,
                score_decay: float | None = None, key_norm: bool = False,
-               score_p: float | None = None) -> qv.Config:
+               score_p: float | None = None, rope_base: float = 0.0) -> qv.Config:
     mode = qv.SCORE_KEY_NORM if key_norm else qv.SCORE_PNORM if score_p is not None else \
         qv.SCORE_DECAY if score_decay is not None else qv.SCORE_CUMULATIVE
     if wl.budget_frac:
@@ -62,7 +62,7 @@ def gpu_config(wl: syn.Workload, layers: int, flags: int = 0, out_dtype: int = q
         capacity_quant=wl.capacity_quant if capacity_quant is None else capacity_quant,
         sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=wl.retier_interval,
         out_dtype=out_dtype, flags=flags, num_splits=num_splits,
-        score_mode=mode, score_decay=score_decay or 0.0, score_p=score_p or 0.0)
+        score_mode=mode, score_decay=score_decay or 0.0, score_p=score_p or 0.0, rope_base=rope_base)
 
 
 def oracle_config(cfg: qv.Config) -> OracleConfig:
@@ -74,7 +74,8 @@ def oracle_config(cfg: qv.Config) -> OracleConfig:
                         if cfg.score_mode == qv.SCORE_DECAY else 1.0,
                         key_norm=cfg.score_mode == qv.SCORE_KEY_NORM,
                         score_p=float(np.float32(cfg.score_p))
-                        if cfg.score_mode == qv.SCORE_PNORM else 0.0)
+                        if cfg.score_mode == qv.SCORE_PNORM else 0.0,
+                        rope_base=float(np.float32(cfg.rope_base)))
 
 
 class Lockstep:
@@ -87,7 +88,8 @@ class Lockstep:
     def __init__(self, wl: syn.Workload, seed: int = 0, layer_ids=(0,), check_seqs=None,
                  flags: int = 0, num_splits: int = 0, steps: int | None = None, log=print,
                  capacity_full=None, capacity_quant=None, score_decay: float | None = None,
-                 key_norm: bool = False, score_p: float | None = None, observed_init: bool = False):
+                 key_norm: bool = False, score_p: float | None = None, observed_init: bool = False,
+                 rope_base: float = 0.0):
         self.wl, self.seed = wl, seed
         self.layer_ids = list(layer_ids)
         self.check_seqs = list(range(wl.batch)) if check_seqs is None else list(check_seqs)
@@ -95,7 +97,7 @@ class Lockstep:
         self.cfg = gpu_config(wl, len(self.layer_ids), flags | qv.FLAG_DEBUG_MASSES,
                               num_splits=num_splits, capacity_full=capacity_full,
                               capacity_quant=capacity_quant, score_decay=score_decay,
-                              key_norm=key_norm, score_p=score_p)
+                              key_norm=key_norm, score_p=score_p, rope_base=rope_base)
         self.key_norm = key_norm
         # modes whose prompt scores the GPU computes itself (key norms, u_0^p)
         self.gpu_prompt_scores = key_norm or score_p is not None

@@ -52,6 +52,8 @@ def test_workspace_size_of_the_8b_32k_layer():
     (dict(max_context=0), qv.qevict.ERR_INVALID_ARG),
     (dict(sink_tokens=65 * 32), qv.qevict.ERR_UNSUPPORTED),
     (dict(score_mode=4), qv.qevict.ERR_INVALID_ARG),
+    (dict(rope_base=-1.0), qv.qevict.ERR_INVALID_ARG),
+    (dict(rope_base=float("inf")), qv.qevict.ERR_INVALID_ARG),
     (dict(score_mode=qv.SCORE_PNORM, score_p=0.5), qv.qevict.ERR_INVALID_ARG),
     (dict(score_mode=qv.SCORE_PNORM, score_p=17.0), qv.qevict.ERR_INVALID_ARG),
     (dict(score_mode=qv.SCORE_DECAY, score_decay=0.0), qv.qevict.ERR_INVALID_ARG),
@@ -69,6 +71,9 @@ def test_ranking_modes_are_accepted():
     # key-norm mode stages the prompt windows' scores ([B][n_w] fp32) after the units
     kn = qv.workspace_size(_cfg(score_mode=qv.SCORE_KEY_NORM))
     assert base + 4 * 1028 <= kn <= base + 4 * 1028 + 256
+    # RoPE: a float32 (cos, sin) table of max_context x 64 pairs after the units
+    rp = qv.workspace_size(_cfg(rope_base=10000.0))
+    assert rp == base + 8 * (32768 + 128) * 64
     # p-norm mode: the same staging plus {completed-period sum, running u} per window and unit
     pn = qv.workspace_size(_cfg(score_mode=qv.SCORE_PNORM, score_p=3.0))
     n_units = 1 * 1

@@ -80,3 +80,14 @@ def test_tier_extremes(kf, kq):
     policy) and more capacity than windows (nothing is evicted)."""
     ls = _lockstep("c2s", capacity_full=kf, capacity_quant=kq, steps=16)
     assert ls.events == 16
+
+
+@pytest.mark.parametrize("name,base", [("c2s", 10000.0), ("c4s", 500000.0), ("c5s", 500000.0),
+                                       ("c7s", 10000.0)])
+def test_rope_lockstep(name, base):
+    """RoPE-aware Quantized tier: codes of the un-rotated keys (bit-exact),
+    attention over dequantized keys rotated back to their positions, promotions
+    rotated in float64 (bit-exact), on int4 W 32, int2 W 64, mixed bits with
+    8-step periods, and sink / recent regions."""
+    ls = _lockstep(name, rope_base=base)
+    assert ls.events > 0
