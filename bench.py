@@ -58,6 +58,8 @@ def parse():
                         "the attention of the other layers; sync: everything on one stream")
     p.add_argument("--no-kernel-events", action="store_true",
                    help="do not time each kernel launch with HIP events (no roofline)")
+    p.add_argument("--rope-base", type=float, default=0.0,
+                   help="RoPE-aware Quantized tier with this base (0: off, the default workload)")
     p.add_argument("--prefill-scores", action="store_true",
                    help="time the initial-window-score kernels on the workload's prompt instead")
     p.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MB",
@@ -268,7 +270,8 @@ def main():
                     quant_bits=wl.bits, max_context=wl.prompt_len + per_layer,
                     capacity_full=wl.capacity_full, capacity_quant=wl.capacity_quant,
                     sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=1,
-                    num_splits=args.splits, flags=qv.FLAG_ASYNC_ROUTING if asyncr else 0)
+                    num_splits=args.splits, flags=qv.FLAG_ASYNC_ROUTING if asyncr else 0,
+                    rope_base=args.rope_base)
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)
     cache = qv.Cache(cfg, stream=stream)
@@ -427,7 +430,7 @@ def main():
                                "heads, head_dim 128, windows of 32, 20% bf16 / 30% int4 group 32 / 50% "
                                "evicted, re-tier every step, drifting queries",
                    "layer_caches_rotated": NL, "global_batch": wl.batch, "seq_len": wl.prompt_len,
-                   "routing": args.routing, "parallelism": "single GPU"},
+                   "routing": args.routing, "rope_base": args.rope_base, "parallelism": "single GPU"},
         "step_GBps": round(bytes_per_step / (ms_per_step * 1e-3) / 1e9, 1),
         "algorithmic_MB_per_step": round(bytes_per_step / 1e6, 3),
         "host_wall_us_per_step": round(wall / args.steps * 1e6, 2),

@@ -135,9 +135,7 @@ __device__ __forceinline__ void softmax_window(const f32x4 (&acc)[TB], float bia
 //                V codes vh.d[0 .. NC), V scale / zero per (kt, vg) at vh.d[NC + 2 (kt NG + vg)] (+1)
 template <int W, bool ROPE = false>
 struct KHalf {
-  // with RoPE a quantized window also holds the scale / zero of the lane's
-  // channels in all four channel blocks
-  static constexpr int N = ROPE && W / 16 + 8 > W / 4 ? W / 16 + 8 : W / 4;
+  static constexpr int N = W / 4;
   u32x4 d[N];
 };
 template <int W>
@@ -170,16 +168,13 @@ __device__ __forceinline__ void fetch_k(const ItemInfo& in, KHalf<W, ROPE>& kh, 
     for (int m = 0; m < NC; ++m)
       if (m < nld) kh.d[m] = ld16(p + (m * 64 + lane) * 16);
     const uint8_t* mk = p + meta_k_off(G);
-    if constexpr (ROPE) {   // scale / zero of channels 32 kb + 8 q .. + 7, kb = 0 .. 3
-      const int qg = lane >> 4;
+    kh.d[NC] = ld16(mk + 16 * r);
+    kh.d[NC + 1] = ld16(mk + 256 + 16 * r);
+    if constexpr (ROPE) {   // (cos, sin) of the window's first position, pairs 8 (r & 7) .. + 7
+      static_assert(KHalf<W, ROPE>::N >= W / 16 + 6, "spare registers for the rotation");
+      const float* c0 = G.rope + 2 * ((int64_t)(G.sink + in.win * W) * (kHeadDim / 2) + 8 * (r & 7));
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        kh.d[NC + kb] = ld16(mk + 2 * (32 * kb + 8 * qg));
-        kh.d[NC + 4 + kb] = ld16(mk + 2 * kHeadDim + 2 * (32 * kb + 8 * qg));
-      }
-    } else {
-      kh.d[NC] = ld16(mk + 16 * r);
-      kh.d[NC + 1] = ld16(mk + 256 + 16 * r);
+      for (int k = 0; k < 4; ++k) kh.d[NC + 2 + k] = ld16(c0 + 4 * k);
     }
   }
 }
@@ -215,11 +210,12 @@ __device__ __forceinline__ void fetch_v(const ItemInfo& in, VHalf<W>& vh, int la
 // QK^T and the online-softmax update of one window: probabilities in p_,
 // the window's (reference, sum) pair in m_w, l_w.  The open window takes this
 // step's key (and stores it into its ring slot).
-// 8 fp16 values of a 16-byte register as floats
-__device__ __forceinline__ void f16x8_to_f32(u32x4 v, float (&f)[8]) {
-  const f16x8 h = __builtin_bit_cast(f16x8, v);
+// a 16-byte register of lane src
+__device__ __forceinline__ u32x4 shfl16(u32x4 v, int src) {
+  u32x4 o;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) f[i] = (float)h[i];
+  for (int i = 0; i < 4; ++i) o[i] = (uint32_t)__shfl((int)v[i], src, 64);
+  return o;
 }
 
 // QK^T of a quantized window with RoPE (keys quantized before rotation): the
@@ -241,16 +237,13 @@ __device__ __forceinline__ void qk_rope_quant(const ItemInfo& in, const KHalf<W,
   for (int m = 0; m < NC; ++m)
 #pragma unroll
     for (int i = 0; i < 4; ++i) kw[4 * m + i] = kh.d[m][i];
-  // q' = R(-p0) q: lane r holds channels 8 r .. 8 r + 7, whose partners (+-64) lane r ^ 8 holds
-  const int p0 = G.sink + in.win * W;
-  const float* c0 = G.rope + 2 * ((int64_t)p0 * (kHeadDim / 2) + 8 * (r & 7));
+  // q' = R(-p0) q: lane r holds channels 8 r .. 8 r + 7, whose partners (+-64) lane r ^ 8
+  // holds; (cos, sin) of p0 for them were loaded with the window
   float cs0[16];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const u32x4 v = ld16(c0 + 4 * k);
+  for (int k = 0; k < 4; ++k)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) cs0[4 * k + i] = __uint_as_float(v[i]);
-  }
+    for (int i = 0; i < 4; ++i) cs0[4 * k + i] = __uint_as_float(kh.d[NC + 2 + k][i]);
   wave_sync_lds();
 #pragma unroll
   for (int k = 0; k < NHS; ++k) {
@@ -294,11 +287,13 @@ __device__ __forceinline__ void qk_rope_quant(const ItemInfo& in, const KHalf<W,
         ca = unpack_codes<2>(code_word<2>(kw, tb * 4 + kb, &ee), ee);
         cb = unpack_codes<2>(code_word<2>(kw, tb * 4 + kb + 2, &ee), ee);
       }
-      float sa[8], za[8], sb[8], zb[8];
-      f16x8_to_f32(kh.d[NC + kb], sa);
-      f16x8_to_f32(kh.d[NC + 4 + kb], za);
-      f16x8_to_f32(kh.d[NC + kb + 2], sb);
-      f16x8_to_f32(kh.d[NC + 4 + kb + 2], zb);
+      // scale / zero of channels 32 kb + 8 qg + i (and + 64): lane 4 kb + qg of
+      // this lane's row holds channels 8 (4 kb + qg) .. + 7 in its compact registers
+      const int src_a = 16 * qg + 4 * kb + qg, src_b = src_a + 8;
+      const f16x8 sa = __builtin_bit_cast(f16x8, shfl16(kh.d[NC], src_a));
+      const f16x8 za = __builtin_bit_cast(f16x8, shfl16(kh.d[NC + 1], src_a));
+      const f16x8 sb = __builtin_bit_cast(f16x8, shfl16(kh.d[NC], src_b));
+      const f16x8 zb = __builtin_bit_cast(f16x8, shfl16(kh.d[NC + 1], src_b));
       const float* cj = G.rope + 2 * ((int64_t)j * (kHeadDim / 2) + 32 * kb + 8 * qg);
       float cs[16];
 #pragma unroll
@@ -310,7 +305,8 @@ __device__ __forceinline__ void qk_rope_quant(const ItemInfo& in, const KHalf<W,
       f16x8 ahi, alo, bhi, blo;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float xa = fmaf(sa[i], (float)ca[i], za[i]), xb = fmaf(sb[i], (float)cb[i], zb[i]);
+        const float xa = fmaf((float)sa[i], (float)ca[i], (float)za[i]);
+        const float xb = fmaf((float)sb[i], (float)cb[i], (float)zb[i]);
         const float c = cs[2 * i], sn = cs[2 * i + 1];
         const float ra = xa * c - xb * sn, rb = xb * c + xa * sn;
         ahi[i] = (_Float16)ra;

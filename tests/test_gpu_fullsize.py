@@ -67,3 +67,8 @@ def test_max_candidates_4000_windows():
         ls.close()
     print(f"[fullsize] cmax: max out err {ls.max_out_err:.2e}, max score err {ls.max_score_err:.2e}",
           flush=True)
+
+
+def test_8b_32k_rope():
+    # the benchmark shape with the RoPE-aware Quantized tier (Llama-3 base 500000)
+    _lockstep("c2", steps=4, rope_base=500000.0)
