@@ -98,3 +98,23 @@ def test_prefill_scores_scratch_size():
         with pytest.raises(qv.QEvictError) as e:
             qv.qevict.prefill_scores_scratch_size(cfg, T, n_obs)
         assert e.value.status == qv.qevict.ERR_INVALID_ARG
+
+
+def test_c_program_uses_the_abi(tmp_path):
+    """tests/c/abi_host.c: the header compiles as C99 and the host-only calls
+    work from C, linked against the built library."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    here = os.path.dirname(os.path.abspath(__file__))
+    root = os.path.dirname(here)
+    lib_dir = os.path.join(root, "paper_2608_05326_amd")
+    exe = str(tmp_path / "abi_host")
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Werror", "-I", os.path.join(root, "include"),
+                    os.path.join(here, "c", "abi_host.c"), "-L", lib_dir, "-lqevict",
+                    "-Wl,-rpath," + lib_dir, "-o", exe], check=True)
+    r = subprocess.run([exe], capture_output=True, text=True)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "FAIL" not in r.stdout
