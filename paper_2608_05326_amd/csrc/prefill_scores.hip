@@ -89,7 +89,6 @@ __global__ __launch_bounds__(256, 4) void k_obs_chunks(ObsArgs a) {
     for (int rt = 0; rt < (nr + 15) / 16; ++rt) {
       const int row = rt * 16 + lr;   // this lane's query row inside the staged rows
       const int rg = r0 + row;
-      const int pos = pos0 + (rg % a.n_obs);
       f32x4 acc[4];
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) acc[kt] = (f32x4){0.f, 0.f, 0.f, 0.f};
@@ -103,6 +102,7 @@ __global__ __launch_bounds__(256, 4) void k_obs_chunks(ObsArgs a) {
       }
       // acc[kt][i]: raw logit of key kbase + 16 kt + 4 lq + i for this row
       if (edge) {
+        const int pos = pos0 + (rg % a.n_obs);   // this row's query position
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
