@@ -788,7 +788,12 @@ constexpr int kMergeThreads = 256;
 constexpr int kSplitGroups = 8;                     // split rows handled in parallel per output block
 
 // NSPT: split rows one output-block thread reads (>= S / 8)
-template <int NSPT>
+// Score update of the merge: attention masses (cumulative or decayed), the
+// attention p-norm, or key norms (separate instantiations, so the default one
+// carries no code of the others)
+enum MergeScore { kScoreMass = 0, kScorePNorm = 1, kScoreKeyNorm = 2 };
+
+template <int NSPT, int MS>
 __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
   const Geometry& G = a.g;
   const int blk = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
@@ -926,7 +931,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
   // to its window, found by the block holding that window's list position
   int kn_pos = -1;
   float kn_delta = 0.f;
-  if (a.key_norm && a.T - 1 >= G.sink) {
+  if (MS == kScoreKeyNorm && a.T - 1 >= G.sink) {
     kn_pos = n_fq + ((a.T - 1 - G.sink) / G.W - a.ring_w0);
     if (blk - nh == kn_pos / per_blk) {   // uniform per block
       const uint16_t* kn = a.k_new + (int64_t)b * G.H_kv * kHeadDim;
@@ -977,9 +982,9 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
   }
   if (hh == 0 && win >= 0) {
     float ns;
-    if (a.key_norm) {
+    if constexpr (MS == kScoreKeyNorm) {
       ns = old_score + (pos == kn_pos ? kn_delta : 0.f);
-    } else if (a.pnorm_p > 0.f) {
+    } else if constexpr (MS == kScorePNorm) {
       // p-norm: {sum of completed periods' u^p, u of this period}; the score
       // is their sum with u^p.  A period's first step closes the previous one,
       // whose u^p the old score already includes.
@@ -1035,9 +1040,16 @@ hipError_t launch_merge(const AttnArgs& a, hipStream_t st) {
   const int n_mass = (a.g.max_items + per_blk - 1) / per_blk;
   dim3 grid(a.g.H_q + n_mass, a.g.B);
   const int need = (a.g.n_split + kSplitGroups - 1) / kSplitGroups;
-  if (need <= 4) hipLaunchKernelGGL(k_merge<4>, grid, dim3(kMergeThreads), 0, st, a);
-  else if (need <= 8) hipLaunchKernelGGL(k_merge<8>, grid, dim3(kMergeThreads), 0, st, a);
-  else hipLaunchKernelGGL(k_merge<32>, grid, dim3(kMergeThreads), 0, st, a);
+  auto go = [&](auto kern) { hipLaunchKernelGGL(kern, grid, dim3(kMergeThreads), 0, st, a); };
+  auto by_split = [&](auto ms) {
+    constexpr int MS = decltype(ms)::value;
+    if (need <= 4) go(k_merge<4, MS>);
+    else if (need <= 8) go(k_merge<8, MS>);
+    else go(k_merge<32, MS>);
+  };
+  if (a.key_norm) by_split(std::integral_constant<int, kScoreKeyNorm>{});
+  else if (a.pnorm_p > 0.f) by_split(std::integral_constant<int, kScorePNorm>{});
+  else by_split(std::integral_constant<int, kScoreMass>{});
   return hipGetLastError();
 }
 }  // namespace qv
