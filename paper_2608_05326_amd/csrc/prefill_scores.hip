@@ -176,27 +176,47 @@ __global__ __launch_bounds__(256) void k_obs_rows(ObsArgs a) {
   }
 }
 
-// score[b][w] = (1 / H_q) * sum over KV heads and rows of l_w * exp2(m_c - M) / L;
-// one wave per window, lane j takes rows j, j + 64, ..., then a butterfly
-__global__ __launch_bounds__(256) void k_obs_windows(ObsArgs a) {
-  const int w = blockIdx.x * 4 + (threadIdx.x >> 6), b = blockIdx.y, lane = threadIdx.x & 63;
-  if (w >= a.n_w) return;   // uniform per wave
-  const int c = a.n_pre + w / (kObsChunkKeys / a.W);
+// score[b][w] = (1 / H_q) * sum over KV heads and rows of l_w * exp2(m_c - M) / L.
+// A workgroup of 256 threads serves wpw windows (1, 2 or 4: enough workgroups
+// for the chip whatever the window count), 256 / wpw threads each: thread t of
+// a window takes rows t, t + 256 / wpw, ... of every KV head; the window's sum
+// is folded by a butterfly per wave, then its waves in order.
+__global__ __launch_bounds__(256) void k_obs_windows(ObsArgs a, int wpw) {
+  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tpw = 256 / wpw;                      // threads per window
+  const int w = blockIdx.x * wpw + tid / tpw, t = tid % tpw;
+  __shared__ float red[4];
   float s = 0.f;
-  for (int g = 0; g < a.H_kv; ++g) {
-    const int64_t bg = (int64_t)b * a.H_kv + g;
-    const float* wl = a.wl + (bg * a.n_w + w) * a.n_rows;
-    const float2* cm = a.cml + (bg * a.n_chunks + c) * a.n_rows;
-    const float2* ml = a.row_ml + bg * a.n_rows;
+  if (w < a.n_w) {
+    const int c = a.n_pre + w / (kObsChunkKeys / a.W);
+    // entries (g, r) = t, t + tpw, ... of the KV head x row list, stepped without division
+    const int nr = a.n_rows, dg = tpw / nr, dr = tpw % nr;
+    int g = t / nr, r = t % nr;
 #pragma unroll 4
-    for (int r = lane; r < a.n_rows; r += 64) {
+    while (g < a.H_kv) {
+      const int64_t bg = (int64_t)b * a.H_kv + g;
       // M is finite for every row; a chunk with no visible key has m = -inf and l = 0
-      const float2 rm = ml[r];
-      s += wl[r] * __builtin_amdgcn_exp2f(cm[r].x - rm.x) * rm.y;
+      const float2 rm = a.row_ml[bg * nr + r];
+      const float m = a.cml[(bg * a.n_chunks + c) * nr + r].x;
+      s += a.wl[(bg * a.n_w + w) * nr + r] * __builtin_amdgcn_exp2f(m - rm.x) * rm.y;
+      r += dr;
+      g += dg;
+      if (r >= nr) {
+        r -= nr;
+        ++g;
+      }
     }
   }
   for (int o = 1; o < 64; o <<= 1) s += __shfl_xor(s, o, 64);
-  if (lane == 0) a.scores[(int64_t)b * a.n_w + w] = s / (float)a.H_q;
+  if (lane == 0) red[wave] = s;
+  __syncthreads();
+  const int wpwv = tpw / 64;                      // waves per window
+  if (t == 0 && w < a.n_w) {
+    const int w0 = wave;                          // this window's first wave
+    float v = red[w0];
+    for (int k = 1; k < wpwv; ++k) v += red[w0 + k];
+    a.scores[(int64_t)b * a.n_w + w] = v / (float)a.H_q;
+  }
 }
 
 hipError_t launch_prefill_scores(const ObsArgs& a, hipStream_t st) {
@@ -206,7 +226,9 @@ hipError_t launch_prefill_scores(const ObsArgs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_obs_rows, dim3((a.n_rows + 15) / 16, a.H_kv, a.B), dim3(256), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(k_obs_windows, dim3((a.n_w + 3) / 4, a.B), dim3(256), 0, st, a);
+  const int64_t nwin = (int64_t)a.n_w * a.B;
+  const int wpw = nwin >= 4096 ? 4 : nwin >= 2048 ? 2 : 1;   // windows per workgroup
+  hipLaunchKernelGGL(k_obs_windows, dim3((a.n_w + wpw - 1) / wpw, a.B), dim3(256), 0, st, a, wpw);
   return hipGetLastError();
 }
 
