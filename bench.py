@@ -21,8 +21,8 @@ Prints one JSON line.  `value` is microseconds per step (lower is better);
 duration, measured with HIP events on the cache's stream around rounds of 16
 back-to-back decode_attend calls with no routing running; `roofline.traffic`
 is the HBM traffic per call from the committed FETCH_SIZE / WRITE_SIZE record
-over the same duration (null when the library sources changed since it was
-taken).
+over the same duration (null when the sources of the attention path changed
+since it was taken).
 """
 from __future__ import annotations
 
@@ -112,15 +112,19 @@ def attend_bytes(wl, n_full, n_q4, n_q2, recent_tokens):
 COUNTERS = os.path.join(ROOT, "profiles", "decode_attend_8b_32k_hbm_counters.md")
 
 
+# sources that build the decode-attention kernels, their launch and the layouts
+# they read (the live list and split plan the re-rank kernel writes)
+ATTEND_SOURCES = ("attend.hip", "retier.hip", "runtime.cpp", "qv_device.h", "qv_layout.h")
+
+
 def kernel_source_hash():
-    """sha256 over the HIP sources of the library (any kernel edit changes it)."""
+    """sha256 over the sources of the decode-attention path (any edit of them changes it)."""
     import hashlib
     d = os.path.join(ROOT, "paper_2608_05326_amd", "csrc")
     h = hashlib.sha256()
-    for f in sorted(os.listdir(d)):
-        if f.endswith((".hip", ".h", ".cpp")):
-            h.update(f.encode())
-            h.update(open(os.path.join(d, f), "rb").read())
+    for f in ATTEND_SOURCES:
+        h.update(f.encode())
+        h.update(open(os.path.join(d, f), "rb").read())
     return h.hexdigest()
 
 
