@@ -279,11 +279,14 @@ def test_smoke_entry_point():
 # asynchronous routing (routing stream + per-layer ordering)
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name", ["c2s", "c3s"])
-def test_async_routing_lockstep(name):
+@pytest.mark.parametrize("name,kw", [("c2s", {}), ("c3s", {}), ("c5s", {"rope_base": 500000.0}),
+                                     ("c5s", {"score_p": 3.0}), ("c2s", {"score_decay": 0.9})])
+def test_async_routing_lockstep(name, kw):
+    """Routing on its own stream, also with RoPE, the p-norm over 8-step periods
+    and the decayed score (the period bookkeeping happens at enqueue time)."""
     import paper_2608_05326_amd as qv
     from tests.gpu_harness import Lockstep
-    ls = Lockstep(syn.get_workload(name), flags=qv.FLAG_ASYNC_ROUTING, steps=12)
+    ls = Lockstep(syn.get_workload(name), flags=qv.FLAG_ASYNC_ROUTING, steps=12, **kw)
     try:
         ls.run()
     finally:
