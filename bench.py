@@ -253,7 +253,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU; the decode path has no "
-                                   "multi-GPU mode (see DESIGN.md for how it would shard)",
+                                   "multi-GPU mode",
                           "n_gpus": args.gpus}))
         return 2
     if args.calibrate_copy > 0:

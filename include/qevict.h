@@ -47,7 +47,7 @@ typedef int32_t qevict_status;
 enum {
   QEVICT_OK = 0,
   QEVICT_ERR_INVALID_ARG = -1,   /* null pointer, index out of range, bad shape        */
-  QEVICT_ERR_UNSUPPORTED = -2,   /* shape or option this build does not implement      */
+  QEVICT_ERR_UNSUPPORTED = -2,   /* shape or option the library does not implement     */
   QEVICT_ERR_WORKSPACE = -3,     /* workspace too small or misaligned                  */
   QEVICT_ERR_BAD_STATE = -4,     /* call out of protocol order, or cache poisoned       */
   QEVICT_ERR_NONFINITE = -5,     /* NaN/Inf in scores or quantizer input               */
@@ -127,9 +127,9 @@ typedef struct {
   int32_t num_layers;
   int32_t num_q_heads;       /* H_q                                                          */
   int32_t num_kv_heads;      /* H_kv; H_q % H_kv == 0 and H_q / H_kv <= 16                  */
-  int32_t head_dim;          /* d; this build supports 128                                   */
+  int32_t head_dim;          /* d; the library supports 128                                  */
   int32_t window_tokens;     /* W; 32 or 64                                                  */
-  int32_t group_size;        /* G; this build requires G == W (keys: one group per channel   */
+  int32_t group_size;        /* G; the library requires G == W (keys: one group per channel  */
                              /*  per window; values: W/... groups of G channels per token)    */
   int32_t quant_bits;        /* 4, 2 or QEVICT_BITS_MIXED_4_2                                */
   int32_t sink_tokens;       /* protected sink prefix |S| (at most 64 windows)               */

@@ -129,7 +129,7 @@ WORKLOADS = {
                    frac_quant="0.4", steps=128, retier_interval=8, **_drift_defaults()),
     # The paper's default operating point on the 8B shape: five sink tokens, 32 recent
     # tokens, routing every 8 steps, int2 tier, quantized fraction q = 0.70 of the
-    # historical byte budget (20% of the full cache), windows of 32 (this build's
+    # historical byte budget (20% of the full cache), windows of 32 (the library's
     # smallest window); capacities from the byte-budget equation.
     "c6": Workload("c6", 6, batch=1, layers=1, num_q_heads=32, num_kv_heads=8, head_dim=128,
                    prompt_len=32768, window=32, group=32, bits=2, frac_full="0", frac_quant="0",
