@@ -215,7 +215,8 @@ qevict_status qevict_cache_destroy(qevict_cache *c);
  *   k, v        [B, H_kv, prompt_len, d] bf16 prompt keys / values
  *   init_scores [B, n_w] fp32, n_w = ceil((prompt_len - sink)/W): initial
  *               cumulative score of every prompt window (also partial ones);
- *               unused (may be NULL) with QEVICT_SCORE_KEY_NORM
+ *               unused (may be NULL) with QEVICT_SCORE_KEY_NORM or when the
+ *               prompt has no window (prompt_len <= sink)
  * The complete windows outside the sink and recent regions are routed at once
  * (TopK on init_scores; Quantized windows are quantized from k, v).  The
  * prompt buffers are only read by work enqueued here. */

@@ -603,13 +603,15 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
   const Geometry& g = c->g;
   if (ls.prefilled) return fail(QEVICT_ERR_BAD_STATE, "layer %d already prefilled", layer);
   const bool key_norm = c->cfg.score_mode == QEVICT_SCORE_KEY_NORM;
-  if (!k || !v || (!init_scores && !key_norm)) return fail(QEVICT_ERR_INVALID_ARG, "null prompt pointer");
-  if (((uintptr_t)k & 15) || ((uintptr_t)v & 15))
-    return fail(QEVICT_ERR_INVALID_ARG, "prompt keys / values must be 16-byte aligned");
   if (prompt_len < g.sink || prompt_len < 1 || prompt_len > c->cfg.max_context)
     return fail(QEVICT_ERR_INVALID_ARG, "prompt_len %d outside [max(1, sink), max_context]", prompt_len);
   const int n_hist = aged_end(g, prompt_len);
   const int n_init = n_started(g, prompt_len);
+  // initial scores are read only for the prompt's windows (none when the prompt is all sink)
+  if (!k || !v || (!init_scores && !key_norm && n_init > 0))
+    return fail(QEVICT_ERR_INVALID_ARG, "null prompt pointer");
+  if (((uintptr_t)k & 15) || ((uintptr_t)v & 15))
+    return fail(QEVICT_ERR_INVALID_ARG, "prompt keys / values must be 16-byte aligned");
   if (n_hist > kMaxCand)
     return fail(QEVICT_ERR_UNSUPPORTED, "%d prompt windows to route; at most %d", n_hist, kMaxCand);
   if (n_init - n_hist > g.NR)

@@ -233,7 +233,8 @@ class Cache:
         """k, v: bf16 [B, H_kv, T, d]; init_scores: float32 [B, n_w] (None with
         the key-norm score)."""
         t = self.torch
-        sc = None if init_scores is None else _ptr(init_scores, t.float32, "init_scores")
+        sc = None if init_scores is None or init_scores.numel() == 0 else \
+            _ptr(init_scores, t.float32, "init_scores")
         self._c(self.lib.qevict_prefill_assign(
             self.handle, layer, _ptr(k, t.bfloat16, "k"), _ptr(v, t.bfloat16, "v"), k.shape[2], sc))
 

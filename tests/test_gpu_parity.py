@@ -91,3 +91,20 @@ def test_rope_lockstep(name, base):
     8-step periods, and sink / recent regions."""
     ls = _lockstep(name, rope_base=base)
     assert ls.events > 0
+
+
+@pytest.mark.parametrize("prompt,sink,steps", [(5, 0, 100), (16, 16, 70)])
+def test_short_prompts(prompt, sink, steps):
+    """A prompt shorter than one window (nothing routed at prefill) and a prompt
+    that is only sink tokens (no prompt window, no initial scores): windows are
+    started, aged and routed during decode (K_f = 1, K_q = 1)."""
+    from tests.gpu_harness import Lockstep
+    wl = syn.get_workload("c2s").replace(name=f"short{prompt}", prompt_len=prompt, sink=sink, steps=steps)
+    ls = Lockstep(wl, capacity_full=1, capacity_quant=1)
+    print(f"[lockstep] short prompt {prompt} sink {sink} steps {steps}", flush=True)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[lockstep] short: max out err {ls.max_out_err:.2e}, promotions {ls.promotions}", flush=True)
+    assert ls.events == steps
