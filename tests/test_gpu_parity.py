@@ -108,3 +108,20 @@ def test_short_prompts(prompt, sink, steps):
         ls.close()
     print(f"[lockstep] short: max out err {ls.max_out_err:.2e}, promotions {ls.promotions}", flush=True)
     assert ls.events == steps
+
+
+@pytest.mark.parametrize("hq,hkv", [(24, 2), (12, 4), (32, 2)])
+def test_head_layouts(hq, hkv):
+    """Query-head counts that are not powers of two (the merge sums heads through
+    LDS instead of a butterfly) and GQA ratios 12 and 16 (four 4-head groups per
+    wave in the attention kernel), plus GQA 3."""
+    from tests.gpu_harness import Lockstep
+    wl = syn.get_workload("c2s").replace(name=f"h{hq}x{hkv}", num_q_heads=hq, num_kv_heads=hkv, steps=16)
+    ls = Lockstep(wl)
+    print(f"[lockstep] heads {hq}/{hkv}", flush=True)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[lockstep] heads {hq}/{hkv}: max out err {ls.max_out_err:.2e}, "
+          f"max score err {ls.max_score_err:.2e}, promotions {ls.promotions}", flush=True)
