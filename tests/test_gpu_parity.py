@@ -125,3 +125,18 @@ def test_head_layouts(hq, hkv):
         ls.close()
     print(f"[lockstep] heads {hq}/{hkv}: max out err {ls.max_out_err:.2e}, "
           f"max score err {ls.max_score_err:.2e}, promotions {ls.promotions}", flush=True)
+
+
+@pytest.mark.parametrize("bits", [4, 42])
+def test_window64_bit_widths(bits):
+    """64-token windows with int4 and with the mixed int4 / int2 tier (c4s is int2)."""
+    wl_name = "c4s"
+    from tests.gpu_harness import Lockstep
+    wl = syn.get_workload(wl_name).replace(name=f"w64b{bits}", bits=bits, steps=16)
+    ls = Lockstep(wl)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[lockstep] W 64 bits {bits}: max out err {ls.max_out_err:.2e}, promotions {ls.promotions}",
+          flush=True)
