@@ -138,23 +138,36 @@ __global__ __launch_bounds__(256, 4) void k_obs_chunks(ObsArgs a) {
   }
 }
 
-// (M, 1 / L) of every row from its chunks' (max, exp-sum) pairs: 16 rows per
-// workgroup, thread (p, r) takes chunks p, p + 16, ... of row r (consecutive
+// (M, 1 / L) of every row from its chunks' (max, exp-sum) pairs: 256 / P rows
+// per workgroup, thread (p, r) takes chunks p, p + P, ... of row r (consecutive
 // threads read consecutive rows): first their max, then their sum relative to
-// it; the 16 partial results are folded in order of p
+// it; the P partial results of a row are folded by a pairwise tree (a fixed order).
+// P = 16: 16 consecutive rows per workgroup keep the loads of a chunk's
+// statistics in whole 128-byte lines (4 rows per workgroup read 32-byte pieces
+// and were three times slower at 1024 chunks).
+__device__ __forceinline__ float2 ml_combine(float2 x, float2 y) {
+  const float mm = fmaxf(x.x, y.x);
+  float ls = 0.f;
+  if (x.x > -INFINITY) ls += x.y * __builtin_amdgcn_exp2f(x.x - mm);
+  if (y.x > -INFINITY) ls += y.y * __builtin_amdgcn_exp2f(y.x - mm);
+  return make_float2(mm, ls);
+}
+
+template <int P>
 __global__ __launch_bounds__(256) void k_obs_rows(ObsArgs a) {
+  constexpr int RPB = 256 / P;   // rows per workgroup
   const int g = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
-  const int rl = tid & 15, p = tid >> 4, r = blockIdx.x * 16 + rl;
+  const int rl = tid % RPB, p = tid / RPB, r = blockIdx.x * RPB + rl;
   const int64_t bg = (int64_t)b * a.H_kv + g;
-  __shared__ float2 part[16][16];
+  __shared__ float2 part[P][RPB];
   float m = -INFINITY, l = 0.f;
   if (r < a.n_rows) {
     const float2* cm = a.cml + bg * a.n_chunks * a.n_rows + r;
 #pragma unroll 4
-    for (int c = p; c < a.n_chunks; c += 16) m = fmaxf(m, cm[(int64_t)c * a.n_rows].x);
+    for (int c = p; c < a.n_chunks; c += P) m = fmaxf(m, cm[(int64_t)c * a.n_rows].x);
     if (m > -INFINITY) {
 #pragma unroll 4
-      for (int c = p; c < a.n_chunks; c += 16) {
+      for (int c = p; c < a.n_chunks; c += P) {
         const float2 s = cm[(int64_t)c * a.n_rows];
         l += s.y * __builtin_amdgcn_exp2f(s.x - m);   // exp2(-inf) = 0 for empty chunks
       }
@@ -162,17 +175,13 @@ __global__ __launch_bounds__(256) void k_obs_rows(ObsArgs a) {
   }
   part[p][rl] = make_float2(m, l);
   __syncthreads();
+  for (int h = P / 2; h > 0; h >>= 1) {
+    if (p < h) part[p][rl] = ml_combine(part[p][rl], part[p + h][rl]);
+    __syncthreads();
+  }
   if (p == 0 && r < a.n_rows) {
-    for (int q = 1; q < 16; ++q) {
-      const float2 s = part[q][rl];
-      const float mm = fmaxf(m, s.x);
-      float ls = 0.f;
-      if (m > -INFINITY) ls += l * __builtin_amdgcn_exp2f(m - mm);
-      if (s.x > -INFINITY) ls += s.y * __builtin_amdgcn_exp2f(s.x - mm);
-      m = mm;
-      l = ls;
-    }
-    a.row_ml[bg * a.n_rows + r] = make_float2(m, l > 0.f ? 1.f / l : 0.f);
+    const float2 t = part[0][rl];
+    a.row_ml[bg * a.n_rows + r] = make_float2(t.x, t.y > 0.f ? 1.f / t.y : 0.f);
   }
 }
 
@@ -224,7 +233,7 @@ hipError_t launch_prefill_scores(const ObsArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(k_obs_chunks, dim3(a.n_blk, a.H_kv, a.B), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_obs_rows, dim3((a.n_rows + 15) / 16, a.H_kv, a.B), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(k_obs_rows<16>, dim3((a.n_rows + 15) / 16, a.H_kv, a.B), dim3(256), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int64_t nwin = (int64_t)a.n_w * a.B;
   const int wpw = nwin >= 4096 ? 4 : nwin >= 2048 ? 2 : 1;   // windows per workgroup
