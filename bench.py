@@ -91,6 +91,19 @@ def to_dev(bits):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
 
 
+def workload_desc(wl):
+    if wl.name == "c2":
+        return ("Llama-3-8B-shaped layer, 32768-token context, batch 1, 32 query / 8 KV heads, "
+                "head_dim 128, windows of 32, 20% bf16 / 30% int4 group 32 / 50% evicted, re-tier "
+                "every step, drifting queries")
+    bits = {4: "int4", 2: "int2", 42: "int4 / int2 by rank"}[wl.bits]
+    tiers = (f"byte budget {wl.budget_frac} of the full cache, quantized share {wl.q_frac}"
+             if wl.budget_frac else f"{wl.frac_full} bf16 / {wl.frac_quant} quantized")
+    return (f"{wl.prompt_len}-token context, batch {wl.batch}, {wl.num_q_heads} query / "
+            f"{wl.num_kv_heads} KV heads, head_dim {wl.head_dim}, windows of {wl.window}, {bits} "
+            f"group {wl.group}, {tiers}, sink {wl.sink}, recent {wl.recent}, re-tier every step")
+
+
 def attend_bytes(wl, n_full, n_q4, n_q2, recent_tokens):
     """Algorithmic bytes of one attention pass of one sequence-layer.
 
@@ -284,24 +297,31 @@ def main():
 
     # ---- prefill every layer cache (prompt generated on the host, in parallel) ----
     def gen(layer):
-        k, v = syn.prompt_kv(wl, args.seed, 0, layer)
-        return layer, k, v, syn.init_scores(wl, args.seed, 0, layer)
+        kv = [syn.prompt_kv(wl, args.seed, b, layer) for b in range(wl.batch)]
+        init = np.stack([syn.init_scores(wl, args.seed, b, layer) for b in range(wl.batch)])
+        return layer, np.stack([x[0] for x in kv]), np.stack([x[1] for x in kv]), init
 
     t0 = time.time()
     with ThreadPoolExecutor(max_workers=8) as ex:
         for layer, k, v, init in ex.map(gen, range(NL)):
-            K, V = to_dev(k[None]), to_dev(v[None])
-            S = torch.from_numpy(init[None].copy()).cuda()
+            K, V = to_dev(k), to_dev(v)                  # [B, H_kv, T, d]
+            S = torch.from_numpy(np.ascontiguousarray(init)).cuda()
             cache.prefill_assign(layer, K, V, S)
             torch.cuda.synchronize()
             del K, V, S
     print(f"[bench] prefilled {NL} layers in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
 
     # ---- per-step inputs, resident on the GPU before timing ----
-    dec = [syn.decode_inputs(wl, args.seed, 0, layer, per_layer) for layer in range(NL)]
-    Q = [to_dev(d[0][:, None]) for d in dec]     # [steps, B, H_q, d]
-    KN = [to_dev(d[1][:, None]) for d in dec]
-    VN = [to_dev(d[2][:, None]) for d in dec]
+    dec = [[syn.decode_inputs(wl, args.seed, b, layer, per_layer) for b in range(wl.batch)]
+           for layer in range(NL)]
+    Q = [to_dev(np.stack([x[0] for x in d], axis=1)) for d in dec]     # [steps, B, H_q, d]
+    KN = [to_dev(np.stack([x[1] for x in d], axis=1)) for d in dec]
+    VN = [to_dev(np.stack([x[2] for x in d], axis=1)) for d in dec]
+    # the decode calls below pass raw pointers: check every extent on the host first
+    for l in range(NL):
+        assert tuple(Q[l].shape) == (per_layer, wl.batch, wl.num_q_heads, wl.head_dim), Q[l].shape
+        for x in (KN[l], VN[l]):
+            assert tuple(x.shape) == (per_layer, wl.batch, wl.num_kv_heads, wl.head_dim), x.shape
     out = torch.empty((wl.batch, wl.num_q_heads, wl.head_dim), dtype=torch.float32, device="cuda")
 
     import ctypes
@@ -351,7 +371,7 @@ def main():
     run_steps(0, args.warmup)
     cache.join_routing()
     torch.cuda.synchronize()
-    st0 = [cache.get_state(l, 0) for l in range(NL)]
+    st0 = [[cache.get_state(l, b) for b in range(wl.batch)] for l in range(NL)]
 
     # ---- timed region ----
     torch.cuda.synchronize()
@@ -408,13 +428,14 @@ def main():
     total_bytes = 0
     for i in range(args.warmup, args.warmup + args.steps):
         layer = i % NL
-        st = st0[layer]
-        n_full = int(np.sum(st["tiers"] == qv.TIER_FULL))
-        bits = st["bits"][st["tiers"] == qv.TIER_QUANT]
         T = wl.prompt_len + (i // NL) + 1
         recent = (T - wl.sink) - ((T - wl.sink) // wl.window) * wl.window
         recent = recent if recent else wl.window
-        total_bytes += attend_bytes(wl, n_full, int(np.sum(bits == 4)), int(np.sum(bits == 2)), recent)
+        for st in st0[layer]:   # every sequence of the batch
+            n_full = int(np.sum(st["tiers"] == qv.TIER_FULL))
+            bits = st["bits"][st["tiers"] == qv.TIER_QUANT]
+            total_bytes += attend_bytes(wl, n_full, int(np.sum(bits == 4)), int(np.sum(bits == 2)),
+                                        recent)
     bytes_per_step = total_bytes / args.steps
 
     res = {
@@ -428,11 +449,9 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16+int4 (fp32 accumulate)",
+        "dtype": "bf16+int4 (fp32 accumulate)" if wl.bits == 4 else "bf16+int2/int4 (fp32 accumulate)",
         "data": "synthetic",
-        "config": {"workload": "Llama-3-8B-shaped layer, 32768-token context, batch 1, 32 query / 8 KV "
-                               "heads, head_dim 128, windows of 32, 20% bf16 / 30% int4 group 32 / 50% "
-                               "evicted, re-tier every step, drifting queries",
+        "config": {"workload": workload_desc(wl),
                    "layer_caches_rotated": NL, "global_batch": wl.batch, "seq_len": wl.prompt_len,
                    "routing": args.routing, "rope_base": args.rope_base, "parallelism": "single GPU"},
         "step_GBps": round(bytes_per_step / (ms_per_step * 1e-3) / 1e9, 1),

@@ -8,6 +8,7 @@ creating a cache does, and there is no CPU fallback: a missing library raises.
 from __future__ import annotations
 
 import ctypes
+import math
 import dataclasses
 import os
 
@@ -184,11 +185,16 @@ def prefill_scores_scratch_size(cfg: Config, prompt_len: int, n_obs: int) -> int
     return n.value
 
 
-def _ptr(t, torch_dtype=None, name="tensor"):
+def _ptr(t, torch_dtype=None, name="tensor", shape=None):
+    """Device address of a contiguous tensor; with `shape`, the tensor must hold
+    exactly that many elements (the kernels read and write whole extents)."""
     if not t.is_cuda or not t.is_contiguous():
         raise ValueError(f"{name} must be a contiguous device tensor")
     if torch_dtype is not None and t.dtype != torch_dtype:
         raise ValueError(f"{name} must be {torch_dtype}, got {t.dtype}")
+    if shape is not None and t.numel() != math.prod(shape):
+        raise ValueError(f"{name} must hold {' x '.join(map(str, shape))} values, "
+                         f"got shape {tuple(t.shape)}")
     return ctypes.c_void_p(t.data_ptr())
 
 
@@ -233,10 +239,16 @@ class Cache:
         """k, v: bf16 [B, H_kv, T, d]; init_scores: float32 [B, n_w] (None with
         the key-norm score)."""
         t = self.torch
+        c = self.cfg
+        if k.dim() != 4:
+            raise ValueError(f"k must be [B, H_kv, T, d], got shape {tuple(k.shape)}")
+        T = k.shape[2]
+        kv = (c.batch, c.num_kv_heads, T, c.head_dim)
+        n_w = max(0, -(-(T - c.sink_tokens) // c.window_tokens))
         sc = None if init_scores is None or init_scores.numel() == 0 else \
-            _ptr(init_scores, t.float32, "init_scores")
+            _ptr(init_scores, t.float32, "init_scores", (c.batch, n_w))
         self._c(self.lib.qevict_prefill_assign(
-            self.handle, layer, _ptr(k, t.bfloat16, "k"), _ptr(v, t.bfloat16, "v"), k.shape[2], sc))
+            self.handle, layer, _ptr(k, t.bfloat16, "k", kv), _ptr(v, t.bfloat16, "v", kv), T, sc))
 
     def prefill_scores(self, q_obs, k, scores=None, scratch=None):
         """Initial window scores from the observation queries' attention.
@@ -271,10 +283,12 @@ class Cache:
 
     def decode_attend(self, layer: int, q, k_new, v_new, out):
         t = self.torch
-        odt = t.bfloat16 if self.cfg.out_dtype == OUT_BF16 else t.float32
+        c = self.cfg
+        odt = t.bfloat16 if c.out_dtype == OUT_BF16 else t.float32
+        qs, ks = (c.batch, c.num_q_heads, c.head_dim), (c.batch, c.num_kv_heads, c.head_dim)
         self._c(self.lib.qevict_decode_attend(
-            self.handle, layer, _ptr(q, t.bfloat16, "q"), _ptr(k_new, t.bfloat16, "k_new"),
-            _ptr(v_new, t.bfloat16, "v_new"), _ptr(out, odt, "out")))
+            self.handle, layer, _ptr(q, t.bfloat16, "q", qs), _ptr(k_new, t.bfloat16, "k_new", ks),
+            _ptr(v_new, t.bfloat16, "v_new", ks), _ptr(out, odt, "out", qs)))
 
     def retier(self, layer: int, stats: bool = False):
         if stats:
@@ -331,6 +345,8 @@ class Cache:
 
     def debug_shift_keys(self, layer: int, seq: int, window: int, delta):
         dlt = np.ascontiguousarray(delta, dtype=np.float32)
+        if dlt.size != self.cfg.num_kv_heads * self.cfg.head_dim:
+            raise ValueError(f"delta must hold H_kv x d values, got shape {dlt.shape}")
         self._c(self.lib.qevict_debug_shift_keys(self.handle, layer, seq, window,
                                                  dlt.ctypes.data_as(ctypes.c_void_p)))
 

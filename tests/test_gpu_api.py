@@ -130,6 +130,15 @@ def test_protocol_and_argument_errors():
             c.retier(1)
         assert ex.value.status == qv.ERR_INVALID_ARG
         K, V, S = _prompt(wl)
+        # extents that differ from the configuration are rejected on the host
+        with pytest.raises(ValueError):                    # two sequences for a batch of one
+            c.prefill_assign(0, torch.cat([K, K]), torch.cat([V, V]), S)
+        with pytest.raises(ValueError):                    # scores for one window too many
+            c.prefill_assign(0, K, V, torch.cat([S, S[:, :1]], dim=1))
+        with pytest.raises(ValueError):
+            c.decode_attend(0, torch.cat([q, q]), kn, vn, out)
+        with pytest.raises(ValueError):
+            c.decode_attend(0, q, kn[:, :1].contiguous(), vn, out)
         c.prefill_assign(0, K, V, S)
         with pytest.raises(qv.QEvictError) as ex:          # second prefill of a layer
             c.prefill_assign(0, K, V, S)
