@@ -449,7 +449,7 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16+int4 (fp32 accumulate)" if wl.bits == 4 else "bf16+int2/int4 (fp32 accumulate)",
+        "dtype": "bf16+" + {4: "int4", 2: "int2", 42: "int4/int2"}[wl.bits] + " (fp32 accumulate)",
         "data": "synthetic",
         "config": {"workload": workload_desc(wl),
                    "layer_caches_rotated": NL, "global_batch": wl.batch, "seq_len": wl.prompt_len,
@@ -463,7 +463,10 @@ def main():
     }
     if attend_us:
         ach = bytes_per_step / (attend_us * 1e-6) / 1e9
-        rec = measured_traffic()
+        # the counter record was taken on the default run (8B / 32K workload, no RoPE,
+        # library split count): other runs report no traffic
+        default_run = args.workload == "c2" and args.rope_base == 0 and args.splits == 0
+        rec = measured_traffic() if default_run else None
         traffic = None
         if rec:
             traffic = round(rec["hbm_bytes_per_launch"] / (attend_us * 1e-6) / 1e9, 1)
