@@ -17,6 +17,10 @@
  *    unless a comment says "host".  bf16 values are passed as uint16_t bit
  *    patterns.  The caller owns every buffer; the library never allocates or
  *    frees device memory: all state lives in the caller's workspace.
+ *  - Each buffer must hold the full extent its comment gives, with B, H_q,
+ *    H_kv and d taken from the configuration: the kernels read and write
+ *    whole extents and cannot check a buffer's size (null pointers and
+ *    misalignment are rejected on the host).
  *  - Work is enqueued on the HIP stream given to qevict_cache_init and is
  *    asynchronous unless the comment says "synchronous".  Inputs must stay
  *    valid until the stream has passed the call.
