@@ -28,6 +28,7 @@ from __future__ import annotations
 
 import argparse
 import json
+from fractions import Fraction
 import os
 import sys
 import time
@@ -101,7 +102,8 @@ def workload_desc(wl):
              if wl.budget_frac else f"{wl.frac_full} bf16 / {wl.frac_quant} quantized")
     return (f"{wl.prompt_len}-token context, batch {wl.batch}, {wl.num_q_heads} query / "
             f"{wl.num_kv_heads} KV heads, head_dim {wl.head_dim}, windows of {wl.window}, {bits} "
-            f"group {wl.group}, {tiers}, sink {wl.sink}, recent {wl.recent}, re-tier every step")
+            f"group {wl.group}, {tiers}, sink {wl.sink}, recent {wl.recent}, "
+            + ("re-tier every step" if wl.retier_interval == 1 else f"re-tier every {wl.retier_interval} steps"))
 
 
 def attend_bytes(wl, n_full, n_q4, n_q2, recent_tokens):
@@ -282,11 +284,22 @@ def main():
     # + four rounds of attention timing and two of routing statistics after the timed steps
     per_layer = -(-(args.warmup + args.steps) // NL) + 7
     asyncr = args.routing == "async"
+    R = wl.retier_interval            # routing event after every R-th step of a layer cache
+    kf, kq = wl.capacity_full, wl.capacity_quant
+    if wl.budget_frac:
+        # byte budget: a fraction of the prompt's full bf16 cache, quantized share q
+        full = 2 * wl.num_kv_heads * wl.head_dim * wl.prompt_len * 2
+        probe = qv.Config(batch=wl.batch, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                          window_tokens=wl.window, group_size=wl.group, quant_bits=wl.bits,
+                          max_context=wl.prompt_len + per_layer, capacity_full=0, capacity_quant=0,
+                          sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=R)
+        kf, kq = qv.qevict.capacities_for_budget(probe, int(Fraction(wl.budget_frac) * full),
+                                                 int(Fraction(wl.q_frac) * 1000))
     cfg = qv.Config(batch=wl.batch, num_layers=NL, num_q_heads=wl.num_q_heads,
                     num_kv_heads=wl.num_kv_heads, window_tokens=wl.window, group_size=wl.group,
                     quant_bits=wl.bits, max_context=wl.prompt_len + per_layer,
-                    capacity_full=wl.capacity_full, capacity_quant=wl.capacity_quant,
-                    sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=1,
+                    capacity_full=kf, capacity_quant=kq,
+                    sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=R,
                     num_splits=args.splits, flags=qv.FLAG_ASYNC_ROUTING if asyncr else 0,
                     rope_base=args.rope_base)
     stream = torch.cuda.Stream()
@@ -339,6 +352,8 @@ def main():
             raise RuntimeError(lib.qevict_last_error().decode())
 
     def route(layer):
+        if counter[layer] % R:        # not the end of a routing period
+            return
         if lib.qevict_retier(h, layer, None):
             raise RuntimeError(lib.qevict_last_error().decode())
 
@@ -453,7 +468,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": workload_desc(wl),
                    "layer_caches_rotated": NL, "global_batch": wl.batch, "seq_len": wl.prompt_len,
-                   "routing": args.routing, "rope_base": args.rope_base, "parallelism": "single GPU"},
+                   "routing": args.routing, "routing_interval": R, "rope_base": args.rope_base,
+                   "parallelism": "single GPU"},
         "step_GBps": round(bytes_per_step / (ms_per_step * 1e-3) / 1e9, 1),
         "algorithmic_MB_per_step": round(bytes_per_step / 1e6, 3),
         "host_wall_us_per_step": round(wall / args.steps * 1e6, 2),
