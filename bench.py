@@ -22,7 +22,12 @@ duration, measured with HIP events on the cache's stream around rounds of 16
 back-to-back decode_attend calls with no routing running; `roofline.traffic`
 is the HBM traffic per call from the committed FETCH_SIZE / WRITE_SIZE record
 over the same duration (null when the sources of the attention path changed
-since it was taken).
+since it was taken, and on any run other than the default one it covers).
+
+`--workload` runs another synthetic shape instead (all sequences of its batch,
+byte-budget capacities where it gives a budget, a routing event after every
+R-th step of a cache at its routing interval R); such runs are context, not
+the benchmark line.
 """
 from __future__ import annotations
 
