@@ -398,6 +398,18 @@ class QEvictUnit:
         # original bf16 keys / values of every token ever appended
         self.k = np.zeros((c.num_kv_heads, max_tokens, c.head_dim))
         self.v = np.zeros((c.num_kv_heads, max_tokens, c.head_dim))
+        # every token position as attention reads it now: the originals for sink,
+        # open and aged tokens, the bf16 copy for Full windows, z + s c for
+        # Quantized ones; att_live marks the positions attention sees (evicted
+        # windows' rows are masked out).  Refreshed whenever a window changes tier
+        # or its ledger changes (see _refresh); accessible() is the same set
+        # assembled from the tier map.
+        self.att_k = np.zeros((c.num_kv_heads, max_tokens, c.head_dim))
+        self.att_v = np.zeros((c.num_kv_heads, max_tokens, c.head_dim))
+        self.att_live = np.zeros(max_tokens, dtype=bool)
+        self.owner = np.full(max_tokens, -1, dtype=np.int64)   # window of each position, -1 = sink
+        if max_tokens > c.sink:
+            self.owner[c.sink:] = (np.arange(c.sink, max_tokens) - c.sink) // c.window
         self.T = 0
         self.state = np.full(self.n_win_cap, -1, dtype=np.int64)   # -1: not started
         self.score = np.zeros(self.n_win_cap)
@@ -440,6 +452,26 @@ class QEvictUnit:
             kh = rope_rotate(kh, *self._rope(w))
         return kh, vh
 
+    def _refresh(self, w: int):
+        """Rewrite window w's rows of the attention-domain copy from its tier:
+        bf16 copy (Full), z + s c (Quantized), originals (open / aged), or
+        masked out (Evicted)."""
+        a, b = self.win_range(w)
+        b = min(b, self.T)
+        st = self.state[w]
+        if st == EVICTED:
+            self.att_live[a:b] = False
+            return
+        if st == FULL:
+            kk, vv = self.full_k[w], self.full_v[w]
+        elif st == QUANT:
+            kk, vv = self._dequantize(w)
+        else:
+            kk, vv = self.k[:, a:b], self.v[:, a:b]
+        self.att_k[:, a:b] = kk[:, :b - a]
+        self.att_v[:, a:b] = vv[:, :b - a]
+        self.att_live[a:b] = True
+
     def _age(self):
         """OPEN -> AGED once a window is complete and older than the recent region."""
         c = self.cfg
@@ -464,6 +496,9 @@ class QEvictUnit:
         T = k.shape[1]
         self.k[:, :T] = k
         self.v[:, :T] = v
+        self.att_k[:, :T] = k
+        self.att_v[:, :T] = v
+        self.att_live[:T] = True
         self.T = T
         self._start_windows()
         n = int(np.sum(self.state >= 0))
@@ -505,6 +540,9 @@ class QEvictUnit:
         c = self.cfg
         self.k[:, self.T] = k_new
         self.v[:, self.T] = v_new
+        self.att_k[:, self.T] = k_new       # sink or open-window token: attended as given
+        self.att_v[:, self.T] = v_new
+        self.att_live[self.T] = True
         self.T += 1
         self._start_windows()
         if c.key_norm and self.T - 1 >= c.sink:   # the token's share of its window's key-norm score
@@ -546,39 +584,48 @@ class QEvictUnit:
         """Attention of all query heads; accumulate window scores.
 
         q: float64 [H_q, d].  Returns (out [H_q, d], mass [H_q, n_win_cap],
-        sink_mass [H_q]).  The score update adds, for every accessible window,
-        the attention mass its tokens received averaged over the H_q heads.
+        sink_mass [H_q]).  Each query head attends with softmax(q k^T * scale)
+        over the accessible tokens (the live rows of the attention-domain copy,
+        i.e. the set accessible() lists); the score update adds, for every
+        accessible window, the attention mass its tokens received averaged over
+        the H_q heads.
         """
         c = self.cfg
+        T = self.T
         out = np.zeros((c.num_q_heads, c.head_dim))
         mass = np.zeros((c.num_q_heads, self.n_win_cap))
         sink_mass = np.zeros(c.num_q_heads)
-        kk, vv, owner = self.accessible()
+        live = self.att_live[:T]
+        owner = self.owner[:T][live]
         win = owner >= 0
-        for h in range(c.num_q_heads):
-            g = h // c.gqa
-            logits = (kk[g] @ q[h]) * c.scale
-            e = np.exp(logits - logits.max())
-            p = e / e.sum()
-            out[h] = p @ vv[g]
-            mass[h] = np.bincount(owner[win], weights=p[win], minlength=self.n_win_cap)
-            sink_mass[h] = p[~win].sum()
-        live = (self.state >= 0) & (self.state != EVICTED)
+        for g in range(c.num_kv_heads):
+            hs = slice(g * c.gqa, (g + 1) * c.gqa)       # the query heads reading KV head g
+            logits = (self.att_k[g, :T] @ q[hs].T) * c.scale    # [T, heads of the group]
+            logits[~live] = -np.inf
+            e = np.exp(logits - logits.max(axis=0))
+            p = e / e.sum(axis=0)
+            out[hs] = p.T @ self.att_v[g, :T]
+            for j in range(c.gqa):
+                h = g * c.gqa + j
+                pl = p[live, j]
+                mass[h] = np.bincount(owner[win], weights=pl[win], minlength=self.n_win_cap)
+                sink_mass[h] = pl[~win].sum()
+        live_w = (self.state >= 0) & (self.state != EVICTED)
         if self.new_period and c.score_decay != 1.0:
-            self.score[live] *= c.score_decay
+            self.score[live_w] *= c.score_decay
         self.new_period = False
         if c.score_p:
-            self.u_cur[live] += mass[:, live].sum(axis=0) / c.num_q_heads
-            self._pnorm_scores(np.nonzero(live)[0])
+            self.u_cur[live_w] += mass[:, live_w].sum(axis=0) / c.num_q_heads
+            self._pnorm_scores(np.nonzero(live_w)[0])
         elif not c.key_norm:
-            self.score[live] += mass[:, live].sum(axis=0) / c.num_q_heads
+            self.score[live_w] += mass[:, live_w].sum(axis=0) / c.num_q_heads
         return out, mass, sink_mass
 
     def step(self, q, k_new, v_new):
         self.append(k_new, v_new)
         return self.attend(q)
 
-    # -- routing event (Algorithm 1) ---------------------------------------
+    # -- routing event (Sec. 4.3 candidate pool, TopK and state transitions; Algorithm 1)
     def candidates(self):
         return [int(w) for w in np.nonzero((self.state == FULL) | (self.state == QUANT)
                                            | (self.state == AGED))[0]]
@@ -589,6 +636,26 @@ class QEvictUnit:
         live = (self.state[:n] >= 0) & (self.state[:n] != EVICTED)
         self.score[:n][live] = np.asarray(scores, dtype=np.float64)[:n][live]
 
+    # What a routing event does to one candidate, by (its state before the event,
+    # the tier the ranking gives it, its ledger entry before the event; None = no
+    # entry).  The moves are those of the state diagram Full <-> Quantized ->
+    # Evicted under the write-once ledger (Sec. 4.3, migration-stable
+    # quantization and the state-transition equation; Algorithm 1 applies the
+    # same moves): codes are made once, at a window's first entry into the
+    # quantized tier, a promotion leaves them dormant and a later demotion
+    # reactivates them.  A candidate ranked below K_f + K_q is evicted whatever
+    # its state: its copies are released and its entry deleted.
+    MOVES = {
+        (FULL, FULL, None): "keep",
+        (FULL, FULL, DORMANT): "keep",
+        (QUANT, QUANT, ACTIVE): "keep",
+        (QUANT, FULL, ACTIVE): "promote",      # bf16 copy of z + s c; the entry goes dormant
+        (AGED, FULL, None): "admit",           # bf16 copy of the original tokens
+        (FULL, QUANT, None): "quantize",       # first demotion: codes from the bf16 copy
+        (AGED, QUANT, None): "quantize",       # codes from the original tokens
+        (FULL, QUANT, DORMANT): "reactivate",  # the earlier codes, no requantization
+    }
+
     def route(self):
         c = self.cfg
         cand = self.candidates()
@@ -596,46 +663,51 @@ class QEvictUnit:
         was_q = frozenset(w for w in cand if self.state[w] == QUANT)
         full, quant, evict = tier_split(order, c.capacity_full, c.capacity_quant,
                                         was_q, c.no_promotion)
-        # F: promote (dequantize, ledger dormant) or admit an aged window
-        for w in full:
-            if self.state[w] == QUANT:
+        new_tier = dict.fromkeys(full, FULL)
+        new_tier.update(dict.fromkeys(quant, QUANT))
+        new_tier.update(dict.fromkeys(evict, EVICTED))
+        # mixed widths: an entry created now takes 4 bits in the upper half of the
+        # new quantized tier (by rank), 2 below, and keeps them for its lifetime
+        q_rank = {w: r for r, w in enumerate(quant)}
+        half = -(-c.capacity_quant // 2)
+        for w in order:
+            nt = new_tier[w]
+            e = self.ledger.get(w)
+            move = "evict" if nt == EVICTED else \
+                self.MOVES[(int(self.state[w]), nt, None if e is None else e["state"])]
+            if move == "promote":
                 kh, vh = self._dequantize(w)
                 self.full_k[w] = rne_bf16(kh)
                 self.full_v[w] = rne_bf16(vh)
-                self.ledger[w]["state"] = DORMANT
+                e["state"] = DORMANT
                 self.stats["promotions"] += 1
-            elif self.state[w] == AGED:
+            elif move == "admit":
                 a, b = self.win_range(w)
                 self.full_k[w] = self.k[:, a:b].copy()
                 self.full_v[w] = self.v[:, a:b].copy()
                 self.stats["admissions_full"] += 1
-            self.state[w] = FULL
-        # Q: quantize once, or reactivate a dormant entry
-        half = -(-c.capacity_quant // 2)
-        for rank, w in enumerate(quant):
-            if w not in self.ledger:
+            elif move == "quantize":
                 if self.state[w] == FULL:
                     src_k, src_v = self.full_k[w], self.full_v[w]
                 else:
                     a, b = self.win_range(w)
                     src_k, src_v = self.k[:, a:b], self.v[:, a:b]
-                bits = c.bits if c.bits in (2, 4) else (4 if rank < half else 2)
+                bits = c.bits if c.bits in (2, 4) else (4 if q_rank[w] < half else 2)
                 self.ledger[w] = self._quantize(w, src_k, src_v, bits)
                 self.stats["first_quantizations"] += 1
                 self.quant_count += 1
-            elif self.ledger[w]["state"] == DORMANT:
-                self.ledger[w]["state"] = ACTIVE
+            elif move == "reactivate":
+                e["state"] = ACTIVE
                 self.stats["reactivations"] += 1
-            self.full_k.pop(w, None)
-            self.full_v.pop(w, None)
-            self.state[w] = QUANT
-        # E: release, delete the ledger entry
-        for w in evict:
-            self.full_k.pop(w, None)
-            self.full_v.pop(w, None)
-            self.ledger.pop(w, None)
-            self.state[w] = EVICTED
-            self.stats["evictions"] += 1
+            elif move == "evict":
+                self.ledger.pop(w, None)
+                self.stats["evictions"] += 1
+            if nt != FULL:
+                self.full_k.pop(w, None)
+                self.full_v.pop(w, None)
+            self.state[w] = nt
+            if move != "keep":
+                self._refresh(w)
         self.new_period = True
         if c.score_p:                     # the routing event closes the period
             for w in np.nonzero(self.state >= 0)[0]:
@@ -664,6 +736,7 @@ class QEvictUnit:
             e["state"] = ACTIVE
         del self.full_k[w], self.full_v[w]
         self.state[w] = QUANT
+        self._refresh(w)
 
     def promote_one(self, w: int):
         """Quantized -> Full: bf16 values from the ledger (RNE of z + s c), the
@@ -680,6 +753,7 @@ class QEvictUnit:
         self.full_v[w] = rne_bf16(vh)
         self.ledger[w]["state"] = DORMANT
         self.state[w] = FULL
+        self._refresh(w)
 
     # -- perturbation used by the forced-promotion workload -------------------
     def shift_key_zero_points(self, w: int, delta):
@@ -692,6 +766,8 @@ class QEvictUnit:
         e = self.ledger[w]
         d = np.asarray(delta, dtype=np.float32).astype(np.float64)
         e["kz"] = rne_fp16(e["kz"] + d[:, None, :])
+        if self.state[w] == QUANT:
+            self._refresh(w)
 
     # -- views used by tests -------------------------------------------------
     def tiers(self):

@@ -11,7 +11,7 @@
 import numpy as np
 import torch
 
-from oracle.qevict_oracle import (EVICTED, FULL, QUANT, OracleConfig, QEvictUnit,
+from oracle.qevict_oracle import (AGED, EVICTED, FULL, QUANT, OracleConfig, QEvictUnit,
                                   dequantize_window)
 from synthetic import bf16_bits_to_f32, f32_to_bf16_bits
 
@@ -120,3 +120,47 @@ def test_promoted_window_holds_bf16_of_dequantized_values():
     bf = ref_k.to(torch.bfloat16).to(torch.float64).numpy()
     np.testing.assert_array_equal(u.full_k[w][exact32], bf[exact32])
     assert np.all(np.abs(u.full_k[w] - kh) <= np.abs(kh) * 2.0 ** -8)
+
+
+def test_attention_copy_follows_every_tier_change():
+    """attend() reads the live rows of the oracle's attention-domain copy; along a
+    trajectory with promotions, first quantizations, reactivations, evictions,
+    admissions, manual moves and a key shift, it equals textbook attention over
+    the set accessible() assembles from the tier map, and the masses equal the
+    per-window sums of those probabilities."""
+    u, rng = _unit(hq=8, hkv=2, kf=3, kq=4, T=16 * 12 + 5, sink=5, recent=9, steps=40, seed=21)
+    kinds = set()
+    for t in range(40):
+        q = _bf16(rng, (8, 64), 1.5)
+        kn, vn = _bf16(rng, (2, 64)), _bf16(rng, (2, 64))
+        u.append(kn, vn)
+        kk, vv, owner = u.accessible()
+        ref = _sdpa(q, kk, vv, u.cfg.scale)
+        logits = np.einsum("hnd,hd->hn", np.repeat(kk, 4, axis=0), q) * u.cfg.scale
+        p = np.exp(logits - logits.max(axis=1, keepdims=True))
+        p /= p.sum(axis=1, keepdims=True)
+        out, mass, sink_mass = u.attend(q)
+        np.testing.assert_allclose(out, ref, rtol=1e-11, atol=1e-12)
+        for w in range(u.n_win_cap):
+            np.testing.assert_allclose(mass[:, w], p[:, owner == w].sum(axis=1), rtol=0, atol=1e-12)
+        np.testing.assert_allclose(sink_mass, p[:, owner < 0].sum(axis=1), rtol=0, atol=1e-12)
+        # stir the scores so that windows move both ways, then route
+        live = (u.state >= 0) & (u.state != EVICTED)
+        u.score[live] += rng.uniform(0, 0.3, size=live.sum())
+        if t % 3 == 0:
+            u.score[u.state == AGED] += 5.0      # some aged windows enter Full directly
+        before = dict(u.stats)
+        u.route()
+        kinds |= {k for k in before if u.stats[k] > before[k]}
+        if t == 10:
+            qw = np.nonzero(u.state == QUANT)[0]
+            u.shift_key_zero_points(int(qw[0]), rng.normal(size=(2, 64)).astype(np.float32))
+        if t == 20:
+            fw = np.nonzero(u.state == FULL)[0]
+            if np.sum(u.state == QUANT) < 4:
+                u.quantize_one(int(fw[0]))
+            qw = np.nonzero(u.state == QUANT)[0]
+            if np.sum(u.state == FULL) < 3:
+                u.promote_one(int(qw[0]))
+    assert {"promotions", "first_quantizations", "reactivations", "evictions",
+            "admissions_full"} <= kinds, kinds
