@@ -886,14 +886,15 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
   const float2 mr = maybe ? mref[(int64_t)pos * nh + hh] : make_float2(-INFINITY, 0.f);
   const int wl = (maybe && hh == 0) ? iwin[min(pos, G.max_fq)] : -1;   // used when pos < n_fq
   const float old_score = (maybe && hh == 0) ? iscore[pos] : 0.f;
-  // M_h, L_h: P consecutive threads per head (P a power of two, P * H_q <= 256),
-  // thread j folds splits j, j + P, j + 2P, ... (consecutive threads read
-  // consecutive rows), then a butterfly over the P lanes combines the
-  // (max, sum) pairs
+  // M_h, L_h: P consecutive threads per head (P a power of two, P * H_q <= 256,
+  // P <= 64 so that the P threads of a head sit in one wave), thread j folds
+  // splits j, j + P, j + 2P, ... (consecutive threads read consecutive rows),
+  // then a butterfly over the P lanes combines the (max, sum) pairs
   int P = 1;
-  while (2 * P * nh <= kMergeThreads) P *= 2;
+  while (2 * P * nh <= kMergeThreads && P < 64) P *= 2;
   const int C = (S + P - 1) / P;
-  constexpr int kMaxC = 32;   // C <= S * H_q / 128 <= 32 (S * H_q <= 4096, P * H_q > 128)
+  // C <= 32: with P = 64, S <= 256 splits; otherwise P * H_q > 128 and S * H_q <= 4096
+  constexpr int kMaxC = 32;
   {
     const int h = tid / P, j = tid % P;
     const bool hv = h < nh;

@@ -26,13 +26,15 @@ def _lockstep(name, **kw):
 
 
 def test_c1_forced_promotions():
-    ls = _lockstep("c1")
+    ls = _lockstep("c1", independent_seqs=[0])
     assert ls.promotions >= ls.wl.steps // ls.wl.shift_every
+    print("[lockstep] c1 independent " + "; ".join(ls.report_independent()), flush=True)
 
 
 @pytest.mark.parametrize("name", ["c1s", "c2s", "c4s", "c5s", "c3s"])
 def test_small_workloads_lockstep(name):
-    _lockstep(name)
+    ls = _lockstep(name, independent_seqs=[0])
+    print(f"[lockstep] {name} independent " + "; ".join(ls.report_independent()), flush=True)
 
 
 @pytest.mark.parametrize("name,decay", [("c2s", 0.99), ("c5s", 0.9)])
@@ -110,11 +112,13 @@ def test_short_prompts(prompt, sink, steps):
     assert ls.events == steps
 
 
-@pytest.mark.parametrize("hq,hkv", [(24, 2), (12, 4), (32, 2)])
+@pytest.mark.parametrize("hq,hkv", [(24, 2), (12, 4), (32, 2), (1, 1), (2, 1), (2, 2)])
 def test_head_layouts(hq, hkv):
     """Query-head counts that are not powers of two (the merge sums heads through
     LDS instead of a butterfly) and GQA ratios 12 and 16 (four 4-head groups per
-    wave in the attention kernel), plus GQA 3."""
+    wave in the attention kernel), plus GQA 3; one and two query heads (the
+    per-head split statistics are folded by 64 threads of one wave, and the
+    window masses must still sum to one per head)."""
     from tests.gpu_harness import Lockstep
     wl = syn.get_workload("c2s").replace(name=f"h{hq}x{hkv}", num_q_heads=hq, num_kv_heads=hkv, steps=16)
     ls = Lockstep(wl)
