@@ -7,6 +7,14 @@ quantization codes and parameters, and promoted bf16 values must then agree
 bit for bit.  Attention outputs must agree to max-abs <= 2e-3 * ||o||_2 per
 (sequence, head) row, cumulative scores to 1e-4 relative with the floor
 1e-7 * sum of scores.
+
+Independent trajectory: beside each lockstep unit, a sample of sequences also
+has an oracle unit that never adopts the GPU's scores; it routes on its own
+float64 scores.  Until its tier map first differs from the GPU's, its outputs
+and scores are held to the same bars; the first difference is recorded with
+the relative score gap between the windows that changed places (per tier
+boundary), and it must be a near-tie (gap <= 1e-4), the only way fp32 and
+float64 scores may legitimately rank windows differently.
 """
 from __future__ import annotations
 
@@ -89,7 +97,7 @@ class Lockstep:
                  flags: int = 0, num_splits: int = 0, steps: int | None = None, log=print,
                  capacity_full=None, capacity_quant=None, score_decay: float | None = None,
                  key_norm: bool = False, score_p: float | None = None, observed_init: bool = False,
-                 rope_base: float = 0.0):
+                 rope_base: float = 0.0, independent_seqs=None, progress_every: int = 0):
         self.wl, self.seed = wl, seed
         self.layer_ids = list(layer_ids)
         self.check_seqs = list(range(wl.batch)) if check_seqs is None else list(check_seqs)
@@ -108,6 +116,13 @@ class Lockstep:
         self.ocfg = oracle_config(self.cfg)
         self.units = {(li, b): QEvictUnit(self.ocfg, wl.max_context)
                       for li in range(len(self.layer_ids)) for b in self.check_seqs}
+        # independent-trajectory units (own scores, never adopted)
+        ind = [] if independent_seqs is None else list(independent_seqs)
+        assert set(ind) <= set(self.check_seqs), "independent sequences must be mirrored"
+        self.indep = {(li, b): QEvictUnit(self.ocfg, wl.max_context)
+                      for li in range(len(self.layer_ids)) for b in ind}
+        self.divergence = {}          # (li, b) -> first divergence record
+        self.progress_every = progress_every
         self.log = log
         self.inputs = {}
         self.t = 0
@@ -169,6 +184,62 @@ class Lockstep:
             assert np.all(err <= SCORE_TOL), f"score rel err {err.max():.3e} at window {np.argmax(err)}"
         return st
 
+    def check_scores(self, u, st, what):
+        n = st["n"]
+        live = (u.state[:n] >= 0) & (u.state[:n] != 4)
+        so = u.score[:n][live]
+        sg = st["scores"][live].astype(np.float64)
+        floor = 1e-7 * np.abs(so).sum()
+        err = np.abs(sg - so) / np.maximum(np.abs(so), floor)
+        assert np.all(err <= SCORE_TOL), f"{what}: score rel err {err.max():.3e}"
+
+    def compare_masses(self, got, mass, sink, u, t, b):
+        """Per-head window masses of the step (the score increments before the
+        head average): 1e-4 relative, floor 1e-7 (a head's masses sum to 1)."""
+        n = min(u.n_win_cap, got.shape[1] - 1)
+        ref = mass[:, :n]
+        err = np.abs(got[:, :n].astype(np.float64) - ref) / np.maximum(np.abs(ref), 1e-7)
+        assert np.all(err <= SCORE_TOL), \
+            f"step {t} seq {b}: window mass rel err {err.max():.3e} (head, window " \
+            f"{np.unravel_index(np.argmax(err), err.shape)})"
+        tot = got[:, :n].astype(np.float64).sum(axis=1) + got[:, -1]
+        assert np.all(np.abs(tot - 1.0) <= 1e-5), f"step {t} seq {b}: head masses sum to {tot}"
+
+    def check_independent(self, li, b, pre_scores, where, st=None):
+        """Tier maps (and bit widths) of the GPU and the independent unit after a
+        routing event; the first difference is recorded and must be a near-tie."""
+        ui = self.indep[(li, b)]
+        if st is None:
+            st = self.cache.get_state(li, b)
+        n = st["n"]
+        tg, ti = st["tiers"], abi_tiers(ui, n)
+        bg = st["bits"][:n].astype(np.int64)
+        bi = np.zeros(n, np.int64)
+        for w, e in ui.ledger.items():
+            if w < n:
+                bi[w] = e["bits"]
+        quant = tg == qv.TIER_QUANT
+        diff = np.nonzero((tg != ti) | (quant & (ti == qv.TIER_QUANT) & (bg != bi)))[0]
+        if len(diff) == 0:
+            assert np.array_equal(st["ledger"], ui.ledger_states()[:n]), \
+                f"independent ledger states at {where} (tiers agree)"
+            return
+        sc = ui.score if pre_scores is None else pre_scores
+        groups = {}
+        for w in diff:
+            pair = tuple(sorted((int(tg[w]), int(ti[w]))))
+            key = "bits" if pair[0] == pair[1] else {(2, 3): "full/quant", (3, 4): "quant/evict",
+                                                     (2, 4): "full/evict"}.get(pair, str(pair))
+            groups.setdefault(key, []).append(float(sc[w]))
+        gaps = {k: (max(v) - min(v)) / max(abs(x) for x in v) if len(v) > 1 else float("inf")
+                for k, v in groups.items()}
+        self.divergence[(li, b)] = dict(where=where, n_windows=int(len(diff)),
+                                        gaps={k: f"{g:.2e}" for k, g in gaps.items()})
+        self.log(f"[lockstep] independent layer {li} seq {b}: first divergence at {where}, "
+                 f"windows {diff[:8].tolist()}, relative score gaps {gaps}")
+        assert all(g <= SCORE_TOL for g in gaps.values()), \
+            f"independent run diverged at {where} without a near-tie: gaps {gaps}"
+
     # ---- phases ------------------------------------------------------------
     def prefill(self):
         wl = self.wl
@@ -204,6 +275,8 @@ class Lockstep:
                     # key-norm and p-norm prompt scores: the GPU computes its own
                     self.units[(li, b)].prefill(from_bf16_bits(ks[b]), from_bf16_bits(vs[b]), inits[b],
                                                 route=not self.gpu_prompt_scores)
+                if (li, b) in self.indep:
+                    self.indep[(li, b)].prefill(from_bf16_bits(ks[b]), from_bf16_bits(vs[b]), inits[b])
             self.cache.prefill_assign(li, K, V, S)
             torch.cuda.synchronize()
             del K, V
@@ -222,6 +295,8 @@ class Lockstep:
                 self.compare_state(li, b)
                 self.compare_memory(li, b)
                 self.compare_ledgers(li, b, sorted(u.ledger))
+                if (li, b) in self.indep:
+                    self.check_independent(li, b, None, "prefill")
                 full = [w for w in range(u.n_win_cap) if u.state[w] == 2]
                 self.compare_full(li, b, full[:: max(1, len(full) // 16)])
 
@@ -239,6 +314,8 @@ class Lockstep:
             self.cache.debug_shift_keys(li, b, w, delta)
             if (li, b) in self.units:
                 self.units[(li, b)].shift_key_zero_points(w, delta)
+            if (li, b) in self.indep and (li, b) not in self.divergence:
+                self.indep[(li, b)].shift_key_zero_points(w, delta)
 
     def step(self):
         wl, t = self.wl, self.t
@@ -253,6 +330,8 @@ class Lockstep:
             out = torch.empty((B, Hq, d), dtype=torch.float32, device="cuda")
             self.cache.decode_attend(li, to_dev_bf16(qs), to_dev_bf16(kn), to_dev_bf16(vn), out)
             out = out.cpu().numpy()
+            gm = self.cache.debug_masses(li)
+            pre_scores = {}
             for b in self.check_seqs:
                 u = self.units[(li, b)]
                 o, mass, sink = u.step(from_bf16_bits(qs[b]), from_bf16_bits(kn[b]),
@@ -260,9 +339,18 @@ class Lockstep:
                 err = np.abs(out[b] - o).max(axis=1) / np.linalg.norm(o, axis=1)
                 self.max_out_err = max(self.max_out_err, float(err.max()))
                 assert np.all(err <= OUT_TOL), f"step {t} seq {b}: out rel err {err.max():.3e}"
+                if not self.key_norm:
+                    self.compare_masses(gm[b], mass, sink, u, t, b)
                 st = self.compare_state(li, b)
+                pre_scores[b] = st["scores"].astype(np.float64)
                 if routing:
-                    u.adopt_scores(st["scores"].astype(np.float64))
+                    u.adopt_scores(pre_scores[b])
+                if (li, b) in self.indep and (li, b) not in self.divergence:
+                    ui = self.indep[(li, b)]
+                    oi, _, _ = ui.step(from_bf16_bits(qs[b]), from_bf16_bits(kn[b]), from_bf16_bits(vn[b]))
+                    erri = np.abs(out[b] - oi).max(axis=1) / np.linalg.norm(oi, axis=1)
+                    assert np.all(erri <= OUT_TOL), f"independent step {t} seq {b}: out rel err {erri.max():.3e}"
+                    self.check_scores(ui, st, f"independent step {t} seq {b}")
             if routing:
                 stats = self.cache.retier(li, stats=True)
                 self.events += 1
@@ -283,13 +371,33 @@ class Lockstep:
                     self.compare_full(li, b, promoted + admitted)
                     for w in promoted:
                         assert u.ledger[w]["state"] == DORMANT
+                    if (li, b) in self.indep and (li, b) not in self.divergence:
+                        ui = self.indep[(li, b)]
+                        pre = ui.score.copy()
+                        ui.route()
+                        self.check_independent(li, b, pre, f"step {t}", st)
         self.t += 1
+        if self.progress_every and self.t % self.progress_every == 0:
+            self.log(f"[lockstep] {self.wl.name}: step {self.t}/{self.steps}, max out err "
+                     f"{self.max_out_err:.2e}, max score err {self.max_score_err:.2e}, "
+                     f"promotions {self.promotions}, diverged {sorted(self.divergence)}")
 
     def run(self):
         self.prefill()
         for _ in range(self.steps):
             self.step()
         return self
+
+    def report_independent(self):
+        """One line per independent unit: no divergence, or its first divergence."""
+        lines = []
+        for key in sorted(self.indep):
+            d = self.divergence.get(key)
+            lines.append(f"layer {key[0]} seq {key[1]}: " +
+                         ("no divergence" if d is None else
+                          f"first divergence at {d['where']}: {d['n_windows']} windows, "
+                          f"boundaries {d['gaps']}"))
+        return lines
 
     def close(self):
         self.cache.close()
