@@ -16,7 +16,9 @@
  *  - Tensor arguments are HIP device pointers to contiguous row-major data
  *    unless a comment says "host".  bf16 values are passed as uint16_t bit
  *    patterns.  The caller owns every buffer; the library never allocates or
- *    frees device memory: all state lives in the caller's workspace.
+ *    frees device memory: all state lives in the caller's workspace (the one
+ *    exception is the fixed per-device scratch array behind
+ *    qevict_prefill_scores_noalloc, part of the library's code object).
  *  - Each buffer must hold the full extent its comment gives, with B, H_q,
  *    H_kv and d taken from the configuration: the kernels read and write
  *    whole extents and cannot check a buffer's size (null pointers and
@@ -253,6 +255,25 @@ qevict_status qevict_prefill_scores_scratch_size(const qevict_config *cfg, int32
 qevict_status qevict_prefill_scores(qevict_cache *c, const uint16_t *q_obs, int32_t n_obs,
                                     const uint16_t *k, int32_t prompt_len, void *scratch,
                                     size_t scratch_bytes, float *scores);
+
+/* The same initial window scores without a caller scratch buffer, for callers
+ * that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation).  The three kernels of
+ * qevict_prefill_scores run on a fixed scratch array that the library keeps
+ * in device memory, one per device, for the life of the process
+ * (QEVICT_STATIC_SCRATCH_BYTES = 16 MiB, enough for a batch-1 32K-token prompt
+ * with 32 observation queries at 8 KV heads and GQA 4); its address on the
+ * device current at qevict_cache_init is looked up then.  This call allocates
+ * nothing.  Arguments and results are those of qevict_prefill_scores (bitwise
+ * the same scores).  Fails with QEVICT_ERR_WORKSPACE, enqueuing nothing, when
+ * the prompt needs more scratch than the array holds
+ * (qevict_prefill_scores_scratch_size tells).  Every call on one device shares
+ * that device's array, which keeps the last call's contents (every entry a
+ * call reads is written by the same call first): calls that overlap on one
+ * device, on different streams or from different threads, race. */
+#define QEVICT_STATIC_SCRATCH_BYTES (16u << 20)
+qevict_status qevict_prefill_scores_noalloc(qevict_cache *c, const uint16_t *q_obs, int32_t n_obs,
+                                            const uint16_t *k, int32_t prompt_len, float *scores);
 
 /* One decode step of one layer (Sec. 4.1 decode attention; Sec. 4.2 score).
  *   q      [B, H_q, d]  bf16 queries

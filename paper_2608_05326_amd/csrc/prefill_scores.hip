@@ -24,9 +24,41 @@
 // over the lanes l, l ^ 16, l ^ 32, l ^ 48.  Each wave owns one chunk (its A operands
 // stay in registers for every row); the query rows are staged in LDS, 128 at
 // a time.
+#include <mutex>
+
 #include "qv_device.h"
 
 namespace qv {
+
+// Fixed scratch of the allocation-free entry point (qevict_prefill_scores_noalloc):
+// every device the library runs on holds one copy for the life of the process.
+// Host code never uses this name as an address: the per-device address comes
+// from static_obs_scratch(), looked up once per device at cache creation.
+static __device__ __align__(256) uint8_t scratch[kStaticObsScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// Device address of `scratch` on the current device (looked up on the first
+// call for that device, with it current).
+hipError_t static_obs_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 constexpr int kObsChunkKeys = 64;      // keys per wave
 constexpr int kObsRows = 128;          // query rows staged in LDS at once

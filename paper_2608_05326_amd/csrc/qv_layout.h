@@ -73,6 +73,8 @@ constexpr int kQEntry = 6;
 constexpr int kSpareFull = 8;
 // sink windows per sequence (keeps the attention split costs in 32 bits)
 constexpr int kMaxSinkWindows = 64;
+// bytes of the fixed per-device scratch of the allocation-free initial-score call
+constexpr int64_t kStaticObsScratchBytes = 16LL << 20;
 
 constexpr int kScorePnorm = 3;   // score_mode of the attention p-norm ranking
 

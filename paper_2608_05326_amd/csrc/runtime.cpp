@@ -35,10 +35,12 @@ hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st);
 hipError_t launch_key_norm_init(const KeyNormArgs& a, hipStream_t st);
 hipError_t launch_score_pow(const ScorePowArgs& a, hipStream_t st);
 hipError_t launch_prefill_scores(const ObsArgs& a, hipStream_t st);
+hipError_t static_obs_scratch(void** ptr);
 }  // namespace qv
 
 using namespace qv;
 static_assert(kScorePnorm == QEVICT_SCORE_PNORM, "score mode numbering");
+static_assert(kStaticObsScratchBytes == QEVICT_STATIC_SCRATCH_BYTES, "fixed scratch size");
 
 namespace {
 
@@ -88,6 +90,7 @@ struct qevict_cache {
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
   hipStream_t stream = nullptr;
+  void* static_scratch = nullptr;           // this device's fixed initial-score scratch
   // Asynchronous routing (QEVICT_FLAG_ASYNC_ROUTING): routing requests are queued
   // and launched on rstream in batches of route_batch layers, behind one wait
   // for the cache stream; a cross-stream wait costs the host far more than a
@@ -557,6 +560,8 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
       return hip_fail(e, "creating the routing stream");
     }
   }
+  // the fixed scratch of qevict_prefill_scores_noalloc on this (the current) device
+  if (e == hipSuccess) e = static_obs_scratch(&c->static_scratch);
   if (e == hipSuccess && cfg->rope_base > 0.f) {
     float* tab = (float*)(c->ws + kHeaderBytes + (int64_t)cfg->num_layers * cfg->batch * c->L.unit_bytes +
                           score_staging_bytes(cfg, c->g));
@@ -703,9 +708,9 @@ qevict_status qevict_prefill_scores_scratch_size(const qevict_config* cfg, int32
   return QEVICT_OK;
 }
 
-qevict_status qevict_prefill_scores(qevict_cache* c, const uint16_t* q_obs, int32_t n_obs,
-                                    const uint16_t* k, int32_t prompt_len, void* scratch,
-                                    size_t scratch_bytes, float* scores) {
+static qevict_status prefill_scores_impl(qevict_cache* c, const uint16_t* q_obs, int32_t n_obs,
+                                         const uint16_t* k, int32_t prompt_len, void* scratch,
+                                         size_t scratch_bytes, float* scores) {
   if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache handle is NULL");
   const qevict_config& cfg = c->cfg;
   qevict_status s = obs_check(&cfg, prompt_len, n_obs);
@@ -748,6 +753,28 @@ qevict_status qevict_prefill_scores(qevict_cache* c, const uint16_t* q_obs, int3
   const hipError_t e = timed(c, 4, c->stream, [&] { return launch_prefill_scores(a, c->stream); });
   if (e != hipSuccess) return hip_fail(e, "prefill_scores launch");
   return QEVICT_OK;
+}
+
+qevict_status qevict_prefill_scores(qevict_cache* c, const uint16_t* q_obs, int32_t n_obs,
+                                    const uint16_t* k, int32_t prompt_len, void* scratch,
+                                    size_t scratch_bytes, float* scores) {
+  return prefill_scores_impl(c, q_obs, n_obs, k, prompt_len, scratch, scratch_bytes, scores);
+}
+
+qevict_status qevict_prefill_scores_noalloc(qevict_cache* c, const uint16_t* q_obs, int32_t n_obs,
+                                            const uint16_t* k, int32_t prompt_len, float* scores) {
+  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache handle is NULL");
+  qevict_status s = obs_check(&c->cfg, prompt_len, n_obs);
+  if (s) return s;
+  const int64_t need = obs_scratch(&c->cfg, prompt_len, n_obs).bytes;
+  if (need > kStaticObsScratchBytes)
+    return fail(QEVICT_ERR_WORKSPACE,
+                "this prompt needs %lld bytes of scratch; the fixed scratch holds %lld "
+                "(use qevict_prefill_scores with a caller buffer)",
+                (long long)need, (long long)kStaticObsScratchBytes);
+  if (!c->static_scratch) return fail(QEVICT_ERR_DEVICE, "fixed scratch not available on this device");
+  return prefill_scores_impl(c, q_obs, n_obs, k, prompt_len, c->static_scratch,
+                             (size_t)kStaticObsScratchBytes, scores);
 }
 
 qevict_status qevict_decode_attend(qevict_cache* c, int32_t layer, const uint16_t* q,

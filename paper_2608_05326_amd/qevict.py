@@ -36,6 +36,7 @@ SYMBOLS = (
     "qevict_profile_enable", "qevict_profile_read", "qevict_last_attend_bytes", "qevict_join_routing",
     "qevict_status_string", "qevict_last_error", "qevict_prefill_scores_scratch_size",
     "qevict_prefill_scores", "qevict_capacities_for_budget", "qevict_memory_report",
+    "qevict_prefill_scores_noalloc",
 )
 
 
@@ -142,6 +143,7 @@ def load_library(path: str | None = None):
         "qevict_prefill_scores": [vp, vp, i32, vp, i32, vp, ctypes.c_size_t, vp],
         "qevict_capacities_for_budget": [P(_Config), i64, i32, P(i32), P(i32)],
         "qevict_memory_report": [vp, i32, i32, P(MemoryReport)],
+        "qevict_prefill_scores_noalloc": [vp, vp, i32, vp, i32, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -273,6 +275,23 @@ class Cache:
             self.handle, _ptr(q_obs, t.bfloat16, "q_obs"), n_obs, _ptr(k, t.bfloat16, "k"), T,
             _ptr(scratch, None, "scratch"), scratch.numel() * scratch.element_size(),
             _ptr(scores, t.float32, "scores") if n_w else None))
+        return scores
+
+    def prefill_scores_noalloc(self, q_obs, k, scores):
+        """qevict_prefill_scores on the library's fixed per-device scratch (no
+        scratch argument; the call allocates nothing).  q_obs: bf16
+        [B, H_q, n_obs, d]; k: bf16 [B, H_kv, T, d]; scores: float32 [B, n_w]."""
+        t = self.torch
+        cfg = self.cfg
+        B, n_obs, T = cfg.batch, q_obs.shape[2], k.shape[2]
+        if tuple(q_obs.shape) != (B, cfg.num_q_heads, n_obs, cfg.head_dim):
+            raise ValueError(f"q_obs shape {tuple(q_obs.shape)}")
+        if tuple(k.shape) != (B, cfg.num_kv_heads, T, cfg.head_dim):
+            raise ValueError(f"k shape {tuple(k.shape)}")
+        n_w = max(0, -(-(T - cfg.sink_tokens) // cfg.window_tokens))
+        self._c(self.lib.qevict_prefill_scores_noalloc(
+            self.handle, _ptr(q_obs, t.bfloat16, "q_obs"), n_obs, _ptr(k, t.bfloat16, "k"), T,
+            _ptr(scores, t.float32, "scores", (B, n_w)) if n_w else None))
         return scores
 
     def memory_report(self, layer: int, seq: int) -> dict:
