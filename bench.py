@@ -16,18 +16,27 @@ routing work runs on the library's routing stream (QEVICT_FLAG_ASYNC_ROUTING),
 overlapping the attention of the following layers; --routing sync keeps every
 kernel on one stream.
 
-Prints one JSON line.  `value` is microseconds per step (lower is better);
-`roofline` reports decode_attend's algorithmic bytes per call over its average
-duration, measured with HIP events on the cache's stream around rounds of 16
-back-to-back decode_attend calls with no routing running; `roofline.traffic`
-is the HBM traffic per call from the committed FETCH_SIZE / WRITE_SIZE record
-over the same duration (null when the sources of the attention path changed
-since it was taken, and on any run other than the default one it covers).
+Prints one JSON line.  `value` is microseconds per step (lower is better):
+the GPU time of the K timed steps on the cache's stream (HIP events), taken
+in steady state -- the routing requests the warm-up left queued run inside the
+timed region, and those still queued when it closes are drained after it and
+reported as `routing_tail_us` -- divided by K.  `roofline` reports
+decode_attend's algorithmic bytes per call over its average duration (the
+attention pass and the split merge), measured with HIP events on the cache's
+stream around rounds of back-to-back decode_attend calls with no routing
+running; `roofline.traffic` is the HBM traffic per call from the committed
+FETCH_SIZE / WRITE_SIZE record over the same duration (null when the sources
+of the attention path changed since it was taken, and on any run other than
+the default one it covers).  Initial window scores come from the prompt's last
+W queries attending to the prompt (qevict_prefill_scores); its time per layer
+is reported as `prefill_scores_us_per_layer`.
 
 `--workload` runs another synthetic shape instead (all sequences of its batch,
 byte-budget capacities where it gives a budget, a routing event after every
 R-th step of a cache at its routing interval R); such runs are context, not
-the benchmark line.
+the benchmark line.  The 32-layer batch-8 workload runs its 32 layers back to
+back per decode step: `value` is then microseconds per decode step of the
+whole model.
 """
 from __future__ import annotations
 
@@ -68,6 +77,9 @@ def parse():
                    help="RoPE-aware Quantized tier with this base (0: off, the default workload)")
     p.add_argument("--prefill-scores", action="store_true",
                    help="time the initial-window-score kernels on the workload's prompt instead")
+    p.add_argument("--init-scores", choices=("prompt", "synthetic"), default="prompt",
+                   help="initial window scores: prompt attention of the last W prompt queries "
+                        "(qevict_prefill_scores, the default), or the synthetic log-normal scores")
     p.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MB",
                    help="only run 8 plain device-to-device copies of this many MB (hardware "
                         "counter calibration) and exit")
@@ -105,7 +117,8 @@ def workload_desc(wl):
     bits = {4: "int4", 2: "int2", 42: "int4 / int2 by rank"}[wl.bits]
     tiers = (f"byte budget {wl.budget_frac} of the full cache, quantized share {wl.q_frac}"
              if wl.budget_frac else f"{wl.frac_full} bf16 / {wl.frac_quant} quantized")
-    return (f"{wl.prompt_len}-token context, batch {wl.batch}, {wl.num_q_heads} query / "
+    layers = f"{wl.layers} layers back to back per step, " if wl.layers > 1 else ""
+    return (f"{layers}{wl.prompt_len}-token context, batch {wl.batch}, {wl.num_q_heads} query / "
             f"{wl.num_kv_heads} KV heads, head_dim {wl.head_dim}, windows of {wl.window}, {bits} "
             f"group {wl.group}, {tiers}, sink {wl.sink}, recent {wl.recent}, "
             + ("re-tier every step" if wl.retier_interval == 1 else f"re-tier every {wl.retier_interval} steps"))
@@ -171,13 +184,23 @@ def blas_threads():
         return 1
 
 
-def cpu_baseline(wl, seed, budget_s):
-    """The float64 oracle stepping one sequence-layer of the same workload."""
+def cpu_baseline(wl, seed, budget_s, units_per_step=1):
+    """The float64 oracle stepping one sequence-layer of the same workload (append,
+    attention and score accumulation every step, routing at the workload's
+    interval).  A step of a workload with several sequences or layers is
+    `units_per_step` such unit steps: the time of one is scaled by that count."""
     from oracle.qevict_oracle import OracleConfig, QEvictUnit
     import synthetic as syn
     cores = blas_threads()
+    kf, kq = wl.capacity_full, wl.capacity_quant
+    if wl.budget_frac:
+        from oracle.qevict_oracle import tier_capacities
+        full = 2 * wl.num_kv_heads * wl.head_dim * wl.prompt_len * 2
+        kf, kq = tier_capacities(int(Fraction(wl.budget_frac) * full), int(Fraction(wl.q_frac) * 1000),
+                                 wl.num_kv_heads, wl.head_dim, wl.window, wl.group, wl.bits,
+                                 wl.sink, wl.recent)
     cfg = OracleConfig(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, wl.group, wl.bits,
-                       wl.capacity_full, wl.capacity_quant)
+                       kf, kq, sink=wl.sink, recent=wl.recent)
     u = QEvictUnit(cfg, wl.max_context)
     k, v = syn.prompt_kv(wl, seed, 0, 0)
     f = syn.bf16_bits_to_f32
@@ -188,12 +211,17 @@ def cpu_baseline(wl, seed, budget_s):
     t0 = time.perf_counter()
     while n < wl.steps and (n < 3 or time.perf_counter() - t0 < budget_s):
         u.step(f(qs[n]).astype(np.float64), f(ks[n]).astype(np.float64), f(vs[n]).astype(np.float64))
-        u.route()
+        if (n + 1) % wl.retier_interval == 0:
+            u.route()
         n += 1
     dt = time.perf_counter() - t0
-    return {"value": round(dt / n * 1e6, 1), "unit": "us/step", "cores": cores, "kind": "oracle",
-            "sample": f"{n} decode steps (attend + score + route) of one 32K-context layer after "
-                      f"prefill, float64 numpy, {dt:.1f} s"}
+    per = dt / n * 1e6 * units_per_step
+    sample = (f"{n} decode steps (attend + score + route every {wl.retier_interval}) of one "
+              f"{wl.prompt_len}-token sequence-layer after prefill, float64 numpy, {dt:.1f} s")
+    if units_per_step > 1:
+        sample += f"; times {units_per_step} sequence-layers per step (extrapolated)"
+    return {"value": round(per, 1), "unit": "us/step", "cores": cores, "kind": "oracle",
+            "sample": sample}
 
 
 def bench_prefill_scores(args):
@@ -269,6 +297,19 @@ def bench_prefill_scores(args):
     return 0
 
 
+def host_cpu():
+    """Host CPU model name and logical CPU count."""
+    model = None
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model, os.cpu_count()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -285,9 +326,15 @@ def main():
     import synthetic as syn
 
     wl = syn.get_workload(args.workload)
-    NL = args.instances
-    # + four rounds of attention timing and two of routing statistics after the timed steps
-    per_layer = -(-(args.warmup + args.steps) // NL) + 7
+    # A workload of several layers (the 32-layer batch-8 one) runs all of them back
+    # to back per decode step; a single-layer workload rotates `instances`
+    # independent layer caches, one layer call per step.
+    whole_model = wl.layers > 1
+    NL = wl.layers if whole_model else args.instances
+    LPS = NL if whole_model else 1                 # layer calls per step
+    prof_rounds = 4                   # rounds of back-to-back decode_attend timing
+    # + the attention and routing timing rounds and two rounds of routing statistics
+    per_layer = -(-((args.warmup + args.steps) * LPS) // NL) + prof_rounds + 2 + 2 + 1
     asyncr = args.routing == "async"
     R = wl.retier_interval            # routing event after every R-th step of a layer cache
     kf, kq = wl.capacity_full, wl.capacity_quant
@@ -310,23 +357,48 @@ def main():
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)
     cache = qv.Cache(cfg, stream=stream)
-    print(f"[bench] workspace {cache.workspace.numel() / 1e6:.1f} MB for {NL} layer caches",
-          file=sys.stderr, flush=True)
+    print(f"[bench] workspace {cache.workspace.numel() / 1e6:.1f} MB for {NL} layer caches of "
+          f"batch {wl.batch}", file=sys.stderr, flush=True)
 
-    # ---- prefill every layer cache (prompt generated on the host, in parallel) ----
+    # ---- prefill every layer cache; initial window scores from the prompt's last
+    # W queries attending to the prompt (qevict_prefill_scores), unless asked for
+    # the synthetic scores ----
+    observed = args.init_scores == "prompt"
+    n_obs = wl.window
+
     def gen(layer):
         kv = [syn.prompt_kv(wl, args.seed, b, layer) for b in range(wl.batch)]
-        init = np.stack([syn.init_scores(wl, args.seed, b, layer) for b in range(wl.batch)])
+        if observed:
+            init = np.stack([syn.observation_queries(wl, args.seed, b, layer, n_obs)
+                             for b in range(wl.batch)])
+        else:
+            init = np.stack([syn.init_scores(wl, args.seed, b, layer) for b in range(wl.batch)])
         return layer, np.stack([x[0] for x in kv]), np.stack([x[1] for x in kv]), init
 
     t0 = time.time()
+    ps_ms = []
+    scratch = None
     with ThreadPoolExecutor(max_workers=8) as ex:
         for layer, k, v, init in ex.map(gen, range(NL)):
             K, V = to_dev(k), to_dev(v)                  # [B, H_kv, T, d]
-            S = torch.from_numpy(np.ascontiguousarray(init)).cuda()
+            if observed:
+                Qo = to_dev(init)                        # [B, H_q, n_obs, d]
+                if scratch is None:
+                    scratch = torch.empty(qv.qevict.prefill_scores_scratch_size(cfg, wl.prompt_len, n_obs),
+                                          dtype=torch.uint8, device="cuda")
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                S = cache.prefill_scores(Qo, K, scratch=scratch)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ps_ms.append(e0.elapsed_time(e1))
+                del Qo
+            else:
+                S = torch.from_numpy(np.ascontiguousarray(init)).cuda()
             cache.prefill_assign(layer, K, V, S)
             torch.cuda.synchronize()
             del K, V, S
+    del scratch
     print(f"[bench] prefilled {NL} layers in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
 
     # ---- per-step inputs, resident on the GPU before timing ----
@@ -335,6 +407,7 @@ def main():
     Q = [to_dev(np.stack([x[0] for x in d], axis=1)) for d in dec]     # [steps, B, H_q, d]
     KN = [to_dev(np.stack([x[1] for x in d], axis=1)) for d in dec]
     VN = [to_dev(np.stack([x[2] for x in d], axis=1)) for d in dec]
+    del dec
     # the decode calls below pass raw pointers: check every extent on the host first
     for l in range(NL):
         assert tuple(Q[l].shape) == (per_layer, wl.batch, wl.num_q_heads, wl.head_dim), Q[l].shape
@@ -362,57 +435,58 @@ def main():
         if lib.qevict_retier(h, layer, None):
             raise RuntimeError(lib.qevict_last_error().decode())
 
-    # A step is one layer cache's decode_attend followed (before that cache is
-    # used again) by its retier; steps cycle over the layer caches.  With
-    # synchronous routing the steps run in rounds -- the decode_attend of every
-    # cache, then the retier of each -- so one pair of events brackets the
-    # back-to-back attention calls of a round.
-    def run_steps(first, count, events=None):
+    # A layer call is one layer cache's decode_attend followed (before that cache is
+    # used again) by its retier; layer calls cycle over the caches.  With
+    # asynchronous routing the retier goes to the library's routing stream and the
+    # next layer's attention proceeds; with synchronous routing the calls run in
+    # rounds (the decode_attend of every cache, then the retier of each).
+    def run_calls(first, count):
         i = first
         while i < first + count:
             layers = [(i + k) % NL for k in range(min(NL - i % NL, first + count - i))]
-            if asyncr and events is None:
+            if asyncr:
                 for l in layers:
                     attend(l)
                     route(l)
             else:
-                if events is not None:
-                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    e0.record(stream)
                 for l in layers:
                     attend(l)
-                if events is not None:
-                    e1.record(stream)
-                    events.append((e0, e1, len(layers)))
                 for l in layers:
                     route(l)
             i += len(layers)
 
-    run_steps(0, args.warmup)
-    cache.join_routing()
+    run_calls(0, args.warmup * LPS)
     torch.cuda.synchronize()
     st0 = [[cache.get_state(l, b) for b in range(wl.batch)] for l in range(NL)]
 
-    # ---- timed region ----
+    # ---- timed region: K steps in steady state.  Routing requests still queued
+    # when it closes (asynchronous routing) are drained after it and reported
+    # apart; the requests queued by the warm-up run inside it. ----
     torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    attn_events = []
     ev0.record(stream)
     t_wall = time.perf_counter()
-    run_steps(args.warmup, args.steps, None if (asyncr or args.no_kernel_events) else attn_events)
-    cache.join_routing()
+    run_calls(args.warmup * LPS, args.steps * LPS)
     ev1.record(stream)
-    torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
+    torch.cuda.synchronize()
     gpu_ms = ev0.elapsed_time(ev1)
     ms_per_step = gpu_ms / args.steps
-    done = args.warmup + args.steps
+    d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    d0.record(stream)
+    cache.join_routing()
+    d1.record(stream)
+    torch.cuda.synchronize()
+    drain_us = d0.elapsed_time(d1) * 1e3
+    done = (args.warmup + args.steps) * LPS
 
-    # ---- attention timing with asynchronous routing: rounds of back-to-back
-    # decode_attend calls with no routing running beside them (each round starts
-    # after the previous round's routing and routes only after its attention) ----
-    if asyncr and not args.no_kernel_events:
-        for _ in range(4):
+    # ---- decode_attend timing: rounds of NL back-to-back calls (one per layer
+    # cache) bracketed by HIP events on the cache's stream, with no routing
+    # running beside them (each round starts after the previous round's routing
+    # and routes only after its attention) ----
+    attn_events = []
+    if not args.no_kernel_events:
+        for _ in range(max(1, prof_rounds)):
             cache.join_routing()
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -420,16 +494,28 @@ def main():
             for l in range(NL):
                 attend(l)
             e1.record(stream)
-            attn_events.append((e0, e1, NL))
             torch.cuda.synchronize()
+            attn_events.append((e0.elapsed_time(e1), NL))
             for l in range(NL):
                 route(l)
             done += NL
         cache.join_routing()
         torch.cuda.synchronize()
-    attend_us = None
-    if attn_events:
-        attend_us = sum(a.elapsed_time(b) for a, b, _ in attn_events) * 1e3 / sum(n for _, _, n in attn_events)
+    # ---- routing kernels: HIP events around every re-rank and migration launch
+    # (the library's profile counters, on the stream each runs on) over a few
+    # more rounds; each such duration also holds the launch's dispatch ----
+    lp = None
+    if not args.no_kernel_events:
+        cache.profile_enable(True)
+        for _ in range(2):
+            for l in range(NL):
+                attend(l)
+                route(l)
+            done += NL
+        cache.join_routing()
+        torch.cuda.synchronize()
+        lp = {k: cache.profile_read(k) for k in (2, 3)}
+        cache.profile_enable(False)
 
     # ---- routing activity: two more (untimed) rounds with the retier stats read back ----
     promo = react = evict = 0
@@ -438,15 +524,16 @@ def main():
         for l in range(NL):
             attend(l)
         for l in range(NL):
-            s_ = cache.retier(l, stats=True)
-            promo += s_["promotions"]
-            react += s_["reactivations"]
-            evict += s_["evictions"]
-            n_ev += 1
+            if counter[l] % R == 0:
+                s_ = cache.retier(l, stats=True)
+                promo += s_["promotions"]
+                react += s_["reactivations"]
+                evict += s_["evictions"]
+                n_ev += 1
 
     # ---- algorithmic bytes of the timed attention launches ----
     total_bytes = 0
-    for i in range(args.warmup, args.warmup + args.steps):
+    for i in range(args.warmup * LPS, (args.warmup + args.steps) * LPS):
         layer = i % NL
         T = wl.prompt_len + (i // NL) + 1
         recent = (T - wl.sink) - ((T - wl.sink) // wl.window) * wl.window
@@ -456,8 +543,10 @@ def main():
             bits = st["bits"][st["tiers"] == qv.TIER_QUANT]
             total_bytes += attend_bytes(wl, n_full, int(np.sum(bits == 4)), int(np.sum(bits == 2)),
                                         recent)
+    bytes_per_call = total_bytes / (args.steps * LPS)
     bytes_per_step = total_bytes / args.steps
 
+    cpu_model, n_cpu = host_cpu()
     res = {
         "metric": METRIC,
         "value": round(ms_per_step * 1e3, 3),
@@ -472,18 +561,37 @@ def main():
         "dtype": "bf16+" + {4: "int4", 2: "int2", 42: "int4/int2"}[wl.bits] + " (fp32 accumulate)",
         "data": "synthetic",
         "config": {"workload": workload_desc(wl),
-                   "layer_caches_rotated": NL, "global_batch": wl.batch, "seq_len": wl.prompt_len,
-                   "routing": args.routing, "routing_interval": R, "rope_base": args.rope_base,
+                   "layer_caches": NL, "layer_calls_per_step": LPS, "global_batch": wl.batch,
+                   "seq_len": wl.prompt_len, "routing": args.routing, "routing_interval": R,
+                   "init_scores": "prompt attention (qevict_prefill_scores, W observation queries)"
+                   if observed else "synthetic", "rope_base": args.rope_base,
                    "parallelism": "single GPU"},
         "step_GBps": round(bytes_per_step / (ms_per_step * 1e-3) / 1e9, 1),
         "algorithmic_MB_per_step": round(bytes_per_step / 1e6, 3),
         "host_wall_us_per_step": round(wall / args.steps * 1e6, 2),
-        "attend_us_per_launch": round(attend_us, 3) if attend_us else None,
-        "routing_per_step": {"promotions": round(promo / n_ev, 2), "reactivations": round(react / n_ev, 2),
-                             "evictions": round(evict / n_ev, 2)},
+        "routing_tail_us": round(drain_us, 1),
+        # moves per routing event of one sequence-layer (an event every R steps)
+        "routing_per_event": {"promotions": round(promo / max(n_ev * wl.batch, 1), 2),
+                              "reactivations": round(react / max(n_ev * wl.batch, 1), 2),
+                              "evictions": round(evict / max(n_ev * wl.batch, 1), 2)},
     }
-    if attend_us:
-        ach = bytes_per_step / (attend_us * 1e-6) / 1e9
+    if ps_ms:
+        res["prefill_scores_us_per_layer"] = round(sum(ps_ms[1:] or ps_ms) / len(ps_ms[1:] or ps_ms) * 1e3, 1)
+    if lp:
+        per = {k: (lp[k][0] * 1e3 / lp[k][1] if lp[k][1] else None) for k in lp}
+        if per[2] is not None:
+            ev_us = per[2] + (per[3] or 0.0)
+            # per-launch event durations (each holds its dispatch, about 2 us): upper bounds
+            res["routing_kernel_us"] = {"rerank": round(per[2], 2),
+                                        "migrate": round(per[3], 2) if per[3] is not None else None}
+            res["routing_us_per_event"] = round(ev_us, 2)
+            # App. H cost model: routing cost per generated token = (T_rank + T_migrate) / R;
+            # the scores are accumulated inside every step's attention (no separate pass)
+            res["routing_us_per_token_amortized"] = round(ev_us / R, 3)
+    if attn_events:
+        attend_us = sum(ms for ms, _ in attn_events) * 1e3 / sum(n for _, n in attn_events)
+        res["attend_us_per_launch"] = round(attend_us, 3)
+        ach = bytes_per_call / (attend_us * 1e-6) / 1e9
         # the counter record was taken on the default run (8B / 32K workload, no RoPE,
         # library split count): other runs report no traffic
         default_run = args.workload == "c2" and args.rope_base == 0 and args.splits == 0
@@ -495,7 +603,9 @@ def main():
         res["roofline"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
                            "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": traffic}
     if not args.no_cpu:
-        res["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(wl, args.seed, args.cpu_seconds, LPS * wl.batch)
+        res["cpu_baseline"]["host_cpus"] = n_cpu
+        res["cpu_baseline"]["cpu_model"] = cpu_model
     print(json.dumps(res))
     cache.close()
     return 0

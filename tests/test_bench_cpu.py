@@ -49,3 +49,13 @@ def test_workload_line_names_the_shape(name, words):
     d = bench.workload_desc(syn.get_workload(name))
     for w in words:
         assert w in d, (w, d)
+
+
+def test_whole_model_workload_line():
+    d = bench.workload_desc(syn.get_workload("c3"))
+    assert d.startswith("32 layers back to back per step"), d
+
+
+def test_host_cpu_reports_count():
+    model, n = bench.host_cpu()
+    assert n == os.cpu_count() and n >= 1
