@@ -43,17 +43,26 @@ void* g_scratch_ptr[kMaxDevices] = {};
 }  // namespace
 
 // Device address of `scratch` on the current device (looked up on the first
-// call for that device, with it current).
-hipError_t static_obs_scratch(void** ptr) {
+// call for that device, with it current).  *what names the HIP call that failed.
+hipError_t static_obs_scratch(void** ptr, const char** what) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  if (e != hipSuccess) {
+    *what = "hipGetDevice";
+    return e;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    *what = "device index";
+    return hipErrorInvalidDevice;
+  }
   std::lock_guard<std::mutex> lock(g_scratch_mu);
   if (!g_scratch_ptr[dev]) {
     void* p = nullptr;
     e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess) {
+      *what = "hipGetSymbolAddress";
+      return e;
+    }
     g_scratch_ptr[dev] = p;
   }
   *ptr = g_scratch_ptr[dev];

@@ -35,7 +35,7 @@ hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st);
 hipError_t launch_key_norm_init(const KeyNormArgs& a, hipStream_t st);
 hipError_t launch_score_pow(const ScorePowArgs& a, hipStream_t st);
 hipError_t launch_prefill_scores(const ObsArgs& a, hipStream_t st);
-hipError_t static_obs_scratch(void** ptr);
+hipError_t static_obs_scratch(void** ptr, const char** what);
 }  // namespace qv
 
 using namespace qv;
@@ -560,8 +560,15 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
       return hip_fail(e, "creating the routing stream");
     }
   }
-  // the fixed scratch of qevict_prefill_scores_noalloc on this (the current) device
-  if (e == hipSuccess) e = static_obs_scratch(&c->static_scratch);
+  // the fixed scratch of qevict_prefill_scores_noalloc on this (the current)
+  // device; if the lookup fails here, that call retries it and reports the error
+  if (e == hipSuccess) {
+    const char* what = nullptr;
+    if (static_obs_scratch(&c->static_scratch, &what) != hipSuccess) {
+      c->static_scratch = nullptr;
+      (void)hipGetLastError();   // the failed lookup leaves no sticky error behind
+    }
+  }
   if (e == hipSuccess && cfg->rope_base > 0.f) {
     float* tab = (float*)(c->ws + kHeaderBytes + (int64_t)cfg->num_layers * cfg->batch * c->L.unit_bytes +
                           score_staging_bytes(cfg, c->g));
@@ -772,7 +779,14 @@ qevict_status qevict_prefill_scores_noalloc(qevict_cache* c, const uint16_t* q_o
                 "this prompt needs %lld bytes of scratch; the fixed scratch holds %lld "
                 "(use qevict_prefill_scores with a caller buffer)",
                 (long long)need, (long long)kStaticObsScratchBytes);
-  if (!c->static_scratch) return fail(QEVICT_ERR_DEVICE, "fixed scratch not available on this device");
+  if (!c->static_scratch) {
+    const char* what = "lookup";
+    const hipError_t e = static_obs_scratch(&c->static_scratch, &what);
+    if (e != hipSuccess) {
+      c->static_scratch = nullptr;
+      return fail(QEVICT_ERR_DEVICE, "fixed scratch address (%s): %s", what, hipGetErrorString(e));
+    }
+  }
   return prefill_scores_impl(c, q_obs, n_obs, k, prompt_len, c->static_scratch,
                              (size_t)kStaticObsScratchBytes, scores);
 }

@@ -119,6 +119,10 @@ def load_library(path: str | None = None):
     p = path or LIB_PATH
     if not os.path.exists(p):
         raise RuntimeError(f"{p} is missing: build it with `python -m paper_2608_05326_amd.build`")
+    # torch carries its own HIP runtime: load it first so that the library binds
+    # to the runtime torch's device memory and streams come from (loaded the
+    # other way round, creating a cache fails with "no ROCm-capable device")
+    import torch  # noqa: F401
     lib = ctypes.CDLL(p)
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     P = ctypes.POINTER
