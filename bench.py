@@ -132,7 +132,7 @@ def attend_bytes(wl, n_full, n_q4, n_q2, recent_tokens):
     read and written.  Evicted windows and split partials are not counted.
     """
     h, d, w = wl.num_kv_heads, wl.head_dim, wl.window
-    meta = h * (d * (w // wl.group) * 4 + w * (d // wl.group) * 4)
+    meta = h * (d * 4 + w * (d // wl.group) * 4)   # keys: one group per channel
     full = n_full * 2 * h * w * d * 2
     q4 = n_q4 * (2 * h * w * d * 4 // 8 + meta)
     q2 = n_q2 * (2 * h * w * d * 2 // 8 + meta)

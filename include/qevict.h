@@ -134,9 +134,10 @@ typedef struct {
   int32_t num_q_heads;       /* H_q                                                          */
   int32_t num_kv_heads;      /* H_kv; H_q % H_kv == 0 and H_q / H_kv <= 16                  */
   int32_t head_dim;          /* d; the library supports 128                                  */
-  int32_t window_tokens;     /* W; 32 or 64                                                  */
-  int32_t group_size;        /* G; the library requires G == W (keys: one group per channel  */
-                             /*  per window; values: W/... groups of G channels per token)    */
+  int32_t window_tokens;     /* W; 8, 32 or 64                                               */
+  int32_t group_size;        /* G, the value group: values are quantized per token in groups  */
+                             /* of G channels, keys per channel across the window's W tokens;  */
+                             /* G == W for W = 32 or 64, G == 32 for W = 8 (no RoPE then)     */
   int32_t quant_bits;        /* 4, 2 or QEVICT_BITS_MIXED_4_2                                */
   int32_t sink_tokens;       /* protected sink prefix |S| (at most 64 windows)               */
   int32_t recent_tokens;     /* protected recent region: a window is routed only once it is  */
@@ -172,7 +173,7 @@ typedef struct {
  * Per-window costs (one layer, one sequence):
  *   M_f = 4 H_kv W d (bf16 keys and values) + 4 (slot index) + 4 (position)
  *   M_q = 2 H_kv W d b / 8 (codes, b = 4 for QEVICT_BITS_MIXED_4_2: the slot
- *         size) + 4 H_kv d W / G (key scale and zero point, fp16)
+ *         size) + 4 H_kv d (key scale and zero point per channel, fp16)
  *         + 4 H_kv W d / G (value scale and zero point) + 4 + 4 (slot index,
  *         position) + 2 (ledger state and bit width)
  * budget_bytes is per layer and sequence; q is given in thousandths
@@ -310,7 +311,7 @@ qevict_status qevict_get_state(qevict_cache *c, int32_t layer, int32_t seq, int8
 
 /* Copy one window out in natural layouts (synchronous; host buffers, NULL to skip).
  *   codes_k, codes_v [H_kv, W, d] uint8 codes of the window's ledger
- *   meta_k  [H_kv, 2, W/G, d] fp16 bits: scale then zero point per key group
+ *   meta_k  [H_kv, 2, d] fp16 bits: scale then zero point per key group (channel)
  *   meta_v  [H_kv, 2, W, d/G] fp16 bits: scale then zero point per value group
  *   full_k, full_v [H_kv, W, d] bf16 bits of the Full-tier copy
  * Returns QEVICT_ERR_BAD_STATE when a requested part does not exist. */

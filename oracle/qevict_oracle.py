@@ -177,20 +177,22 @@ def quantize_groups(x, bits: int):
 def quantize_window(k, v, bits: int, group: int) -> dict:
     """Quantize one window: k, v float64 [H_kv, W, d] (bf16 values).
 
-    Keys: one group per (KV head, channel, G consecutive tokens) -> per-channel
-    scale/zero across the token dimension.  Values: one group per (KV head,
-    token, G consecutive channels) -> per-token scale/zero across channels.
+    Keys: one group per (KV head, channel) across the window's W tokens ->
+    per-channel scale/zero across the token dimension.  Values: one group per
+    (KV head, token, G consecutive channels) -> per-token scale/zero across
+    channels (Sec. 4.3, migration-stable quantization; the group sizes are
+    readings: the window for keys, G for values).
     """
     h, w, d = k.shape
-    if w % group or d % group:
-        raise ValueError("group must divide the window and the head dim")
-    kg = k.reshape(h, w // group, group, d).transpose(0, 1, 3, 2).reshape(-1, group)
+    if d % group:
+        raise ValueError("the value group must divide the head dim")
+    kg = k.transpose(0, 2, 1).reshape(-1, w)            # [H_kv * d, W]: one row per channel
     kz, ks, kc = quantize_groups(kg, bits)
-    kc = kc.reshape(h, w // group, d, group).transpose(0, 1, 3, 2).reshape(h, w, d)
+    kc = kc.reshape(h, d, w).transpose(0, 2, 1)
     vg = v.reshape(-1, group)
     vz, vs, vc = quantize_groups(vg, bits)
     return dict(bits=bits, group=group,
-                kz=kz.reshape(h, w // group, d), ks=ks.reshape(h, w // group, d), kc=kc,
+                kz=kz.reshape(h, 1, d), ks=ks.reshape(h, 1, d), kc=kc,
                 vz=vz.reshape(h, w, d // group), vs=vs.reshape(h, w, d // group),
                 vc=vc.reshape(h, w, d), state=ACTIVE)
 
@@ -198,11 +200,9 @@ def quantize_window(k, v, bits: int, group: int) -> dict:
 def dequantize_window(e: dict):
     """x_hat = z + s c for keys and values (exact in float64)."""
     g = e["group"]
-    kz = np.repeat(e["kz"], g, axis=1)
-    ks = np.repeat(e["ks"], g, axis=1)
     vz = np.repeat(e["vz"], g, axis=2)
     vs = np.repeat(e["vs"], g, axis=2)
-    return kz + ks * e["kc"], vz + vs * e["vc"]
+    return e["kz"] + e["ks"] * e["kc"], vz + vs * e["vc"]
 
 
 # ----------------------------------------------------------------------------
@@ -257,15 +257,15 @@ def window_costs(num_kv_heads: int, head_dim: int, window: int, group: int, bits
     Full: bf16 keys and values, plus a slot index and a position (4 bytes each).
     Quantized: packed b-bit codes of keys and values (b = 4 for the mixed
     int4/int2 tier, whose slots hold the larger record), fp16 scale and zero
-    point per key group (channel x W/G token groups) and per value group (token
-    x d/G channel groups), slot index and position, and a 2-byte ledger entry
+    point per key group (one per channel) and per value group (token x d/G
+    channel groups), slot index and position, and a 2-byte ledger entry
     (state, bit width) -- the codes, parameters, positions and persistent
     indexing state the paper lists.
     """
     b = 2 if bits == 2 else 4
     kv_elems = 2 * num_kv_heads * window * head_dim
     m_f = 2 * kv_elems + 4 + 4
-    params = 2 * 2 * num_kv_heads * head_dim * (window // group) \
+    params = 2 * 2 * num_kv_heads * head_dim \
         + 2 * 2 * num_kv_heads * window * (head_dim // group)
     m_q = kv_elems * b // 8 + params + 4 + 4 + 2
     return m_f, m_q
@@ -295,7 +295,7 @@ def memory_report(unit: "QEvictUnit") -> dict:
     c = unit.cfg
     H, d, W, G = c.num_kv_heads, c.head_dim, c.window, c.group
     tok = 2 * 2 * H * d
-    meta = 2 * 2 * H * d * (W // G) + 2 * 2 * H * W * (d // G)
+    meta = 2 * 2 * H * d + 2 * 2 * H * W * (d // G)
     r = dict(sink=tok * min(c.sink, unit.T), recent=0, full=0, quant_codes=0, quant_meta=0,
              position=0, ledger=0)
     routed = int(np.sum((unit.state == FULL) | (unit.state == QUANT) | (unit.state == EVICTED)))

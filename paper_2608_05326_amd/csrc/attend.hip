@@ -27,6 +27,16 @@ __device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
 __device__ __forceinline__ f32x4 mfma_f16(f16x8 a, f16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
+// 16x16x16 MFMAs of the P.V product of 8-token windows (k = 16 tokens of which
+// the window fills 8): A lane 16 q + r holds A[r][4 q + j], B lane holds B[4 q + j][r]
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f32x4 mfma16_bf16(bf16x4 a, bf16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma16_f16(f16x4 a, f16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
+}
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *(const u32x4*)p; }
 // Completes this wave's LDS operations before the next ones (LDS traffic of one
 // wave is ordered; the memory clobber keeps the compiler from moving accesses).
@@ -133,14 +143,24 @@ __device__ __forceinline__ void softmax_window(const f32x4 (&acc)[TB], float bia
 //   bf16 window: K chunks (tb, kb) at kh.d[tb * 4 + kb]; V chunks (kt, cb) at vh.d[kt * 8 + cb]
 //   quantized:   K codes kh.d[0 .. NC), K scale / zero (compact) kh.d[NC], kh.d[NC + 1];
 //                V codes vh.d[0 .. NC), V scale / zero per (kt, vg) at vh.d[NC + 2 (kt NG + vg)] (+1)
+//   8-token window: bf16 K chunks kb at kh.d[kb] (lanes r < 8), V chunks cp at
+//                vh.d[cp] (lanes q < 2); quantized K codes kh.d[0], compact key
+//                scale / zero kh.d[1], kh.d[2]; V codes vh.d[0], V scale / zero of
+//                value group g for the lane's 4 tokens vh.d[1 + g]
+// (entries of code registers before the compact key meta, and its index)
+template <int W>
+constexpr int key_code_regs() { return W == 8 ? 1 : W / 16; }
+// 16-token row tiles of a window's QK^T (an 8-token window fills half of one)
+template <int W>
+constexpr int row_tiles() { return W == 8 ? 1 : W / 16; }
 template <int W, bool ROPE = false>
 struct KHalf {
-  static constexpr int N = W / 4;
+  static constexpr int N = W == 8 ? 4 : W / 4;
   u32x4 d[N];
 };
 template <int W>
 struct VHalf {
-  static constexpr int N = W == 32 ? 10 : 16;
+  static constexpr int N = W == 8 ? 5 : (W == 32 ? 10 : 16);
   u32x4 d[N];
 };
 
@@ -156,7 +176,26 @@ __device__ __forceinline__ void fetch_k(const ItemInfo& in, KHalf<W, ROPE>& kh, 
                                         const Geometry& G) {
   constexpr int TB = W / 16, NC = W / 16;
   const uint8_t* p = in.p;
-  if (in.kind == KIND_BF16) {
+  if constexpr (W == 8) {
+    const bool row = r < 8;   // lanes of the window's 8 token rows
+    const int qg = lane >> 4;
+    if (in.kind == KIND_BF16) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) kh.d[kb] = row ? ld16(p + ((kb * 4 + qg) * 8 + r) * 16) : (u32x4){0, 0, 0, 0};
+    } else {
+      kh.d[3] = (u32x4){0, 0, 0, 0};
+      if (in.kind == KIND_Q4) {
+        kh.d[0] = row ? ld16(p + (qg * 8 + r) * 16) : (u32x4){0, 0, 0, 0};
+      } else {
+        const uint2 c2 = row ? *(const uint2*)(p + (qg * 8 + r) * 8) : make_uint2(0, 0);
+        kh.d[0] = (u32x4){c2.x, c2.y, 0, 0};
+      }
+      const uint8_t* mk = p + meta_k_off(G);
+      kh.d[1] = ld16(mk + 16 * r);
+      kh.d[2] = ld16(mk + 256 + 16 * r);
+    }
+    return;
+  } else if (in.kind == KIND_BF16) {
 #pragma unroll
     for (int i = 0; i < 4 * TB; ++i) kh.d[i] = ld16(p + (i * 64 + lane) * 16);
   } else {
@@ -184,7 +223,28 @@ __device__ __forceinline__ void fetch_v(const ItemInfo& in, VHalf<W>& vh, int la
                                         const Geometry& G) {
   constexpr int KT = W / 32, NC = W / 16, NG = kHeadDim / W;
   const uint8_t* p = in.p;
-  if (in.kind == KIND_BF16) {
+  if constexpr (W == 8) {
+    const bool col = qg < 2;   // lanes of the window's 8 tokens in the B operand
+    const int r = lane & 15;
+    if (in.kind == KIND_BF16) {
+      const int64_t vbase = (int64_t)W * kHeadDim * 2;
+#pragma unroll
+      for (int cp = 0; cp < 4; ++cp)
+        vh.d[cp] = col ? ld16(p + vbase + ((cp * 2 + qg) * 16 + r) * 16) : (u32x4){0, 0, 0, 0};
+      vh.d[4] = (u32x4){0, 0, 0, 0};
+    } else {
+      if (in.kind == KIND_Q4) {
+        vh.d[0] = col ? ld16(p + G.qcodes_bytes + (qg * 16 + r) * 16) : (u32x4){0, 0, 0, 0};
+      } else {
+        const uint2 c2 = col ? *(const uint2*)(p + G.qcodes_bytes + (qg * 16 + r) * 8) : make_uint2(0, 0);
+        vh.d[0] = (u32x4){c2.x, c2.y, 0, 0};
+      }
+#pragma unroll
+      for (int vg = 0; vg < 4; ++vg)
+        vh.d[1 + vg] = col ? ld16(p + meta_v_off(G) + ((qg * 4 + vg) * 16)) : (u32x4){0, 0, 0, 0};
+    }
+    return;
+  } else if (in.kind == KIND_BF16) {
     const int64_t vbase = (int64_t)W * kHeadDim * 2;
 #pragma unroll
     for (int i = 0; i < VHalf<W>::N; ++i)
@@ -328,9 +388,9 @@ template <int W, int NHS, bool ROPE>
 __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh, WaveState& st,
                                           const bf16x8 (&qop)[4], const float (&qf)[NHS][8],
                                           uint8_t* qlds, const AttnArgs& a, int b, int g, int lane,
-                                          int qg, int r, float (&p_)[W / 16][4], float* m_w,
+                                          int qg, int r, float (&p_)[row_tiles<W>()][4], float* m_w,
                                           float* l_w) {
-  constexpr int TB = W / 16;
+  constexpr int TB = row_tiles<W>();
   const Geometry& G = a.g;
   const int gqa = G.gqa;
   const int ntok = in.ntok;
@@ -354,7 +414,11 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
             const uint32_t old = kh.d[tb * 4 + kb][i], nv = v[i];
             kh.d[tb * 4 + kb][i] = sel ? nv : old;
           }
-          if (sel) *(u32x4*)(pw + ((tb * 4 + kb) * 64 + lane) * 16) = v;
+          if (sel) {
+            const int64_t off = W == 8 ? (int64_t)((kb * 4 + qg) * 8 + r) * 16
+                                       : (int64_t)((tb * 4 + kb) * 64 + lane) * 16;
+            *(u32x4*)(pw + off) = v;
+          }
         }
       }
     }
@@ -371,7 +435,7 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
     softmax_window<TB, NHS>(acc, 0.f, ntok, G.scale_log2, qg, st, p_, m_w, l_w);
   } else {
     // ---- quantized window: int4 or int2 codes ----
-    constexpr int NC = W / 16;
+    constexpr int NC = key_code_regs<W>();
     const bool is4 = in.kind == KIND_Q4;
     uint32_t kw[4 * NC];
 #pragma unroll
@@ -444,14 +508,100 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
   }
 }
 
+// P.V of an 8-token window: 16x16x16 MFMAs whose A operand is the lane's four
+// probabilities as the QK^T accumulator left them (head r, tokens 4 qg .. + 3)
+// and whose B operand holds the window's values in lanes qg < 2; the other
+// token columns carry zero probabilities and zero values.  The open window
+// takes this step's value (and stores it); tokens past the end of a partial
+// window contribute nothing.
+template <int NHS>
+__device__ __forceinline__ void process_v8(const ItemInfo& in, VHalf<8>& vh, WaveState& st,
+                                           const float (&p_)[1][4], float m_w, float l_w,
+                                           const AttnArgs& a, int b, int g, int qg, int r,
+                                           float2* mref) {
+  const Geometry& G = a.g;
+  const int gqa = G.gqa;
+  const int ntok = in.ntok;
+  if (in.kind == KIND_BF16) {
+    if (in.open) {
+      const int pos = ntok - 1;   // token 4 qp + jp: element jp of lanes qg == qp
+      const int qp = pos >> 2, jp = pos & 3;
+      const uint16_t* vn = a.v_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
+      uint8_t* pw = const_cast<uint8_t*>(in.p);
+      const bool vgrp = qg == qp;
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb) {
+        const uint32_t val = vn[16 * cb + r];
+        if (vgrp) *(uint16_t*)(pw + v_elem_off(8, pos, 16 * cb + r)) = (uint16_t)val;
+        const int wi = (cb & 1) * 2 + (jp >> 1);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t wv = vh.d[cb >> 1][i];
+          const uint32_t lo = (wv & 0xFFFF0000u) | val, hi = (wv & 0x0000FFFFu) | (val << 16);
+          vh.d[cb >> 1][i] = (vgrp && i == wi) ? ((jp & 1) ? hi : lo) : wv;
+        }
+      }
+    }
+    if (ntok < 8) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t0 = 4 * qg + 2 * (i & 1);
+        const uint32_t mask = (t0 < ntok ? 0x0000FFFFu : 0u) | (t0 + 1 < ntok ? 0xFFFF0000u : 0u);
+#pragma unroll
+        for (int cp = 0; cp < 4; ++cp) vh.d[cp][i] &= mask;
+      }
+    }
+    bf16x4 pv;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) pv[j] = (__bf16)p_[0][j];
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) {
+      const u32x4 d = vh.d[cb >> 1];
+      const uint32_t w0 = (cb & 1) ? d[2] : d[0], w1 = (cb & 1) ? d[3] : d[1];
+      const bf16x4 vb = __builtin_bit_cast(bf16x4, make_uint2(w0, w1));
+      st.o[cb] = mfma16_bf16(pv, vb, st.o[cb]);
+    }
+  } else {
+    const bool is4 = in.kind == KIND_Q4;
+    const u32x4 cw = vh.d[0];
+    f16x4 pv;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) pv[j] = (_Float16)p_[0][j];
+#pragma unroll
+    for (int cp = 0; cp < 4; ++cp) {
+      // codes of channel blocks 2 cp (elements 0..3) and 2 cp + 1 (4..7), tokens 4 qg + j
+      const uint32_t w4 = cw[cp], w2 = cw[cp >> 1];
+      const f16x8 c8 = is4 ? unpack_codes<4>(w4, 0) : unpack_codes<2>(w2, cp & 1);
+      // value group cp: scales then zero points of the lane's four tokens
+      const u32x4 m = vh.d[1 + cp];
+      const uint32_t m0 = m[0], m1 = m[1], m2 = m[2], m3 = m[3];
+      const f16x2 s01 = __builtin_bit_cast(f16x2, m0), s23 = __builtin_bit_cast(f16x2, m1);
+      const f16x2 z01 = __builtin_bit_cast(f16x2, m2), z23 = __builtin_bit_cast(f16x2, m3);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const f16x2 c01 = {c8[4 * e], c8[4 * e + 1]}, c23 = {c8[4 * e + 2], c8[4 * e + 3]};
+        const f16x2 v01 = __builtin_elementwise_fma(s01, c01, z01);
+        const f16x2 v23 = __builtin_elementwise_fma(s23, c23, z23);
+        const f16x4 vv = {v01[0], v01[1], v23[0], v23[1]};
+        st.o[2 * cp + e] = mfma16_f16(pv, vv, st.o[2 * cp + e]);
+      }
+    }
+  }
+  if (qg == 0 && r < gqa) mref[(int64_t)in.it * G.H_q + g * gqa + r] = make_float2(m_w, l_w);
+}
+
 // P.V of one window into the running output, then the window's statistics.
 // The open window takes this step's value (and stores it); tokens past the end
 // of a partial window contribute nothing.
 template <int W, int NHS>
 __device__ __forceinline__ void process_v(const ItemInfo& in, VHalf<W>& vh, WaveState& st,
-                                          const float (&p_)[W / 16][4], float m_w, float l_w,
+                                          const float (&p_)[row_tiles<W>()][4], float m_w, float l_w,
                                           const AttnArgs& a, int b, int g, int qg, int r,
                                           float2* mref) {
+  if constexpr (W == 8) {
+    process_v8<NHS>(in, vh, st, p_, m_w, l_w, a, b, g, qg, r, mref);
+    return;
+  }
   constexpr int KT = W / 32;
   const Geometry& G = a.g;
   const int gqa = G.gqa;
@@ -501,7 +651,7 @@ __device__ __forceinline__ void process_v(const ItemInfo& in, VHalf<W>& vh, Wave
         st.o[cb] = mfma_bf16(pv, __builtin_bit_cast(bf16x8, vh.d[kt * 8 + cb]), st.o[cb]);
     }
   } else {
-    constexpr int NC = W / 16;
+    constexpr int NC = key_code_regs<W>();   // (8-token windows take process_v8)
     constexpr int NG = kHeadDim / W;
     const bool is4 = in.kind == KIND_Q4;
     uint32_t vw[4 * NC];
@@ -721,7 +871,7 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   };
 
   // ---- window loop: this wave's contiguous run of windows ----
-  constexpr int TB = W / 16;
+  constexpr int TB = row_tiles<W>();
   KHalf<W, ROPE> KA;
   VHalf<W> V;
   float p_[TB][4];
@@ -1024,6 +1174,10 @@ hipError_t launch_attend(const AttnArgs& a, hipStream_t st) {
       else if (nhs == 2) go(k_attend<64, 2, 2, true>);
       else go(k_attend<64, 4, 2, true>);
     }
+  } else if (a.g.W == 8) {
+    if (nhs == 1) go(k_attend<8, 1, 2, false>);
+    else if (nhs == 2) go(k_attend<8, 2, 2, false>);
+    else go(k_attend<8, 4, 2, false>);
   } else if (a.g.W == 32) {
     if (nhs == 1) go(k_attend<32, 1, 2, false>);
     else if (nhs == 2) go(k_attend<32, 2, 2, false>);

@@ -91,6 +91,9 @@ __device__ __forceinline__ uint32_t quant_code(float x, const QParams& p, int nm
 // key entry / chunk e has channel block 32 (e & 3), value entry / chunk e has
 // channel block 16 (e & 7), and an int2 word's two entries share their half.
 constexpr int kParts = 4;
+// value group (channels) of a window length: G = W, except 32 for 8-token windows
+template <int W>
+constexpr int value_group() { return W == 8 ? 32 : W; }
 // LDS row of one token's 128 channels, padded by 16 bytes so that 16-byte
 // accesses to 16 consecutive tokens fall in distinct banks
 constexpr int kLdsRow = kHeadDim + 8;
@@ -129,7 +132,7 @@ __device__ __forceinline__ float2 rope_cs(const Geometry& G, int p, int i) {
 constexpr int kMigrateThreads = 256;
 // (the RoPE variants hold both key halves and their rotation: one wave fewer)
 template <int W, bool ROPE = false>
-constexpr int migrate_waves_per_simd() { return (W == 32 ? 5 : 4) - (ROPE ? 1 : 0); }
+constexpr int migrate_waves_per_simd() { return (W <= 32 ? 5 : 4) - (ROPE ? 1 : 0); }
 
 template <int W, int NB, bool ROPE>
 __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk, const uint16_t* sv,
@@ -171,6 +174,55 @@ __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk
   }
 }
 
+// Codes of one KV head of an 8-token window (layout of the header): thread
+// (lane, word) of this part forms one 32-bit word.  Keys: lane (q, r < 8) of
+// token r, words of channel blocks kb = 2 h, 2 h + 1 (int2: one word holding
+// both); values: lane (q < 2, r), words of channel-block pairs cp = 2 h, 2 h + 1
+// (int2: one word), value group cp.
+template <int NB>
+__device__ __forceinline__ void pack_codes8(const Geometry& G, const uint16_t* sk, const uint16_t* sv,
+                                            const QParams* pk, const QParams* pv, uint8_t* rec, int tid,
+                                            int part) {
+  constexpr int nmax = (1 << NB) - 1;
+  constexpr int WPH = NB == 4 ? 2 : 1;    // words of a lane in one channel half
+  constexpr int LB = NB == 4 ? 16 : 8;    // code bytes of a lane
+  constexpr int NG = kHeadDim / 32;
+  const int area = part >> 1, h = part & 1;
+  if (tid >= 32 * WPH) return;
+  const int ln = tid % 32, wl = tid / 32;
+  const int word = WPH * h + wl;          // int4: block kb / pair cp; int2: the half's word
+  uint32_t wd = 0;
+  if (area == 0) {
+    const int q = ln >> 3, r = ln & 7;    // token r, channels 32 kb + 8 q + j
+#pragma unroll
+    for (int ee = 0; ee < 4 / NB; ++ee) {
+      const int kb = NB == 4 ? word : 2 * word + ee;
+      const int c0 = 32 * kb + 8 * q;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float x = bf16_to_f32(sk[r * kLdsRow + c0 + j]);
+        wd |= quant_code(x, pk[c0 + j], nmax) << ((j & 1) * 16 + NB * (4 * ee + (j >> 1)));
+      }
+    }
+    *(uint32_t*)(rec + (q * 8 + r) * LB + 4 * word) = wd;
+  } else {
+    const int q = ln >> 4, r = ln & 15;   // tokens 4 q + j, channel 16 cb + r
+#pragma unroll
+    for (int ee = 0; ee < 4 / NB; ++ee) {
+      const int cp = NB == 4 ? word : 2 * word + ee;
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int t = 4 * q + j, c = 16 * (2 * cp + e) + r;
+          const float x = bf16_to_f32(sv[t * kLdsRow + c]);
+          wd |= quant_code(x, pv[t * NG + cp], nmax) << ((j & 1) * 16 + NB * (4 * ee + 2 * e + (j >> 1)));
+        }
+    }
+    *(uint32_t*)(rec + G.qcodes_bytes + (q * 16 + r) * LB + 4 * word) = wd;
+  }
+}
+
 // Load one part of one KV head of a window into LDS in natural [t][c] layout.
 template <int W, bool ROPE>
 __device__ __forceinline__ void load_window(const MigrateArgs& a, uint8_t* ub, int b, int g, int w, int src_kind,
@@ -186,6 +238,26 @@ __device__ __forceinline__ void load_window(const MigrateArgs& a, uint8_t* ub, i
     for (int i = tid; i < W * 8 * hv.nh; i += blockDim.x) {
       const int t = (i >> 3) % W, c = 64 * (hv.h0 + i / (W * 8)) + 8 * (i & 7);
       *(u32x4*)(dst + t * kLdsRow + c) = *(const u32x4*)(src + t * kHeadDim + c);
+    }
+  } else if constexpr (W == 8) {
+    // 16-byte pieces of this half: keys (kb, q, r < 8), values (cp, q < 2, r)
+    const uint8_t* p = ub + (src_kind == SRC_FSLOT ? a.L.fpool : a.L.ring) +
+                       (int64_t)src_idx * G.fslot_bytes + g * G.fhead_bytes;
+    for (int i = tid; i < 64; i += blockDim.x) {
+      if (area == 0) {
+        const int kb = 2 * h + (i >> 5), q = (i >> 3) & 3, r = i & 7;
+        *(u32x4*)(sk + r * kLdsRow + 32 * kb + 8 * q) = *(const u32x4*)(p + ((kb * 4 + q) * 8 + r) * 16);
+      } else {
+        const int cp = 2 * h + (i >> 5), q = (i >> 4) & 1, r = i & 15;
+        const u32x4 x = *(const u32x4*)(p + (int64_t)W * kHeadDim * 2 + ((cp * 2 + q) * 16 + r) * 16);
+        const uint32_t vw[4] = {x[0], x[1], x[2], x[3]};
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            sv[(4 * q + j) * kLdsRow + 16 * (2 * cp + e) + r] =
+                (uint16_t)(vw[2 * e + (j >> 1)] >> (16 * (j & 1)));
+      }
     }
   } else {
     const uint8_t* p = ub + (src_kind == SRC_FSLOT ? a.L.fpool : a.L.ring) +
@@ -259,7 +331,7 @@ struct QuantLds {
   uint16_t sk[W * kLdsRow];
   uint16_t sv[W * kLdsRow];
   QParams pk[kHeadDim];
-  QParams pv[W * (kHeadDim / W)];
+  QParams pv[W * (kHeadDim / value_group<W>())];
 };
 
 template <int W, bool ROPE>
@@ -267,8 +339,10 @@ __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub,
                                               const WorkEntry& ent, QuantLds<W>& sm, int32_t* counts,
                                               int part) {
   const Geometry& G = a.g;
-  constexpr int NG = kHeadDim / W;             // value groups per token
-  constexpr int NGH = 64 / W;                  // value groups per token in one channel half
+  constexpr int GV = value_group<W>();         // channels of a value group
+  constexpr int NG = kHeadDim / GV;            // value groups per token
+  constexpr int NGH = 64 / GV;                 // value groups per token in one channel half
+  constexpr int NX = W > GV ? W : GV;          // values of the largest group
   const int tid = threadIdx.x;
   const int area = part >> 1, h = part & 1;
   const int w = ent.v[0], src_kind = ent.v[1], src_idx = ent.v[2], dst = ent.v[3], nb = ent.v[4];
@@ -282,10 +356,13 @@ __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub,
     __syncthreads();
   }
   uint8_t* rec = ub + a.L.qpool + (int64_t)dst * G.qslot_bytes + g * G.qrec_bytes;
-  // ---- group parameters: one thread per group of this part (64 per half) ----
-  if (tid < 64 * hv.nh) {
-    float x[W];
+  // ---- group parameters: one thread per group of this part (keys: 64 channels
+  // per half; values: W tokens x NGH groups per half) ----
+  const int n_groups = area == 0 ? 64 * hv.nh : W * NGH;
+  if (tid < n_groups) {
+    float x[NX];
     int c = 0, t = 0, vg = 0;
+    const int n = area == 0 ? W : GV;   // values in the group
     if (area == 0) {
       c = 64 * hv.h0 + tid;
 #pragma unroll
@@ -293,9 +370,9 @@ __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub,
     } else {
       t = tid / NGH;
       vg = NGH * h + tid % NGH;
-      const u32x4* row = (const u32x4*)(sv + t * kLdsRow + vg * W);
+      const u32x4* row = (const u32x4*)(sv + t * kLdsRow + vg * GV);
 #pragma unroll
-      for (int k = 0; k < W / 8; ++k) {
+      for (int k = 0; k < GV / 8; ++k) {
         const u32x4 v = row[k];
         const uint32_t vw[4] = {v[0], v[1], v[2], v[3]};
 #pragma unroll
@@ -304,9 +381,11 @@ __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub,
     }
     float lo = x[0], hi = x[0];
 #pragma unroll
-    for (int i = 1; i < W; ++i) {
-      lo = fminf(lo, x[i]);
-      hi = fmaxf(hi, x[i]);
+    for (int i = 1; i < NX; ++i) {
+      if (i < n) {
+        lo = fminf(lo, x[i]);
+        hi = fmaxf(hi, x[i]);
+      }
     }
     uint16_t zb = 0, sb = 0;
     const QParams p = group_params(lo, hi, nb, &zb, &sb, counts);
@@ -317,15 +396,20 @@ __device__ __forceinline__ void quantize_task(const MigrateArgs& a, uint8_t* ub,
       mk[kHeadDim + c] = zb;
     } else {
       sm.pv[t * NG + vg] = p;
-      uint16_t* mv = (uint16_t*)(rec + meta_v_elem(G, t, vg));
-      mv[0] = sb;
-      mv[8] = zb;
+      uint8_t* mv = rec + meta_v_elem(G, t, vg);
+      *(uint16_t*)mv = sb;
+      *(uint16_t*)(mv + meta_v_zero_delta(G)) = zb;
     }
   }
   __syncthreads();
   // ---- codes, packed ----
-  if (nb == 4) pack_codes<W, 4, ROPE>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
-  else pack_codes<W, 2, ROPE>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
+  if constexpr (W == 8) {
+    if (nb == 4) pack_codes8<4>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
+    else pack_codes8<2>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
+  } else {
+    if (nb == 4) pack_codes<W, 4, ROPE>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
+    else pack_codes<W, 2, ROPE>(G, sk, sv, sm.pk, sm.pv, rec, tid, part);
+  }
 }
 
 // 8 bf16 values z_j + s_j c_j (exact in float64, one rounding) packed for a 16-byte store
@@ -440,6 +524,63 @@ __device__ __forceinline__ void promote_from_record(const Geometry& G, const uin
   }
 }
 
+// Promotion of one KV head of an 8-token window from its record: one thread per
+// 16-byte piece of this part's half (keys: block kb, lane (q, r < 8); values:
+// block pair cp, lane (q < 2, r)), its values z + s c formed exactly in float64
+// and rounded once to bf16.
+template <int NB>
+__device__ __forceinline__ void promote_from_record8(const Geometry& G, const uint8_t* rec, uint8_t* dp,
+                                                     int tid, int part) {
+  constexpr uint32_t mask = (1u << NB) - 1u;
+  constexpr int LB = NB == 4 ? 16 : 8;
+  const int area = part >> 1, h = part & 1;
+  if (tid >= 64) return;
+  uint32_t outw[4];
+  if (area == 0) {
+    const int kb = 2 * h + (tid >> 5), q = (tid >> 3) & 3, r = tid & 7;
+    const int word = NB == 4 ? kb : kb >> 1, ee = NB == 4 ? 0 : kb & 1;
+    const uint32_t wd = *(const uint32_t*)(rec + (q * 8 + r) * LB + 4 * word);
+    const uint8_t* ps = rec + meta_k_off(G) + 2 * (32 * kb + 8 * q);
+    const u32x4 s8 = *(const u32x4*)ps, z8 = *(const u32x4*)(ps + 2 * kHeadDim);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint32_t pair = 0;
+#pragma unroll
+      for (int o = 0; o < 2; ++o) {
+        const uint32_t code = (wd >> (o * 16 + NB * (4 * ee + i))) & mask;
+        const double sj = fp16_bits_to_f64((uint16_t)(s8[i] >> (16 * o)));
+        const double zj = fp16_bits_to_f64((uint16_t)(z8[i] >> (16 * o)));
+        pair |= (uint32_t)f64_to_bf16_rne(zj + sj * (double)code) << (16 * o);
+      }
+      outw[i] = pair;
+    }
+    *(u32x4*)(dp + ((kb * 4 + q) * 8 + r) * 16) = (u32x4){outw[0], outw[1], outw[2], outw[3]};
+  } else {
+    const int cp = 2 * h + (tid >> 5), q = (tid >> 4) & 1, r = tid & 15;
+    const int word = NB == 4 ? cp : cp >> 1, ee = NB == 4 ? 0 : cp & 1;
+    const uint32_t wd = *(const uint32_t*)(rec + G.qcodes_bytes + (q * 16 + r) * LB + 4 * word);
+    // value group cp: scales then zero points of tokens 4 q .. 4 q + 3
+    const u32x4 m = *(const u32x4*)(rec + meta_v_off(G) + (q * 4 + cp) * 16);
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int jp = 0; jp < 2; ++jp) {
+        uint32_t pair = 0;
+#pragma unroll
+        for (int o = 0; o < 2; ++o) {
+          const int j = 2 * jp + o;
+          const uint32_t code = (wd >> (o * 16 + NB * (4 * ee + 2 * e + jp))) & mask;
+          const double sj = fp16_bits_to_f64((uint16_t)(m[j >> 1] >> (16 * (j & 1))));
+          const double zj = fp16_bits_to_f64((uint16_t)(m[2 + (j >> 1)] >> (16 * (j & 1))));
+          pair |= (uint32_t)f64_to_bf16_rne(zj + sj * (double)code) << (16 * o);
+        }
+        outw[2 * e + jp] = pair;
+      }
+    *(u32x4*)(dp + (int64_t)8 * kHeadDim * 2 + ((cp * 2 + q) * 16 + r) * 16) =
+        (u32x4){outw[0], outw[1], outw[2], outw[3]};
+  }
+}
+
 template <int W, bool ROPE>
 __device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, int b, int g,
                                              const WorkEntry& ent, int part) {
@@ -450,7 +591,16 @@ __device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, 
   uint8_t* dp = ub + a.L.fpool + (int64_t)dst * G.fslot_bytes + g * G.fhead_bytes;
   const int64_t area_off = area == 0 ? 0 : (int64_t)W * kHeadDim * 2;
   const Halves hv = part_halves<ROPE>(area, h);
-  if (src_kind == SRC_RING) {
+  if (W == 8 && src_kind == SRC_RING) {
+    // the half's 16-byte pieces: keys (kb, q, r < 8), values (cp, q < 2, r)
+    const uint8_t* sp = ub + a.L.ring + (int64_t)src_idx * G.fslot_bytes + g * G.fhead_bytes;
+    for (int i = tid; i < 64; i += blockDim.x) {
+      const int64_t off = area == 0 ? (int64_t)(((2 * h + (i >> 5)) * 4 + ((i >> 3) & 3)) * 8 + (i & 7)) * 16
+                                    : (int64_t)W * kHeadDim * 2 +
+                                          (int64_t)(((2 * h + (i >> 5)) * 2 + ((i >> 4) & 1)) * 16 + (i & 15)) * 16;
+      *(u32x4*)(dp + off) = *(const u32x4*)(sp + off);
+    }
+  } else if (src_kind == SRC_RING) {
     const uint8_t* sp = ub + a.L.ring + (int64_t)src_idx * G.fslot_bytes + g * G.fhead_bytes;
     for (int i = tid; i < (W / 8) * 64 * hv.nh; i += blockDim.x) {
       const int ih = i / ((W / 8) * 64), il = i % ((W / 8) * 64);
@@ -463,7 +613,7 @@ __device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, 
       const uint16_t* ks = a.src_k + row0 * kHeadDim;
       for (int i = tid; i < W * 8 * hv.nh; i += blockDim.x) {
         const int t = (i >> 3) % W, c = 64 * (hv.h0 + i / (W * 8)) + 8 * (i & 7);
-        *(u32x4*)(dp + k_elem_off(t, c)) = *(const u32x4*)(ks + t * kHeadDim + c);
+        *(u32x4*)(dp + k_elem_off(W, t, c)) = *(const u32x4*)(ks + t * kHeadDim + c);
       }
     } else {
       const uint16_t* vs = a.src_v + row0 * kHeadDim;
@@ -475,8 +625,13 @@ __device__ __forceinline__ void promote_task(const MigrateArgs& a, uint8_t* ub, 
   } else {   // SRC_QSLOT
     const uint8_t* rec = ub + a.L.qpool + (int64_t)src_idx * G.qslot_bytes + g * G.qrec_bytes;
     const int p0 = G.sink + w * W;   // position of the window's first token
-    if (nb == 4) promote_from_record<W, 4, ROPE>(G, rec, dp, tid, part, p0);
-    else promote_from_record<W, 2, ROPE>(G, rec, dp, tid, part, p0);
+    if constexpr (W == 8) {
+      if (nb == 4) promote_from_record8<4>(G, rec, dp, tid, part);
+      else promote_from_record8<2>(G, rec, dp, tid, part);
+    } else {
+      if (nb == 4) promote_from_record<W, 4, ROPE>(G, rec, dp, tid, part, p0);
+      else promote_from_record<W, 2, ROPE>(G, rec, dp, tid, part, p0);
+    }
   }
 }
 
@@ -541,7 +696,7 @@ __global__ __launch_bounds__(256) void k_pack_tokens(PackArgs a) {
       dp = ub + a.L.ring + (int64_t)(w % G.NR) * G.fslot_bytes + g * G.fhead_bytes;
       tt = (t - G.sink) % G.W;
     }
-    *(uint16_t*)(dp + k_elem_off(tt, c)) = a.src_k[(row0 + t) * kHeadDim + c];
+    *(uint16_t*)(dp + k_elem_off(G.W, tt, c)) = a.src_k[(row0 + t) * kHeadDim + c];
     *(uint16_t*)(dp + v_elem_off(G.W, tt, c)) = a.src_v[(row0 + t) * kHeadDim + c];
   }
 }
@@ -560,7 +715,8 @@ hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, 
     if (a.g.W == 32) hipLaunchKernelGGL((k_migrate<32, true>), grid, dim3(kMigrateThreads), 0, st, a);
     else hipLaunchKernelGGL((k_migrate<64, true>), grid, dim3(kMigrateThreads), 0, st, a);
   } else {
-    if (a.g.W == 32) hipLaunchKernelGGL((k_migrate<32, false>), grid, dim3(kMigrateThreads), 0, st, a);
+    if (a.g.W == 8) hipLaunchKernelGGL((k_migrate<8, false>), grid, dim3(kMigrateThreads), 0, st, a);
+    else if (a.g.W == 32) hipLaunchKernelGGL((k_migrate<32, false>), grid, dim3(kMigrateThreads), 0, st, a);
     else hipLaunchKernelGGL((k_migrate<64, false>), grid, dim3(kMigrateThreads), 0, st, a);
   }
   return hipGetLastError();

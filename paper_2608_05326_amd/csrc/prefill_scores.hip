@@ -105,7 +105,7 @@ __global__ __launch_bounds__(256, 4) void k_obs_chunks(ObsArgs a) {
   const int pos0 = T - a.n_obs;   // position of observation row j = pos0 + j
   // only a chunk reaching below key 0 or past the first observation position masks keys
   const bool edge = kbase < 0 || kbase + kObsChunkKeys - 1 > pos0;
-  const int wpc = kObsChunkKeys / a.W;          // windows per chunk: 2 (W = 32) or 1 (W = 64)
+  const int wpc = kObsChunkKeys / a.W;          // windows per chunk: 8 (W = 8), 2 (W = 32) or 1 (W = 64)
   const int w0 = (c - a.n_pre) * wpc;           // first window of the chunk (< 0: sink chunk)
   const int64_t bg = (int64_t)b * a.H_kv + g;
   const float sc = a.scale_log2;
@@ -168,12 +168,27 @@ __global__ __launch_bounds__(256, 4) void k_obs_chunks(ObsArgs a) {
         lB += __builtin_amdgcn_exp2f(fmaf(acc[2][i], sc, -mu));
         lB += __builtin_amdgcn_exp2f(fmaf(acc[3][i], sc, -mu));
       }
+      if (wpc == 8) {
+        // 8-token windows: tile kt holds windows 2 kt (lanes lq 0, 1) and 2 kt + 1
+        // (lq 2, 3); the pair sums land in lanes lq 0 and 2
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+          float lt = 0.f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) lt += __builtin_amdgcn_exp2f(fmaf(acc[kt][i], sc, -mu));
+          lt += __shfl_xor(lt, 16, 64);
+          const int w = w0 + 2 * kt + (lq >> 1);
+          if (row < nr && (lq & 1) == 0 && w >= 0 && w < a.n_w) wl_a[(int64_t)(w - w0) * n_rows + rg] = lt;
+        }
+      }
       lA = rows_sum(lA);
       lB = rows_sum(lB);
       if (row < nr) {
         if (lq == 0) cml_out[rg] = make_float2(m, lA + lB);
-        if (lq == 1 && has_a) wl_a[rg] = wpc == 2 ? lA : lA + lB;
-        if (lq == 2 && has_b) wl_a[n_rows + rg] = lB;
+        if (wpc <= 2) {
+          if (lq == 1 && has_a) wl_a[rg] = wpc == 2 ? lA : lA + lB;
+          if (lq == 2 && has_b) wl_a[n_rows + rg] = lB;
+        }
       }
     }
   }

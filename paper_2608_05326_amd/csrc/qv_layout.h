@@ -25,6 +25,24 @@
 //   K meta: fp16 scale[128] then zero[128] (one key group per channel per window).
 //   V meta: per (kt, q, value group g): fp16 scale[8] then zero[8] for the 8
 //           tokens tok(kt, q, 0..7).
+//
+// 8-token windows (values in groups of G = 32 channels) use their own chunks:
+//   bf16 K: chunk kb (channels 32 kb ..), 512 B: lane L = 16q + r, r < 8, holds
+//           K[r][32 kb + 8 q + j] at ((kb * 4 + q) * 8 + r) * 16 + 2 j -- rows 0..7
+//           of the QK^T A operand (rows 8..15 of the tile stay empty);
+//   bf16 V: chunk cp (channel blocks 2 cp and 2 cp + 1), 512 B: lane L = 16q + r,
+//           q < 2, holds V[4 q + j][16 (2 cp + e) + r] at
+//           ((cp * 2 + q) * 16 + r) * 16 + 8 e + 2 j -- the B operand (tokens
+//           4 q .. 4 q + 3) of a 16x16x16 P.V MFMA for channel block 2 cp + e;
+//   K codes: lane (q, r < 8) holds the 32 codes of token r, channels 32 kb + 8 q + j,
+//           in 16 B (int4: word kb) or 8 B (int2: word kb / 2, entry kb % 2) at
+//           (q * 8 + r) * (16 or 8); code j = 2i + o at bit 16 o + b (4 e' + i);
+//   V codes: lane (q < 2, r) holds the codes of tokens 4 q + j, channel blocks
+//           cb = 0..7 (channel 16 cb + r): word cp (int4) or word cp / 2, entry
+//           cp % 2 (int2) holds, at position i' = 2 (cb % 2) + j / 2, o = j % 2,
+//           the code of token 4 q + j of block cb; lane offset (q * 16 + r) * (16 or 8);
+//   K meta as above; V meta: per (q < 2, value group g < 4): fp16 scale[4] then
+//           zero[4] for tokens 4 q .. 4 q + 3 at (q * 4 + g) * 16.
 #pragma once
 #include <stdint.h>
 
@@ -119,8 +137,10 @@ struct UnitLayout {
 QV_HD int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 
 // ---- bf16 slot offsets (bytes inside one KV head block) ---------------------
-QV_HD int64_t k_elem_off(int t, int c) {
-  int tb = t >> 4, r = t & 15, kb = c >> 5, q = (c >> 3) & 3, j = c & 7;
+QV_HD int64_t k_elem_off(int W, int t, int c) {
+  const int kb = c >> 5, q = (c >> 3) & 3, j = c & 7;
+  if (W == 8) return ((int64_t)((kb * 4 + q) * 8 + t) * 16) + j * 2;
+  const int tb = t >> 4, r = t & 15;
   return ((int64_t)((tb * 4 + kb) * 64 + q * 16 + r) * 16) + j * 2;
 }
 QV_HD void v_tok_pos(int t, int* kt, int* q, int* j) {
@@ -131,9 +151,13 @@ QV_HD void v_tok_pos(int t, int* kt, int* q, int* j) {
 }
 QV_HD int v_tok(int kt, int q, int j) { return 32 * kt + 16 * (j >> 2) + 4 * q + (j & 3); }
 QV_HD int64_t v_elem_off(int W, int t, int c) {
+  const int cb = c >> 4, r = c & 15;
+  if (W == 8) {
+    const int q = t >> 2, j = t & 3, cp = cb >> 1, e = cb & 1;
+    return (int64_t)W * kHeadDim * 2 + ((int64_t)((cp * 2 + q) * 16 + r) * 16) + 8 * e + 2 * j;
+  }
   int kt, q, j;
   v_tok_pos(t, &kt, &q, &j);
-  int cb = c >> 4, r = c & 15;
   return (int64_t)W * kHeadDim * 2 + ((int64_t)((kt * 8 + cb) * 64 + q * 16 + r) * 16) + j * 2;
 }
 
@@ -158,16 +182,36 @@ QV_HD void v_code_pos(int t, int c, int* e, int* L, int* j) {
   *L = q * 16 + (c & 15);
   *j = jj;
 }
+// 8-token windows: byte offset inside a code area and bit shift of the code of
+// token t, channel c (area 0 keys, 1 values)
+QV_HD void code_loc8(int bits, int area, int t, int c, int64_t* byte_off, int* shift) {
+  const int lb = bits == 4 ? 16 : 8;   // bytes of codes per lane
+  if (area == 0) {
+    const int kb = c >> 5, q = (c >> 3) & 3, j = c & 7;
+    const int word = bits == 4 ? kb : kb >> 1, ee = bits == 4 ? 0 : kb & 1;
+    *byte_off = (int64_t)(q * 8 + t) * lb + 4 * word;
+    *shift = (j & 1) * 16 + bits * (4 * ee + (j >> 1));
+  } else {
+    const int q = t >> 2, j = t & 3, cb = c >> 4, r = c & 15, cp = cb >> 1;
+    const int word = bits == 4 ? cp : cp >> 1, ee = bits == 4 ? 0 : cp & 1;
+    const int i = 2 * (cb & 1) + (j >> 1);
+    *byte_off = (int64_t)(q * 16 + r) * lb + 4 * word;
+    *shift = (j & 1) * 16 + bits * (4 * ee + i);
+  }
+}
 // meta offsets inside a record (after the two code areas)
 QV_HD int64_t meta_k_off(const Geometry& g) { return 2 * g.qcodes_bytes; }
 QV_HD int64_t meta_v_off(const Geometry& g) { return 2 * g.qcodes_bytes + 4 * kHeadDim; }
-// byte offset of the V scale of token t, value group vg (zero point at +16)
+// byte offset of the V scale of token t, value group vg; its zero point follows
+// meta_v_zero_delta bytes later
 QV_HD int64_t meta_v_elem(const Geometry& g, int t, int vg) {
+  if (g.W == 8) return meta_v_off(g) + (int64_t)(((t >> 2) * 4 + vg) * 16) + (t & 3) * 2;
   int kt, q, j;
   v_tok_pos(t, &kt, &q, &j);
   int ng = kHeadDim / g.G;
   return meta_v_off(g) + ((int64_t)((kt * 4 + q) * ng + vg) * 32) + j * 2;
 }
+QV_HD int meta_v_zero_delta(const Geometry& g) { return g.W == 8 ? 8 : 16; }
 
 QV_HD int item_cost(const Geometry& g, int kind) {
   return kind == KIND_BF16 ? g.cost_bf16 : (kind == KIND_Q4 ? g.cost_q4 : g.cost_q2);

@@ -127,10 +127,16 @@ qevict_status check_config(const qevict_config* c) {
   if (c->num_q_heads / c->num_kv_heads > kMaxGqa || c->num_q_heads > 64)
     return fail(QEVICT_ERR_UNSUPPORTED, "at most 16 query heads per KV head and 64 query heads");
   if (c->head_dim != kHeadDim) return fail(QEVICT_ERR_UNSUPPORTED, "head_dim must be 128");
-  if (c->window_tokens != 32 && c->window_tokens != 64)
-    return fail(QEVICT_ERR_UNSUPPORTED, "window_tokens must be 32 or 64");
-  if (c->group_size != c->window_tokens)
-    return fail(QEVICT_ERR_UNSUPPORTED, "group_size must equal window_tokens");
+  if (c->window_tokens != 8 && c->window_tokens != 32 && c->window_tokens != 64)
+    return fail(QEVICT_ERR_UNSUPPORTED, "window_tokens must be 8, 32 or 64");
+  if (c->window_tokens == 8) {
+    if (c->group_size != 32)
+      return fail(QEVICT_ERR_UNSUPPORTED, "8-token windows take value groups of 32 channels (group_size 32)");
+    if (c->rope_base > 0.f)
+      return fail(QEVICT_ERR_UNSUPPORTED, "the RoPE-aware tier needs windows of 32 or 64 tokens");
+  } else if (c->group_size != c->window_tokens) {
+    return fail(QEVICT_ERR_UNSUPPORTED, "group_size must equal window_tokens (32 or 64)");
+  }
   if (c->quant_bits != 4 && c->quant_bits != 2 && c->quant_bits != QEVICT_BITS_MIXED_4_2)
     return fail(QEVICT_ERR_UNSUPPORTED, "quant_bits must be 4, 2 or 42");
   if (c->sink_tokens < 0 || c->recent_tokens < 0 || c->capacity_full < 0 || c->capacity_quant < 0)
@@ -220,10 +226,11 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   g->qslot_bytes = g->qrec_bytes * g->H_kv;
   // split-balancing weights (per 32 tokens): a bf16 window moves twice the bytes
   // of an int4 one, which carries the code expansion instead; measured per-wave
-  // times are close, so the weights are nearly equal
-  g->cost_bf16 = 16 * (g->W / 32);
-  g->cost_q4 = 16 * (g->W / 32);
-  g->cost_q2 = 14 * (g->W / 32);
+  // times are close, so the weights are nearly equal.  An 8-token window costs
+  // the same whatever its tier: its fixed per-window work outweighs its bytes.
+  g->cost_bf16 = g->W == 8 ? 4 : 16 * (g->W / 32);
+  g->cost_q4 = g->W == 8 ? 4 : 16 * (g->W / 32);
+  g->cost_q2 = g->W == 8 ? 4 : 14 * (g->W / 32);
   int64_t off = 0;
   auto take = [&](int64_t bytes) {
     int64_t o = off;
@@ -497,7 +504,7 @@ qevict_status qevict_capacities_for_budget(const qevict_config* cfg, int64_t bud
                 (long long)budget_bytes, (long long)protect);
   const int64_t hist = budget_bytes - protect;
   const int64_t m_f = 4 * Hkv * W * d + 8;
-  const int64_t m_q = 2 * Hkv * W * d * bits / 8 + 4 * Hkv * d * (W / G) + 4 * Hkv * W * (d / G) + 10;
+  const int64_t m_q = 2 * Hkv * W * d * bits / 8 + 4 * Hkv * d + 4 * Hkv * W * (d / G) + 10;
   // exact: floor(((1000 - q) / 1000) * hist / m_f); hist < 2^48 keeps the products in range
   if (hist >= ((int64_t)1 << 48)) return fail(QEVICT_ERR_INVALID_ARG, "budget too large");
   const int64_t kf = (1000 - q_permille) * hist / (1000 * m_f);
@@ -992,7 +999,7 @@ qevict_status qevict_memory_report(qevict_cache* c, int32_t layer, int32_t seq, 
   if (s) return s;
   const int64_t T = c->layers[layer].T, Hkv = g.H_kv, d = g.d, W = g.W, G = g.G;
   const int64_t tok = 4 * Hkv * d;   // bf16 key and value of one token
-  const int64_t meta = 4 * Hkv * d * (W / G) + 4 * Hkv * W * (d / G);
+  const int64_t meta = 4 * Hkv * d + 4 * Hkv * W * (d / G);
   int64_t routed = 0;
   qevict_memory m{};
   m.sink = tok * std::min<int64_t>(g.sink, T);
@@ -1058,23 +1065,31 @@ qevict_status qevict_export_window(qevict_cache* c, int32_t layer, int32_t seq, 
         int ee, L, j, sh;
         int64_t off;
         if (codes_k) {
-          k_code_pos(t, ch, &ee, &L, &j);
-          code_loc(nb, ee, L, j, &off, &sh);
+          if (W == 8) {
+            code_loc8(nb, 0, t, ch, &off, &sh);
+          } else {
+            k_code_pos(t, ch, &ee, &L, &j);
+            code_loc(nb, ee, L, j, &off, &sh);
+          }
           uint32_t w32;
           memcpy(&w32, r + off, 4);
           codes_k[o] = (uint8_t)((w32 >> sh) & ((1u << nb) - 1));
         }
         if (codes_v) {
-          v_code_pos(t, ch, &ee, &L, &j);
-          code_loc(nb, ee, L, j, &off, &sh);
+          if (W == 8) {
+            code_loc8(nb, 1, t, ch, &off, &sh);
+          } else {
+            v_code_pos(t, ch, &ee, &L, &j);
+            code_loc(nb, ee, L, j, &off, &sh);
+          }
           uint32_t w32;
           memcpy(&w32, r + g.qcodes_bytes + off, 4);
           codes_v[o] = (uint8_t)((w32 >> sh) & ((1u << nb) - 1));
         }
-        if (full_k) memcpy(full_k + o, f + k_elem_off(t, ch), 2);
+        if (full_k) memcpy(full_k + o, f + k_elem_off(W, t, ch), 2);
         if (full_v) memcpy(full_v + o, f + v_elem_off(W, t, ch), 2);
       }
-    if (meta_k) {   // [h][2][W/G][d]; W == G: one group per channel
+    if (meta_k) {   // [h][2][d]: one key group per channel
       memcpy(meta_k + (int64_t)h * 2 * d, r + meta_k_off(g), 2 * d);
       memcpy(meta_k + (int64_t)h * 2 * d + d, r + meta_k_off(g) + 2 * d, 2 * d);
     }
@@ -1083,7 +1098,7 @@ qevict_status qevict_export_window(qevict_cache* c, int32_t layer, int32_t seq, 
         for (int vg = 0; vg < ng; ++vg) {
           const int64_t mo = meta_v_elem(g, t, vg);
           memcpy(meta_v + ((int64_t)h * 2 * W + t) * ng + vg, r + mo, 2);
-          memcpy(meta_v + ((int64_t)h * 2 * W + W + t) * ng + vg, r + mo + 16, 2);
+          memcpy(meta_v + ((int64_t)h * 2 * W + W + t) * ng + vg, r + mo + meta_v_zero_delta(g), 2);
         }
     }
   }

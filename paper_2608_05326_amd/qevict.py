@@ -85,7 +85,7 @@ class Config:
     capacity_quant: int
     num_layers: int = 1
     head_dim: int = 128
-    group_size: int = 0          # 0: same as window_tokens
+    group_size: int = 0          # 0: window_tokens (32 for 8-token windows)
     sink_tokens: int = 0
     recent_tokens: int = 0
     retier_interval: int = 1
@@ -103,8 +103,8 @@ class Config:
         c.abi_version = ABI_VERSION
         for f in dataclasses.fields(self):
             setattr(c, f.name, getattr(self, f.name))
-        if not self.group_size:
-            c.group_size = self.window_tokens
+        if not self.group_size:   # the value group: 32 channels for 8-token windows, else W
+            c.group_size = 32 if self.window_tokens == 8 else self.window_tokens
         return c
 
 
@@ -221,7 +221,7 @@ class Cache:
             ctypes.byref(cfg.to_c()), ctypes.c_void_p(self.workspace.data_ptr()),
             self.workspace.numel(), ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h)))
         self.handle = h
-        gr = cfg.group_size or cfg.window_tokens
+        gr = cfg.group_size or (32 if cfg.window_tokens == 8 else cfg.window_tokens)
         self.n_cap = -(-(cfg.max_context - cfg.sink_tokens) // cfg.window_tokens)
         self._gr = gr
 
@@ -354,7 +354,7 @@ class Cache:
         if quant:
             out["codes_k"] = np.zeros((h, w, d), np.uint8)
             out["codes_v"] = np.zeros((h, w, d), np.uint8)
-            out["meta_k"] = np.zeros((h, 2, w // gr, d), np.uint16)
+            out["meta_k"] = np.zeros((h, 2, 1, d), np.uint16)   # one key group per channel
             out["meta_v"] = np.zeros((h, 2, w, d // gr), np.uint16)
             for i, k in enumerate(("codes_k", "codes_v", "meta_k", "meta_v")):
                 ptrs[i] = out[k].ctypes.data_as(ctypes.c_void_p)

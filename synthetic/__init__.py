@@ -43,7 +43,7 @@ class Workload:
     head_dim: int
     prompt_len: int
     window: int              # W: tokens per window
-    group: int               # G: quantization group length
+    group: int               # G: value quantization group (channels); keys group over the window
     bits: int                # 4, 2, or 42 (= int4 for the top half of the quantized tier, int2 below)
     frac_full: str           # fraction of prefill windows kept in bf16 (decimal string, exact)
     frac_quant: str          # fraction kept quantized
@@ -135,6 +135,12 @@ WORKLOADS = {
                    prompt_len=32768, window=32, group=32, bits=2, frac_full="0", frac_quant="0",
                    steps=128, retier_interval=8, sink=5, recent=32, budget_frac="0.2", q_frac="0.7",
                    **_drift_defaults()),
+    # The paper's default point with its 8-token windows (Omega = 8): values in groups
+    # of 32 channels, keys per channel across the window; byte-budget capacities.
+    "c6w8": Workload("c6w8", 8, batch=1, layers=1, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                     prompt_len=32768, window=8, group=32, bits=2, frac_full="0", frac_quant="0",
+                     steps=128, retier_interval=8, sink=5, recent=32, budget_frac="0.2", q_frac="0.7",
+                     **_drift_defaults()),
 }
 
 # Reduced-size variants with the same head layouts and tier policies: they span
@@ -152,6 +158,7 @@ WORKLOADS.update({
     "c7s": WORKLOADS["c5"].replace(name="c7s", config_id=7, batch=2, prompt_len=32 * 90 + 3, steps=30,
                                    sink=80, recent=70, retier_interval=3, frac_full="0.2",
                                    frac_quant="0.3"),
+    "c6w8s": WORKLOADS["c6w8"].replace(name="c6w8s", prompt_len=8 * 300 + 13, steps=40),
 })
 
 

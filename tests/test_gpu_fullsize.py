@@ -85,3 +85,11 @@ def test_max_candidates_4000_windows():
 def test_8b_32k_rope():
     # the benchmark shape with the RoPE-aware Quantized tier (Llama-3 base 500000)
     _lockstep("c2", steps=16, rope_base=500000.0)
+
+
+def test_8b_32k_paper_default_eight_token_windows():
+    # the paper's default point with its 8-token windows: sink 5, recent 32, int2,
+    # byte budget 20% with q = 0.70 (244 bf16 + 2025 int2 windows of 4091), routing
+    # every 8 steps, 128 steps
+    ls = _lockstep("c6w8")
+    assert ls.events == 16

@@ -144,3 +144,37 @@ def test_window64_bit_widths(bits):
         ls.close()
     print(f"[lockstep] W 64 bits {bits}: max out err {ls.max_out_err:.2e}, promotions {ls.promotions}",
           flush=True)
+
+
+@pytest.mark.parametrize("bits", [2, 4, 42])
+def test_window8_paper_default(bits):
+    """The paper's 8-token windows at its default point (sink 5, recent 32,
+    routing every 8 steps, byte-budget capacities with q = 0.70) at reduced
+    size: int2 as in the paper, int4, and the mixed tier."""
+    from tests.gpu_harness import Lockstep
+    wl = syn.get_workload("c6w8s").replace(name=f"c6w8s-b{bits}", bits=bits)
+    ls = Lockstep(wl, independent_seqs=[0])
+    print(f"[lockstep] {wl.name} steps={ls.steps}", flush=True)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[lockstep] W 8 bits {bits}: max out err {ls.max_out_err:.2e}, max score err "
+          f"{ls.max_score_err:.2e}, promotions {ls.promotions} over {ls.events} events; "
+          + "; ".join(ls.report_independent()), flush=True)
+
+
+def test_window8_routing_every_step():
+    """8-token windows on the 8B head layout with a routing event after every
+    step (windows age, are admitted, quantized and promoted each step), int4."""
+    from tests.gpu_harness import Lockstep
+    wl = syn.get_workload("c2s").replace(name="w8r1", window=8, group=32, prompt_len=8 * 200 + 3,
+                                         steps=40)
+    ls = Lockstep(wl, independent_seqs=[0])
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[lockstep] W 8 R 1: max out err {ls.max_out_err:.2e}, promotions {ls.promotions}; "
+          + "; ".join(ls.report_independent()), flush=True)
+    assert ls.promotions > 0

@@ -2,7 +2,7 @@
 against the float64 oracle: scores within 1e-4 relative (floor 1e-7 of the
 total), on seeded synthetic prompts: several key blocks with a ragged tail,
 more query rows than one LDS chunk, n_obs = 1, n_obs = T, sinks with partial
-windows, both window sizes, GQA 1 to 8, and the full 32K / 64K prompt
+windows, every window size, GQA 1 to 8, and the full 32K / 64K prompt
 shapes of the 8B and 70B layouts.  Also: bitwise repeatability and the
 prefill that consumes the scores.
 """
@@ -41,6 +41,8 @@ CASES = [
     (1, 4, 4, 32, 256, 1, 0),        # GQA 1, one query, exactly one block
     (1, 16, 2, 64, 40, 40, 3),       # every prompt query observes, one partial block
     (1, 8, 2, 32, 20, 4, 20),        # the whole prompt is sink: no window
+    (1, 32, 8, 8, 1037, 32, 5),      # 8-token windows: eight per 64-key block, sink, ragged tail
+    (2, 8, 2, 8, 300, 9, 0),         # 8-token windows, GQA 4, batch 2
 ]
 
 

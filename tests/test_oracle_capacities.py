@@ -31,6 +31,15 @@ def test_worked_example_paper_default_8b():
     assert budget - b_hist == 151_552
 
 
+def test_paper_default_point_eight_token_windows():
+    """The same budget with the paper's 8-token windows (values in 32-channel groups)."""
+    # M_f = 2 x 8 x 8 x 128 x 2 B + 8 = 32,776;  M_q = 4,096 (int2 codes) + 4,096 (key
+    # scale / zero per channel) + 1,024 (value scale / zero per token and 32 channels) + 10
+    assert window_costs(8, 128, 8, 32, 2) == (32_776, 9_226)
+    # K_f = floor(0.3 x 26,691,993 / 32,776) = floor(244.31), K_q = floor(0.7 x ... / 9,226) = floor(2025.18)
+    assert tier_capacities(26_843_545, 700, 8, 128, 8, 32, 2, 5, 32) == (244, 2025)
+
+
 @pytest.mark.parametrize("q", [0, 150, 500, 700, 999, 1000])
 @pytest.mark.parametrize("bits,W", [(2, 32), (4, 32), (42, 32), (2, 64)])
 def test_floor_properties(q, bits, W):
@@ -59,12 +68,14 @@ def test_library_matches_oracle():
         (8, 32, 2, 5, 32, 26_843_545, 700), (8, 32, 4, 0, 0, 13_421_772, 300),
         (8, 64, 2, 64, 128, 50_000_000, 900), (8, 32, 42, 40, 70, 7_000_000, 550),
         (1, 32, 4, 0, 100, 3_000_000, 0), (4, 64, 2, 3, 0, 1_000_000, 1000),
+        (8, 8, 2, 5, 32, 26_843_545, 700), (8, 8, 42, 0, 16, 5_000_000, 400),
     ]:
+        G = 32 if W == 8 else W
         cfg = qv.Config(batch=1, num_q_heads=4 * H_kv, num_kv_heads=H_kv, window_tokens=W,
                         quant_bits=bits, max_context=65536, capacity_full=0, capacity_quant=0,
                         sink_tokens=sink, recent_tokens=recent)
         assert qv.qevict.capacities_for_budget(cfg, budget, q) == \
-            tier_capacities(budget, q, H_kv, 128, W, W, bits, sink, recent)
+            tier_capacities(budget, q, H_kv, 128, W, G, bits, sink, recent)
     with pytest.raises(qv.QEvictError):
         qv.qevict.capacities_for_budget(cfg, 10, 500)
     with pytest.raises(qv.QEvictError):

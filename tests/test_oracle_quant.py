@@ -112,10 +112,12 @@ def test_error_bound_and_minimality(bits):
     assert np.all((s == 0) | (z + prev * n < x.max(1)))
 
 
-def test_window_layout_groups():
-    """Keys: one (s, z) per channel across the window's tokens; values: per token per G channels."""
+@pytest.mark.parametrize("w,g", [(32, 32), (64, 64), (8, 32)])
+def test_window_layout_groups(w, g):
+    """Keys: one (s, z) per channel across the window's tokens; values: per token per G
+    channels (8-token windows keep 32-channel value groups)."""
     rng = np.random.default_rng(7)
-    h, w, d, g = 2, 32, 128, 32
+    h, d = 2, 128
     k = _bf16_round(rng.normal(size=(h, w, d)))
     v = _bf16_round(rng.normal(size=(h, w, d)))
     e = quantize_window(k, v, 4, g)
@@ -124,9 +126,9 @@ def test_window_layout_groups():
     z, s, c = quantize_groups(k[1, :, 5][None, :], 4)
     assert e["kz"][1, 0, 5] == z[0] and e["ks"][1, 0, 5] == s[0]
     assert np.array_equal(e["kc"][1, :, 5], c[0])
-    # token 7, channels 64..95 of head 0 is one value group
-    z, s, c = quantize_groups(v[0, 7, 64:96][None, :], 4)
-    assert e["vz"][0, 7, 2] == z[0] and np.array_equal(e["vc"][0, 7, 64:96], c[0])
+    # token 7, channels g .. 2g - 1 of head 0 is one value group
+    z, s, c = quantize_groups(v[0, 7, g:2 * g][None, :], 4)
+    assert e["vz"][0, 7, 1] == z[0] and np.array_equal(e["vc"][0, 7, g:2 * g], c[0])
     kh, vh = dequantize_window(e)
-    assert np.all(np.abs(kh - k) <= np.repeat(e["ks"], g, axis=1) / 2)
+    assert np.all(np.abs(kh - k) <= e["ks"] / 2)
     assert np.all(np.abs(vh - v) <= np.repeat(e["vs"], g, axis=2) / 2)
