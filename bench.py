@@ -333,8 +333,10 @@ def main():
     NL = wl.layers if whole_model else args.instances
     LPS = NL if whole_model else 1                 # layer calls per step
     prof_rounds = 4                   # rounds of back-to-back decode_attend timing
-    # + the attention and routing timing rounds and two rounds of routing statistics
-    per_layer = -(-((args.warmup + args.steps) * LPS) // NL) + prof_rounds + 2 + 2 + 1
+    # routing timing and routing statistics each take two routing periods (R steps
+    # of every layer cache, so that every cache routes at least twice)
+    route_rounds = 2 * max(1, wl.retier_interval)
+    per_layer = -(-((args.warmup + args.steps) * LPS) // NL) + prof_rounds + 2 * route_rounds + 1
     asyncr = args.routing == "async"
     R = wl.retier_interval            # routing event after every R-th step of a layer cache
     kf, kq = wl.capacity_full, wl.capacity_quant
@@ -507,7 +509,7 @@ def main():
     lp = None
     if not args.no_kernel_events:
         cache.profile_enable(True)
-        for _ in range(2):
+        for _ in range(route_rounds):
             for l in range(NL):
                 attend(l)
                 route(l)
@@ -517,10 +519,10 @@ def main():
         lp = {k: cache.profile_read(k) for k in (2, 3)}
         cache.profile_enable(False)
 
-    # ---- routing activity: two more (untimed) rounds with the retier stats read back ----
+    # ---- routing activity: more (untimed) rounds with the retier stats read back ----
     promo = react = evict = 0
     n_ev = 0
-    for _ in range(2):
+    for _ in range(route_rounds):
         for l in range(NL):
             attend(l)
         for l in range(NL):

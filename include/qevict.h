@@ -294,12 +294,19 @@ qevict_status qevict_decode_attend(qevict_cache *c, int32_t layer, const uint16_
  * batch totals. */
 qevict_status qevict_retier(qevict_cache *c, int32_t layer, qevict_retier_stats *stats);
 
-/* Manual single-window moves (synchronous), with the same ledger rules:
- * quantize_window moves a Full window to Quantized (quantizing it once, or
- * reactivating its dormant ledger); QEVICT_ERR_CAPACITY if Q already holds
- * K_q windows.  promote_window moves a Quantized window to Full (bf16
- * reconstruction, ledger dormant); QEVICT_ERR_CAPACITY if F is full.
- * QEVICT_ERR_BAD_STATE if the window is not in the source tier. */
+/* Manual single-window moves (synchronous), with the ledger rules of a routing
+ * event (Sec. 4.3, migration-stable quantization and the state-transition
+ * equation; Algorithm 1): quantize_window moves a Full window to Quantized,
+ * quantizing it once (its first demotion: asymmetric codes, keys per channel
+ * across the window's tokens, values per token in groups of G channels, fp16
+ * scale and zero point) or reactivating its dormant ledger without
+ * requantizing; QEVICT_ERR_CAPACITY if Q already holds K_q windows.
+ * promote_window moves a Quantized window to Full: bf16 reconstruction of the
+ * low-bit values z + s c (rounded once), the ledger kept dormant;
+ * QEVICT_ERR_CAPACITY if F already holds K_f windows, QEVICT_ERR_BAD_STATE
+ * under QEVICT_FLAG_NO_PROMOTION.  QEVICT_ERR_BAD_STATE if the window is not
+ * in the source tier; QEVICT_ERR_INVALID_ARG for a sequence or window index
+ * out of range.  The cache's stream is synchronised. */
 qevict_status qevict_quantize_window(qevict_cache *c, int32_t layer, int32_t seq, int32_t window);
 qevict_status qevict_promote_window(qevict_cache *c, int32_t layer, int32_t seq, int32_t window);
 

@@ -77,7 +77,9 @@ __device__ __forceinline__ f32x4 mfma_obs(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// four workgroups per compute unit (at most 128 VGPRs)
+// four workgroups per compute unit (at most 128 VGPRs); W8: 8-token windows (eight
+// per chunk), a separate instantiation so the other window sizes carry none of it
+template <bool W8>
 __global__ __launch_bounds__(256, 4) void k_obs_chunks(ObsArgs a) {
   const int g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -168,7 +170,7 @@ __global__ __launch_bounds__(256, 4) void k_obs_chunks(ObsArgs a) {
         lB += __builtin_amdgcn_exp2f(fmaf(acc[2][i], sc, -mu));
         lB += __builtin_amdgcn_exp2f(fmaf(acc[3][i], sc, -mu));
       }
-      if (wpc == 8) {
+      if constexpr (W8) {
         // 8-token windows: tile kt holds windows 2 kt (lanes lq 0, 1) and 2 kt + 1
         // (lq 2, 3); the pair sums land in lanes lq 0 and 2
 #pragma unroll
@@ -185,7 +187,7 @@ __global__ __launch_bounds__(256, 4) void k_obs_chunks(ObsArgs a) {
       lB = rows_sum(lB);
       if (row < nr) {
         if (lq == 0) cml_out[rg] = make_float2(m, lA + lB);
-        if (wpc <= 2) {
+        if constexpr (!W8) {
           if (lq == 1 && has_a) wl_a[rg] = wpc == 2 ? lA : lA + lB;
           if (lq == 2 && has_b) wl_a[n_rows + rg] = lB;
         }
@@ -286,7 +288,8 @@ __global__ __launch_bounds__(256) void k_obs_windows(ObsArgs a, int wpw) {
 
 hipError_t launch_prefill_scores(const ObsArgs& a, hipStream_t st) {
   if (a.n_w <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_obs_chunks, dim3(a.n_blk, a.H_kv, a.B), dim3(256), 0, st, a);
+  if (a.W == 8) hipLaunchKernelGGL(k_obs_chunks<true>, dim3(a.n_blk, a.H_kv, a.B), dim3(256), 0, st, a);
+  else hipLaunchKernelGGL(k_obs_chunks<false>, dim3(a.n_blk, a.H_kv, a.B), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_obs_rows<16>, dim3((a.n_rows + 15) / 16, a.H_kv, a.B), dim3(256), 0, st, a);

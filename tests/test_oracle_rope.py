@@ -94,8 +94,13 @@ def test_codes_describe_the_pre_rope_keys_and_promotion_rotates_back():
     for w in quant:
         a = sink + w * W
         pos = list(range(a, a + W))
-        pre = rne_bf16(_complex_rotate(k[:, a:a + W], pos, base, -1.0))
-        e = quantize_window(pre, v[:, a:a + W], 4, W)
+        # the pre-RoPE keys the codes describe (the float32 un-rotation rounded to
+        # bf16) agree with the exact float64 un-rotation to within one bf16 step
+        exact = _complex_rotate(k[:, a:a + W], pos, base, -1.0)
+        recipe = rne_bf16(rope_unrotate_f32(k[:, a:a + W], *rope_cos_sin(base, D, pos)).astype(np.float64))
+        assert np.all(np.abs(recipe - exact) <= 2.0 ** -7 * np.abs(exact) + 2.0 ** -133)
+        # and the ledger holds exactly the quantization of those keys
+        e = quantize_window(recipe, v[:, a:a + W], 4, W)
         led = u.ledger[w]
         assert np.array_equal(led["kc"], e["kc"]) and np.array_equal(led["ks"], e["ks"])
         assert np.array_equal(led["kz"], e["kz"]) and np.array_equal(led["vc"], e["vc"])
