@@ -4,10 +4,12 @@
 // One 1024-thread workgroup per sequence:
 //   1. candidates = current Full and Quantized windows (the live list, in
 //      window order) followed by the windows that left the recent region;
-//   2. 64-bit keys (score descending, then window ascending) sorted with a
-//      bitonic network in LDS;
-//   3. sorted position < K_f -> Full, < K_f + K_q -> Quantized, else Evicted
-//      (one-way policy: Full only from candidates that are not Quantized);
+//   2. 64-bit keys (score descending, then window ascending) define the total
+//      order; the keys at positions K_f, K_f + ceil(K_q / 2) and K_f + K_q are
+//      found by selection (histogram refinement), so no full sort is needed;
+//   3. position < K_f -> Full, < K_f + K_q -> Quantized, else Evicted (the
+//      one-way policy, Full only from candidates that are not Quantized,
+//      sorts the keys and counts along the sorted order);
 //   4. Algorithm 1 transitions: promotions keep the ledger dormant, first
 //      demotions request a quantization, dormant ledgers are reactivated,
 //      evictions release slots and delete the ledger;
@@ -308,13 +310,352 @@ __device__ void sort_runs(uint64_t* skey, int n_cand) {
   __syncthreads();
 }
 
+// Minimum and maximum of one 64-bit value per lane across a wave (VALU only).
+template <int J>
+__device__ __forceinline__ void minmax_step(uint64_t& mn, uint64_t& mx, int lane) {
+  const uint64_t a = ((uint64_t)lane_xor<J>((uint32_t)(mn >> 32), lane) << 32) | lane_xor<J>((uint32_t)mn, lane);
+  const uint64_t b = ((uint64_t)lane_xor<J>((uint32_t)(mx >> 32), lane) << 32) | lane_xor<J>((uint32_t)mx, lane);
+  mn = a < mn ? a : mn;
+  mx = b > mx ? b : mx;
+}
+
+// Order statistics of the candidate keys (unique 64-bit values, thread t holding
+// candidates t + k * kRetierThreads, k < kc, c < n_cand): thr[i] = the key at
+// ascending position target[i], or ~0 when target[i] >= n_cand or the target is
+// not asked for (want bit i clear).  Sorted position p < target[i] then holds
+// exactly for the keys below thr[i].
+//
+// Each target keeps a key interval [lo, hi] that contains its key and the rank
+// r of that key within the interval.  A round splits an interval of span 2^m
+// into at most 1024 equal buckets (width 2^(m-10)), counts the keys per bucket
+// and keeps the bucket holding rank r: ten bits of the interval per round, so
+// at most seven rounds for 64-bit keys, and one round when the first split
+// already leaves at most kSelSmall keys in the bucket (the usual case).  The
+// keys of the final interval (at most kSelSmall) are then ranked by pairwise
+// comparison.  LDS: `hist` 3 x 1024 counters, `sel` the intervals and results.
+constexpr int kSelBuckets = 1024;
+constexpr int kSelSmall = 64;
+struct SelLds {
+  int32_t hist[3][kSelBuckets];
+  uint64_t list[3][kSelSmall];
+  uint64_t wmin[kRetierThreads / 64], wmax[kRetierThreads / 64];
+  uint64_t lo[3], hi[3], thr[3];
+  int32_t r[3], cnt[3], nlist[3];
+  // one-round path (select_tiers)
+  uint32_t swmin[kRetierThreads / 64], swmax[kRetierThreads / 64];
+  uint32_t blo[3], bhi[3];
+  int32_t br[3], bcnt[3];
+};
+
+__device__ void select_thresholds(const uint64_t (&key)[kMaxCand / kRetierThreads], int kc, int n_cand,
+                                  const int (&target)[3], int want, SelLds& s, uint64_t (&thr)[3]) {
+  constexpr int PER = kMaxCand / kRetierThreads;
+  constexpr int NW = kRetierThreads / 64;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int i = tid; i < 3 * kSelBuckets; i += kRetierThreads) (&s.hist[0][0])[i] = 0;
+  if (tid < 3) s.nlist[tid] = 0;
+  uint64_t mn = ~0ull, mx = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    if (k < kc && tid + k * kRetierThreads < n_cand) {
+      mn = key[k] < mn ? key[k] : mn;
+      mx = key[k] > mx ? key[k] : mx;
+    }
+  }
+  minmax_step<1>(mn, mx, lane);
+  minmax_step<2>(mn, mx, lane);
+  minmax_step<4>(mn, mx, lane);
+  minmax_step<8>(mn, mx, lane);
+  minmax_step<16>(mn, mx, lane);
+  minmax_step<32>(mn, mx, lane);
+  if (lane == 0) {
+    s.wmin[wave] = mn;
+    s.wmax[wave] = mx;
+  }
+  __syncthreads();
+  mn = ~0ull;
+  mx = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    mn = s.wmin[w] < mn ? s.wmin[w] : mn;
+    mx = s.wmax[w] > mx ? s.wmax[w] : mx;
+  }
+  uint64_t lo[3], hi[3];
+  int r[3], cnt[3];
+  bool act[3];
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {
+    act[i] = ((want >> i) & 1) != 0 && target[i] >= 0 && target[i] < n_cand;
+    lo[i] = mn;
+    hi[i] = mx;
+    r[i] = target[i];
+    cnt[i] = n_cand;
+  }
+  // uniform across the workgroup: every thread holds the same intervals
+  for (int round = 0; round < 8; ++round) {
+    bool refine[3];
+    int sh[3];
+    bool any = false;
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      refine[i] = act[i] && cnt[i] > kSelSmall;
+      const uint64_t span = hi[i] - lo[i];
+      const int bl = span == 0 ? 0 : 64 - __builtin_clzll(span);
+      sh[i] = bl > 10 ? bl - 10 : 0;
+      any |= refine[i];
+    }
+    if (!any) break;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      if (k >= kc || tid + k * kRetierThreads >= n_cand) continue;
+      const uint64_t x = key[k];
+#pragma unroll
+      for (int i = 0; i < 3; ++i)
+        if (refine[i] && x >= lo[i] && x <= hi[i]) atomicAdd(&s.hist[i][(int)((x - lo[i]) >> sh[i])], 1);
+    }
+    __syncthreads();
+    // wave i scans target i's counters (16 per lane), clears them for the next
+    // round and publishes the bucket that holds rank r
+    if (wave < 3 && refine[wave]) {
+      const int i = wave;
+      int h[16];
+      int4* row = (int4*)&s.hist[i][16 * lane];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int4 v = row[q];
+        h[4 * q] = v.x; h[4 * q + 1] = v.y; h[4 * q + 2] = v.z; h[4 * q + 3] = v.w;
+        row[q] = make_int4(0, 0, 0, 0);
+      }
+      int sum = 0;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sum += h[j];
+      const int inc = wave_inclusive_scan(sum);
+      const int exc = inc - sum;
+      if (exc <= r[i] && r[i] < inc) {   // exactly one lane
+        int cum = exc, bk = 0, nr = 0, nc = 0;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          if (nc == 0 && r[i] < cum + h[j]) {
+            bk = 16 * lane + j;
+            nr = r[i] - cum;
+            nc = h[j];
+          }
+          cum += h[j];
+        }
+        const uint64_t nlo = lo[i] + ((uint64_t)bk << sh[i]);
+        const uint64_t wd = (1ull << sh[i]) - 1;
+        const uint64_t top = nlo > ~0ull - wd ? ~0ull : nlo + wd;
+        s.lo[i] = nlo;
+        s.hi[i] = top < hi[i] ? top : hi[i];
+        s.r[i] = nr;
+        s.cnt[i] = nc;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      if (refine[i]) {
+        lo[i] = s.lo[i];
+        hi[i] = s.hi[i];
+        r[i] = s.r[i];
+        cnt[i] = s.cnt[i];
+      }
+    }
+  }
+  // the keys left in each interval, ranked pairwise
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    if (k >= kc || tid + k * kRetierThreads >= n_cand) continue;
+    const uint64_t x = key[k];
+#pragma unroll
+    for (int i = 0; i < 3; ++i)
+      if (act[i] && x >= lo[i] && x <= hi[i]) {
+        const int p = atomicAdd(&s.nlist[i], 1);
+        if (p < kSelSmall) s.list[i][p] = x;
+      }
+  }
+  __syncthreads();
+  if (wave < 3 && act[wave]) {
+    const int i = wave;
+    const int n = cnt[i];
+    const uint64_t x = lane < n ? s.list[i][lane] : ~0ull;
+    int below = 0;
+    for (int j = 0; j < n; ++j) below += s.list[i][j] < x ? 1 : 0;
+    if (lane < n && below == r[i]) s.thr[i] = x;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 3; ++i) thr[i] = act[i] ? s.thr[i] : ~0ull;
+}
+
+// Upper word of a candidate's key: the score part (a monotone map of the float)
+__device__ __forceinline__ uint32_t key_hi(float f) { return (uint32_t)(rank_key(f, 0u) >> 32); }
+
+// Minimum and maximum of one 32-bit value per lane across a wave, valid in lane
+// 63 (row shifts within 16-lane rows, then row broadcasts; DPP, no LDS).
+__device__ __forceinline__ void wave_minmax_u32(uint32_t& mn, uint32_t& mx) {
+#define QV_MM(ctrl, rmask)                                                                   \
+  mn = min(mn, (uint32_t)__builtin_amdgcn_update_dpp((int)mn, (int)mn, ctrl, rmask, 0xF, false)); \
+  mx = max(mx, (uint32_t)__builtin_amdgcn_update_dpp((int)mx, (int)mx, ctrl, rmask, 0xF, false));
+  QV_MM(0x111, 0xF)   // row_shr:1
+  QV_MM(0x112, 0xF)   // row_shr:2
+  QV_MM(0x114, 0xF)   // row_shr:4
+  QV_MM(0x118, 0xF)   // row_shr:8
+  QV_MM(0x142, 0xA)   // row_bcast:15 -> rows 1, 3
+  QV_MM(0x143, 0xC)   // row_bcast:31 -> rows 2, 3
+#undef QV_MM
+}
+
+// Tier positions of the candidates in one histogram round (the usual case).
+// Before this call (ahead of the barrier that follows the first loads) every
+// wave has stored the minimum and maximum upper key word of its candidates in
+// s.swmin / s.swmax, and s.hist[0] and s.nlist are zero.  The range of upper
+// words is cut into at most 1024 equal buckets; for each target the bucket that
+// holds its position, the rank r within it and its count are found.  A key
+// below the bucket lies below the target; a key above it does not; a key in a
+// bucket of one key is the target's own key; in a bucket of more keys its rank
+// among them is compared with r.  A bucket of more than kSelSmall keys (ties or
+// heavy clustering) falls back to the general refinement (select_thresholds).
+// Result: bit i of below[k] is set when key k lies below position target[i]
+// (always set for a target past the last candidate or not asked for).
+__device__ void select_tiers(const uint64_t (&key)[kMaxCand / kRetierThreads], int kc, int n_cand,
+                             const int (&target)[3], int want, SelLds& s,
+                             uint32_t (&below)[kMaxCand / kRetierThreads]) {
+  constexpr int PER = kMaxCand / kRetierThreads;
+  constexpr int NW = kRetierThreads / 64;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  bool act[3];
+  bool any = false;
+  uint32_t all = 0;
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {
+    act[i] = ((want >> i) & 1) != 0 && target[i] >= 0 && target[i] < n_cand;
+    any |= act[i];
+    all |= act[i] ? 0u : 1u << i;
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) below[k] = all;
+  if (!any) return;
+  uint32_t mn = ~0u, mx = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    mn = min(mn, s.swmin[w]);
+    mx = max(mx, s.swmax[w]);
+  }
+  mn = __builtin_amdgcn_readfirstlane(mn);
+  mx = __builtin_amdgcn_readfirstlane(mx);
+  const uint32_t span = mx - mn;
+  const int bl = span == 0 ? 0 : 32 - __builtin_clz(span);
+  const int sh = bl > 10 ? bl - 10 : 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    if (k >= kc || tid + k * kRetierThreads >= n_cand) continue;
+    atomicAdd(&s.hist[0][((uint32_t)(key[k] >> 32) - mn) >> sh], 1);
+  }
+  __syncthreads();
+  // wave i finds target i's bucket (16 counters per lane)
+  if (wave < 3 && act[wave]) {
+    const int i = wave;
+    const int t = target[i];
+    int h[16];
+    const int4* row = (const int4*)&s.hist[0][16 * lane];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int4 v = row[q];
+      h[4 * q] = v.x; h[4 * q + 1] = v.y; h[4 * q + 2] = v.z; h[4 * q + 3] = v.w;
+    }
+    int sum = 0;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) sum += h[j];
+    const int inc = wave_inclusive_scan(sum);
+    const int exc = inc - sum;
+    if (exc <= t && t < inc) {   // exactly one lane
+      // bucket j of this lane: the first whose running end passes t
+      int cum = exc, bk = 0, before = exc, nc = 0;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const bool past = cum + h[j] <= t;
+        bk += past ? 1 : 0;
+        before = past ? cum + h[j] : before;
+        cum += h[j];
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) nc = j == bk ? h[j] : nc;
+      const uint32_t b = (uint32_t)(16 * lane + bk);
+      const uint64_t top = ((uint64_t)b << sh) + ((1ull << sh) - 1);
+      s.blo[i] = mn + (b << sh);
+      s.bhi[i] = mn + (uint32_t)(top < span ? top : span);
+      s.br[i] = t - before;
+      s.bcnt[i] = nc;
+    }
+  }
+  __syncthreads();
+  uint64_t lo[3], hi[3];
+  int r[3], cnt[3];
+  bool big = false, need_list = false;
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {
+    lo[i] = (uint64_t)__builtin_amdgcn_readfirstlane(s.blo[i]) << 32;
+    hi[i] = ((uint64_t)__builtin_amdgcn_readfirstlane(s.bhi[i]) << 32) | 0xFFFFFFFFull;
+    r[i] = __builtin_amdgcn_readfirstlane(s.br[i]);
+    cnt[i] = __builtin_amdgcn_readfirstlane(s.bcnt[i]);
+    big |= act[i] && cnt[i] > kSelSmall;
+    need_list |= act[i] && cnt[i] > 1;
+  }
+  if (big) {
+    uint64_t thr[3];
+    select_thresholds(key, kc, n_cand, target, want, s, thr);
+#pragma unroll
+    for (int k = 0; k < PER; ++k)
+      below[k] = (key[k] < thr[0] ? 1u : 0u) | (key[k] < thr[1] ? 2u : 0u) | (key[k] < thr[2] ? 4u : 0u);
+    return;
+  }
+  if (need_list) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      if (k >= kc || tid + k * kRetierThreads >= n_cand) continue;
+      const uint64_t x = key[k];
+#pragma unroll
+      for (int i = 0; i < 3; ++i)
+        if (act[i] && cnt[i] > 1 && x >= lo[i] && x <= hi[i]) {
+          const int p = atomicAdd(&s.nlist[i], 1);
+          if (p < kSelSmall) s.list[i][p] = x;
+        }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    if (k >= kc || tid + k * kRetierThreads >= n_cand) continue;
+    const uint64_t x = key[k];
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      bool b = true;
+      if (act[i]) {
+        if (x < lo[i]) {
+          b = true;
+        } else if (x > hi[i] || cnt[i] <= 1) {
+          b = false;   // above the bucket, or the target's own key
+        } else {
+          int rk = 0;
+          for (int j = 0; j < cnt[i]; ++j) rk += s.list[i][j] < x ? 1 : 0;
+          b = rk < r[i];
+        }
+      }
+      m |= b ? 1u << i : 0u;
+    }
+    below[k] = m;
+  }
+}
+
 __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   const Geometry& G = a.g;
   const int b = blockIdx.x, tid = threadIdx.x;
   constexpr int NT = kRetierThreads;
   constexpr int PER = kMaxCand / NT;
 
-  __shared__ uint64_t skey[kMaxCand];
+  __shared__ __attribute__((aligned(16))) uint64_t skey[kMaxCand];   // sort keys or SelLds
   __shared__ int32_t sinfo[kMaxCand];
   __shared__ int32_t sa[kMaxCand];
   __shared__ int32_t sown[2 * kMaxCand];      // slot owners: Full slots, then quantized slots
@@ -398,15 +739,46 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       score[w] = v;
     }
   }
+  // tier selection, ahead of the barrier: the range of the candidates' upper key
+  // words per wave, and cleared first-round counters
+  const bool one_way = (G.flags & 1u) != 0;
+  SelLds& sel = *reinterpret_cast<SelLds*>(skey);
+  if (!one_way) {
+    const int lane = tid & 63, wave = tid >> 6;
+    uint32_t wlo = ~0u, whi = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int c = tid + k * NT;
+      if (c < n_fq) {
+        const uint32_t u = key_hi(spec_sc[k]);
+        wlo = min(wlo, u);
+        whi = max(whi, u);
+      }
+      if (c < n_aged) {
+        const uint32_t u = key_hi(spec_aged[k]);
+        wlo = min(wlo, u);
+        whi = max(whi, u);
+      }
+    }
+    wave_minmax_u32(wlo, whi);
+    if (lane == 63) {
+      sel.swmin[wave] = wlo;
+      sel.swmax[wave] = whi;
+    }
+    for (int i = tid; i < kSelBuckets; i += NT) sel.hist[0][i] = 0;
+    if (tid < 3) sel.nlist[tid] = 0;
+  }
   __syncthreads();
 
   int my_w[PER], my_old[PER], my_led[PER], my_fs[PER], my_qs[PER], my_bits[PER];
   float my_sc[PER];
+  uint64_t my_key[PER];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int c = tid + k * NT;
     my_w[k] = -1;
     my_sc[k] = 0.f;
+    my_key[k] = ~0ull;
     if (k >= kc || c >= n_cand) continue;
     if (c < n_fq) {
       const int32_t ref = spec_ref[k], aux = spec_aux[k];
@@ -436,29 +808,35 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       my_bits[k] = 0;
     }
     if (!__builtin_isfinite(my_sc[k])) set_error(counts, ERR_NONFINITE);
-    skey[c] = rank_key(my_sc[k], (uint32_t)c);
+    my_key[k] = rank_key(my_sc[k], (uint32_t)c);
+    if (one_way) skey[c] = my_key[k];
   }
-  int n_pow = 1;
-  while (n_pow < n_cand) n_pow <<= 1;
-  __syncthreads();
-
-  // ---- sort ----
-  if (n_cand <= NT) sort_runs(skey, n_cand);
-  else if (n_pow <= NT) sort_candidates<1>(skey, n_cand, n_pow);
-  else if (n_pow <= 2 * NT) sort_candidates<2>(skey, n_cand, n_pow);
-  else sort_candidates<4>(skey, n_cand, n_pow);
 
   // ---- tier by sorted position ----
-  const bool one_way = (G.flags & 1u) != 0;
+  // info = new tier | (position - K_f) << 8; only whether that rank lies in the
+  // upper half of the Quantized tier is used (mixed widths)
+  const int half_q = (G.K_q + 1) / 2;
+  int my_info[PER];
   if (!one_way) {
-    for (int p = tid; p < n_cand; p += NT) {
-      const int c = (int)(skey[p] & 0xFFFFFFFFu);
-      const int nt = p < G.K_f ? T_FULL : (p < G.K_f + G.K_q ? T_QUANT : T_EVICTED);
-      const int rq = p - G.K_f;
-      sinfo[c] = nt | ((rq < 0 ? 0 : rq) << 8);
+    // the three positions that decide a tier and a width, found by selection
+    // (no full sort): p < K_f <=> key < thr[0], p < K_f + half_q <=> key < thr[1],
+    // p < K_f + K_q <=> key < thr[2]
+    const int target[3] = {G.K_f, G.K_f + half_q, G.K_f + G.K_q};
+    uint32_t bel[PER];
+    select_tiers(my_key, kc, n_cand, target, G.bits_cfg == 42 ? 7 : 5, sel, bel);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int nt = (bel[k] & 1u) ? T_FULL : ((bel[k] & 4u) ? T_QUANT : T_EVICTED);
+      my_info[k] = nt | (((bel[k] & 2u) ? 0 : half_q) << 8);
     }
-    __syncthreads();
   } else {
+    int n_pow = 1;
+    while (n_pow < n_cand) n_pow <<= 1;
+    __syncthreads();
+    if (n_cand <= NT) sort_runs(skey, n_cand);
+    else if (n_pow <= NT) sort_candidates<1>(skey, n_cand, n_pow);
+    else if (n_pow <= 2 * NT) sort_candidates<2>(skey, n_cand, n_pow);
+    else sort_candidates<4>(skey, n_cand, n_pow);
     // Full only from candidates that are not currently Quantized
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
@@ -498,10 +876,14 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       }
     }
     __syncthreads();
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int c = tid + k * NT;
+      my_info[k] = k < kc && c < n_cand ? sinfo[c] : T_EVICTED;
+    }
   }
 
   // ---- transitions; release slots (in the LDS owner tables) ----
-  const int half_q = (G.K_q + 1) / 2;
   int my_nt[PER], my_req[PER], my_nb[PER];
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
@@ -509,7 +891,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     my_req[k] = 0;
     my_nt[k] = T_EVICTED;
     if (k >= kc || c >= n_cand) continue;
-    const int info = sinfo[c];
+    const int info = my_info[k];
     const int nt = info & 0xFF, rq = info >> 8;
     const int old = my_old[k], led = my_led[k];
     my_nt[k] = nt;

@@ -97,8 +97,11 @@ class Lockstep:
                  flags: int = 0, num_splits: int = 0, steps: int | None = None, log=print,
                  capacity_full=None, capacity_quant=None, score_decay: float | None = None,
                  key_norm: bool = False, score_p: float | None = None, observed_init: bool = False,
-                 rope_base: float = 0.0, independent_seqs=None, progress_every: int = 0):
+                 rope_base: float = 0.0, independent_seqs=None, progress_every: int = 0,
+                 init_transform=None):
         self.wl, self.seed = wl, seed
+        # optional map applied to the synthetic prompt scores (e.g. to plant ties)
+        self.init_transform = init_transform
         self.layer_ids = list(layer_ids)
         self.check_seqs = list(range(wl.batch)) if check_seqs is None else list(check_seqs)
         self.steps = wl.steps if steps is None else steps
@@ -247,7 +250,10 @@ class Lockstep:
 
         def gen(b, layer):
             k, v = syn.prompt_kv(wl, self.seed, b, layer)
-            return k, v, syn.init_scores(wl, self.seed, b, layer)
+            init = syn.init_scores(wl, self.seed, b, layer)
+            if self.init_transform is not None:
+                init = np.ascontiguousarray(self.init_transform(init), dtype=np.float32)
+            return k, v, init
 
         for li, layer in enumerate(self.layer_ids):
             with ThreadPoolExecutor(max_workers=min(8, wl.batch)) as ex:

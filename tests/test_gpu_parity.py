@@ -178,3 +178,36 @@ def test_window8_routing_every_step():
     print(f"[lockstep] W 8 R 1: max out err {ls.max_out_err:.2e}, promotions {ls.promotions}; "
           + "; ".join(ls.report_independent()), flush=True)
     assert ls.promotions > 0
+
+
+@pytest.mark.parametrize("pattern", ["all_equal", "three_values", "coarse_grid", "outlier"])
+@pytest.mark.parametrize("wl_name", ["c2s", "c5s"])
+def test_tier_selection_with_tied_scores(wl_name, pattern):
+    """The re-rank kernel selects tier positions by counting keys per bucket of
+    the score range.  Planted prompt scores make buckets hold many equal keys
+    (all equal, three values: the general refinement), a few equal keys
+    (coarse grid: ranked pairwise within the bucket) or squeeze the bulk into
+    one bucket beside a far outlier; tiers must still follow the total order
+    (score descending, then window) at the prefill routing and every later
+    event, on the 8B head layout (int4) and the 70B one (mixed int4 / int2)."""
+    from tests.gpu_harness import Lockstep
+
+    def transform(x):
+        if pattern == "all_equal":
+            return np.ones_like(x)
+        if pattern == "three_values":
+            return np.choose(np.arange(x.size) % 3, [0.5, 1.0, 2.0]).astype(np.float32)
+        if pattern == "coarse_grid":
+            return np.round(x * 8.0) / 8.0
+        y = x.copy()
+        y[y.size // 2] = 1e30
+        return y
+
+    wl = syn.get_workload(wl_name).replace(steps=9)   # the 70B layout routes every 8 steps
+    ls = Lockstep(wl, init_transform=transform)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[lockstep] {wl_name} {pattern}: max out err {ls.max_out_err:.2e}, events {ls.events}",
+          flush=True)
