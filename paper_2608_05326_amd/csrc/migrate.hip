@@ -32,17 +32,10 @@ __device__ __forceinline__ bool quant_params(float lo, float hi, int nbits, uint
 }
 
 // Parameters of one quantization group as the code pass uses them: fp16 zero
-// and scale widened to fp32 (exact), the fp32 reciprocal of the scale, and
-// whether every half-step boundary z + (k + 1/2) s (0 <= k <= n) is exactly
-// representable in fp32 (then the decision needs no float64).
+// and scale widened to fp32 (exact) and the fp32 reciprocal of the scale.
 struct QParams {
-  float z, s, inv_s, exact32;
+  float z, s, inv_s, pad;
 };
-
-__device__ __forceinline__ double fp16_ulp(uint16_t h) {
-  const int e = (h >> 10) & 0x1F;
-  return __builtin_ldexp(1.0, (e > 1 ? e : 1) - 25);
-}
 
 __device__ __forceinline__ QParams group_params(float lo, float hi, int nbits, uint16_t* zb, uint16_t* sb,
                                 int32_t* counts) {
@@ -52,35 +45,26 @@ __device__ __forceinline__ QParams group_params(float lo, float hi, int nbits, u
   p.z = (float)z;
   p.s = (float)s;
   p.inv_s = s > 0.0 ? 1.f / (float)s : 0.f;
-  // z and every k s / 2 are multiples of u; a boundary below 2^24 u in magnitude is exact
-  const double u = fmin(fp16_ulp(*zb), 0.5 * fp16_ulp(*sb));
-  const double span = fabs(z) + (double)(1 << nbits) * s;
-  p.exact32 = span < __builtin_ldexp(u, 24) ? 1.f : 0.f;
+  p.pad = 0.f;
   return p;
 }
 
 // Round-half-even code of x in the group: an fp32 estimate of (x - z) / s
 // (within one of the exact result), then the exact decision against the
-// neighbouring half-step boundaries, without branches.  The boundaries are
-// formed in fp32 when exact for the group, else in float64 where they always
-// are (fp16 operands, |c| <= 16).
+// neighbouring half-step boundaries z + (c +- 1/2) s, formed in float64 where
+// they are exact (fp16 operands, |c| <= 16).  Written without branches or
+// selects between paths, so that the codes of a lane's entries and their
+// parameter loads overlap.
 __device__ __forceinline__ uint32_t quant_code(float x, const QParams& p, int nmax) {
   const float nm = (float)nmax;
   float c = rintf((x - p.z) * p.inv_s);
   c = fminf(fmaxf(c, 0.f), nm);
-  const bool odd = (((int)c) & 1) != 0;
-  bool up, dn;
-  if (p.exact32 != 0.f) {
-    const float hi = fmaf(c + 0.5f, p.s, p.z), lo = fmaf(c - 0.5f, p.s, p.z);
-    up = x > hi || (x == hi && odd);
-    dn = x < lo || (x == lo && odd);
-  } else {
-    const double xd = x, cd = c, z = p.z, s = p.s;
-    const double hi = z + (cd + 0.5) * s, lo = z + (cd - 0.5) * s;
-    up = xd > hi || (xd == hi && odd);
-    dn = xd < lo || (xd == lo && odd);
-  }
-  c = (up && c < nm) ? c + 1.f : ((dn && c > 0.f) ? c - 1.f : c);
+  const int odd = ((int)c) & 1;
+  const double xd = x, cd = c, zd = p.z, sd = p.s;
+  const double hi = zd + (cd + 0.5) * sd, lo = zd + (cd - 0.5) * sd;
+  const int up = ((xd > hi) | ((xd == hi) & odd)) & (c < nm);
+  const int dn = ((xd < lo) | ((xd == lo) & odd)) & (c > 0.f);
+  c += (float)(up - dn);   // at most one of the two holds
   return p.s == 0.f ? 0u : (uint32_t)c;
 }
 
@@ -97,7 +81,6 @@ constexpr int value_group() { return W == 8 ? 32 : W; }
 // LDS row of one token's 128 channels, padded by 16 bytes so that 16-byte
 // accesses to 16 consecutive tokens fall in distinct banks
 constexpr int kLdsRow = kHeadDim + 8;
-__device__ __forceinline__ int entry_half(int area, int e) { return area == 0 ? (e & 3) >> 1 : (e & 7) >> 2; }
 // bf16 chunk (= code entry) index of local chunk cl of channel half h of an area
 __device__ __forceinline__ int part_chunk(int area, int h, int cl) {
   return area == 0 ? (cl >> 1) * 4 + 2 * h + (cl & 1) : (cl >> 2) * 8 + 4 * h + (cl & 3);
@@ -112,10 +95,6 @@ template <bool ROPE>
 __device__ __forceinline__ Halves part_halves(int area, int h) {
   if (ROPE && area == 0) return Halves{0, h == 0 ? 2 : 0};
   return Halves{h, 1};
-}
-template <bool ROPE>
-__device__ __forceinline__ bool owns_entry(int area, int h, int e) {
-  return (ROPE && area == 0) ? h == 0 : entry_half(area, e) == h;
 }
 // RoPE (cos, sin) of position p, channel pair i
 __device__ __forceinline__ float2 rope_cs(const Geometry& G, int p, int i) {
@@ -143,9 +122,27 @@ __device__ __forceinline__ void pack_codes(const Geometry& G, const uint16_t* sk
   constexpr int NG = kHeadDim / W;
   constexpr int nmax = (1 << NB) - 1;
   const int area = part >> 1, h = part & 1;
-  for (int tk = tid; tk < NBLK * 256; tk += kMigrateThreads) {
-    const int comp = tk & 3, L = (tk >> 2) & 63, m = tk >> 8;
-    if (!owns_entry<ROPE>(area, h, (m * 4 + comp) * PER)) continue;
+  // Only the words this part owns are enumerated, one word (m, comp) per wave
+  // pass, so that every lane of a wave forms codes (entry halves: keys by
+  // (e & 3) >> 1, values by (e & 7) >> 2; with RoPE part 0 takes every key word)
+  const bool all_keys = ROPE && area == 0;
+  const int n_own = all_keys ? (h == 0 ? NBLK * 4 : 0) : NBLK * 2;
+  for (int u = tid; u < n_own * 64; u += kMigrateThreads) {
+    const int L = u & 63, o = u >> 6;
+    int m, comp;
+    if (all_keys) {
+      m = o >> 2;
+      comp = o & 3;
+    } else if (area == 0) {
+      m = o >> 1;
+      comp = NB == 4 ? 2 * h + (o & 1) : h + 2 * (o & 1);
+    } else if (NB == 4) {
+      m = 2 * (o >> 2) + h;
+      comp = o & 3;
+    } else {
+      m = o >> 1;
+      comp = 2 * h + (o & 1);
+    }
     const int q = L >> 4, r = L & 15;
     uint32_t wd = 0;
 #pragma unroll
@@ -496,9 +493,12 @@ __device__ __forceinline__ void promote_from_record(const Geometry& G, const uin
   constexpr int PER = 4 / NB;
   const int ng = kHeadDim / G.G;
   const int area = part >> 1, h = part & 1;
-  for (int tk = tid; tk < E * 64; tk += kMigrateThreads) {
-    const int L = tk & 63, ei = tk >> 6;
-    if (!owns_entry<ROPE>(area, h, ei)) continue;
+  // only the entries this part owns, one per wave pass (see pack_codes)
+  const bool all_keys = ROPE && area == 0;
+  const int n_own = all_keys ? (h == 0 ? E : 0) : E / 2;
+  for (int tk = tid; tk < n_own * 64; tk += kMigrateThreads) {
+    const int L = tk & 63, o = tk >> 6;
+    const int ei = all_keys ? o : (area == 0 ? 4 * (o >> 1) + 2 * h + (o & 1) : 8 * (o >> 2) + 4 * h + (o & 3));
     if (ROPE && area == 0) {
       *(u32x4*)(dp + ((int64_t)ei * 64 + L) * 16) = rope_key8<NB>(G, rec, ei, L, p0);
       continue;
