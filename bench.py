@@ -201,15 +201,17 @@ def cpu_baseline(wl, seed, budget_s, units_per_step=1):
                                  wl.sink, wl.recent)
     cfg = OracleConfig(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, wl.group, wl.bits,
                        kf, kq, sink=wl.sink, recent=wl.recent)
-    u = QEvictUnit(cfg, wl.max_context)
+    # decode steps beyond the workload's own count, so that the sample fills the budget
+    n_max = max(wl.steps, 2048)
+    u = QEvictUnit(cfg, wl.prompt_len + n_max)
     k, v = syn.prompt_kv(wl, seed, 0, 0)
     f = syn.bf16_bits_to_f32
     u.prefill(f(k).astype(np.float64), f(v).astype(np.float64), syn.init_scores(wl, seed, 0, 0))
     del k, v
-    qs, ks, vs = syn.decode_inputs(wl, seed, 0, 0, wl.steps)
+    qs, ks, vs = syn.decode_inputs(wl, seed, 0, 0, n_max)
     n = 0
     t0 = time.perf_counter()
-    while n < wl.steps and (n < 3 or time.perf_counter() - t0 < budget_s):
+    while n < n_max and (n < 3 or time.perf_counter() - t0 < budget_s):
         u.step(f(qs[n]).astype(np.float64), f(ks[n]).astype(np.float64), f(vs[n]).astype(np.float64))
         if (n + 1) % wl.retier_interval == 0:
             u.route()
@@ -505,17 +507,23 @@ def main():
         torch.cuda.synchronize()
     # ---- routing kernels: HIP events around every re-rank and migration launch
     # (the library's profile counters, on the stream each runs on) over a few
-    # more rounds; each such duration also holds the launch's dispatch ----
+    # more rounds, with nothing else on the GPU while they run (the attention of
+    # a round finishes first), so that each duration is the routing latency and
+    # not a wait for compute units held by other layers' attention; each such
+    # duration also holds the launch's dispatch ----
     lp = None
     if not args.no_kernel_events:
         cache.profile_enable(True)
         for _ in range(route_rounds):
             for l in range(NL):
                 attend(l)
+            cache.join_routing()
+            torch.cuda.synchronize()
+            for l in range(NL):
                 route(l)
+            cache.join_routing()
+            torch.cuda.synchronize()
             done += NL
-        cache.join_routing()
-        torch.cuda.synchronize()
         lp = {k: cache.profile_read(k) for k in (2, 3)}
         cache.profile_enable(False)
 
