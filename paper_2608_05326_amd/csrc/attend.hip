@@ -267,6 +267,160 @@ __device__ __forceinline__ void fetch_v(const ItemInfo& in, VHalf<W>& vh, int la
   }
 }
 
+// ---- the next window of a wave's run, fetched into the wave's LDS slot ----
+//
+// Direct global-to-LDS loads (16 bytes a lane; the instruction writes lane L's
+// bytes at slot row + 16 L, a whole 1 KiB row), so the next window's bytes are
+// in flight while the current window is computed, without registers to hold
+// them.  The slot holds, one 1 KiB row each, the registers fetch_k / fetch_v
+// would fill for the item's kind: the K registers first, then the V registers;
+// read_slot turns them back into the same registers, with the same lanes and
+// registers zeroed.  Used for 8-token windows (about nine windows a wave at
+// the paper's default point, each loaded while the previous one is computed)
+// with at most four query heads per KV head (compact q*s staging).  With
+// 32-token windows a wave has about two windows, and issuing the next
+// window's 16 loads and copying it out of the LDS cost as much as the overlap
+// gains, so those keep their windows in registers only.
+template <int W, int NHS, bool ROPE>
+constexpr bool use_slot() { return NHS == 1 && !ROPE && W == 8; }
+template <int W>
+constexpr int slot_bytes() { return W == 8 ? 8 * 1024 : 16 * 1024; }
+
+__device__ __forceinline__ void dma16(const void* g, uint8_t* lds_row) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds_row, 16, 0, 0);
+}
+
+template <int W>
+__device__ __forceinline__ void issue_slot(const ItemInfo& in, uint8_t* slot, int lane, int r, int qg,
+                                           const Geometry& G) {
+  const uint8_t* p = in.p;
+  const bool q4 = in.kind == KIND_Q4;
+  if constexpr (W == 8) {
+    const bool row = r < 8, col = qg < 2;
+    if (in.kind == KIND_BF16) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+        if (row) dma16(p + ((kb * 4 + qg) * 8 + r) * 16, slot + kb * 1024);
+      const int64_t vbase = (int64_t)W * kHeadDim * 2;
+#pragma unroll
+      for (int cp = 0; cp < 4; ++cp)
+        if (col) dma16(p + vbase + ((cp * 2 + qg) * 16 + r) * 16, slot + (4 + cp) * 1024);
+    } else {
+      // int2 codes are 8 bytes a lane: the row's upper 8 bytes (the next lane's
+      // codes, or the following area of the record) are not used
+      if (row) dma16(p + (qg * 8 + r) * (q4 ? 16 : 8), slot);
+      const uint8_t* mk = p + meta_k_off(G);
+      dma16(mk + 16 * r, slot + 1024);
+      dma16(mk + 256 + 16 * r, slot + 2 * 1024);
+      if (col) dma16(p + G.qcodes_bytes + (qg * 16 + r) * (q4 ? 16 : 8), slot + 3 * 1024);
+#pragma unroll
+      for (int vg = 0; vg < 4; ++vg)
+        if (col) dma16(p + meta_v_off(G) + (qg * 4 + vg) * 16, slot + (4 + vg) * 1024);
+    }
+  } else {
+    constexpr int TB = W / 16, NC = W / 16, KT = W / 32, NG = kHeadDim / W;
+    static_assert((4 * TB + 8 * KT) * 1024 <= slot_bytes<W>() &&
+                  (2 * NC + 2 + 2 * KT * NG) * 1024 <= slot_bytes<W>(), "rows of the slot");
+    if (in.kind == KIND_BF16) {
+#pragma unroll
+      for (int i = 0; i < 4 * TB; ++i) dma16(p + (i * 64 + lane) * 16, slot + i * 1024);
+      const int64_t vbase = (int64_t)W * kHeadDim * 2;
+#pragma unroll
+      for (int i = 0; i < 8 * KT; ++i) dma16(p + vbase + (i * 64 + lane) * 16, slot + (4 * TB + i) * 1024);
+    } else {
+      const int nld = q4 ? NC : NC / 2;
+#pragma unroll
+      for (int m = 0; m < NC; ++m)
+        if (m < nld) dma16(p + (m * 64 + lane) * 16, slot + m * 1024);
+      const uint8_t* mk = p + meta_k_off(G);
+      dma16(mk + 16 * r, slot + NC * 1024);
+      dma16(mk + 256 + 16 * r, slot + (NC + 1) * 1024);
+#pragma unroll
+      for (int m = 0; m < NC; ++m)
+        if (m < nld) dma16(p + G.qcodes_bytes + (m * 64 + lane) * 16, slot + (NC + 2 + m) * 1024);
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+        for (int vg = 0; vg < NG; ++vg) {
+          const uint8_t* pm = p + meta_v_off(G) + ((kt * 4 + qg) * NG + vg) * 32;
+          const int row0 = 2 * NC + 2 + (kt * NG + vg) * 2;
+          dma16(pm, slot + row0 * 1024);
+          dma16(pm + 16, slot + (row0 + 1) * 1024);
+        }
+    }
+  }
+}
+
+template <int W, bool ROPE>
+__device__ __forceinline__ void read_slot(const ItemInfo& in, const uint8_t* slot, KHalf<W, ROPE>& kh,
+                                          VHalf<W>& vh, int lane, int r, int qg) {
+  const u32x4 z = {0, 0, 0, 0};
+  auto rd = [&](int row) { return *(const u32x4*)(slot + row * 1024 + lane * 16); };
+  const bool q4 = in.kind == KIND_Q4;
+  if constexpr (W == 8) {
+    const bool row = r < 8, col = qg < 2;
+    if (in.kind == KIND_BF16) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) kh.d[kb] = row ? rd(kb) : z;
+#pragma unroll
+      for (int cp = 0; cp < 4; ++cp) vh.d[cp] = col ? rd(4 + cp) : z;
+      vh.d[4] = z;
+    } else {
+      u32x4 c = row ? rd(0) : z;
+      if (!q4) c = (u32x4){c[0], c[1], 0u, 0u};
+      kh.d[0] = c;
+      kh.d[1] = rd(1);
+      kh.d[2] = rd(2);
+      kh.d[3] = z;
+      u32x4 cv = col ? rd(3) : z;
+      if (!q4) cv = (u32x4){cv[0], cv[1], 0u, 0u};
+      vh.d[0] = cv;
+#pragma unroll
+      for (int vg = 0; vg < 4; ++vg) vh.d[1 + vg] = col ? rd(4 + vg) : z;
+    }
+  } else {
+    constexpr int TB = W / 16, NC = W / 16, KT = W / 32, NG = kHeadDim / W;
+    if (in.kind == KIND_BF16) {
+#pragma unroll
+      for (int i = 0; i < 4 * TB; ++i) kh.d[i] = rd(i);
+#pragma unroll
+      for (int i = 0; i < VHalf<W>::N; ++i) vh.d[i] = i < 8 * KT ? rd(4 * TB + i) : z;
+    } else {
+      const int nld = q4 ? NC : NC / 2;
+#pragma unroll
+      for (int i = 0; i < KHalf<W, ROPE>::N; ++i) kh.d[i] = z;
+#pragma unroll
+      for (int m = 0; m < NC; ++m)
+        if (m < nld) kh.d[m] = rd(m);
+      kh.d[NC] = rd(NC);
+      kh.d[NC + 1] = rd(NC + 1);
+#pragma unroll
+      for (int i = 0; i < VHalf<W>::N; ++i) vh.d[i] = z;
+#pragma unroll
+      for (int m = 0; m < NC; ++m)
+        if (m < nld) vh.d[m] = rd(NC + 2 + m);
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+        for (int vg = 0; vg < NG; ++vg) {
+          const int row0 = 2 * NC + 2 + (kt * NG + vg) * 2;
+          vh.d[NC + (kt * NG + vg) * 2] = rd(row0);
+          vh.d[NC + 1 + (kt * NG + vg) * 2] = rd(row0 + 1);
+        }
+    }
+  }
+}
+
+// Offset of a q*s operand entry in the per-wave staging area: the B operand of
+// the QK^T MFMA, lane L = 16 q + r holding channels 8 q .. of block kb for head
+// r.  With at most four query heads per KV head only lanes r < 4 carry heads,
+// and the staging area holds just those 16 lanes (the others read zeros).
+template <bool COMPACT>
+__device__ __forceinline__ int qst_off(int hilo, int kb, int L) {
+  if constexpr (COMPACT) return ((hilo * 4 + kb) * 16 + 4 * (L >> 4) + (L & 15)) * 16;
+  else return ((hilo * 4 + kb) * 64 + L) * 16;
+}
+
 // QK^T and the online-softmax update of one window: probabilities in p_,
 // the window's (reference, sum) pair in m_w, l_w.  The open window takes this
 // step's key (and stores it into its ring slot).
@@ -391,6 +545,7 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
                                           int qg, int r, float (&p_)[row_tiles<W>()][4], float* m_w,
                                           float* l_w) {
   constexpr int TB = row_tiles<W>();
+  constexpr bool CQ = use_slot<W, NHS, ROPE>();   // compact q*s staging
   const Geometry& G = a.g;
   const int gqa = G.gqa;
   const int ntok = in.ntok;
@@ -467,8 +622,8 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
       if (hh < gqa) {
         const int dst = 16 * (r & 3) + hh;   // lane of the B operand: head hh, channel group r & 3
         const int kb = r >> 2;
-        *(u32x4*)(qlds + ((0 * 4 + kb) * 64 + dst) * 16) = __builtin_bit_cast(u32x4, hi8);
-        *(u32x4*)(qlds + ((1 * 4 + kb) * 64 + dst) * 16) = __builtin_bit_cast(u32x4, lo8);
+        *(u32x4*)(qlds + qst_off<CQ>(0, kb, dst)) = __builtin_bit_cast(u32x4, hi8);
+        *(u32x4*)(qlds + qst_off<CQ>(1, kb, dst)) = __builtin_bit_cast(u32x4, lo8);
       }
       bias_k[k] = row16_sum(bsum);   // q . z of head qg + 4k (same value in all 16 lanes)
     }
@@ -482,8 +637,13 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
     f16x8 qhi[4], qlo[4];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      qhi[kb] = __builtin_bit_cast(f16x8, ld16(qlds + ((0 * 4 + kb) * 64 + lane) * 16));
-      qlo[kb] = __builtin_bit_cast(f16x8, ld16(qlds + ((1 * 4 + kb) * 64 + lane) * 16));
+      if (!CQ || r < 4) {
+        qhi[kb] = __builtin_bit_cast(f16x8, ld16(qlds + qst_off<CQ>(0, kb, lane)));
+        qlo[kb] = __builtin_bit_cast(f16x8, ld16(qlds + qst_off<CQ>(1, kb, lane)));
+      } else {
+        qhi[kb] = (f16x8){};
+        qlo[kb] = (f16x8){};
+      }
     }
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
@@ -699,6 +859,12 @@ __device__ __forceinline__ void process_v(const ItemInfo& in, VHalf<W>& vh, Wave
 }
 
 constexpr int kAttnSmemFixed = 4 * 16 * 130 * 4;   // q*s staging per wave / end-of-split merge
+// Dynamic LDS of a workgroup before its live-list entries: the q*s staging of
+// the four waves (compact when the LDS slots are used: the slots are a static
+// array of their own, which also holds the end-of-split merge; otherwise the
+// merge reuses the staging area)
+template <int W, int NHS, bool ROPE>
+constexpr int attn_smem_fixed() { return use_slot<W, NHS, ROPE>() ? 4 * 2048 : kAttnSmemFixed; }
 
 // MINB workgroups of four waves per compute unit: at most 512 / MINB VGPRs per lane
 template <int W, int NHS, int MINB, bool ROPE>
@@ -710,8 +876,11 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   const int gqa = G.gqa;
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  uint8_t* qlds = smem + wave * 8192;   // [hi/lo][kb][lane] x 16 B
-  int32_t* s_ref = (int32_t*)(smem + kAttnSmemFixed);   // live-list entries
+  constexpr bool SLOT = use_slot<W, NHS, ROPE>();
+  // q*s staging: [hi/lo][kb][lane] x 16 B (compact: lanes r < 4 only)
+  uint8_t* qlds = smem + wave * (SLOT ? 2048 : 8192);
+  uint8_t* mo_base = smem;   // end-of-split merge of the four waves
+  int32_t* s_ref = (int32_t*)(smem + attn_smem_fixed<W, NHS, ROPE>());   // live-list entries
 
   uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
   const int32_t* counts = (const int32_t*)(ub + a.L.counts);
@@ -762,7 +931,7 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   }
   // zero this lane's q*s operand slots (padded heads keep zeros)
 #pragma unroll
-  for (int i = 0; i < 8; ++i) *(u32x4*)(qlds + (i * 64 + lane) * 16) = (u32x4){0, 0, 0, 0};
+  for (int i = 0; i < (SLOT ? 2 : 8); ++i) *(u32x4*)(qlds + (i * 64 + lane) * 16) = (u32x4){0, 0, 0, 0};
 
   // ---- this wave's item range: from the plan, else computed here ----
   const int n_extra = a.n_ring + a.n_sink_items;
@@ -822,8 +991,8 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
     if (n_all == 0 && tid < 5) s_range[tid] = 0;
     __syncthreads();
 
-    first = s_range[wave];
-    last = s_range[wave + 1];
+    first = __builtin_amdgcn_readfirstlane(s_range[wave]);
+    last = __builtin_amdgcn_readfirstlane(s_range[wave + 1]);
   }
 
   WaveState st;
@@ -853,6 +1022,7 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
       } else {
         ref = s_ref[it];
       }
+      ref = __builtin_amdgcn_readfirstlane(ref);   // one item per wave: scalar branches on its kind
       in.kind = ref >> 28;
       const int64_t slot = ref & 0x0FFFFFFF;
       in.p = in.kind == KIND_BF16 ? fpool + slot * G.fslot_bytes + g * G.fhead_bytes
@@ -876,27 +1046,58 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   VHalf<W> V;
   float p_[TB][4];
   float m_w, l_w;
-  for (int it = first; it < last; ++it) {
-    const ItemInfo ia = info(it);
-    fetch_k<W, ROPE>(ia, KA, lane, r, G);
-    fetch_v<W>(ia, V, lane, qg, G);
-    process_k<W, NHS, ROPE>(ia, KA, st, qop, qf, qlds, a, b, g, lane, qg, r, p_, &m_w, &l_w);
-    process_v<W, NHS>(ia, V, st, p_, m_w, l_w, a, b, g, qg, r, mref);
+  if constexpr (SLOT) {
+    // Every window of the run goes through the wave's LDS slot: wait for it,
+    // move it to the registers, start the next window's loads into the slot,
+    // then compute, so that each window's loads overlap the previous window's
+    // computation.  No register-destination load is pending while slot loads
+    // are in flight (the compiler would then wait for all of them).  A
+    // separate array, so that the compiler can tell the slot from the q*s
+    // staging.
+    __shared__ __attribute__((aligned(16))) uint8_t s_slots[4 * slot_bytes<W>()];
+    uint8_t* slot = s_slots + wave * slot_bytes<W>();   // this wave's next window
+    mo_base = s_slots;
+    if (first < last) {
+      ItemInfo ia = info(first);
+      issue_slot<W>(ia, slot, lane, r, qg, G);
+      for (int it = first; it < last; ++it) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        read_slot<W, ROPE>(ia, slot, KA, V, lane, r, qg);
+        wave_sync_lds();
+        const bool has = it + 1 < last;
+        const ItemInfo ib = info(has ? it + 1 : it);   // (no conditional copy of the record)
+        if (has) issue_slot<W>(ib, slot, lane, r, qg, G);
+        __builtin_amdgcn_sched_barrier(0);
+        process_k<W, NHS, ROPE>(ia, KA, st, qop, qf, qlds, a, b, g, lane, qg, r, p_, &m_w, &l_w);
+        process_v<W, NHS>(ia, V, st, p_, m_w, l_w, a, b, g, qg, r, mref);
+        ia = ib;
+      }
+    }
+  } else {
+    for (int it = first; it < last; ++it) {
+      const ItemInfo ia = info(it);
+      fetch_k<W, ROPE>(ia, KA, lane, r, G);
+      fetch_v<W>(ia, V, lane, qg, G);
+      process_k<W, NHS, ROPE>(ia, KA, st, qop, qf, qlds, a, b, g, lane, qg, r, p_, &m_w, &l_w);
+      process_v<W, NHS>(ia, V, st, p_, m_w, l_w, a, b, g, qg, r, mref);
+    }
   }
 
   // ---- merge the 4 waves of this split in LDS, write the split partial ----
+  if constexpr (SLOT) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the last slot loads
   __syncthreads();
-  float* mo = (float*)smem;   // [wave][head < 16][130]
+  constexpr int MH = SLOT ? 4 : 16;   // heads per wave in the merge buffer (gqa <= MH)
+  float* mo = (float*)mo_base;        // [wave][head < MH][130]
   if (qg == 0 && r < gqa) {
-    mo[(wave * 16 + r) * 130 + 128] = st.m;
-    mo[(wave * 16 + r) * 130 + 129] = st.l;
+    mo[(wave * MH + r) * 130 + 128] = st.m;
+    mo[(wave * MH + r) * 130 + 129] = st.l;
   }
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const int row = 4 * qg + v;
     if (row < gqa) {
 #pragma unroll
-      for (int cb = 0; cb < 8; ++cb) mo[(wave * 16 + row) * 130 + 16 * cb + r] = st.o[cb][v];
+      for (int cb = 0; cb < 8; ++cb) mo[(wave * MH + row) * 130 + 16 * cb + r] = st.o[cb][v];
     }
   }
   __syncthreads();
@@ -906,16 +1107,16 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
     const int h = idx >> 7, c = idx & 127;
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, mo[(w * 16 + h) * 130 + 128]);
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, mo[(w * MH + h) * 130 + 128]);
     float o = 0.f, L = 0.f;
     if (M > -INFINITY) {
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        const float mw = mo[(w * 16 + h) * 130 + 128];
+        const float mw = mo[(w * MH + h) * 130 + 128];
         if (mw > -INFINITY) {
           const float f = __builtin_amdgcn_exp2f(mw - M);
-          o += mo[(w * 16 + h) * 130 + c] * f;
-          L += mo[(w * 16 + h) * 130 + 129] * f;
+          o += mo[(w * MH + h) * 130 + c] * f;
+          L += mo[(w * MH + h) * 130 + 129] * f;
         }
       }
     }
@@ -1156,38 +1357,33 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(AttnArgs a) {
 
 // ---- launchers -------------------------------------------------------------
 namespace qv {
-hipError_t launch_attend(const AttnArgs& a, hipStream_t st) {
+template <int W, int NHS, bool ROPE>
+hipError_t launch_attend_t(const AttnArgs& a, hipStream_t st) {
   dim3 grid(a.g.n_split, a.g.H_kv, a.g.B);
-  const int nhs = (a.g.gqa + 3) / 4;
-  const size_t smem = kAttnSmemFixed + 4 * (size_t)(a.g.max_fq + 1);
-  auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, grid, dim3(kAttnThreads), smem, st, a);
-  };
-  // pipelined window loop where the extra K buffer keeps two waves per SIMD
-  if (a.g.rope) {
-    if (a.g.W == 32) {
-      if (nhs == 1) go(k_attend<32, 1, 2, true>);
-      else if (nhs == 2) go(k_attend<32, 2, 2, true>);
-      else go(k_attend<32, 4, 2, true>);
-    } else {
-      if (nhs == 1) go(k_attend<64, 1, 2, true>);
-      else if (nhs == 2) go(k_attend<64, 2, 2, true>);
-      else go(k_attend<64, 4, 2, true>);
-    }
-  } else if (a.g.W == 8) {
-    if (nhs == 1) go(k_attend<8, 1, 2, false>);
-    else if (nhs == 2) go(k_attend<8, 2, 2, false>);
-    else go(k_attend<8, 4, 2, false>);
-  } else if (a.g.W == 32) {
-    if (nhs == 1) go(k_attend<32, 1, 2, false>);
-    else if (nhs == 2) go(k_attend<32, 2, 2, false>);
-    else go(k_attend<32, 4, 2, false>);
-  } else {
-    if (nhs == 1) go(k_attend<64, 1, 2, false>);
-    else if (nhs == 2) go(k_attend<64, 2, 2, false>);
-    else go(k_attend<64, 4, 2, false>);
-  }
+  const size_t smem = attn_smem_fixed<W, NHS, ROPE>() + 4 * (size_t)(a.g.max_fq + 1);
+  if (smem > 160 * 1024) return hipErrorInvalidValue;   // live list too long for the LDS
+  hipLaunchKernelGGL((k_attend<W, NHS, 2, ROPE>), grid, dim3(kAttnThreads), smem, st, a);
   return hipGetLastError();
+}
+
+hipError_t launch_attend(const AttnArgs& a, hipStream_t st) {
+  const int nhs = (a.g.gqa + 3) / 4;
+  auto by_heads = [&](auto w, auto rope) -> hipError_t {
+    constexpr int Wv = decltype(w)::value;
+    constexpr bool Rv = decltype(rope)::value;
+    if (nhs == 1) return launch_attend_t<Wv, 1, Rv>(a, st);
+    if (nhs == 2) return launch_attend_t<Wv, 2, Rv>(a, st);
+    return launch_attend_t<Wv, 4, Rv>(a, st);
+  };
+  using T = std::true_type;
+  using F = std::false_type;
+  if (a.g.rope) {
+    if (a.g.W == 32) return by_heads(std::integral_constant<int, 32>{}, T{});
+    return by_heads(std::integral_constant<int, 64>{}, T{});
+  }
+  if (a.g.W == 8) return by_heads(std::integral_constant<int, 8>{}, F{});
+  if (a.g.W == 32) return by_heads(std::integral_constant<int, 32>{}, F{});
+  return by_heads(std::integral_constant<int, 64>{}, F{});
 }
 
 hipError_t launch_merge(const AttnArgs& a, hipStream_t st) {
