@@ -269,145 +269,74 @@ __device__ __forceinline__ void fetch_v(const ItemInfo& in, VHalf<W>& vh, int la
 
 // ---- the next window of a wave's run, fetched into the wave's LDS slot ----
 //
-// Direct global-to-LDS loads (16 bytes a lane; the instruction writes lane L's
-// bytes at slot row + 16 L, a whole 1 KiB row), so the next window's bytes are
-// in flight while the current window is computed, without registers to hold
-// them.  The slot holds, one 1 KiB row each, the registers fetch_k / fetch_v
-// would fill for the item's kind: the K registers first, then the V registers;
-// read_slot turns them back into the same registers, with the same lanes and
-// registers zeroed.  Used for 8-token windows (about nine windows a wave at
-// the paper's default point, each loaded while the previous one is computed)
-// with at most four query heads per KV head (compact q*s staging).  With
-// 32-token windows a wave has about two windows, and issuing the next
-// window's 16 loads and copying it out of the LDS cost as much as the overlap
-// gains, so those keep their windows in registers only.
+// 8-token windows: direct global-to-LDS loads (16 bytes a lane; the
+// instruction writes lane L's bytes at slot row + 16 L) copy the window's
+// record as it lies in its pool -- 4 KiB for a bf16 window, at most 2 KiB for a
+// quantized record -- so the next window's bytes are in flight while the
+// current window is computed, without registers to hold them.  read_slot then
+// gathers the operand registers fetch_k / fetch_v would fill (lanes outside a
+// window's operand lanes zeroed), many lanes reading the same LDS word where
+// the registers repeat (key scale / zero, value scale / zero).  Used with at
+// most four query heads per KV head (compact q*s staging, so that two
+// workgroups per compute unit keep their LDS).  With 32-token windows a wave
+// has about two windows, and issuing the next window's loads and copying it out
+// of the LDS cost as much as the overlap gains, so those keep their windows in
+// registers only.
 template <int W, int NHS, bool ROPE>
 constexpr bool use_slot() { return NHS == 1 && !ROPE && W == 8; }
 template <int W>
-constexpr int slot_bytes() { return W == 8 ? 8 * 1024 : 16 * 1024; }
+constexpr int slot_bytes() { return 4 * 1024; }
 
 __device__ __forceinline__ void dma16(const void* g, uint8_t* lds_row) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds_row, 16, 0, 0);
 }
 
+// bytes of the item's record: a bf16 window (keys then values), or a quantized
+// record (key codes, value codes, key scale / zero, value scale / zero)
 template <int W>
-__device__ __forceinline__ void issue_slot(const ItemInfo& in, uint8_t* slot, int lane, int r, int qg,
-                                           const Geometry& G) {
-  const uint8_t* p = in.p;
-  const bool q4 = in.kind == KIND_Q4;
-  if constexpr (W == 8) {
-    const bool row = r < 8, col = qg < 2;
-    if (in.kind == KIND_BF16) {
+__device__ __forceinline__ int slot_record_bytes(const ItemInfo& in, const Geometry& G) {
+  return in.kind == KIND_BF16 ? 2 * W * kHeadDim * 2 : (int)G.qrec_bytes;
+}
+
+template <int W>
+__device__ __forceinline__ void issue_slot(const ItemInfo& in, uint8_t* slot, int lane, const Geometry& G) {
+  static_assert(W == 8, "8-token windows");
+  const int n = slot_record_bytes<W>(in, G);
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-        if (row) dma16(p + ((kb * 4 + qg) * 8 + r) * 16, slot + kb * 1024);
-      const int64_t vbase = (int64_t)W * kHeadDim * 2;
-#pragma unroll
-      for (int cp = 0; cp < 4; ++cp)
-        if (col) dma16(p + vbase + ((cp * 2 + qg) * 16 + r) * 16, slot + (4 + cp) * 1024);
-    } else {
-      // int2 codes are 8 bytes a lane: the row's upper 8 bytes (the next lane's
-      // codes, or the following area of the record) are not used
-      if (row) dma16(p + (qg * 8 + r) * (q4 ? 16 : 8), slot);
-      const uint8_t* mk = p + meta_k_off(G);
-      dma16(mk + 16 * r, slot + 1024);
-      dma16(mk + 256 + 16 * r, slot + 2 * 1024);
-      if (col) dma16(p + G.qcodes_bytes + (qg * 16 + r) * (q4 ? 16 : 8), slot + 3 * 1024);
-#pragma unroll
-      for (int vg = 0; vg < 4; ++vg)
-        if (col) dma16(p + meta_v_off(G) + (qg * 4 + vg) * 16, slot + (4 + vg) * 1024);
-    }
-  } else {
-    constexpr int TB = W / 16, NC = W / 16, KT = W / 32, NG = kHeadDim / W;
-    static_assert((4 * TB + 8 * KT) * 1024 <= slot_bytes<W>() &&
-                  (2 * NC + 2 + 2 * KT * NG) * 1024 <= slot_bytes<W>(), "rows of the slot");
-    if (in.kind == KIND_BF16) {
-#pragma unroll
-      for (int i = 0; i < 4 * TB; ++i) dma16(p + (i * 64 + lane) * 16, slot + i * 1024);
-      const int64_t vbase = (int64_t)W * kHeadDim * 2;
-#pragma unroll
-      for (int i = 0; i < 8 * KT; ++i) dma16(p + vbase + (i * 64 + lane) * 16, slot + (4 * TB + i) * 1024);
-    } else {
-      const int nld = q4 ? NC : NC / 2;
-#pragma unroll
-      for (int m = 0; m < NC; ++m)
-        if (m < nld) dma16(p + (m * 64 + lane) * 16, slot + m * 1024);
-      const uint8_t* mk = p + meta_k_off(G);
-      dma16(mk + 16 * r, slot + NC * 1024);
-      dma16(mk + 256 + 16 * r, slot + (NC + 1) * 1024);
-#pragma unroll
-      for (int m = 0; m < NC; ++m)
-        if (m < nld) dma16(p + G.qcodes_bytes + (m * 64 + lane) * 16, slot + (NC + 2 + m) * 1024);
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-        for (int vg = 0; vg < NG; ++vg) {
-          const uint8_t* pm = p + meta_v_off(G) + ((kt * 4 + qg) * NG + vg) * 32;
-          const int row0 = 2 * NC + 2 + (kt * NG + vg) * 2;
-          dma16(pm, slot + row0 * 1024);
-          dma16(pm + 16, slot + (row0 + 1) * 1024);
-        }
-    }
+  for (int row = 0; row < slot_bytes<W>() / 1024; ++row) {
+    if (row * 1024 >= n) break;   // uniform
+    if (row * 1024 + lane * 16 < n) dma16(in.p + row * 1024 + lane * 16, slot + row * 1024);
   }
 }
 
 template <int W, bool ROPE>
 __device__ __forceinline__ void read_slot(const ItemInfo& in, const uint8_t* slot, KHalf<W, ROPE>& kh,
-                                          VHalf<W>& vh, int lane, int r, int qg) {
+                                          VHalf<W>& vh, int lane, int r, int qg, const Geometry& G) {
+  static_assert(W == 8, "8-token windows");
   const u32x4 z = {0, 0, 0, 0};
-  auto rd = [&](int row) { return *(const u32x4*)(slot + row * 1024 + lane * 16); };
-  const bool q4 = in.kind == KIND_Q4;
-  if constexpr (W == 8) {
-    const bool row = r < 8, col = qg < 2;
-    if (in.kind == KIND_BF16) {
+  auto rd = [&](int off) { return *(const u32x4*)(slot + off); };
+  auto rd8 = [&](int off) {
+    const uint2 v = *(const uint2*)(slot + off);
+    return (u32x4){v.x, v.y, 0u, 0u};
+  };
+  const bool row = r < 8, col = qg < 2;
+  if (in.kind == KIND_BF16) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) kh.d[kb] = row ? rd(kb) : z;
+    for (int kb = 0; kb < 4; ++kb) kh.d[kb] = row ? rd(((kb * 4 + qg) * 8 + r) * 16) : z;
+    const int vbase = W * kHeadDim * 2;
 #pragma unroll
-      for (int cp = 0; cp < 4; ++cp) vh.d[cp] = col ? rd(4 + cp) : z;
-      vh.d[4] = z;
-    } else {
-      u32x4 c = row ? rd(0) : z;
-      if (!q4) c = (u32x4){c[0], c[1], 0u, 0u};
-      kh.d[0] = c;
-      kh.d[1] = rd(1);
-      kh.d[2] = rd(2);
-      kh.d[3] = z;
-      u32x4 cv = col ? rd(3) : z;
-      if (!q4) cv = (u32x4){cv[0], cv[1], 0u, 0u};
-      vh.d[0] = cv;
-#pragma unroll
-      for (int vg = 0; vg < 4; ++vg) vh.d[1 + vg] = col ? rd(4 + vg) : z;
-    }
+    for (int cp = 0; cp < 4; ++cp) vh.d[cp] = col ? rd(vbase + ((cp * 2 + qg) * 16 + r) * 16) : z;
+    vh.d[4] = z;
   } else {
-    constexpr int TB = W / 16, NC = W / 16, KT = W / 32, NG = kHeadDim / W;
-    if (in.kind == KIND_BF16) {
+    const bool q4 = in.kind == KIND_Q4;
+    const int qc = (int)G.qcodes_bytes, mk = (int)meta_k_off(G), mv = (int)meta_v_off(G);
+    kh.d[0] = row ? (q4 ? rd((qg * 8 + r) * 16) : rd8((qg * 8 + r) * 8)) : z;
+    kh.d[1] = rd(mk + 16 * r);
+    kh.d[2] = rd(mk + 256 + 16 * r);
+    kh.d[3] = z;
+    vh.d[0] = col ? (q4 ? rd(qc + (qg * 16 + r) * 16) : rd8(qc + (qg * 16 + r) * 8)) : z;
 #pragma unroll
-      for (int i = 0; i < 4 * TB; ++i) kh.d[i] = rd(i);
-#pragma unroll
-      for (int i = 0; i < VHalf<W>::N; ++i) vh.d[i] = i < 8 * KT ? rd(4 * TB + i) : z;
-    } else {
-      const int nld = q4 ? NC : NC / 2;
-#pragma unroll
-      for (int i = 0; i < KHalf<W, ROPE>::N; ++i) kh.d[i] = z;
-#pragma unroll
-      for (int m = 0; m < NC; ++m)
-        if (m < nld) kh.d[m] = rd(m);
-      kh.d[NC] = rd(NC);
-      kh.d[NC + 1] = rd(NC + 1);
-#pragma unroll
-      for (int i = 0; i < VHalf<W>::N; ++i) vh.d[i] = z;
-#pragma unroll
-      for (int m = 0; m < NC; ++m)
-        if (m < nld) vh.d[m] = rd(NC + 2 + m);
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-        for (int vg = 0; vg < NG; ++vg) {
-          const int row0 = 2 * NC + 2 + (kt * NG + vg) * 2;
-          vh.d[NC + (kt * NG + vg) * 2] = rd(row0);
-          vh.d[NC + 1 + (kt * NG + vg) * 2] = rd(row0 + 1);
-        }
-    }
+    for (int vg = 0; vg < 4; ++vg) vh.d[1 + vg] = col ? rd(mv + (qg * 4 + vg) * 16) : z;
   }
 }
 
@@ -1059,14 +988,14 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
     mo_base = s_slots;
     if (first < last) {
       ItemInfo ia = info(first);
-      issue_slot<W>(ia, slot, lane, r, qg, G);
+      issue_slot<W>(ia, slot, lane, G);
       for (int it = first; it < last; ++it) {
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        read_slot<W, ROPE>(ia, slot, KA, V, lane, r, qg);
+        read_slot<W, ROPE>(ia, slot, KA, V, lane, r, qg, G);
         wave_sync_lds();
         const bool has = it + 1 < last;
         const ItemInfo ib = info(has ? it + 1 : it);   // (no conditional copy of the record)
-        if (has) issue_slot<W>(ib, slot, lane, r, qg, G);
+        if (has) issue_slot<W>(ib, slot, lane, G);
         __builtin_amdgcn_sched_barrier(0);
         process_k<W, NHS, ROPE>(ia, KA, st, qop, qf, qlds, a, b, g, lane, qg, r, p_, &m_w, &l_w);
         process_v<W, NHS>(ia, V, st, p_, m_w, l_w, a, b, g, qg, r, mref);
