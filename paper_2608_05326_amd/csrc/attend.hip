@@ -822,14 +822,22 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   // live list with their cost prefixes (and the previous entry's), queries ----
   const int n_fq = __builtin_amdgcn_readfirstlane(counts[CNT_ITEMS]);
   const int base_cost = __builtin_amdgcn_readfirstlane(counts[CNT_COST]);
-  // the re-rank kernel's split plan for this step (first item, end item, first refs)
-  const bool plan_ok = __builtin_amdgcn_readfirstlane(counts[CNT_PLAN_T]) == a.T;
-  const int32_t* prec = (const int32_t*)(ub + a.L.plan) +
-                        (s * 4 + __builtin_amdgcn_readfirstlane(wave)) * kPlanRec;
-  static_assert(kPlanRec == 8, "plan record: first, end, 6 refs");
-  const int p_first = __builtin_amdgcn_readfirstlane(prec[0]);
-  const int p_last = __builtin_amdgcn_readfirstlane(prec[1]);
-  const int p_refs = lane < kPlanRefs ? prec[2 + lane] : 0;   // lane k: ref of item first + k
+  // the re-rank kernel's split plans (first item, end item, first refs): this
+  // wave's record in both slots, then the one whose step range holds T
+  static_assert(kPlanSlots == 2 && kPlanRec == 8, "plan record: first, end, 6 refs");
+  const int u_rec = s * 4 + __builtin_amdgcn_readfirstlane(wave);
+  const int32_t* prec0 = (const int32_t*)(ub + a.L.plan) + u_rec * kPlanRec;
+  const int32_t* prec1 = prec0 + 4 * G.n_split * kPlanRec;
+  int ptag[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) ptag[j] = __builtin_amdgcn_readfirstlane(counts[CNT_PLAN_T0 + j]);
+  const int rec0 = lane < kPlanRec ? prec0[lane] : 0;   // lane k: record word k
+  const int rec1 = lane < kPlanRec ? prec1[lane] : 0;
+  const bool in0 = ptag[0] <= a.T && a.T <= ptag[1];
+  const bool plan_ok = in0 || (ptag[2] <= a.T && a.T <= ptag[3]);
+  const int rec = in0 ? rec0 : rec1;
+  const int p_first = __builtin_amdgcn_readlane(rec, 0);
+  const int p_last = __builtin_amdgcn_readlane(rec, 1);
   int32_t lc[4], lp[4], lr[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
@@ -911,11 +919,25 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
         place(i, c0, c1);
       }
     }
-    for (int i = tid + 4 * kAttnThreads; i < n_all; i += kAttnThreads) {   // long lists
-      if (i < n_fq) s_ref[i] = iref[i];
-      const int c1 = i <= n_fq ? icost[i] : base_cost + (i - n_fq) * cF;
-      const int c0 = i - 1 <= n_fq ? icost[i - 1] : base_cost + (i - 1 - n_fq) * cF;
-      place(i, c0, c1);
+    // long lists: rounds of four entries per thread, all loads of a round first
+    for (int i0 = 4 * kAttnThreads; i0 < n_all; i0 += 4 * kAttnThreads) {
+      int xc[4], xp[4], xr[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int i = i0 + tid + k * kAttnThreads;
+        xc[k] = i <= n_fq ? icost[i] : 0;
+        xp[k] = i - 1 <= n_fq ? icost[i - 1] : 0;
+        xr[k] = i < n_fq ? iref[i] : 0;
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int i = i0 + tid + k * kAttnThreads;
+        if (i >= n_all) break;
+        if (i < n_fq) s_ref[i] = xr[k];
+        const int c1 = i <= n_fq ? xc[k] : base_cost + (i - n_fq) * cF;
+        const int c0 = i - 1 <= n_fq ? xp[k] : base_cost + (i - 1 - n_fq) * cF;
+        place(i, c0, c1);
+      }
     }
     if (n_all == 0 && tid < 5) s_range[tid] = 0;
     __syncthreads();
@@ -947,7 +969,7 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
       int32_t ref;
       if (plan_ok) {
         const int k = it - first;
-        ref = k < kPlanRefs ? __builtin_amdgcn_readlane(p_refs, k) : iref[it];
+        ref = k < kPlanRefs ? __builtin_amdgcn_readlane(rec, 2 + k) : iref[it];
       } else {
         ref = s_ref[it];
       }

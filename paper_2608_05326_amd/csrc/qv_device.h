@@ -41,8 +41,11 @@ struct RetierArgs {
   int32_t aged_w0, aged_w1; // aged windows entering the candidate pool
   const float* init_scores; // prefill: [B][n_init]
   int32_t n_init;
-  int32_t plan_T;           // sequence length of the next decode step (its split plan), or -1
-  int32_t plan_extra;       // recent-region + sink windows that step attends after the live list
+  // split plans for the decode steps up to the next routing event, one per slot:
+  // the sequence lengths [plan_t0, plan_t1] it serves (plan_t0 <= 0: none) and the
+  // recent-region + sink windows those steps attend after the live list
+  int32_t plan_t0[kPlanSlots], plan_t1[kPlanSlots];
+  int32_t plan_extra[kPlanSlots];
 };
 
 struct MigrateArgs {

@@ -70,12 +70,18 @@ enum : int32_t { KIND_BF16 = 0, KIND_Q4 = 1, KIND_Q2 = 2 };
 // aux = qslot | (bits << 28)
 // per-unit counters
 // (CNT_COST: summed split-balancing cost of the live list, item_cost[CNT_ITEMS];
-//  CNT_PLAN_T: sequence length the split plan was made for, -1 none)
+//  CNT_PLAN_T0 + 2j .. CNT_PLAN_T1 + 2j: the sequence lengths split plan slot j
+//  holds for, first > last when it holds none)
 enum : int32_t { CNT_ITEMS = 0, CNT_QUANT = 1, CNT_PROMOTE = 2, CNT_ERROR = 3, CNT_BYTES_LO = 4,
-                 CNT_COST = 5, CNT_PLAN_T = 6, CNT_N = 16 };
-// split plan record: first item, end item, list refs of the first kPlanRefs items
+                 CNT_COST = 5, CNT_PLAN_T0 = 6, CNT_PLAN_T1 = 7, CNT_N = 16 };
+// split plan record: first item, end item, list refs of the first kPlanRefs items.
+// A plan depends on the live list and on the number of recent-region and sink
+// windows after it, which grows by one each time a window starts; the list only
+// changes at a routing event, so kPlanSlots plans (one per such count) cover the
+// steps up to the next event.
 constexpr int kPlanRefs = 6;
 constexpr int kPlanRec = 2 + kPlanRefs;
+constexpr int kPlanSlots = 2;
 // device error bits
 enum : int32_t { ERR_NONFINITE = 1, ERR_POOL = 2, ERR_RANGE = 4, ERR_CAND = 8 };
 // stats slots (same order as qevict_retier_stats)

@@ -1046,23 +1046,25 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   for (int i = tid; i < G.n_qslots; i += NT) qowner[i] = qown[i];
 
   // ---- rebuild the live list (window order) with its cost prefix ----
-  // The split plan of the next decode step is filled in on the way: the attention
-  // splits the items (the live list, then plan_extra recent-region and sink
-  // windows of cost cost_bf16) at the cuts ceil(u total / 4S), u = 0..4S, and the
-  // wave of part u starts at the first item whose start cost reaches cut u.  The
-  // items' cost intervals (start, end] partition (0, total], so cut u >= 1 lies in
-  // exactly one of them and part u starts at the item after it (cut 0: item 0).
-  // Cut u lies in (start, end] <=> start 4S < u total <= end 4S.
+  // The split plans of the next decode steps are filled in on the way: the
+  // attention splits the items (the live list, then plan_extra recent-region and
+  // sink windows of cost cost_bf16) at the cuts ceil(u total / 4S), u = 0..4S, and
+  // the wave of part u starts at the first item whose start cost reaches cut u.
+  // The items' cost intervals (start, end] partition (0, total], so cut u >= 1 lies
+  // in exactly one of them and part u starts at the item after it (cut 0: item 0).
+  // Cut u lies in (start, end] <=> start 4S < u total <= end 4S.  One plan per
+  // slot, each for its own number of windows after the list.
   int n_items, total_live;
   int32_t* s_pref = sinfo;   // LDS copy of the new list's refs (free once the work lists are written)
-  int32_t* s_first = sown;   // part u's first item (owner tables are written back)
-  const bool plan = a.plan_T > 0;
   const int S4 = 4 * G.n_split;
-  auto cover = [&](int start, int end, int total, int next) {
+  // part u's first item in slot j: sown[j (S4 + 1) + u] (owner tables are written back)
+  auto cover = [&](int j, int start, int end, int total, int next) {
+    int32_t* s_first = sown + j * (S4 + 1);
     const int u_lo = (int)((uint32_t)start * (uint32_t)S4 / (uint32_t)total) + 1;
     const int u_hi = (int)((uint32_t)end * (uint32_t)S4 / (uint32_t)total);
     for (int u = u_lo; u <= u_hi; ++u) s_first[u] = next;
   };
+  static_assert(kPlanSlots * (4 * 256 + 1) <= 2 * kMaxCand, "plan slots fit the owner tables");
   __syncthreads();
   {
     bool fl[3][PER];
@@ -1078,13 +1080,17 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     flag_scan<3>(fl, rk, tots, tmp, kc);
     n_items = tots[0] + tots[1] + tots[2];
     total_live = tots[0] * G.cost_bf16 + tots[1] * G.cost_q4 + tots[2] * G.cost_q2;
-    const int total = total_live + a.plan_extra * G.cost_bf16;   // the planned step's total
-    if (plan) {
+    int total[kPlanSlots];   // the planned steps' totals
+#pragma unroll
+    for (int j = 0; j < kPlanSlots; ++j) {
+      total[j] = total_live + a.plan_extra[j] * G.cost_bf16;
+      if (a.plan_t0[j] <= 0) continue;
+      int32_t* s_first = sown + j * (S4 + 1);
       if (tid == 0) s_first[0] = 0;
-      if (total == 0)
+      if (total[j] == 0)
         for (int u = tid; u <= S4; u += NT) s_first[u] = 0;
-      for (int j = tid; j < a.plan_extra; j += NT)   // recent-region and sink windows
-        cover(total_live + j * G.cost_bf16, total_live + (j + 1) * G.cost_bf16, total, n_items + j + 1);
+      for (int e = tid; e < a.plan_extra[j]; e += NT)   // recent-region and sink windows
+        cover(j, total_live + e * G.cost_bf16, total_live + (e + 1) * G.cost_bf16, total[j], n_items + e + 1);
     }
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
@@ -1102,7 +1108,9 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       iscore[pos] = my_sc[k];
       icost[pos] = cost;
       s_pref[pos] = ref;
-      if (plan) cover(cost, cost + item_cost(G, kind), total, pos + 1);
+#pragma unroll
+      for (int j = 0; j < kPlanSlots; ++j)
+        if (a.plan_t0[j] > 0) cover(j, cost, cost + item_cost(G, kind), total[j], pos + 1);
     }
     if (tid == 0) {
       icost[n_items] = total_live;
@@ -1120,9 +1128,12 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   }
   if (tid < ST_N) stats[tid] = sstat[tid];
 
-  // ---- split plan records: part u = 4 s + w ----
-  if (plan) {
-    int32_t* prec = (int32_t*)(ub + a.L.plan);
+  // ---- split plan records: slot j, part u = 4 s + w ----
+#pragma unroll
+  for (int j = 0; j < kPlanSlots; ++j) {
+    if (a.plan_t0[j] <= 0) continue;
+    const int32_t* s_first = sown + j * (S4 + 1);
+    int32_t* prec = (int32_t*)(ub + a.L.plan) + j * S4 * kPlanRec;
     for (int u = tid; u < S4; u += NT) {
       const int first = s_first[u];
       int32_t r[kPlanRefs];
@@ -1134,7 +1145,10 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       q[1] = (u32x4){(uint32_t)r[2], (uint32_t)r[3], (uint32_t)r[4], (uint32_t)r[5]};
     }
   }
-  if (tid == 0) counts[CNT_PLAN_T] = a.plan_T;
+  if (tid < 2 * kPlanSlots) {
+    const int j = tid >> 1;
+    counts[CNT_PLAN_T0 + tid] = (tid & 1) ? a.plan_t1[j] : a.plan_t0[j];
+  }
 }
 
 // Manual single-window move (one thread): F -> Q (quantize once or reactivate)
@@ -1212,7 +1226,10 @@ __global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
   }
   icost[n] = run;
   counts[CNT_COST] = run;
-  counts[CNT_PLAN_T] = -1;   // the split plan no longer matches the list
+  for (int j = 0; j < kPlanSlots; ++j) {   // the split plans no longer match the list
+    counts[CNT_PLAN_T0 + 2 * j] = -1;
+    counts[CNT_PLAN_T1 + 2 * j] = -2;
+  }
 }
 
 // Key-norm scores of the prompt windows (appendix, key-norm equation):

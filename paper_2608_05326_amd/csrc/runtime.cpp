@@ -262,7 +262,7 @@ void plan(const qevict_config* c, Geometry* g, UnitLayout* L) {
   L->pml = take(8LL * g->H_q * g->n_split);
   L->mref = take(8LL * g->H_q * g->max_items);
   L->dbg_mass = take((c->flags & QEVICT_FLAG_DEBUG_MASSES) ? 4LL * g->H_q * (g->nwc + 1) : 0);
-  L->plan = take(4LL * kPlanRec * 4 * g->n_split);
+  L->plan = take(4LL * kPlanRec * 4 * g->n_split * kPlanSlots);
   L->pnorm = take(c->score_mode == QEVICT_SCORE_PNORM ? 8LL * g->nwc : 0);
   L->unit_bytes = align256(off);
 }
@@ -428,15 +428,33 @@ void fill_common(qevict_cache* c, int layer, Geometry* g, UnitLayout* L, uint8_t
 }
 
 int n_started(const Geometry& g, int T) { return T <= g.sink ? 0 : ceil_div(T - g.sink, g.W); }
-// Split plan the re-rank kernel prepares for the next decode step (sequence length
-// T_next, windows below routed_end routed): that step's T, and its recent-region +
-// sink windows, or T = -1 when the step could not run.
-void plan_next(const Geometry& g, int max_context, int T_next, int routed_end, int32_t* plan_T,
-               int32_t* plan_extra) {
-  const int n_ring = n_started(g, T_next) - routed_end;
-  const bool ok = T_next <= max_context && n_ring >= 0 && n_ring <= g.NR;
-  *plan_T = ok ? T_next : -1;
-  *plan_extra = ok ? n_ring + g.NS : 0;
+// Split plans the re-rank kernel prepares for the decode steps up to the next
+// routing event (sequence lengths T_next .. T_next + R - 1, windows below routed_end
+// routed): consecutive steps with the same number of recent-region + sink windows
+// share a plan slot; steps past the slots, past max_context or with more unrouted
+// windows than the ring holds get none (the attention kernel then splits the list
+// itself).
+void plan_next(const Geometry& g, int max_context, int T_next, int R, int routed_end, RetierArgs* ra) {
+  for (int j = 0; j < kPlanSlots; ++j) {
+    ra->plan_t0[j] = -1;
+    ra->plan_t1[j] = -2;
+    ra->plan_extra[j] = 0;
+  }
+  int ns = 0;
+  for (int k = 0; k < R; ++k) {
+    const int T = T_next + k;
+    const int n_ring = n_started(g, T) - routed_end;
+    if (T > max_context || n_ring < 0 || n_ring > g.NR) break;
+    const int extra = n_ring + g.NS;
+    if (ns > 0 && extra == ra->plan_extra[ns - 1]) {
+      ra->plan_t1[ns - 1] = T;
+      continue;
+    }
+    if (ns == kPlanSlots) break;
+    ra->plan_t0[ns] = ra->plan_t1[ns] = T;
+    ra->plan_extra[ns] = extra;
+    ++ns;
+  }
 }
 int aged_end(const Geometry& g, int T) {
   int n = T - g.recent - g.sink;
@@ -657,8 +675,8 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
     e = launch_score_pow(pa2, c->stream);
     init_scores = staging;
   }
-  RetierArgs ra{gg, L, base, 1, 0, n_hist, init_scores, n_init, -1, 0};
-  plan_next(g, c->cfg.max_context, prompt_len + 1, n_hist, &ra.plan_T, &ra.plan_extra);
+  RetierArgs ra{gg, L, base, 1, 0, n_hist, init_scores, n_init, {}, {}, {}};
+  plan_next(g, c->cfg.max_context, prompt_len + 1, c->cfg.retier_interval, n_hist, &ra);
   if (e == hipSuccess) e = timed(c, 2, c->stream, [&] { return launch_retier(ra, c->stream); });
   MigrateArgs ma{gg, L, base, k, v, prompt_len};
   if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_migrate(ma, g.K_q, g.K_f, c->stream); });
@@ -855,8 +873,8 @@ qevict_status qevict_retier(qevict_cache* c, int32_t layer, qevict_retier_stats*
   UnitLayout L;
   uint8_t* base;
   fill_common(c, layer, &gg, &L, &base);
-  RetierArgs ra{gg, L, base, 0, a0, a1 > a0 ? a1 : a0, nullptr, 0, -1, 0};
-  plan_next(g, c->cfg.max_context, ls.T + 1, a1 > a0 ? a1 : a0, &ra.plan_T, &ra.plan_extra);
+  RetierArgs ra{gg, L, base, 0, a0, a1 > a0 ? a1 : a0, nullptr, 0, {}, {}, {}};
+  plan_next(g, c->cfg.max_context, ls.T + 1, c->cfg.retier_interval, a1 > a0 ? a1 : a0, &ra);
   MigrateArgs ma{gg, L, base, nullptr, nullptr, 0};
   // grid of the migration launch: sized for the windows a routing event usually
   // moves (a few per step between events); larger events loop inside the kernel
