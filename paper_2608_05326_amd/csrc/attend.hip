@@ -267,25 +267,32 @@ __device__ __forceinline__ void fetch_v(const ItemInfo& in, VHalf<W>& vh, int la
   }
 }
 
-// ---- the next window of a wave's run, fetched into the wave's LDS slot ----
+// ---- 8-token windows: two windows per pass of the latency chain ----
 //
-// 8-token windows: direct global-to-LDS loads (16 bytes a lane; the
-// instruction writes lane L's bytes at slot row + 16 L) copy the window's
-// record as it lies in its pool -- 4 KiB for a bf16 window, at most 2 KiB for a
-// quantized record -- so the next window's bytes are in flight while the
-// current window is computed, without registers to hold them.  read_slot then
-// gathers the operand registers fetch_k / fetch_v would fill (lanes outside a
-// window's operand lanes zeroed), many lanes reading the same LDS word where
-// the registers repeat (key scale / zero, value scale / zero).  Used with at
-// most four query heads per KV head (compact q*s staging, so that two
-// workgroups per compute unit keep their LDS).  With 32-token windows a wave
-// has about two windows, and issuing the next window's loads and copying it out
-// of the LDS cost as much as the overlap gains, so those keep their windows in
+// With at most four query heads per KV head the 16 columns of the QK^T tile
+// have room for the heads of two windows: window A's heads in columns 0..3 and
+// window B's in columns 4..7, A's keys in rows 0..7 and B's in rows 8..15.  A
+// column keeps the logits of its own window's rows (the others are masked), so
+// each column block is an online softmax of its own (a stream), and P.V
+// (K = 16 tokens: A's in lane groups 0, 1, B's in 2, 3) accumulates stream 0
+// into O rows 0..3 and stream 1 into rows 4..7; the two streams of a head are
+// merged at the end of the run.  A pass -- slot wait, operand reads, MFMAs,
+// row max, exponentials, sums -- so serves two windows.  Consecutive windows of
+// a run are paired when they are of one kind.
+//
+// Both records of the next pair go straight from their pools into the wave's
+// LDS slot (direct global-to-LDS loads, 16 bytes a lane; the instruction writes
+// lane L's bytes at slot row + 16 L) while the current pair is computed, without
+// registers to hold them; the records are copied as they lie in their pools --
+// 4 KiB for a bf16 window, at most 2 KiB for a quantized record.  No
+// register-destination load is pending while slot loads are in flight (the
+// compiler would then wait for all of them).  With 32-token windows a wave has
+// about two windows, and issuing the next window's loads and copying it out of
+// the LDS cost as much as the overlap gains, so those keep their windows in
 // registers only.
 template <int W, int NHS, bool ROPE>
 constexpr bool use_slot() { return NHS == 1 && !ROPE && W == 8; }
-template <int W>
-constexpr int slot_bytes() { return 4 * 1024; }
+constexpr int kPairSlot = 4 * 1024;   // LDS bytes per window of a pair
 
 __device__ __forceinline__ void dma16(const void* g, uint8_t* lds_row) {
   __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds_row, 16, 0, 0);
@@ -298,57 +305,261 @@ __device__ __forceinline__ int slot_record_bytes(const ItemInfo& in, const Geome
   return in.kind == KIND_BF16 ? 2 * W * kHeadDim * 2 : (int)G.qrec_bytes;
 }
 
-template <int W>
-__device__ __forceinline__ void issue_slot(const ItemInfo& in, uint8_t* slot, int lane, const Geometry& G) {
-  static_assert(W == 8, "8-token windows");
-  const int n = slot_record_bytes<W>(in, G);
+__device__ __forceinline__ void issue_record(const ItemInfo& in, uint8_t* dst, int lane, const Geometry& G) {
+  const int n = slot_record_bytes<8>(in, G);
 #pragma unroll
-  for (int row = 0; row < slot_bytes<W>() / 1024; ++row) {
+  for (int row = 0; row < kPairSlot / 1024; ++row) {
     if (row * 1024 >= n) break;   // uniform
-    if (row * 1024 + lane * 16 < n) dma16(in.p + row * 1024 + lane * 16, slot + row * 1024);
+    if (row * 1024 + lane * 16 < n) dma16(in.p + row * 1024 + lane * 16, dst + row * 1024);
   }
 }
 
-template <int W, bool ROPE>
-__device__ __forceinline__ void read_slot(const ItemInfo& in, const uint8_t* slot, KHalf<W, ROPE>& kh,
-                                          VHalf<W>& vh, int lane, int r, int qg, const Geometry& G) {
-  static_assert(W == 8, "8-token windows");
+// Operand registers of a pair, gathered from the slot: K rows r (window r >> 3,
+// token r & 7), V lane groups qg (window qg >> 1, tokens 4 (qg & 1) ..); lanes of
+// an absent window B read zeros.  Quantized windows: the B operand q*s of the
+// lane's column (head r & 3 of window (r >> 2) & 1, channels 32 kb + 8 qg + i)
+// split into exact fp16 hi + lo, and the column's bias q.z.
+__device__ __forceinline__ void read_pair(int kind, bool pb, const uint8_t* slot, KHalf<8, false>& kh,
+                                          VHalf<8>& vh, f16x8 (&qhi)[4], f16x8 (&qlo)[4], float* bias,
+                                          const bf16x8 (&qop)[4], int r, int qg, const Geometry& G) {
   const u32x4 z = {0, 0, 0, 0};
-  auto rd = [&](int off) { return *(const u32x4*)(slot + off); };
-  auto rd8 = [&](int off) {
-    const uint2 v = *(const uint2*)(slot + off);
+  auto rd = [&](const uint8_t* s, int off) { return *(const u32x4*)(s + off); };
+  auto rd8 = [&](const uint8_t* s, int off) {
+    const uint2 v = *(const uint2*)(s + off);
     return (u32x4){v.x, v.y, 0u, 0u};
   };
-  const bool row = r < 8, col = qg < 2;
-  if (in.kind == KIND_BF16) {
+  const bool krow = r < 8 || pb, vcol = qg < 2 || pb;
+  const uint8_t* ks = slot + (r >= 8 ? kPairSlot : 0);
+  const uint8_t* vs = slot + (qg >= 2 ? kPairSlot : 0);
+  const int rr = r & 7, qq = qg & 1;
+  if (kind == KIND_BF16) {
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) kh.d[kb] = row ? rd(((kb * 4 + qg) * 8 + r) * 16) : z;
-    const int vbase = W * kHeadDim * 2;
+    for (int kb = 0; kb < 4; ++kb) kh.d[kb] = krow ? rd(ks, ((kb * 4 + qg) * 8 + rr) * 16) : z;
+    const int vbase = 8 * kHeadDim * 2;
 #pragma unroll
-    for (int cp = 0; cp < 4; ++cp) vh.d[cp] = col ? rd(vbase + ((cp * 2 + qg) * 16 + r) * 16) : z;
+    for (int cp = 0; cp < 4; ++cp) vh.d[cp] = vcol ? rd(vs, vbase + ((cp * 2 + qq) * 16 + r) * 16) : z;
     vh.d[4] = z;
-  } else {
-    const bool q4 = in.kind == KIND_Q4;
-    const int qc = (int)G.qcodes_bytes, mk = (int)meta_k_off(G), mv = (int)meta_v_off(G);
-    kh.d[0] = row ? (q4 ? rd((qg * 8 + r) * 16) : rd8((qg * 8 + r) * 8)) : z;
-    kh.d[1] = rd(mk + 16 * r);
-    kh.d[2] = rd(mk + 256 + 16 * r);
-    kh.d[3] = z;
-    vh.d[0] = col ? (q4 ? rd(qc + (qg * 16 + r) * 16) : rd8(qc + (qg * 16 + r) * 8)) : z;
-#pragma unroll
-    for (int vg = 0; vg < 4; ++vg) vh.d[1 + vg] = col ? rd(mv + (qg * 4 + vg) * 16) : z;
+    *bias = 0.f;
+    return;
   }
+  const bool q4 = kind == KIND_Q4;
+  const int qc = (int)G.qcodes_bytes, mk = (int)meta_k_off(G), mv = (int)meta_v_off(G);
+  kh.d[0] = krow ? (q4 ? rd(ks, (qg * 8 + rr) * 16) : rd8(ks, (qg * 8 + rr) * 8)) : z;
+  vh.d[0] = vcol ? (q4 ? rd(vs, qc + (qq * 16 + r) * 16) : rd8(vs, qc + (qq * 16 + r) * 8)) : z;
+#pragma unroll
+  for (int vg = 0; vg < 4; ++vg) vh.d[1 + vg] = vcol ? rd(vs, mv + (qq * 4 + vg) * 16) : z;
+  const int jc = (r >> 2) & 1;
+  const bool ccol = r < 8 && (jc == 0 || pb);
+  const uint8_t* cs = slot + (jc ? kPairSlot : 0);
+  float bsum = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    const u32x4 s4 = ccol ? rd(cs, mk + 64 * kb + 16 * qg) : z;         // key scales
+    const u32x4 z4 = ccol ? rd(cs, mk + 256 + 64 * kb + 16 * qg) : z;   // key zero points
+    const u32x4 qb = __builtin_bit_cast(u32x4, qop[kb]);
+    f16x8 hi8, lo8;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float qv = __uint_as_float((i & 1) ? (qb[i >> 1] & 0xFFFF0000u) : (qb[i >> 1] << 16));
+      const float sv = (float)__builtin_bit_cast(_Float16, (uint16_t)(s4[i >> 1] >> (16 * (i & 1))));
+      const float zv = (float)__builtin_bit_cast(_Float16, (uint16_t)(z4[i >> 1] >> (16 * (i & 1))));
+      const float qs = qv * sv;   // exact: 8-bit x 11-bit significands
+      const _Float16 h = (_Float16)qs;
+      hi8[i] = h;
+      lo8[i] = (_Float16)(qs - (float)h);
+      bsum = fmaf(qv, zv, bsum);
+    }
+    qhi[kb] = hi8;
+    qlo[kb] = lo8;
+  }
+  *bias = rows_sum(bsum);   // q . z of the column over its 128 channels
+}
+
+// The open window takes this step's key and value (and stores them into its
+// ring slot); it is the pair's window j.
+__device__ __forceinline__ void patch_open8(const ItemInfo& in, int j, KHalf<8, false>& kh, VHalf<8>& vh,
+                                            const AttnArgs& a, int b, int g, int qg, int r) {
+  const Geometry& G = a.g;
+  const int pos = in.ntok - 1;
+  uint8_t* pw = const_cast<uint8_t*>(in.p);
+  const uint16_t* kn = a.k_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
+  const bool krow = r == 8 * j + pos;   // lanes of the token's key row
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    const u32x4 v = ld16(kn + 32 * kb + 8 * qg);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) kh.d[kb][i] = krow ? v[i] : kh.d[kb][i];
+    if (krow) *(u32x4*)(pw + ((kb * 4 + qg) * 8 + pos) * 16) = v;
+  }
+  // value: element jp of the lanes of group 2 j + qp
+  const uint16_t* vn = a.v_new + ((int64_t)b * G.H_kv + g) * kHeadDim;
+  const int qp = pos >> 2, jp = pos & 3;
+  const bool vgrp = qg == 2 * j + qp;
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) {
+    const uint32_t val = vn[16 * cb + r];
+    if (vgrp) *(uint16_t*)(pw + v_elem_off(8, pos, 16 * cb + r)) = (uint16_t)val;
+    const int wi = (cb & 1) * 2 + (jp >> 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t wv = vh.d[cb >> 1][i];
+      const uint32_t lo = (wv & 0xFFFF0000u) | val, hi = (wv & 0x0000FFFFu) | (val << 16);
+      vh.d[cb >> 1][i] = (vgrp && i == wi) ? ((jp & 1) ? hi : lo) : wv;
+    }
+  }
+}
+
+// QK^T and the online-softmax update of a pair: the lane's probabilities of
+// column r (rows 4 qg .. + 3) in p, the column's sum in *lw.  Masked entries
+// are -inf, and a stream without any row yet keeps reference -inf and sum 0.
+__device__ __forceinline__ void pair_k(int kind, bool pb, int ntA, int ntB, const KHalf<8, false>& kh,
+                                       const bf16x8 (&qop)[4], const f16x8 (&qhi)[4],
+                                       const f16x8 (&qlo)[4], float bias, float scale_log2, int qg,
+                                       int r, WaveState& st, float (&p)[4], float* lw_out) {
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (kind == KIND_BF16) {
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) acc = mfma_bf16(__builtin_bit_cast(bf16x8, kh.d[kb]), qop[kb], acc);
+  } else {
+    const bool q4 = kind == KIND_Q4;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const f16x8 cv = q4 ? unpack_codes<4>(kh.d[0][kb], 0) : unpack_codes<2>(kh.d[0][kb >> 1], kb & 1);
+      acc = mfma_f16(cv, qhi[kb], acc);
+      acc = mfma_f16(cv, qlo[kb], acc);
+    }
+  }
+  const int jc = (r >> 2) & 1;
+  const bool cval = r < 8 && (jc == 0 || pb) && (qg >> 1) == jc;   // rows of the column's window
+  const int ntok = jc ? ntB : ntA;
+  float x[4];
+  float mw = -INFINITY;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const bool ok = cval && 4 * (qg & 1) + v < ntok;
+    x[v] = ok ? (acc[v] + bias) * scale_log2 : -INFINITY;
+    mw = fmaxf(mw, x[v]);
+  }
+  mw = rows_max(mw);
+  if (__builtin_amdgcn_ballot_w64(mw > st.m + kRescaleSlack) != 0) {
+    const float m_new = fmaxf(st.m, mw);
+    const float alpha = m_new == st.m ? 1.f : __builtin_amdgcn_exp2f(st.m - m_new);
+    st.l *= alpha;
+    st.m = m_new;
+    // O row 4 qg + v: the alpha of lane 4 qg + v (rows 8..15 stay zero)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const float a0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), v));
+      const float a1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), 4 + v));
+      const float av = qg == 0 ? a0 : a1;
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb) st.o[cb][v] *= av;
+    }
+  }
+  float lw = 0.f;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    p[v] = x[v] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(x[v] - st.m);
+    lw += p[v];
+  }
+  lw = rows_sum(lw);
+  st.l += lw;
+  *lw_out = lw;
+}
+
+// P.V of a pair (16x16x16 MFMAs: the A operand is the lane's four
+// probabilities of column r, the B operand the values of tokens 4 qg .. + 3),
+// then the windows' statistics: (m_w, l_w) of stream j, head h from lane 4 j + h.
+__device__ __forceinline__ void pair_v(int kind, bool pb, int itA, int itB, int ntA, int ntB, VHalf<8>& vh,
+                                       WaveState& st, const float (&p)[4], float lw, const AttnArgs& a,
+                                       int g, int qg, int r, float2* mref) {
+  const Geometry& G = a.g;
+  if (kind == KIND_BF16) {
+    const int ntok = qg >= 2 ? ntB : ntA;
+    if (ntok < 8) {   // tokens past the end of a partial window contribute nothing
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t0 = 4 * (qg & 1) + 2 * (i & 1);
+        const uint32_t mask = (t0 < ntok ? 0x0000FFFFu : 0u) | (t0 + 1 < ntok ? 0xFFFF0000u : 0u);
+#pragma unroll
+        for (int cp = 0; cp < 4; ++cp) vh.d[cp][i] &= mask;
+      }
+    }
+    bf16x4 pv;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) pv[j] = (__bf16)p[j];
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) {
+      const u32x4 d = vh.d[cb >> 1];
+      const uint32_t w0 = (cb & 1) ? d[2] : d[0], w1 = (cb & 1) ? d[3] : d[1];
+      st.o[cb] = mfma16_bf16(pv, __builtin_bit_cast(bf16x4, make_uint2(w0, w1)), st.o[cb]);
+    }
+  } else {
+    const bool q4 = kind == KIND_Q4;
+    const u32x4 cw = vh.d[0];
+    f16x4 pv;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) pv[j] = (_Float16)p[j];
+#pragma unroll
+    for (int cp = 0; cp < 4; ++cp) {
+      // codes of channel blocks 2 cp (elements 0..3) and 2 cp + 1 (4..7), tokens 4 qg + j
+      const f16x8 c8 = q4 ? unpack_codes<4>(cw[cp], 0) : unpack_codes<2>(cw[cp >> 1], cp & 1);
+      // value group cp: scales then zero points of the lane's four tokens
+      // (elements copied out first: a bit cast of a vector element reads element 0)
+      const u32x4 m = vh.d[1 + cp];
+      const uint32_t m0 = m[0], m1 = m[1], m2 = m[2], m3 = m[3];
+      const f16x2 s01 = __builtin_bit_cast(f16x2, m0), s23 = __builtin_bit_cast(f16x2, m1);
+      const f16x2 z01 = __builtin_bit_cast(f16x2, m2), z23 = __builtin_bit_cast(f16x2, m3);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const f16x2 c01 = {c8[4 * e], c8[4 * e + 1]}, c23 = {c8[4 * e + 2], c8[4 * e + 3]};
+        const f16x2 v01 = __builtin_elementwise_fma(s01, c01, z01);
+        const f16x2 v23 = __builtin_elementwise_fma(s23, c23, z23);
+        const f16x4 vv = {v01[0], v01[1], v23[0], v23[1]};
+        st.o[2 * cp + e] = mfma16_f16(pv, vv, st.o[2 * cp + e]);
+      }
+    }
+  }
+  const int jc = r >> 2, h = r & 3;
+  if (qg == 0 && r < 8 && h < G.gqa && (jc == 0 || pb))
+    mref[(int64_t)(jc ? itB : itA) * G.H_q + g * G.gqa + h] = make_float2(st.m, lw);
+  (void)ntB;
+}
+
+// End of a run: each head's two streams (O rows h and 4 + h, references and sums
+// in lanes h and 4 + h) merged into O row h and lane h.
+__device__ __forceinline__ void merge_streams(WaveState& st, int qg, int r) {
+  float f0[4], f1[4], M[4], L[4];
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const float m0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(st.m), h));
+    const float m1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(st.m), 4 + h));
+    const float l0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(st.l), h));
+    const float l1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(st.l), 4 + h));
+    M[h] = fmaxf(m0, m1);
+    f0[h] = m0 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m0 - M[h]);
+    f1[h] = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M[h]);
+    L[h] = l0 * f0[h] + l1 * f1[h];
+  }
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const float fv = qg == 0 ? f0[v] : (qg == 1 ? f1[v] : 0.f);
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) {
+      const uint32_t u = __float_as_uint(st.o[cb][v] * fv);
+      const auto s = __builtin_amdgcn_permlane16_swap(u, u, false, false);   // lane ^ 16
+      const uint32_t s0 = s[0], s1 = s[1];
+      st.o[cb][v] = __uint_as_float(s0) + __uint_as_float(s1);
+    }
+  }
+  const int h = r & 3;
+  st.m = h == 0 ? M[0] : (h == 1 ? M[1] : (h == 2 ? M[2] : M[3]));
+  st.l = h == 0 ? L[0] : (h == 1 ? L[1] : (h == 2 ? L[2] : L[3]));
 }
 
 // Offset of a q*s operand entry in the per-wave staging area: the B operand of
-// the QK^T MFMA, lane L = 16 q + r holding channels 8 q .. of block kb for head
-// r.  With at most four query heads per KV head only lanes r < 4 carry heads,
-// and the staging area holds just those 16 lanes (the others read zeros).
-template <bool COMPACT>
-__device__ __forceinline__ int qst_off(int hilo, int kb, int L) {
-  if constexpr (COMPACT) return ((hilo * 4 + kb) * 16 + 4 * (L >> 4) + (L & 15)) * 16;
-  else return ((hilo * 4 + kb) * 64 + L) * 16;
-}
+// the QK^T MFMA, lane L = 16 q + r holding channels 8 q .. of block kb for head r.
+__device__ __forceinline__ int qst_off(int hilo, int kb, int L) { return ((hilo * 4 + kb) * 64 + L) * 16; }
 
 // QK^T and the online-softmax update of one window: probabilities in p_,
 // the window's (reference, sum) pair in m_w, l_w.  The open window takes this
@@ -474,7 +685,6 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
                                           int qg, int r, float (&p_)[row_tiles<W>()][4], float* m_w,
                                           float* l_w) {
   constexpr int TB = row_tiles<W>();
-  constexpr bool CQ = use_slot<W, NHS, ROPE>();   // compact q*s staging
   const Geometry& G = a.g;
   const int gqa = G.gqa;
   const int ntok = in.ntok;
@@ -551,8 +761,8 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
       if (hh < gqa) {
         const int dst = 16 * (r & 3) + hh;   // lane of the B operand: head hh, channel group r & 3
         const int kb = r >> 2;
-        *(u32x4*)(qlds + qst_off<CQ>(0, kb, dst)) = __builtin_bit_cast(u32x4, hi8);
-        *(u32x4*)(qlds + qst_off<CQ>(1, kb, dst)) = __builtin_bit_cast(u32x4, lo8);
+        *(u32x4*)(qlds + qst_off(0, kb, dst)) = __builtin_bit_cast(u32x4, hi8);
+        *(u32x4*)(qlds + qst_off(1, kb, dst)) = __builtin_bit_cast(u32x4, lo8);
       }
       bias_k[k] = row16_sum(bsum);   // q . z of head qg + 4k (same value in all 16 lanes)
     }
@@ -566,13 +776,8 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
     f16x8 qhi[4], qlo[4];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      if (!CQ || r < 4) {
-        qhi[kb] = __builtin_bit_cast(f16x8, ld16(qlds + qst_off<CQ>(0, kb, lane)));
-        qlo[kb] = __builtin_bit_cast(f16x8, ld16(qlds + qst_off<CQ>(1, kb, lane)));
-      } else {
-        qhi[kb] = (f16x8){};
-        qlo[kb] = (f16x8){};
-      }
+      qhi[kb] = __builtin_bit_cast(f16x8, ld16(qlds + qst_off(0, kb, lane)));
+      qlo[kb] = __builtin_bit_cast(f16x8, ld16(qlds + qst_off(1, kb, lane)));
     }
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
@@ -793,7 +998,7 @@ constexpr int kAttnSmemFixed = 4 * 16 * 130 * 4;   // q*s staging per wave / end
 // array of their own, which also holds the end-of-split merge; otherwise the
 // merge reuses the staging area)
 template <int W, int NHS, bool ROPE>
-constexpr int attn_smem_fixed() { return use_slot<W, NHS, ROPE>() ? 4 * 2048 : kAttnSmemFixed; }
+constexpr int attn_smem_fixed() { return use_slot<W, NHS, ROPE>() ? 0 : kAttnSmemFixed; }
 
 // MINB workgroups of four waves per compute unit: at most 512 / MINB VGPRs per lane
 template <int W, int NHS, int MINB, bool ROPE>
@@ -806,8 +1011,8 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
 
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   constexpr bool SLOT = use_slot<W, NHS, ROPE>();
-  // q*s staging: [hi/lo][kb][lane] x 16 B (compact: lanes r < 4 only)
-  uint8_t* qlds = smem + wave * (SLOT ? 2048 : 8192);
+  // q*s staging: [hi/lo][kb][lane] x 16 B (pairs of 8-token windows form q*s in registers)
+  uint8_t* qlds = smem + wave * 8192;
   uint8_t* mo_base = smem;   // end-of-split merge of the four waves
   int32_t* s_ref = (int32_t*)(smem + attn_smem_fixed<W, NHS, ROPE>());   // live-list entries
 
@@ -850,8 +1055,10 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   bf16x8 qop[4];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
+    // column r: head r (pairs of 8-token windows: head r & 3 of column block r >> 2)
+    const int hc = SLOT ? (r < 8 ? (r & 3) : gqa) : r;
     u32x4 v = {0, 0, 0, 0};
-    if (r < gqa) v = ld16(qbase + r * kHeadDim + 32 * kb + 8 * qg);
+    if (hc < gqa) v = ld16(qbase + hc * kHeadDim + 32 * kb + 8 * qg);
     qop[kb] = __builtin_bit_cast(bf16x8, v);
   }
   float qf[NHS][8];   // compact: head qg + 4k, channels 8r .. 8r + 7
@@ -867,8 +1074,10 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
     }
   }
   // zero this lane's q*s operand slots (padded heads keep zeros)
+  if constexpr (!SLOT) {
 #pragma unroll
-  for (int i = 0; i < (SLOT ? 2 : 8); ++i) *(u32x4*)(qlds + (i * 64 + lane) * 16) = (u32x4){0, 0, 0, 0};
+    for (int i = 0; i < 8; ++i) *(u32x4*)(qlds + (i * 64 + lane) * 16) = (u32x4){0, 0, 0, 0};
+  }
 
   // ---- this wave's item range: from the plan, else computed here ----
   const int n_extra = a.n_ring + a.n_sink_items;
@@ -946,6 +1155,13 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
     last = __builtin_amdgcn_readfirstlane(s_range[wave + 1]);
   }
 
+  // plan path: list refs of a run past the plan record's first ones, one per lane
+  int run_ref = 0;
+  if (plan_ok && last - first > kPlanRefs) {   // uniform
+    const int i = first + kPlanRefs + lane;
+    run_ref = i < last && i < n_fq ? iref[i] : 0;
+  }
+
   WaveState st;
   st.m = -INFINITY;
   st.l = 0.f;
@@ -969,7 +1185,9 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
       int32_t ref;
       if (plan_ok) {
         const int k = it - first;
-        ref = k < kPlanRefs ? __builtin_amdgcn_readlane(rec, 2 + k) : iref[it];
+        ref = k < kPlanRefs        ? __builtin_amdgcn_readlane(rec, 2 + k)
+              : k < kPlanRefs + 64 ? __builtin_amdgcn_readlane(run_ref, k - kPlanRefs)
+                                   : iref[it];
       } else {
         ref = s_ref[it];
       }
@@ -998,32 +1216,49 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   float p_[TB][4];
   float m_w, l_w;
   if constexpr (SLOT) {
-    // Every window of the run goes through the wave's LDS slot: wait for it,
-    // move it to the registers, start the next window's loads into the slot,
-    // then compute, so that each window's loads overlap the previous window's
-    // computation.  No register-destination load is pending while slot loads
-    // are in flight (the compiler would then wait for all of them).  A
-    // separate array, so that the compiler can tell the slot from the q*s
-    // staging.
-    __shared__ __attribute__((aligned(16))) uint8_t s_slots[4 * slot_bytes<W>()];
-    uint8_t* slot = s_slots + wave * slot_bytes<W>();   // this wave's next window
+    // pairs of windows through the wave's LDS slot: wait for the pair, gather its
+    // operands, start the next pair's loads into the slot, then compute
+    __shared__ __attribute__((aligned(16))) uint8_t s_slots[4 * 2 * kPairSlot];
+    uint8_t* slot = s_slots + wave * 2 * kPairSlot;
     mo_base = s_slots;
+    // the pair starting at item i: its second item, and whether it has one
+    auto pair_at = [&](int i, ItemInfo& x, ItemInfo& y) {
+      x = info(i);
+      y = info(i + 1 < last ? i + 1 : i);
+      return i + 1 < last && y.kind == x.kind;
+    };
     if (first < last) {
-      ItemInfo ia = info(first);
-      issue_slot<W>(ia, slot, lane, G);
-      for (int it = first; it < last; ++it) {
+      ItemInfo ia, ib;
+      bool pb = pair_at(first, ia, ib);
+      issue_record(ia, slot, lane, G);
+      if (pb) issue_record(ib, slot + kPairSlot, lane, G);
+      f16x8 qhi[4], qlo[4];
+      float bias;
+      for (int it = first; it < last;) {
+        const int nxt = it + (pb ? 2 : 1);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        read_slot<W, ROPE>(ia, slot, KA, V, lane, r, qg, G);
+        read_pair(ia.kind, pb, slot, KA, V, qhi, qlo, &bias, qop, r, qg, G);
         wave_sync_lds();
-        const bool has = it + 1 < last;
-        const ItemInfo ib = info(has ? it + 1 : it);   // (no conditional copy of the record)
-        if (has) issue_slot<W>(ib, slot, lane, G);
+        if (ia.open) patch_open8(ia, 0, KA, V, a, b, g, qg, r);
+        if (pb && ib.open) patch_open8(ib, 1, KA, V, a, b, g, qg, r);
+        ItemInfo na, nb;
+        const bool has = nxt < last;
+        const bool npb = pair_at(has ? nxt : it, na, nb) && has;
+        if (has) {
+          issue_record(na, slot, lane, G);
+          if (npb) issue_record(nb, slot + kPairSlot, lane, G);
+        }
         __builtin_amdgcn_sched_barrier(0);
-        process_k<W, NHS, ROPE>(ia, KA, st, qop, qf, qlds, a, b, g, lane, qg, r, p_, &m_w, &l_w);
-        process_v<W, NHS>(ia, V, st, p_, m_w, l_w, a, b, g, qg, r, mref);
-        ia = ib;
+        float lw;
+        pair_k(ia.kind, pb, ia.ntok, ib.ntok, KA, qop, qhi, qlo, bias, G.scale_log2, qg, r, st, p_[0], &lw);
+        pair_v(ia.kind, pb, ia.it, ib.it, ia.ntok, ib.ntok, V, st, p_[0], lw, a, g, qg, r, mref);
+        ia = na;
+        ib = nb;
+        pb = npb;
+        it = nxt;
       }
     }
+    merge_streams(st, qg, r);
   } else {
     for (int it = first; it < last; ++it) {
       const ItemInfo ia = info(it);

@@ -180,6 +180,27 @@ def test_window8_routing_every_step():
     assert ls.promotions > 0
 
 
+@pytest.mark.parametrize("hq,hkv,splits", [(8, 8, 0), (6, 2, 0), (4, 2, 1), (32, 8, 64)])
+def test_window8_head_layouts_and_splits(hq, hkv, splits):
+    """8-token windows with at most four query heads per KV head are computed in
+    pairs, one window per column block of the QK^T tile: GQA 1 and 3 (blocks
+    partly empty), GQA 2 on one split (every wave a long run of pairs), and 64
+    splits (short runs: waves with one window, an unpaired last window, or none),
+    with the paper's sink / recent regions and int2 codes."""
+    from tests.gpu_harness import Lockstep
+    wl = syn.get_workload("c6w8s").replace(name=f"w8h{hq}x{hkv}s{splits}", num_q_heads=hq,
+                                           num_kv_heads=hkv, steps=24)
+    ls = Lockstep(wl, num_splits=splits)
+    print(f"[lockstep] {wl.name}", flush=True)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[lockstep] W 8 heads {hq}/{hkv} splits {splits}: max out err {ls.max_out_err:.2e}, "
+          f"max score err {ls.max_score_err:.2e}, promotions {ls.promotions}", flush=True)
+    assert ls.events > 0
+
+
 @pytest.mark.parametrize("pattern", ["all_equal", "three_values", "coarse_grid", "outlier"])
 @pytest.mark.parametrize("wl_name", ["c2s", "c5s"])
 def test_tier_selection_with_tied_scores(wl_name, pattern):
