@@ -322,56 +322,99 @@ __device__ __forceinline__ void issue_record(const ItemInfo& in, uint8_t* dst, i
 __device__ __forceinline__ void read_pair(int kind, bool pb, const uint8_t* slot, KHalf<8, false>& kh,
                                           VHalf<8>& vh, f16x8 (&qhi)[4], f16x8 (&qlo)[4], float* bias,
                                           const bf16x8 (&qop)[4], int r, int qg, const Geometry& G) {
+  // Every read is unconditional (all addresses lie in the slot; lanes of an
+  // absent window read stale bytes and select zeros), so the reads issue back
+  // to back and one wait covers them.
   const u32x4 z = {0, 0, 0, 0};
   auto rd = [&](const uint8_t* s, int off) { return *(const u32x4*)(s + off); };
-  auto rd8 = [&](const uint8_t* s, int off) {
-    const uint2 v = *(const uint2*)(s + off);
-    return (u32x4){v.x, v.y, 0u, 0u};
+  auto sel = [&](bool c, u32x4 v) {
+    u32x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = c ? v[i] : 0u;
+    return o;
   };
   const bool krow = r < 8 || pb, vcol = qg < 2 || pb;
   const uint8_t* ks = slot + (r >= 8 ? kPairSlot : 0);
   const uint8_t* vs = slot + (qg >= 2 ? kPairSlot : 0);
   const int rr = r & 7, qq = qg & 1;
   if (kind == KIND_BF16) {
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) kh.d[kb] = krow ? rd(ks, ((kb * 4 + qg) * 8 + rr) * 16) : z;
     const int vbase = 8 * kHeadDim * 2;
+    u32x4 kv[4], vv[4];
 #pragma unroll
-    for (int cp = 0; cp < 4; ++cp) vh.d[cp] = vcol ? rd(vs, vbase + ((cp * 2 + qq) * 16 + r) * 16) : z;
+    for (int kb = 0; kb < 4; ++kb) kv[kb] = rd(ks, ((kb * 4 + qg) * 8 + rr) * 16);
+#pragma unroll
+    for (int cp = 0; cp < 4; ++cp) vv[cp] = rd(vs, vbase + ((cp * 2 + qq) * 16 + r) * 16);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) kh.d[kb] = sel(krow, kv[kb]);
+#pragma unroll
+    for (int cp = 0; cp < 4; ++cp) vh.d[cp] = sel(vcol, vv[cp]);
     vh.d[4] = z;
     *bias = 0.f;
     return;
   }
+  // codes: 16 bytes a lane (int4), 8 (int2: the upper half of the read is the
+  // next lane's and is dropped)
   const bool q4 = kind == KIND_Q4;
   const int qc = (int)G.qcodes_bytes, mk = (int)meta_k_off(G), mv = (int)meta_v_off(G);
-  kh.d[0] = krow ? (q4 ? rd(ks, (qg * 8 + rr) * 16) : rd8(ks, (qg * 8 + rr) * 8)) : z;
-  vh.d[0] = vcol ? (q4 ? rd(vs, qc + (qq * 16 + r) * 16) : rd8(vs, qc + (qq * 16 + r) * 8)) : z;
+  const int cb = q4 ? 16 : 8;
+  const u32x4 kc = rd(ks, (qg * 8 + rr) * cb);
+  const u32x4 vc = rd(vs, qc + (qq * 16 + r) * cb);
+  u32x4 vm[4];
 #pragma unroll
-  for (int vg = 0; vg < 4; ++vg) vh.d[1 + vg] = vcol ? rd(vs, mv + (qq * 4 + vg) * 16) : z;
-  const int jc = (r >> 2) & 1;
-  const bool ccol = r < 8 && (jc == 0 || pb);
+  for (int vg = 0; vg < 4; ++vg) vm[vg] = rd(vs, mv + (qq * 4 + vg) * 16);
+  // q*s of column c = r & 7 (head c & 3 of window c >> 2): lanes r < 8 form
+  // channel blocks kb = 0, 1 and lanes r + 8 blocks 2, 3 of the same column, whose
+  // halves lane r then takes with a half-row rotation (lanes r >= 8 keep operands
+  // of masked columns)
+  const int jc = (r >> 2) & 1, kb0 = (r >> 3) * 2;
+  const bool cval = jc == 0 || pb;
   const uint8_t* cs = slot + (jc ? kPairSlot : 0);
-  float bsum = 0.f;
+  u32x4 s4[2], z4[2];
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    const u32x4 s4 = ccol ? rd(cs, mk + 64 * kb + 16 * qg) : z;         // key scales
-    const u32x4 z4 = ccol ? rd(cs, mk + 256 + 64 * kb + 16 * qg) : z;   // key zero points
-    const u32x4 qb = __builtin_bit_cast(u32x4, qop[kb]);
+  for (int k = 0; k < 2; ++k) {
+    s4[k] = rd(cs, mk + 64 * (kb0 + k) + 16 * qg);         // key scales
+    z4[k] = rd(cs, mk + 256 + 64 * (kb0 + k) + 16 * qg);   // key zero points
+  }
+  const uint32_t hm = q4 ? ~0u : 0u;
+  kh.d[0] = sel(krow, (u32x4){kc[0], kc[1], kc[2] & hm, kc[3] & hm});
+  vh.d[0] = sel(vcol, (u32x4){vc[0], vc[1], vc[2] & hm, vc[3] & hm});
+#pragma unroll
+  for (int vg = 0; vg < 4; ++vg) vh.d[1 + vg] = sel(vcol, vm[vg]);
+  float bsum = 0.f;
+  u32x4 mh[2], ml[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const u32x4 sk = sel(cval, s4[k]), zk = sel(cval, z4[k]);
+    const u32x4 qb = __builtin_bit_cast(u32x4, r < 8 ? qop[k] : qop[2 + k]);
     f16x8 hi8, lo8;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const float qv = __uint_as_float((i & 1) ? (qb[i >> 1] & 0xFFFF0000u) : (qb[i >> 1] << 16));
-      const float sv = (float)__builtin_bit_cast(_Float16, (uint16_t)(s4[i >> 1] >> (16 * (i & 1))));
-      const float zv = (float)__builtin_bit_cast(_Float16, (uint16_t)(z4[i >> 1] >> (16 * (i & 1))));
+      const float sv = (float)__builtin_bit_cast(_Float16, (uint16_t)(sk[i >> 1] >> (16 * (i & 1))));
+      const float zv = (float)__builtin_bit_cast(_Float16, (uint16_t)(zk[i >> 1] >> (16 * (i & 1))));
       const float qs = qv * sv;   // exact: 8-bit x 11-bit significands
       const _Float16 h = (_Float16)qs;
       hi8[i] = h;
       lo8[i] = (_Float16)(qs - (float)h);
       bsum = fmaf(qv, zv, bsum);
     }
-    qhi[kb] = hi8;
-    qlo[kb] = lo8;
+    mh[k] = __builtin_bit_cast(u32x4, hi8);
+    ml[k] = __builtin_bit_cast(u32x4, lo8);
   }
+  auto ror8 = [](u32x4 v) {   // lane r takes lane r ^ 8 of its 16-lane row
+    u32x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v[i], 0x128, 0xF, 0xF, false);
+    return o;
+  };
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    qhi[k] = __builtin_bit_cast(f16x8, mh[k]);
+    qlo[k] = __builtin_bit_cast(f16x8, ml[k]);
+    qhi[2 + k] = __builtin_bit_cast(f16x8, ror8(mh[k]));
+    qlo[2 + k] = __builtin_bit_cast(f16x8, ror8(ml[k]));
+  }
+  bsum += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(bsum), 0x128, 0xF, 0xF, false));
   *bias = rows_sum(bsum);   // q . z of the column over its 128 channels
 }
 
@@ -1055,8 +1098,9 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   bf16x8 qop[4];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
-    // column r: head r (pairs of 8-token windows: head r & 3 of column block r >> 2)
-    const int hc = SLOT ? (r < 8 ? (r & 3) : gqa) : r;
+    // column r: head r (pairs of 8-token windows: head r & 3 of column block
+    // (r >> 2) & 1; columns 8..15 repeat 0..7 and are masked)
+    const int hc = SLOT ? (r & 3) : r;
     u32x4 v = {0, 0, 0, 0};
     if (hc < gqa) v = ld16(qbase + hc * kHeadDim + 32 * kb + 8 * qg);
     qop[kb] = __builtin_bit_cast(bf16x8, v);
