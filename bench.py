@@ -591,7 +591,9 @@ def main():
         per = {k: (lp[k][0] * 1e3 / lp[k][1] if lp[k][1] else None) for k in lp}
         if per[2] is not None:
             ev_us = per[2] + (per[3] or 0.0)
-            # per-launch event durations (each holds its dispatch, about 2 us): upper bounds
+            # per layer routing event: event durations of the launches (each holds its
+            # dispatch, about 2 us) over the layers they served (asynchronous routing
+            # launches the events of a batch of layers together)
             res["routing_kernel_us"] = {"rerank": round(per[2], 2),
                                         "migrate": round(per[3], 2) if per[3] is not None else None}
             res["routing_us_per_event"] = round(ev_us, 2)

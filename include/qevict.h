@@ -81,7 +81,8 @@ enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT =
 /* Routing work (re-rank, quantize, promote) of qevict_retier runs on a stream
  * the library owns, so the routing of one layer overlaps the attention of the
  * layers after it.  Requests are launched in batches (up to num_layers / 2,
- * at most 8, layers per batch): a batch runs after everything enqueued on the
+ * at most 8, layers per batch; one re-rank launch and one migration launch
+ * serve all layers of a batch): a batch runs after everything enqueued on the
  * cache's stream before it was launched, which includes each of its layers'
  * latest decode_attend.  Every later call that touches a layer (decode_attend,
  * prefill, retier, manual moves, state queries) launches that layer's queued
@@ -342,7 +343,9 @@ qevict_status qevict_debug_masses(qevict_cache *c, int32_t layer, float *masses,
  * 3 migrations (quantize and promote / admit, one launch), 4 initial window
  * scores (qevict_prefill_scores, its three launches together).  read
  * returns the summed milliseconds and the number of timed launches since
- * enable, and is synchronous. */
+ * enable (for 2 and 3: the number of layer routing events, since with
+ * QEVICT_FLAG_ASYNC_ROUTING one launch serves the queued events of up to
+ * eight layers), and is synchronous. */
 qevict_status qevict_profile_enable(qevict_cache *c, int32_t on);
 qevict_status qevict_profile_read(qevict_cache *c, int32_t kernel, double *total_ms, int64_t *count);
 

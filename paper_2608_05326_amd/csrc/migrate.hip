@@ -648,7 +648,7 @@ __global__ __launch_bounds__(kMigrateThreads, (migrate_waves_per_simd<W, ROPE>()
   const Geometry& G = a.g;
   const int b = blockIdx.y;
   __shared__ __attribute__((aligned(16))) QuantLds<W> sm;
-  uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
+  uint8_t* ub = a.base[blockIdx.z] + (int64_t)b * a.L.unit_bytes;
   int32_t* counts = (int32_t*)(ub + a.L.counts);
   const int32_t* qlist = (const int32_t*)(ub + a.L.qlist);
   const int32_t* plist = (const int32_t*)(ub + a.L.plist);
@@ -710,7 +710,7 @@ static int migrate_half(const Geometry& g, int entries) {
 
 hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, hipStream_t st) {
   const int mx = max_quant > max_promote ? max_quant : max_promote;
-  const dim3 grid(2 * migrate_half(a.g, mx), a.g.B);
+  const dim3 grid(2 * migrate_half(a.g, mx), a.g.B, a.n_units);
   if (a.g.rope) {
     if (a.g.W == 32) hipLaunchKernelGGL((k_migrate<32, true>), grid, dim3(kMigrateThreads), 0, st, a);
     else hipLaunchKernelGGL((k_migrate<64, true>), grid, dim3(kMigrateThreads), 0, st, a);

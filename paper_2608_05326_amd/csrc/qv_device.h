@@ -33,14 +33,12 @@ struct AttnArgs {
   int32_t period_start;     // 1: first step after a routing event (or prefill)
 };
 
-struct RetierArgs {
-  Geometry g;
-  UnitLayout L;
-  uint8_t* base;
-  int32_t prefill;          // 1: candidates are the prompt's historical windows
+// Routing events of up to kRouteBatch layers go to one launch (one workgroup row
+// per layer): the per-layer part of an event.
+constexpr int kRouteBatch = 8;
+struct RetierUnit {
+  uint8_t* base;            // the layer's first unit (sequence 0)
   int32_t aged_w0, aged_w1; // aged windows entering the candidate pool
-  const float* init_scores; // prefill: [B][n_init]
-  int32_t n_init;
   // split plans for the decode steps up to the next routing event, one per slot:
   // the sequence lengths [plan_t0, plan_t1] it serves (plan_t0 <= 0: none) and the
   // recent-region + sink windows those steps attend after the live list
@@ -48,10 +46,21 @@ struct RetierArgs {
   int32_t plan_extra[kPlanSlots];
 };
 
+struct RetierArgs {
+  Geometry g;
+  UnitLayout L;
+  int32_t prefill;          // 1: candidates are the prompt's historical windows
+  const float* init_scores; // prefill: [B][n_init]
+  int32_t n_init;
+  int32_t n_units;          // layers of this launch: workgroup row y serves unit[y]
+  RetierUnit unit[kRouteBatch];
+};
+
 struct MigrateArgs {
   Geometry g;
   UnitLayout L;
-  uint8_t* base;
+  int32_t n_units;          // layers of this launch: workgroup layer z serves base[z]
+  uint8_t* base[kRouteBatch];
   const uint16_t* src_k;    // prompt keys [B][H_kv][T][d] (prefill only)
   const uint16_t* src_v;
   int32_t src_T;

@@ -652,6 +652,7 @@ __device__ void select_tiers(const uint64_t (&key)[kMaxCand / kRetierThreads], i
 __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   const Geometry& G = a.g;
   const int b = blockIdx.x, tid = threadIdx.x;
+  const RetierUnit& U = a.unit[blockIdx.y];   // this workgroup's layer
   constexpr int NT = kRetierThreads;
   constexpr int PER = kMaxCand / NT;
 
@@ -665,7 +666,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   int32_t* fown = sown;
   int32_t* qown = sown + G.n_fslots;
 
-  uint8_t* ub = a.base + (int64_t)b * a.L.unit_bytes;
+  uint8_t* ub = U.base + (int64_t)b * a.L.unit_bytes;
   int8_t* tier = (int8_t*)(ub + a.L.tier);
   int8_t* ledger = (int8_t*)(ub + a.L.ledger);
   int8_t* bits = (int8_t*)(ub + a.L.bits);
@@ -689,7 +690,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   // Entries are read up to the list's capacity without waiting for its length;
   // the slot owner tables and the scores of the windows entering the pool (a
   // range known from the arguments) are read in the same round.
-  const int n_aged = a.aged_w1 - a.aged_w0;
+  const int n_aged = U.aged_w1 - U.aged_w0;
   const int ko = (max(G.n_fslots, G.n_qslots) + NT - 1) / NT;   // owner-table slices
   int spec_ref[PER], spec_aux[PER], spec_win[PER], spec_fo[PER], spec_qo[PER];
   float spec_sc[PER], spec_aged[PER];
@@ -703,7 +704,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     spec_sc[k] = ok ? iscore[c] : 0.f;
     spec_fo[k] = k < ko && c < G.n_fslots ? fowner[c] : -1;
     spec_qo[k] = k < ko && c < G.n_qslots ? qowner[c] : -1;
-    const int w = a.aged_w0 + c;
+    const int w = U.aged_w0 + c;
     spec_aged[k] = c >= n_aged ? 0.f
                  : (a.prefill ? a.init_scores[(int64_t)b * a.n_init + w] : score[w]);
   }
@@ -711,7 +712,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   // region; at most NR of them have started)
   float ring_sc = 0.f;
   if (tid < G.NR) {
-    const int w = a.aged_w1 + tid;
+    const int w = U.aged_w1 + tid;
     if (a.prefill) ring_sc = w < a.n_init ? a.init_scores[(int64_t)b * a.n_init + w] : 0.f;
     else ring_sc = w < G.nwc ? score[w] : 0.f;
   }
@@ -799,7 +800,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
         my_bits[k] = kind == KIND_Q4 ? 4 : 2;
       }
     } else {
-      my_w[k] = a.aged_w0 + (c - n_fq);
+      my_w[k] = U.aged_w0 + (c - n_fq);
       my_sc[k] = __int_as_float(sinfo[c - n_fq]);
       my_old[k] = T_OPEN;   // aged, entering the pool
       my_fs[k] = -1;
@@ -1083,13 +1084,13 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
     int total[kPlanSlots];   // the planned steps' totals
 #pragma unroll
     for (int j = 0; j < kPlanSlots; ++j) {
-      total[j] = total_live + a.plan_extra[j] * G.cost_bf16;
-      if (a.plan_t0[j] <= 0) continue;
+      total[j] = total_live + U.plan_extra[j] * G.cost_bf16;
+      if (U.plan_t0[j] <= 0) continue;
       int32_t* s_first = sown + j * (S4 + 1);
       if (tid == 0) s_first[0] = 0;
       if (total[j] == 0)
         for (int u = tid; u <= S4; u += NT) s_first[u] = 0;
-      for (int e = tid; e < a.plan_extra[j]; e += NT)   // recent-region and sink windows
+      for (int e = tid; e < U.plan_extra[j]; e += NT)   // recent-region and sink windows
         cover(j, total_live + e * G.cost_bf16, total_live + (e + 1) * G.cost_bf16, total[j], n_items + e + 1);
     }
 #pragma unroll
@@ -1110,7 +1111,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
       s_pref[pos] = ref;
 #pragma unroll
       for (int j = 0; j < kPlanSlots; ++j)
-        if (a.plan_t0[j] > 0) cover(j, cost, cost + item_cost(G, kind), total[j], pos + 1);
+        if (U.plan_t0[j] > 0) cover(j, cost, cost + item_cost(G, kind), total[j], pos + 1);
     }
     if (tid == 0) {
       icost[n_items] = total_live;
@@ -1131,7 +1132,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   // ---- split plan records: slot j, part u = 4 s + w ----
 #pragma unroll
   for (int j = 0; j < kPlanSlots; ++j) {
-    if (a.plan_t0[j] <= 0) continue;
+    if (U.plan_t0[j] <= 0) continue;
     const int32_t* s_first = sown + j * (S4 + 1);
     int32_t* prec = (int32_t*)(ub + a.L.plan) + j * S4 * kPlanRec;
     for (int u = tid; u < S4; u += NT) {
@@ -1147,7 +1148,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   }
   if (tid < 2 * kPlanSlots) {
     const int j = tid >> 1;
-    counts[CNT_PLAN_T0 + tid] = (tid & 1) ? a.plan_t1[j] : a.plan_t0[j];
+    counts[CNT_PLAN_T0 + tid] = (tid & 1) ? U.plan_t1[j] : U.plan_t0[j];
   }
 }
 
@@ -1155,7 +1156,7 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
 // or Q -> F (promotion), with the same ledger rules as a routing event.
 __global__ void k_manual_move(RetierArgs a, int seq, int window, int to_quant) {
   const Geometry& G = a.g;
-  uint8_t* ub = a.base + (int64_t)seq * a.L.unit_bytes;
+  uint8_t* ub = a.unit[0].base + (int64_t)seq * a.L.unit_bytes;
   int8_t* tier = (int8_t*)(ub + a.L.tier);
   int8_t* ledger = (int8_t*)(ub + a.L.ledger);
   int8_t* bits = (int8_t*)(ub + a.L.bits);
@@ -1324,7 +1325,7 @@ hipError_t launch_score_pow(const ScorePowArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_retier(const RetierArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_retier, dim3(a.g.B), dim3(kRetierThreads), 0, st, a);
+  hipLaunchKernelGGL(k_retier, dim3(a.g.B, a.n_units), dim3(kRetierThreads), 0, st, a);
   return hipGetLastError();
 }
 hipError_t launch_manual_move(const RetierArgs& a, int seq, int window, int to_quant, hipStream_t st) {

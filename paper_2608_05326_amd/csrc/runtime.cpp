@@ -71,13 +71,13 @@ struct LayerState {
 
 struct TimedLaunch {
   int kernel;
+  int units;   // layer routing events the launch serves (1 for other kernels)
   hipEvent_t start, stop;
 };
 
 struct RouteRequest {
   int layer;
-  RetierArgs ra;
-  MigrateArgs ma;
+  RetierUnit unit;
   int max_quant, max_promote;
 };
 
@@ -326,7 +326,7 @@ void fold_pending(qevict_cache* c) {
     float ms = 0.f;
     if (hipEventElapsedTime(&ms, t.start, t.stop) == hipSuccess) {
       c->prof_ms[t.kernel] += ms;
-      c->prof_n[t.kernel] += 1;
+      c->prof_n[t.kernel] += t.units;
     }
     c->free_events.push_back(t.start);
     c->free_events.push_back(t.stop);
@@ -335,7 +335,7 @@ void fold_pending(qevict_cache* c) {
 }
 
 template <typename F>
-hipError_t timed(qevict_cache* c, int kernel, hipStream_t st, F&& launch) {
+hipError_t timed(qevict_cache* c, int kernel, hipStream_t st, F&& launch, int units = 1) {
   if (!c->profiling) return launch();
   if (c->pending.size() > 2048) fold_pending(c);
   hipEvent_t a = take_event(c), b = take_event(c);
@@ -343,7 +343,7 @@ hipError_t timed(qevict_cache* c, int kernel, hipStream_t st, F&& launch) {
   (void)hipEventRecord(a, st);
   hipError_t e = launch();
   (void)hipEventRecord(b, st);
-  c->pending.push_back({kernel, a, b});
+  c->pending.push_back({kernel, units, a, b});
   return e;
 }
 
@@ -354,11 +354,21 @@ hipError_t flush_routing(qevict_cache* c) {
   hipStream_t rs = c->rstream;
   hipError_t e = hipEventRecord(c->main_ev, c->stream);
   if (e == hipSuccess) e = hipStreamWaitEvent(rs, c->main_ev, 0);
-  for (const RouteRequest& r : c->route_queue) {
-    if (e == hipSuccess) e = timed(c, 2, rs, [&] { return launch_retier(r.ra, rs); });
-    if (e == hipSuccess)
-      e = timed(c, 3, rs, [&] { return launch_migrate(r.ma, r.max_quant, r.max_promote, rs); });
+  // one re-rank launch and one migration launch for the queued layers (distinct
+  // layers: a layer is queued at most once)
+  const int n = (int)c->route_queue.size();
+  RetierArgs ra{c->g, c->L, 0, nullptr, 0, n, {}};
+  MigrateArgs ma{c->g, c->L, n, {}, nullptr, nullptr, 0};
+  int mq = 0, mp = 0;
+  for (int i = 0; i < n; ++i) {
+    const RouteRequest& r = c->route_queue[i];
+    ra.unit[i] = r.unit;
+    ma.base[i] = r.unit.base;
+    mq = std::max(mq, r.max_quant);
+    mp = std::max(mp, r.max_promote);
   }
+  if (e == hipSuccess) e = timed(c, 2, rs, [&] { return launch_retier(ra, rs); }, n);
+  if (e == hipSuccess) e = timed(c, 3, rs, [&] { return launch_migrate(ma, mq, mp, rs); }, n);
   const int slot = c->next_batch_ev;
   c->next_batch_ev = (slot + 1) % (int)c->batch_ev.size();
   if (e == hipSuccess) e = hipEventRecord(c->batch_ev[slot], rs);
@@ -434,7 +444,7 @@ int n_started(const Geometry& g, int T) { return T <= g.sink ? 0 : ceil_div(T - 
 // share a plan slot; steps past the slots, past max_context or with more unrouted
 // windows than the ring holds get none (the attention kernel then splits the list
 // itself).
-void plan_next(const Geometry& g, int max_context, int T_next, int R, int routed_end, RetierArgs* ra) {
+void plan_next(const Geometry& g, int max_context, int T_next, int R, int routed_end, RetierUnit* ra) {
   for (int j = 0; j < kPlanSlots; ++j) {
     ra->plan_t0[j] = -1;
     ra->plan_t1[j] = -2;
@@ -571,7 +581,7 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
   if (cfg->flags & QEVICT_FLAG_ASYNC_ROUTING) {
     e = hipStreamCreateWithFlags(&c->rstream, hipStreamNonBlocking);   // default priority
     const int nl = cfg->num_layers;
-    c->route_batch = nl / 2 < 1 ? 1 : (nl / 2 > 8 ? 8 : nl / 2);
+    c->route_batch = nl / 2 < 1 ? 1 : (nl / 2 > kRouteBatch ? kRouteBatch : nl / 2);
     c->route_queued.assign(nl, 0);
     c->route_ev_idx.assign(nl, -1);
     c->batch_ev.assign(nl + 1, nullptr);
@@ -675,10 +685,13 @@ qevict_status qevict_prefill_assign(qevict_cache* c, int32_t layer, const uint16
     e = launch_score_pow(pa2, c->stream);
     init_scores = staging;
   }
-  RetierArgs ra{gg, L, base, 1, 0, n_hist, init_scores, n_init, {}, {}, {}};
-  plan_next(g, c->cfg.max_context, prompt_len + 1, c->cfg.retier_interval, n_hist, &ra);
+  RetierArgs ra{gg, L, 1, init_scores, n_init, 1, {}};
+  ra.unit[0].base = base;
+  ra.unit[0].aged_w0 = 0;
+  ra.unit[0].aged_w1 = n_hist;
+  plan_next(g, c->cfg.max_context, prompt_len + 1, c->cfg.retier_interval, n_hist, &ra.unit[0]);
   if (e == hipSuccess) e = timed(c, 2, c->stream, [&] { return launch_retier(ra, c->stream); });
-  MigrateArgs ma{gg, L, base, k, v, prompt_len};
+  MigrateArgs ma{gg, L, 1, {base}, k, v, prompt_len};
   if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_migrate(ma, g.K_q, g.K_f, c->stream); });
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   ls.T = prompt_len;
@@ -873,20 +886,26 @@ qevict_status qevict_retier(qevict_cache* c, int32_t layer, qevict_retier_stats*
   UnitLayout L;
   uint8_t* base;
   fill_common(c, layer, &gg, &L, &base);
-  RetierArgs ra{gg, L, base, 0, a0, a1 > a0 ? a1 : a0, nullptr, 0, {}, {}, {}};
-  plan_next(g, c->cfg.max_context, ls.T + 1, c->cfg.retier_interval, a1 > a0 ? a1 : a0, &ra);
-  MigrateArgs ma{gg, L, base, nullptr, nullptr, 0};
+  RetierUnit unit{};
+  unit.base = base;
+  unit.aged_w0 = a0;
+  unit.aged_w1 = a1 > a0 ? a1 : a0;
+  plan_next(g, c->cfg.max_context, ls.T + 1, c->cfg.retier_interval, unit.aged_w1, &unit);
   // grid of the migration launch: sized for the windows a routing event usually
   // moves (a few per step between events); larger events loop inside the kernel
   const int max_q = std::min(std::max(g.K_q, g.K_f), 4 * c->cfg.retier_interval);
   hipError_t e = hipSuccess;
   if (c->rstream) {
     // asynchronous routing: queue the request; a batch is launched on the
-    // routing stream once it is full (or the layer is needed again)
-    c->route_queue.push_back(RouteRequest{layer, ra, ma, max_q, max_q});
+    // routing stream once it is full (or the layer is needed again); a layer
+    // queued already goes to the next batch
+    if (c->route_queued[layer] && (e = flush_routing(c)) != hipSuccess) return hip_fail(e, "retier launch");
+    c->route_queue.push_back(RouteRequest{layer, unit, max_q, max_q});
     c->route_queued[layer] = 1;
     if (stats || (int)c->route_queue.size() >= c->route_batch) e = flush_routing(c);
   } else {
+    RetierArgs ra{gg, L, 0, nullptr, 0, 1, {unit}};
+    MigrateArgs ma{gg, L, 1, {base}, nullptr, nullptr, 0};
     e = timed(c, 2, c->stream, [&] { return launch_retier(ra, c->stream); });
     if (e == hipSuccess) e = timed(c, 3, c->stream, [&] { return launch_migrate(ma, max_q, max_q, c->stream); });
   }
@@ -958,11 +977,12 @@ static qevict_status manual_move(qevict_cache* c, int layer, int seq, int window
   UnitLayout L;
   uint8_t* base;
   fill_common(c, layer, &gg, &L, &base);
-  RetierArgs ra{gg, L, base, 0, 0, 0, nullptr, 0, -1, 0};
+  RetierArgs ra{gg, L, 0, nullptr, 0, 1, {}};
+  ra.unit[0].base = base;
   // the migration kernels read work lists per sequence: run them on this sequence only
   Geometry one = gg;
   one.B = 1;
-  MigrateArgs ma{one, L, unit_base(c, layer, seq), nullptr, nullptr, 0};
+  MigrateArgs ma{one, L, 1, {unit_base(c, layer, seq)}, nullptr, nullptr, 0};
   e = launch_manual_move(ra, seq, window, to_quant, c->stream);
   if (e == hipSuccess) e = launch_migrate(ma, 1, 1, c->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
