@@ -1195,8 +1195,10 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
     if (n_all == 0 && tid < 5) s_range[tid] = 0;
     __syncthreads();
 
-    first = __builtin_amdgcn_readfirstlane(s_range[wave]);
-    last = __builtin_amdgcn_readfirstlane(s_range[wave + 1]);
+    // (the 8-token pair loop wants its run bounds in scalar registers; for the
+    // others that costs registers in the loop)
+    first = SLOT ? __builtin_amdgcn_readfirstlane(s_range[wave]) : s_range[wave];
+    last = SLOT ? __builtin_amdgcn_readfirstlane(s_range[wave + 1]) : s_range[wave + 1];
   }
 
   // plan path: list refs of a run past the plan record's first ones, one per lane
