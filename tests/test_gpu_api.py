@@ -302,13 +302,16 @@ def test_async_routing_lockstep(name, kw):
         ls.close()
 
 
-@pytest.mark.parametrize("n_layers", [4, 9])
-def test_async_routing_interleaved_layers_match_sync(n_layers):
+@pytest.mark.parametrize("n_layers,twice", [(4, False), (9, False), (16, False), (5, True)])
+def test_async_routing_interleaved_layers_match_sync(n_layers, twice):
     """Several layers stepped back to back with no host synchronisation: the
     routing of each layer overlaps the attention of the others and every
     output and final state equals the single-stream run bit for bit.  Routing
-    requests are launched in batches (2 layers with 4 layers, 4 with 9), so with
-    9 layers the last layer's request is still queued when its state is read."""
+    requests are launched in batches, one re-rank and one migration launch per
+    batch (2 layers with 4 layers, 4 with 9, 8 with 16), so with 9 layers the
+    last layer's request is still queued when its state is read; with `twice`
+    every layer is routed twice per step, and a layer already queued starts a
+    new batch."""
     import paper_2608_05326_amd as qv
     from tests.gpu_harness import gpu_config, to_dev_bf16
     torch = _torch()
@@ -332,6 +335,8 @@ def test_async_routing_interleaved_layers_match_sync(n_layers):
                     out = torch.empty((1, wl.num_q_heads, 128), dtype=torch.float32, device="cuda")
                     c.decode_attend(l, *ins[l][t], out)
                     c.retier(l)
+                    if twice:
+                        c.retier(l)
                     outs.append(out)
             last = c.get_state(n_layers - 1, 0)
             c.join_routing()

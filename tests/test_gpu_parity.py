@@ -180,6 +180,27 @@ def test_window8_routing_every_step():
     assert ls.promotions > 0
 
 
+@pytest.mark.parametrize("name,window,R,steps", [("c6w8s", 8, 10, 40), ("c6s", 32, 40, 90)])
+def test_split_plans_over_routing_periods(name, window, R, steps):
+    """The re-rank kernel writes split plans for the steps up to the next routing
+    event, one slot per count of recent-region windows (two slots); with a
+    routing interval longer than W + 1 some steps of a period need a third count
+    and split the list in the attention kernel.  Outputs and masses against the
+    oracle across those boundaries, 8- and 32-token windows."""
+    from tests.gpu_harness import Lockstep
+    wl = syn.get_workload(name).replace(name=f"{name}-r{R}", retier_interval=R, steps=steps)
+    assert wl.window == window and R - 1 > window
+    ls = Lockstep(wl)
+    print(f"[lockstep] {wl.name}", flush=True)
+    try:
+        ls.run()
+    finally:
+        ls.close()
+    print(f"[lockstep] plans W {window} R {R}: max out err {ls.max_out_err:.2e}, "
+          f"max score err {ls.max_score_err:.2e}, events {ls.events}", flush=True)
+    assert ls.events >= 2
+
+
 @pytest.mark.parametrize("hq,hkv,splits", [(8, 8, 0), (6, 2, 0), (4, 2, 1), (32, 8, 64)])
 def test_window8_head_layouts_and_splits(hq, hkv, splits):
     """8-token windows with at most four query heads per KV head are computed in
