@@ -28,8 +28,9 @@ running; `roofline.traffic` is the HBM traffic per call from the committed
 FETCH_SIZE / WRITE_SIZE record over the same duration (null when the sources
 of the attention path changed since it was taken, and on any run other than
 the default one it covers).  Initial window scores come from the prompt's last
-W queries attending to the prompt (qevict_prefill_scores); its time per layer
-is reported as `prefill_scores_us_per_layer`.
+W queries attending to the prompt (qevict_prefill_scores); the latency of one
+such call (host marshalling and its three launches, GPU otherwise idle) is
+reported as `prefill_scores_call_us`.
 
 `--workload` runs another synthetic shape instead (all sequences of its batch,
 byte-budget capacities where it gives a budget, a routing event after every
@@ -586,7 +587,10 @@ def main():
                               "evictions": round(evict / max(n_ev * wl.batch, 1), 2)},
     }
     if ps_ms:
-        res["prefill_scores_us_per_layer"] = round(sum(ps_ms[1:] or ps_ms) / len(ps_ms[1:] or ps_ms) * 1e3, 1)
+        # latency of one initial-score call while the GPU is otherwise idle: HIP events
+        # around the binding call, so its host-side marshalling and the three launches
+        # are inside (kernel times: `bench.py --prefill-scores` and the profiles)
+        res["prefill_scores_call_us"] = round(sum(ps_ms[1:] or ps_ms) / len(ps_ms[1:] or ps_ms) * 1e3, 1)
     if lp:
         per = {k: (lp[k][0] * 1e3 / lp[k][1] if lp[k][1] else None) for k in lp}
         if per[2] is not None:

@@ -171,7 +171,9 @@ struct ItemInfo {
   bool open;
 };
 
-template <int W, bool ROPE>
+// RQ: the key scale / zero registers hold channels 32 (r >> 2) + 8 qg .. + 7 (the
+// block the lane forms q*s for in registers) instead of 8 r .. 8 r + 7
+template <int W, bool ROPE, bool RQ = false>
 __device__ __forceinline__ void fetch_k(const ItemInfo& in, KHalf<W, ROPE>& kh, int lane, int r,
                                         const Geometry& G) {
   constexpr int TB = W / 16, NC = W / 16;
@@ -207,8 +209,9 @@ __device__ __forceinline__ void fetch_k(const ItemInfo& in, KHalf<W, ROPE>& kh, 
     for (int m = 0; m < NC; ++m)
       if (m < nld) kh.d[m] = ld16(p + (m * 64 + lane) * 16);
     const uint8_t* mk = p + meta_k_off(G);
-    kh.d[NC] = ld16(mk + 16 * r);
-    kh.d[NC + 1] = ld16(mk + 256 + 16 * r);
+    const int mo = RQ ? 64 * (r >> 2) + 16 * (lane >> 4) : 16 * r;
+    kh.d[NC] = ld16(mk + mo);
+    kh.d[NC + 1] = ld16(mk + 256 + mo);
     if constexpr (ROPE) {   // (cos, sin) of the window's first position, pairs 8 (r & 7) .. + 7
       static_assert(KHalf<W, ROPE>::N >= W / 16 + 6, "spare registers for the rotation");
       const float* c0 = G.rope + 2 * ((int64_t)(G.sink + in.win * W) * (kHeadDim / 2) + 8 * (r & 7));
@@ -292,6 +295,23 @@ __device__ __forceinline__ void fetch_v(const ItemInfo& in, VHalf<W>& vh, int la
 // registers only.
 template <int W, int NHS, bool ROPE>
 constexpr bool use_slot() { return NHS == 1 && !ROPE && W == 8; }
+// q*s of a quantized window formed in registers (64-token windows, at most four
+// query heads per KV head): lane (q, r) forms channel block r >> 2 of column r & 3,
+// and lane r takes the other blocks of its column from lanes r + 4, r + 8 and
+// r + 12 with row rotations (columns 4..15 repeat heads 0..3; their logits are
+// computed and never used).  With 32-token windows the LDS staging measured
+// slightly faster, so those keep it.
+template <int W, int NHS, bool ROPE>
+constexpr bool use_reg_qs() { return NHS == 1 && !ROPE && W == 64; }
+
+// lane r of each 16-lane row takes lane (r + 16 - N) mod 16 (row rotation right by N)
+template <int N>
+__device__ __forceinline__ u32x4 row_ror(u32x4 v) {
+  u32x4 o;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v[i], 0x120 + N, 0xF, 0xF, false);
+  return o;
+}
 constexpr int kPairSlot = 4 * 1024;   // LDS bytes per window of a pair
 
 __device__ __forceinline__ void dma16(const void* g, uint8_t* lds_row) {
@@ -781,6 +801,49 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
       for (int i = 0; i < 4; ++i) kw[4 * m + i] = kh.d[m][i];
     const u32x4 ks8 = kh.d[NC], kz8 = kh.d[NC + 1];
 
+    f16x8 qhi[4], qlo[4];
+    float bias = 0.f;
+    if constexpr (use_reg_qs<W, NHS, ROPE>()) {
+      // q*s of column r & 3, channels 32 kb + 8 q + i of block kb = r >> 2, split
+      // into exact fp16 hi + lo; the column's other blocks from lanes r + 4j
+      // (block kb = r >> 2 of the query picked with masks: a select over the array
+      // would become an indexed access, which the compiler puts in scratch)
+      const int kbl = r >> 2;
+      u32x4 qb = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const uint32_t m = kbl == kb ? ~0u : 0u;
+        const u32x4 v = __builtin_bit_cast(u32x4, qop[kb]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) qb[i] |= v[i] & m;
+      }
+      float bsum = 0.f;
+      f16x8 hi8, lo8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float qv = __uint_as_float((i & 1) ? (qb[i >> 1] & 0xFFFF0000u) : (qb[i >> 1] << 16));
+        const float sv = (float)__builtin_bit_cast(_Float16, (uint16_t)(ks8[i >> 1] >> (16 * (i & 1))));
+        const float zv = (float)__builtin_bit_cast(_Float16, (uint16_t)(kz8[i >> 1] >> (16 * (i & 1))));
+        const float qs = qv * sv;   // exact: 8-bit x 11-bit significands
+        const _Float16 h = (_Float16)qs;
+        hi8[i] = h;
+        lo8[i] = (_Float16)(qs - (float)h);
+        bsum = fmaf(qv, zv, bsum);
+      }
+      const u32x4 mh = __builtin_bit_cast(u32x4, hi8), ml = __builtin_bit_cast(u32x4, lo8);
+      qhi[0] = hi8;
+      qlo[0] = lo8;
+      qhi[1] = __builtin_bit_cast(f16x8, row_ror<12>(mh));   // lane r + 4
+      qlo[1] = __builtin_bit_cast(f16x8, row_ror<12>(ml));
+      qhi[2] = __builtin_bit_cast(f16x8, row_ror<8>(mh));    // lane r + 8
+      qlo[2] = __builtin_bit_cast(f16x8, row_ror<8>(ml));
+      qhi[3] = __builtin_bit_cast(f16x8, row_ror<4>(mh));    // lane r + 12
+      qlo[3] = __builtin_bit_cast(f16x8, row_ror<4>(ml));
+      // q . z of the column: its four blocks (lanes r + 4j), then the four lane groups
+      bsum += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(bsum), 0x128, 0xF, 0xF, false));
+      bsum += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(bsum), 0x124, 0xF, 0xF, false));
+      bias = rows_sum(bsum);
+    } else {
     // q*s split into exact fp16 hi + lo, written as the B operand layout
     float bias_k[NHS];
     wave_sync_lds();
@@ -809,18 +872,17 @@ __device__ __forceinline__ void process_k(const ItemInfo& in, KHalf<W, ROPE>& kh
       }
       bias_k[k] = row16_sum(bsum);   // q . z of head qg + 4k (same value in all 16 lanes)
     }
-    float bias = 0.f;
 #pragma unroll
     for (int k = 0; k < NHS; ++k) {
       const float t = __shfl(bias_k[k], 16 * (r & 3));
       if ((r >> 2) == k) bias = t;
     }
     wave_sync_lds();
-    f16x8 qhi[4], qlo[4];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       qhi[kb] = __builtin_bit_cast(f16x8, ld16(qlds + qst_off(0, kb, lane)));
       qlo[kb] = __builtin_bit_cast(f16x8, ld16(qlds + qst_off(1, kb, lane)));
+    }
     }
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
@@ -1100,7 +1162,7 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   for (int kb = 0; kb < 4; ++kb) {
     // column r: head r (pairs of 8-token windows: head r & 3 of column block
     // (r >> 2) & 1; columns 8..15 repeat 0..7 and are masked)
-    const int hc = SLOT ? (r & 3) : r;
+    const int hc = (SLOT || use_reg_qs<W, NHS, ROPE>()) ? (r & 3) : r;
     u32x4 v = {0, 0, 0, 0};
     if (hc < gqa) v = ld16(qbase + hc * kHeadDim + 32 * kb + 8 * qg);
     qop[kb] = __builtin_bit_cast(bf16x8, v);
@@ -1118,7 +1180,7 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
     }
   }
   // zero this lane's q*s operand slots (padded heads keep zeros)
-  if constexpr (!SLOT) {
+  if constexpr (!SLOT && !use_reg_qs<W, NHS, ROPE>()) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) *(u32x4*)(qlds + (i * 64 + lane) * 16) = (u32x4){0, 0, 0, 0};
   }
@@ -1308,7 +1370,7 @@ __global__ __launch_bounds__(kAttnThreads, MINB) void k_attend(AttnArgs a) {
   } else {
     for (int it = first; it < last; ++it) {
       const ItemInfo ia = info(it);
-      fetch_k<W, ROPE>(ia, KA, lane, r, G);
+      fetch_k<W, ROPE, use_reg_qs<W, NHS, ROPE>()>(ia, KA, lane, r, G);
       fetch_v<W>(ia, V, lane, qg, G);
       process_k<W, NHS, ROPE>(ia, KA, st, qop, qf, qlds, a, b, g, lane, qg, r, p_, &m_w, &l_w);
       process_v<W, NHS>(ia, V, st, p_, m_w, l_w, a, b, g, qg, r, mref);

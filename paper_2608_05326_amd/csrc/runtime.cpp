@@ -357,6 +357,7 @@ hipError_t flush_routing(qevict_cache* c) {
   // one re-rank launch and one migration launch for the queued layers (distinct
   // layers: a layer is queued at most once)
   const int n = (int)c->route_queue.size();
+  if (n > kRouteBatch) return hipErrorInvalidValue;   // (batches are flushed at route_batch <= kRouteBatch)
   RetierArgs ra{c->g, c->L, 0, nullptr, 0, n, {}};
   MigrateArgs ma{c->g, c->L, n, {}, nullptr, nullptr, 0};
   int mq = 0, mp = 0;
