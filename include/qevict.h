@@ -337,6 +337,9 @@ qevict_status qevict_debug_shift_keys(qevict_cache *c, int32_t layer, int32_t se
  * needs QEVICT_FLAG_DEBUG_MASSES).  masses: host [B, H_q, n_cap + 1] fp32,
  * the last column is the sink mass; n_cap from qevict_get_state's capacity. */
 qevict_status qevict_debug_masses(qevict_cache *c, int32_t layer, float *masses, int32_t n_cap);
+/* The same for the cache's full window capacity: masses host [B, H_q, N_w + 1]
+ * fp32, N_w = ceil((max_context - sink_tokens) / window_tokens). */
+qevict_status qevict_debug_last_masses(qevict_cache *c, int32_t layer, float *masses);
 
 /* Kernel timing with HIP events on the cache's stream (off by default).
  * kernel: 0 attention pass, 1 split merge + score accumulation, 2 re-rank,

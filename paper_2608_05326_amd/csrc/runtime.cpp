@@ -1192,6 +1192,12 @@ qevict_status qevict_debug_masses(qevict_cache* c, int32_t layer, float* masses,
   return QEVICT_OK;
 }
 
+qevict_status qevict_debug_last_masses(qevict_cache* c, int32_t layer, float* masses) {
+  qevict_status s = check_handle(c, layer);
+  if (s) return s;
+  return qevict_debug_masses(c, layer, masses, c->g.nwc);
+}
+
 qevict_status qevict_profile_enable(qevict_cache* c, int32_t on) {
   if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
   fold_pending(c);

@@ -353,3 +353,25 @@ def test_async_routing_interleaved_layers_match_sync(n_layers, twice):
     for a, b in zip(s_sync, s_async):
         for k in ("tiers", "scores", "ledger", "bits"):
             assert np.array_equal(a[k], b[k]), k
+
+
+def test_debug_last_masses_matches_debug_masses():
+    """The debug call for the cache's full window capacity returns the per-head
+    window masses of the last step (each head's masses, sink included, sum to 1)."""
+    import paper_2608_05326_amd as qv
+    from tests.gpu_harness import gpu_config, to_dev_bf16
+    torch = _torch()
+    wl = syn.get_workload("c2s")
+    c = qv.Cache(gpu_config(wl, 1, qv.FLAG_DEBUG_MASSES))
+    try:
+        k, v = syn.prompt_kv(wl, 0, 0, 0)
+        s = syn.init_scores(wl, 0, 0, 0)
+        c.prefill_assign(0, to_dev_bf16(k[None]), to_dev_bf16(v[None]), torch.from_numpy(s[None].copy()).cuda())
+        q, kn, vn = (to_dev_bf16(x[0][None]) for x in syn.decode_inputs(wl, 0, 0, 0, 1))
+        out = torch.empty((1, wl.num_q_heads, 128), dtype=torch.float32, device="cuda")
+        c.decode_attend(0, q, kn, vn, out)
+        a, b = c.debug_masses(0), c.debug_last_masses(0)
+        assert np.array_equal(a, b)
+        assert np.allclose(b.sum(axis=-1, dtype=np.float64), 1.0, atol=1e-5)
+    finally:
+        c.close()
