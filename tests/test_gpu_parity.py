@@ -201,13 +201,14 @@ def test_split_plans_over_routing_periods(name, window, R, steps):
     assert ls.events >= 2
 
 
-@pytest.mark.parametrize("hq,hkv,splits", [(8, 8, 0), (6, 2, 0), (4, 2, 1), (32, 8, 64)])
+@pytest.mark.parametrize("hq,hkv,splits", [(8, 8, 0), (6, 2, 0), (4, 2, 1), (32, 8, 64), (16, 2, 0)])
 def test_window8_head_layouts_and_splits(hq, hkv, splits):
     """8-token windows with at most four query heads per KV head are computed in
     pairs, one window per column block of the QK^T tile: GQA 1 and 3 (blocks
     partly empty), GQA 2 on one split (every wave a long run of pairs), and 64
     splits (short runs: waves with one window, an unpaired last window, or none),
-    with the paper's sink / recent regions and int2 codes."""
+    with the paper's sink / recent regions and int2 codes; GQA 8 takes the
+    one-window-at-a-time path."""
     from tests.gpu_harness import Lockstep
     wl = syn.get_workload("c6w8s").replace(name=f"w8h{hq}x{hkv}s{splits}", num_q_heads=hq,
                                            num_kv_heads=hkv, steps=24)
