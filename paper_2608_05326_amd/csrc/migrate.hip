@@ -648,6 +648,7 @@ __global__ __launch_bounds__(kMigrateThreads, (migrate_waves_per_simd<W, ROPE>()
   const Geometry& G = a.g;
   const int b = blockIdx.y;
   __shared__ __attribute__((aligned(16))) QuantLds<W> sm;
+  if (a.gate_fail && __hip_atomic_load(a.gate_fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
   uint8_t* ub = a.base[blockIdx.z] + (int64_t)b * a.L.unit_bytes;
   int32_t* counts = (int32_t*)(ub + a.L.counts);
   const int32_t* qlist = (const int32_t*)(ub + a.L.qlist);

@@ -36,6 +36,9 @@ struct AttnArgs {
 // Routing events of up to kRouteBatch layers go to one launch (one workgroup row
 // per layer): the per-layer part of an event.
 constexpr int kRouteBatch = 8;
+// polls of the routing stream's wait for the cache stream before it gives up even
+// if the wall clock has not passed its limit (each poll sleeps about 1024 clocks)
+constexpr int64_t kGateMaxPolls = 40000000;
 struct RetierUnit {
   uint8_t* base;            // the layer's first unit (sequence 0)
   int32_t aged_w0, aged_w1; // aged windows entering the candidate pool
@@ -54,6 +57,7 @@ struct RetierArgs {
   int32_t n_init;
   int32_t n_units;          // layers of this launch: workgroup row y serves unit[y]
   RetierUnit unit[kRouteBatch];
+  const int32_t* gate_fail; // routing stream: nonzero when its wait for the cache stream timed out
 };
 
 struct MigrateArgs {
@@ -64,6 +68,7 @@ struct MigrateArgs {
   const uint16_t* src_k;    // prompt keys [B][H_kv][T][d] (prefill only)
   const uint16_t* src_v;
   int32_t src_T;
+  const int32_t* gate_fail; // as RetierArgs::gate_fail
 };
 
 struct KeyNormArgs {        // key-norm scores of the prompt windows

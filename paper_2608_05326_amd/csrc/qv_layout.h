@@ -83,7 +83,7 @@ constexpr int kPlanRefs = 6;
 constexpr int kPlanRec = 2 + kPlanRefs;
 constexpr int kPlanSlots = 2;
 // device error bits
-enum : int32_t { ERR_NONFINITE = 1, ERR_POOL = 2, ERR_RANGE = 4, ERR_CAND = 8 };
+enum : int32_t { ERR_NONFINITE = 1, ERR_POOL = 2, ERR_RANGE = 4, ERR_CAND = 8, ERR_GATE = 16 };
 // stats slots (same order as qevict_retier_stats)
 enum : int32_t { ST_PROMO = 0, ST_ADMIT = 1, ST_FIRSTQ = 2, ST_REACT = 3, ST_EVICT = 4,
                  ST_NF = 5, ST_NQ4 = 6, ST_NQ2 = 7, ST_N = 8 };

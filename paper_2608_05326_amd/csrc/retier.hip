@@ -685,6 +685,11 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   int32_t* counts = (int32_t*)(ub + a.L.counts);
   int32_t* stats = (int32_t*)(ub + a.L.stats);
 
+  // a routing batch whose wait for the cache stream timed out leaves the layer as it is
+  if (a.gate_fail && __hip_atomic_load(a.gate_fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+    if (tid == 0) set_error(counts, ERR_GATE);
+    return;
+  }
   if (tid < ST_N) sstat[tid] = 0;
   // ---- one round of loads: the live list carries every candidate's state.
   // Entries are read up to the list's capacity without waiting for its length;
@@ -1285,6 +1290,44 @@ __global__ __launch_bounds__(256) void k_score_pow(ScorePowArgs a) {
   if (i >= a.n) return;
   const float x = a.in[i];
   a.out[i] = x >= 0.f ? powf(x, a.p) : __builtin_nanf("");
+}
+
+// Ordering of the routing stream after the cache stream without a queue-level
+// wait (a barrier packet waiting on another queue's signal measurably delays the
+// cache stream's own dispatches here).  The cache stream publishes a sequence
+// number after the work a routing batch must follow; kernel completion makes that
+// work visible device-wide, and the release store orders the number after it.
+// The routing stream starts each batch with a one-wave wait for the number
+// (acquire); past `ticks` of the wall clock (or a poll cap, should the clock not
+// advance) it raises the gate failure word instead, and the batch's re-rank and
+// migration kernels then do nothing.
+__global__ void k_gate_publish(uint64_t* seq, uint64_t value, int32_t* clear) {
+  if (threadIdx.x != 0) return;
+  if (clear) __hip_atomic_store(clear, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(seq, value, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ void k_gate_wait(const uint64_t* seq, uint64_t value, int32_t* fail, int64_t ticks) {
+  if (threadIdx.x != 0) return;
+  const int64_t t0 = (int64_t)wall_clock64();
+  for (int64_t polls = 0; __hip_atomic_load(seq, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < value;
+       ++polls) {
+    if ((int64_t)wall_clock64() - t0 > ticks || polls > kGateMaxPolls) {
+      __hip_atomic_store(fail, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    __builtin_amdgcn_s_sleep(16);
+  }
+}
+
+hipError_t launch_gate_publish(uint64_t* seq, uint64_t value, int32_t* clear, hipStream_t st) {
+  hipLaunchKernelGGL(k_gate_publish, dim3(1), dim3(64), 0, st, seq, value, clear);
+  return hipGetLastError();
+}
+hipError_t launch_gate_wait(const uint64_t* seq, uint64_t value, int32_t* fail, int64_t ticks,
+                            hipStream_t st) {
+  hipLaunchKernelGGL(k_gate_wait, dim3(1), dim3(64), 0, st, seq, value, fail, ticks);
+  return hipGetLastError();
 }
 
 // State initialisation of every unit block (grid-stride over units).

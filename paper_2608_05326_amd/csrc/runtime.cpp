@@ -30,6 +30,9 @@ hipError_t launch_retier(const RetierArgs& a, hipStream_t st);
 hipError_t launch_manual_move(const RetierArgs& a, int seq, int window, int to_quant, hipStream_t st);
 hipError_t launch_init_units(const Geometry& g, const UnitLayout& L, uint8_t* base, int n_units,
                              hipStream_t st);
+hipError_t launch_gate_publish(uint64_t* seq, uint64_t value, int32_t* clear, hipStream_t st);
+hipError_t launch_gate_wait(const uint64_t* seq, uint64_t value, int32_t* fail, int64_t ticks,
+                            hipStream_t st);
 hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, hipStream_t st);
 hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st);
 hipError_t launch_key_norm_init(const KeyNormArgs& a, hipStream_t st);
@@ -57,6 +60,11 @@ qevict_status fail(qevict_status s, const char* fmt, ...) {
 }
 
 constexpr int64_t kHeaderBytes = 256;
+// workspace header: the routing gate's published sequence number (uint64) and its
+// failure word (int32)
+constexpr int64_t kHdrGateSeq = 0;
+constexpr int64_t kHdrGateFail = 8;
+constexpr double kGateSeconds = 10.0;
 constexpr int kNumTimed = 5;
 
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
@@ -93,10 +101,13 @@ struct qevict_cache {
   void* static_scratch = nullptr;           // this device's fixed initial-score scratch
   // Asynchronous routing (QEVICT_FLAG_ASYNC_ROUTING): routing requests are queued
   // and launched on rstream in batches of route_batch layers, behind one wait
-  // for the cache stream; a cross-stream wait costs the host far more than a
-  // launch, so it is paid once per batch.
+  // for the cache stream (a device-side gate: the cache stream publishes
+  // gate_seq in the workspace header, the routing stream's first kernel waits for it).
   hipStream_t rstream = nullptr;
-  hipEvent_t main_ev = nullptr;             // cache stream position a batch waits for
+  uint64_t gate_seq = 0;                    // last number published for a batch
+  int64_t gate_ticks = 0;                   // the gate's time limit in wall-clock ticks
+  int64_t clock_khz = 0;                    // the wall clock's rate
+  bool gate_publish = true;                 // false only to test the time-out path
   std::vector<hipEvent_t> batch_ev;         // ring: end of a launched batch
   std::vector<char> batch_joined;           // the cache stream already waits for that batch
   int next_batch_ev = 0;
@@ -352,14 +363,17 @@ hipError_t timed(qevict_cache* c, int kernel, hipStream_t st, F&& launch, int un
 hipError_t flush_routing(qevict_cache* c) {
   if (c->route_queue.empty()) return hipSuccess;
   hipStream_t rs = c->rstream;
-  hipError_t e = hipEventRecord(c->main_ev, c->stream);
-  if (e == hipSuccess) e = hipStreamWaitEvent(rs, c->main_ev, 0);
+  uint64_t* gate = (uint64_t*)(c->ws + kHdrGateSeq);
+  int32_t* gate_fail = (int32_t*)(c->ws + kHdrGateFail);
+  const uint64_t seq = ++c->gate_seq;
+  hipError_t e = c->gate_publish ? launch_gate_publish(gate, seq, nullptr, c->stream) : hipSuccess;
+  if (e == hipSuccess) e = launch_gate_wait(gate, seq, gate_fail, c->gate_ticks, rs);
   // one re-rank launch and one migration launch for the queued layers (distinct
   // layers: a layer is queued at most once)
   const int n = (int)c->route_queue.size();
   if (n > kRouteBatch) return hipErrorInvalidValue;   // (batches are flushed at route_batch <= kRouteBatch)
-  RetierArgs ra{c->g, c->L, 0, nullptr, 0, n, {}};
-  MigrateArgs ma{c->g, c->L, n, {}, nullptr, nullptr, 0};
+  RetierArgs ra{c->g, c->L, 0, nullptr, 0, n, {}, gate_fail};
+  MigrateArgs ma{c->g, c->L, n, {}, nullptr, nullptr, 0, gate_fail};
   int mq = 0, mp = 0;
   for (int i = 0; i < n; ++i) {
     const RouteRequest& r = c->route_queue[i];
@@ -426,6 +440,9 @@ qevict_status device_errors(qevict_cache* c, int layer) {
       const int f = cnt[CNT_ERROR];
       if (f & ERR_NONFINITE) return fail(QEVICT_ERR_NONFINITE, "non-finite window score (seq %d)", b);
       if (f & ERR_RANGE) return fail(QEVICT_ERR_NONFINITE, "quantizer input outside fp16 range (seq %d)", b);
+      if (f & ERR_GATE)
+        return fail(QEVICT_ERR_BAD_STATE, "routing skipped: the routing stream waited more than %.0f s for "
+                    "the cache stream (seq %d)", kGateSeconds, b);
       return fail(QEVICT_ERR_BAD_STATE, "device error flags 0x%x (seq %d)", f, b);
     }
   }
@@ -589,8 +606,19 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
     c->batch_joined.assign(nl + 1, 0);
     // both streams run on this device: a device-scope release is enough
     const unsigned fl = hipEventDisableTiming | hipEventDisableSystemFence;
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&c->main_ev, fl);
     for (int i = 0; i <= nl && e == hipSuccess; ++i) e = hipEventCreateWithFlags(&c->batch_ev[i], fl);
+    int dev = 0, khz = 0;
+    if (e == hipSuccess) e = hipGetDevice(&dev);
+    if (e == hipSuccess && (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+                            khz <= 0)) {
+      (void)hipGetLastError();
+      khz = 100000;                                    // the wall clock's usual 100 MHz
+    }
+    c->clock_khz = khz;
+    c->gate_ticks = (int64_t)(kGateSeconds * 1e3 * khz);
+    if (e == hipSuccess)   // sequence 0 and no failure
+      e = launch_gate_publish((uint64_t*)(c->ws + kHdrGateSeq), 0, (int32_t*)(c->ws + kHdrGateFail),
+                              c->stream);
     if (e != hipSuccess) {
       qevict_cache_destroy(c);
       return hip_fail(e, "creating the routing stream");
@@ -629,7 +657,6 @@ qevict_status qevict_cache_destroy(qevict_cache* c) {
     (void)flush_routing(c);
     (void)hipStreamSynchronize(c->rstream);
   }
-  if (c->main_ev) (void)hipEventDestroy(c->main_ev);
   for (auto e : c->batch_ev)
     if (e) (void)hipEventDestroy(e);
   if (c->rstream) (void)hipStreamDestroy(c->rstream);
@@ -1196,6 +1223,16 @@ qevict_status qevict_debug_last_masses(qevict_cache* c, int32_t layer, float* ma
   qevict_status s = check_handle(c, layer);
   if (s) return s;
   return qevict_debug_masses(c, layer, masses, c->g.nwc);
+}
+
+qevict_status qevict_debug_routing_gate(qevict_cache* c, int64_t timeout_us, int32_t publish) {
+  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
+  if (!c->rstream) return fail(QEVICT_ERR_INVALID_ARG, "the cache has no routing stream");
+  if (timeout_us <= 0) return fail(QEVICT_ERR_INVALID_ARG, "timeout_us must be positive");
+  if (hipError_t e = flush_routing(c)) return hip_fail(e, "launching queued routing");
+  c->gate_ticks = timeout_us * c->clock_khz / 1000;
+  c->gate_publish = publish != 0;
+  return QEVICT_OK;
 }
 
 qevict_status qevict_profile_enable(qevict_cache* c, int32_t on) {

@@ -33,7 +33,7 @@ SYMBOLS = (
     "qevict_workspace_size", "qevict_cache_init", "qevict_cache_destroy", "qevict_prefill_assign",
     "qevict_decode_attend", "qevict_retier", "qevict_quantize_window", "qevict_promote_window",
     "qevict_get_state", "qevict_export_window", "qevict_debug_shift_keys", "qevict_debug_masses",
-    "qevict_debug_last_masses",
+    "qevict_debug_last_masses", "qevict_debug_routing_gate",
     "qevict_profile_enable", "qevict_profile_read", "qevict_last_attend_bytes", "qevict_join_routing",
     "qevict_status_string", "qevict_last_error", "qevict_prefill_scores_scratch_size",
     "qevict_prefill_scores", "qevict_capacities_for_budget", "qevict_memory_report",
@@ -141,6 +141,7 @@ def load_library(path: str | None = None):
         "qevict_debug_shift_keys": [vp, i32, i32, i32, vp],
         "qevict_debug_masses": [vp, i32, vp, i32],
         "qevict_debug_last_masses": [vp, i32, vp],
+        "qevict_debug_routing_gate": [vp, i64, i32],
         "qevict_profile_enable": [vp, i32],
         "qevict_profile_read": [vp, i32, P(ctypes.c_double), P(i64)],
         "qevict_last_attend_bytes": [vp, i32, P(i64)],
@@ -374,6 +375,9 @@ class Cache:
             raise ValueError(f"delta must hold H_kv x d values, got shape {dlt.shape}")
         self._c(self.lib.qevict_debug_shift_keys(self.handle, layer, seq, window,
                                                  dlt.ctypes.data_as(ctypes.c_void_p)))
+
+    def debug_routing_gate(self, timeout_us: int, publish: bool):
+        self._c(self.lib.qevict_debug_routing_gate(self.handle, int(timeout_us), int(bool(publish))))
 
     def debug_last_masses(self, layer: int) -> np.ndarray:
         c = self.cfg

@@ -355,6 +355,57 @@ def test_async_routing_interleaved_layers_match_sync(n_layers, twice):
             assert np.array_equal(a[k], b[k]), k
 
 
+def test_routing_gate_time_out_skips_routing_and_reports():
+    """The routing stream waits on the device for the cache stream's published
+    sequence number.  Forced from the host to time out (the cache stream stops
+    publishing, 2 ms limit): the waiting batch's re-rank and migrations leave
+    the layer as it was, the layer's next synchronous call reports
+    QEVICT_ERR_BAD_STATE naming the skipped routing, later calls report the
+    poisoned cache, and destroying the cache returns (every wait ended)."""
+    import paper_2608_05326_amd as qv
+    from paper_2608_05326_amd.qevict import QEvictError
+    from tests.gpu_harness import gpu_config, to_dev_bf16
+    torch = _torch()
+    wl = syn.get_workload("c2s")
+    c = qv.Cache(gpu_config(wl, 2, 0))
+    try:
+        with pytest.raises(QEvictError) as ei:
+            c.debug_routing_gate(2000, False)          # no routing stream
+        assert ei.value.status == -1
+    finally:
+        c.close()
+    c = qv.Cache(gpu_config(wl, 2, qv.FLAG_ASYNC_ROUTING))
+    try:
+        for l in range(2):
+            k, v = syn.prompt_kv(wl, 0, 0, l)
+            s = syn.init_scores(wl, 0, 0, l)
+            c.prefill_assign(l, to_dev_bf16(k[None]), to_dev_bf16(v[None]),
+                             torch.from_numpy(s[None].copy()).cuda())
+        with pytest.raises(QEvictError):
+            c.debug_routing_gate(0, False)
+        dec = [syn.decode_inputs(wl, 0, 0, l, 1) for l in range(2)]
+        out = torch.empty((1, wl.num_q_heads, 128), dtype=torch.float32, device="cuda")
+        # a routed step first: the gate releases it
+        c.decode_attend(0, *(to_dev_bf16(x[0][None]) for x in dec[0]), out)
+        c.retier(0)
+        c.join_routing()
+        torch.cuda.synchronize()
+        c.get_state(0, 0)
+        c.debug_routing_gate(2000, False)
+        c.decode_attend(1, *(to_dev_bf16(x[0][None]) for x in dec[1]), out)
+        c.retier(1)
+        c.join_routing()
+        torch.cuda.synchronize()
+        with pytest.raises(QEvictError) as ei:
+            c.get_state(1, 0)
+        assert ei.value.status == -4 and "routing skipped" in str(ei.value), str(ei.value)
+        with pytest.raises(QEvictError) as ei:
+            c.get_state(0, 0)
+        assert ei.value.status == -4
+    finally:
+        c.close()
+
+
 def test_debug_last_masses_matches_debug_masses():
     """The debug call for the cache's full window capacity returns the per-head
     window masses of the last step (each head's masses, sink included, sum to 1)."""
