@@ -84,17 +84,25 @@ enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT =
  * at most 8, layers per batch; one re-rank launch and one migration launch
  * serve all layers of a batch): a batch runs after everything enqueued on the
  * cache's stream before it was launched, which includes each of its layers'
- * latest decode_attend.  That order is kept on the device: a one-thread kernel
- * on the cache's stream publishes a sequence number in the workspace header
- * and a one-wave kernel on the routing stream waits for it (no queue-level
- * wait, which delays the cache's stream).  A batch whose wait exceeds 10 s is
- * skipped and its layers' next synchronous call returns QEVICT_ERR_BAD_STATE;
- * for the same reason the cache's stream must not be under HIP graph capture
- * while routing is requested.  Every later call that touches a layer
+ * latest decode_attend.  That order is kept on the device: a one-thread
+ * kernel on the cache's stream publishes a sequence number in the workspace
+ * header and a one-wave kernel on the routing stream waits for it.  A batch
+ * whose wait exceeds 10 s is skipped and its layers' next synchronous call
+ * returns QEVICT_ERR_BAD_STATE; for the same reason the cache's stream must
+ * not be under HIP graph capture while routing is requested (unless
+ * QEVICT_FLAG_ROUTING_QUEUE_WAIT is set).  Every later call that touches a layer
  * (decode_attend, prefill, retier, manual moves, state queries) launches that
  * layer's queued request if needed and orders the cache's stream after its
  * routing; qevict_join_routing does so for every layer. */
 #define QEVICT_FLAG_ASYNC_ROUTING 0x4u
+/* With QEVICT_FLAG_ASYNC_ROUTING only: order each routing batch after the
+ * cache's stream with a queue-level wait (hipStreamWaitEvent on the routing
+ * stream) instead of the device-side wait.  That wait stalls the cache's
+ * stream by about 12 us a batch on this hardware, a pure cost while routing
+ * keeps up, but room for the routing work when it runs every step with few
+ * layer calls between a batch and its layers' next use (measured: 4 layer
+ * caches of 128K context, 64-token windows, routing every step). */
+#define QEVICT_FLAG_ROUTING_QUEUE_WAIT 0x8u
 
 /* Window ranking functions (the hierarchy needs only an order over windows:
  * Sec. 4.2 and the appendix on alternative ranking functions).
@@ -347,14 +355,14 @@ qevict_status qevict_debug_masses(qevict_cache *c, int32_t layer, float *masses,
  * fp32, N_w = ceil((max_context - sink_tokens) / window_tokens). */
 qevict_status qevict_debug_last_masses(qevict_cache *c, int32_t layer, float *masses);
 
-/* Test support for the routing stream's wait (QEVICT_FLAG_ASYNC_ROUTING only,
- * else QEVICT_ERR_INVALID_ARG): set its time limit to timeout_us microseconds
- * (> 0) and, with publish = 0, stop the cache's stream from releasing later
- * routing batches, so that each of them times out, leaves its layers
- * unchanged and makes their next synchronous call return QEVICT_ERR_BAD_STATE.
- * Launches queued routing first; a cache whose wait timed out is for
- * destruction only. */
-qevict_status qevict_debug_routing_gate(qevict_cache *c, int64_t timeout_us, int32_t publish);
+/* Test support for the routing stream's device-side wait (a cache with
+ * QEVICT_FLAG_ASYNC_ROUTING and without QEVICT_FLAG_ROUTING_QUEUE_WAIT, else
+ * QEVICT_ERR_INVALID_ARG): launches queued routing, then sets the wait's time
+ * limit to timeout_us microseconds (> 0) and, with release = 0, stops the
+ * cache's stream from releasing later routing batches, so that each of them
+ * times out, leaves its layers unchanged and makes their next synchronous
+ * call return QEVICT_ERR_BAD_STATE (such a cache is for destruction only). */
+qevict_status qevict_debug_routing_gate(qevict_cache *c, int64_t timeout_us, int32_t release);
 
 /* Kernel timing with HIP events on the cache's stream (off by default).
  * kernel: 0 attention pass, 1 split merge + score accumulation, 2 re-rank,

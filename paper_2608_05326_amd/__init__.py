@@ -11,7 +11,7 @@ from .qevict import (  # noqa: F401
     ERR_CAPACITY, ERR_DEVICE,
     TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED,
     LEDGER_NONE, LEDGER_ACTIVE, LEDGER_DORMANT, BITS_MIXED_4_2, OUT_F32, OUT_BF16,
-    FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING,
+    FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING, FLAG_ROUTING_QUEUE_WAIT,
     KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_MIGRATE, SCORE_CUMULATIVE, SCORE_DECAY, SCORE_KEY_NORM,
     SCORE_PNORM,
 )

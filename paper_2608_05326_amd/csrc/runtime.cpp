@@ -101,13 +101,16 @@ struct qevict_cache {
   void* static_scratch = nullptr;           // this device's fixed initial-score scratch
   // Asynchronous routing (QEVICT_FLAG_ASYNC_ROUTING): routing requests are queued
   // and launched on rstream in batches of route_batch layers, behind one wait
-  // for the cache stream (a device-side gate: the cache stream publishes
-  // gate_seq in the workspace header, the routing stream's first kernel waits for it).
+  // for the cache stream: a device-side gate (the cache stream publishes gate_seq
+  // in the workspace header, the routing stream's first kernel waits for it) or,
+  // with QEVICT_FLAG_ROUTING_QUEUE_WAIT, a queue-level wait on main_ev.
   hipStream_t rstream = nullptr;
+  bool queue_wait = false;
+  hipEvent_t main_ev = nullptr;             // cache stream position of a queue-level wait
   uint64_t gate_seq = 0;                    // last number published for a batch
   int64_t gate_ticks = 0;                   // the gate's time limit in wall-clock ticks
   int64_t clock_khz = 0;                    // the wall clock's rate
-  bool gate_publish = true;                 // false only to test the time-out path
+  bool gate_release = true;                 // false only to test the time-out path
   std::vector<hipEvent_t> batch_ev;         // ring: end of a launched batch
   std::vector<char> batch_joined;           // the cache stream already waits for that batch
   int next_batch_ev = 0;
@@ -159,8 +162,11 @@ qevict_status check_config(const qevict_config* c) {
   if (c->retier_interval < 1) return fail(QEVICT_ERR_INVALID_ARG, "retier_interval must be >= 1");
   if (c->out_dtype != QEVICT_OUT_F32 && c->out_dtype != QEVICT_OUT_BF16)
     return fail(QEVICT_ERR_INVALID_ARG, "out_dtype");
-  if (c->flags & ~(QEVICT_FLAG_NO_PROMOTION | QEVICT_FLAG_DEBUG_MASSES | QEVICT_FLAG_ASYNC_ROUTING))
+  if (c->flags & ~(QEVICT_FLAG_NO_PROMOTION | QEVICT_FLAG_DEBUG_MASSES | QEVICT_FLAG_ASYNC_ROUTING |
+                   QEVICT_FLAG_ROUTING_QUEUE_WAIT))
     return fail(QEVICT_ERR_INVALID_ARG, "unknown flags 0x%x", c->flags);
+  if ((c->flags & QEVICT_FLAG_ROUTING_QUEUE_WAIT) && !(c->flags & QEVICT_FLAG_ASYNC_ROUTING))
+    return fail(QEVICT_ERR_INVALID_ARG, "QEVICT_FLAG_ROUTING_QUEUE_WAIT needs QEVICT_FLAG_ASYNC_ROUTING");
   if (!(c->softmax_scale >= 0.f) || !std::isfinite(c->softmax_scale))
     return fail(QEVICT_ERR_INVALID_ARG, "softmax_scale");
   if (c->score_mode != QEVICT_SCORE_CUMULATIVE && c->score_mode != QEVICT_SCORE_DECAY &&
@@ -365,9 +371,21 @@ hipError_t flush_routing(qevict_cache* c) {
   hipStream_t rs = c->rstream;
   uint64_t* gate = (uint64_t*)(c->ws + kHdrGateSeq);
   int32_t* gate_fail = (int32_t*)(c->ws + kHdrGateFail);
-  const uint64_t seq = ++c->gate_seq;
-  hipError_t e = c->gate_publish ? launch_gate_publish(gate, seq, nullptr, c->stream) : hipSuccess;
-  if (e == hipSuccess) e = launch_gate_wait(gate, seq, gate_fail, c->gate_ticks, rs);
+  hipError_t e = hipSuccess;
+  // A queue-level wait (a barrier packet on the routing stream waiting for the
+  // cache stream's event) stalls the cache stream's own dispatches by about 12 us
+  // a batch; the device-side gate does not.  The stall gives routing that runs
+  // every step room on the GPU (its re-rank workgroups each need a whole compute
+  // unit), which pays when few layer calls separate a batch from its layers'
+  // next use: QEVICT_FLAG_ROUTING_QUEUE_WAIT.
+  if (c->queue_wait) {
+    e = hipEventRecord(c->main_ev, c->stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(rs, c->main_ev, 0);
+  } else {
+    const uint64_t seq = ++c->gate_seq;
+    if (c->gate_release) e = launch_gate_publish(gate, seq, nullptr, c->stream);
+    if (e == hipSuccess) e = launch_gate_wait(gate, seq, gate_fail, c->gate_ticks, rs);
+  }
   // one re-rank launch and one migration launch for the queued layers (distinct
   // layers: a layer is queued at most once)
   const int n = (int)c->route_queue.size();
@@ -598,6 +616,7 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
   hipError_t e = hipSuccess;
   if (cfg->flags & QEVICT_FLAG_ASYNC_ROUTING) {
     e = hipStreamCreateWithFlags(&c->rstream, hipStreamNonBlocking);   // default priority
+    c->queue_wait = (cfg->flags & QEVICT_FLAG_ROUTING_QUEUE_WAIT) != 0;
     const int nl = cfg->num_layers;
     c->route_batch = nl / 2 < 1 ? 1 : (nl / 2 > kRouteBatch ? kRouteBatch : nl / 2);
     c->route_queued.assign(nl, 0);
@@ -606,6 +625,7 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
     c->batch_joined.assign(nl + 1, 0);
     // both streams run on this device: a device-scope release is enough
     const unsigned fl = hipEventDisableTiming | hipEventDisableSystemFence;
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&c->main_ev, fl);
     for (int i = 0; i <= nl && e == hipSuccess; ++i) e = hipEventCreateWithFlags(&c->batch_ev[i], fl);
     int dev = 0, khz = 0;
     if (e == hipSuccess) e = hipGetDevice(&dev);
@@ -657,6 +677,7 @@ qevict_status qevict_cache_destroy(qevict_cache* c) {
     (void)flush_routing(c);
     (void)hipStreamSynchronize(c->rstream);
   }
+  if (c->main_ev) (void)hipEventDestroy(c->main_ev);
   for (auto e : c->batch_ev)
     if (e) (void)hipEventDestroy(e);
   if (c->rstream) (void)hipStreamDestroy(c->rstream);
@@ -1225,13 +1246,14 @@ qevict_status qevict_debug_last_masses(qevict_cache* c, int32_t layer, float* ma
   return qevict_debug_masses(c, layer, masses, c->g.nwc);
 }
 
-qevict_status qevict_debug_routing_gate(qevict_cache* c, int64_t timeout_us, int32_t publish) {
+qevict_status qevict_debug_routing_gate(qevict_cache* c, int64_t timeout_us, int32_t release) {
   if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
-  if (!c->rstream) return fail(QEVICT_ERR_INVALID_ARG, "the cache has no routing stream");
+  if (!c->rstream || c->queue_wait)
+    return fail(QEVICT_ERR_INVALID_ARG, "the cache orders no routing with the device-side wait");
   if (timeout_us <= 0) return fail(QEVICT_ERR_INVALID_ARG, "timeout_us must be positive");
   if (hipError_t e = flush_routing(c)) return hip_fail(e, "launching queued routing");
   c->gate_ticks = timeout_us * c->clock_khz / 1000;
-  c->gate_publish = publish != 0;
+  c->gate_release = release != 0;
   return QEVICT_OK;
 }
 

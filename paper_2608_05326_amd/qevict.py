@@ -24,7 +24,7 @@ TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED = 0, 1, 2, 3, 4
 LEDGER_NONE, LEDGER_ACTIVE, LEDGER_DORMANT = 0, 1, 2
 BITS_MIXED_4_2 = 42
 OUT_F32, OUT_BF16 = 0, 1
-FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING = 0x1, 0x2, 0x4
+FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING, FLAG_ROUTING_QUEUE_WAIT = 0x1, 0x2, 0x4, 0x8
 KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_MIGRATE = range(4)
 SCORE_CUMULATIVE, SCORE_DECAY, SCORE_KEY_NORM, SCORE_PNORM = 0, 1, 2, 3
 
@@ -376,8 +376,8 @@ class Cache:
         self._c(self.lib.qevict_debug_shift_keys(self.handle, layer, seq, window,
                                                  dlt.ctypes.data_as(ctypes.c_void_p)))
 
-    def debug_routing_gate(self, timeout_us: int, publish: bool):
-        self._c(self.lib.qevict_debug_routing_gate(self.handle, int(timeout_us), int(bool(publish))))
+    def debug_routing_gate(self, timeout_us: int, release: bool):
+        self._c(self.lib.qevict_debug_routing_gate(self.handle, int(timeout_us), int(bool(release))))
 
     def debug_last_masses(self, layer: int) -> np.ndarray:
         c = self.cfg

@@ -302,8 +302,10 @@ def test_async_routing_lockstep(name, kw):
         ls.close()
 
 
-@pytest.mark.parametrize("n_layers,twice", [(4, False), (9, False), (16, False), (5, True)])
-def test_async_routing_interleaved_layers_match_sync(n_layers, twice):
+@pytest.mark.parametrize("n_layers,twice,queue_wait", [(4, False, False), (9, False, False),
+                                                       (16, False, False), (5, True, False),
+                                                       (4, False, True), (9, False, True)])
+def test_async_routing_interleaved_layers_match_sync(n_layers, twice, queue_wait):
     """Several layers stepped back to back with no host synchronisation: the
     routing of each layer overlaps the attention of the others and every
     output and final state equals the single-stream run bit for bit.  Routing
@@ -311,7 +313,8 @@ def test_async_routing_interleaved_layers_match_sync(n_layers, twice):
     batch (2 layers with 4 layers, 4 with 9, 8 with 16), so with 9 layers the
     last layer's request is still queued when its state is read; with `twice`
     every layer is routed twice per step, and a layer already queued starts a
-    new batch."""
+    new batch.  Batches follow the cache stream through the device-side wait,
+    or with `queue_wait` a queue-level wait (QEVICT_FLAG_ROUTING_QUEUE_WAIT)."""
     import paper_2608_05326_amd as qv
     from tests.gpu_harness import gpu_config, to_dev_bf16
     torch = _torch()
@@ -347,7 +350,7 @@ def test_async_routing_interleaved_layers_match_sync(n_layers, twice):
             c.close()
 
     o_sync, s_sync = run(0)
-    o_async, s_async = run(qv.FLAG_ASYNC_ROUTING)
+    o_async, s_async = run(qv.FLAG_ASYNC_ROUTING | (qv.FLAG_ROUTING_QUEUE_WAIT if queue_wait else 0))
     for a, b in zip(o_sync, o_async):
         assert torch.equal(a, b)
     for a, b in zip(s_sync, s_async):
@@ -367,13 +370,14 @@ def test_routing_gate_time_out_skips_routing_and_reports():
     from tests.gpu_harness import gpu_config, to_dev_bf16
     torch = _torch()
     wl = syn.get_workload("c2s")
-    c = qv.Cache(gpu_config(wl, 2, 0))
-    try:
-        with pytest.raises(QEvictError) as ei:
-            c.debug_routing_gate(2000, False)          # no routing stream
-        assert ei.value.status == -1
-    finally:
-        c.close()
+    for flags in (0, qv.FLAG_ASYNC_ROUTING | qv.FLAG_ROUTING_QUEUE_WAIT):
+        c = qv.Cache(gpu_config(wl, 2, flags))
+        try:
+            with pytest.raises(QEvictError) as ei:
+                c.debug_routing_gate(2000, False)      # no device-side wait to test
+            assert ei.value.status == -1
+        finally:
+            c.close()
     c = qv.Cache(gpu_config(wl, 2, qv.FLAG_ASYNC_ROUTING))
     try:
         for l in range(2):
