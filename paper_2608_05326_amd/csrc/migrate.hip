@@ -648,7 +648,10 @@ __global__ __launch_bounds__(kMigrateThreads, (migrate_waves_per_simd<W, ROPE>()
   const Geometry& G = a.g;
   const int b = blockIdx.y;
   __shared__ __attribute__((aligned(16))) QuantLds<W> sm;
-  if (a.gate_fail && __hip_atomic_load(a.gate_fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+  // a routing batch whose wait for the cache stream timed out moves nothing (the
+  // word is read with the first loads)
+  const int gate_failed =
+      a.gate_fail ? __hip_atomic_load(a.gate_fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
   uint8_t* ub = a.base[blockIdx.z] + (int64_t)b * a.L.unit_bytes;
   int32_t* counts = (int32_t*)(ub + a.L.counts);
   const int32_t* qlist = (const int32_t*)(ub + a.L.qlist);
@@ -660,7 +663,7 @@ __global__ __launch_bounds__(kMigrateThreads, (migrate_waves_per_simd<W, ROPE>()
   const int per_entry = G.H_kv * kParts;
   const int e0 = x0 / per_entry;
   const WorkEntry first = load_entry(list, e0 <= G.max_fq ? e0 : 0);   // lists hold max_fq + 1 entries
-  const int n_tasks = (quant ? counts[CNT_QUANT] : counts[CNT_PROMOTE]) * per_entry;
+  const int n_tasks = gate_failed ? 0 : (quant ? counts[CNT_QUANT] : counts[CNT_PROMOTE]) * per_entry;
   for (int task = x0; task < n_tasks; task += half) {
     const int e = task / per_entry, g = (task / kParts) % G.H_kv, part = task % kParts;
     const WorkEntry ent = task == x0 ? first : load_entry(list, e);

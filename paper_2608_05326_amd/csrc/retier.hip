@@ -685,11 +685,10 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   int32_t* counts = (int32_t*)(ub + a.L.counts);
   int32_t* stats = (int32_t*)(ub + a.L.stats);
 
-  // a routing batch whose wait for the cache stream timed out leaves the layer as it is
-  if (a.gate_fail && __hip_atomic_load(a.gate_fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-    if (tid == 0) set_error(counts, ERR_GATE);
-    return;
-  }
+  // a routing batch whose wait for the cache stream timed out leaves the layer as it
+  // is: the word is read with the first round of loads and tested before any store
+  const int gate_failed =
+      a.gate_fail ? __hip_atomic_load(a.gate_fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
   if (tid < ST_N) sstat[tid] = 0;
   // ---- one round of loads: the live list carries every candidate's state.
   // Entries are read up to the list's capacity without waiting for its length;
@@ -723,6 +722,10 @@ __global__ __launch_bounds__(kRetierThreads) void k_retier(RetierArgs a) {
   }
   const int n_fq = a.prefill ? 0 : counts[CNT_ITEMS];
   const int n_cand = n_fq + n_aged;
+  if (gate_failed) {
+    if (tid == 0) set_error(counts, ERR_GATE);
+    return;
+  }
   if (n_cand > kMaxCand) {
     if (tid == 0) set_error(counts, ERR_CAND);
     return;
