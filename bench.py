@@ -69,11 +69,11 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle baseline time budget")
     p.add_argument("--no-cpu", action="store_true")
     p.add_argument("--splits", type=int, default=0, help="split-K factor (0 = library default)")
-    p.add_argument("--routing", choices=("async", "queue", "sync"), default="async",
+    p.add_argument("--routing", choices=("async", "queue", "device", "sync"), default="async",
                    help="async: a layer's routing runs on the library's routing stream, overlapping "
-                        "the attention of the other layers, ordered after the cache stream on the "
-                        "device; queue: the same with a queue-level wait (QEVICT_FLAG_ROUTING_QUEUE_WAIT); "
-                        "sync: everything on one stream")
+                        "the attention of the other layers, ordered after the cache stream as the "
+                        "library chooses; queue / device: the same, always with the queue-level / "
+                        "device-side wait; sync: everything on one stream")
     p.add_argument("--no-kernel-events", action="store_true",
                    help="do not time each kernel launch with HIP events (no roofline)")
     p.add_argument("--rope-base", type=float, default=0.0,
@@ -342,7 +342,7 @@ def main():
     # of every layer cache, so that every cache routes at least twice)
     route_rounds = 2 * max(1, wl.retier_interval)
     per_layer = -(-((args.warmup + args.steps) * LPS) // NL) + prof_rounds + 2 * route_rounds + 1
-    asyncr = args.routing in ("async", "queue")
+    asyncr = args.routing in ("async", "queue", "device")
     R = wl.retier_interval            # routing event after every R-th step of a layer cache
     kf, kq = wl.capacity_full, wl.capacity_quant
     if wl.budget_frac:
@@ -361,7 +361,8 @@ def main():
                     sink_tokens=wl.sink, recent_tokens=wl.recent, retier_interval=R,
                     num_splits=args.splits,
                     flags=(qv.FLAG_ASYNC_ROUTING if asyncr else 0) |
-                          (qv.FLAG_ROUTING_QUEUE_WAIT if args.routing == "queue" else 0),
+                          (qv.FLAG_ROUTING_QUEUE_WAIT if args.routing == "queue" else 0) |
+                          (qv.FLAG_ROUTING_DEVICE_WAIT if args.routing == "device" else 0),
                     rope_base=args.rope_base)
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)

@@ -84,25 +84,28 @@ enum { QEVICT_LEDGER_NONE = 0, QEVICT_LEDGER_ACTIVE = 1, QEVICT_LEDGER_DORMANT =
  * at most 8, layers per batch; one re-rank launch and one migration launch
  * serve all layers of a batch): a batch runs after everything enqueued on the
  * cache's stream before it was launched, which includes each of its layers'
- * latest decode_attend.  That order is kept on the device: a one-thread
- * kernel on the cache's stream publishes a sequence number in the workspace
- * header and a one-wave kernel on the routing stream waits for it.  A batch
- * whose wait exceeds 10 s is skipped and its layers' next synchronous call
- * returns QEVICT_ERR_BAD_STATE; for the same reason the cache's stream must
- * not be under HIP graph capture while routing is requested (unless
- * QEVICT_FLAG_ROUTING_QUEUE_WAIT is set).  Every later call that touches a layer
+ * latest decode_attend.  That order is kept either on the device (a
+ * one-thread kernel on the cache's stream publishes a sequence number in the
+ * workspace header and a one-wave kernel on the routing stream waits for it)
+ * or by a queue-level wait (hipStreamWaitEvent on the routing stream), which
+ * stalls the cache's stream by about 12 us a batch on this hardware.  The
+ * cache takes the device-side wait when a migration workgroup fits on a
+ * compute unit beside two attention workgroups (registers and LDS of the
+ * kernels its configuration launches), so that routing proceeds beside
+ * attention, and the queue-level wait otherwise, whose stall then gives the
+ * routing work room (qevict_routing_order reports the choice).  A batch whose
+ * device-side wait exceeds 10 s is skipped and its layers' next synchronous
+ * call returns QEVICT_ERR_BAD_STATE; for the same reason the cache's stream
+ * must not be under HIP graph capture while routing is requested.  Every later call that touches a layer
  * (decode_attend, prefill, retier, manual moves, state queries) launches that
  * layer's queued request if needed and orders the cache's stream after its
  * routing; qevict_join_routing does so for every layer. */
 #define QEVICT_FLAG_ASYNC_ROUTING 0x4u
-/* With QEVICT_FLAG_ASYNC_ROUTING only: order each routing batch after the
- * cache's stream with a queue-level wait (hipStreamWaitEvent on the routing
- * stream) instead of the device-side wait.  That wait stalls the cache's
- * stream by about 12 us a batch on this hardware, a pure cost while routing
- * keeps up, but room for the routing work when it runs every step with few
- * layer calls between a batch and its layers' next use (measured: 4 layer
- * caches of 128K context, 64-token windows, routing every step). */
+/* With QEVICT_FLAG_ASYNC_ROUTING only, at most one of the two: always order
+ * routing batches with the queue-level wait, or always with the device-side
+ * wait, instead of the choice by kernel footprints. */
 #define QEVICT_FLAG_ROUTING_QUEUE_WAIT 0x8u
+#define QEVICT_FLAG_ROUTING_DEVICE_WAIT 0x10u
 
 /* Window ranking functions (the hierarchy needs only an order over windows:
  * Sec. 4.2 and the appendix on alternative ranking functions).
@@ -355,14 +358,20 @@ qevict_status qevict_debug_masses(qevict_cache *c, int32_t layer, float *masses,
  * fp32, N_w = ceil((max_context - sink_tokens) / window_tokens). */
 qevict_status qevict_debug_last_masses(qevict_cache *c, int32_t layer, float *masses);
 
-/* Test support for the routing stream's device-side wait (a cache with
- * QEVICT_FLAG_ASYNC_ROUTING and without QEVICT_FLAG_ROUTING_QUEUE_WAIT, else
- * QEVICT_ERR_INVALID_ARG): launches queued routing, then sets the wait's time
+/* Test support for the routing stream's device-side wait (a cache whose
+ * qevict_routing_order is QEVICT_ROUTING_GATE, else QEVICT_ERR_INVALID_ARG):
+ * launches queued routing, then sets the wait's time
  * limit to timeout_us microseconds (> 0) and, with release = 0, stops the
  * cache's stream from releasing later routing batches, so that each of them
  * times out, leaves its layers unchanged and makes their next synchronous
  * call return QEVICT_ERR_BAD_STATE (such a cache is for destruction only). */
 qevict_status qevict_debug_routing_gate(qevict_cache *c, int64_t timeout_us, int32_t release);
+
+/* How the cache orders routing batches after its stream: QEVICT_ROUTING_SYNC
+ * (no routing stream), QEVICT_ROUTING_GATE (device-side wait) or
+ * QEVICT_ROUTING_QUEUE_WAIT (see QEVICT_FLAG_ASYNC_ROUTING). */
+enum { QEVICT_ROUTING_SYNC = 0, QEVICT_ROUTING_GATE = 1, QEVICT_ROUTING_QUEUE_WAIT = 2 };
+qevict_status qevict_routing_order(qevict_cache *c, int32_t *order);
 
 /* Kernel timing with HIP events on the cache's stream (off by default).
  * kernel: 0 attention pass, 1 split merge + score accumulation, 2 re-rank,

@@ -12,6 +12,7 @@ from .qevict import (  # noqa: F401
     TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED,
     LEDGER_NONE, LEDGER_ACTIVE, LEDGER_DORMANT, BITS_MIXED_4_2, OUT_F32, OUT_BF16,
     FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING, FLAG_ROUTING_QUEUE_WAIT,
+    FLAG_ROUTING_DEVICE_WAIT,
     KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_MIGRATE, SCORE_CUMULATIVE, SCORE_DECAY, SCORE_KEY_NORM,
     SCORE_PNORM,
 )

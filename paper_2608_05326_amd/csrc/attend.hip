@@ -1660,24 +1660,46 @@ hipError_t launch_attend_t(const AttnArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_attend(const AttnArgs& a, hipStream_t st) {
-  const int nhs = (a.g.gqa + 3) / 4;
+// Calls f(W, NHS, ROPE) (integral constants) for the attention instantiation of a
+// geometry: window size, 16-row head sets per KV head, RoPE-aware quantized tier.
+template <class F>
+hipError_t attend_variant(const Geometry& g, F&& f) {
+  const int nhs = (g.gqa + 3) / 4;
   auto by_heads = [&](auto w, auto rope) -> hipError_t {
-    constexpr int Wv = decltype(w)::value;
-    constexpr bool Rv = decltype(rope)::value;
-    if (nhs == 1) return launch_attend_t<Wv, 1, Rv>(a, st);
-    if (nhs == 2) return launch_attend_t<Wv, 2, Rv>(a, st);
-    return launch_attend_t<Wv, 4, Rv>(a, st);
+    if (nhs == 1) return f(w, std::integral_constant<int, 1>{}, rope);
+    if (nhs == 2) return f(w, std::integral_constant<int, 2>{}, rope);
+    return f(w, std::integral_constant<int, 4>{}, rope);
   };
   using T = std::true_type;
-  using F = std::false_type;
-  if (a.g.rope) {
-    if (a.g.W == 32) return by_heads(std::integral_constant<int, 32>{}, T{});
+  using Fa = std::false_type;
+  if (g.rope) {
+    if (g.W == 32) return by_heads(std::integral_constant<int, 32>{}, T{});
     return by_heads(std::integral_constant<int, 64>{}, T{});
   }
-  if (a.g.W == 8) return by_heads(std::integral_constant<int, 8>{}, F{});
-  if (a.g.W == 32) return by_heads(std::integral_constant<int, 32>{}, F{});
-  return by_heads(std::integral_constant<int, 64>{}, F{});
+  if (g.W == 8) return by_heads(std::integral_constant<int, 8>{}, Fa{});
+  if (g.W == 32) return by_heads(std::integral_constant<int, 32>{}, Fa{});
+  return by_heads(std::integral_constant<int, 64>{}, Fa{});
+}
+
+hipError_t launch_attend(const AttnArgs& a, hipStream_t st) {
+  return attend_variant(a.g, [&](auto w, auto nhs, auto rope) {
+    return launch_attend_t<decltype(w)::value, decltype(nhs)::value, decltype(rope)::value>(a, st);
+  });
+}
+
+// Registers per lane and LDS bytes per workgroup of the attention kernel a
+// geometry launches.
+hipError_t attend_footprint(const Geometry& g, int* vgprs, size_t* lds) {
+  return attend_variant(g, [&](auto w, auto nhs, auto rope) {
+    constexpr int Wv = decltype(w)::value, Nv = decltype(nhs)::value;
+    constexpr bool Rv = decltype(rope)::value;
+    hipFuncAttributes fa;
+    hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(&k_attend<Wv, Nv, 2, Rv>));
+    if (e != hipSuccess) return e;
+    *vgprs = fa.numRegs;
+    *lds = fa.sharedSizeBytes + attn_smem_fixed<Wv, Nv, Rv>() + 4 * (size_t)(g.max_fq + 1);
+    return hipSuccess;
+  });
 }
 
 hipError_t launch_merge(const AttnArgs& a, hipStream_t st) {

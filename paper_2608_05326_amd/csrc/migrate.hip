@@ -725,6 +725,21 @@ hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, 
   }
   return hipGetLastError();
 }
+// Registers per lane and LDS bytes per workgroup of the migration kernel a
+// geometry launches.
+hipError_t migrate_footprint(const Geometry& g, int* vgprs, size_t* lds) {
+  const void* k = g.rope ? (g.W == 32 ? reinterpret_cast<const void*>(&k_migrate<32, true>)
+                                      : reinterpret_cast<const void*>(&k_migrate<64, true>))
+                 : g.W == 8  ? reinterpret_cast<const void*>(&k_migrate<8, false>)
+                 : g.W == 32 ? reinterpret_cast<const void*>(&k_migrate<32, false>)
+                             : reinterpret_cast<const void*>(&k_migrate<64, false>);
+  hipFuncAttributes fa;
+  hipError_t e = hipFuncGetAttributes(&fa, k);
+  if (e != hipSuccess) return e;
+  *vgprs = fa.numRegs;
+  *lds = fa.sharedSizeBytes;
+  return hipSuccess;
+}
 hipError_t launch_pack_tokens(const PackArgs& a, hipStream_t st) {
   if (a.tok1 <= a.tok0) return hipSuccess;
   hipLaunchKernelGGL(k_pack_tokens, dim3(a.g.H_kv, a.g.B), dim3(256), 0, st, a);

@@ -31,6 +31,8 @@ hipError_t launch_manual_move(const RetierArgs& a, int seq, int window, int to_q
 hipError_t launch_init_units(const Geometry& g, const UnitLayout& L, uint8_t* base, int n_units,
                              hipStream_t st);
 hipError_t launch_gate_publish(uint64_t* seq, uint64_t value, int32_t* clear, hipStream_t st);
+hipError_t attend_footprint(const Geometry& g, int* vgprs, size_t* lds);
+hipError_t migrate_footprint(const Geometry& g, int* vgprs, size_t* lds);
 hipError_t launch_gate_wait(const uint64_t* seq, uint64_t value, int32_t* fail, int64_t ticks,
                             hipStream_t st);
 hipError_t launch_migrate(const MigrateArgs& a, int max_quant, int max_promote, hipStream_t st);
@@ -102,8 +104,8 @@ struct qevict_cache {
   // Asynchronous routing (QEVICT_FLAG_ASYNC_ROUTING): routing requests are queued
   // and launched on rstream in batches of route_batch layers, behind one wait
   // for the cache stream: a device-side gate (the cache stream publishes gate_seq
-  // in the workspace header, the routing stream's first kernel waits for it) or,
-  // with QEVICT_FLAG_ROUTING_QUEUE_WAIT, a queue-level wait on main_ev.
+  // in the workspace header, the routing stream's first kernel waits for it) or a
+  // queue-level wait on main_ev (queue_wait; see routing_fits_beside_attention).
   hipStream_t rstream = nullptr;
   bool queue_wait = false;
   hipEvent_t main_ev = nullptr;             // cache stream position of a queue-level wait
@@ -163,10 +165,13 @@ qevict_status check_config(const qevict_config* c) {
   if (c->out_dtype != QEVICT_OUT_F32 && c->out_dtype != QEVICT_OUT_BF16)
     return fail(QEVICT_ERR_INVALID_ARG, "out_dtype");
   if (c->flags & ~(QEVICT_FLAG_NO_PROMOTION | QEVICT_FLAG_DEBUG_MASSES | QEVICT_FLAG_ASYNC_ROUTING |
-                   QEVICT_FLAG_ROUTING_QUEUE_WAIT))
+                   QEVICT_FLAG_ROUTING_QUEUE_WAIT | QEVICT_FLAG_ROUTING_DEVICE_WAIT))
     return fail(QEVICT_ERR_INVALID_ARG, "unknown flags 0x%x", c->flags);
-  if ((c->flags & QEVICT_FLAG_ROUTING_QUEUE_WAIT) && !(c->flags & QEVICT_FLAG_ASYNC_ROUTING))
-    return fail(QEVICT_ERR_INVALID_ARG, "QEVICT_FLAG_ROUTING_QUEUE_WAIT needs QEVICT_FLAG_ASYNC_ROUTING");
+  const uint32_t order_flags = c->flags & (QEVICT_FLAG_ROUTING_QUEUE_WAIT | QEVICT_FLAG_ROUTING_DEVICE_WAIT);
+  if (order_flags && !(c->flags & QEVICT_FLAG_ASYNC_ROUTING))
+    return fail(QEVICT_ERR_INVALID_ARG, "routing order flags need QEVICT_FLAG_ASYNC_ROUTING");
+  if (order_flags == (QEVICT_FLAG_ROUTING_QUEUE_WAIT | QEVICT_FLAG_ROUTING_DEVICE_WAIT))
+    return fail(QEVICT_ERR_INVALID_ARG, "at most one routing order flag");
   if (!(c->softmax_scale >= 0.f) || !std::isfinite(c->softmax_scale))
     return fail(QEVICT_ERR_INVALID_ARG, "softmax_scale");
   if (c->score_mode != QEVICT_SCORE_CUMULATIVE && c->score_mode != QEVICT_SCORE_DECAY &&
@@ -362,6 +367,27 @@ hipError_t timed(qevict_cache* c, int kernel, hipStream_t st, F&& launch, int un
   (void)hipEventRecord(b, st);
   c->pending.push_back({kernel, units, a, b});
   return e;
+}
+
+// Whether a migration workgroup fits on a compute unit beside the two attention
+// workgroups it holds during a decode step (both kernels run one wave per SIMD):
+// registers of two attention waves and one migration wave per SIMD, LDS of the
+// three workgroups.  Routing ordered by the device-side gate then proceeds beside
+// attention.  Where it does not fit it waits for compute units that attention
+// leaves free, and the queue-level wait, whose stall of the cache stream (about
+// 12 us a batch) gives it that room, was measured faster: 128K context with
+// 64-token windows (256-register attention), the RoPE-aware tier (256), GQA 8
+// (217 plus a 79-register migration wave), 8-token windows (222 plus 96) with 16
+// layer caches.
+hipError_t routing_fits_beside_attention(const Geometry& g, bool* fits) {
+  int av = 0, mv = 0;
+  size_t al = 0, ml = 0;
+  hipError_t e = attend_footprint(g, &av, &al);
+  if (e == hipSuccess) e = migrate_footprint(g, &mv, &ml);
+  if (e != hipSuccess) return e;
+  auto granule = [](int v) { return (v + 7) / 8 * 8; };   // VGPR allocation granule
+  *fits = 2 * granule(av) + granule(mv) <= 512 && 2 * al + ml <= 160 * 1024;
+  return hipSuccess;
 }
 
 // Asynchronous routing: launch the queued routing requests on the routing
@@ -616,7 +642,6 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
   hipError_t e = hipSuccess;
   if (cfg->flags & QEVICT_FLAG_ASYNC_ROUTING) {
     e = hipStreamCreateWithFlags(&c->rstream, hipStreamNonBlocking);   // default priority
-    c->queue_wait = (cfg->flags & QEVICT_FLAG_ROUTING_QUEUE_WAIT) != 0;
     const int nl = cfg->num_layers;
     c->route_batch = nl / 2 < 1 ? 1 : (nl / 2 > kRouteBatch ? kRouteBatch : nl / 2);
     c->route_queued.assign(nl, 0);
@@ -660,6 +685,12 @@ qevict_status qevict_cache_init(const qevict_config* cfg, void* workspace, size_
     e = hipMemcpyAsync(tab, host.data(), host.size() * sizeof(float), hipMemcpyHostToDevice, c->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(c->stream);   // the host table goes out of scope
     c->g.rope = tab;
+  }
+  if (e == hipSuccess && c->rstream) {
+    bool beside = false;
+    e = routing_fits_beside_attention(c->g, &beside);
+    c->queue_wait = (cfg->flags & QEVICT_FLAG_ROUTING_QUEUE_WAIT) ||
+                    (!(cfg->flags & QEVICT_FLAG_ROUTING_DEVICE_WAIT) && !beside);
   }
   if (e == hipSuccess) e = launch_init_units(c->g, c->L, c->ws + kHeaderBytes, cfg->num_layers * cfg->batch,
                                    c->stream);
@@ -1244,6 +1275,13 @@ qevict_status qevict_debug_last_masses(qevict_cache* c, int32_t layer, float* ma
   qevict_status s = check_handle(c, layer);
   if (s) return s;
   return qevict_debug_masses(c, layer, masses, c->g.nwc);
+}
+
+qevict_status qevict_routing_order(qevict_cache* c, int32_t* order) {
+  if (!c) return fail(QEVICT_ERR_INVALID_ARG, "cache is NULL");
+  if (!order) return fail(QEVICT_ERR_INVALID_ARG, "order is NULL");
+  *order = !c->rstream ? QEVICT_ROUTING_SYNC : c->queue_wait ? QEVICT_ROUTING_QUEUE_WAIT : QEVICT_ROUTING_GATE;
+  return QEVICT_OK;
 }
 
 qevict_status qevict_debug_routing_gate(qevict_cache* c, int64_t timeout_us, int32_t release) {

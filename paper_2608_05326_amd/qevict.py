@@ -24,7 +24,8 @@ TIER_UNUSED, TIER_OPEN, TIER_FULL, TIER_QUANT, TIER_EVICTED = 0, 1, 2, 3, 4
 LEDGER_NONE, LEDGER_ACTIVE, LEDGER_DORMANT = 0, 1, 2
 BITS_MIXED_4_2 = 42
 OUT_F32, OUT_BF16 = 0, 1
-FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING, FLAG_ROUTING_QUEUE_WAIT = 0x1, 0x2, 0x4, 0x8
+FLAG_NO_PROMOTION, FLAG_DEBUG_MASSES, FLAG_ASYNC_ROUTING = 0x1, 0x2, 0x4
+FLAG_ROUTING_QUEUE_WAIT, FLAG_ROUTING_DEVICE_WAIT = 0x8, 0x10
 KERNEL_ATTEND, KERNEL_MERGE, KERNEL_RETIER, KERNEL_MIGRATE = range(4)
 SCORE_CUMULATIVE, SCORE_DECAY, SCORE_KEY_NORM, SCORE_PNORM = 0, 1, 2, 3
 
@@ -33,7 +34,7 @@ SYMBOLS = (
     "qevict_workspace_size", "qevict_cache_init", "qevict_cache_destroy", "qevict_prefill_assign",
     "qevict_decode_attend", "qevict_retier", "qevict_quantize_window", "qevict_promote_window",
     "qevict_get_state", "qevict_export_window", "qevict_debug_shift_keys", "qevict_debug_masses",
-    "qevict_debug_last_masses", "qevict_debug_routing_gate",
+    "qevict_debug_last_masses", "qevict_debug_routing_gate", "qevict_routing_order",
     "qevict_profile_enable", "qevict_profile_read", "qevict_last_attend_bytes", "qevict_join_routing",
     "qevict_status_string", "qevict_last_error", "qevict_prefill_scores_scratch_size",
     "qevict_prefill_scores", "qevict_capacities_for_budget", "qevict_memory_report",
@@ -142,6 +143,7 @@ def load_library(path: str | None = None):
         "qevict_debug_masses": [vp, i32, vp, i32],
         "qevict_debug_last_masses": [vp, i32, vp],
         "qevict_debug_routing_gate": [vp, i64, i32],
+        "qevict_routing_order": [vp, P(i32)],
         "qevict_profile_enable": [vp, i32],
         "qevict_profile_read": [vp, i32, P(ctypes.c_double), P(i64)],
         "qevict_last_attend_bytes": [vp, i32, P(i64)],
@@ -375,6 +377,13 @@ class Cache:
             raise ValueError(f"delta must hold H_kv x d values, got shape {dlt.shape}")
         self._c(self.lib.qevict_debug_shift_keys(self.handle, layer, seq, window,
                                                  dlt.ctypes.data_as(ctypes.c_void_p)))
+
+    ROUTING_SYNC, ROUTING_GATE, ROUTING_QUEUE_WAIT = 0, 1, 2
+
+    def routing_order(self) -> int:
+        o = ctypes.c_int32()
+        self._c(self.lib.qevict_routing_order(self.handle, ctypes.byref(o)))
+        return o.value
 
     def debug_routing_gate(self, timeout_us: int, release: bool):
         self._c(self.lib.qevict_debug_routing_gate(self.handle, int(timeout_us), int(bool(release))))

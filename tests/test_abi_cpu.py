@@ -50,6 +50,9 @@ def test_workspace_size_of_the_8b_32k_layer():
     (dict(retier_interval=0), qv.qevict.ERR_INVALID_ARG),
     (dict(flags=0x80), qv.qevict.ERR_INVALID_ARG),
     (dict(flags=qv.FLAG_ROUTING_QUEUE_WAIT), qv.qevict.ERR_INVALID_ARG),   # needs async routing
+    (dict(flags=qv.FLAG_ROUTING_DEVICE_WAIT), qv.qevict.ERR_INVALID_ARG),
+    (dict(flags=qv.FLAG_ASYNC_ROUTING | qv.FLAG_ROUTING_QUEUE_WAIT | qv.FLAG_ROUTING_DEVICE_WAIT),
+     qv.qevict.ERR_INVALID_ARG),                                            # at most one order
     (dict(max_context=0), qv.qevict.ERR_INVALID_ARG),
     (dict(sink_tokens=65 * 32), qv.qevict.ERR_UNSUPPORTED),
     (dict(score_mode=4), qv.qevict.ERR_INVALID_ARG),

@@ -358,6 +358,33 @@ def test_async_routing_interleaved_layers_match_sync(n_layers, twice, queue_wait
             assert np.array_equal(a[k], b[k]), k
 
 
+@pytest.mark.parametrize("name,kw,flags,order", [
+    ("c2s", {}, "async", "gate"),                     # 32-token windows, GQA 4: 204 + 204 + 79 registers
+    ("c6s", {}, "async", "gate"),
+    ("c2s", {"rope_base": 500000.0}, "async", "queue"),   # RoPE-aware attention: 256 registers
+    ("c4s", {}, "async", "queue"),                    # 64-token windows: 256 registers
+    ("c5s", {}, "async", "queue"),                    # GQA 8: 217 + 217 + 79
+    ("c6w8s", {}, "async", "queue"),                  # 8-token windows: 222 + 222 + 96
+    ("c2s", {}, "async+queue", "queue"),
+    ("c6w8s", {}, "async+device", "gate"),
+    ("c2s", {}, "sync", "sync"),
+])
+def test_routing_order_follows_kernel_footprints(name, kw, flags, order):
+    """Routing batches follow the cache stream through the device-side wait
+    where a migration workgroup fits on a compute unit beside two attention
+    workgroups, else through the queue-level wait; either flag forces one."""
+    import paper_2608_05326_amd as qv
+    from tests.gpu_harness import gpu_config
+    f = {"async": qv.FLAG_ASYNC_ROUTING, "async+queue": qv.FLAG_ASYNC_ROUTING | qv.FLAG_ROUTING_QUEUE_WAIT,
+         "async+device": qv.FLAG_ASYNC_ROUTING | qv.FLAG_ROUTING_DEVICE_WAIT, "sync": 0}[flags]
+    c = qv.Cache(gpu_config(syn.get_workload(name), 1, f, **kw))
+    try:
+        want = {"gate": c.ROUTING_GATE, "queue": c.ROUTING_QUEUE_WAIT, "sync": c.ROUTING_SYNC}[order]
+        assert c.routing_order() == want
+    finally:
+        c.close()
+
+
 def test_routing_gate_time_out_skips_routing_and_reports():
     """The routing stream waits on the device for the cache stream's published
     sequence number.  Forced from the host to time out (the cache stream stops
