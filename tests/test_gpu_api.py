@@ -288,14 +288,19 @@ def test_smoke_entry_point():
 # asynchronous routing (routing stream + per-layer ordering)
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name,kw", [("c2s", {}), ("c3s", {}), ("c5s", {"rope_base": 500000.0}),
-                                     ("c5s", {"score_p": 3.0}), ("c2s", {"score_decay": 0.9})])
-def test_async_routing_lockstep(name, kw):
+@pytest.mark.parametrize("name,kw,order", [("c2s", {}, None), ("c3s", {}, None),
+                                           ("c5s", {"rope_base": 500000.0}, None),
+                                           ("c5s", {"score_p": 3.0}, None), ("c2s", {"score_decay": 0.9}, None),
+                                           ("c4s", {}, None), ("c6w8s", {}, "device"), ("c2s", {}, "queue")])
+def test_async_routing_lockstep(name, kw, order):
     """Routing on its own stream, also with RoPE, the p-norm over 8-step periods
-    and the decayed score (the period bookkeeping happens at enqueue time)."""
+    and the decayed score (the period bookkeeping happens at enqueue time), with
+    the ordering the cache chooses (queue-level wait for c4s and c5s, the
+    device-side gate for the others) or a forced one (`order`)."""
     import paper_2608_05326_amd as qv
     from tests.gpu_harness import Lockstep
-    ls = Lockstep(syn.get_workload(name), flags=qv.FLAG_ASYNC_ROUTING, steps=12, **kw)
+    extra = {None: 0, "device": qv.FLAG_ROUTING_DEVICE_WAIT, "queue": qv.FLAG_ROUTING_QUEUE_WAIT}[order]
+    ls = Lockstep(syn.get_workload(name), flags=qv.FLAG_ASYNC_ROUTING | extra, steps=12, **kw)
     try:
         ls.run()
     finally:
