@@ -367,6 +367,7 @@ def main():
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)
     cache = qv.Cache(cfg, stream=stream)
+    order = cache.routing_order()
     print(f"[bench] workspace {cache.workspace.numel() / 1e6:.1f} MB for {NL} layer caches of "
           f"batch {wl.batch}", file=sys.stderr, flush=True)
 
@@ -578,7 +579,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": workload_desc(wl),
                    "layer_caches": NL, "layer_calls_per_step": LPS, "global_batch": wl.batch,
-                   "seq_len": wl.prompt_len, "routing": args.routing, "routing_interval": R,
+                   "seq_len": wl.prompt_len, "routing": args.routing,
+                   "routing_order": {0: "single stream", 1: "device-side gate", 2: "queue-level wait"}[order],
+                   "routing_interval": R,
                    "init_scores": "prompt attention (qevict_prefill_scores, W observation queries)"
                    if observed else "synthetic", "rope_base": args.rope_base,
                    "parallelism": "single GPU"},
