@@ -400,10 +400,9 @@ hipError_t flush_routing(qevict_cache* c) {
   hipError_t e = hipSuccess;
   // A queue-level wait (a barrier packet on the routing stream waiting for the
   // cache stream's event) stalls the cache stream's own dispatches by about 12 us
-  // a batch; the device-side gate does not.  The stall gives routing that runs
-  // every step room on the GPU (its re-rank workgroups each need a whole compute
-  // unit), which pays when few layer calls separate a batch from its layers'
-  // next use: QEVICT_FLAG_ROUTING_QUEUE_WAIT.
+  // a batch; the device-side gate does not.  The stall is what gives routing room
+  // where its kernels do not fit beside attention (queue_wait, chosen at cache
+  // creation by routing_fits_beside_attention or forced by a flag).
   if (c->queue_wait) {
     e = hipEventRecord(c->main_ev, c->stream);
     if (e == hipSuccess) e = hipStreamWaitEvent(rs, c->main_ev, 0);
